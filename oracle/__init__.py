@@ -1,0 +1,18 @@
+"""CPU oracle (test infrastructure only).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  The product path never does: it fails when its own HIP
+library is missing instead of falling back here.
+"""
+from .fgref import (  # noqa: F401
+    build,
+    lib_path,
+    gspmm,
+    gsddmm,
+    edge_softmax,
+    max_threads,
+    MSG_COPY_SRC,
+    MSG_SRC_MUL_EDGE,
+    RED_SUM,
+    RED_MAX,
+)

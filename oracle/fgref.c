@@ -1,0 +1,219 @@
+/*
+ * fgref.c -- plain CPU oracle for FeatGraph's generalized SpMM, generalized
+ * SDDMM and the edge softmax that links them in an attention layer.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header or constant with the GPU library; it is deliberately slow and
+ * written so that each function can be checked against the paper by eye.
+ *
+ * Graph convention: CSR whose rows are destination vertices.  For row v the
+ * stored edges are p = indptr[v] .. indptr[v+1]-1 in storage order, the
+ * source vertex is u = indices[p] and the edge id is e = edge_ids[p] (or p
+ * when edge_ids is NULL).  Vertex data is row-major [vertices, H, dh]; edge
+ * data is row-major [edge id, H].
+ *
+ * Precision: inputs and outputs are fp32; sums and dot products accumulate
+ * in fp64 and are rounded to fp32 once.  Where a float comparison decides an
+ * index (max / argmax) the compared message is the fp32 value, exactly as
+ * the GPU path sees it.
+ *
+ * Threading: rows are independent, each row is computed by one thread in a
+ * fixed order, so results do not depend on the thread count.
+ *
+ * Return value of every entry point: 0 on success, a negative number for
+ * invalid arguments (nothing written in that case).
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <omp.h>
+
+#define FGREF_EXPORT __attribute__((visibility("default")))
+
+enum { MSG_COPY_SRC = 0, MSG_SRC_MUL_EDGE = 1 };
+enum { RED_SUM = 0, RED_MAX = 1 };
+
+static int set_threads(int num_threads) {
+  if (num_threads > 0) omp_set_num_threads(num_threads);
+  return 0;
+}
+
+/* Row of the i-th selected output: either rows[i] or i itself. */
+static int64_t pick_row(const int64_t* rows, int64_t i) { return rows ? rows[i] : i; }
+
+static int check_rows(const int64_t* rows, int64_t num_sel, int64_t num_rows) {
+  if (!rows) return 0;
+  for (int64_t i = 0; i < num_sel; ++i)
+    if (rows[i] < 0 || rows[i] >= num_rows) return -1;
+  return 0;
+}
+
+/*
+ * Generalized SpMM (Sec. II-A Eq. 1: h_v = (+)_{u in N(v)} phi(x_u, x_v, x_uv);
+ * Eq. 3 is the case phi = copy source, (+) = sum).  The message function phi
+ * is one of
+ *   copy_src      : m = X[u, h, k]
+ *   src_mul_edge  : m = (float)(W[e, h] * X[u, h, k])   (product rounded to fp32)
+ * and the aggregator (+) is sum or max (Sec. III-B: any commutative reducer).
+ *
+ * sum : out[v,h,k] = (float) sum_p (double) m            (empty row -> 0)
+ * max : out[v,h,k] = max_p m, arg[v,h,k] = the smallest edge id attaining it;
+ *       empty row -> out 0, arg -1.  Equality is IEEE equality, so -0 == +0
+ *       and the edge id decides between them.
+ *
+ * Output i (0 <= i < num_sel) is row pick_row(rows, i); with rows == NULL all
+ * num_rows rows are computed (num_sel must then equal num_rows).
+ * term_norm (optional, sum only) receives sqrt(sum_p m^2) per output element.
+ */
+FGREF_EXPORT int fgref_gspmm(int64_t num_rows, int64_t num_cols, const int32_t* indptr,
+                             const int32_t* indices, const int32_t* edge_ids, int64_t nnz_total,
+                             int msg, int red, int64_t H, int64_t dh, const float* x,
+                             const float* edge_val, const int64_t* rows, int64_t num_sel,
+                             float* out, int32_t* arg, double* term_norm, int num_threads) {
+  if (H < 1 || dh < 1 || num_rows < 0 || num_cols < 0 || !indptr || !out) return -1;
+  if (msg != MSG_COPY_SRC && msg != MSG_SRC_MUL_EDGE) return -1;
+  if (red != RED_SUM && red != RED_MAX) return -1;
+  if (msg == MSG_SRC_MUL_EDGE && !edge_val) return -1;
+  if (red == RED_MAX && !arg) return -1;
+  if (!rows && num_sel != num_rows) return -1;
+  if (check_rows(rows, num_sel, num_rows)) return -1;
+  set_threads(num_threads);
+  const int64_t F = H * dh;
+  int bad = 0;
+
+#pragma omp parallel for schedule(dynamic, 64) reduction(| : bad)
+  for (int64_t i = 0; i < num_sel; ++i) {
+    const int64_t v = pick_row(rows, i);
+    const int64_t p0 = indptr[v], p1 = indptr[v + 1];
+    for (int64_t h = 0; h < H; ++h) {
+      for (int64_t k = 0; k < dh; ++k) {
+        const int64_t f = h * dh + k;
+        double acc = 0.0, sq = 0.0;
+        float best = 0.0f;
+        int32_t best_e = -1;
+        for (int64_t p = p0; p < p1; ++p) {
+          const int64_t u = indices[p];
+          const int64_t e = edge_ids ? edge_ids[p] : p;
+          if (u < 0 || u >= num_cols || e < 0 || e >= nnz_total) { bad |= 1; continue; }
+          float m = x[u * F + f];
+          if (msg == MSG_SRC_MUL_EDGE) m = edge_val[e * H + h] * m;
+          if (red == RED_SUM) {
+            acc += (double)m;
+            sq += (double)m * (double)m;
+          } else if (best_e == -1 || m > best || (m == best && e < best_e)) {
+            best = m;
+            best_e = (int32_t)e;
+          }
+        }
+        if (red == RED_SUM) {
+          out[i * F + f] = (float)acc;
+          if (term_norm) term_norm[i * F + f] = sqrt(sq);
+        } else {
+          out[i * F + f] = best_e == -1 ? 0.0f : best;
+          arg[i * F + f] = best_e;
+        }
+      }
+    }
+  }
+  return bad ? -2 : 0;
+}
+
+/*
+ * Generalized SDDMM with the dot-product edge function (Sec. II-A Eq. 2 with
+ * psi(x_u, x_v, x_uv) = x_u x_v^T, Eq. 4), per head for multi-head attention
+ * (Fig. 4b: H dot products of length dh):
+ *   out[e, h] = (float) sum_k (double) Xs[u, h, k] * (double) Xd[v, h, k]
+ * for every stored edge (v <- u) with id e of the selected rows.  Outputs of
+ * edges outside the selected rows are left untouched.  term_norm (optional,
+ * indexed like out) receives sqrt(sum_k (Xs*Xd)^2).
+ */
+FGREF_EXPORT int fgref_gsddmm(int64_t num_rows, int64_t num_cols, const int32_t* indptr,
+                              const int32_t* indices, const int32_t* edge_ids, int64_t nnz_total,
+                              int64_t H, int64_t dh, const float* xs, const float* xd,
+                              const int64_t* rows, int64_t num_sel, float* out, double* term_norm,
+                              int num_threads) {
+  if (H < 1 || dh < 1 || num_rows < 0 || num_cols < 0 || !indptr || !out) return -1;
+  if (!rows && num_sel != num_rows) return -1;
+  if (check_rows(rows, num_sel, num_rows)) return -1;
+  set_threads(num_threads);
+  const int64_t F = H * dh;
+  int bad = 0;
+
+#pragma omp parallel for schedule(dynamic, 64) reduction(| : bad)
+  for (int64_t i = 0; i < num_sel; ++i) {
+    const int64_t v = pick_row(rows, i);
+    for (int64_t p = indptr[v]; p < indptr[v + 1]; ++p) {
+      const int64_t u = indices[p];
+      const int64_t e = edge_ids ? edge_ids[p] : p;
+      if (u < 0 || u >= num_cols || e < 0 || e >= nnz_total) { bad |= 1; continue; }
+      for (int64_t h = 0; h < H; ++h) {
+        double acc = 0.0, sq = 0.0;
+        for (int64_t k = 0; k < dh; ++k) {
+          const double t = (double)xs[u * F + h * dh + k] * (double)xd[v * F + h * dh + k];
+          acc += t;
+          sq += t * t;
+        }
+        out[e * H + h] = (float)acc;
+        if (term_norm) term_norm[e * H + h] = sqrt(sq);
+      }
+    }
+  }
+  return bad ? -2 : 0;
+}
+
+/*
+ * Edge softmax over each destination's in-edges, per head, optionally after
+ * a leaky ReLU (the attention normalisation of a graph attention layer):
+ *   s'  = s > 0 ? s : slope * s           (fp64)
+ *   out[e, h] = exp(s'_e - m) / sum_{p in row} exp(s'_p - m),  m = max_p s'_p
+ * Subtracting the row maximum does not change the value.  Rows with no edges
+ * write nothing.  Computed in fp64 and rounded to fp32 once.
+ */
+FGREF_EXPORT int fgref_edge_softmax(int64_t num_rows, const int32_t* indptr,
+                                    const int32_t* edge_ids, int64_t nnz_total, int64_t H,
+                                    const float* scores, int apply_leaky_relu, float slope,
+                                    const int64_t* rows, int64_t num_sel, float* out,
+                                    int num_threads) {
+  if (H < 1 || num_rows < 0 || !indptr || !scores || !out) return -1;
+  if (!rows && num_sel != num_rows) return -1;
+  if (check_rows(rows, num_sel, num_rows)) return -1;
+  set_threads(num_threads);
+  int bad = 0;
+
+#pragma omp parallel for schedule(dynamic, 64) reduction(| : bad)
+  for (int64_t i = 0; i < num_sel; ++i) {
+    const int64_t v = pick_row(rows, i);
+    const int64_t p0 = indptr[v], p1 = indptr[v + 1];
+    for (int64_t p = p0; p < p1; ++p) {
+      const int64_t e = edge_ids ? edge_ids[p] : p;
+      if (e < 0 || e >= nnz_total) bad |= 1;
+    }
+    if (bad) continue;
+    for (int64_t h = 0; h < H; ++h) {
+      double m = -INFINITY;
+      for (int64_t p = p0; p < p1; ++p) {
+        const int64_t e = edge_ids ? edge_ids[p] : p;
+        double s = scores[e * H + h];
+        if (apply_leaky_relu && !(s > 0.0)) s = (double)slope * s;
+        if (s > m) m = s;
+      }
+      double z = 0.0;
+      for (int64_t p = p0; p < p1; ++p) {
+        const int64_t e = edge_ids ? edge_ids[p] : p;
+        double s = scores[e * H + h];
+        if (apply_leaky_relu && !(s > 0.0)) s = (double)slope * s;
+        z += exp(s - m);
+      }
+      for (int64_t p = p0; p < p1; ++p) {
+        const int64_t e = edge_ids ? edge_ids[p] : p;
+        double s = scores[e * H + h];
+        if (apply_leaky_relu && !(s > 0.0)) s = (double)slope * s;
+        out[e * H + h] = (float)(exp(s - m) / z);
+      }
+    }
+  }
+  return bad ? -2 : 0;
+}
+
+FGREF_EXPORT int fgref_max_threads(void) { return omp_get_max_threads(); }

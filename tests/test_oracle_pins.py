@@ -1,0 +1,385 @@
+"""Pins of the CPU oracle against things other than itself.
+
+Each test ties one oracle function to a hand-worked example, a dense
+brute-force definition (numpy / scipy / torch autograd in fp64), a closed form
+or an invariant, so that a dropped term, a wrong sign or index, or a swapped
+operand in the oracle fails at least one of them.  CPU only.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+
+import synth
+from synth import CSR, coo_to_csr, csr_to_csc, csr_rows
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module")
+def O(oracle_lib):
+    return oracle_lib
+
+
+def _rand_graph(seed, n_rows=300, n_cols=None, e=3000, empty_frac=0.2):
+    rng = np.random.default_rng(seed)
+    n_cols = n_rows if n_cols is None else n_cols
+    return synth.small_random_graph(rng, n_rows, n_cols, e, empty_frac)
+
+
+def _dense_count(g: CSR) -> np.ndarray:
+    a = np.zeros((g.num_rows, g.num_cols), np.float64)
+    np.add.at(a, (csr_rows(g), g.indices), 1.0)
+    return a
+
+
+def _eids(g: CSR) -> np.ndarray:
+    return np.arange(g.nnz, dtype=np.int64) if g.edge_ids is None else g.edge_ids.astype(np.int64)
+
+
+# ---------------------------------------------------------------- golden
+
+
+def _golden_graph():
+    gd = json.load(open(os.path.join(GOLDEN, "hand_worked_4v.json")))
+    c = gd["csr_rows_are_destinations"]
+    g = CSR(4, 4, np.array(c["indptr"], np.int32), np.array(c["indices"], np.int32))
+    # the CSR must be what the generation-order edge list sorts into
+    e = np.array(gd["edges_src_to_dst_generation_order"])
+    g2 = coo_to_csr(e[:, 1], e[:, 0], 4, 4)
+    np.testing.assert_array_equal(g2.indptr, g.indptr)
+    np.testing.assert_array_equal(g2.indices, g.indices)
+    return gd, g
+
+
+def test_golden_spmm(O):
+    gd, g = _golden_graph()
+    x = np.array(gd["x"], np.float32)
+    w = np.array(gd["w"], np.float32)
+    out = O.gspmm(g, x)
+    np.testing.assert_array_equal(out, np.array(gd["copy_src_sum"]["value"], np.float32))
+    out, arg = O.gspmm(g, x, red=O.RED_MAX)
+    np.testing.assert_array_equal(out, np.array(gd["copy_src_max"]["value"], np.float32))
+    np.testing.assert_array_equal(arg, np.array(gd["copy_src_max"]["arg"], np.int32))
+    out = O.gspmm(g, x, msg=O.MSG_SRC_MUL_EDGE, edge_val=w)
+    np.testing.assert_array_equal(out, np.array(gd["src_mul_edge_sum"]["value"], np.float32))
+    out, arg = O.gspmm(g, x, msg=O.MSG_SRC_MUL_EDGE, red=O.RED_MAX, edge_val=w)
+    np.testing.assert_array_equal(out, np.array(gd["src_mul_edge_max"]["value"], np.float32))
+    np.testing.assert_array_equal(arg, np.array(gd["src_mul_edge_max"]["arg"], np.int32))
+
+
+def test_golden_sddmm_softmax(O):
+    gd, g = _golden_graph()
+    x = np.array(gd["x"], np.float32)
+    y = np.array(gd["y_dst"], np.float32)
+    s = O.gsddmm(g, x, y)[:, 0]
+    np.testing.assert_array_equal(s, np.array(gd["sddmm_dot_x_src_y_dst"]["value"], np.float32))
+    ent = gd["edge_softmax_of_sddmm_leaky_0.2"]
+    a = O.edge_softmax(g, s, leaky=True, slope=0.2)[:, 0]
+    np.testing.assert_allclose(a, ent["value"], rtol=1e-6, atol=0)
+    ent = gd["edge_softmax_of_sddmm_no_leaky"]
+    a = O.edge_softmax(g, np.array(ent["scores_override"], np.float32), leaky=False)[:, 0]
+    np.testing.assert_allclose(a, ent["value"], rtol=1e-6, atol=0)
+
+
+# ---------------------------------------------------------------- gSpMM sum
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_spmm_sum_equals_dense_product(O, seed):
+    g = _rand_graph(seed, n_rows=257, n_cols=190, e=4000)
+    x = np.random.default_rng(100 + seed).standard_normal((g.num_cols, 19)).astype(np.float32)
+    ref = _dense_count(g) @ x.astype(np.float64)
+    out = O.gspmm(g, x)
+    # one fp32 rounding of an fp64 sum: equal up to the last bit
+    np.testing.assert_allclose(out, ref, rtol=2.5e-7, atol=1e-12)
+
+
+@pytest.mark.parametrize("heads", [1, 4])
+def test_spmm_weighted_sum_equals_scipy(O, heads):
+    g = _rand_graph(7, n_rows=200, e=5000)
+    rng = np.random.default_rng(8)
+    dh = 6
+    x = rng.standard_normal((g.num_cols, heads * dh)).astype(np.float32)
+    w = rng.uniform(-2, 2, size=(g.nnz, heads)).astype(np.float32)
+    out = O.gspmm(g, x, msg=O.MSG_SRC_MUL_EDGE, edge_val=w, heads=heads)
+    for h in range(heads):
+        # scipy may canonicalise (sum duplicates in) the arrays it is given: pass copies
+        a = sp.csr_matrix((w[:, h].astype(np.float64), g.indices.copy(), g.indptr.copy()),
+                          shape=(g.num_rows, g.num_cols))
+        ref = a @ x[:, h * dh:(h + 1) * dh].astype(np.float64)
+        absref = abs(a) @ np.abs(x[:, h * dh:(h + 1) * dh].astype(np.float64))
+        # the oracle rounds each product to fp32 (<= 2^-24 relative per term)
+        err = np.abs(out[:, h * dh:(h + 1) * dh] - ref)
+        assert np.all(err <= 2.0 ** -23 * absref + 1e-30)
+
+
+def test_spmm_integer_inputs_exact(O):
+    g = _rand_graph(3, n_rows=500, e=20000, empty_frac=0.1)
+    rng = np.random.default_rng(4)
+    x = rng.integers(-8, 9, size=(g.num_cols, 5)).astype(np.float32)
+    w = rng.integers(-3, 4, size=g.nnz).astype(np.float32)
+    a = sp.csr_matrix((w.astype(np.int64), g.indices.copy(), g.indptr.copy()),
+                      shape=(g.num_rows, g.num_cols))
+    ref = a @ x.astype(np.int64)
+    out = O.gspmm(g, x, msg=O.MSG_SRC_MUL_EDGE, edge_val=w)
+    np.testing.assert_array_equal(out, ref.astype(np.float32))
+    ref = _dense_count(g).astype(np.int64) @ x.astype(np.int64)
+    np.testing.assert_array_equal(O.gspmm(g, x), ref.astype(np.float32))
+
+
+def test_spmm_ones_give_degrees(O):
+    g = _rand_graph(5, n_rows=400, e=6000, empty_frac=0.3)
+    ones = np.ones((g.num_cols, 3), np.float32)
+    out = O.gspmm(g, ones)
+    np.testing.assert_array_equal(out[:, 0], g.degrees().astype(np.float32))
+    # on the transposed graph the same features give out-degrees
+    csc = csr_to_csc(g)
+    out_t = O.gspmm(csc, np.ones((csc.num_cols, 2), np.float32))
+    np.testing.assert_array_equal(out_t[:, 1],
+                                  np.bincount(g.indices, minlength=g.num_cols).astype(np.float32))
+
+
+# ---------------------------------------------------------------- gSpMM max / argmax
+
+
+def _brute_max(g, x, w=None):
+    F = x.shape[1]
+    H = 1 if w is None else w.shape[1]
+    dh = F // H
+    eids = _eids(g)
+    out = np.zeros((g.num_rows, F), np.float32)
+    arg = np.full((g.num_rows, F), -1, np.int32)
+    for v in range(g.num_rows):
+        p = np.arange(g.indptr[v], g.indptr[v + 1])
+        if p.size == 0:
+            continue
+        m = x[g.indices[p]].astype(np.float32)
+        if w is not None:
+            m = (np.repeat(w[eids[p]], dh, axis=1) * m).astype(np.float32)
+        best = m.max(axis=0)
+        for f in range(F):
+            hit = eids[p][m[:, f] == best[f]]
+            out[v, f] = best[f]
+            arg[v, f] = hit.min()
+    return out, arg
+
+
+@pytest.mark.parametrize("transpose", [False, True])
+def test_spmm_max_argmax_brute_force(O, transpose):
+    g = _rand_graph(11, n_rows=120, e=2400, empty_frac=0.15)
+    if transpose:
+        g = csr_to_csc(g)  # edge ids are no longer positions
+    rng = np.random.default_rng(12)
+    x = rng.integers(-3, 4, size=(g.num_cols, 7)).astype(np.float32)  # many ties
+    out, arg = O.gspmm(g, x, red=O.RED_MAX, nnz_total=g.nnz)
+    bo, ba = _brute_max(g, x)
+    np.testing.assert_array_equal(out, bo)
+    np.testing.assert_array_equal(arg, ba)
+    w = rng.integers(-2, 3, size=(g.nnz, 1)).astype(np.float32)
+    out, arg = O.gspmm(g, x, msg=O.MSG_SRC_MUL_EDGE, red=O.RED_MAX, edge_val=w)
+    bo, ba = _brute_max(g, x, w)
+    np.testing.assert_array_equal(out, bo)
+    np.testing.assert_array_equal(arg, ba)
+
+
+def test_spmm_max_signed_zero_and_neg_inf(O):
+    # row 0: -0.0 (e0) and +0.0 (e1) tie -> e0 wins and its bits are kept
+    # row 1: +0.0 (e2) then -0.0 (e3) -> e2 wins, +0.0
+    # row 2: all -inf -> value -inf, first edge id
+    g = CSR(3, 4, np.array([0, 2, 4, 6], np.int32), np.array([0, 1, 1, 0, 2, 3], np.int32))
+    x = np.array([[-0.0], [0.0], [-np.inf], [-np.inf]], np.float32)
+    out, arg = O.gspmm(g, x, red=O.RED_MAX)
+    assert np.signbit(out[0, 0]) and arg[0, 0] == 0
+    assert not np.signbit(out[1, 0]) and arg[1, 0] == 2
+    assert out[2, 0] == -np.inf and arg[2, 0] == 4
+
+
+def test_spmm_max_all_equal_takes_first_edge(O):
+    g = _rand_graph(13, n_rows=50, e=500, empty_frac=0.0)
+    out, arg = O.gspmm(g, np.ones((g.num_cols, 2), np.float32), red=O.RED_MAX)
+    deg = g.degrees()
+    np.testing.assert_array_equal(arg[deg > 0, 0], g.indptr[:-1][deg > 0])
+    np.testing.assert_array_equal(out[deg > 0], 1.0)
+    np.testing.assert_array_equal(arg[deg == 0], -1)
+
+
+# ---------------------------------------------------------------- gSDDMM
+
+
+@pytest.mark.parametrize("heads,dh", [(1, 9), (3, 4)])
+def test_sddmm_equals_masked_dense_product(O, heads, dh):
+    g = _rand_graph(21, n_rows=150, n_cols=170, e=3000)
+    rng = np.random.default_rng(22)
+    xs = rng.standard_normal((g.num_cols, heads * dh)).astype(np.float32)
+    xd = rng.standard_normal((g.num_rows, heads * dh)).astype(np.float32)
+    out = O.gsddmm(g, xs, xd, heads=heads)
+    dst, src = csr_rows(g), g.indices
+    for h in range(heads):
+        sl = slice(h * dh, (h + 1) * dh)
+        dense = xd[:, sl].astype(np.float64) @ xs[:, sl].astype(np.float64).T  # [rows, cols]
+        ref = dense[dst, src]
+        np.testing.assert_allclose(out[:, h], ref, rtol=2.5e-7, atol=1e-12)
+
+
+def test_sddmm_integer_exact_and_transpose_consistent(O):
+    g = _rand_graph(23, n_rows=200, e=4000)
+    rng = np.random.default_rng(24)
+    x = rng.integers(-8, 9, size=(g.num_cols, 16)).astype(np.float32)
+    y = rng.integers(-8, 9, size=(g.num_rows, 16)).astype(np.float32)
+    out = O.gsddmm(g, x, y)[:, 0]
+    ref = np.einsum("ek,ek->e", x[g.indices].astype(np.int64), y[csr_rows(g)].astype(np.int64))
+    np.testing.assert_array_equal(out, ref.astype(np.float32))
+    # same edge values through the transposed graph (rows = sources, by edge id)
+    csc = csr_to_csc(g)
+    out_t = O.gsddmm(csc, y, x, nnz_total=g.nnz)[:, 0]
+    np.testing.assert_array_equal(out_t, out)
+
+
+# ---------------------------------------------------------------- duality / adjoint
+
+
+def test_adjoint_identity(O):
+    """<dY, A X> = <A^T dY, X> = sum_e SDDMM(X, dY)[e] (Sec. II-A: the gradient of
+    SpMM w.r.t. A is an SDDMM)."""
+    rng = np.random.default_rng(31)
+    g = synth.rmat_graph(np.random.SeedSequence(31), rng, 10, 1000, 20000)
+    csc = csr_to_csc(g)
+    x = rng.standard_normal((g.num_cols, 8)).astype(np.float32)
+    dy = rng.standard_normal((g.num_rows, 8)).astype(np.float32)
+    fwd = O.gspmm(g, x).astype(np.float64)
+    bwd = O.gspmm(csc, dy).astype(np.float64)
+    da = O.gsddmm(g, x, dy)[:, 0].astype(np.float64)
+    a = np.sum(dy * fwd)
+    b = np.sum(bwd * x)
+    c = np.sum(da)
+    scale = np.sum(np.abs(dy.astype(np.float64)) * (_dense_count(g) @ np.abs(x.astype(np.float64))))
+    assert abs(a - b) <= 1e-6 * scale
+    assert abs(a - c) <= 1e-6 * scale
+
+
+def test_edge_weight_gradient_is_sddmm(O):
+    """d<dY, A(w) X>/dw_e from torch autograd on a dense A(w) equals the SDDMM of
+    X and dY at edge e."""
+    torch = pytest.importorskip("torch")
+    g = _rand_graph(41, n_rows=60, n_cols=70, e=700)
+    rng = np.random.default_rng(42)
+    x = rng.standard_normal((g.num_cols, 5)).astype(np.float32)
+    dy = rng.standard_normal((g.num_rows, 5)).astype(np.float32)
+    w = torch.ones(g.nnz, dtype=torch.float64, requires_grad=True)
+    a = torch.zeros(g.num_rows, g.num_cols, dtype=torch.float64)
+    idx = (torch.from_numpy(csr_rows(g).astype(np.int64)), torch.from_numpy(g.indices.astype(np.int64)))
+    a = a.index_put(idx, w, accumulate=True)
+    loss = (torch.from_numpy(dy).double() * (a @ torch.from_numpy(x).double())).sum()
+    loss.backward()
+    da = O.gsddmm(g, x, dy)[:, 0]
+    np.testing.assert_allclose(da, w.grad.numpy(), rtol=2.5e-7, atol=1e-12)
+
+
+def test_sddmm_gradient_is_spmm(O):
+    """The gradient of an SDDMM is an SpMM (Sec. II-A): with scores
+    s_e = Xs[src]·Xd[dst] and upstream gradient g_e,
+    dL/dXs = SpMM over the transposed graph of Xd scaled by g (src_mul_edge, sum)."""
+    torch = pytest.importorskip("torch")
+    g = _rand_graph(43, n_rows=80, n_cols=90, e=900)
+    csc = csr_to_csc(g)
+    rng = np.random.default_rng(44)
+    xs = rng.standard_normal((g.num_cols, 6)).astype(np.float32)
+    xd = rng.standard_normal((g.num_rows, 6)).astype(np.float32)
+    ge = rng.standard_normal(g.nnz).astype(np.float32)
+    txs = torch.from_numpy(xs).double().requires_grad_(True)
+    s = (txs[torch.from_numpy(g.indices.astype(np.int64))]
+         * torch.from_numpy(xd).double()[torch.from_numpy(csr_rows(g).astype(np.int64))]).sum(1)
+    (s * torch.from_numpy(ge).double()).sum().backward()
+    dxs = O.gspmm(csc, xd, msg=O.MSG_SRC_MUL_EDGE, edge_val=ge.reshape(-1, 1))
+    # the oracle rounds g_e * Xd to fp32 per term
+    np.testing.assert_allclose(dxs, txs.grad.numpy(), rtol=1e-5, atol=1e-5)
+
+
+# ---------------------------------------------------------------- edge softmax
+
+
+@pytest.mark.parametrize("heads,leaky", [(1, True), (4, True), (2, False)])
+def test_edge_softmax_matches_torch_softmax(O, heads, leaky):
+    torch = pytest.importorskip("torch")
+    g = _rand_graph(51, n_rows=100, e=2500, empty_frac=0.2)
+    rng = np.random.default_rng(52)
+    s = (3 * rng.standard_normal((g.nnz, heads))).astype(np.float32)
+    out = O.edge_softmax(g, s, heads=heads, leaky=leaky, slope=0.2)
+    ts = torch.from_numpy(s).double()
+    if leaky:
+        ts = torch.nn.functional.leaky_relu(ts, negative_slope=float(np.float32(0.2)))
+    for v in range(g.num_rows):
+        a, b = g.indptr[v], g.indptr[v + 1]
+        if a == b:
+            continue
+        ref = torch.softmax(ts[a:b], dim=0).numpy()
+        np.testing.assert_allclose(out[a:b], ref, rtol=1e-6, atol=1e-12)
+
+
+def test_edge_softmax_invariants(O):
+    g = _rand_graph(53, n_rows=300, e=5000, empty_frac=0.2)
+    rng = np.random.default_rng(54)
+    s = rng.standard_normal((g.nnz, 3)).astype(np.float32) * 10
+    out = O.edge_softmax(g, s, heads=3)
+    rs = np.add.reduceat(out.astype(np.float64), g.indptr[:-1][g.degrees() > 0], axis=0)
+    np.testing.assert_allclose(rs, 1.0, rtol=0, atol=1e-6)
+    # equal scores -> 1/deg; a single edge -> 1
+    out = O.edge_softmax(g, np.full((g.nnz, 1), 0.7, np.float32))
+    deg = np.repeat(g.degrees(), g.degrees())
+    np.testing.assert_allclose(out[:, 0], 1.0 / deg, rtol=1e-7)
+    # empty rows write nothing: untouched outputs stay NaN-filled
+    assert not np.isnan(out).any()
+
+
+def test_edge_softmax_through_edge_ids(O):
+    """Softmax over the transposed graph normalises over out-edges, indexed by
+    edge id; the result equals a softmax grouped by source vertex."""
+    g = _rand_graph(55, n_rows=80, e=900, empty_frac=0.0)
+    csc = csr_to_csc(g)
+    s = np.random.default_rng(56).standard_normal((g.nnz, 1)).astype(np.float32)
+    out = O.edge_softmax(csc, s, leaky=False, nnz_total=g.nnz)[:, 0]
+    src = g.indices
+    for u in np.unique(src)[:40]:
+        m = src == u
+        e = np.exp(s[m, 0].astype(np.float64) - s[m, 0].max())
+        np.testing.assert_allclose(out[m], e / e.sum(), rtol=1e-6)
+
+
+# ---------------------------------------------------------------- determinism / row selection
+
+
+def test_thread_count_invariance_and_row_selection(O):
+    g = _rand_graph(61, n_rows=700, e=30000, empty_frac=0.1)
+    rng = np.random.default_rng(62)
+    x = rng.standard_normal((g.num_cols, 12)).astype(np.float32)
+    w = rng.random((g.nnz, 2)).astype(np.float32)
+    for kw in (dict(), dict(msg=O.MSG_SRC_MUL_EDGE, edge_val=w, heads=2)):
+        a1 = O.gspmm(g, x, threads=1, **kw)
+        a8 = O.gspmm(g, x, threads=8, **kw)
+        np.testing.assert_array_equal(a1, a8)
+        rows = rng.choice(g.num_rows, 50, replace=False)
+        np.testing.assert_array_equal(O.gspmm(g, x, rows=rows, **kw), a1[rows])
+        m1, i1 = O.gspmm(g, x, red=O.RED_MAX, threads=1, **kw)
+        m8, i8 = O.gspmm(g, x, red=O.RED_MAX, threads=8, **kw)
+        np.testing.assert_array_equal(m1, m8)
+        np.testing.assert_array_equal(i1, i8)
+    s1 = O.gsddmm(g, x, x[: g.num_rows], threads=1)
+    s8 = O.gsddmm(g, x, x[: g.num_rows], threads=8)
+    np.testing.assert_array_equal(s1, s8)
+    np.testing.assert_array_equal(O.edge_softmax(g, s1, threads=1), O.edge_softmax(g, s1, threads=8))
+
+
+def test_invalid_arguments_rejected(O):
+    g = _rand_graph(71, n_rows=10, e=30)
+    x = np.ones((g.num_cols, 4), np.float32)
+    with pytest.raises(ValueError):
+        O.gspmm(g, x, msg=O.MSG_SRC_MUL_EDGE)  # missing edge values
+    with pytest.raises(ValueError):
+        O.gspmm(g, x, rows=[0, 10])  # row out of range
+    bad = CSR(g.num_rows, g.num_cols, g.indptr, g.indices.copy())
+    bad.indices[0] = g.num_cols  # source out of range
+    with pytest.raises(ValueError):
+        O.gspmm(bad, x)
