@@ -1,0 +1,200 @@
+/*
+ * featgraph_hip.h -- C ABI of the gfx950 (MI355X) library for FeatGraph's two
+ * feature-dimension sparse templates (Hu et al., "FeatGraph: A Flexible and
+ * Efficient Backend for Graph Neural Network Systems", SC20):
+ *
+ *   generalized SpMM   (vertex-wise, Sec. II-A Eq. 1 and Eq. 3; the spmm
+ *                       template of Sec. III-B / Fig. 3)
+ *   generalized SDDMM  (edge-wise, Sec. II-A Eq. 2 and Eq. 4; the sddmm
+ *                       template of Sec. III-B / Fig. 4, multi-head Fig. 4b)
+ *   edge softmax       (per-destination normalisation of edge scores that
+ *                       sits between the two in an attention layer)
+ *
+ * The paper's user-defined message / edge functions become a closed set of
+ * operators (the builtin message functions it supports, Sec. III-B): copy the
+ * source feature, or multiply it by an edge value (one scalar per edge and
+ * head); reducers sum and max (with the edge id of the maximum).
+ *
+ * ---------------------------------------------------------------------------
+ * Conventions shared by every entry point
+ * ---------------------------------------------------------------------------
+ * Graph      CSR with rows = DESTINATION vertices (row v lists the in-edges of
+ *            v, so Eq. 1 reduces over in-neighbours).  indptr/indices/edge_ids
+ *            are int32 DEVICE arrays.  The edge id of stored entry p is
+ *            edge_ids[p], or p when edge_ids is NULL.  A transposed graph (CSC:
+ *            rows = source vertices) is passed the same way with edge_ids set
+ *            to the CSR positions, so edge data keeps one indexing.
+ * Features   fp32, row-major, DEVICE memory.  Vertex data is [vertices, H, dh]
+ *            (H heads of head_dim dh, F = H*dh floats per vertex); edge data is
+ *            [edge id, H].  All offsets are computed in 64-bit.
+ * Streams    `stream` is a hipStream_t passed as void* (NULL = null stream).
+ *            Every compute call only enqueues work on it and returns; device
+ *            faults surface at the caller's next synchronisation.
+ * Ownership  The caller owns every array and the stream.  The library allocates
+ *            device memory only in fg_plan_create (freed by fg_plan_destroy).
+ * Errors     The return code is the only error channel.  Argument checks run on
+ *            the host before anything is enqueued; on failure nothing is
+ *            written.  FG_ERR_HIP means a HIP call failed (launch or copy).
+ *            Indices are NOT range-checked on the device: a graph whose
+ *            indices/edge_ids lie outside [0, num_cols) / [0, nnz_total) is
+ *            undefined behaviour (check it on the host first).
+ * Aliasing   Outputs must not overlap inputs (checked where sizes are known).
+ * Limits     nnz <= INT32_MAX; F = H*dh <= FG_MAX_WIDTH.
+ * Precision  fp32 in, fp32 accumulate, fp32 out; no fast-math.  Max compares
+ *            the fp32 message values exactly (IEEE ==, so -0 == +0).
+ */
+#ifndef FEATGRAPH_HIP_H_
+#define FEATGRAPH_HIP_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FG_ABI_VERSION 1
+#define FG_MAX_WIDTH (1 << 16) /* largest supported F = H*dh */
+
+typedef enum fg_status {
+  FG_OK = 0,
+  FG_ERR_INVALID_ARG = -1, /* a host-side argument check failed */
+  FG_ERR_UNSUPPORTED = -2, /* valid but not implemented combination */
+  FG_ERR_HIP = -3,         /* a HIP runtime call failed */
+  FG_ERR_NO_MEMORY = -4    /* device or host allocation failed (plan only) */
+} fg_status;
+
+/* Message function phi of Eq. 1 (Sec. III-B builtins). */
+typedef enum fg_msg_op {
+  FG_MSG_COPY_SRC = 0,    /* m = x_src[u, h, :]                            */
+  FG_MSG_SRC_MUL_EDGE = 1 /* m = edge_val[e, h] * x_src[u, h, :]           */
+} fg_msg_op;
+
+/* Aggregator of Eq. 1 (any commutative reducer; sum as in GCN, Eq. 3; max as
+ * in GraphSage-style and MLP aggregation, Fig. 1). */
+typedef enum fg_reduce_op {
+  FG_REDUCE_SUM = 0, /* out = sum of messages; empty row -> 0                 */
+  FG_REDUCE_MAX = 1  /* out = max of messages and arg = the smallest edge id
+                        attaining it; empty row -> out 0, arg -1              */
+} fg_reduce_op;
+
+/* Edge function psi of Eq. 2. */
+typedef enum fg_edge_op {
+  FG_EDGE_DOT = 0 /* out[e, h] = sum_k x_src[u, h, k] * x_dst[v, h, k] (Eq. 4,
+                     per head as in Fig. 4b)                                 */
+} fg_edge_op;
+
+typedef struct fg_graph {
+  int64_t num_rows; /* destination vertices (CSR rows)                          */
+  int64_t num_cols; /* source vertices                                          */
+  int64_t nnz;      /* stored edges = indptr[num_rows]                          */
+  int64_t nnz_total;/* size of the edge-id space edge data is indexed by; 0
+                       means nnz (set it to the CSR's nnz for a transposed graph) */
+  const int32_t* indptr;   /* [num_rows+1], indptr[0] = 0, nondecreasing        */
+  const int32_t* indices;  /* [nnz] source vertex of each stored edge           */
+  const int32_t* edge_ids; /* [nnz] edge id of each stored edge, or NULL        */
+} fg_graph;
+
+/* ---------------------------------------------------------------------------
+ * Plan: the degree-aware work decomposition of one graph.
+ *
+ * Rows with more than `segment_edges` edges are cut into segments of that many
+ * edges, each handled by its own wavefront; their partial results are merged
+ * in segment order by a second, deterministic pass.  Long segments are
+ * scheduled first.  This replaces the paper's per-block row assignment
+ * (Sec. III-C, adaptive parallelization) with one that stays balanced on
+ * power-law graphs.  Built once per graph, like the per-topology kernels the
+ * paper amortises over training epochs (Sec. IV-B).
+ * ------------------------------------------------------------------------- */
+typedef struct fg_plan fg_plan; /* opaque; owns a device segment table + workspace */
+
+typedef struct fg_plan_options {
+  int32_t segment_edges; /* max edges per segment; 0 -> library default         */
+  int32_t reserved[7];   /* must be zero                                        */
+} fg_plan_options;
+
+typedef struct fg_plan_info {
+  int64_t num_rows, nnz;
+  int64_t num_segments;   /* wavefront work items                               */
+  int64_t num_split_rows; /* rows cut into more than one segment                */
+  int64_t num_slots;      /* segments of split rows (partial-result slots)      */
+  int64_t max_width;      /* largest F the workspace holds                      */
+  int64_t workspace_bytes;
+  int32_t segment_edges;
+  int32_t reserved;
+} fg_plan_info;
+
+/* One work item of the schedule (host view; the device table holds the same). */
+typedef struct fg_segment {
+  int32_t row;   /* destination row                                             */
+  int32_t begin; /* first stored edge (CSR position)                            */
+  int32_t end;   /* one past the last stored edge                               */
+  int32_t slot;  /* -1: whole row, results go to the output directly;
+                    >= 0: partial-result slot of a split row                    */
+} fg_segment;
+
+/* Builds the schedule on the host from a HOST copy of indptr.  Writes at most
+ * `capacity` segments to `segs` (may be NULL to only count) and the counts to
+ * the optional out-pointers.  Pure host function: no HIP call. */
+fg_status fg_schedule_host(const int32_t* indptr_host, int64_t num_rows, int32_t segment_edges,
+                           fg_segment* segs, int64_t capacity, int64_t* num_segments,
+                           int64_t* num_split_rows, int64_t* num_slots);
+
+/* Creates a plan for graph `g` and features up to `max_width` = H*dh floats.
+ * indptr_host: optional HOST copy of g->indptr (saves a device-to-host copy).
+ * opt: may be NULL.  Allocates device memory; synchronises `stream` once.
+ * The plan is bound to g->indptr, num_rows and nnz: calls with another graph
+ * are rejected with FG_ERR_INVALID_ARG.  A plan holds a mutable workspace:
+ * calls that share a plan must be ordered on one stream. */
+fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host, int64_t max_width,
+                         const fg_plan_options* opt, fg_plan** out, void* stream);
+fg_status fg_plan_destroy(fg_plan* plan);
+fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info);
+
+/* ---------------------------------------------------------------------------
+ * Generalized SpMM (Sec. II-A Eq. 1; Sec. III-B featgraph.spmm):
+ *   out[v, h, k] = (+)_{stored edges p of row v} phi(p)[h, k]
+ * x_src    [num_cols, H, dh]
+ * edge_val [nnz_total, H] indexed by edge id; required iff msg = SRC_MUL_EDGE
+ * out      [num_rows, H, dh]; every element is written
+ * arg_eid  [num_rows, H, dh] int32; required iff red = MAX, else must be NULL
+ * plan     NULL -> one wavefront per row (no load balancing); else a plan of
+ *          this graph with max_width >= H*dh
+ * Sums are fp32 in an order that depends on the schedule (deterministic for a
+ * given plan).  Max/argmax is exact and schedule-independent.
+ * ------------------------------------------------------------------------- */
+fg_status fg_gspmm(const fg_graph* g, fg_msg_op msg, fg_reduce_op red, int32_t num_heads,
+                   int64_t head_dim, const float* x_src, const float* edge_val, float* out,
+                   int32_t* arg_eid, fg_plan* plan, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Generalized SDDMM (Sec. II-A Eq. 2 and Eq. 4; Sec. III-B featgraph.sddmm;
+ * multi-head edge function of Fig. 4b):
+ *   out[e, h] = sum_k x_src[indices[p], h, k] * x_dst[v, h, k]
+ * for every stored edge p of every row v, e = its edge id.
+ * x_src [num_cols, H, dh]; x_dst [num_rows, H, dh]; out [nnz_total, H]
+ * (entries of edge ids not stored in g are left untouched).
+ * fp32 accumulation, tree reduction across the lanes that hold one head.
+ * ------------------------------------------------------------------------- */
+fg_status fg_gsddmm(const fg_graph* g, fg_edge_op op, int32_t num_heads, int64_t head_dim,
+                    const float* x_src, const float* x_dst, float* out, fg_plan* plan,
+                    void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Edge softmax over each row's stored edges, per head, optionally after a
+ * leaky ReLU:  s' = s > 0 ? s : negative_slope * s;
+ *              out[e, h] = exp(s'_e - m) / sum_row exp(s' - m),  m = row max.
+ * scores, out [nnz_total, H] indexed by edge id; rows without edges write
+ * nothing.  `out` may equal `scores` only if no two stored edges share an id.
+ * ------------------------------------------------------------------------- */
+fg_status fg_edge_softmax(const fg_graph* g, int32_t num_heads, const float* scores,
+                          int32_t apply_leaky_relu, float negative_slope, float* out,
+                          fg_plan* plan, void* stream);
+
+const char* fg_status_string(fg_status s); /* static storage, never NULL */
+int32_t fg_abi_version(void);              /* == FG_ABI_VERSION */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FEATGRAPH_HIP_H_ */

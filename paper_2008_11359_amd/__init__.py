@@ -1,0 +1,371 @@
+"""gfx950 (MI355X) generalized SpMM / SDDMM / edge softmax -- Python binding.
+
+Thin ctypes marshalling over the C ABI declared in ``include/featgraph_hip.h``
+(library ``_build/libfeatgraph_hip.so``).  PyTorch provides device memory and
+the current HIP stream; every step of the computation runs in the library's
+kernels.  There is no CPU fallback: importing this package fails when the
+library has not been built, and calls fail when a tensor is not on the GPU.
+
+    g = Graph.from_csr(csr)                   # device copy of a CSR (rows = destinations)
+    plan = Plan(g, max_width=128)             # degree-aware schedule, built once per graph
+    h = gspmm(g, x, plan=plan)                # copy_src + sum      (GCN aggregation, Eq. 3)
+    h, arg = gspmm(g, x, reduce="max", plan=plan)
+    s = gsddmm(g, x, x, plan=plan)            # per-edge dot        (Eq. 4)
+    a = edge_softmax(g, s, leaky=True, slope=0.2, plan=plan)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+try:
+    import torch
+except ImportError as exc:  # pragma: no cover
+    raise ImportError("paper_2008_11359_amd needs PyTorch (ROCm) for device memory") from exc
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_build", "libfeatgraph_hip.so")
+
+FG_OK, FG_ERR_INVALID_ARG, FG_ERR_UNSUPPORTED, FG_ERR_HIP, FG_ERR_NO_MEMORY = 0, -1, -2, -3, -4
+MSG_OPS = {"copy_src": 0, "src_mul_edge": 1}
+REDUCE_OPS = {"sum": 0, "max": 1}
+EDGE_OPS = {"dot": 0}
+ABI_VERSION = 1
+
+
+class FgError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__("%s: %s (status %d)" % (what, status_string(status), status))
+        self.status = status
+
+
+class _Graph(ctypes.Structure):
+    _fields_ = [
+        ("num_rows", ctypes.c_int64),
+        ("num_cols", ctypes.c_int64),
+        ("nnz", ctypes.c_int64),
+        ("nnz_total", ctypes.c_int64),
+        ("indptr", ctypes.c_void_p),
+        ("indices", ctypes.c_void_p),
+        ("edge_ids", ctypes.c_void_p),
+    ]
+
+
+class _PlanOptions(ctypes.Structure):
+    _fields_ = [("segment_edges", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7)]
+
+
+class _PlanInfo(ctypes.Structure):
+    _fields_ = [
+        ("num_rows", ctypes.c_int64),
+        ("nnz", ctypes.c_int64),
+        ("num_segments", ctypes.c_int64),
+        ("num_split_rows", ctypes.c_int64),
+        ("num_slots", ctypes.c_int64),
+        ("max_width", ctypes.c_int64),
+        ("workspace_bytes", ctypes.c_int64),
+        ("segment_edges", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
+class Segment(ctypes.Structure):
+    _fields_ = [("row", ctypes.c_int32), ("begin", ctypes.c_int32), ("end", ctypes.c_int32),
+                ("slot", ctypes.c_int32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            "HIP library %s is missing: build it with `python -m paper_2008_11359_amd.build` "
+            "(there is no CPU fallback)" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    gp = ctypes.POINTER(_Graph)
+    lib.fg_status_string.restype = ctypes.c_char_p
+    lib.fg_status_string.argtypes = [ctypes.c_int]
+    lib.fg_abi_version.restype = i32
+    lib.fg_schedule_host.restype = ctypes.c_int
+    lib.fg_schedule_host.argtypes = [vp, i64, i32, vp, i64, ctypes.POINTER(i64),
+                                     ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    lib.fg_plan_create.restype = ctypes.c_int
+    lib.fg_plan_create.argtypes = [gp, vp, i64, ctypes.POINTER(_PlanOptions),
+                                   ctypes.POINTER(vp), vp]
+    lib.fg_plan_destroy.restype = ctypes.c_int
+    lib.fg_plan_destroy.argtypes = [vp]
+    lib.fg_plan_get_info.restype = ctypes.c_int
+    lib.fg_plan_get_info.argtypes = [vp, ctypes.POINTER(_PlanInfo)]
+    lib.fg_gspmm.restype = ctypes.c_int
+    lib.fg_gspmm.argtypes = [gp, ctypes.c_int, ctypes.c_int, i32, i64, vp, vp, vp, vp, vp, vp]
+    lib.fg_gsddmm.restype = ctypes.c_int
+    lib.fg_gsddmm.argtypes = [gp, ctypes.c_int, i32, i64, vp, vp, vp, vp, vp]
+    lib.fg_edge_softmax.restype = ctypes.c_int
+    lib.fg_edge_softmax.argtypes = [gp, i32, vp, i32, ctypes.c_float, vp, vp, vp]
+    if lib.fg_abi_version() != ABI_VERSION:
+        raise ImportError("ABI version mismatch: library %d, binding %d"
+                          % (lib.fg_abi_version(), ABI_VERSION))
+    return lib
+
+
+_lib = _load()
+
+
+def status_string(status: int) -> str:
+    return _lib.fg_status_string(int(status)).decode()
+
+
+def _check(status: int, what: str) -> None:
+    if status != FG_OK:
+        raise FgError(status, what)
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _dev_tensor(t: torch.Tensor, dtype: torch.dtype, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor (there is no CPU path)" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return t
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+# ----------------------------------------------------------------------------
+# graphs and plans
+# ----------------------------------------------------------------------------
+
+
+class Graph:
+    """A CSR graph in device memory; rows are destination vertices.
+
+    ``edge_ids`` (optional) gives each stored edge's id; ``nnz_total`` is the
+    size of the edge-id space (for a transposed graph: the CSR's nnz).
+    """
+
+    def __init__(self, num_rows: int, num_cols: int, indptr: torch.Tensor, indices: torch.Tensor,
+                 edge_ids: Optional[torch.Tensor] = None, nnz_total: int = 0,
+                 indptr_host: Optional[np.ndarray] = None):
+        self.indptr = _dev_tensor(indptr, torch.int32, "indptr")
+        self.indices = _dev_tensor(indices, torch.int32, "indices")
+        self.edge_ids = None if edge_ids is None else _dev_tensor(edge_ids, torch.int32, "edge_ids")
+        if self.indptr.numel() != num_rows + 1:
+            raise ValueError("indptr must have num_rows + 1 entries")
+        self.num_rows = int(num_rows)
+        self.num_cols = int(num_cols)
+        self.nnz = int(self.indices.numel())
+        self.nnz_total = int(nnz_total) if nnz_total else self.nnz
+        if self.edge_ids is not None and self.edge_ids.numel() != self.nnz:
+            raise ValueError("edge_ids must have nnz entries")
+        self.indptr_host = None if indptr_host is None else np.ascontiguousarray(
+            indptr_host, dtype=np.int32)
+        self._c = _Graph(self.num_rows, self.num_cols, self.nnz, self.nnz_total,
+                         self.indptr.data_ptr(), self.indices.data_ptr() if self.nnz else None,
+                         _ptr(self.edge_ids))
+
+    @classmethod
+    def from_csr(cls, csr, device="cuda", nnz_total: int = 0, check: bool = True) -> "Graph":
+        """Copies a host CSR (numpy int32 ``indptr``/``indices``/``edge_ids``)
+        to the device.  With ``check`` the structure is validated on the host
+        first, since the kernels do not range-check indices."""
+        indptr = np.ascontiguousarray(csr.indptr, dtype=np.int32)
+        indices = np.ascontiguousarray(csr.indices, dtype=np.int32)
+        eids = getattr(csr, "edge_ids", None)
+        nt = int(nnz_total) if nnz_total else int(indptr[-1])
+        if check:
+            _check_host_csr(csr.num_rows, csr.num_cols, indptr, indices, eids, nt)
+        dev = torch.device(device)
+        t_ip = torch.from_numpy(indptr).to(dev)
+        t_ix = torch.from_numpy(indices).to(dev)
+        t_e = None if eids is None else torch.from_numpy(
+            np.ascontiguousarray(eids, dtype=np.int32)).to(dev)
+        return cls(csr.num_rows, csr.num_cols, t_ip, t_ix, t_e, nt, indptr_host=indptr)
+
+
+def _check_host_csr(num_rows, num_cols, indptr, indices, eids, nnz_total):
+    if indptr.shape != (num_rows + 1,) or indptr[0] != 0:
+        raise ValueError("bad indptr")
+    if num_rows and np.any(np.diff(indptr.astype(np.int64)) < 0):
+        raise ValueError("indptr must be nondecreasing")
+    nnz = int(indptr[-1])
+    if indices.shape != (nnz,):
+        raise ValueError("indices must have indptr[-1] entries")
+    if nnz and (indices.min() < 0 or indices.max() >= num_cols):
+        raise ValueError("indices out of range")
+    if eids is not None:
+        eids = np.asarray(eids)
+        if eids.shape != (nnz,) or (nnz and (eids.min() < 0 or eids.max() >= nnz_total)):
+            raise ValueError("edge_ids out of range")
+    elif nnz_total < nnz:
+        raise ValueError("nnz_total smaller than nnz")
+
+
+class Plan:
+    """Degree-aware schedule of one graph (segments of at most
+    ``segment_edges`` edges, partial-result workspace for features up to
+    ``max_width`` floats).  Owns device memory until ``close()``."""
+
+    def __init__(self, g: Graph, max_width: int, segment_edges: int = 0):
+        opt = _PlanOptions()
+        opt.segment_edges = int(segment_edges)
+        h = ctypes.c_void_p()
+        ip = g.indptr_host
+        st = _lib.fg_plan_create(ctypes.byref(g._c), None if ip is None else ip.ctypes.data,
+                                 int(max_width), ctypes.byref(opt), ctypes.byref(h), _stream())
+        _check(st, "fg_plan_create")
+        self._h = h
+        self.graph = g
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise ValueError("plan is closed")
+        return self._h
+
+    def info(self) -> dict:
+        inf = _PlanInfo()
+        _check(_lib.fg_plan_get_info(self.handle, ctypes.byref(inf)), "fg_plan_get_info")
+        return {k: getattr(inf, k) for k, _ in _PlanInfo._fields_ if k != "reserved"}
+
+    def close(self) -> None:
+        if self._h is not None:
+            torch.cuda.current_stream().synchronize()
+            _check(_lib.fg_plan_destroy(self._h), "fg_plan_destroy")
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def schedule_host(indptr: np.ndarray, segment_edges: int = 0):
+    """The plan's schedule computed on the host (no GPU needed).  Returns
+    (segments as an [n, 4] int32 array of row, begin, end, slot;
+    num_split_rows, num_slots)."""
+    ip = np.ascontiguousarray(indptr, dtype=np.int32)
+    n_seg, n_split, n_slot = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(_lib.fg_schedule_host(ip.ctypes.data, ip.size - 1, int(segment_edges), None, 0,
+                                 ctypes.byref(n_seg), ctypes.byref(n_split), ctypes.byref(n_slot)),
+           "fg_schedule_host")
+    segs = np.zeros((n_seg.value, 4), np.int32)
+    _check(_lib.fg_schedule_host(ip.ctypes.data, ip.size - 1, int(segment_edges),
+                                 segs.ctypes.data, n_seg.value, None, None, None),
+           "fg_schedule_host")
+    return segs, n_split.value, n_slot.value
+
+
+def _plan_handle(plan: Optional[Plan]):
+    return None if plan is None else plan.handle
+
+
+# ----------------------------------------------------------------------------
+# the three operators
+# ----------------------------------------------------------------------------
+
+
+def gspmm(g: Graph, x: torch.Tensor, edge: Optional[torch.Tensor] = None, msg: str = "copy_src",
+          reduce: str = "sum", heads: int = 1, plan: Optional[Plan] = None,
+          out: Optional[torch.Tensor] = None, arg: Optional[torch.Tensor] = None):
+    """Generalized SpMM: out[v] = reduce over in-edges (u -> v, id e) of
+    msg(x[u], edge[e]).  x: [num_cols, F] or [num_cols, H, dh] fp32.  edge:
+    [nnz_total] or [nnz_total, H] fp32 for msg='src_mul_edge'.  Returns out
+    (shape of x with num_rows rows) and, for reduce='max', the int32 edge id
+    of each maximum (-1 for rows without edges)."""
+    if msg not in MSG_OPS or reduce not in REDUCE_OPS:
+        raise ValueError("unknown msg %r or reduce %r" % (msg, reduce))
+    x = _dev_tensor(x, torch.float32, "x")
+    if x.shape[0] != g.num_cols:
+        raise ValueError("x must have num_cols rows")
+    F = int(np.prod(x.shape[1:])) if x.dim() > 1 else 1
+    if x.dim() == 3:
+        heads = int(x.shape[1])
+    if F % heads:
+        raise ValueError("feature width not divisible by heads")
+    dh = F // heads
+    if msg == "src_mul_edge":
+        if edge is None:
+            raise ValueError("src_mul_edge needs edge values")
+        edge = _dev_tensor(edge, torch.float32, "edge")
+        if edge.numel() != g.nnz_total * heads:
+            raise ValueError("edge must have nnz_total * heads values")
+    elif edge is not None:
+        raise ValueError("copy_src takes no edge values")
+    shape = (g.num_rows,) + tuple(x.shape[1:])
+    out = torch.empty(shape, dtype=torch.float32, device=x.device) if out is None else \
+        _dev_tensor(out, torch.float32, "out")
+    if out.numel() != g.num_rows * F:
+        raise ValueError("out has the wrong size")
+    if reduce == "max":
+        arg = torch.empty(shape, dtype=torch.int32, device=x.device) if arg is None else \
+            _dev_tensor(arg, torch.int32, "arg")
+        if arg.numel() != g.num_rows * F:
+            raise ValueError("arg has the wrong size")
+    else:
+        arg = None
+    st = _lib.fg_gspmm(ctypes.byref(g._c), MSG_OPS[msg], REDUCE_OPS[reduce], heads, dh,
+                       _ptr(x), _ptr(edge), _ptr(out), _ptr(arg), _plan_handle(plan), _stream())
+    _check(st, "fg_gspmm")
+    return (out, arg) if reduce == "max" else out
+
+
+def gsddmm(g: Graph, x_src: torch.Tensor, x_dst: Optional[torch.Tensor] = None, heads: int = 1,
+           op: str = "dot", plan: Optional[Plan] = None, out: Optional[torch.Tensor] = None):
+    """Generalized SDDMM: out[e, h] = x_src[u, h, :] . x_dst[v, h, :] for every
+    stored edge u -> v with id e.  x_dst defaults to x_src (square graphs).
+    Returns [nnz_total, H] (or [nnz_total] for H = 1 and 2-D inputs)."""
+    if op not in EDGE_OPS:
+        raise ValueError("unknown edge op %r" % op)
+    x_src = _dev_tensor(x_src, torch.float32, "x_src")
+    x_dst = x_src if x_dst is None else _dev_tensor(x_dst, torch.float32, "x_dst")
+    if x_src.shape[0] != g.num_cols or x_dst.shape[0] != g.num_rows:
+        raise ValueError("x_src needs num_cols rows and x_dst num_rows rows")
+    if x_src.shape[1:] != x_dst.shape[1:]:
+        raise ValueError("x_src and x_dst must have the same feature shape")
+    if x_src.dim() == 3:
+        heads = int(x_src.shape[1])
+    F = int(np.prod(x_src.shape[1:])) if x_src.dim() > 1 else 1
+    if F % heads:
+        raise ValueError("feature width not divisible by heads")
+    shape = (g.nnz_total, heads) if (heads > 1 or x_src.dim() == 3) else (g.nnz_total,)
+    out = torch.empty(shape, dtype=torch.float32, device=x_src.device) if out is None else \
+        _dev_tensor(out, torch.float32, "out")
+    if out.numel() != g.nnz_total * heads:
+        raise ValueError("out has the wrong size")
+    st = _lib.fg_gsddmm(ctypes.byref(g._c), EDGE_OPS[op], heads, F // heads, _ptr(x_src),
+                        _ptr(x_dst), _ptr(out), _plan_handle(plan), _stream())
+    _check(st, "fg_gsddmm")
+    return out
+
+
+def edge_softmax(g: Graph, scores: torch.Tensor, leaky: bool = True, slope: float = 0.2,
+                 plan: Optional[Plan] = None, out: Optional[torch.Tensor] = None):
+    """Softmax of edge scores [nnz_total] or [nnz_total, H] over each row's
+    stored edges, per head, after an optional leaky ReLU."""
+    scores = _dev_tensor(scores, torch.float32, "scores")
+    if scores.shape[0] != g.nnz_total:
+        raise ValueError("scores must have nnz_total rows")
+    heads = int(scores.shape[1]) if scores.dim() == 2 else 1
+    out = torch.empty_like(scores) if out is None else _dev_tensor(out, torch.float32, "out")
+    if out.numel() != scores.numel():
+        raise ValueError("out has the wrong size")
+    st = _lib.fg_edge_softmax(ctypes.byref(g._c), heads, _ptr(scores), 1 if leaky else 0,
+                              float(slope), _ptr(out), _plan_handle(plan), _stream())
+    _check(st, "fg_edge_softmax")
+    return out
+
+
+__all__ = ["Graph", "Plan", "gspmm", "gsddmm", "edge_softmax", "schedule_host", "FgError",
+           "status_string", "LIB_PATH"]

@@ -1,0 +1,53 @@
+// Internal interface between the C-ABI layer (fg_api.cpp) and the gfx950
+// kernels (fg_kernels.hip).  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace fg {
+
+// One wavefront work item.  Same layout as fg_segment in the public header.
+struct Seg {
+  int32_t row, begin, end, slot;
+};
+
+// One split row: its partial-result slots are [slot_begin, slot_end).
+struct Fix {
+  int32_t row, slot_begin, slot_end, pad;
+};
+
+// Device view of a plan (all pointers are device memory).
+struct PlanView {
+  const Seg* segs = nullptr;      // [num_segments]; segs[s].slot == s for s < num_slots
+  const Fix* fix = nullptr;       // [num_split_rows]
+  const int32_t* slot_fix = nullptr;  // [num_slots] -> index into fix
+  float* ws_f = nullptr;          // [num_slots * ws_width] partial values
+  int32_t* ws_i = nullptr;        // [num_slots * ws_width] partial argmax edge ids
+  int64_t num_segments = 0, num_split_rows = 0, num_slots = 0;
+  int64_t ws_width = 0;           // floats per slot
+};
+
+struct GraphView {
+  int64_t num_rows, num_cols, nnz, nnz_total;
+  const int32_t* indptr;
+  const int32_t* indices;
+  const int32_t* edge_ids;
+};
+
+enum MsgOp { kCopySrc = 0, kSrcMulEdge = 1 };
+enum RedOp { kSum = 0, kMax = 1 };
+
+// Each launcher enqueues its kernels on `stream` and returns the result of
+// hipGetLastError() after the last launch.  `plan` may be null (one wavefront
+// per row).  Arguments are assumed validated by the caller.
+hipError_t launch_gspmm(const GraphView& g, const PlanView* plan, int msg, int red, int64_t H,
+                        int64_t dh, const float* x, const float* ev, float* out, int32_t* arg,
+                        hipStream_t stream);
+hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, int64_t dh,
+                         const float* xs, const float* xd, float* out, hipStream_t stream);
+hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t H,
+                               const float* scores, bool leaky, float slope, float* out,
+                               hipStream_t stream);
+
+}  // namespace fg

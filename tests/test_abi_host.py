@@ -1,0 +1,205 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+public header declares, rejects invalid arguments on the host before any
+launch, and builds a correct degree-aware schedule."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2008_11359_amd as fg
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "featgraph_hip.h")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fg_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert len(names) >= 9
+    out = subprocess.run(["nm", "-D", "--defined-only", fg.LIB_PATH], check=True,
+                         capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (fg_\w+)", out))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    for n in names:
+        getattr(fg._lib, n)  # resolvable through ctypes too
+
+
+def test_version_and_status_strings():
+    assert fg._lib.fg_abi_version() == fg.ABI_VERSION == 1
+    for s in (0, -1, -2, -3, -4):
+        assert fg.status_string(s) and fg.status_string(s) != "unknown status"
+    assert fg.status_string(7) == "unknown status"
+
+
+def _graph_struct(num_rows=4, num_cols=4, nnz=7, nnz_total=0, fake=0x1000):
+    # fake, never dereferenced: every call below must fail host validation first
+    return fg._Graph(num_rows, num_cols, nnz, nnz_total, fake, fake + 0x100, None)
+
+
+FAKE_X, FAKE_OUT, FAKE_ARG, FAKE_EV = 0x10000, 0x20000, 0x30000, 0x40000
+
+
+@pytest.mark.parametrize("case", [
+    "null_graph", "neg_rows", "huge_nnz", "no_indptr", "zero_heads", "zero_dh", "too_wide",
+    "bad_msg", "bad_red", "mul_without_edge", "copy_with_edge", "max_without_arg",
+    "sum_with_arg", "no_x", "no_out", "out_aliases_x", "nnz_total_too_small"])
+def test_gspmm_rejects_invalid_arguments(case):
+    L = fg._lib
+    g = _graph_struct()
+    args = dict(msg=0, red=0, H=1, dh=4, x=FAKE_X, ev=None, out=FAKE_OUT, arg=None)
+    gp = ctypes.byref(g)
+    if case == "null_graph":
+        gp = None
+    elif case == "neg_rows":
+        g.num_rows = -1
+    elif case == "huge_nnz":
+        g.nnz = 1 << 31
+    elif case == "no_indptr":
+        g.indptr = None
+    elif case == "zero_heads":
+        args["H"] = 0
+    elif case == "zero_dh":
+        args["dh"] = 0
+    elif case == "too_wide":
+        args["H"], args["dh"] = 1 << 9, 1 << 8
+    elif case == "bad_msg":
+        args["msg"] = 5
+    elif case == "bad_red":
+        args["red"] = -1
+    elif case == "mul_without_edge":
+        args["msg"] = 1
+    elif case == "copy_with_edge":
+        args["ev"] = FAKE_EV
+    elif case == "max_without_arg":
+        args["red"] = 1
+    elif case == "sum_with_arg":
+        args["arg"] = FAKE_ARG
+    elif case == "no_x":
+        args["x"] = None
+    elif case == "no_out":
+        args["out"] = None
+    elif case == "out_aliases_x":
+        args["out"] = FAKE_X + 8
+    elif case == "nnz_total_too_small":
+        g.nnz_total = 3
+    st = L.fg_gspmm(gp, args["msg"], args["red"], args["H"], args["dh"], args["x"], args["ev"],
+                    args["out"], args["arg"], None, None)
+    assert st == fg.FG_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("case", ["bad_op", "no_xs", "no_out", "out_aliases_xd", "bad_heads"])
+def test_gsddmm_rejects_invalid_arguments(case):
+    L = fg._lib
+    g = _graph_struct()
+    op, H, dh, xs, xd, out = 0, 1, 4, FAKE_X, FAKE_X + 0x1000, FAKE_OUT
+    if case == "bad_op":
+        op = 3
+    elif case == "no_xs":
+        xs = None
+    elif case == "no_out":
+        out = None
+    elif case == "out_aliases_xd":
+        out = xd + 4
+    elif case == "bad_heads":
+        H = -2
+    assert L.fg_gsddmm(ctypes.byref(g), op, H, dh, xs, xd, out, None, None) == fg.FG_ERR_INVALID_ARG
+
+
+def test_edge_softmax_rejects_invalid_arguments():
+    L = fg._lib
+    g = _graph_struct()
+    assert L.fg_edge_softmax(ctypes.byref(g), 0, FAKE_X, 1, 0.2, FAKE_OUT, None, None) == -1
+    assert L.fg_edge_softmax(ctypes.byref(g), 1, None, 1, 0.2, FAKE_OUT, None, None) == -1
+    # partial overlap of out and scores (exact aliasing is allowed)
+    assert L.fg_edge_softmax(ctypes.byref(g), 1, FAKE_X, 1, 0.2, FAKE_X + 4, None, None) == -1
+
+
+def test_plan_create_rejects_invalid_arguments():
+    L = fg._lib
+    g = _graph_struct()
+    h = ctypes.c_void_p()
+    opt = fg._PlanOptions()
+    assert L.fg_plan_create(ctypes.byref(g), None, 0, None, ctypes.byref(h), None) == -1
+    assert L.fg_plan_create(ctypes.byref(g), None, 8, None, None, None) == -1
+    opt.reserved[2] = 1
+    assert L.fg_plan_create(ctypes.byref(g), None, 8, ctypes.byref(opt), ctypes.byref(h),
+                            None) == -1
+    opt.reserved[2] = 0
+    opt.segment_edges = -5
+    assert L.fg_plan_create(ctypes.byref(g), None, 8, ctypes.byref(opt), ctypes.byref(h),
+                            None) == -1
+    # an inconsistent host indptr is rejected before any device allocation
+    ip = np.array([0, 3, 2, 4, 7], np.int32)
+    assert L.fg_plan_create(ctypes.byref(g), ip.ctypes.data, 8, None, ctypes.byref(h),
+                            None) == -1
+    ip = np.array([0, 3, 4, 4, 6], np.int32)  # last entry != nnz
+    assert L.fg_plan_create(ctypes.byref(g), ip.ctypes.data, 8, None, ctypes.byref(h),
+                            None) == -1
+    assert L.fg_plan_destroy(None) == -1
+    assert L.fg_plan_get_info(None, None) == -1
+
+
+def test_binding_refuses_cpu_tensors():
+    csr = synth.small_random_graph(np.random.default_rng(0), 8, 8, 20)
+    with pytest.raises((ValueError, RuntimeError, AssertionError)):
+        fg.Graph(8, 8, torch.from_numpy(csr.indptr), torch.from_numpy(csr.indices))
+
+
+# ---------------------------------------------------------------- schedule
+
+
+def _check_schedule(indptr, S):
+    segs, n_split, n_slot = fg.schedule_host(indptr, S)
+    num_rows = indptr.size - 1
+    deg = np.diff(indptr.astype(np.int64))
+    # every edge covered exactly once, every row present
+    cover = np.zeros(int(indptr[-1]), np.int32)
+    rows_seen = np.zeros(num_rows, np.int32)
+    for r, b, e, s in segs:
+        assert indptr[r] <= b <= e <= indptr[r + 1]
+        cover[b:e] += 1
+        rows_seen[r] += 1
+    assert np.all(cover == 1)
+    assert np.all(rows_seen >= 1)
+    # split rows: deg > S, pieces <= S and balanced, slots = positions
+    split = deg > S
+    assert n_split == int(split.sum())
+    assert n_slot == int(np.sum(-(-deg[split] // S)))
+    assert np.all(segs[:n_slot, 3] == np.arange(n_slot))
+    assert np.all(segs[n_slot:, 3] == -1)
+    lens = segs[:, 2] - segs[:, 1]
+    assert np.all(lens <= S)
+    for r in np.nonzero(split)[0]:
+        ls = lens[:n_slot][segs[:n_slot, 0] == r]
+        assert ls.max() - ls.min() <= 1
+    # whole rows: decreasing degree, then empty rows
+    tail = lens[n_slot:]
+    assert np.all(np.diff(tail) <= 0)
+    assert np.all(rows_seen[~split] == 1)
+    return segs
+
+
+@pytest.mark.parametrize("S", [1, 7, 64, 1024])
+def test_schedule_covers_every_edge(S):
+    w = synth.make_config("rmat_233k_115m", scale_down=512)
+    _check_schedule(w.csr.indptr, S)
+
+
+def test_schedule_edge_cases():
+    _check_schedule(np.zeros(1, np.int32), 8)            # no rows
+    _check_schedule(np.zeros(6, np.int32), 8)            # only empty rows
+    _check_schedule(np.array([0, 100], np.int32), 8)     # one hub row
+    _check_schedule(np.array([0, 8, 16, 17], np.int32), 8)
+    with pytest.raises(fg.FgError):
+        fg.schedule_host(np.array([0, 5, 3], np.int32), 8)

@@ -1,0 +1,388 @@
+"""GPU path vs the CPU oracle, through the C ABI (via the ctypes binding).
+
+Tolerance (floating-point sums and dots): |y - ref| <= 1e-5 * sqrt(max(n, 1))
+* max(|ref|, ||t||_2), with n the reduction length (in-degree for sums and
+softmax, d or dh for dots) and ||t||_2 the L2 norm of the n fp64 terms from the
+oracle.  Softmax: |y - ref| <= 1e-5 * sqrt(n) * |ref| + 1e-12.  Max/argmax and
+integer-valued inputs: bit-exact.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from synth import csr_rows, csr_to_csc, make_config
+
+pytestmark = pytest.mark.gpu
+
+fg = None  # imported lazily so that collection works without the library
+
+
+def setup_module(module):
+    global fg
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    import paper_2008_11359_amd as _fg
+
+    fg = _fg
+    if not __import__("os").path.exists(O.lib_path()):
+        O.build()
+
+
+def say(*a):
+    print("[gpu]", *a, flush=True)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def assert_close_sum(y, ref, tnorm, n):
+    y = np.asarray(y, np.float64).reshape(ref.shape)
+    n = np.broadcast_to(np.maximum(np.asarray(n, np.float64), 1.0), ref.shape) if np.ndim(n) else \
+        np.full(ref.shape, max(float(n), 1.0))
+    bound = 1e-5 * np.sqrt(n) * np.maximum(np.abs(ref), tnorm)
+    err = np.abs(y - ref)
+    bad = err > bound
+    assert not bad.any(), "max excess %g at %s (y=%r ref=%r bound=%r)" % (
+        (err - bound).max(), np.argwhere(bad)[0], y[bad][0], ref[bad][0], bound[bad][0])
+
+
+def assert_close_softmax(y, ref, n):
+    y = np.asarray(y, np.float64)
+    ref = np.asarray(ref, np.float64)
+    bound = 1e-5 * np.sqrt(np.maximum(n, 1)) * np.abs(ref) + 1e-12
+    bad = np.abs(y - ref) > bound
+    assert not bad.any(), "softmax mismatch at %s: %r vs %r" % (np.argwhere(bad)[0], y[bad][0],
+                                                                 ref[bad][0])
+
+
+def row_edges(g, rows):
+    """Stored positions of the given rows (in row order)."""
+    return np.concatenate([np.arange(g.indptr[r], g.indptr[r + 1]) for r in rows] or
+                          [np.zeros(0, np.int64)]).astype(np.int64)
+
+
+def edge_ids_of(g, pos):
+    return pos if g.edge_ids is None else g.edge_ids[pos].astype(np.int64)
+
+
+def sample_rows(g, k, seed, extra=()):
+    rng = np.random.default_rng(seed)
+    deg = g.degrees()
+    top = np.argsort(-deg, kind="stable")[:8]
+    empty = np.nonzero(deg == 0)[0][:4]
+    rnd = rng.choice(g.num_rows, size=min(k, g.num_rows), replace=False)
+    return np.unique(np.concatenate([top, empty, rnd, np.asarray(extra, np.int64)])).astype(np.int64)
+
+
+# ----------------------------------------------------------------------------
+# one checker per operator, oracle on selected rows
+# ----------------------------------------------------------------------------
+
+
+def check_spmm(csr, G, x, rows=None, plan=None, edge=None, reduce="sum", heads=1,
+               nnz_total=None, exact=False):
+    F = int(np.prod(x.shape[1:]))
+    msg = "copy_src" if edge is None else "src_mul_edge"
+    tx = dev(x)
+    te = None if edge is None else dev(edge)
+    say("gspmm", msg, reduce, "rows=%d nnz=%d F=%d H=%d plan=%s" % (
+        csr.num_rows, csr.nnz, F, heads, None if plan is None else plan.info()["segment_edges"]))
+    res = fg.gspmm(G, tx, te, msg=msg, reduce=reduce, heads=heads, plan=plan)
+    sel = np.arange(csr.num_rows) if rows is None else rows
+    kw = dict(msg=O.MSG_COPY_SRC if edge is None else O.MSG_SRC_MUL_EDGE, heads=heads,
+              edge_val=None if edge is None else edge.reshape(-1, heads), rows=rows,
+              nnz_total=nnz_total)
+    x2 = x.reshape(csr.num_cols, F)
+    if reduce == "max":
+        out, arg = host(res[0]).reshape(csr.num_rows, F), host(res[1]).reshape(csr.num_rows, F)
+        ro, ra = O.gspmm(csr, x2, red=O.RED_MAX, **kw)
+        np.testing.assert_array_equal(out[sel].view(np.uint32), ro.view(np.uint32))
+        np.testing.assert_array_equal(arg[sel], ra)
+        return res
+    out = host(res).reshape(csr.num_rows, F)
+    ro, norm = O.gspmm(csr, x2, red=O.RED_SUM, with_norm=True, **kw)
+    if exact:
+        np.testing.assert_array_equal(out[sel], ro)
+    else:
+        deg = csr.degrees()[sel][:, None]
+        assert_close_sum(out[sel], ro.astype(np.float64), norm, deg)
+    return res
+
+
+def check_sddmm(csr, G, xs, xd, rows=None, plan=None, heads=1, nnz_total=None, exact=False):
+    F = int(np.prod(xs.shape[1:]))
+    say("gsddmm rows=%d nnz=%d F=%d H=%d plan=%s" % (
+        csr.num_rows, csr.nnz, F, heads, None if plan is None else plan.info()["segment_edges"]))
+    res = fg.gsddmm(G, dev(xs), dev(xd), heads=heads, plan=plan)
+    nt = csr.nnz if nnz_total is None else nnz_total
+    out = host(res).reshape(nt, heads)
+    ro, norm = O.gsddmm(csr, xs.reshape(csr.num_cols, F), xd.reshape(csr.num_rows, F),
+                        heads=heads, rows=rows, nnz_total=nt, with_norm=True)
+    sel = np.arange(csr.num_rows) if rows is None else rows
+    e = edge_ids_of(csr, row_edges(csr, sel))
+    if exact:
+        np.testing.assert_array_equal(out[e], ro[e])
+    else:
+        assert_close_sum(out[e], ro[e].astype(np.float64), norm[e], F // heads)
+    return res
+
+
+def check_softmax(csr, G, scores, rows=None, plan=None, heads=1, leaky=True, nnz_total=None):
+    say("edge_softmax rows=%d nnz=%d H=%d" % (csr.num_rows, csr.nnz, heads))
+    ts = dev(scores)
+    res = fg.edge_softmax(G, ts, leaky=leaky, slope=0.2, plan=plan)
+    nt = csr.nnz if nnz_total is None else nnz_total
+    out = host(res).reshape(nt, heads)
+    ro = O.edge_softmax(csr, scores.reshape(nt, heads), heads=heads, leaky=leaky, slope=0.2,
+                        rows=rows, nnz_total=nt)
+    sel = np.arange(csr.num_rows) if rows is None else rows
+    pos = row_edges(csr, sel)
+    e = edge_ids_of(csr, pos)
+    deg = np.repeat(csr.degrees()[sel], csr.degrees()[sel])[:, None]
+    assert_close_softmax(out[e], ro[e], deg)
+    return res
+
+
+def plans_for(G, width, sizes=(0, 1, 5, 64)):
+    yield None
+    for s in sizes:
+        yield fg.Plan(G, max_width=width, segment_edges=s)
+
+
+# ----------------------------------------------------------------------------
+# tiny uniform graph: every operator, exact and rounded inputs, many schedules
+# ----------------------------------------------------------------------------
+
+
+def test_tiny_uniform_all_ops():
+    w = make_config("tiny_uniform_1k")
+    csr = w.csr
+    G = fg.Graph.from_csr(csr)
+    x = w.arrays["x"]
+    xi = np.random.default_rng(5).integers(-8, 9, size=x.shape).astype(np.float32)
+    wgt = np.random.default_rng(6).random(csr.nnz, dtype=np.float32)
+    for plan in plans_for(G, 32):
+        check_spmm(csr, G, x, plan=plan)
+        check_spmm(csr, G, xi, plan=plan, exact=True)
+        check_spmm(csr, G, x, plan=plan, reduce="max")
+        check_spmm(csr, G, xi, plan=plan, reduce="max")  # many ties
+        check_spmm(csr, G, x, plan=plan, edge=wgt)
+        check_spmm(csr, G, x, plan=plan, edge=wgt, reduce="max")
+        s = check_sddmm(csr, G, x, x, plan=plan)
+        check_sddmm(csr, G, xi, xi, plan=plan, exact=True)
+        check_softmax(csr, G, host(s), plan=plan)
+        check_softmax(csr, G, host(s), plan=plan, leaky=False)
+
+
+# ----------------------------------------------------------------------------
+# widths, heads, fallbacks and edge cases on a small power-law graph
+# ----------------------------------------------------------------------------
+
+
+@pytest.fixture(scope="module")
+def small_rmat():
+    rng = np.random.default_rng(77)
+    csr = synth.rmat_graph(np.random.SeedSequence(77), rng, 11, 2000, 40000)
+    deg = csr.degrees()
+    assert deg.max() > 500 and (deg == 0).any()
+    return csr, fg.Graph.from_csr(csr)
+
+
+@pytest.mark.parametrize("d", [1, 3, 16, 32, 33, 64, 128, 257, 512, 1040])
+def test_widths(small_rmat, d):
+    csr, G = small_rmat
+    rng = np.random.default_rng(d)
+    x = rng.standard_normal((csr.num_cols, d)).astype(np.float32)
+    xd = rng.standard_normal((csr.num_rows, d)).astype(np.float32)
+    wgt = rng.random(csr.nnz, dtype=np.float32)
+    for plan in plans_for(G, d, sizes=(64,)):
+        check_spmm(csr, G, x, plan=plan)
+        check_spmm(csr, G, x, plan=plan, reduce="max")
+        check_spmm(csr, G, x, plan=plan, edge=wgt)
+        check_sddmm(csr, G, x, xd, plan=plan)
+
+
+@pytest.mark.parametrize("heads,dh", [(8, 16), (2, 4), (4, 8), (3, 12), (8, 6), (5, 3), (2, 64),
+                                      (70, 2)])
+def test_heads(small_rmat, heads, dh):
+    csr, G = small_rmat
+    rng = np.random.default_rng(heads * 100 + dh)
+    x = rng.standard_normal((csr.num_cols, heads, dh)).astype(np.float32)
+    for plan in plans_for(G, heads * dh, sizes=(64,)):
+        s = check_sddmm(csr, G, x, x, plan=plan, heads=heads)
+        a = check_softmax(csr, G, host(s), plan=plan, heads=heads)
+        check_spmm(csr, G, x, plan=plan, edge=host(a), heads=heads)
+        check_spmm(csr, G, x, plan=plan, edge=host(a), heads=heads, reduce="max")
+
+
+def test_transposed_graph_with_edge_ids(small_rmat):
+    csr, _ = small_rmat
+    csc = csr_to_csc(csr)
+    G = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+    rng = np.random.default_rng(3)
+    y = rng.standard_normal((csc.num_cols, 24)).astype(np.float32)
+    x = rng.standard_normal((csc.num_rows, 24)).astype(np.float32)
+    wgt = rng.random((csr.nnz, 1), dtype=np.float32)
+    for plan in plans_for(G, 24, sizes=(16,)):
+        check_spmm(csc, G, y, plan=plan, nnz_total=csr.nnz)
+        check_spmm(csc, G, y, plan=plan, edge=wgt, nnz_total=csr.nnz)
+        check_spmm(csc, G, y, plan=plan, reduce="max", nnz_total=csr.nnz)
+        check_sddmm(csc, G, y, x, plan=plan, nnz_total=csr.nnz)
+        check_softmax(csc, G, rng.standard_normal(csr.nnz).astype(np.float32), plan=plan,
+                      nnz_total=csr.nnz)
+
+
+def test_edge_cases():
+    # no rows at all
+    empty = synth.CSR(0, 5, np.zeros(1, np.int32), np.zeros(0, np.int32))
+    G = fg.Graph.from_csr(empty)
+    out = fg.gspmm(G, dev(np.ones((5, 4), np.float32)))
+    assert out.shape == (0, 4)
+    # rows but no edges: sum 0, max 0 / -1, sddmm / softmax write nothing
+    noedge = synth.CSR(3, 5, np.zeros(4, np.int32), np.zeros(0, np.int32))
+    G = fg.Graph.from_csr(noedge)
+    for plan in (None, fg.Plan(G, 8, 4)):
+        o = host(fg.gspmm(G, dev(np.ones((5, 8), np.float32)), plan=plan))
+        assert np.all(o == 0)
+        o, a = fg.gspmm(G, dev(np.ones((5, 8), np.float32)), reduce="max", plan=plan)
+        assert np.all(host(o) == 0) and np.all(host(a) == -1)
+        s = fg.gsddmm(G, dev(np.ones((5, 8), np.float32)), dev(np.ones((3, 8), np.float32)),
+                      plan=plan)
+        assert s.numel() == 0
+    # signed zeros, -inf rows, duplicate edges, single-edge rows
+    g = synth.CSR(4, 4, np.array([0, 2, 4, 6, 7], np.int32),
+                  np.array([0, 1, 1, 0, 2, 3, 1], np.int32))
+    x = np.array([[-0.0, 1.0], [0.0, 1.0], [-np.inf, -np.inf], [-np.inf, 5.0]], np.float32)
+    G = fg.Graph.from_csr(g)
+    for plan in (None, fg.Plan(G, 2, 1)):
+        check_spmm(g, G, x, plan=plan, reduce="max")
+    dup = synth.CSR(2, 3, np.array([0, 5, 6], np.int32), np.array([1, 1, 1, 2, 2, 0], np.int32))
+    G = fg.Graph.from_csr(dup)
+    xi = np.array([[1, 2, 3, 4], [5, 5, 5, 5], [5, 0, 5, 0]], np.float32)
+    for plan in (None, fg.Plan(G, 4, 2)):
+        check_spmm(dup, G, xi, plan=plan, reduce="max")
+        check_spmm(dup, G, xi, plan=plan, exact=True)
+        s = check_sddmm(dup, G, xi, xi[:2], plan=plan, exact=True)
+        a = host(fg.edge_softmax(G, dev(np.full(6, 3.0, np.float32)), plan=plan))
+        np.testing.assert_allclose(a, [0.2] * 5 + [1.0], rtol=1e-6)
+        del s
+
+
+def test_determinism_and_plan_independence(small_rmat):
+    csr, G = small_rmat
+    x = np.random.default_rng(9).standard_normal((csr.num_cols, 128)).astype(np.float32)
+    tx = dev(x)
+    plan = fg.Plan(G, 128, 32)
+    a1 = host(fg.gspmm(G, tx, plan=plan))
+    a2 = host(fg.gspmm(G, tx, plan=plan))
+    np.testing.assert_array_equal(a1.view(np.uint32), a2.view(np.uint32))
+    m1, i1 = (host(t) for t in fg.gspmm(G, tx, reduce="max", plan=plan))
+    m0, i0 = (host(t) for t in fg.gspmm(G, tx, reduce="max"))
+    np.testing.assert_array_equal(m1.view(np.uint32), m0.view(np.uint32))
+    np.testing.assert_array_equal(i1, i0)
+    s1 = host(fg.gsddmm(G, tx, tx[: csr.num_rows].contiguous(), plan=plan))
+    s2 = host(fg.gsddmm(G, tx, tx[: csr.num_rows].contiguous()))
+    np.testing.assert_array_equal(s1.view(np.uint32), s2.view(np.uint32))
+
+
+def test_plan_bound_to_its_graph(small_rmat):
+    csr, G = small_rmat
+    other = fg.Graph.from_csr(csr)  # same structure, different device arrays
+    plan = fg.Plan(G, 16)
+    x = dev(np.ones((csr.num_cols, 16), np.float32))
+    with pytest.raises(fg.FgError):
+        fg.gspmm(other, x, plan=plan)
+    with pytest.raises(fg.FgError):
+        fg.gspmm(G, dev(np.ones((csr.num_cols, 32), np.float32)), plan=plan)  # too wide
+
+
+# ----------------------------------------------------------------------------
+# the five named workloads at full size (sampled rows against the oracle)
+# ----------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("d", [32, 64, 128, 256, 512])
+def test_uniform_deg100_full(d):
+    w = make_config("uniform_deg100_100k", d=d)
+    csr = w.csr
+    G = fg.Graph.from_csr(csr)
+    x = w.arrays["x"]
+    rows = sample_rows(csr, 3000, d)
+    plan = fg.Plan(G, d)
+    check_spmm(csr, G, x, rows=rows, plan=plan)
+    check_sddmm(csr, G, x, x, rows=rows, plan=plan)
+    # property over every row: all-ones features sum to the in-degree (100)
+    o = host(fg.gspmm(G, dev(np.ones((csr.num_cols, d), np.float32)), plan=plan))
+    assert np.all(o == 100.0)
+
+
+@pytest.fixture(scope="module")
+def rmat_full():
+    w = make_config("rmat_233k_115m")
+    return w, fg.Graph.from_csr(w.csr)
+
+
+@pytest.mark.slow
+def test_rmat_233k_full(rmat_full):
+    w, G = rmat_full
+    csr = w.csr
+    x, wgt = w.arrays["x"], w.arrays["w"]
+    plan = fg.Plan(G, 128)
+    info = plan.info()
+    say("plan", info)
+    assert info["num_split_rows"] > 0
+    rows = sample_rows(csr, 2000, 3)
+    check_spmm(csr, G, x, rows=rows, plan=plan, edge=wgt)
+    check_spmm(csr, G, x, rows=rows, plan=plan, reduce="max")
+    s = check_sddmm(csr, G, x, x, rows=rows, plan=plan)
+    check_softmax(csr, G, host(s), rows=rows, plan=plan)
+    o = host(fg.gspmm(G, dev(np.ones((csr.num_cols, 128), np.float32)), plan=plan))
+    np.testing.assert_array_equal(o[:, 0], csr.degrees().astype(np.float32))
+    np.testing.assert_array_equal(o[:, 127], csr.degrees().astype(np.float32))
+
+
+@pytest.mark.slow
+def test_clustered_gat_layer_full():
+    w = make_config("clustered_133k_deg300")
+    csr = w.csr
+    G = fg.Graph.from_csr(csr)
+    x = w.arrays["x"]
+    plan = fg.Plan(G, 128)
+    rows = sample_rows(csr, 1500, 4)
+    s = check_sddmm(csr, G, x, x, rows=rows, plan=plan, heads=8)
+    a = check_softmax(csr, G, host(s), rows=rows, plan=plan, heads=8)
+    check_spmm(csr, G, x, rows=rows, plan=plan, edge=host(a), heads=8)
+    # softmax rows sum to one for every row and head
+    rs = np.add.reduceat(host(a).astype(np.float64), csr.indptr[:-1], axis=0)
+    np.testing.assert_allclose(rs, 1.0, atol=1e-5 * math.sqrt(300))
+
+
+@pytest.mark.slow
+def test_rmat_train_step_full():
+    w = make_config("rmat_1m_33m_train")
+    csr, csc = w.csr, w.csc
+    Gf = fg.Graph.from_csr(csr)
+    Gb = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+    x, dy = w.arrays["x"], w.arrays["dy"]
+    pf, pb = fg.Plan(Gf, 256), fg.Plan(Gb, 256)
+    rows_f = sample_rows(csr, 1500, 5)
+    rows_b = sample_rows(csc, 1500, 6)
+    y = check_spmm(csr, Gf, x, rows=rows_f, plan=pf)
+    dx = check_spmm(csc, Gb, dy, rows=rows_b, plan=pb, nnz_total=csr.nnz)
+    da = check_sddmm(csr, Gf, x, dy, rows=rows_f, plan=pf)
+    # adjoint identity over the whole graph: <dY, A X> = <A^T dY, X> = sum_e dA_e
+    tdy, tx = dev(dy).double(), dev(x).double()
+    a = float((tdy * y.double()).sum())
+    b = float((dx.double() * tx).sum())
+    c = float(da.double().sum())
+    scale = float((tdy.abs() * fg.gspmm(Gf, dev(np.abs(x)), plan=pf).double()).sum())
+    assert abs(a - b) <= 1e-5 * scale and abs(a - c) <= 1e-5 * scale
