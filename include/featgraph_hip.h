@@ -97,9 +97,10 @@ typedef struct fg_graph {
 /* ---------------------------------------------------------------------------
  * Plan: the degree-aware work decomposition of one graph.
  *
- * Rows with more than `segment_edges` edges are cut into segments of that many
- * edges, each handled by its own wavefront; their partial results are merged
- * in segment order by a second, deterministic pass.  Long segments are
+ * Rows with more than `segment_edges` edges are cut into k = ceil(deg / S)
+ * segments of (nearly) equal length, at most `max_row_segments` per row (longer
+ * segments beyond that), each handled by its own wavefront; their partial
+ * results are merged by a second, deterministic pass.  Long segments are
  * scheduled first.  This replaces the paper's per-block row assignment
  * (Sec. III-C, adaptive parallelization) with one that stays balanced on
  * power-law graphs.  Built once per graph, like the per-topology kernels the
@@ -108,8 +109,9 @@ typedef struct fg_graph {
 typedef struct fg_plan fg_plan; /* opaque; owns a device segment table + workspace */
 
 typedef struct fg_plan_options {
-  int32_t segment_edges; /* max edges per segment; 0 -> library default         */
-  int32_t reserved[7];   /* must be zero                                        */
+  int32_t segment_edges;    /* S: target edges per segment; 0 -> default (1024) */
+  int32_t max_row_segments; /* cap on segments per row; 0 -> default (128)      */
+  int32_t reserved[6];      /* must be zero                                     */
 } fg_plan_options;
 
 typedef struct fg_plan_info {
@@ -120,7 +122,7 @@ typedef struct fg_plan_info {
   int64_t max_width;      /* largest F the workspace holds                      */
   int64_t workspace_bytes;
   int32_t segment_edges;
-  int32_t reserved;
+  int32_t max_row_segments;
 } fg_plan_info;
 
 /* One work item of the schedule (host view; the device table holds the same). */
@@ -132,12 +134,14 @@ typedef struct fg_segment {
                     >= 0: partial-result slot of a split row                    */
 } fg_segment;
 
-/* Builds the schedule on the host from a HOST copy of indptr.  Writes at most
- * `capacity` segments to `segs` (may be NULL to only count) and the counts to
- * the optional out-pointers.  Pure host function: no HIP call. */
-fg_status fg_schedule_host(const int32_t* indptr_host, int64_t num_rows, int32_t segment_edges,
-                           fg_segment* segs, int64_t capacity, int64_t* num_segments,
-                           int64_t* num_split_rows, int64_t* num_slots);
+/* Builds the schedule on the host from a HOST copy of indptr (opt may be NULL).
+ * Writes at most `capacity` segments to `segs` (may be NULL to only count) and
+ * the counts to the optional out-pointers.  Pure host function: no HIP call.
+ * Order: segments of split rows first (longest segments first; segs[s].slot
+ * == s), then whole rows by decreasing degree, then rows without edges. */
+fg_status fg_schedule_host(const int32_t* indptr_host, int64_t num_rows,
+                           const fg_plan_options* opt, fg_segment* segs, int64_t capacity,
+                           int64_t* num_segments, int64_t* num_split_rows, int64_t* num_slots);
 
 /* Creates a plan for graph `g` and features up to `max_width` = H*dh floats.
  * indptr_host: optional HOST copy of g->indptr (saves a device-to-host copy).

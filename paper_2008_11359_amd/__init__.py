@@ -55,7 +55,8 @@ class _Graph(ctypes.Structure):
 
 
 class _PlanOptions(ctypes.Structure):
-    _fields_ = [("segment_edges", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7)]
+    _fields_ = [("segment_edges", ctypes.c_int32), ("max_row_segments", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 6)]
 
 
 class _PlanInfo(ctypes.Structure):
@@ -68,7 +69,7 @@ class _PlanInfo(ctypes.Structure):
         ("max_width", ctypes.c_int64),
         ("workspace_bytes", ctypes.c_int64),
         ("segment_edges", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("max_row_segments", ctypes.c_int32),
     ]
 
 
@@ -89,8 +90,9 @@ def _load():
     lib.fg_status_string.argtypes = [ctypes.c_int]
     lib.fg_abi_version.restype = i32
     lib.fg_schedule_host.restype = ctypes.c_int
-    lib.fg_schedule_host.argtypes = [vp, i64, i32, vp, i64, ctypes.POINTER(i64),
-                                     ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    lib.fg_schedule_host.argtypes = [vp, i64, ctypes.POINTER(_PlanOptions), vp, i64,
+                                     ctypes.POINTER(i64), ctypes.POINTER(i64),
+                                     ctypes.POINTER(i64)]
     lib.fg_plan_create.restype = ctypes.c_int
     lib.fg_plan_create.argtypes = [gp, vp, i64, ctypes.POINTER(_PlanOptions),
                                    ctypes.POINTER(vp), vp]
@@ -212,13 +214,14 @@ def _check_host_csr(num_rows, num_cols, indptr, indices, eids, nnz_total):
 
 
 class Plan:
-    """Degree-aware schedule of one graph (segments of at most
-    ``segment_edges`` edges, partial-result workspace for features up to
-    ``max_width`` floats).  Owns device memory until ``close()``."""
+    """Degree-aware schedule of one graph: rows longer than ``segment_edges``
+    are cut into equal segments (at most ``max_row_segments`` per row), with a
+    partial-result workspace for features up to ``max_width`` floats.  Zero
+    selects the library defaults.  Owns device memory until ``close()``."""
 
-    def __init__(self, g: Graph, max_width: int, segment_edges: int = 0):
-        opt = _PlanOptions()
-        opt.segment_edges = int(segment_edges)
+    def __init__(self, g: Graph, max_width: int, segment_edges: int = 0,
+                 max_row_segments: int = 0):
+        opt = _options(segment_edges, max_row_segments)
         h = ctypes.c_void_p()
         ip = g.indptr_host
         st = _lib.fg_plan_create(ctypes.byref(g._c), None if ip is None else ip.ctypes.data,
@@ -236,7 +239,7 @@ class Plan:
     def info(self) -> dict:
         inf = _PlanInfo()
         _check(_lib.fg_plan_get_info(self.handle, ctypes.byref(inf)), "fg_plan_get_info")
-        return {k: getattr(inf, k) for k, _ in _PlanInfo._fields_ if k != "reserved"}
+        return {k: getattr(inf, k) for k, _ in _PlanInfo._fields_}
 
     def close(self) -> None:
         if self._h is not None:
@@ -251,17 +254,25 @@ class Plan:
             pass
 
 
-def schedule_host(indptr: np.ndarray, segment_edges: int = 0):
+def _options(segment_edges: int = 0, max_row_segments: int = 0) -> _PlanOptions:
+    opt = _PlanOptions()
+    opt.segment_edges = int(segment_edges)
+    opt.max_row_segments = int(max_row_segments)
+    return opt
+
+
+def schedule_host(indptr: np.ndarray, segment_edges: int = 0, max_row_segments: int = 0):
     """The plan's schedule computed on the host (no GPU needed).  Returns
     (segments as an [n, 4] int32 array of row, begin, end, slot;
     num_split_rows, num_slots)."""
     ip = np.ascontiguousarray(indptr, dtype=np.int32)
+    opt = _options(segment_edges, max_row_segments)
     n_seg, n_split, n_slot = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
-    _check(_lib.fg_schedule_host(ip.ctypes.data, ip.size - 1, int(segment_edges), None, 0,
+    _check(_lib.fg_schedule_host(ip.ctypes.data, ip.size - 1, ctypes.byref(opt), None, 0,
                                  ctypes.byref(n_seg), ctypes.byref(n_split), ctypes.byref(n_slot)),
            "fg_schedule_host")
     segs = np.zeros((n_seg.value, 4), np.int32)
-    _check(_lib.fg_schedule_host(ip.ctypes.data, ip.size - 1, int(segment_edges),
+    _check(_lib.fg_schedule_host(ip.ctypes.data, ip.size - 1, ctypes.byref(opt),
                                  segs.ctypes.data, n_seg.value, None, None, None),
            "fg_schedule_host")
     return segs, n_split.value, n_slot.value

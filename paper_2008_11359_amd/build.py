@@ -30,6 +30,18 @@ DEVICE = [
 ]
 
 
+def source_digest() -> str:
+    """SHA-256 over the library sources; identifies the kernels a profile
+    or counter measurement was taken with."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     objs = []

@@ -14,10 +14,10 @@
 struct fg_plan {
   int64_t num_rows = 0, nnz = 0, max_width = 0;
   const int32_t* indptr = nullptr;  // device pointer the plan was built for
-  int32_t segment_edges = 0;
+  int32_t segment_edges = 0, max_row_segments = 0;
   int device = 0;
   fg::PlanView view;
-  void* mem[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+  void* mem[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   int64_t workspace_bytes = 0;
 };
 
@@ -25,6 +25,8 @@ namespace {
 
 constexpr int32_t kDefaultSegmentEdges = 1024;
 constexpr int32_t kMaxSegmentEdges = 1 << 24;
+constexpr int32_t kDefaultMaxRowSegments = 128;
+constexpr int32_t kMaxRowSegmentsLimit = 1 << 20;
 
 fg_status check_graph(const fg_graph* g) {
   if (!g) return FG_ERR_INVALID_ARG;
@@ -83,47 +85,81 @@ bool indptr_valid(const int32_t* ip, int64_t num_rows, int64_t nnz) {
   return true;
 }
 
-// The schedule.  Order: segments of split rows first (their slot equals their
-// position), then whole rows by decreasing degree (ties by row id), empty rows
-// last -- long work items start first so the tail of the launch stays short.
-void build_schedule(const int32_t* ip, int64_t num_rows, int32_t S, std::vector<fg::Seg>& segs,
-                    std::vector<fg::Fix>& fix, std::vector<int32_t>& slot_fix) {
+// Segment length and count of one row: k = ceil(deg / S) pieces, at most
+// `cap`; a row is split when k >= 2.
+struct Cut {
+  int64_t k;
+};
+
+Cut cut_row(int64_t deg, int32_t S, int32_t cap) {
+  int64_t k = deg > S ? (deg + S - 1) / S : 1;
+  if (k > cap) k = cap;
+  return Cut{k};
+}
+
+// The schedule.  Order: segments of split rows first, rows with the longest
+// segments first (ties by row id), slots numbered in that order so slot ==
+// position; then whole rows by decreasing degree (ties by row id); rows
+// without edges last.  Long work items start first, which keeps the tail of a
+// launch short (longest-processing-time-first list scheduling).
+void build_schedule(const int32_t* ip, int64_t num_rows, int32_t S, int32_t cap,
+                    std::vector<fg::Seg>& segs, std::vector<fg::Fix>& fix,
+                    std::vector<int32_t>& slot_fix) {
   segs.clear();
   fix.clear();
   slot_fix.clear();
-  std::vector<int32_t> whole;
-  std::vector<int32_t> empty;
+  std::vector<int32_t> split, whole, empty;
   for (int64_t r = 0; r < num_rows; ++r) {
     const int64_t deg = (int64_t)ip[r + 1] - ip[r];
-    if (deg > S) {
-      const int64_t k = (deg + S - 1) / S;  // pieces of (nearly) equal length
-      fg::Fix fx;
-      fx.row = (int32_t)r;
-      fx.slot_begin = (int32_t)segs.size();
-      for (int64_t i = 0; i < k; ++i) {
-        fg::Seg s;
-        s.row = (int32_t)r;
-        s.begin = (int32_t)(ip[r] + deg * i / k);
-        s.end = (int32_t)(ip[r] + deg * (i + 1) / k);
-        s.slot = (int32_t)segs.size();
-        slot_fix.push_back((int32_t)fix.size());
-        segs.push_back(s);
-      }
-      fx.slot_end = (int32_t)segs.size();
-      fx.pad = 0;
-      fix.push_back(fx);
-    } else if (deg > 0) {
-      whole.push_back((int32_t)r);
-    } else {
-      empty.push_back((int32_t)r);
-    }
+    if (deg == 0) empty.push_back((int32_t)r);
+    else if (cut_row(deg, S, cap).k >= 2) split.push_back((int32_t)r);
+    else whole.push_back((int32_t)r);
   }
-  std::stable_sort(whole.begin(), whole.end(), [ip](int32_t a, int32_t b) {
-    return ip[a + 1] - ip[a] > ip[b + 1] - ip[b];
+  auto deg_of = [ip](int32_t r) { return (int64_t)ip[r + 1] - ip[r]; };
+  std::stable_sort(split.begin(), split.end(), [&](int32_t a, int32_t b) {
+    const int64_t da = deg_of(a), db = deg_of(b);
+    const int64_t ka = cut_row(da, S, cap).k, kb = cut_row(db, S, cap).k;
+    return da * kb > db * ka;  // da/ka > db/kb: longer segments first
   });
+  std::stable_sort(whole.begin(), whole.end(),
+                   [&](int32_t a, int32_t b) { return deg_of(a) > deg_of(b); });
+  for (int32_t r : split) {
+    const int64_t deg = deg_of(r);
+    const int64_t k = cut_row(deg, S, cap).k;
+    fg::Fix fx;
+    fx.row = r;
+    fx.slot_begin = (int32_t)segs.size();
+    for (int64_t i = 0; i < k; ++i) {
+      fg::Seg s;
+      s.row = r;
+      s.begin = (int32_t)(ip[r] + deg * i / k);
+      s.end = (int32_t)(ip[r] + deg * (i + 1) / k);
+      s.slot = (int32_t)segs.size();
+      slot_fix.push_back((int32_t)fix.size());
+      segs.push_back(s);
+    }
+    fx.slot_end = (int32_t)segs.size();
+    fx.pad = 0;
+    fix.push_back(fx);
+  }
   segs.reserve(segs.size() + whole.size() + empty.size());
   for (int32_t r : whole) segs.push_back(fg::Seg{r, ip[r], ip[r + 1], -1});
   for (int32_t r : empty) segs.push_back(fg::Seg{r, ip[r], ip[r], -1});
+}
+
+fg_status read_options(const fg_plan_options* opt, int32_t* S, int32_t* cap) {
+  *S = kDefaultSegmentEdges;
+  *cap = kDefaultMaxRowSegments;
+  if (!opt) return FG_OK;
+  for (int32_t r : opt->reserved)
+    if (r != 0) return FG_ERR_INVALID_ARG;
+  if (opt->segment_edges < 0 || opt->segment_edges > kMaxSegmentEdges) return FG_ERR_INVALID_ARG;
+  if (opt->max_row_segments < 0 || opt->max_row_segments > kMaxRowSegmentsLimit)
+    return FG_ERR_INVALID_ARG;
+  if (opt->segment_edges) *S = opt->segment_edges;
+  if (opt->max_row_segments) *cap = opt->max_row_segments;
+  if (*cap < 2) return FG_ERR_INVALID_ARG;
+  return FG_OK;
 }
 
 }  // namespace
@@ -143,19 +179,20 @@ const char* fg_status_string(fg_status s) {
 
 int32_t fg_abi_version(void) { return FG_ABI_VERSION; }
 
-fg_status fg_schedule_host(const int32_t* indptr_host, int64_t num_rows, int32_t segment_edges,
-                           fg_segment* segs, int64_t capacity, int64_t* num_segments,
-                           int64_t* num_split_rows, int64_t* num_slots) {
+fg_status fg_schedule_host(const int32_t* indptr_host, int64_t num_rows,
+                           const fg_plan_options* opt, fg_segment* segs, int64_t capacity,
+                           int64_t* num_segments, int64_t* num_split_rows, int64_t* num_slots) {
   if (!indptr_host || num_rows < 0 || num_rows >= INT32_MAX || capacity < 0)
     return FG_ERR_INVALID_ARG;
-  if (segment_edges < 0 || segment_edges > kMaxSegmentEdges) return FG_ERR_INVALID_ARG;
-  const int32_t S = segment_edges ? segment_edges : kDefaultSegmentEdges;
+  int32_t S, cap;
+  fg_status st = read_options(opt, &S, &cap);
+  if (st != FG_OK) return st;
   if (!indptr_valid(indptr_host, num_rows, indptr_host[num_rows])) return FG_ERR_INVALID_ARG;
   std::vector<fg::Seg> s;
   std::vector<fg::Fix> fx;
   std::vector<int32_t> sf;
   try {
-    build_schedule(indptr_host, num_rows, S, s, fx, sf);
+    build_schedule(indptr_host, num_rows, S, cap, s, fx, sf);
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
   }
@@ -196,13 +233,8 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host, int64_t 
   fg_status st = check_graph(g);
   if (st != FG_OK) return st;
   if (max_width < 1 || max_width > FG_MAX_WIDTH) return FG_ERR_INVALID_ARG;
-  int32_t S = kDefaultSegmentEdges;
-  if (opt) {
-    for (int32_t r : opt->reserved)
-      if (r != 0) return FG_ERR_INVALID_ARG;
-    if (opt->segment_edges < 0 || opt->segment_edges > kMaxSegmentEdges) return FG_ERR_INVALID_ARG;
-    if (opt->segment_edges) S = opt->segment_edges;
-  }
+  int32_t S, cap;
+  if ((st = read_options(opt, &S, &cap)) != FG_OK) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
 
   std::vector<int32_t> ip_copy;
@@ -226,7 +258,7 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host, int64_t 
   std::vector<int32_t> slot_fix;
   fg_plan* p = nullptr;
   try {
-    build_schedule(ip, g->num_rows, S, segs, fix, slot_fix);
+    build_schedule(ip, g->num_rows, S, cap, segs, fix, slot_fix);
     p = new fg_plan();
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
@@ -236,6 +268,7 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host, int64_t 
   p->max_width = max_width;
   p->indptr = g->indptr;
   p->segment_edges = S;
+  p->max_row_segments = cap;
   if (hipGetDevice(&p->device) != hipSuccess) {
     delete p;
     return FG_ERR_HIP;
@@ -243,14 +276,16 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host, int64_t 
   const int64_t nslots = (int64_t)slot_fix.size();
   // workspace per slot: F partial values (sum / max) or 2*H softmax pairs
   const int64_t ws_width = 2 * max_width;
-  const size_t bytes[5] = {
+  const int64_t nsplit = (int64_t)fix.size();
+  const size_t bytes[6] = {
       sizeof(fg::Seg) * std::max<size_t>(segs.size(), 1),
       sizeof(fg::Fix) * std::max<size_t>(fix.size(), 1),
       sizeof(int32_t) * std::max<size_t>(slot_fix.size(), 1),
       sizeof(float) * (size_t)std::max<int64_t>(nslots * ws_width, 1),
       sizeof(int32_t) * (size_t)std::max<int64_t>(nslots * max_width, 1),
+      sizeof(float) * (size_t)std::max<int64_t>(nsplit * ws_width, 1),
   };
-  for (int i = 0; i < 5; ++i) {
+  for (int i = 0; i < 6; ++i) {
     if (hipMalloc(&p->mem[i], bytes[i]) != hipSuccess) {
       p->mem[i] = nullptr;
       fg_plan_destroy(p);
@@ -277,11 +312,12 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host, int64_t 
   p->view.slot_fix = static_cast<const int32_t*>(p->mem[2]);
   p->view.ws_f = static_cast<float*>(p->mem[3]);
   p->view.ws_i = static_cast<int32_t*>(p->mem[4]);
+  p->view.ws_row = static_cast<float*>(p->mem[5]);
   p->view.num_segments = (int64_t)segs.size();
   p->view.num_split_rows = (int64_t)fix.size();
   p->view.num_slots = nslots;
   p->view.ws_width = ws_width;
-  p->workspace_bytes = (int64_t)(bytes[3] + bytes[4]);
+  p->workspace_bytes = (int64_t)(bytes[3] + bytes[4] + bytes[5]);
   *out = p;
   return FG_OK;
 }
@@ -297,6 +333,7 @@ fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info) {
   info->max_width = plan->max_width;
   info->workspace_bytes = plan->workspace_bytes;
   info->segment_edges = plan->segment_edges;
+  info->max_row_segments = plan->max_row_segments;
   return FG_OK;
 }
 

@@ -24,6 +24,7 @@ struct PlanView {
   const int32_t* slot_fix = nullptr;  // [num_slots] -> index into fix
   float* ws_f = nullptr;          // [num_slots * ws_width] partial values
   int32_t* ws_i = nullptr;        // [num_slots * ws_width] partial argmax edge ids
+  float* ws_row = nullptr;        // [num_split_rows * ws_width] merged per-row values
   int64_t num_segments = 0, num_split_rows = 0, num_slots = 0;
   int64_t ws_width = 0;           // floats per slot
 };

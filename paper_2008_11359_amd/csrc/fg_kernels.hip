@@ -6,14 +6,15 @@
 // or a segment of a row taken from the plan's degree-aware schedule.  The
 // feature dimension is spread across lanes (the paper binds it to threads,
 // Sec. III-B GPU FDS and Sec. III-C vertex parallelization) with float4
-// accesses, so one X row of 128 floats is one 512-byte request of 32 lanes and
-// a wavefront works on 64/G edges at once, G = lanes per feature row.
-// Neighbour indices (and edge values) of up to 64 edges are fetched with one
-// coalesced load per lane and broadcast to the lanes that need them with
-// cross-lane permutes.  SDDMM dot products reduce across the lanes of a
-// feature row with xor butterflies (the paper's tree reduction, Fig. 4 FDS).
-// No atomics: split rows write partial results that a second kernel merges in
-// a fixed order, so every result is deterministic for a given plan.
+// accesses: G lanes cover one feature row (G*4 floats per pass), so one row of
+// 128 floats is one 512-byte request of 32 lanes and a wavefront works on
+// 64/G edges at once.  Neighbour indices (and edge values) of up to 64 edges
+// are fetched with one coalesced load per lane and handed to the lane groups
+// with scalar readlanes (one or two groups) or cross-lane permutes.  SDDMM dot
+// products reduce across the lanes of a feature row with DPP row operations
+// (the paper's tree reduction, Fig. 4 FDS), never through memory.  No atomics:
+// split rows write partial results that a second kernel merges in a fixed
+// order, so every result is deterministic for a given plan.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <math.h>
@@ -70,6 +71,56 @@ __device__ __forceinline__ bool takes_over(float m, int32_t e, float best, int32
   return m > best || (m == best && e < best_e);
 }
 
+// ---- cross-lane primitives --------------------------------------------------
+
+// DPP controls (GFX9 encoding, valid on gfx950).
+constexpr int kDppQuadXor1 = 0xB1;      // quad_perm:[1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;      // quad_perm:[2,3,0,1]
+constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppRowMirror = 0x140;
+constexpr int kDppRowBcast15 = 0x142;   // lane 15 of each row -> next row
+constexpr int kDppRowBcast31 = 0x143;   // lane 31 -> rows 2 and 3
+
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROW_MASK, 0xF, false));
+}
+
+// Sum over aligned groups of W lanes (W a power of two <= 64).  The total is
+// valid in lane W-1 of every group; for W <= 16 in every lane of the group.
+// Every lane of the wavefront must execute this.
+template <int W>
+__device__ __forceinline__ float group_sum(float v) {
+  if constexpr (W >= 2) v += dpp_f<kDppQuadXor1>(v);
+  if constexpr (W >= 4) v += dpp_f<kDppQuadXor2>(v);
+  if constexpr (W >= 8) v += dpp_f<kDppRowHalfMirror>(v);
+  if constexpr (W >= 16) v += dpp_f<kDppRowMirror>(v);
+  if constexpr (W >= 32) v += dpp_f<kDppRowBcast15, 0xA>(v);
+  if constexpr (W >= 64) v += dpp_f<kDppRowBcast31, 0x8>(v);
+  return v;
+}
+
+// Value of lane (jb + gid) where jb is wave-uniform and gid < NG is the lane
+// group of the caller.  One or two groups use scalar readlanes.
+template <int NG>
+__device__ __forceinline__ int bcast_lane(int v, int jb, int gid) {
+  if constexpr (NG == 1) {
+    return __builtin_amdgcn_readlane(v, jb);
+  } else if constexpr (NG == 2) {
+    const int a = __builtin_amdgcn_readlane(v, jb);
+    const int b = __builtin_amdgcn_readlane(v, jb + 1);
+    return gid ? b : a;
+  } else {
+    return __shfl(v, jb + gid);
+  }
+}
+
+template <int NG>
+__device__ __forceinline__ float bcast_lane_f(float v, int jb, int gid) {
+  return __builtin_bit_cast(float, bcast_lane<NG>(__builtin_bit_cast(int, v), jb, gid));
+}
+
 // ----------------------------------------------------------------------------
 // generalized SpMM
 // ----------------------------------------------------------------------------
@@ -89,55 +140,87 @@ struct SpmmParams {
   int64_t F;
   int32_t H;
   int32_t dh;
-  int32_t logG;
+  int32_t logG;  // runtime group width (generic kernel only)
 };
 
-// VEC: floats per lane access (4 or 1); NV: accesses per lane per edge (the
-// feature chunk is G*VEC*NV floats, chunk index = blockIdx.y); U: edges in
-// flight per lane group; MUL: src_mul_edge message; MAX: max/argmax reducer;
-// SEG: items come from a plan.
-template <int VEC, int NV, int U, bool MUL, bool MAX, bool SEG>
-__global__ __launch_bounds__(kBlock) void spmm_kernel(SpmmParams p) {
+struct Item {
+  int64_t row, b, e;
+  int32_t slot;
+};
+
+template <bool SEG>
+__device__ __forceinline__ Item load_item(const Seg* segs, const int32_t* indptr, int64_t item) {
+  Item it;
+  if constexpr (SEG) {
+    const Seg s = segs[item];
+    it.row = s.row; it.b = s.begin; it.e = s.end; it.slot = s.slot;
+  } else {
+    it.row = item; it.b = indptr[item]; it.e = indptr[item + 1]; it.slot = -1;
+  }
+  return it;
+}
+
+// Writes one lane's accumulated vector: to the plan workspace for a split
+// row's segment, else to the output (max: empty -> 0 / -1).
+template <int VEC, bool MAX, bool SEG>
+__device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, int64_t f,
+                                           const float (&acc)[VEC], const int32_t (&am)[VEC]) {
+  if (SEG && it.slot >= 0) {
+    store_vec<VEC>(p.ws_f + (int64_t)it.slot * p.F + f, acc);
+    if constexpr (MAX) store_vec_i<VEC>(p.ws_i + (int64_t)it.slot * p.F + f, am);
+  } else if constexpr (MAX) {
+    float o[VEC];
+    int32_t a[VEC];
+#pragma unroll
+    for (int c = 0; c < VEC; ++c) {
+      const bool none = am[c] == INT_MAX;
+      o[c] = none ? 0.0f : acc[c];
+      a[c] = none ? -1 : am[c];
+    }
+    store_vec<VEC>(p.out + it.row * p.F + f, o);
+    store_vec_i<VEC>(p.arg + it.row * p.F + f, a);
+  } else {
+    store_vec<VEC>(p.out + it.row * p.F + f, acc);
+  }
+}
+
+// Fast path: float4 lanes, G (compile time) lanes per feature row, NV float4
+// per lane per edge (feature chunk G*4*NV = blockIdx.y), U edges in flight per
+// lane group, MUL: src_mul_edge, MAX: max/argmax, SEG: items from a plan.
+template <int G, int NV, int U, bool MUL, bool MAX, bool SEG>
+__global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
+  constexpr int NG = kWave / G;
+  static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
-  int64_t row, b, e;
-  int32_t slot = -1;
-  if constexpr (SEG) {
-    const Seg s = p.segs[item];
-    row = s.row; b = s.begin; e = s.end; slot = s.slot;
-  } else {
-    row = item; b = p.indptr[item]; e = p.indptr[item + 1];
-  }
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
   const int lane = lane_id();
-  const int G = 1 << p.logG;
-  const int ngroups = kWave >> p.logG;
-  const int gid = lane >> p.logG;
-  const int li = lane & (G - 1);
+  const int gid = lane / G;
+  const int li = lane % G;
   const int64_t F = p.F;
-  const int64_t c0 = (int64_t)blockIdx.y * G * VEC * NV;
+  const int64_t c0 = (int64_t)blockIdx.y * (G * 4 * NV);
 
   int64_t f[NV];
   bool act[NV];
   int hv[NV];
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
-    f[v] = c0 + (int64_t)(v * G + li) * VEC;
+    f[v] = c0 + (int64_t)(v * G + li) * 4;
     act[v] = f[v] < F;
     hv[v] = (MUL && act[v]) ? (int)(f[v] / p.dh) : 0;
   }
-
-  float acc[NV][VEC];
-  int32_t am[NV][VEC];
+  float acc[NV][4];
+  int32_t am[NV][4];
 #pragma unroll
   for (int v = 0; v < NV; ++v)
 #pragma unroll
-    for (int c = 0; c < VEC; ++c) {
+    for (int c = 0; c < 4; ++c) {
       acc[v][c] = MAX ? -INFINITY : 0.0f;
       am[v][c] = INT_MAX;
     }
 
-  for (int64_t base = b; base < e; base += kWave) {
-    const int cnt = (int)min((int64_t)kWave, e - base);
+  for (int64_t base = it.b; base < it.e; base += kWave) {
+    const int cnt = (int)min((int64_t)kWave, it.e - base);
     int my_src = 0, my_eid = 0;
     float my_w = 0.0f;
     if (lane < cnt) {
@@ -148,8 +231,121 @@ __global__ __launch_bounds__(kBlock) void spmm_kernel(SpmmParams p) {
         if (p.H == 1) my_w = p.ev[my_eid];
       }
     }
+    for (int j0 = 0; j0 < cnt; j0 += NG * U) {
+      float val[U][NV][4];
+      float wv[U][NV];
+      int32_t eu[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int jb = j0 + u * NG;
+        ok[u] = jb + gid < cnt;
+        const int src = bcast_lane<NG>(my_src, jb, gid);
+        eu[u] = (MAX || MUL) ? bcast_lane<NG>(my_eid, jb, gid) : 0;
+        const float w1 = MUL ? bcast_lane_f<NG>(my_w, jb, gid) : 1.0f;
+        const float* xr = p.x + (int64_t)src * F;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          if (ok[u] && act[v]) {
+            load_vec<4>(xr + f[v], val[u][v]);
+            wv[u][v] = (MUL && p.H != 1) ? p.ev[(int64_t)eu[u] * p.H + hv[v]] : w1;
+          } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) val[u][v][c] = MAX ? -INFINITY : 0.0f;
+            wv[u][v] = 1.0f;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            if constexpr (MAX) {
+              const float m = MUL ? wv[u][v] * val[u][v][c] : val[u][v][c];
+              if (ok[u] && takes_over(m, eu[u], acc[v][c], am[v][c])) {
+                acc[v][c] = m;
+                am[v][c] = eu[u];
+              }
+            } else if constexpr (MUL) {
+              acc[v][c] += wv[u][v] * val[u][v][c];
+            } else {
+              acc[v][c] += val[u][v][c];
+            }
+          }
+    }
+  }
+
+  // merge the lane groups (each holds a strided subset of the edges)
+#pragma unroll
+  for (int s = G; s < kWave; s <<= 1) {
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        if constexpr (MAX) {
+          const float ob = __shfl_xor(acc[v][c], s);
+          const int32_t oa = __shfl_xor(am[v][c], s);
+          if (takes_over(ob, oa, acc[v][c], am[v][c])) {
+            acc[v][c] = ob;
+            am[v][c] = oa;
+          }
+        } else {
+          acc[v][c] += __shfl_xor(acc[v][c], s);
+        }
+      }
+  }
+  if (gid != 0) return;
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+    if (act[v]) spmm_store<4, MAX, SEG>(p, it, f[v], acc[v], am[v]);
+}
+
+// Generic path: any width (scalar lanes), runtime group width G = 2^logG.
+template <int NV, int U, bool MUL, bool MAX, bool SEG>
+__global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
+  const int64_t item = wave_item();
+  if (item >= p.n_items) return;
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  const int lane = lane_id();
+  const int G = 1 << p.logG;
+  const int ngroups = kWave >> p.logG;
+  const int gid = lane >> p.logG;
+  const int li = lane & (G - 1);
+  const int64_t F = p.F;
+  const int64_t c0 = (int64_t)blockIdx.y * G * NV;
+
+  int64_t f[NV];
+  bool act[NV];
+  int hv[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    f[v] = c0 + (int64_t)(v * G + li);
+    act[v] = f[v] < F;
+    hv[v] = (MUL && act[v]) ? (int)(f[v] / p.dh) : 0;
+  }
+  float acc[NV][1];
+  int32_t am[NV][1];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    acc[v][0] = MAX ? -INFINITY : 0.0f;
+    am[v][0] = INT_MAX;
+  }
+
+  for (int64_t base = it.b; base < it.e; base += kWave) {
+    const int cnt = (int)min((int64_t)kWave, it.e - base);
+    int my_src = 0, my_eid = 0;
+    float my_w = 0.0f;
+    if (lane < cnt) {
+      my_src = p.indices[base + lane];
+      if constexpr (MAX || MUL) my_eid = p.eids ? p.eids[base + lane] : (int)(base + lane);
+      if constexpr (MUL) {
+        if (p.H == 1) my_w = p.ev[my_eid];
+      }
+    }
     for (int j0 = 0; j0 < cnt; j0 += ngroups * U) {
-      float val[U][NV][VEC];
+      float val[U][NV];
       float wv[U][NV];
       int32_t eu[U];
       bool ok[U];
@@ -165,106 +361,122 @@ __global__ __launch_bounds__(kBlock) void spmm_kernel(SpmmParams p) {
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
           if (ok[u] && act[v]) {
-            load_vec<VEC>(xr + f[v], val[u][v]);
+            val[u][v] = xr[f[v]];
             wv[u][v] = (MUL && p.H != 1) ? p.ev[(int64_t)eu[u] * p.H + hv[v]] : w1;
           } else {
-#pragma unroll
-            for (int c = 0; c < VEC; ++c) val[u][v][c] = MAX ? -INFINITY : 0.0f;
+            val[u][v] = MAX ? -INFINITY : 0.0f;
             wv[u][v] = 1.0f;
           }
         }
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
+      for (int u = 0; u < U; ++u)
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
-#pragma unroll
-          for (int c = 0; c < VEC; ++c) {
-            if constexpr (MAX) {
-              const float m = MUL ? wv[u][v] * val[u][v][c] : val[u][v][c];
-              if (ok[u] && takes_over(m, eu[u], acc[v][c], am[v][c])) {
-                acc[v][c] = m;
-                am[v][c] = eu[u];
-              }
-            } else {
-              if (MUL) acc[v][c] += wv[u][v] * val[u][v][c];
-              else acc[v][c] += val[u][v][c];
+          if constexpr (MAX) {
+            const float m = MUL ? wv[u][v] * val[u][v] : val[u][v];
+            if (ok[u] && takes_over(m, eu[u], acc[v][0], am[v][0])) {
+              acc[v][0] = m;
+              am[v][0] = eu[u];
             }
+          } else if constexpr (MUL) {
+            acc[v][0] += wv[u][v] * val[u][v];
+          } else {
+            acc[v][0] += val[u][v];
           }
         }
-      }
     }
   }
-
-  // merge the lane groups (each holds a strided subset of the edges)
   for (int s = G; s < kWave; s <<= 1) {
 #pragma unroll
-    for (int v = 0; v < NV; ++v)
-#pragma unroll
-      for (int c = 0; c < VEC; ++c) {
-        if constexpr (MAX) {
-          const float ob = __shfl_xor(acc[v][c], s);
-          const int32_t oa = __shfl_xor(am[v][c], s);
-          if (takes_over(ob, oa, acc[v][c], am[v][c])) {
-            acc[v][c] = ob;
-            am[v][c] = oa;
-          }
-        } else {
-          acc[v][c] += __shfl_xor(acc[v][c], s);
+    for (int v = 0; v < NV; ++v) {
+      if constexpr (MAX) {
+        const float ob = __shfl_xor(acc[v][0], s);
+        const int32_t oa = __shfl_xor(am[v][0], s);
+        if (takes_over(ob, oa, acc[v][0], am[v][0])) {
+          acc[v][0] = ob;
+          am[v][0] = oa;
         }
+      } else {
+        acc[v][0] += __shfl_xor(acc[v][0], s);
       }
+    }
   }
   if (gid != 0) return;
-
 #pragma unroll
-  for (int v = 0; v < NV; ++v) {
-    if (!act[v]) continue;
-    if (SEG && slot >= 0) {
-      store_vec<VEC>(p.ws_f + (int64_t)slot * F + f[v], acc[v]);
-      if constexpr (MAX) store_vec_i<VEC>(p.ws_i + (int64_t)slot * F + f[v], am[v]);
-    } else if constexpr (MAX) {
-      float o[VEC];
-      int32_t a[VEC];
-#pragma unroll
-      for (int c = 0; c < VEC; ++c) {
-        const bool none = am[v][c] == INT_MAX;
-        o[c] = none ? 0.0f : acc[v][c];
-        a[c] = none ? -1 : am[v][c];
-      }
-      store_vec<VEC>(p.out + row * F + f[v], o);
-      store_vec_i<VEC>(p.arg + row * F + f[v], a);
-    } else {
-      store_vec<VEC>(p.out + row * F + f[v], acc[v]);
-    }
-  }
+  for (int v = 0; v < NV; ++v)
+    if (act[v]) spmm_store<1, MAX, SEG>(p, it, f[v], acc[v], am[v]);
 }
 
-// Merges the partial results of each split row, slot by slot in order.
+// Merges the partial results of each split row.  Block = 4 wavefronts over a
+// tile of 64 feature columns (blockIdx.y); wavefront w takes slots
+// sb+w, sb+w+4, ... in increasing order (4 loads in flight), then the four
+// wavefront results are combined in order w = 0..3.
 template <bool MAX>
-__global__ __launch_bounds__(256) void spmm_fixup_kernel(const Fix* fix, const float* ws_f,
-                                                         const int32_t* ws_i, int64_t F,
-                                                         float* out, int32_t* arg) {
-  const int64_t f = (int64_t)blockIdx.y * 256 + threadIdx.x;
-  if (f >= F) return;
+__global__ __launch_bounds__(kBlock) void spmm_fixup_kernel(const Fix* fix, const float* ws_f,
+                                                            const int32_t* ws_i, int64_t F,
+                                                            float* out, int32_t* arg) {
+  __shared__ float red_v[kWavesPerBlock][kWave];
+  __shared__ int32_t red_a[kWavesPerBlock][kWave];
+  const int w = threadIdx.x >> 6;
+  const int lane = lane_id();
+  const int64_t col = (int64_t)blockIdx.y * kWave + lane;
+  const bool valid = col < F;
   const Fix fx = fix[blockIdx.x];
-  if constexpr (MAX) {
-    float best = -INFINITY;
-    int32_t be = INT_MAX;
-    for (int s = fx.slot_begin; s < fx.slot_end; ++s) {
-      const float m = ws_f[(int64_t)s * F + f];
-      const int32_t a = ws_i[(int64_t)s * F + f];
-      if (takes_over(m, a, best, be)) {
-        best = m;
-        be = a;
+  constexpr int kStride = kWavesPerBlock;
+  float acc = MAX ? -INFINITY : 0.0f;
+  int32_t am = INT_MAX;
+  if (valid) {
+    for (int s0 = fx.slot_begin + w; s0 < fx.slot_end; s0 += 4 * kStride) {
+      float v[4];
+      int32_t a[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int s = s0 + k * kStride;
+        v[k] = MAX ? -INFINITY : 0.0f;
+        a[k] = INT_MAX;
+        if (s < fx.slot_end) {
+          v[k] = ws_f[(int64_t)s * F + col];
+          if constexpr (MAX) a[k] = ws_i[(int64_t)s * F + col];
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if constexpr (MAX) {
+          if (takes_over(v[k], a[k], acc, am)) {
+            acc = v[k];
+            am = a[k];
+          }
+        } else {
+          acc += v[k];
+        }
       }
     }
-    const bool none = be == INT_MAX;
-    out[(int64_t)fx.row * F + f] = none ? 0.0f : best;
-    arg[(int64_t)fx.row * F + f] = none ? -1 : be;
+  }
+  red_v[w][lane] = acc;
+  red_a[w][lane] = am;
+  __syncthreads();
+  if (w != 0 || !valid) return;
+  acc = red_v[0][lane];
+  am = red_a[0][lane];
+#pragma unroll
+  for (int k = 1; k < kWavesPerBlock; ++k) {
+    if constexpr (MAX) {
+      if (takes_over(red_v[k][lane], red_a[k][lane], acc, am)) {
+        acc = red_v[k][lane];
+        am = red_a[k][lane];
+      }
+    } else {
+      acc += red_v[k][lane];
+    }
+  }
+  const int64_t o = (int64_t)fx.row * F + col;
+  if constexpr (MAX) {
+    const bool none = am == INT_MAX;
+    out[o] = none ? 0.0f : acc;
+    arg[o] = none ? -1 : am;
   } else {
-    float acc = 0.0f;
-    for (int s = fx.slot_begin; s < fx.slot_end; ++s) acc += ws_f[(int64_t)s * F + f];
-    out[(int64_t)fx.row * F + f] = acc;
+    out[o] = acc;
   }
 }
 
@@ -284,26 +496,149 @@ struct SddmmParams {
   int64_t F;
   int32_t H;
   int32_t dh;
-  int32_t logG;  // lanes per feature row
-  int32_t logS;  // lanes per head (HEADED only)
+  int32_t logG;  // lanes per feature row (runtime kernels)
+  int32_t logS;  // lanes per head (runtime headed kernel)
 };
 
-// The destination row's features stay in registers for the whole item; each
-// edge gathers its source row, multiplies, and reduces across the lanes of one
-// head with xor butterflies.  Requires the whole row in one chunk
-// (F <= G*VEC*NV) and, when HEADED, dh/VEC = 2^logS lanes per head.
-template <int VEC, int NV, int U, bool HEADED, bool SEG>
-__global__ __launch_bounds__(kBlock) void sddmm_kernel(SddmmParams p) {
+// Single head, float4 lanes, G lanes per feature row, NV float4 per lane.  The
+// destination row stays in registers for the whole item; each edge gathers
+// its source row, multiplies, and reduces across its G lanes with DPP.
+template <int G, int NV, int U, bool SEG>
+__global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
+  constexpr int NG = kWave / G;
+  static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
-  int64_t row, b, e;
-  if constexpr (SEG) {
-    const Seg s = p.segs[item];
-    row = s.row; b = s.begin; e = s.end;
-  } else {
-    row = item; b = p.indptr[item]; e = p.indptr[item + 1];
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.b >= it.e) return;
+  const int lane = lane_id();
+  const int gid = lane / G;
+  const int li = lane % G;
+  const int64_t F = p.F;
+
+  int64_t f[NV];
+  bool act[NV];
+  float xd[NV][4];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    f[v] = (int64_t)(v * G + li) * 4;
+    act[v] = f[v] < F;
+    if (act[v]) {
+      load_vec<4>(p.xd + it.row * F + f[v], xd[v]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) xd[v][c] = 0.0f;
+    }
   }
-  if (b >= e) return;
+
+  for (int64_t base = it.b; base < it.e; base += kWave) {
+    const int cnt = (int)min((int64_t)kWave, it.e - base);
+    int my_src = 0, my_eid = 0;
+    if (lane < cnt) {
+      my_src = __builtin_nontemporal_load(p.indices + base + lane);
+      my_eid = p.eids ? __builtin_nontemporal_load(p.eids + base + lane) : (int)(base + lane);
+    }
+    for (int j0 = 0; j0 < cnt; j0 += NG * U) {
+      float val[U][NV][4];
+      int32_t eu[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int jb = j0 + u * NG;
+        ok[u] = jb + gid < cnt;
+        const int src = bcast_lane<NG>(my_src, jb, gid);
+        eu[u] = bcast_lane<NG>(my_eid, jb, gid);
+        const float* xr = p.xs + (int64_t)src * F;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          if (ok[u] && act[v]) {
+            load_vec<4>(xr + f[v], val[u][v]);
+          } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) val[u][v][c] = 0.0f;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float part = 0.0f;
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) part += val[u][v][c] * xd[v][c];
+        part = group_sum<G>(part);
+        if (ok[u] && li == G - 1) p.out[eu[u]] = part;
+      }
+    }
+  }
+}
+
+// Several heads, float4 lanes, S lanes per head (compile time), G lanes per
+// feature row (runtime, <= 64, one float4 per lane).
+template <int S, bool SEG>
+__global__ __launch_bounds__(kBlock) void sddmm_headed_kernel(SddmmParams p) {
+  constexpr int U = 4;
+  const int64_t item = wave_item();
+  if (item >= p.n_items) return;
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.b >= it.e) return;
+  const int lane = lane_id();
+  const int G = 1 << p.logG;
+  const int ngroups = kWave >> p.logG;
+  const int gid = lane >> p.logG;
+  const int li = lane & (G - 1);
+  const int64_t F = p.F;
+  const int64_t f = (int64_t)li * 4;
+  const bool act = f < F;
+  const int64_t h = act ? f / p.dh : 0;
+  float xd[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (act) load_vec<4>(p.xd + it.row * F + f, xd);
+
+  for (int64_t base = it.b; base < it.e; base += kWave) {
+    const int cnt = (int)min((int64_t)kWave, it.e - base);
+    int my_src = 0, my_eid = 0;
+    if (lane < cnt) {
+      my_src = __builtin_nontemporal_load(p.indices + base + lane);
+      my_eid = p.eids ? __builtin_nontemporal_load(p.eids + base + lane) : (int)(base + lane);
+    }
+    for (int j0 = 0; j0 < cnt; j0 += ngroups * U) {
+      float val[U][4];
+      int32_t eu[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = j0 + u * ngroups + gid;
+        ok[u] = j < cnt;
+        const int jl = j & (kWave - 1);
+        const int src = __shfl(my_src, jl);
+        eu[u] = __shfl(my_eid, jl);
+        if (ok[u] && act) {
+          load_vec<4>(p.xs + (int64_t)src * F + f, val[u]);
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) val[u][c] = 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float part = 0.0f;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) part += val[u][c] * xd[c];
+        part = group_sum<S>(part);
+        if (ok[u] && act && (li % S) == S - 1) p.out[(int64_t)eu[u] * p.H + h] = part;
+      }
+    }
+  }
+}
+
+// Scalar lanes, runtime widths: G = 2^logG lanes per feature row, NV values
+// per lane; when HEADED, 2^logS lanes per head.  Reductions use xor permutes.
+template <int NV, int U, bool HEADED, bool SEG>
+__global__ __launch_bounds__(kBlock) void sddmm_scalar_kernel(SddmmParams p) {
+  const int64_t item = wave_item();
+  if (item >= p.n_items) return;
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.b >= it.e) return;
   const int lane = lane_id();
   const int G = 1 << p.logG;
   const int ngroups = kWave >> p.logG;
@@ -314,28 +649,23 @@ __global__ __launch_bounds__(kBlock) void sddmm_kernel(SddmmParams p) {
 
   int64_t f[NV];
   bool act[NV];
-  float xd[NV][VEC];
+  float xd[NV];
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
-    f[v] = (int64_t)(v * G + li) * VEC;
+    f[v] = (int64_t)(v * G + li);
     act[v] = f[v] < F;
-    if (act[v]) {
-      load_vec<VEC>(p.xd + row * F + f[v], xd[v]);
-    } else {
-#pragma unroll
-      for (int c = 0; c < VEC; ++c) xd[v][c] = 0.0f;
-    }
+    xd[v] = act[v] ? p.xd[it.row * F + f[v]] : 0.0f;
   }
 
-  for (int64_t base = b; base < e; base += kWave) {
-    const int cnt = (int)min((int64_t)kWave, e - base);
+  for (int64_t base = it.b; base < it.e; base += kWave) {
+    const int cnt = (int)min((int64_t)kWave, it.e - base);
     int my_src = 0, my_eid = 0;
     if (lane < cnt) {
-      my_src = __builtin_nontemporal_load(p.indices + base + lane);
-      my_eid = p.eids ? __builtin_nontemporal_load(p.eids + base + lane) : (int)(base + lane);
+      my_src = p.indices[base + lane];
+      my_eid = p.eids ? p.eids[base + lane] : (int)(base + lane);
     }
     for (int j0 = 0; j0 < cnt; j0 += ngroups * U) {
-      float val[U][NV][VEC];
+      float val[U][NV];
       int32_t eu[U];
       bool ok[U];
 #pragma unroll
@@ -345,33 +675,22 @@ __global__ __launch_bounds__(kBlock) void sddmm_kernel(SddmmParams p) {
         const int jl = j & (kWave - 1);
         const int src = __shfl(my_src, jl);
         eu[u] = __shfl(my_eid, jl);
-        const float* xr = p.xs + (int64_t)src * F;
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          if (ok[u] && act[v]) {
-            load_vec<VEC>(xr + f[v], val[u][v]);
-          } else {
-#pragma unroll
-            for (int c = 0; c < VEC; ++c) val[u][v][c] = 0.0f;
-          }
-        }
+        for (int v = 0; v < NV; ++v)
+          val[u][v] = (ok[u] && act[v]) ? p.xs[(int64_t)src * F + f[v]] : 0.0f;
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         if constexpr (!HEADED) {
           float part = 0.0f;
 #pragma unroll
-          for (int v = 0; v < NV; ++v)
-#pragma unroll
-            for (int c = 0; c < VEC; ++c) part += val[u][v][c] * xd[v][c];
+          for (int v = 0; v < NV; ++v) part += val[u][v] * xd[v];
           for (int s = 1; s < G; s <<= 1) part += __shfl_xor(part, s);
           if (ok[u] && li == 0) p.out[eu[u]] = part;
         } else {
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            float part = 0.0f;
-#pragma unroll
-            for (int c = 0; c < VEC; ++c) part += val[u][v][c] * xd[v][c];
+            float part = val[u][v] * xd[v];
             for (int s = 1; s < S; s <<= 1) part += __shfl_xor(part, s);
             if (ok[u] && act[v] && (li & (S - 1)) == 0)
               p.out[(int64_t)eu[u] * p.H + f[v] / p.dh] = part;
@@ -382,29 +701,24 @@ __global__ __launch_bounds__(kBlock) void sddmm_kernel(SddmmParams p) {
   }
 }
 
-// Fallback for shapes the lane mapping above does not cover (odd head sizes,
-// very wide rows): one lane per (edge, head) pair, sequential dot product.
+// Fallback for shapes the lane mappings above do not cover (head sizes that
+// are not a power of two lanes, very wide rows): one lane per (edge, head)
+// pair, sequential dot product.
 template <bool SEG>
 __global__ __launch_bounds__(kBlock) void sddmm_generic_kernel(SddmmParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
-  int64_t row, b, e;
-  if constexpr (SEG) {
-    const Seg s = p.segs[item];
-    row = s.row; b = s.begin; e = s.end;
-  } else {
-    row = item; b = p.indptr[item]; e = p.indptr[item + 1];
-  }
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
   const int lane = lane_id();
   const int64_t H = p.H, dh = p.dh, F = p.F;
-  const int64_t total = (e - b) * H;
+  const int64_t total = (it.e - it.b) * H;
   for (int64_t t = lane; t < total; t += kWave) {
-    const int64_t q = b + t / H;
+    const int64_t q = it.b + t / H;
     const int64_t h = t % H;
     const int64_t src = p.indices[q];
     const int64_t eid = p.eids ? p.eids[q] : q;
     const float* a = p.xs + src * F + h * dh;
-    const float* d = p.xd + row * F + h * dh;
+    const float* d = p.xd + it.row * F + h * dh;
     float acc = 0.0f;
     for (int64_t k = 0; k < dh; ++k) acc += a[k] * d[k];
     p.out[eid * H + h] = acc;
@@ -423,7 +737,8 @@ struct SoftmaxParams {
   const Seg* segs;
   const Fix* fix;
   const int32_t* slot_fix;
-  float* ws;  // [slot][H][2] = (running max, scaled sum)
+  float* ws;      // [slot][H][2]  per-segment (max, scaled sum)
+  float* ws_row;  // [split row][H][2] merged per row
   int64_t n_items;
   int32_t H;
   int32_t leaky;
@@ -434,7 +749,7 @@ __device__ __forceinline__ float leaky_relu(float s, int on, float slope) {
   return (on && !(s > 0.0f)) ? slope * s : s;
 }
 
-// (m, z) represents sum_i exp(x_i - m) = z.  Combining two such pairs.
+// (m, z) stands for sum_i exp(x_i - m) = z.  Merging two such pairs.
 __device__ __forceinline__ void lse_merge(float& m, float& z, float om, float oz) {
   if (om == -INFINITY) return;
   if (m == -INFINITY) {
@@ -447,24 +762,27 @@ __device__ __forceinline__ void lse_merge(float& m, float& z, float om, float oz
   m = nm;
 }
 
+__device__ __forceinline__ void lse_push(float& m, float& z, float s) {
+  if (s > m) {
+    z = z * expf(m - s) + 1.0f;
+    m = s;
+  } else {
+    z += expf(s - m);
+  }
+}
+
+constexpr int kSoftmaxU = 4;  // scores in flight per lane
+
 // Lanes map to (edge offset, head) pairs: hc = heads per pass, epw = 64/hc
-// edges per pass.  Pass 1 keeps a running (max, sum); lanes of one head then
-// merge in a fixed tree; pass 2 writes exp(s' - m) / z.  Segments of split
-// rows stop after pass 1 and leave (m, z) in the workspace.
+// edges per pass.  Pass 1 keeps a running (max, sum) per lane; lanes of one
+// head then merge in a fixed tree; pass 2 writes exp(s' - m) / z.  Segments
+// of split rows stop after pass 1 and leave (m, z) in the workspace.
 template <bool SEG>
 __global__ __launch_bounds__(kBlock) void softmax_kernel(SoftmaxParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
-  int64_t row, b, e;
-  int32_t slot = -1;
-  if constexpr (SEG) {
-    const Seg s = p.segs[item];
-    row = s.row; b = s.begin; e = s.end; slot = s.slot;
-  } else {
-    row = item; b = p.indptr[item]; e = p.indptr[item + 1];
-  }
-  (void)row;
-  if (b >= e) return;
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.b >= it.e) return;
   const int lane = lane_id();
   const int H = p.H;
   for (int h0 = 0; h0 < H; h0 += kWave) {
@@ -475,15 +793,20 @@ __global__ __launch_bounds__(kBlock) void softmax_kernel(SoftmaxParams p) {
     const bool active = eo < epw;
     float m = -INFINITY, z = 0.0f;
     if (active) {
-      for (int64_t q = b + eo; q < e; q += epw) {
-        const int64_t eid = p.eids ? p.eids[q] : q;
-        const float s = leaky_relu(p.scores[eid * H + h], p.leaky, p.slope);
-        if (s > m) {
-          z = z * expf(m - s) + 1.0f;
-          m = s;
-        } else {
-          z += expf(s - m);
+      for (int64_t q0 = it.b + eo; q0 < it.e; q0 += (int64_t)kSoftmaxU * epw) {
+        float sv[kSoftmaxU];
+#pragma unroll
+        for (int k = 0; k < kSoftmaxU; ++k) {
+          const int64_t q = q0 + (int64_t)k * epw;
+          sv[k] = -INFINITY;
+          if (q < it.e) {
+            const int64_t eid = p.eids ? p.eids[q] : q;
+            sv[k] = leaky_relu(p.scores[eid * H + h], p.leaky, p.slope);
+          }
         }
+#pragma unroll
+        for (int k = 0; k < kSoftmaxU; ++k)
+          if (q0 + (int64_t)k * epw < it.e) lse_push(m, z, sv[k]);
       }
     }
     // tree over edge offsets: offset eo merges eo + k for k = 1, 2, 4, ...
@@ -495,31 +818,84 @@ __global__ __launch_bounds__(kBlock) void softmax_kernel(SoftmaxParams p) {
     }
     m = __shfl(m, lane % hc);
     z = __shfl(z, lane % hc);
-    if (SEG && slot >= 0) {
+    if (SEG && it.slot >= 0) {
       if (active && eo == 0) {
-        p.ws[((int64_t)slot * H + h) * 2 + 0] = m;
-        p.ws[((int64_t)slot * H + h) * 2 + 1] = z;
+        p.ws[((int64_t)it.slot * H + h) * 2 + 0] = m;
+        p.ws[((int64_t)it.slot * H + h) * 2 + 1] = z;
       }
       continue;
     }
     if (active) {
       const float inv = 1.0f / z;
-      for (int64_t q = b + eo; q < e; q += epw) {
-        const int64_t eid = p.eids ? p.eids[q] : q;
-        const float s = leaky_relu(p.scores[eid * H + h], p.leaky, p.slope);
-        p.out[eid * H + h] = expf(s - m) * inv;
+      for (int64_t q0 = it.b + eo; q0 < it.e; q0 += (int64_t)kSoftmaxU * epw) {
+        float sv[kSoftmaxU];
+        int64_t ev[kSoftmaxU];
+#pragma unroll
+        for (int k = 0; k < kSoftmaxU; ++k) {
+          const int64_t q = q0 + (int64_t)k * epw;
+          ev[k] = -1;
+          if (q < it.e) {
+            ev[k] = p.eids ? p.eids[q] : q;
+            sv[k] = leaky_relu(p.scores[ev[k] * H + h], p.leaky, p.slope);
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < kSoftmaxU; ++k)
+          if (ev[k] >= 0) p.out[ev[k] * H + h] = expf(sv[k] - m) * inv;
       }
     }
   }
 }
 
-// Second pass for segments of split rows: merge the row's (m, z) partials in
-// slot order, then normalise this segment's edges.  Item = slot.
+// Merges the per-segment (m, z) of each split row into one pair per head.
+// Block = 4 wavefronts; lane (eo, head) of wavefront w takes slots
+// t = w*epw + eo, t + 4*epw, ... in order; the 4*epw partial pairs are then
+// merged in order of t by the first lane of each head.
+__global__ __launch_bounds__(kBlock) void softmax_rowstats_kernel(SoftmaxParams p) {
+  __shared__ float red_m[kBlock];
+  __shared__ float red_z[kBlock];
+  const Fix fx = p.fix[blockIdx.x];
+  const int w = threadIdx.x >> 6;
+  const int lane = lane_id();
+  const int H = p.H;
+  for (int h0 = 0; h0 < H; h0 += kWave) {
+    const int hc = min(H - h0, kWave);
+    const int epw = kWave / hc;
+    const int eo = lane / hc;
+    const int hh = lane % hc;
+    const int h = h0 + hh;
+    const int lanes = kWavesPerBlock * epw;
+    const int t = w * epw + eo;
+    float m = -INFINITY, z = 0.0f;
+    if (eo < epw) {
+      for (int s = fx.slot_begin + t; s < fx.slot_end; s += lanes)
+        lse_merge(m, z, p.ws[((int64_t)s * H + h) * 2 + 0], p.ws[((int64_t)s * H + h) * 2 + 1]);
+    }
+    red_m[threadIdx.x] = m;
+    red_z[threadIdx.x] = z;
+    __syncthreads();
+    if (t == 0 && eo < epw) {
+      // thread index of slot-lane tt for head hh: (tt / epw) * 64 + (tt % epw) * hc + hh;
+      // slot-lanes at or beyond the row's slot count hold nothing
+      const int used = min(lanes, fx.slot_end - fx.slot_begin);
+      for (int tt = 1; tt < used; ++tt) {
+        const int idx = (tt / epw) * kWave + (tt % epw) * hc + hh;
+        lse_merge(m, z, red_m[idx], red_z[idx]);
+      }
+      p.ws_row[((int64_t)blockIdx.x * H + h) * 2 + 0] = m;
+      p.ws_row[((int64_t)blockIdx.x * H + h) * 2 + 1] = z;
+    }
+    __syncthreads();
+  }
+}
+
+// Second pass for segments of split rows: normalise this segment's edges with
+// its row's merged (m, z).  Item = slot.
 __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, int64_t n_slots) {
   const int64_t slot = wave_item();
   if (slot >= n_slots) return;
   const Seg s = p.segs[slot];
-  const Fix fx = p.fix[p.slot_fix[slot]];
+  const int64_t fi = p.slot_fix[slot];
   const int lane = lane_id();
   const int H = p.H;
   for (int h0 = 0; h0 < H; h0 += kWave) {
@@ -528,14 +904,23 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
     const int eo = lane / hc;
     const int h = h0 + lane % hc;
     if (eo >= epw) continue;
-    float m = -INFINITY, z = 0.0f;
-    for (int t = fx.slot_begin; t < fx.slot_end; ++t)
-      lse_merge(m, z, p.ws[((int64_t)t * H + h) * 2 + 0], p.ws[((int64_t)t * H + h) * 2 + 1]);
-    const float inv = 1.0f / z;
-    for (int64_t q = s.begin + eo; q < s.end; q += epw) {
-      const int64_t eid = p.eids ? p.eids[q] : q;
-      const float sc = leaky_relu(p.scores[eid * H + h], p.leaky, p.slope);
-      p.out[eid * H + h] = expf(sc - m) * inv;
+    const float m = p.ws_row[(fi * H + h) * 2 + 0];
+    const float inv = 1.0f / p.ws_row[(fi * H + h) * 2 + 1];
+    for (int64_t q0 = s.begin + eo; q0 < s.end; q0 += (int64_t)kSoftmaxU * epw) {
+      float sv[kSoftmaxU];
+      int64_t ev[kSoftmaxU];
+#pragma unroll
+      for (int k = 0; k < kSoftmaxU; ++k) {
+        const int64_t q = q0 + (int64_t)k * epw;
+        ev[k] = -1;
+        if (q < s.end) {
+          ev[k] = p.eids ? p.eids[q] : q;
+          sv[k] = leaky_relu(p.scores[ev[k] * H + h], p.leaky, p.slope);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kSoftmaxU; ++k)
+        if (ev[k] >= 0) p.out[ev[k] * H + h] = expf(sv[k] - m) * inv;
     }
   }
 }
@@ -556,52 +941,61 @@ dim3 grid_for(int64_t items, int64_t chunks) {
   return dim3((unsigned)((items + kWavesPerBlock - 1) / kWavesPerBlock), (unsigned)chunks, 1);
 }
 
-template <int VEC, int NV, int U, bool MUL, bool MAX>
-void spmm_go(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
-  if (seg)
-    hipLaunchKernelGGL((spmm_kernel<VEC, NV, U, MUL, MAX, true>), grid, dim3(kBlock), 0, st, prm);
-  else
-    hipLaunchKernelGGL((spmm_kernel<VEC, NV, U, MUL, MAX, false>), grid, dim3(kBlock), 0, st, prm);
+#define FG_LAUNCH(kernel, grid, stream, ...) \
+  hipLaunchKernelGGL((kernel), (grid), dim3(kBlock), 0, (stream), __VA_ARGS__)
+
+template <int G, int NV, int U, bool MUL, bool MAX>
+void spmm_fast_seg(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+  if (seg) FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, true>), grid, st, prm);
+  else FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, false>), grid, st, prm);
 }
 
-template <int VEC, int NV, int U>
-void spmm_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 grid, hipStream_t st) {
+template <int G, int NV, int U>
+void spmm_fast_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 grid,
+                   hipStream_t st) {
   if (mul) {
-    if (mx) spmm_go<VEC, NV, U, true, true>(prm, seg, grid, st);
-    else spmm_go<VEC, NV, U, true, false>(prm, seg, grid, st);
+    if (mx) spmm_fast_seg<G, NV, U, true, true>(prm, seg, grid, st);
+    else spmm_fast_seg<G, NV, U, true, false>(prm, seg, grid, st);
   } else {
-    if (mx) spmm_go<VEC, NV, U, false, true>(prm, seg, grid, st);
-    else spmm_go<VEC, NV, U, false, false>(prm, seg, grid, st);
+    if (mx) spmm_fast_seg<G, NV, U, false, true>(prm, seg, grid, st);
+    else spmm_fast_seg<G, NV, U, false, false>(prm, seg, grid, st);
   }
 }
 
-template <int VEC>
-void spmm_nv(const SpmmParams& prm, int nv, bool mul, bool mx, bool seg, dim3 grid,
-             hipStream_t st) {
-  if (nv == 1) spmm_ops<VEC, 1, 4>(prm, mul, mx, seg, grid, st);
-  else if (nv == 2) spmm_ops<VEC, 2, 2>(prm, mul, mx, seg, grid, st);
-  else spmm_ops<VEC, 4, 1>(prm, mul, mx, seg, grid, st);
+template <int NV, int U, bool MUL, bool MAX>
+void spmm_generic_seg(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+  if (seg) FG_LAUNCH((spmm_generic_kernel<NV, U, MUL, MAX, true>), grid, st, prm);
+  else FG_LAUNCH((spmm_generic_kernel<NV, U, MUL, MAX, false>), grid, st, prm);
 }
 
-template <int VEC, int NV, int U, bool HEADED>
-void sddmm_go(const SddmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
-  if (seg)
-    hipLaunchKernelGGL((sddmm_kernel<VEC, NV, U, HEADED, true>), grid, dim3(kBlock), 0, st, prm);
-  else
-    hipLaunchKernelGGL((sddmm_kernel<VEC, NV, U, HEADED, false>), grid, dim3(kBlock), 0, st, prm);
-}
-
-template <int VEC>
-void sddmm_nv(const SddmmParams& prm, int nv, bool headed, bool seg, dim3 grid, hipStream_t st) {
-  if (headed) {
-    if (nv == 1) sddmm_go<VEC, 1, 4, true>(prm, seg, grid, st);
-    else if (nv == 2) sddmm_go<VEC, 2, 2, true>(prm, seg, grid, st);
-    else sddmm_go<VEC, 4, 1, true>(prm, seg, grid, st);
+template <int NV, int U>
+void spmm_generic_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 grid,
+                      hipStream_t st) {
+  if (mul) {
+    if (mx) spmm_generic_seg<NV, U, true, true>(prm, seg, grid, st);
+    else spmm_generic_seg<NV, U, true, false>(prm, seg, grid, st);
   } else {
-    if (nv == 1) sddmm_go<VEC, 1, 4, false>(prm, seg, grid, st);
-    else if (nv == 2) sddmm_go<VEC, 2, 2, false>(prm, seg, grid, st);
-    else sddmm_go<VEC, 4, 1, false>(prm, seg, grid, st);
+    if (mx) spmm_generic_seg<NV, U, false, true>(prm, seg, grid, st);
+    else spmm_generic_seg<NV, U, false, false>(prm, seg, grid, st);
   }
+}
+
+template <int G, int NV, int U>
+void sddmm_fast_go(const SddmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+  if (seg) FG_LAUNCH((sddmm_fast_kernel<G, NV, U, true>), grid, st, prm);
+  else FG_LAUNCH((sddmm_fast_kernel<G, NV, U, false>), grid, st, prm);
+}
+
+template <int S>
+void sddmm_headed_go(const SddmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+  if (seg) FG_LAUNCH((sddmm_headed_kernel<S, true>), grid, st, prm);
+  else FG_LAUNCH((sddmm_headed_kernel<S, false>), grid, st, prm);
+}
+
+template <int NV, int U, bool HEADED>
+void sddmm_scalar_go(const SddmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+  if (seg) FG_LAUNCH((sddmm_scalar_kernel<NV, U, HEADED, true>), grid, st, prm);
+  else FG_LAUNCH((sddmm_scalar_kernel<NV, U, HEADED, false>), grid, st, prm);
 }
 
 }  // namespace
@@ -613,20 +1007,9 @@ hipError_t launch_gspmm(const GraphView& g, const PlanView* plan, int msg, int r
   const int64_t F = H * dh;
   const bool mul = msg == kSrcMulEdge;
   const bool mx = red == kMax;
+  const bool seg = plan != nullptr;
   const bool vec4 = (F % 4 == 0) && (H == 1 || dh % 4 == 0) && aligned16(x) && aligned16(out) &&
                     (!mx || aligned16(arg));
-  const int VEC = vec4 ? 4 : 1;
-  const int64_t Q = F / VEC;
-  int logG, nv;
-  int64_t chunks = 1;
-  if (Q <= kWave) {
-    logG = ilog2_ceil(Q);
-    nv = 1;
-  } else {
-    logG = 6;
-    nv = Q <= 2 * kWave ? 2 : 4;
-    chunks = (Q + (int64_t)kWave * nv - 1) / ((int64_t)kWave * nv);
-  }
   SpmmParams prm;
   prm.indptr = g.indptr;
   prm.indices = g.indices;
@@ -635,28 +1018,48 @@ hipError_t launch_gspmm(const GraphView& g, const PlanView* plan, int msg, int r
   prm.ev = ev;
   prm.out = out;
   prm.arg = arg;
-  prm.segs = plan ? plan->segs : nullptr;
-  prm.ws_f = plan ? plan->ws_f : nullptr;
-  prm.ws_i = plan ? plan->ws_i : nullptr;
-  prm.n_items = plan ? plan->num_segments : g.num_rows;
+  prm.segs = seg ? plan->segs : nullptr;
+  prm.ws_f = seg ? plan->ws_f : nullptr;
+  prm.ws_i = seg ? plan->ws_i : nullptr;
+  prm.n_items = seg ? plan->num_segments : g.num_rows;
   prm.F = F;
   prm.H = (int32_t)H;
   prm.dh = (int32_t)dh;
-  prm.logG = logG;
-  const bool seg = plan != nullptr;
-  const dim3 grid = grid_for(prm.n_items, chunks);
-  if (vec4) spmm_nv<4>(prm, nv, mul, mx, seg, grid, stream);
-  else spmm_nv<1>(prm, nv, mul, mx, seg, grid, stream);
+  prm.logG = 6;
+  if (vec4) {
+    const int64_t Q = F / 4;  // float4 per row
+    if (Q <= 4) spmm_fast_ops<4, 1, 4>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
+    else if (Q <= 8) spmm_fast_ops<8, 1, 8>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
+    else if (Q <= 16) spmm_fast_ops<16, 1, 8>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
+    else if (Q <= 32) spmm_fast_ops<32, 1, 8>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
+    else if (Q <= 64) spmm_fast_ops<64, 1, 8>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
+    else if (Q <= 128) spmm_fast_ops<64, 2, 4>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
+    else spmm_fast_ops<64, 4, 2>(prm, mul, mx, seg, grid_for(prm.n_items, (Q + 255) / 256), stream);
+  } else {
+    // scalar lanes: G = 2^ceil(log2 F) up to 64, then NV values per lane
+    int nv = 1;
+    int64_t chunks = 1;
+    if (F <= kWave) {
+      prm.logG = ilog2_ceil(F);
+    } else {
+      nv = F <= 2 * kWave ? 2 : 4;
+      chunks = (F + (int64_t)kWave * nv - 1) / ((int64_t)kWave * nv);
+    }
+    const dim3 grid = grid_for(prm.n_items, chunks);
+    if (nv == 1) spmm_generic_ops<1, 4>(prm, mul, mx, seg, grid, stream);
+    else if (nv == 2) spmm_generic_ops<2, 2>(prm, mul, mx, seg, grid, stream);
+    else spmm_generic_ops<4, 1>(prm, mul, mx, seg, grid, stream);
+  }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  if (plan && plan->num_split_rows > 0) {
-    const dim3 fgrid((unsigned)plan->num_split_rows, (unsigned)((F + 255) / 256), 1);
+  if (seg && plan->num_split_rows > 0) {
+    const dim3 fgrid((unsigned)plan->num_split_rows, (unsigned)((F + kWave - 1) / kWave), 1);
     if (mx)
-      hipLaunchKernelGGL((spmm_fixup_kernel<true>), fgrid, dim3(256), 0, stream, plan->fix,
-                         plan->ws_f, plan->ws_i, F, out, arg);
+      FG_LAUNCH((spmm_fixup_kernel<true>), fgrid, stream, plan->fix, plan->ws_f, plan->ws_i, F,
+                out, arg);
     else
-      hipLaunchKernelGGL((spmm_fixup_kernel<false>), fgrid, dim3(256), 0, stream, plan->fix,
-                         plan->ws_f, plan->ws_i, F, out, arg);
+      FG_LAUNCH((spmm_fixup_kernel<false>), fgrid, stream, plan->fix, plan->ws_f, plan->ws_i, F,
+                out, arg);
     err = hipGetLastError();
   }
   return err;
@@ -666,23 +1069,7 @@ hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, in
                          const float* xs, const float* xd, float* out, hipStream_t stream) {
   if (g.num_rows == 0 || g.nnz == 0) return hipSuccess;
   const int64_t F = H * dh;
-  const bool vec4 = (F % 4 == 0) && (H == 1 || dh % 4 == 0) && aligned16(xs) && aligned16(xd);
-  const int VEC = vec4 ? 4 : 1;
-  const int64_t Q = F / VEC;
-  const bool headed = H > 1;
-  int logS = 0;
-  bool generic = Q > 4 * kWave;
-  if (headed) {
-    const int64_t S = dh / VEC;
-    logS = ilog2_ceil(S);
-    if ((int64_t(1) << logS) != S || S > kWave) generic = true;
-  }
-  int logG = 6, nv = 1;
-  if (Q <= kWave) {
-    logG = ilog2_ceil(Q);
-  } else {
-    nv = Q <= 2 * kWave ? 2 : 4;
-  }
+  const bool seg = plan != nullptr;
   SddmmParams prm;
   prm.indptr = g.indptr;
   prm.indices = g.indices;
@@ -690,22 +1077,56 @@ hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, in
   prm.xs = xs;
   prm.xd = xd;
   prm.out = out;
-  prm.segs = plan ? plan->segs : nullptr;
-  prm.n_items = plan ? plan->num_segments : g.num_rows;
+  prm.segs = seg ? plan->segs : nullptr;
+  prm.n_items = seg ? plan->num_segments : g.num_rows;
   prm.F = F;
   prm.H = (int32_t)H;
   prm.dh = (int32_t)dh;
-  prm.logG = logG;
-  prm.logS = logS;
-  const bool seg = plan != nullptr;
+  prm.logG = 6;
+  prm.logS = 0;
   const dim3 grid = grid_for(prm.n_items, 1);
+  const bool vec4 = (F % 4 == 0) && (H == 1 || dh % 4 == 0) && aligned16(xs) && aligned16(xd);
+  if (vec4 && H == 1 && F <= 4 * 4 * kWave) {
+    const int64_t Q = F / 4;
+    if (Q <= 4) sddmm_fast_go<4, 1, 4>(prm, seg, grid, stream);
+    else if (Q <= 8) sddmm_fast_go<8, 1, 8>(prm, seg, grid, stream);
+    else if (Q <= 16) sddmm_fast_go<16, 1, 8>(prm, seg, grid, stream);
+    else if (Q <= 32) sddmm_fast_go<32, 1, 8>(prm, seg, grid, stream);
+    else if (Q <= 64) sddmm_fast_go<64, 1, 8>(prm, seg, grid, stream);
+    else if (Q <= 128) sddmm_fast_go<64, 2, 4>(prm, seg, grid, stream);
+    else sddmm_fast_go<64, 4, 2>(prm, seg, grid, stream);
+    return hipGetLastError();
+  }
+  if (vec4 && H > 1 && F <= 4 * kWave && (dh == 16 || dh == 32 || dh == 64)) {
+    prm.logG = ilog2_ceil(F / 4);
+    if (dh == 16) sddmm_headed_go<4>(prm, seg, grid, stream);
+    else if (dh == 32) sddmm_headed_go<8>(prm, seg, grid, stream);
+    else sddmm_headed_go<16>(prm, seg, grid, stream);
+    return hipGetLastError();
+  }
+  // scalar lanes: one value per lane, G = 2^ceil(log2 F) <= 64, NV <= 4
+  const bool headed = H > 1;
+  bool generic = F > 4 * kWave;
+  if (headed) {
+    prm.logS = ilog2_ceil(dh);
+    if ((int64_t(1) << prm.logS) != dh || dh > kWave) generic = true;
+  }
   if (generic) {
-    if (seg) hipLaunchKernelGGL((sddmm_generic_kernel<true>), grid, dim3(kBlock), 0, stream, prm);
-    else hipLaunchKernelGGL((sddmm_generic_kernel<false>), grid, dim3(kBlock), 0, stream, prm);
-  } else if (vec4) {
-    sddmm_nv<4>(prm, nv, headed, seg, grid, stream);
+    if (seg) FG_LAUNCH((sddmm_generic_kernel<true>), grid, stream, prm);
+    else FG_LAUNCH((sddmm_generic_kernel<false>), grid, stream, prm);
+    return hipGetLastError();
+  }
+  int nv = 1;
+  if (F <= kWave) prm.logG = ilog2_ceil(F);
+  else nv = F <= 2 * kWave ? 2 : 4;
+  if (headed) {
+    if (nv == 1) sddmm_scalar_go<1, 4, true>(prm, seg, grid, stream);
+    else if (nv == 2) sddmm_scalar_go<2, 2, true>(prm, seg, grid, stream);
+    else sddmm_scalar_go<4, 1, true>(prm, seg, grid, stream);
   } else {
-    sddmm_nv<1>(prm, nv, headed, seg, grid, stream);
+    if (nv == 1) sddmm_scalar_go<1, 4, false>(prm, seg, grid, stream);
+    else if (nv == 2) sddmm_scalar_go<2, 2, false>(prm, seg, grid, stream);
+    else sddmm_scalar_go<4, 1, false>(prm, seg, grid, stream);
   }
   return hipGetLastError();
 }
@@ -723,17 +1144,20 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
   prm.fix = plan ? plan->fix : nullptr;
   prm.slot_fix = plan ? plan->slot_fix : nullptr;
   prm.ws = plan ? plan->ws_f : nullptr;
+  prm.ws_row = plan ? plan->ws_row : nullptr;
   prm.n_items = plan ? plan->num_segments : g.num_rows;
   prm.H = (int32_t)H;
   prm.leaky = leaky ? 1 : 0;
   prm.slope = slope;
   const dim3 grid = grid_for(prm.n_items, 1);
-  if (plan) hipLaunchKernelGGL((softmax_kernel<true>), grid, dim3(kBlock), 0, stream, prm);
-  else hipLaunchKernelGGL((softmax_kernel<false>), grid, dim3(kBlock), 0, stream, prm);
+  if (plan) FG_LAUNCH((softmax_kernel<true>), grid, stream, prm);
+  else FG_LAUNCH((softmax_kernel<false>), grid, stream, prm);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || !plan || plan->num_slots == 0) return err;
-  hipLaunchKernelGGL(softmax_split_kernel, grid_for(plan->num_slots, 1), dim3(kBlock), 0, stream,
-                     prm, plan->num_slots);
+  FG_LAUNCH(softmax_rowstats_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, prm);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  FG_LAUNCH(softmax_split_kernel, grid_for(plan->num_slots, 1), stream, prm, plan->num_slots);
   return hipGetLastError();
 }
 

@@ -136,6 +136,10 @@ def test_plan_create_rejects_invalid_arguments():
     assert L.fg_plan_create(ctypes.byref(g), None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1
     opt.reserved[2] = 0
+    opt.max_row_segments = 1  # a row must be allowed at least two pieces
+    assert L.fg_plan_create(ctypes.byref(g), None, 8, ctypes.byref(opt), ctypes.byref(h),
+                            None) == -1
+    opt.max_row_segments = 0
     opt.segment_edges = -5
     assert L.fg_plan_create(ctypes.byref(g), None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1
@@ -159,8 +163,8 @@ def test_binding_refuses_cpu_tensors():
 # ---------------------------------------------------------------- schedule
 
 
-def _check_schedule(indptr, S):
-    segs, n_split, n_slot = fg.schedule_host(indptr, S)
+def _check_schedule(indptr, S, cap=128):
+    segs, n_split, n_slot = fg.schedule_host(indptr, S, cap)
     num_rows = indptr.size - 1
     deg = np.diff(indptr.astype(np.int64))
     # every edge covered exactly once, every row present
@@ -172,28 +176,33 @@ def _check_schedule(indptr, S):
         rows_seen[r] += 1
     assert np.all(cover == 1)
     assert np.all(rows_seen >= 1)
-    # split rows: deg > S, pieces <= S and balanced, slots = positions
-    split = deg > S
+    # k = min(ceil(deg / S), cap) pieces; split when k >= 2
+    k = np.minimum(np.maximum(-(-deg // S), 1), cap)
+    split = k >= 2
     assert n_split == int(split.sum())
-    assert n_slot == int(np.sum(-(-deg[split] // S)))
+    assert n_slot == int(k[split].sum())
+    assert np.all(rows_seen == k)
     assert np.all(segs[:n_slot, 3] == np.arange(n_slot))
     assert np.all(segs[n_slot:, 3] == -1)
     lens = segs[:, 2] - segs[:, 1]
-    assert np.all(lens <= S)
+    assert np.all(lens <= np.maximum(S, -(-deg[segs[:, 0]] // cap)))
     for r in np.nonzero(split)[0]:
-        ls = lens[:n_slot][segs[:n_slot, 0] == r]
+        sl = np.nonzero(segs[:n_slot, 0] == r)[0]
+        assert np.all(np.diff(sl) == 1)  # a split row's slots are contiguous
+        ls = lens[sl]
         assert ls.max() - ls.min() <= 1
-    # whole rows: decreasing degree, then empty rows
+    # longest segments first among split rows, then whole rows by degree, empty last
+    if n_slot:
+        assert np.all(np.diff(deg[segs[:n_slot, 0]] / k[segs[:n_slot, 0]]) <= 1e-9)
     tail = lens[n_slot:]
     assert np.all(np.diff(tail) <= 0)
-    assert np.all(rows_seen[~split] == 1)
     return segs
 
 
-@pytest.mark.parametrize("S", [1, 7, 64, 1024])
-def test_schedule_covers_every_edge(S):
+@pytest.mark.parametrize("S,cap", [(1, 128), (7, 128), (64, 2), (64, 128), (1024, 4)])
+def test_schedule_covers_every_edge(S, cap):
     w = synth.make_config("rmat_233k_115m", scale_down=512)
-    _check_schedule(w.csr.indptr, S)
+    _check_schedule(w.csr.indptr, S, cap)
 
 
 def test_schedule_edge_cases():
