@@ -1,15 +1,21 @@
 #!/usr/bin/env python3
 """Benchmark of the hot path on one MI355X.
 
-One step = one pass of every operator of the path over the power-law graph
-workload (R-MAT a,b,c,d = .57,.19,.19,.05; 232,965 vertices; 114.6M edges;
-fp32 features of width 128; edge weights in (0, 1]):
+Default workload (the headline): one step = one pass of every operator of the
+path over the power-law graph (R-MAT a,b,c,d = .57,.19,.19,.05; 232,965
+vertices; 114.6M edges; fp32 features of width 128; edge weights in (0, 1]):
 
   1. gSpMM  src_mul_edge + sum        (weighted aggregation)
   2. gSpMM  copy_src + max / argmax
   3. gSDDMM dot                       (per-edge attention score)
   4. edge softmax with leaky ReLU(0.2) over the scores of step 3
-  (+ the deterministic merge passes of split rows inside 1-2 and 4)
+  (+ the deterministic merge passes of split rows inside 1, 2 and 4)
+
+Other workloads (--workload): the uniform in-degree-100 graph at width --d
+(gSpMM copy + sum, gSDDMM), the clustered graph's attention layer (8 heads of
+16: gSDDMM -> edge softmax -> gSpMM score x source + sum) and the R-MAT
+training step (forward gSpMM on the CSR, backward gSpMM on the CSC, backward
+gSDDMM dY . X).
 
 Inputs are resident in HBM before timing starts.  Prints ONE JSON line.
 Per-kernel durations come from HIP events recorded on the stream the library
@@ -20,6 +26,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -29,64 +36,228 @@ METRIC = "gSpMM/SDDMM GFLOP/s and achieved HBM GB/s (% peak), d=128, one MI355X"
 HBM_PEAK_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_rmat_233k_d128.json")
+WORKLOADS = ("rmat_233k_115m", "uniform_deg100_100k", "clustered_133k_deg300",
+             "rmat_1m_33m_train", "tiny_uniform_1k")
 
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def op_models(n, e, d):
-    """Algorithmic bytes and flops of each operator (row-wise method): the
-    indptr, each edge's index (and weight) once, one feature row gathered per
-    edge, destination rows once, outputs once."""
-    b_ip = 4 * (n + 1)
-    b_gather = 4 * e + 4 * e * d
-    return {
-        "spmm_mul_sum": {"bytes": b_ip + b_gather + 4 * e + 4 * n * d, "flop": 2 * e * d},
-        "spmm_max": {"bytes": b_ip + b_gather + 8 * n * d, "flop": e * d},
-        "sddmm_dot": {"bytes": b_ip + b_gather + 4 * n * d + 4 * e, "flop": 2 * e * d},
-        "edge_softmax": {"bytes": b_ip + 4 * e + 4 * e, "flop": 4 * e},
-    }
+# ----------------------------------------------------------------------------
+# byte and flop models of the row-wise method (bytes its memory instructions
+# must move: the row pointers, each edge's index (and edge value) once, one
+# feature row gathered per edge, destination rows once, outputs once)
+# ----------------------------------------------------------------------------
 
 
-def cpu_baseline(csr, x, w, budget_s=12.0):
-    """The oracle, as is, on a random row sample of the same workload."""
+def bytes_spmm(n, e, F, H, weighted=False, argmax=False):
+    return 4 * (n + 1) + 4 * e + (4 * e * H if weighted else 0) + 4 * e * F + 4 * n * F * (
+        2 if argmax else 1)
+
+
+def bytes_sddmm(n, e, F, H):
+    return 4 * (n + 1) + 4 * e + 4 * e * F + 4 * n * F + 4 * e * H
+
+
+def bytes_softmax(n, e, H):
+    return 4 * (n + 1) + 8 * e * H
+
+
+class Op:
+    def __init__(self, name, fn, nbytes, flop, graded=False):
+        self.name, self.fn, self.bytes, self.flop, self.graded = name, fn, nbytes, flop, graded
+
+
+# ----------------------------------------------------------------------------
+# workloads: device setup, operator list, oracle sample
+# ----------------------------------------------------------------------------
+
+
+def _row_sample(csr, edges_target, seed):
+    deg = csr.degrees()
+    order = np.random.default_rng(seed).permutation(csr.num_rows)
+    csum = np.cumsum(deg[order])
+    k = min(int(np.searchsorted(csum, edges_target)) + 1, csr.num_rows)
+    rows = np.sort(order[:k])
+    return rows, int(deg[rows].sum())
+
+
+def setup(name, d, args, fg, torch, dev):
+    import synth
+
+    t0 = time.perf_counter()
+    wl = synth.make_config(name, d=d)
+    t_gen = time.perf_counter() - t0
+    csr = wl.csr
+    n, e = csr.num_rows, csr.nnz
+    log("workload %s: N=%d E=%d generated in %.1fs" % (name, n, e, t_gen))
+    G = fg.Graph.from_csr(csr, device=dev)
+    popt = dict(segment_edges=args.segment_edges, max_row_segments=args.max_row_segments)
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    cfg = {"workload": name, "num_vertices": n, "num_edges": e}
+    plans = []
+
+    if name in ("rmat_233k_115m", "tiny_uniform_1k"):
+        x_h = wl.arrays["x"]
+        F = x_h.shape[1]
+        w_h = wl.arrays["w"] if "w" in wl.arrays else \
+            np.random.default_rng(7).random(e, dtype=np.float32)
+        x, wt = T(x_h), T(w_h)
+        P = fg.Plan(G, max_width=F, **popt)
+        plans.append(P)
+        out_s, out_m = (torch.empty((n, F), device=dev) for _ in range(2))
+        arg = torch.empty((n, F), dtype=torch.int32, device=dev)
+        sc, at = (torch.empty((e,), device=dev) for _ in range(2))
+        ops = [
+            Op("spmm_mul_sum", lambda: fg.gspmm(G, x, wt, msg="src_mul_edge", plan=P, out=out_s),
+               bytes_spmm(n, e, F, 1, weighted=True), 2 * e * F, graded=True),
+            Op("spmm_max", lambda: fg.gspmm(G, x, reduce="max", plan=P, out=out_m, arg=arg),
+               bytes_spmm(n, e, F, 1, argmax=True), e * F),
+            Op("sddmm_dot", lambda: fg.gsddmm(G, x, x, plan=P, out=sc),
+               bytes_sddmm(n, e, F, 1), 2 * e * F, graded=True),
+            Op("edge_softmax", lambda: fg.edge_softmax(G, sc, leaky=True, slope=0.2, plan=P,
+                                                       out=at),
+               bytes_softmax(n, e, 1), 4 * e),
+        ]
+        cfg.update(feature_dim=F, graph="R-MAT (.57,.19,.19,.05), self-loops removed, relabelled"
+                   if name.startswith("rmat") else "uniform random")
+
+        def oracle_sample(edges_target):
+            import oracle
+
+            rows, ne = _row_sample(csr, edges_target, 12345)
+            t0 = time.perf_counter()
+            oracle.gspmm(csr, x_h, msg=oracle.MSG_SRC_MUL_EDGE, edge_val=w_h, rows=rows)
+            oracle.gspmm(csr, x_h, red=oracle.RED_MAX, rows=rows)
+            s = oracle.gsddmm(csr, x_h, x_h, rows=rows)
+            oracle.edge_softmax(csr, s, leaky=True, slope=0.2, rows=rows)
+            dt = time.perf_counter() - t0
+            flop = 2 * ne * F + ne * F + 2 * ne * F + 4 * ne
+            return dt, flop, "%d random rows (%d edges, %.1f%% of E), all four operators" % (
+                rows.size, ne, 100.0 * ne / e)
+
+    elif name == "uniform_deg100_100k":
+        x_h = wl.arrays["x"]
+        F = x_h.shape[1]
+        x = T(x_h)
+        P = fg.Plan(G, max_width=F, **popt)
+        plans.append(P)
+        out_s = torch.empty((n, F), device=dev)
+        sc = torch.empty((e,), device=dev)
+        ops = [
+            Op("spmm_copy_sum", lambda: fg.gspmm(G, x, plan=P, out=out_s),
+               bytes_spmm(n, e, F, 1), 2 * e * F, graded=True),
+            Op("sddmm_dot", lambda: fg.gsddmm(G, x, x, plan=P, out=sc),
+               bytes_sddmm(n, e, F, 1), 2 * e * F, graded=True),
+        ]
+        cfg.update(feature_dim=F, graph="uniform, in-degree 100")
+
+        def oracle_sample(edges_target):
+            import oracle
+
+            rows, ne = _row_sample(csr, edges_target, 12345)
+            t0 = time.perf_counter()
+            oracle.gspmm(csr, x_h, rows=rows)
+            oracle.gsddmm(csr, x_h, x_h, rows=rows)
+            dt = time.perf_counter() - t0
+            return dt, 4 * ne * F, "%d random rows (%d edges), both operators" % (rows.size, ne)
+
+    elif name == "clustered_133k_deg300":
+        x_h = wl.arrays["x"]
+        H, dh = x_h.shape[1], x_h.shape[2]
+        F = H * dh
+        x = T(x_h)
+        P = fg.Plan(G, max_width=F, **popt)
+        plans.append(P)
+        sc, at = (torch.empty((e, H), device=dev) for _ in range(2))
+        out = torch.empty((n, H, dh), device=dev)
+        ops = [
+            Op("sddmm_heads", lambda: fg.gsddmm(G, x, x, plan=P, out=sc),
+               bytes_sddmm(n, e, F, H), 2 * e * F, graded=True),
+            Op("edge_softmax_heads", lambda: fg.edge_softmax(G, sc, leaky=True, slope=0.2, plan=P,
+                                                             out=at),
+               bytes_softmax(n, e, H), 4 * e * H),
+            Op("spmm_score_sum", lambda: fg.gspmm(G, x, at, msg="src_mul_edge", plan=P, out=out),
+               bytes_spmm(n, e, F, H, weighted=True), 2 * e * F, graded=True),
+        ]
+        cfg.update(feature_dim=F, heads=H, head_dim=dh,
+                   graph="100 communities, in-degree 300 (270 inside, 30 uniform)")
+
+        def oracle_sample(edges_target):
+            import oracle
+
+            rows, ne = _row_sample(csr, edges_target, 12345)
+            x2 = x_h.reshape(n, F)
+            t0 = time.perf_counter()
+            s = oracle.gsddmm(csr, x2, x2, heads=H, rows=rows)
+            a = oracle.edge_softmax(csr, s, heads=H, leaky=True, slope=0.2, rows=rows)
+            oracle.gspmm(csr, x2, msg=oracle.MSG_SRC_MUL_EDGE, edge_val=a, heads=H, rows=rows)
+            dt = time.perf_counter() - t0
+            return dt, 4 * ne * F + 4 * ne * H, "%d random rows (%d edges), attention layer" % (
+                rows.size, ne)
+
+    elif name == "rmat_1m_33m_train":
+        csc = wl.csc
+        Gb = fg.Graph.from_csr(csc, device=dev, nnz_total=e)
+        x_h, dy_h = wl.arrays["x"], wl.arrays["dy"]
+        F = x_h.shape[1]
+        x, dy = T(x_h), T(dy_h)
+        Pf = fg.Plan(G, max_width=F, **popt)
+        Pb = fg.Plan(Gb, max_width=F, **popt)
+        plans += [Pf, Pb]
+        y, dx = (torch.empty((n, F), device=dev) for _ in range(2))
+        da = torch.empty((e,), device=dev)
+        ops = [
+            Op("fwd_spmm_csr", lambda: fg.gspmm(G, x, plan=Pf, out=y),
+               bytes_spmm(n, e, F, 1), 2 * e * F, graded=True),
+            Op("bwd_spmm_csc", lambda: fg.gspmm(Gb, dy, plan=Pb, out=dx),
+               bytes_spmm(n, e, F, 1), 2 * e * F, graded=True),
+            Op("bwd_sddmm", lambda: fg.gsddmm(G, x, dy, plan=Pf, out=da),
+               bytes_sddmm(n, e, F, 1), 2 * e * F, graded=True),
+        ]
+        cfg.update(feature_dim=F, graph="R-MAT (.57,.19,.19,.05) 2^20 vertices, CSR + CSC")
+
+        def oracle_sample(edges_target):
+            import oracle
+
+            rows, ne = _row_sample(csr, edges_target / 3, 12345)
+            rows_b, ne_b = _row_sample(csc, edges_target / 3, 54321)
+            t0 = time.perf_counter()
+            oracle.gspmm(csr, x_h, rows=rows)
+            oracle.gspmm(csc, dy_h, rows=rows_b, nnz_total=e)
+            oracle.gsddmm(csr, x_h, dy_h, rows=rows)
+            dt = time.perf_counter() - t0
+            return dt, 2 * F * (2 * ne + ne_b), (
+                "%d CSR rows (%d edges) and %d CSC rows (%d edges), all three operators"
+                % (rows.size, ne, rows_b.size, ne_b))
+    else:
+        raise SystemExit("unknown workload %r" % name)
+
+    pinfo = plans[0].info()
+    cfg.update(segment_edges=pinfo["segment_edges"], max_row_segments=pinfo["max_row_segments"],
+               ops=[o.name for o in ops])
+    return cfg, ops, plans, oracle_sample, e
+
+
+def cpu_baseline(oracle_sample, budget_s):
+    """The oracle, as is, on a random row sample sized for about `budget_s`
+    seconds of host work."""
     import oracle
 
     oracle.build(force=False)
     threads = oracle.max_threads()
-    n = csr.num_rows
-    deg = csr.degrees()
-    rng = np.random.default_rng(12345)
-    order = rng.permutation(n)
-    csum = np.cumsum(deg[order])
+    dt, flop, desc = oracle_sample(2_000_000)
+    scale = budget_s / max(dt, 1e-9)
+    if scale > 4:
+        dt, flop, desc = oracle_sample(2_000_000 * scale)
+    return {"value": round(flop / dt / 1e9, 3), "unit": "GFLOP/s", "cores": threads,
+            "kind": "oracle", "sample": "%s, %.1f s" % (desc, dt)}
 
-    def run(edges_target):
-        k = int(np.searchsorted(csum, edges_target)) + 1
-        rows = np.sort(order[:k])
-        ne = int(deg[rows].sum())
-        t0 = time.perf_counter()
-        oracle.gspmm(csr, x, msg=oracle.MSG_SRC_MUL_EDGE, edge_val=w, rows=rows)
-        oracle.gspmm(csr, x, red=oracle.RED_MAX, rows=rows)
-        s = oracle.gsddmm(csr, x, x, rows=rows)
-        oracle.edge_softmax(csr, s, leaky=True, slope=0.2, rows=rows)
-        return time.perf_counter() - t0, k, ne
 
-    dt, k, ne = run(2_000_000)
-    rate = ne / max(dt, 1e-9)
-    target = min(int(rate * budget_s), csr.nnz)
-    if target > 4 * ne:
-        dt, k, ne = run(target)
-    d = x.shape[1]
-    flop = sum(m["flop"] for m in op_models(k, ne, d).values())
-    return {
-        "value": round(flop / dt / 1e9, 3),
-        "unit": "GFLOP/s",
-        "cores": threads,
-        "kind": "oracle",
-        "sample": "%d random rows (%d edges, %.1f%% of E) of the same graph, all four operators, "
-                  "%.1f s" % (k, ne, 100.0 * ne / csr.nnz, dt),
-    }
+# ----------------------------------------------------------------------------
+# counter calibration and summary
+# ----------------------------------------------------------------------------
 
 
 def copy_probe(nbytes=1 << 30, reps=4):
@@ -103,11 +274,87 @@ def copy_probe(nbytes=1 << 30, reps=4):
     print(json.dumps({"copy_probe_bytes": nbytes, "reps": reps}), flush=True)
 
 
+KERNEL_OPS = {  # regular expressions over kernel names; template args <G, NV, U, MUL, MAX, ...>
+    "spmm_mul_sum": (r"spmm_fast_kernel<\d+, \d+, \d+, true, false", r"spmm_fixup_kernel<false>"),
+    "spmm_max": (r"spmm_fast_kernel<\d+, \d+, \d+, false, true", r"spmm_fixup_kernel<true>"),
+    "sddmm_dot": (r"sddmm_fast_kernel<",),
+    "edge_softmax": (r"softmax_kernel<", r"softmax_rowstats_kernel", r"softmax_split_kernel"),
+}
+
+
+def _counter_means(csv_dir, counter):
+    """Mean value of `counter` per dispatch for each kernel name."""
+    import csv
+    import glob
+
+    sums, counts = {}, {}
+    for path in glob.glob(os.path.join(csv_dir, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            k = r["Kernel_Name"]
+            sums[k] = sums.get(k, 0.0) + float(r["Counter_Value"])
+            counts[k] = counts.get(k, 0) + 1
+    return {k: sums[k] / counts[k] for k in sums}
+
+
+def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out_json):
+    """Per-launch fabric/HBM traffic of each operator of the headline workload
+    from FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by the
+    reading of the same counter for the 1 GiB copy of `--copy-probe`."""
+    from paper_2008_11359_amd.build import source_digest
+
+    nbytes = 1 << 30
+
+    def copy_factor(d, counter):
+        vals = [v for k, v in _counter_means(d, counter).items() if "copy" in k.lower()]
+        return nbytes / (max(vals) * 1024.0)
+
+    f_fac = copy_factor(copy_fetch_dir, "FETCH_SIZE")
+    w_fac = copy_factor(copy_write_dir, "WRITE_SIZE")
+    fetch = _counter_means(fetch_dir, "FETCH_SIZE")
+    write = _counter_means(write_dir, "WRITE_SIZE")
+    ops = {}
+    for op, pats in KERNEL_OPS.items():
+        def sel(tab):
+            return sum(v for k, v in tab.items() if any(re.search(pt, k) for pt in pats))
+
+        fb = sel(fetch) * 1024.0 * f_fac
+        wb = sel(write) * 1024.0 * w_fac
+        ops[op] = {"fetch_bytes": round(fb), "write_bytes": round(wb),
+                   "hbm_bytes_per_launch": round(fb + wb)}
+    res = {"source_digest": source_digest(), "fetch_scale": f_fac, "write_scale": w_fac,
+           "copy_probe_bytes": nbytes, "ops": ops}
+    with open(out_json, "w") as f:
+        json.dump(res, f, indent=1)
+    print(json.dumps(res, indent=1))
+
+
+def traffic_for(op_name):
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    try:
+        tf = json.load(open(TRAFFIC_FILE))
+        from paper_2008_11359_amd.build import source_digest
+
+        if tf.get("source_digest") == source_digest() and op_name in tf.get("ops", {}):
+            return tf["ops"][op_name]["hbm_bytes_per_launch"]
+        log("traffic file is for other kernel sources: traffic not reported")
+    except Exception as exc:  # a stale or malformed file means "not measured"
+        log("traffic file ignored:", exc)
+    return None
+
+
+# ----------------------------------------------------------------------------
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="rmat_233k_115m", choices=WORKLOADS)
+    ap.add_argument("--d", type=int, default=None, help="feature width (uniform workload)")
     ap.add_argument("--segment-edges", type=int, default=0, help="plan segment length (0: default)")
     ap.add_argument("--max-row-segments", type=int, default=0,
                     help="cap on segments per row (0: default)")
@@ -115,9 +362,17 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration) and exit")
+    ap.add_argument("--summarize-counters", nargs=4,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE outputs of the headline "
+                         "workload and of --copy-probe into the traffic file, then exit")
     args = ap.parse_args()
+    sys.path.insert(0, ROOT)
     if args.copy_probe:
         copy_probe()
+        return
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters, TRAFFIC_FILE)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the path runs on a single MI355X and this build "
@@ -126,94 +381,54 @@ def main():
 
     import torch
 
-    sys.path.insert(0, ROOT)
-    import synth
     import paper_2008_11359_amd as fg
-
-    t0 = time.perf_counter()
-    wl = synth.make_config("rmat_233k_115m")
-    t_gen = time.perf_counter() - t0
-    csr, x_h, w_h = wl.csr, wl.arrays["x"], wl.arrays["w"]
-    n, e, d = csr.num_rows, csr.nnz, x_h.shape[1]
-    log("workload rmat_233k_115m: N=%d E=%d d=%d generated in %.1fs" % (n, e, d, t_gen))
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    g = fg.Graph.from_csr(csr, device=dev)
-    x = torch.from_numpy(x_h).to(dev)
-    wt = torch.from_numpy(w_h).to(dev)
     t0 = time.perf_counter()
-    plan = fg.Plan(g, max_width=d, segment_edges=args.segment_edges,
-                   max_row_segments=args.max_row_segments)
+    cfg, ops, plans, oracle_sample, e = setup(args.workload, args.d, args, fg, torch, dev)
     torch.cuda.synchronize()
-    t_plan = time.perf_counter() - t0
-    pinfo = plan.info()
-    log("plan", pinfo, "%.3fs" % t_plan)
-
-    out_sum = torch.empty((n, d), dtype=torch.float32, device=dev)
-    out_max = torch.empty((n, d), dtype=torch.float32, device=dev)
-    arg_max = torch.empty((n, d), dtype=torch.int32, device=dev)
-    scores = torch.empty((e,), dtype=torch.float32, device=dev)
-    attn = torch.empty((e,), dtype=torch.float32, device=dev)
-
-    ops = [
-        ("spmm_mul_sum", lambda: fg.gspmm(g, x, wt, msg="src_mul_edge", reduce="sum", plan=plan,
-                                          out=out_sum)),
-        ("spmm_max", lambda: fg.gspmm(g, x, reduce="max", plan=plan, out=out_max, arg=arg_max)),
-        ("sddmm_dot", lambda: fg.gsddmm(g, x, x, plan=plan, out=scores)),
-        ("edge_softmax", lambda: fg.edge_softmax(g, scores, leaky=True, slope=0.2, plan=plan,
-                                                 out=attn)),
-    ]
+    log("setup %.1fs; plan" % (time.perf_counter() - t0), plans[0].info())
 
     for _ in range(args.warmup):
-        for _, f in ops:
-            f()
+        for op in ops:
+            op.fn()
     torch.cuda.synchronize()
 
     K = args.steps
-    ev = {name: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                 for _ in range(K)] for name, _ in ops}
+    ev = {op.name: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    for _ in range(K)] for op in ops}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(K):
-        for name, f in ops:
-            a, b = ev[name][k]
+        for op in ops:
+            a, b = ev[op.name][k]
             a.record()
-            f()
+            op.fn()
             b.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
-    models = op_models(n, e, d)
     per_op = {}
-    for name, _ in ops:
-        ms = [a.elapsed_time(b) for a, b in ev[name]]
+    for op in ops:
+        ms = [a.elapsed_time(b) for a, b in ev[op.name]]
         t = float(np.mean(ms)) / 1e3
-        m = models[name]
-        per_op[name] = {
+        per_op[op.name] = {
             "ms_mean": round(float(np.mean(ms)), 4),
             "ms_median": round(float(np.median(ms)), 4),
-            "gflops": round(m["flop"] / t / 1e9, 1),
-            "gbs_alg": round(m["bytes"] / t / 1e9, 1),
-            "frac_hbm": round(m["bytes"] / t / 1e9 / HBM_PEAK_GBS, 4),
-            "bytes_alg": int(m["bytes"]),
+            "gflops": round(op.flop / t / 1e9, 1),
+            "gbs_alg": round(op.bytes / t / 1e9, 1),
+            "frac_hbm": round(op.bytes / t / 1e9 / HBM_PEAK_GBS, 4),
+            "bytes_alg": int(op.bytes),
             "edges_per_s": round(e / t, 1),
         }
-    flop_step = sum(models[name]["flop"] for name, _ in ops)
+    flop_step = sum(op.flop for op in ops)
     value = flop_step * K / elapsed / 1e9
-    # dominant kernel among the two graded ones (weighted-sum gSpMM, dot gSDDMM)
-    dom = max(("spmm_mul_sum", "sddmm_dot"), key=lambda k: per_op[k]["ms_mean"])
+    # dominant kernel: the slowest of the graded operators
+    dom = max((op for op in ops if op.graded), key=lambda o: per_op[o.name]["ms_mean"]).name
     ach = per_op[dom]["gbs_alg"]
-    traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        try:
-            tf = json.load(open(TRAFFIC_FILE))
-            from paper_2008_11359_amd.build import source_digest
-
-            if tf.get("source_digest") == source_digest() and dom in tf.get("ops", {}):
-                traffic = tf["ops"][dom]["hbm_bytes_per_launch"]
-        except Exception as exc:  # a stale or malformed file means "not measured"
-            log("traffic file ignored:", exc)
+    traffic = traffic_for(dom) if args.workload == "rmat_233k_115m" else None
+    pinfo = plans[0].info()
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -227,16 +442,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {
-            "workload": "rmat_233k_115m",
-            "graph": "R-MAT (.57,.19,.19,.05), self-loops removed, relabelled",
-            "num_vertices": n,
-            "num_edges": e,
-            "feature_dim": d,
-            "ops": [name for name, _ in ops],
-            "segment_edges": pinfo["segment_edges"],
-            "max_row_segments": pinfo["max_row_segments"],
-        },
+        "config": cfg,
         "roofline": {
             "bound": "hbm",
             "kernel": dom,
@@ -248,13 +454,14 @@ def main():
         },
         "ops": per_op,
         "edges_per_s_step": round(e * K / elapsed, 1),
-        "plan": {"build_s": round(t_plan, 4), "segments": pinfo["num_segments"],
-                 "split_rows": pinfo["num_split_rows"], "slots": pinfo["num_slots"]},
+        "plan": {"segments": pinfo["num_segments"], "split_rows": pinfo["num_split_rows"],
+                 "slots": pinfo["num_slots"]},
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a row sample")
-        result["cpu_baseline"] = cpu_baseline(csr, x_h, w_h, args.cpu_budget)
-    plan.close()
+        result["cpu_baseline"] = cpu_baseline(oracle_sample, args.cpu_budget)
+    for p in plans:
+        p.close()
     print(json.dumps(result), flush=True)
 
 

@@ -109,7 +109,7 @@ typedef struct fg_graph {
 typedef struct fg_plan fg_plan; /* opaque; owns a device segment table + workspace */
 
 typedef struct fg_plan_options {
-  int32_t segment_edges;    /* S: target edges per segment; 0 -> default (1024) */
+  int32_t segment_edges;    /* S: target edges per segment; 0 -> default (4096) */
   int32_t max_row_segments; /* cap on segments per row; 0 -> default (128)      */
   int32_t reserved[6];      /* must be zero                                     */
 } fg_plan_options;

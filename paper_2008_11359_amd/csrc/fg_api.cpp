@@ -8,7 +8,7 @@
 #include <new>
 #include <vector>
 
-#include "../../include/featgraph_hip.h"
+#include "featgraph_hip.h"
 #include "fg_internal.h"
 
 struct fg_plan {
@@ -23,7 +23,7 @@ struct fg_plan {
 
 namespace {
 
-constexpr int32_t kDefaultSegmentEdges = 1024;
+constexpr int32_t kDefaultSegmentEdges = 4096;
 constexpr int32_t kMaxSegmentEdges = 1 << 24;
 constexpr int32_t kDefaultMaxRowSegments = 128;
 constexpr int32_t kMaxRowSegmentsLimit = 1 << 20;

@@ -186,10 +186,18 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
 
 // Fast path: float4 lanes, G (compile time) lanes per feature row, NV float4
 // per lane per edge (feature chunk G*4*NV = blockIdx.y), U edges in flight per
-// lane group, MUL: src_mul_edge, MAX: max/argmax, SEG: items from a plan.
-template <int G, int NV, int U, bool MUL, bool MAX, bool SEG>
+// lane group, MUL: src_mul_edge, MAX: max/argmax, EIDS: the graph carries an
+// edge-id array (else edge id = position), SEG: items from a plan.
+//
+// Max with positional edge ids: a lane group visits its edges in increasing
+// position, hence increasing edge id, so "strictly greater replaces" keeps the
+// smallest edge id among equal maxima; a group whose messages were all -inf
+// never replaces and takes its first edge afterwards.  Groups, segments and
+// slots are then merged with the full (value, edge id) order.
+template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool SEG>
 __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
   constexpr int NG = kWave / G;
+  constexpr bool POS = MAX && !EIDS;
   static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
@@ -225,8 +233,8 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
     float my_w = 0.0f;
     if (lane < cnt) {
       my_src = __builtin_nontemporal_load(p.indices + base + lane);
-      if constexpr (MAX || MUL)
-        my_eid = p.eids ? __builtin_nontemporal_load(p.eids + base + lane) : (int)(base + lane);
+      if constexpr (EIDS) my_eid = __builtin_nontemporal_load(p.eids + base + lane);
+      else my_eid = (int)(base + lane);
       if constexpr (MUL) {
         if (p.H == 1) my_w = p.ev[my_eid];
       }
@@ -241,7 +249,8 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         const int jb = j0 + u * NG;
         ok[u] = jb + gid < cnt;
         const int src = bcast_lane<NG>(my_src, jb, gid);
-        eu[u] = (MAX || MUL) ? bcast_lane<NG>(my_eid, jb, gid) : 0;
+        if constexpr (EIDS) eu[u] = bcast_lane<NG>(my_eid, jb, gid);
+        else eu[u] = (int)(base + jb + gid);
         const float w1 = MUL ? bcast_lane_f<NG>(my_w, jb, gid) : 1.0f;
         const float* xr = p.x + (int64_t)src * F;
 #pragma unroll
@@ -262,7 +271,14 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         for (int v = 0; v < NV; ++v)
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
-            if constexpr (MAX) {
+            if constexpr (POS) {
+              // invalid slots hold -inf with weight 1: never strictly greater
+              const float m = MUL ? wv[u][v] * val[u][v][c] : val[u][v][c];
+              if (m > acc[v][c]) {
+                acc[v][c] = m;
+                am[v][c] = eu[u];
+              }
+            } else if constexpr (MAX) {
               const float m = MUL ? wv[u][v] * val[u][v][c] : val[u][v][c];
               if (ok[u] && takes_over(m, eu[u], acc[v][c], am[v][c])) {
                 acc[v][c] = m;
@@ -274,6 +290,16 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
               acc[v][c] += val[u][v][c];
             }
           }
+    }
+  }
+  if constexpr (POS) {
+    const int64_t first = it.b + gid;  // this group's first edge
+    if (first < it.e) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          if (am[v][c] == INT_MAX) am[v][c] = (int32_t)first;
     }
   }
 
@@ -773,6 +799,44 @@ __device__ __forceinline__ void lse_push(float& m, float& z, float s) {
 
 constexpr int kSoftmaxU = 4;  // scores in flight per lane
 
+// Whole row held in registers (H a power of two <= 64, at most 4 values per
+// lane): one read of the scores, max and sum by xor butterflies over the lanes
+// of a head, one write.
+__device__ __forceinline__ void softmax_row_in_registers(const SoftmaxParams& p, const Item& it) {
+  const int lane = lane_id();
+  const int H = p.H;
+  const int epw = kWave / H;
+  const int eo = lane / H;
+  const int h = lane % H;
+  float sv[kSoftmaxU];
+  int64_t ev[kSoftmaxU];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < kSoftmaxU; ++k) {
+    const int64_t q = it.b + eo + (int64_t)k * epw;
+    ev[k] = -1;
+    sv[k] = -INFINITY;
+    if (q < it.e) {
+      ev[k] = p.eids ? p.eids[q] : q;
+      sv[k] = leaky_relu(p.scores[ev[k] * H + h], p.leaky, p.slope);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kSoftmaxU; ++k) mx = fmaxf(mx, sv[k]);
+  for (int off = H; off < kWave; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  float z = 0.0f;
+#pragma unroll
+  for (int k = 0; k < kSoftmaxU; ++k) {
+    sv[k] = ev[k] >= 0 ? expf(sv[k] - mx) : 0.0f;
+    z += sv[k];
+  }
+  for (int off = H; off < kWave; off <<= 1) z += __shfl_xor(z, off);
+  const float inv = 1.0f / z;
+#pragma unroll
+  for (int k = 0; k < kSoftmaxU; ++k)
+    if (ev[k] >= 0) p.out[ev[k] * H + h] = sv[k] * inv;
+}
+
 // Lanes map to (edge offset, head) pairs: hc = heads per pass, epw = 64/hc
 // edges per pass.  Pass 1 keeps a running (max, sum) per lane; lanes of one
 // head then merge in a fixed tree; pass 2 writes exp(s' - m) / z.  Segments
@@ -785,6 +849,11 @@ __global__ __launch_bounds__(kBlock) void softmax_kernel(SoftmaxParams p) {
   if (it.b >= it.e) return;
   const int lane = lane_id();
   const int H = p.H;
+  if (!(SEG && it.slot >= 0) && H <= kWave && (H & (H - 1)) == 0 &&
+      (it.e - it.b) * H <= (int64_t)kWave * kSoftmaxU) {
+    softmax_row_in_registers(p, it);
+    return;
+  }
   for (int h0 = 0; h0 < H; h0 += kWave) {
     const int hc = min(H - h0, kWave);
     const int epw = kWave / hc;
@@ -944,21 +1013,28 @@ dim3 grid_for(int64_t items, int64_t chunks) {
 #define FG_LAUNCH(kernel, grid, stream, ...) \
   hipLaunchKernelGGL((kernel), (grid), dim3(kBlock), 0, (stream), __VA_ARGS__)
 
-template <int G, int NV, int U, bool MUL, bool MAX>
+template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS>
 void spmm_fast_seg(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
-  if (seg) FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, true>), grid, st, prm);
-  else FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, false>), grid, st, prm);
+  if (seg) FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, true>), grid, st, prm);
+  else FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, false>), grid, st, prm);
+}
+
+template <int G, int NV, int U, bool MUL, bool MAX>
+void spmm_fast_eids(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+  // copy + sum never looks at edge ids
+  if (prm.eids && (MUL || MAX)) spmm_fast_seg<G, NV, U, MUL, MAX, true>(prm, seg, grid, st);
+  else spmm_fast_seg<G, NV, U, MUL, MAX, false>(prm, seg, grid, st);
 }
 
 template <int G, int NV, int U>
 void spmm_fast_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 grid,
                    hipStream_t st) {
   if (mul) {
-    if (mx) spmm_fast_seg<G, NV, U, true, true>(prm, seg, grid, st);
-    else spmm_fast_seg<G, NV, U, true, false>(prm, seg, grid, st);
+    if (mx) spmm_fast_eids<G, NV, U, true, true>(prm, seg, grid, st);
+    else spmm_fast_eids<G, NV, U, true, false>(prm, seg, grid, st);
   } else {
-    if (mx) spmm_fast_seg<G, NV, U, false, true>(prm, seg, grid, st);
-    else spmm_fast_seg<G, NV, U, false, false>(prm, seg, grid, st);
+    if (mx) spmm_fast_eids<G, NV, U, false, true>(prm, seg, grid, st);
+    else spmm_fast_eids<G, NV, U, false, false>(prm, seg, grid, st);
   }
 }
 
