@@ -181,6 +181,13 @@ def setup(name, d, args, fg, torch, dev):
             Op("spmm_score_sum", lambda: fg.gspmm(G, x, at, msg="src_mul_edge", plan=P, out=out),
                bytes_spmm(n, e, F, H, weighted=True), 2 * e * F, graded=True),
         ]
+        if args.fused:
+            # the same layer in one kernel: each source row gathered once, no [E, H] arrays
+            ops = [Op("gat_fused", lambda: fg.gat_aggregate(G, x, leaky=True, slope=0.2, plan=P,
+                                                             out=out),
+                      4 * (n + 1) + 4 * e + 4 * e * F + 8 * n * F, 4 * e * F + 4 * e * H,
+                      graded=True)]
+            cfg["fused"] = True
         cfg.update(feature_dim=F, heads=H, head_dim=dh,
                    graph="100 communities, in-degree 300 (270 inside, 30 uniform)")
 
@@ -358,6 +365,8 @@ def main():
     ap.add_argument("--segment-edges", type=int, default=0, help="plan segment length (0: default)")
     ap.add_argument("--max-row-segments", type=int, default=0,
                     help="cap on segments per row (0: default)")
+    ap.add_argument("--fused", action="store_true",
+                    help="attention workload: one fused kernel instead of three operators")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--copy-probe", action="store_true",

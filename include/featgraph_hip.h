@@ -194,6 +194,25 @@ fg_status fg_edge_softmax(const fg_graph* g, int32_t num_heads, const float* sco
                           int32_t apply_leaky_relu, float negative_slope, float* out,
                           fg_plan* plan, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Fused attention aggregation: the three steps above in one pass, without
+ * materialising per-edge scores (the paper's point that UDFs are inlined into
+ * the template instead of messages being materialised on every edge,
+ * Sec. III-B and Sec. IV-A).  For every row v and head h:
+ *   s_e  = sum_k x_src[u, h, k] * x_dst[v, h, k]          (Eq. 4 per head, Fig. 4b)
+ *   a_e  = softmax over the row of leaky_relu(s_e)         (optional leaky ReLU)
+ *   out[v, h, :] = sum_e a_e * x_src[u, h, :]              (Eq. 1, src_mul_edge + sum)
+ * equal, up to rounding, to fg_gsddmm -> fg_edge_softmax -> fg_gspmm.  Each
+ * source row is gathered once per edge; rows without edges give 0.
+ * x_src [num_cols, H, dh]; x_dst [num_rows, H, dh]; out [num_rows, H, dh].
+ * Supported shapes: dh % 4 == 0, dh / 4 a power of two, H * dh <= 256, and
+ * 16-byte aligned feature arrays; otherwise FG_ERR_UNSUPPORTED (compose the
+ * three calls instead).  A plan must have max_width >= H * dh.
+ * ------------------------------------------------------------------------- */
+fg_status fg_gat_aggregate(const fg_graph* g, int32_t num_heads, int64_t head_dim,
+                           const float* x_src, const float* x_dst, int32_t apply_leaky_relu,
+                           float negative_slope, float* out, fg_plan* plan, void* stream);
+
 const char* fg_status_string(fg_status s); /* static storage, never NULL */
 int32_t fg_abi_version(void);              /* == FG_ABI_VERSION */
 

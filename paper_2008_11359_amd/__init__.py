@@ -81,7 +81,7 @@ class Segment(ctypes.Structure):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
-            "HIP library %s is missing: build it with `python -m paper_2008_11359_amd.build` "
+            "HIP library %s is missing: build it with `python paper_2008_11359_amd/build.py` "
             "(there is no CPU fallback)" % LIB_PATH)
     lib = ctypes.CDLL(LIB_PATH)
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
@@ -104,6 +104,8 @@ def _load():
     lib.fg_gspmm.argtypes = [gp, ctypes.c_int, ctypes.c_int, i32, i64, vp, vp, vp, vp, vp, vp]
     lib.fg_gsddmm.restype = ctypes.c_int
     lib.fg_gsddmm.argtypes = [gp, ctypes.c_int, i32, i64, vp, vp, vp, vp, vp]
+    lib.fg_gat_aggregate.restype = ctypes.c_int
+    lib.fg_gat_aggregate.argtypes = [gp, i32, i64, vp, vp, i32, ctypes.c_float, vp, vp, vp]
     lib.fg_edge_softmax.restype = ctypes.c_int
     lib.fg_edge_softmax.argtypes = [gp, i32, vp, i32, ctypes.c_float, vp, vp, vp]
     if lib.fg_abi_version() != ABI_VERSION:
@@ -378,5 +380,36 @@ def edge_softmax(g: Graph, scores: torch.Tensor, leaky: bool = True, slope: floa
     return out
 
 
-__all__ = ["Graph", "Plan", "gspmm", "gsddmm", "edge_softmax", "schedule_host", "FgError",
+def gat_aggregate(g: Graph, x_src: torch.Tensor, x_dst: Optional[torch.Tensor] = None,
+                  heads: int = 1, leaky: bool = True, slope: float = 0.2,
+                  plan: Optional[Plan] = None, out: Optional[torch.Tensor] = None):
+    """Fused gsddmm -> edge_softmax -> gspmm(src_mul_edge, sum): for every row
+    v and head h, out[v, h] = sum over in-edges of softmax(leaky(x_src[u, h] .
+    x_dst[v, h])) * x_src[u, h], without per-edge intermediates.  Raises
+    FgError(FG_ERR_UNSUPPORTED) for shapes the fused kernel does not cover."""
+    x_src = _dev_tensor(x_src, torch.float32, "x_src")
+    x_dst = x_src if x_dst is None else _dev_tensor(x_dst, torch.float32, "x_dst")
+    if x_src.shape[0] != g.num_cols or x_dst.shape[0] != g.num_rows:
+        raise ValueError("x_src needs num_cols rows and x_dst num_rows rows")
+    if x_src.shape[1:] != x_dst.shape[1:]:
+        raise ValueError("x_src and x_dst must have the same feature shape")
+    if x_src.dim() == 3:
+        heads = int(x_src.shape[1])
+    F = int(np.prod(x_src.shape[1:])) if x_src.dim() > 1 else 1
+    if F % heads:
+        raise ValueError("feature width not divisible by heads")
+    shape = (g.num_rows,) + tuple(x_src.shape[1:])
+    out = torch.empty(shape, dtype=torch.float32, device=x_src.device) if out is None else \
+        _dev_tensor(out, torch.float32, "out")
+    if out.numel() != g.num_rows * F:
+        raise ValueError("out has the wrong size")
+    st = _lib.fg_gat_aggregate(ctypes.byref(g._c), heads, F // heads, _ptr(x_src), _ptr(x_dst),
+                               1 if leaky else 0, float(slope), _ptr(out), _plan_handle(plan),
+                               _stream())
+    _check(st, "fg_gat_aggregate")
+    return out
+
+
+__all__ = ["Graph", "Plan", "gspmm", "gsddmm", "edge_softmax", "gat_aggregate", "schedule_host",
+           "FgError",
            "status_string", "LIB_PATH"]

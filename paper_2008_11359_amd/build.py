@@ -1,6 +1,7 @@
 """Builds the gfx950 shared library ``_build/libfeatgraph_hip.so`` in-tree.
 
-Run ``python -m paper_2008_11359_amd.build`` (or call ``build()``).  hipcc
+Run ``python paper_2008_11359_amd/build.py`` (by path: importing the package
+would load the library it is about to rebuild).  hipcc
 cross-compiles for gfx950 without a GPU present.  Packed-fp32 instructions are
 disabled for the device code.
 """

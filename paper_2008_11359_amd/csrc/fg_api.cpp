@@ -401,4 +401,27 @@ fg_status fg_edge_softmax(const fg_graph* g, int32_t num_heads, const float* sco
                                           static_cast<hipStream_t>(stream)));
 }
 
+fg_status fg_gat_aggregate(const fg_graph* g, int32_t num_heads, int64_t head_dim,
+                           const float* x_src, const float* x_dst, int32_t apply_leaky_relu,
+                           float negative_slope, float* out, fg_plan* plan, void* stream) {
+  fg_status st = check_graph(g);
+  if (st != FG_OK) return st;
+  if ((st = check_width(num_heads, head_dim)) != FG_OK) return st;
+  const int64_t F = (int64_t)num_heads * head_dim;
+  if (g->num_rows > 0 && !out) return FG_ERR_INVALID_ARG;
+  if (g->nnz > 0 && (!x_src || !x_dst)) return FG_ERR_INVALID_ARG;
+  if ((st = check_plan(plan, g, F)) != FG_OK) return st;
+  const int64_t out_b = g->num_rows * F * 4;
+  if (overlaps(out, out_b, x_src, g->num_cols * F * 4) ||
+      overlaps(out, out_b, x_dst, g->num_rows * F * 4))
+    return FG_ERR_INVALID_ARG;
+  const uintptr_t al = reinterpret_cast<uintptr_t>(x_src) | reinterpret_cast<uintptr_t>(x_dst) |
+                       reinterpret_cast<uintptr_t>(out);
+  if (!fg::gat_fused_supported(num_heads, head_dim) || (al & 15u) != 0) return FG_ERR_UNSUPPORTED;
+  const fg::GraphView gv = view_of(g);
+  return from_hip(fg::launch_gat_fused(gv, plan ? &plan->view : nullptr, num_heads, head_dim,
+                                       x_src, x_dst, apply_leaky_relu != 0, negative_slope, out,
+                                       static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

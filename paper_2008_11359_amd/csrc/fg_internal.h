@@ -51,4 +51,11 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
                                const float* scores, bool leaky, float slope, float* out,
                                hipStream_t stream);
 
+// Fused SDDMM -> leaky ReLU -> edge softmax -> weighted gSpMM.  Supported
+// shapes: dh % 4 == 0, dh / 4 a power of two, H * dh <= 256; aligned inputs.
+bool gat_fused_supported(int64_t H, int64_t dh);
+hipError_t launch_gat_fused(const GraphView& g, const PlanView* plan, int64_t H, int64_t dh,
+                            const float* xs, const float* xd, bool leaky, float slope, float* out,
+                            hipStream_t stream);
+
 }  // namespace fg

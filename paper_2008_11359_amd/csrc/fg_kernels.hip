@@ -769,6 +769,7 @@ struct SoftmaxParams {
   int32_t H;
   int32_t leaky;
   float slope;
+  int32_t contig;  // edge id == position, H a power of two <= 64, 16-byte aligned arrays
 };
 
 __device__ __forceinline__ float leaky_relu(float s, int on, float slope) {
@@ -837,6 +838,236 @@ __device__ __forceinline__ void softmax_row_in_registers(const SoftmaxParams& p,
     if (ev[k] >= 0) p.out[ev[k] * H + h] = sv[k] * inv;
 }
 
+// ---- contiguous rows: edge id == position, so a row's scores are the flat
+// range [b*H, e*H) of the [E, H] array.  Lane l reads float4 number
+// k = l + 64 i of the range starting at T0 = (b*H) rounded down to 4; since H
+// divides 256, element c of every float4 a lane reads has the same head
+// (T0 + 4l + c) mod H.  Partial float4s at the ends (H < 4) use scalar access.
+
+constexpr int kContigRegs = 12;  // float4 per lane held in registers (3072 values)
+
+struct ContigRange {
+  int64_t lo, hi, T0, K;  // valid flat range, aligned start, number of float4
+};
+
+__device__ __forceinline__ ContigRange contig_range(int64_t b, int64_t e, int H) {
+  ContigRange r;
+  r.lo = b * H;
+  r.hi = e * H;
+  r.T0 = r.lo & ~int64_t(3);
+  r.K = (r.hi - r.T0 + 3) >> 2;
+  return r;
+}
+
+// Loads float4 k of the range (leaky ReLU applied); invalid elements get -inf.
+__device__ __forceinline__ void contig_load(const SoftmaxParams& p, const ContigRange& r,
+                                            int64_t k, float (&v)[4]) {
+  const int64_t t0 = r.T0 + 4 * k;
+  if (t0 >= r.lo && t0 + 4 <= r.hi) {
+    load_vec<4>(p.scores + t0, v);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = leaky_relu(v[c], p.leaky, p.slope);
+  } else {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int64_t t = t0 + c;
+      v[c] = (t >= r.lo && t < r.hi) ? leaky_relu(p.scores[t], p.leaky, p.slope) : -INFINITY;
+    }
+  }
+}
+
+__device__ __forceinline__ void contig_store(const SoftmaxParams& p, const ContigRange& r,
+                                             int64_t k, const float (&v)[4]) {
+  const int64_t t0 = r.T0 + 4 * k;
+  if (t0 >= r.lo && t0 + 4 <= r.hi) {
+    store_vec<4>(p.out + t0, v);
+  } else {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int64_t t = t0 + c;
+      if (t >= r.lo && t < r.hi) p.out[t] = v[c];
+    }
+  }
+}
+
+// Combines the 4 slots of a lane that hold the same head (H < 4), then the
+// lanes that hold the same heads (xor over lane bits >= log2(max(H/4, 1))).
+__device__ __forceinline__ void contig_allmax(float (&m)[4], int H) {
+  if (H == 1) {
+    float t = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
+    for (int off = 1; off < kWave; off <<= 1) t = fmaxf(t, __shfl_xor(t, off));
+    m[0] = m[1] = m[2] = m[3] = t;
+  } else if (H == 2) {
+    float a = fmaxf(m[0], m[2]), b = fmaxf(m[1], m[3]);
+    for (int off = 1; off < kWave; off <<= 1) {
+      a = fmaxf(a, __shfl_xor(a, off));
+      b = fmaxf(b, __shfl_xor(b, off));
+    }
+    m[0] = m[2] = a;
+    m[1] = m[3] = b;
+  } else {
+    for (int off = H / 4; off < kWave; off <<= 1)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) m[c] = fmaxf(m[c], __shfl_xor(m[c], off));
+  }
+}
+
+__device__ __forceinline__ void contig_allsum(float (&z)[4], int H) {
+  if (H == 1) {
+    float t = (z[0] + z[1]) + (z[2] + z[3]);
+    for (int off = 1; off < kWave; off <<= 1) t += __shfl_xor(t, off);
+    z[0] = z[1] = z[2] = z[3] = t;
+  } else if (H == 2) {
+    float a = z[0] + z[2], b = z[1] + z[3];
+    for (int off = 1; off < kWave; off <<= 1) {
+      a += __shfl_xor(a, off);
+      b += __shfl_xor(b, off);
+    }
+    z[0] = z[2] = a;
+    z[1] = z[3] = b;
+  } else {
+    for (int off = H / 4; off < kWave; off <<= 1)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) z[c] += __shfl_xor(z[c], off);
+  }
+}
+
+__device__ __forceinline__ void contig_alllse(float (&m)[4], float (&z)[4], int H) {
+  if (H == 1) {
+    for (int c = 1; c < 4; ++c) lse_merge(m[0], z[0], m[c], z[c]);
+    m[1] = m[2] = m[3] = m[0];
+    z[1] = z[2] = z[3] = z[0];
+  } else if (H == 2) {
+    lse_merge(m[0], z[0], m[2], z[2]);
+    lse_merge(m[1], z[1], m[3], z[3]);
+    m[2] = m[0]; z[2] = z[0];
+    m[3] = m[1]; z[3] = z[1];
+  }
+  for (int off = H >= 4 ? H / 4 : 1; off < kWave; off <<= 1)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float om = __shfl_xor(m[c], off), oz = __shfl_xor(z[c], off);
+      lse_merge(m[c], z[c], om, oz);
+    }
+}
+
+// Head of slot c of this lane, and whether this lane publishes that head's
+// per-segment statistics (one lane per head).
+__device__ __forceinline__ int contig_head(const ContigRange& r, int lane, int c, int H) {
+  return (int)((r.T0 + 4 * lane + c) % H);
+}
+
+// Whole row in registers: exact max, one exp per value, one read, one write.
+__device__ __forceinline__ void softmax_contig_regs(const SoftmaxParams& p, const Item& it) {
+  const int lane = lane_id();
+  const int H = p.H;
+  const ContigRange r = contig_range(it.b, it.e, H);
+  const int rounds = (int)((r.K + kWave - 1) / kWave);  // wave-uniform, <= kContigRegs
+  float v[kContigRegs][4];
+  float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+  for (int i = 0; i < kContigRegs; ++i) {
+    const int64_t k = lane + (int64_t)kWave * i;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[i][c] = -INFINITY;
+    if (i < rounds) {
+      if (k < r.K) contig_load(p, r, k, v[i]);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) m[c] = fmaxf(m[c], v[i][c]);
+    }
+  }
+  contig_allmax(m, H);
+  float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int i = 0; i < kContigRegs; ++i) {
+    if (i < rounds) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        v[i][c] = v[i][c] == -INFINITY ? 0.0f : expf(v[i][c] - m[c]);
+        z[c] += v[i][c];
+      }
+    }
+  }
+  contig_allsum(z, H);
+  float inv[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) inv[c] = 1.0f / z[c];
+#pragma unroll
+  for (int i = 0; i < kContigRegs; ++i) {
+    const int64_t k = lane + (int64_t)kWave * i;
+    if (i < rounds && k < r.K) {
+      float o[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) o[c] = v[i][c] * inv[c];
+      contig_store(p, r, k, o);
+    }
+  }
+}
+
+// Longer rows and segments of split rows: running (max, sum) per slot over the
+// float4s, four in flight; then either publish per-segment statistics or
+// re-read and normalise.
+__device__ __forceinline__ void softmax_contig_stream(const SoftmaxParams& p, const Item& it) {
+  const int lane = lane_id();
+  const int H = p.H;
+  const ContigRange r = contig_range(it.b, it.e, H);
+  float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+  float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int64_t k0 = lane; k0 < r.K; k0 += 4 * kWave) {
+    float v[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t k = k0 + (int64_t)kWave * i;
+      if (k < r.K) {
+        contig_load(p, r, k, v[i]);
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) v[i][c] = -INFINITY;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (v[i][c] != -INFINITY) lse_push(m[c], z[c], v[i][c]);
+  }
+  contig_alllse(m, z, H);
+  if (it.slot >= 0) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int h = contig_head(r, lane, c, H);
+      // one publishing lane per head: the lowest lane/slot holding it
+      const bool pub = H >= 4 ? lane < H / 4 : (lane == 0 && c < H);
+      if (pub) {
+        p.ws[((int64_t)it.slot * H + h) * 2 + 0] = m[c];
+        p.ws[((int64_t)it.slot * H + h) * 2 + 1] = z[c];
+      }
+    }
+    return;
+  }
+  float inv[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) inv[c] = 1.0f / z[c];
+  for (int64_t k0 = lane; k0 < r.K; k0 += 4 * kWave) {
+    float v[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t k = k0 + (int64_t)kWave * i;
+      if (k < r.K) contig_load(p, r, k, v[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t k = k0 + (int64_t)kWave * i;
+      if (k < r.K) {
+        float o[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) o[c] = expf(v[i][c] - m[c]) * inv[c];
+        contig_store(p, r, k, o);
+      }
+    }
+  }
+}
+
 // Lanes map to (edge offset, head) pairs: hc = heads per pass, epw = 64/hc
 // edges per pass.  Pass 1 keeps a running (max, sum) per lane; lanes of one
 // head then merge in a fixed tree; pass 2 writes exp(s' - m) / z.  Segments
@@ -849,6 +1080,16 @@ __global__ __launch_bounds__(kBlock) void softmax_kernel(SoftmaxParams p) {
   if (it.b >= it.e) return;
   const int lane = lane_id();
   const int H = p.H;
+  // float4 lanes once a row fills the wavefront or has >= 4 heads; short rows
+  // with one or two heads use one value per lane instead
+  if (p.contig && (H >= 4 || (it.e - it.b) * H > (int64_t)kWave * kSoftmaxU)) {
+    const int64_t nvec = contig_range(it.b, it.e, H).K;
+    if (!(SEG && it.slot >= 0) && nvec <= (int64_t)kWave * kContigRegs)
+      softmax_contig_regs(p, it);
+    else
+      softmax_contig_stream(p, it);
+    return;
+  }
   if (!(SEG && it.slot >= 0) && H <= kWave && (H & (H - 1)) == 0 &&
       (it.e - it.b) * H <= (int64_t)kWave * kSoftmaxU) {
     softmax_row_in_registers(p, it);
@@ -967,6 +1208,35 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
   const int64_t fi = p.slot_fix[slot];
   const int lane = lane_id();
   const int H = p.H;
+  if (p.contig) {
+    const ContigRange r = contig_range(s.begin, s.end, H);
+    float m[4], inv[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int h = contig_head(r, lane, c, H);
+      m[c] = p.ws_row[(fi * H + h) * 2 + 0];
+      inv[c] = 1.0f / p.ws_row[(fi * H + h) * 2 + 1];
+    }
+    for (int64_t k0 = lane; k0 < r.K; k0 += 4 * kWave) {
+      float v[4][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t k = k0 + (int64_t)kWave * i;
+        if (k < r.K) contig_load(p, r, k, v[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t k = k0 + (int64_t)kWave * i;
+        if (k < r.K) {
+          float o[4];
+#pragma unroll
+          for (int c = 0; c < 4; ++c) o[c] = expf(v[i][c] - m[c]) * inv[c];
+          contig_store(p, r, k, o);
+        }
+      }
+    }
+    return;
+  }
   for (int h0 = 0; h0 < H; h0 += kWave) {
     const int hc = min(H - h0, kWave);
     const int epw = kWave / hc;
@@ -991,6 +1261,181 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
       for (int k = 0; k < kSoftmaxU; ++k)
         if (ev[k] >= 0) p.out[ev[k] * H + h] = expf(sv[k] - m) * inv;
     }
+  }
+}
+
+// ----------------------------------------------------------------------------
+// fused attention aggregation: SDDMM -> leaky ReLU -> edge softmax -> gSpMM
+// ----------------------------------------------------------------------------
+
+// Floats per plan slot of the fused attention kernel: F partial sums, then H
+// maxima and H exp-sums, padded so every slot starts 16-byte aligned.
+__host__ __device__ __forceinline__ int64_t gat_ws_stride(int64_t F, int64_t H) {
+  return F + ((2 * H + 3) & ~int64_t(3));
+}
+
+struct GatParams {
+  const int32_t* indptr;
+  const int32_t* indices;
+  const float* xs;
+  const float* xd;
+  float* out;
+  const Seg* segs;
+  float* ws;  // per slot: [F] scaled partial sum, [H] running max, [H] scaled exp-sum
+  int64_t n_items;
+  int64_t F;
+  int32_t H;
+  int32_t dh;
+  int32_t SH;  // lanes per head = dh / 4
+  int32_t leaky;
+  float slope;
+};
+
+// Sum over aligned groups of W lanes, returned in every lane of the group.
+template <int W>
+__device__ __forceinline__ float group_allsum(float v, int gid) {
+  v = group_sum<W>(v);
+  if constexpr (W == 32) {
+    const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 31));
+    const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+    v = gid ? b : a;
+  } else if constexpr (W == 64) {
+    v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+  }
+  return v;
+}
+
+// Merges a running-softmax state (m, z, acc) with another one.
+__device__ __forceinline__ void attn_merge(float& m, float& z, float (&acc)[4], float om, float oz,
+                                           const float (&oacc)[4]) {
+  if (om == -INFINITY) return;
+  if (m == -INFINITY) {
+    m = om;
+    z = oz;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] = oacc[c];
+    return;
+  }
+  const float nm = fmaxf(m, om);
+  const float a = expf(m - nm), b = expf(om - nm);
+  z = z * a + oz * b;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) acc[c] = acc[c] * a + oacc[c] * b;
+  m = nm;
+}
+
+// One wavefront per row or segment; G lanes (float4 each) per feature row,
+// SH lanes per head.  Per edge: dot of the gathered source row with the
+// destination row held in registers, DPP reduction over the head's lanes,
+// leaky ReLU, then an online-softmax update of (max, exp-sum, weighted sum of
+// the same gathered source row).  The source row is read once per edge and no
+// per-edge score is written.
+template <int G, bool SEG>
+__global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
+  constexpr int NG = kWave / G;
+  constexpr int U = NG * 4 <= kWave ? 4 : 1;
+  const int64_t item = wave_item();
+  if (item >= p.n_items) return;
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  const int lane = lane_id();
+  const int gid = lane / G;
+  const int li = lane % G;
+  const int64_t F = p.F;
+  const int64_t f = (int64_t)li * 4;
+  const bool act = f < F;
+  const int h = act ? (int)(f / p.dh) : 0;
+  float xd[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (act) load_vec<4>(p.xd + it.row * F + f, xd);
+  float m = -INFINITY, z = 0.0f;
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+
+  for (int64_t base = it.b; base < it.e; base += kWave) {
+    const int cnt = (int)min((int64_t)kWave, it.e - base);
+    int my_src = 0;
+    if (lane < cnt) my_src = __builtin_nontemporal_load(p.indices + base + lane);
+    for (int j0 = 0; j0 < cnt; j0 += NG * U) {
+      float val[U][4];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int jb = j0 + u * NG;
+        ok[u] = jb + gid < cnt;
+        const int src = bcast_lane<NG>(my_src, jb, gid);
+        if (ok[u] && act) {
+          load_vec<4>(p.xs + (int64_t)src * F + f, val[u]);
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) val[u][c] = 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float part = val[u][0] * xd[0] + val[u][1] * xd[1] + val[u][2] * xd[2] + val[u][3] * xd[3];
+        float sc;
+        switch (p.SH) {  // wave-uniform
+          case 1: sc = part; break;
+          case 2: sc = group_allsum<2>(part, gid); break;
+          case 4: sc = group_allsum<4>(part, gid); break;
+          case 8: sc = group_allsum<8>(part, gid); break;
+          case 16: sc = group_allsum<16>(part, gid); break;
+          case 32: sc = group_allsum<32>(part, gid); break;
+          default: sc = group_allsum<64>(part, gid); break;
+        }
+        sc = leaky_relu(sc, p.leaky, p.slope);
+        if (ok[u]) {
+          const float nm = fmaxf(m, sc);
+          const float a = expf(m - nm), b = expf(sc - nm);
+          z = z * a + b;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[c] = acc[c] * a + b * val[u][c];
+          m = nm;
+        }
+      }
+    }
+  }
+  // merge the lane groups
+  for (int s = G; s < kWave; s <<= 1) {
+    const float om = __shfl_xor(m, s), oz = __shfl_xor(z, s);
+    float oacc[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) oacc[c] = __shfl_xor(acc[c], s);
+    attn_merge(m, z, acc, om, oz, oacc);
+  }
+  if (gid != 0 || !act) return;
+  if (SEG && it.slot >= 0) {
+    float* w = p.ws + (int64_t)it.slot * gat_ws_stride(F, p.H);
+    store_vec<4>(w + f, acc);
+    if (li % p.SH == 0) {
+      w[F + h] = m;
+      w[F + p.H + h] = z;
+    }
+    return;
+  }
+  float o[4];
+  const float inv = z > 0.0f ? 1.0f / z : 0.0f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) o[c] = acc[c] * inv;
+  store_vec<4>(p.out + it.row * F + f, o);
+}
+
+// Merges the per-segment states of each split row and writes acc / z.
+__global__ __launch_bounds__(kBlock) void gat_fixup_kernel(GatParams p, const Fix* fix) {
+  const Fix fx = fix[blockIdx.x];
+  const int64_t F = p.F;
+  const int64_t stride = gat_ws_stride(F, p.H);
+  for (int64_t f = threadIdx.x; f < F; f += kBlock) {
+    const int64_t h = f / p.dh;
+    float m = -INFINITY;
+    for (int s = fx.slot_begin; s < fx.slot_end; ++s) m = fmaxf(m, p.ws[s * stride + F + h]);
+    float z = 0.0f, acc = 0.0f;
+    for (int s = fx.slot_begin; s < fx.slot_end; ++s) {
+      const float ms = p.ws[s * stride + F + h];
+      if (ms == -INFINITY) continue;
+      const float a = expf(ms - m);
+      z += p.ws[s * stride + F + p.H + h] * a;
+      acc += p.ws[s * stride + f] * a;
+    }
+    p.out[(int64_t)fx.row * F + f] = z > 0.0f ? acc / z : 0.0f;
   }
 }
 
@@ -1225,6 +1670,8 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
   prm.H = (int32_t)H;
   prm.leaky = leaky ? 1 : 0;
   prm.slope = slope;
+  prm.contig = (g.edge_ids == nullptr && H <= kWave && (H & (H - 1)) == 0 && aligned16(scores) &&
+                aligned16(out)) ? 1 : 0;
   const dim3 grid = grid_for(prm.n_items, 1);
   if (plan) FG_LAUNCH((softmax_kernel<true>), grid, stream, prm);
   else FG_LAUNCH((softmax_kernel<false>), grid, stream, prm);
@@ -1234,6 +1681,54 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   FG_LAUNCH(softmax_split_kernel, grid_for(plan->num_slots, 1), stream, prm, plan->num_slots);
+  return hipGetLastError();
+}
+
+bool gat_fused_supported(int64_t H, int64_t dh) {
+  const int64_t F = H * dh;
+  if (dh % 4 != 0 || F > 4 * kWave) return false;
+  const int64_t sh = dh / 4;
+  return (sh & (sh - 1)) == 0;
+}
+
+hipError_t launch_gat_fused(const GraphView& g, const PlanView* plan, int64_t H, int64_t dh,
+                            const float* xs, const float* xd, bool leaky, float slope, float* out,
+                            hipStream_t stream) {
+  if (g.num_rows == 0) return hipSuccess;
+  const bool seg = plan != nullptr;
+  GatParams prm;
+  prm.indptr = g.indptr;
+  prm.indices = g.indices;
+  prm.xs = xs;
+  prm.xd = xd;
+  prm.out = out;
+  prm.segs = seg ? plan->segs : nullptr;
+  prm.ws = seg ? plan->ws_f : nullptr;
+  prm.n_items = seg ? plan->num_segments : g.num_rows;
+  prm.F = H * dh;
+  prm.H = (int32_t)H;
+  prm.dh = (int32_t)dh;
+  prm.SH = (int32_t)(dh / 4);
+  prm.leaky = leaky ? 1 : 0;
+  prm.slope = slope;
+  const dim3 grid = grid_for(prm.n_items, 1);
+  const int64_t Q = prm.F / 4;
+  const int G = Q <= 4 ? 4 : Q <= 8 ? 8 : Q <= 16 ? 16 : Q <= 32 ? 32 : 64;
+  // lanes of a head must not straddle the group (SH <= G always holds: dh <= F)
+#define FG_GAT(GG)                                                             \
+  if (seg) FG_LAUNCH((gat_fused_kernel<GG, true>), grid, stream, prm);         \
+  else FG_LAUNCH((gat_fused_kernel<GG, false>), grid, stream, prm);
+  switch (G) {
+    case 4: FG_GAT(4) break;
+    case 8: FG_GAT(8) break;
+    case 16: FG_GAT(16) break;
+    case 32: FG_GAT(32) break;
+    default: FG_GAT(64) break;
+  }
+#undef FG_GAT
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || !seg || plan->num_split_rows == 0) return err;
+  FG_LAUNCH(gat_fixup_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, prm, plan->fix);
   return hipGetLastError();
 }
 

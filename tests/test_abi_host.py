@@ -125,6 +125,27 @@ def test_edge_softmax_rejects_invalid_arguments():
     assert L.fg_edge_softmax(ctypes.byref(g), 1, FAKE_X, 1, 0.2, FAKE_X + 4, None, None) == -1
 
 
+def test_gat_aggregate_rejects_invalid_or_unsupported_arguments():
+    L = fg._lib
+    g = _graph_struct()
+    ok = dict(H=2, dh=8, xs=FAKE_X, xd=FAKE_X + 0x1000, out=FAKE_OUT)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return L.fg_gat_aggregate(ctypes.byref(g), a["H"], a["dh"], a["xs"], a["xd"], 1, 0.2,
+                                  a["out"], None, None)
+
+    assert call(H=0) == fg.FG_ERR_INVALID_ARG
+    assert call(xs=None) == fg.FG_ERR_INVALID_ARG
+    assert call(out=None) == fg.FG_ERR_INVALID_ARG
+    assert call(out=FAKE_X + 16) == fg.FG_ERR_INVALID_ARG  # overlaps x_src
+    # valid but outside the fused kernel's shapes
+    assert call(dh=6) == fg.FG_ERR_UNSUPPORTED     # dh not a multiple of 4
+    assert call(dh=12) == fg.FG_ERR_UNSUPPORTED    # 3 lanes per head
+    assert call(H=8, dh=64) == fg.FG_ERR_UNSUPPORTED  # wider than 256
+    assert call(xs=FAKE_X + 4) == fg.FG_ERR_UNSUPPORTED  # not 16-byte aligned
+
+
 def test_plan_create_rejects_invalid_arguments():
     L = fg._lib
     g = _graph_struct()

@@ -152,6 +152,25 @@ def check_softmax(csr, G, scores, rows=None, plan=None, heads=1, leaky=True, nnz
     return res
 
 
+def check_gat(csr, G, x, rows=None, plan=None, heads=1, leaky=True):
+    """Fused attention aggregation vs the oracle's gsddmm -> edge_softmax ->
+    gspmm(src_mul_edge, sum) on the selected rows."""
+    F = int(np.prod(x.shape[1:]))
+    say("gat_aggregate rows=%d nnz=%d F=%d H=%d plan=%s" % (
+        csr.num_rows, csr.nnz, F, heads, None if plan is None else plan.info()["segment_edges"]))
+    res = fg.gat_aggregate(G, dev(x), heads=heads, leaky=leaky, slope=0.2, plan=plan)
+    out = host(res).reshape(csr.num_rows, F)
+    x2 = x.reshape(csr.num_cols, F)
+    s = O.gsddmm(csr, x2, x2, heads=heads, rows=rows)
+    a = O.edge_softmax(csr, s, heads=heads, leaky=leaky, slope=0.2, rows=rows)
+    ro, norm = O.gspmm(csr, x2, msg=O.MSG_SRC_MUL_EDGE, edge_val=a, heads=heads, rows=rows,
+                       with_norm=True)
+    sel = np.arange(csr.num_rows) if rows is None else rows
+    deg = csr.degrees()[sel][:, None]
+    assert_close_sum(out[sel], ro.astype(np.float64), norm, deg)
+    return res
+
+
 def plans_for(G, width, sizes=(0, 1, 5, 64)):
     yield None
     for s in sizes:
@@ -222,6 +241,25 @@ def test_heads(small_rmat, heads, dh):
         a = check_softmax(csr, G, host(s), plan=plan, heads=heads)
         check_spmm(csr, G, x, plan=plan, edge=host(a), heads=heads)
         check_spmm(csr, G, x, plan=plan, edge=host(a), heads=heads, reduce="max")
+
+
+@pytest.mark.parametrize("heads,dh", [(8, 16), (1, 128), (2, 32), (4, 8), (1, 4), (16, 16),
+                                      (1, 256), (4, 64)])
+def test_gat_fused(small_rmat, heads, dh):
+    csr, G = small_rmat
+    x = np.random.default_rng(heads * 7 + dh).standard_normal(
+        (csr.num_cols, heads, dh)).astype(np.float32)
+    for plan in plans_for(G, heads * dh, sizes=(1, 64)):
+        check_gat(csr, G, x, plan=plan, heads=heads)
+        check_gat(csr, G, x, plan=plan, heads=heads, leaky=False)
+
+
+def test_gat_fused_unsupported_shape_raises(small_rmat):
+    csr, G = small_rmat
+    x = dev(np.ones((csr.num_cols, 3, 12), np.float32))
+    with pytest.raises(fg.FgError) as ei:
+        fg.gat_aggregate(G, x)
+    assert ei.value.status == fg.FG_ERR_UNSUPPORTED
 
 
 def test_transposed_graph_with_edge_ids(small_rmat):
@@ -364,6 +402,8 @@ def test_clustered_gat_layer_full():
     # softmax rows sum to one for every row and head
     rs = np.add.reduceat(host(a).astype(np.float64), csr.indptr[:-1], axis=0)
     np.testing.assert_allclose(rs, 1.0, atol=1e-5 * math.sqrt(300))
+    # the fused layer on the same graph
+    check_gat(csr, G, x, rows=rows, plan=plan, heads=8)
 
 
 @pytest.mark.slow
