@@ -93,7 +93,9 @@ def setup(name, d, args, fg, torch, dev):
     n, e = csr.num_rows, csr.nnz
     log("workload %s: N=%d E=%d generated in %.1fs" % (name, n, e, t_gen))
     G = fg.Graph.from_csr(csr, device=dev)
-    popt = dict(segment_edges=args.segment_edges, max_row_segments=args.max_row_segments)
+    popt = dict(segment_edges=args.segment_edges, max_row_segments=args.max_row_segments,
+                source_slab_rows=args.source_slab_rows,
+                partition_min_degree=args.partition_min_degree)
     T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
     cfg = {"workload": name, "num_vertices": n, "num_edges": e}
     plans = []
@@ -243,23 +245,30 @@ def setup(name, d, args, fg, torch, dev):
 
     pinfo = plans[0].info()
     cfg.update(segment_edges=pinfo["segment_edges"], max_row_segments=pinfo["max_row_segments"],
-               ops=[o.name for o in ops])
+               source_slab_rows=pinfo["source_slab_rows"],
+               partition_min_degree=pinfo["partition_min_degree"], ops=[o.name for o in ops])
     return cfg, ops, plans, oracle_sample, e
 
 
 def cpu_baseline(oracle_sample, budget_s):
-    """The oracle, as is, on a random row sample sized for about `budget_s`
-    seconds of host work."""
+    """The oracle, as is, on a random row sample of the workload, repeated
+    until about `budget_s` seconds of host work have been timed."""
     import oracle
 
     oracle.build(force=False)
     threads = oracle.max_threads()
+    oracle_sample(200_000)  # warm-up: thread pool, page faults
     dt, flop, desc = oracle_sample(2_000_000)
-    scale = budget_s / max(dt, 1e-9)
-    if scale > 4:
-        dt, flop, desc = oracle_sample(2_000_000 * scale)
-    return {"value": round(flop / dt / 1e9, 3), "unit": "GFLOP/s", "cores": threads,
-            "kind": "oracle", "sample": "%s, %.1f s" % (desc, dt)}
+    # size one pass for about a third of the budget (at most the whole graph)
+    target = 2_000_000 * max(1.0, budget_s / 3.0 / max(dt, 1e-9))
+    total_t, total_f, reps = 0.0, 0, 0
+    while total_t < budget_s:
+        dt, flop, desc = oracle_sample(target)
+        total_t += dt
+        total_f += flop
+        reps += 1
+    return {"value": round(total_f / total_t / 1e9, 3), "unit": "GFLOP/s", "cores": threads,
+            "kind": "oracle", "sample": "%s; %d passes, %.1f s" % (desc, reps, total_t)}
 
 
 # ----------------------------------------------------------------------------
@@ -365,6 +374,10 @@ def main():
     ap.add_argument("--segment-edges", type=int, default=0, help="plan segment length (0: default)")
     ap.add_argument("--max-row-segments", type=int, default=0,
                     help="cap on segments per row (0: default)")
+    ap.add_argument("--source-slab-rows", type=int, default=0,
+                    help="source ids per slab of the gather schedule (0: off, <0: automatic)")
+    ap.add_argument("--partition-min-degree", type=int, default=0,
+                    help="smallest row cut at slab boundaries (0: default)")
     ap.add_argument("--fused", action="store_true",
                     help="attention workload: one fused kernel instead of three operators")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -464,7 +477,8 @@ def main():
         "ops": per_op,
         "edges_per_s_step": round(e * K / elapsed, 1),
         "plan": {"segments": pinfo["num_segments"], "split_rows": pinfo["num_split_rows"],
-                 "slots": pinfo["num_slots"]},
+                 "slots": pinfo["num_slots"],
+                 "partitioned_rows": pinfo["num_partitioned_rows"]},
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a row sample")

@@ -95,61 +95,80 @@ typedef struct fg_graph {
 } fg_graph;
 
 /* ---------------------------------------------------------------------------
- * Plan: the degree-aware work decomposition of one graph.
- *
- * Rows with more than `segment_edges` edges are cut into k = ceil(deg / S)
- * segments of (nearly) equal length, at most `max_row_segments` per row (longer
- * segments beyond that), each handled by its own wavefront; their partial
- * results are merged by a second, deterministic pass.  Long segments are
- * scheduled first.  This replaces the paper's per-block row assignment
+ * Plan: the degree-aware work decomposition of one graph, built once per
+ * graph like the per-topology kernels the paper amortises over training
+ * epochs (Sec. IV-B).  It replaces the paper's per-block row assignment
  * (Sec. III-C, adaptive parallelization) with one that stays balanced on
- * power-law graphs.  Built once per graph, like the per-topology kernels the
- * paper amortises over training epochs (Sec. IV-B).
+ * power-law graphs, and revives its 1D source partitioning (Sec. III-C, graph
+ * partitioning) for the L2 of each MI355X die.
+ *
+ * A plan holds two schedules over one workspace:
+ *  - plain (edge softmax): rows with more than S = segment_edges edges are
+ *    cut into k = min(ceil(deg / S), max_row_segments) equal segments; long
+ *    items first, rows without edges last;
+ *  - gather (gSpMM, gSDDMM, fused attention): as plain by default.  With
+ *    source partitioning (opt-in, source_slab_rows != 0), rows with at least
+ *    max(partition_min_degree, 32 * slabs) edges and sorted source ids are cut
+ *    where the source id crosses a multiple of source_slab_rows, then into
+ *    pieces of at most S edges; slab p's pieces run on die p mod 8, slab after
+ *    slab, so each die finds the slab's feature rows in its L2 (more L2 hits,
+ *    more pieces to merge).
+ * Items of rows cut in several pieces write partial results that a second
+ * pass merges in a fixed order, so results are deterministic for a plan.
  * ------------------------------------------------------------------------- */
-typedef struct fg_plan fg_plan; /* opaque; owns a device segment table + workspace */
+typedef struct fg_plan fg_plan; /* opaque; owns device schedules + workspace */
 
 typedef struct fg_plan_options {
-  int32_t segment_edges;    /* S: target edges per segment; 0 -> default (4096) */
-  int32_t max_row_segments; /* cap on segments per row; 0 -> default (128)      */
-  int32_t reserved[6];      /* must be zero                                     */
+  int32_t segment_edges;        /* S: target edges per item; 0 -> default (4096)     */
+  int32_t max_row_segments;     /* cap on items per row (plain cut); 0 -> 128        */
+  int32_t source_slab_rows;     /* source ids per slab of the gather schedule;
+                                   0 -> no source partitioning (default);
+                                   negative -> 2 MiB of features at max_width        */
+  int32_t partition_min_degree; /* smallest row cut by slabs; 0 -> default (1024)    */
+  int32_t reserved[4];          /* must be zero                                      */
 } fg_plan_options;
 
 typedef struct fg_plan_info {
   int64_t num_rows, nnz;
-  int64_t num_segments;   /* wavefront work items                               */
-  int64_t num_split_rows; /* rows cut into more than one segment                */
-  int64_t num_slots;      /* segments of split rows (partial-result slots)      */
-  int64_t max_width;      /* largest F the workspace holds                      */
+  int64_t num_segments;         /* gather schedule: work items (with padding)        */
+  int64_t num_split_rows;       /* gather schedule: rows with several items          */
+  int64_t num_slots;            /* gather schedule: partial-result slots             */
+  int64_t num_partitioned_rows; /* rows cut at source-slab boundaries                */
+  int64_t plain_segments, plain_split_rows, plain_slots; /* edge-softmax schedule    */
+  int64_t max_width;            /* largest F the workspace holds                     */
   int64_t workspace_bytes;
-  int32_t segment_edges;
-  int32_t max_row_segments;
+  int32_t segment_edges, max_row_segments, source_slab_rows, partition_min_degree;
 } fg_plan_info;
 
-/* One work item of the schedule (host view; the device table holds the same). */
+/* One work item of a schedule (host view; the device tables hold the same). */
 typedef struct fg_segment {
-  int32_t row;   /* destination row                                             */
-  int32_t begin; /* first stored edge (CSR position)                            */
-  int32_t end;   /* one past the last stored edge                               */
+  int32_t row;   /* destination row; -1: empty padding item                    */
+  int32_t begin; /* first stored edge (CSR position)                           */
+  int32_t end;   /* one past the last stored edge                              */
   int32_t slot;  /* -1: whole row, results go to the output directly;
-                    >= 0: partial-result slot of a split row                    */
+                    >= 0: partial-result slot of a row cut in several pieces   */
 } fg_segment;
 
-/* Builds the schedule on the host from a HOST copy of indptr (opt may be NULL).
- * Writes at most `capacity` segments to `segs` (may be NULL to only count) and
- * the counts to the optional out-pointers.  Pure host function: no HIP call.
- * Order: segments of split rows first (longest segments first; segs[s].slot
- * == s), then whole rows by decreasing degree, then rows without edges. */
-fg_status fg_schedule_host(const int32_t* indptr_host, int64_t num_rows,
-                           const fg_plan_options* opt, fg_segment* segs, int64_t capacity,
-                           int64_t* num_segments, int64_t* num_split_rows, int64_t* num_slots);
+/* Builds a schedule on the host (which = 0: gather, 1: plain) from HOST
+ * copies of indptr and (optional; NULL: no source partitioning) indices.
+ * Writes at most `capacity` items to `segs` (may be NULL to only count) and
+ * the counts to the optional out-pointers.  Pure host function: no HIP call. */
+fg_status fg_schedule_host(const int32_t* indptr_host, const int32_t* indices_host,
+                           int64_t num_rows, int64_t num_cols, int64_t max_width,
+                           const fg_plan_options* opt, int32_t which, fg_segment* segs,
+                           int64_t capacity, int64_t* num_segments, int64_t* num_split_rows,
+                           int64_t* num_slots);
 
 /* Creates a plan for graph `g` and features up to `max_width` = H*dh floats.
- * indptr_host: optional HOST copy of g->indptr (saves a device-to-host copy).
- * opt: may be NULL.  Allocates device memory; synchronises `stream` once.
- * The plan is bound to g->indptr, num_rows and nnz: calls with another graph
- * are rejected with FG_ERR_INVALID_ARG.  A plan holds a mutable workspace:
- * calls that share a plan must be ordered on one stream. */
-fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host, int64_t max_width,
+ * indptr_host / indices_host: optional HOST copies of g->indptr / g->indices
+ * (without them the plan copies what it needs from the device).  opt may be
+ * NULL.  Validates indptr and indices (FG_ERR_INVALID_ARG), allocates device
+ * memory, synchronises `stream`.  The plan is bound to g->indptr, num_rows and
+ * nnz: calls with another graph are rejected with FG_ERR_INVALID_ARG.  Its
+ * workspace is mutable: calls that share a plan must be ordered on one
+ * stream. */
+fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
+                         const int32_t* indices_host, int64_t max_width,
                          const fg_plan_options* opt, fg_plan** out, void* stream);
 fg_status fg_plan_destroy(fg_plan* plan);
 fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info);

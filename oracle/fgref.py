@@ -16,7 +16,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "fgref.c")
-_LIB = os.path.join(_HERE, "_build", "libfgref.so")
+# FGREF_LIB points the shim at another build of the oracle (the mutation test
+# plants mistakes in copies of fgref.c and checks that the pins catch them)
+_LIB = os.environ.get("FGREF_LIB") or os.path.join(_HERE, "_build", "libfgref.so")
 
 MSG_COPY_SRC, MSG_SRC_MUL_EDGE = 0, 1
 RED_SUM, RED_MAX = 0, 1
@@ -28,18 +30,23 @@ def lib_path() -> str:
     return _LIB
 
 
+def compile_oracle(src: str, out: str) -> str:
+    """gcc build of an oracle source file into a shared library."""
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+           "-fno-fast-math", "-Wall", "-Wextra", "-Wno-unused-parameter",
+           "-o", tmp, src, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
+    return out
+
+
 def build(force: bool = True) -> str:
     """Compile the oracle library; returns its path."""
     if not force and os.path.exists(_LIB):
         return _LIB
-    os.makedirs(os.path.dirname(_LIB), exist_ok=True)
-    tmp = _LIB + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
-           "-fno-fast-math", "-Wall", "-Wextra", "-Wno-unused-parameter",
-           "-o", tmp, _SRC, "-lm"]
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, _LIB)
-    return _LIB
+    return compile_oracle(_SRC, _LIB)
 
 
 def _load():

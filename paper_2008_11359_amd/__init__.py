@@ -56,7 +56,8 @@ class _Graph(ctypes.Structure):
 
 class _PlanOptions(ctypes.Structure):
     _fields_ = [("segment_edges", ctypes.c_int32), ("max_row_segments", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 6)]
+                ("source_slab_rows", ctypes.c_int32), ("partition_min_degree", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 4)]
 
 
 class _PlanInfo(ctypes.Structure):
@@ -66,10 +67,16 @@ class _PlanInfo(ctypes.Structure):
         ("num_segments", ctypes.c_int64),
         ("num_split_rows", ctypes.c_int64),
         ("num_slots", ctypes.c_int64),
+        ("num_partitioned_rows", ctypes.c_int64),
+        ("plain_segments", ctypes.c_int64),
+        ("plain_split_rows", ctypes.c_int64),
+        ("plain_slots", ctypes.c_int64),
         ("max_width", ctypes.c_int64),
         ("workspace_bytes", ctypes.c_int64),
         ("segment_edges", ctypes.c_int32),
         ("max_row_segments", ctypes.c_int32),
+        ("source_slab_rows", ctypes.c_int32),
+        ("partition_min_degree", ctypes.c_int32),
     ]
 
 
@@ -90,11 +97,11 @@ def _load():
     lib.fg_status_string.argtypes = [ctypes.c_int]
     lib.fg_abi_version.restype = i32
     lib.fg_schedule_host.restype = ctypes.c_int
-    lib.fg_schedule_host.argtypes = [vp, i64, ctypes.POINTER(_PlanOptions), vp, i64,
-                                     ctypes.POINTER(i64), ctypes.POINTER(i64),
+    lib.fg_schedule_host.argtypes = [vp, vp, i64, i64, i64, ctypes.POINTER(_PlanOptions), i32,
+                                     vp, i64, ctypes.POINTER(i64), ctypes.POINTER(i64),
                                      ctypes.POINTER(i64)]
     lib.fg_plan_create.restype = ctypes.c_int
-    lib.fg_plan_create.argtypes = [gp, vp, i64, ctypes.POINTER(_PlanOptions),
+    lib.fg_plan_create.argtypes = [gp, vp, vp, i64, ctypes.POINTER(_PlanOptions),
                                    ctypes.POINTER(vp), vp]
     lib.fg_plan_destroy.restype = ctypes.c_int
     lib.fg_plan_destroy.argtypes = [vp]
@@ -160,7 +167,8 @@ class Graph:
 
     def __init__(self, num_rows: int, num_cols: int, indptr: torch.Tensor, indices: torch.Tensor,
                  edge_ids: Optional[torch.Tensor] = None, nnz_total: int = 0,
-                 indptr_host: Optional[np.ndarray] = None):
+                 indptr_host: Optional[np.ndarray] = None,
+                 indices_host: Optional[np.ndarray] = None):
         self.indptr = _dev_tensor(indptr, torch.int32, "indptr")
         self.indices = _dev_tensor(indices, torch.int32, "indices")
         self.edge_ids = None if edge_ids is None else _dev_tensor(edge_ids, torch.int32, "edge_ids")
@@ -174,6 +182,8 @@ class Graph:
             raise ValueError("edge_ids must have nnz entries")
         self.indptr_host = None if indptr_host is None else np.ascontiguousarray(
             indptr_host, dtype=np.int32)
+        self.indices_host = None if indices_host is None else np.ascontiguousarray(
+            indices_host, dtype=np.int32)
         self._c = _Graph(self.num_rows, self.num_cols, self.nnz, self.nnz_total,
                          self.indptr.data_ptr(), self.indices.data_ptr() if self.nnz else None,
                          _ptr(self.edge_ids))
@@ -194,7 +204,8 @@ class Graph:
         t_ix = torch.from_numpy(indices).to(dev)
         t_e = None if eids is None else torch.from_numpy(
             np.ascontiguousarray(eids, dtype=np.int32)).to(dev)
-        return cls(csr.num_rows, csr.num_cols, t_ip, t_ix, t_e, nt, indptr_host=indptr)
+        return cls(csr.num_rows, csr.num_cols, t_ip, t_ix, t_e, nt, indptr_host=indptr,
+                   indices_host=indices)
 
 
 def _check_host_csr(num_rows, num_cols, indptr, indices, eids, nnz_total):
@@ -216,18 +227,23 @@ def _check_host_csr(num_rows, num_cols, indptr, indices, eids, nnz_total):
 
 
 class Plan:
-    """Degree-aware schedule of one graph: rows longer than ``segment_edges``
-    are cut into equal segments (at most ``max_row_segments`` per row), with a
-    partial-result workspace for features up to ``max_width`` floats.  Zero
-    selects the library defaults.  Owns device memory until ``close()``."""
+    """Degree-aware schedules of one graph (see fg_plan_create): rows longer
+    than ``segment_edges`` are cut into equal pieces (at most
+    ``max_row_segments``); with ``source_slab_rows`` != 0 (negative: automatic
+    size) long rows of the gather schedule are also cut at source-slab
+    boundaries for L2 reuse on each die; partial-result workspace for features up to
+    ``max_width`` floats.  Zero selects the library defaults.  Owns device
+    memory until ``close()``."""
 
     def __init__(self, g: Graph, max_width: int, segment_edges: int = 0,
-                 max_row_segments: int = 0):
-        opt = _options(segment_edges, max_row_segments)
+                 max_row_segments: int = 0, source_slab_rows: int = 0,
+                 partition_min_degree: int = 0):
+        opt = _options(segment_edges, max_row_segments, source_slab_rows, partition_min_degree)
         h = ctypes.c_void_p()
-        ip = g.indptr_host
+        ip, ix = g.indptr_host, g.indices_host
         st = _lib.fg_plan_create(ctypes.byref(g._c), None if ip is None else ip.ctypes.data,
-                                 int(max_width), ctypes.byref(opt), ctypes.byref(h), _stream())
+                                 None if ix is None else ix.ctypes.data, int(max_width),
+                                 ctypes.byref(opt), ctypes.byref(h), _stream())
         _check(st, "fg_plan_create")
         self._h = h
         self.graph = g
@@ -256,26 +272,32 @@ class Plan:
             pass
 
 
-def _options(segment_edges: int = 0, max_row_segments: int = 0) -> _PlanOptions:
+def _options(segment_edges: int = 0, max_row_segments: int = 0, source_slab_rows: int = 0,
+             partition_min_degree: int = 0) -> _PlanOptions:
     opt = _PlanOptions()
     opt.segment_edges = int(segment_edges)
     opt.max_row_segments = int(max_row_segments)
+    opt.source_slab_rows = int(source_slab_rows)
+    opt.partition_min_degree = int(partition_min_degree)
     return opt
 
 
-def schedule_host(indptr: np.ndarray, segment_edges: int = 0, max_row_segments: int = 0):
-    """The plan's schedule computed on the host (no GPU needed).  Returns
-    (segments as an [n, 4] int32 array of row, begin, end, slot;
-    num_split_rows, num_slots)."""
+def schedule_host(indptr: np.ndarray, indices: Optional[np.ndarray] = None, num_cols: int = 0,
+                  max_width: int = 128, which: str = "gather", **options):
+    """A plan's schedule computed on the host (no GPU needed); ``indices``
+    (with ``num_cols``) enables source partitioning.  Returns (items as an
+    [n, 4] int32 array of row, begin, end, slot; num_split_rows, num_slots)."""
     ip = np.ascontiguousarray(indptr, dtype=np.int32)
-    opt = _options(segment_edges, max_row_segments)
+    ix = None if indices is None else np.ascontiguousarray(indices, dtype=np.int32)
+    opt = _options(**options)
+    w = {"gather": 0, "plain": 1}[which]
+    args = (ip.ctypes.data, None if ix is None else ix.ctypes.data, ip.size - 1, int(num_cols),
+            int(max_width), ctypes.byref(opt), w)
     n_seg, n_split, n_slot = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
-    _check(_lib.fg_schedule_host(ip.ctypes.data, ip.size - 1, ctypes.byref(opt), None, 0,
-                                 ctypes.byref(n_seg), ctypes.byref(n_split), ctypes.byref(n_slot)),
-           "fg_schedule_host")
+    _check(_lib.fg_schedule_host(*args, None, 0, ctypes.byref(n_seg), ctypes.byref(n_split),
+                                 ctypes.byref(n_slot)), "fg_schedule_host")
     segs = np.zeros((n_seg.value, 4), np.int32)
-    _check(_lib.fg_schedule_host(ip.ctypes.data, ip.size - 1, ctypes.byref(opt),
-                                 segs.ctypes.data, n_seg.value, None, None, None),
+    _check(_lib.fg_schedule_host(*args, segs.ctypes.data, n_seg.value, None, None, None),
            "fg_schedule_host")
     return segs, n_split.value, n_slot.value
 

@@ -11,13 +11,18 @@
 #include "featgraph_hip.h"
 #include "fg_internal.h"
 
+// A plan holds two schedules over one workspace: the "gather" schedule used
+// by the operators that gather source feature rows (gSpMM, gSDDMM, the fused
+// attention kernel) and the plain length-ordered schedule used by edge
+// softmax, which gathers nothing.
 struct fg_plan {
   int64_t num_rows = 0, nnz = 0, max_width = 0;
   const int32_t* indptr = nullptr;  // device pointer the plan was built for
-  int32_t segment_edges = 0, max_row_segments = 0;
+  int32_t segment_edges = 0, max_row_segments = 0, slab_rows = 0, partition_min_degree = 0;
+  int64_t num_partitioned_rows = 0;
   int device = 0;
-  fg::PlanView view;
-  void* mem[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  fg::PlanView gather, plain;
+  std::vector<void*> mem;
   int64_t workspace_bytes = 0;
 };
 
@@ -27,6 +32,7 @@ constexpr int32_t kDefaultSegmentEdges = 4096;
 constexpr int32_t kMaxSegmentEdges = 1 << 24;
 constexpr int32_t kDefaultMaxRowSegments = 128;
 constexpr int32_t kMaxRowSegmentsLimit = 1 << 20;
+constexpr int32_t kDefaultPartitionMinDegree = 1024;
 
 fg_status check_graph(const fg_graph* g) {
   if (!g) return FG_ERR_INVALID_ARG;
@@ -85,81 +91,213 @@ bool indptr_valid(const int32_t* ip, int64_t num_rows, int64_t nnz) {
   return true;
 }
 
-// Segment length and count of one row: k = ceil(deg / S) pieces, at most
-// `cap`; a row is split when k >= 2.
-struct Cut {
-  int64_t k;
+constexpr int kXcds = 8;            // MI355X: 8 accelerator dies, workgroups dealt round-robin
+constexpr int kWavesPerGroup = 4;   // work items per workgroup (kernels launch 4 wavefronts)
+constexpr int64_t kSlabBytes = 2 << 20;  // source slab held in one die's L2 (4 MB) with room to spare
+constexpr int64_t kMinTileEdges = 32;    // partition a row only if tiles average this many edges
+
+struct Options {
+  int32_t S, cap, slab, min_deg;
 };
 
-Cut cut_row(int64_t deg, int32_t S, int32_t cap) {
-  int64_t k = deg > S ? (deg + S - 1) / S : 1;
-  if (k > cap) k = cap;
-  return Cut{k};
+struct Schedule {
+  std::vector<fg::Seg> segs;
+  std::vector<fg::Fix> fix;
+  std::vector<int32_t> slot_fix;  // slot -> index into fix
+  std::vector<int32_t> slot_seg;  // slot -> index into segs
+  int64_t partitioned_rows = 0;
+};
+
+// Pieces of a row cut into k (nearly) equal parts.
+void cut_even(int32_t r, int64_t b, int64_t e, int64_t k, int32_t part,
+              std::vector<std::pair<fg::Seg, int32_t>>& out) {
+  const int64_t len = e - b;
+  for (int64_t i = 0; i < k; ++i)
+    out.push_back({fg::Seg{r, (int32_t)(b + len * i / k), (int32_t)(b + len * (i + 1) / k), -1},
+                   part});
 }
 
-// The schedule.  Order: segments of split rows first, rows with the longest
-// segments first (ties by row id), slots numbered in that order so slot ==
-// position; then whole rows by decreasing degree (ties by row id); rows
-// without edges last.  Long work items start first, which keeps the tail of a
-// launch short (longest-processing-time-first list scheduling).
-void build_schedule(const int32_t* ip, int64_t num_rows, int32_t S, int32_t cap,
-                    std::vector<fg::Seg>& segs, std::vector<fg::Fix>& fix,
-                    std::vector<int32_t>& slot_fix) {
-  segs.clear();
-  fix.clear();
-  slot_fix.clear();
-  std::vector<int32_t> split, whole, empty;
+// Numbers the slots of rows with two or more pieces (consecutive per row, in
+// row order), fills the split-row table, and returns the pieces.
+void number_slots(std::vector<std::pair<fg::Seg, int32_t>>& pieces, Schedule& sc) {
+  // pieces arrive grouped by row, in edge order within a row
+  size_t i = 0;
+  int32_t slot = 0;
+  while (i < pieces.size()) {
+    size_t j = i;
+    while (j < pieces.size() && pieces[j].first.row == pieces[i].first.row) ++j;
+    if (j - i >= 2) {
+      fg::Fix fx;
+      fx.row = pieces[i].first.row;
+      fx.slot_begin = slot;
+      for (size_t t = i; t < j; ++t) {
+        pieces[t].first.slot = slot++;
+        sc.slot_fix.push_back((int32_t)sc.fix.size());
+      }
+      fx.slot_end = slot;
+      fx.pad = 0;
+      sc.fix.push_back(fx);
+    }
+    i = j;
+  }
+  sc.slot_seg.assign(sc.slot_fix.size(), -1);
+}
+
+// Longest first (ties by row, then position).
+bool longer(const fg::Seg& a, const fg::Seg& b) {
+  const int64_t la = (int64_t)a.end - a.begin, lb = (int64_t)b.end - b.begin;
+  if (la != lb) return la > lb;
+  if (a.row != b.row) return a.row < b.row;
+  return a.begin < b.begin;
+}
+
+// Plain schedule: rows with more than S edges are cut into
+// k = min(ceil(deg / S), cap) equal pieces; all items ordered longest first,
+// rows without edges last (longest-processing-time-first list scheduling).
+void build_plain(const int32_t* ip, int64_t num_rows, const Options& o, Schedule& sc) {
+  std::vector<std::pair<fg::Seg, int32_t>> pieces;
   for (int64_t r = 0; r < num_rows; ++r) {
     const int64_t deg = (int64_t)ip[r + 1] - ip[r];
-    if (deg == 0) empty.push_back((int32_t)r);
-    else if (cut_row(deg, S, cap).k >= 2) split.push_back((int32_t)r);
-    else whole.push_back((int32_t)r);
+    int64_t k = deg > o.S ? (deg + o.S - 1) / o.S : 1;
+    if (k > o.cap) k = o.cap;
+    cut_even((int32_t)r, ip[r], ip[r + 1], k, -1, pieces);
   }
-  auto deg_of = [ip](int32_t r) { return (int64_t)ip[r + 1] - ip[r]; };
-  std::stable_sort(split.begin(), split.end(), [&](int32_t a, int32_t b) {
-    const int64_t da = deg_of(a), db = deg_of(b);
-    const int64_t ka = cut_row(da, S, cap).k, kb = cut_row(db, S, cap).k;
-    return da * kb > db * ka;  // da/ka > db/kb: longer segments first
-  });
-  std::stable_sort(whole.begin(), whole.end(),
-                   [&](int32_t a, int32_t b) { return deg_of(a) > deg_of(b); });
-  for (int32_t r : split) {
-    const int64_t deg = deg_of(r);
-    const int64_t k = cut_row(deg, S, cap).k;
-    fg::Fix fx;
-    fx.row = r;
-    fx.slot_begin = (int32_t)segs.size();
-    for (int64_t i = 0; i < k; ++i) {
-      fg::Seg s;
-      s.row = r;
-      s.begin = (int32_t)(ip[r] + deg * i / k);
-      s.end = (int32_t)(ip[r] + deg * (i + 1) / k);
-      s.slot = (int32_t)segs.size();
-      slot_fix.push_back((int32_t)fix.size());
-      segs.push_back(s);
-    }
-    fx.slot_end = (int32_t)segs.size();
-    fx.pad = 0;
-    fix.push_back(fx);
-  }
-  segs.reserve(segs.size() + whole.size() + empty.size());
-  for (int32_t r : whole) segs.push_back(fg::Seg{r, ip[r], ip[r + 1], -1});
-  for (int32_t r : empty) segs.push_back(fg::Seg{r, ip[r], ip[r], -1});
+  number_slots(pieces, sc);
+  sc.segs.reserve(pieces.size());
+  for (auto& pc : pieces) sc.segs.push_back(pc.first);
+  std::stable_sort(sc.segs.begin(), sc.segs.end(), longer);
+  for (size_t i = 0; i < sc.segs.size(); ++i)
+    if (sc.segs[i].slot >= 0) sc.slot_seg[sc.segs[i].slot] = (int32_t)i;
 }
 
-fg_status read_options(const fg_plan_options* opt, int32_t* S, int32_t* cap) {
-  *S = kDefaultSegmentEdges;
-  *cap = kDefaultMaxRowSegments;
+// Gather schedule with source partitioning (the paper's 1D graph partitioning
+// of source vertices, Sec. III-C, sized for one die's L2 instead of a CPU's
+// LLC).  Source ids are cut into slabs of o.slab vertices.  A row with at
+// least max(min_deg, kMinTileEdges * slabs) edges whose sources are sorted is
+// cut at slab boundaries (then into pieces of at most S edges); its pieces go
+// to the stream of die (slab mod 8), ordered by slab, so that each die works
+// through one slab of feature rows at a time and finds them in its L2.  The
+// remaining rows are cut as in the plain schedule and dealt to the streams,
+// longest first, to even out the edges per die.  The streams are interleaved
+// four items (one workgroup) at a time, following the round-robin order in
+// which workgroups reach the dies; exhausted streams are padded with empty
+// items (row = -1) that the kernels skip.
+bool build_partitioned(const int32_t* ip, const int32_t* ix, int64_t num_rows, int64_t num_cols,
+                       const Options& o, Schedule& sc) {
+  const int64_t slabs = (num_cols + o.slab - 1) / o.slab;
+  if (o.slab <= 0 || slabs < 2) return false;
+  const int64_t min_deg = std::max<int64_t>(o.min_deg, kMinTileEdges * slabs);
+  std::vector<std::pair<fg::Seg, int32_t>> pieces;
+  for (int64_t r = 0; r < num_rows; ++r) {
+    const int64_t b = ip[r], e = ip[r + 1], deg = e - b;
+    bool part = deg >= min_deg;
+    for (int64_t q = b + 1; part && q < e; ++q)
+      if (ix[q] < ix[q - 1]) part = false;  // unsorted row: no contiguous slab ranges
+    if (!part) {
+      int64_t k = deg > o.S ? (deg + o.S - 1) / o.S : 1;
+      if (k > o.cap) k = o.cap;
+      cut_even((int32_t)r, b, e, k, -1, pieces);
+      continue;
+    }
+    ++sc.partitioned_rows;
+    int64_t q = b;
+    while (q < e) {
+      const int32_t slab = (int32_t)(ix[q] / o.slab);
+      const int64_t lim = (int64_t)(slab + 1) * o.slab;
+      int64_t t = q;
+      while (t < e && ix[t] < lim) ++t;
+      cut_even((int32_t)r, q, t, (t - q + o.S - 1) / o.S, slab, pieces);
+      q = t;
+    }
+  }
+  if (sc.partitioned_rows == 0) return false;
+  number_slots(pieces, sc);
+
+  // streams: partitioned pieces by (slab, row, position); then the rest
+  std::vector<std::vector<fg::Seg>> stream(kXcds);
+  std::vector<int64_t> load(kXcds, 0);
+  std::vector<std::vector<fg::Seg>> by_slab((size_t)slabs);
+  std::vector<fg::Seg> rest;
+  for (auto& pc : pieces) {
+    if (pc.second >= 0) by_slab[(size_t)pc.second].push_back(pc.first);
+    else rest.push_back(pc.first);
+  }
+  for (int64_t sl = 0; sl < slabs; ++sl) {
+    const int x = (int)(sl % kXcds);
+    for (auto& sg : by_slab[(size_t)sl]) {
+      stream[x].push_back(sg);
+      load[x] += (int64_t)sg.end - sg.begin;
+    }
+  }
+  std::stable_sort(rest.begin(), rest.end(), longer);
+  for (auto& sg : rest) {
+    int x = 0;
+    for (int y = 1; y < kXcds; ++y) {
+      const int64_t len = (int64_t)sg.end - sg.begin;
+      if (len > 0 ? load[y] < load[x] : stream[y].size() < stream[x].size()) x = y;
+    }
+    stream[x].push_back(sg);
+    load[x] += (int64_t)sg.end - sg.begin;
+  }
+  size_t longest = 0;
+  for (auto& st : stream) longest = std::max(longest, st.size());
+  const size_t rounds = (longest + kWavesPerGroup - 1) / kWavesPerGroup;
+  sc.segs.reserve(rounds * kXcds * kWavesPerGroup);
+  const fg::Seg none{-1, 0, 0, -1};
+  for (size_t rd = 0; rd < rounds; ++rd)
+    for (int x = 0; x < kXcds; ++x)
+      for (int w = 0; w < kWavesPerGroup; ++w) {
+        const size_t i = rd * kWavesPerGroup + w;
+        sc.segs.push_back(i < stream[x].size() ? stream[x][i] : none);
+      }
+  for (size_t i = 0; i < sc.segs.size(); ++i)
+    if (sc.segs[i].slot >= 0) sc.slot_seg[sc.segs[i].slot] = (int32_t)i;
+  return true;
+}
+
+fg_status read_options(const fg_plan_options* opt, int64_t max_width, Options* o) {
+  o->S = kDefaultSegmentEdges;
+  o->cap = kDefaultMaxRowSegments;
+  o->slab = 0;  // source partitioning is opt-in (see fg_plan_options)
+  o->min_deg = kDefaultPartitionMinDegree;
   if (!opt) return FG_OK;
   for (int32_t r : opt->reserved)
     if (r != 0) return FG_ERR_INVALID_ARG;
   if (opt->segment_edges < 0 || opt->segment_edges > kMaxSegmentEdges) return FG_ERR_INVALID_ARG;
   if (opt->max_row_segments < 0 || opt->max_row_segments > kMaxRowSegmentsLimit)
     return FG_ERR_INVALID_ARG;
-  if (opt->segment_edges) *S = opt->segment_edges;
-  if (opt->max_row_segments) *cap = opt->max_row_segments;
-  if (*cap < 2) return FG_ERR_INVALID_ARG;
+  if (opt->partition_min_degree < 0) return FG_ERR_INVALID_ARG;
+  if (opt->segment_edges) o->S = opt->segment_edges;
+  if (opt->max_row_segments) o->cap = opt->max_row_segments;
+  if (opt->source_slab_rows > 0) {
+    o->slab = opt->source_slab_rows;
+  } else if (opt->source_slab_rows < 0) {  // automatic: 2 MiB of features per slab
+    o->slab = (int32_t)std::max<int64_t>(64, kSlabBytes / (4 * std::max<int64_t>(max_width, 1)));
+  }
+  if (opt->partition_min_degree) o->min_deg = opt->partition_min_degree;
+  if (o->cap < 2) return FG_ERR_INVALID_ARG;
   return FG_OK;
+}
+
+// Both schedules of a graph.  indices may be null: no source partitioning.
+fg_status make_schedules(const int32_t* ip, const int32_t* ix, int64_t num_rows, int64_t num_cols,
+                         const Options& o, Schedule& gather, Schedule& plain) {
+  try {
+    build_plain(ip, num_rows, o, plain);
+    if (!ix || !build_partitioned(ip, ix, num_rows, num_cols, o, gather)) {
+      gather = plain;
+      gather.partitioned_rows = 0;
+    }
+  } catch (const std::bad_alloc&) {
+    return FG_ERR_NO_MEMORY;
+  }
+  return FG_OK;
+}
+
+bool indices_valid(const int32_t* ix, int64_t nnz, int64_t num_cols) {
+  for (int64_t q = 0; q < nnz; ++q)
+    if (ix[q] < 0 || ix[q] >= num_cols) return false;
+  return true;
 }
 
 }  // namespace
@@ -179,33 +317,36 @@ const char* fg_status_string(fg_status s) {
 
 int32_t fg_abi_version(void) { return FG_ABI_VERSION; }
 
-fg_status fg_schedule_host(const int32_t* indptr_host, int64_t num_rows,
-                           const fg_plan_options* opt, fg_segment* segs, int64_t capacity,
-                           int64_t* num_segments, int64_t* num_split_rows, int64_t* num_slots) {
-  if (!indptr_host || num_rows < 0 || num_rows >= INT32_MAX || capacity < 0)
+fg_status fg_schedule_host(const int32_t* indptr_host, const int32_t* indices_host,
+                           int64_t num_rows, int64_t num_cols, int64_t max_width,
+                           const fg_plan_options* opt, int32_t which, fg_segment* segs,
+                           int64_t capacity, int64_t* num_segments, int64_t* num_split_rows,
+                           int64_t* num_slots) {
+  if (!indptr_host || num_rows < 0 || num_rows >= INT32_MAX || num_cols < 0 ||
+      num_cols > INT32_MAX || capacity < 0 || (which != 0 && which != 1))
     return FG_ERR_INVALID_ARG;
-  int32_t S, cap;
-  fg_status st = read_options(opt, &S, &cap);
+  if (max_width < 1 || max_width > FG_MAX_WIDTH) return FG_ERR_INVALID_ARG;
+  Options o;
+  fg_status st = read_options(opt, max_width, &o);
   if (st != FG_OK) return st;
-  if (!indptr_valid(indptr_host, num_rows, indptr_host[num_rows])) return FG_ERR_INVALID_ARG;
-  std::vector<fg::Seg> s;
-  std::vector<fg::Fix> fx;
-  std::vector<int32_t> sf;
-  try {
-    build_schedule(indptr_host, num_rows, S, cap, s, fx, sf);
-  } catch (const std::bad_alloc&) {
-    return FG_ERR_NO_MEMORY;
-  }
-  if (num_segments) *num_segments = (int64_t)s.size();
-  if (num_split_rows) *num_split_rows = (int64_t)fx.size();
-  if (num_slots) *num_slots = (int64_t)sf.size();
+  const int64_t nnz = indptr_host[num_rows];
+  if (!indptr_valid(indptr_host, num_rows, nnz)) return FG_ERR_INVALID_ARG;
+  if (indices_host && !indices_valid(indices_host, nnz, num_cols)) return FG_ERR_INVALID_ARG;
+  Schedule gather, plain;
+  if ((st = make_schedules(indptr_host, indices_host, num_rows, num_cols, o, gather, plain)) !=
+      FG_OK)
+    return st;
+  const Schedule& sc = which == 0 ? gather : plain;
+  if (num_segments) *num_segments = (int64_t)sc.segs.size();
+  if (num_split_rows) *num_split_rows = (int64_t)sc.fix.size();
+  if (num_slots) *num_slots = (int64_t)sc.slot_fix.size();
   if (segs) {
-    const int64_t n = std::min<int64_t>(capacity, (int64_t)s.size());
+    const int64_t n = std::min<int64_t>(capacity, (int64_t)sc.segs.size());
     for (int64_t i = 0; i < n; ++i) {
-      segs[i].row = s[i].row;
-      segs[i].begin = s[i].begin;
-      segs[i].end = s[i].end;
-      segs[i].slot = s[i].slot;
+      segs[i].row = sc.segs[i].row;
+      segs[i].begin = sc.segs[i].begin;
+      segs[i].end = sc.segs[i].end;
+      segs[i].slot = sc.segs[i].slot;
     }
   }
   return FG_OK;
@@ -226,39 +367,81 @@ fg_status fg_plan_destroy(fg_plan* plan) {
   return st;
 }
 
-fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host, int64_t max_width,
+namespace {
+
+// Device copy of one schedule; the plan owns the allocations.
+fg_status upload(fg_plan* p, const Schedule& sc, fg::PlanView& v, hipStream_t hs) {
+  auto put = [&](const void* src, size_t bytes, void** dst) -> fg_status {
+    void* d = nullptr;
+    if (hipMalloc(&d, std::max<size_t>(bytes, 16)) != hipSuccess) return FG_ERR_NO_MEMORY;
+    p->mem.push_back(d);
+    if (bytes && hipMemcpyAsync(d, src, bytes, hipMemcpyHostToDevice, hs) != hipSuccess)
+      return FG_ERR_HIP;
+    *dst = d;
+    return FG_OK;
+  };
+  void *a, *b, *c, *d;
+  fg_status st;
+  if ((st = put(sc.segs.data(), sizeof(fg::Seg) * sc.segs.size(), &a)) != FG_OK) return st;
+  if ((st = put(sc.fix.data(), sizeof(fg::Fix) * sc.fix.size(), &b)) != FG_OK) return st;
+  if ((st = put(sc.slot_fix.data(), sizeof(int32_t) * sc.slot_fix.size(), &c)) != FG_OK) return st;
+  if ((st = put(sc.slot_seg.data(), sizeof(int32_t) * sc.slot_seg.size(), &d)) != FG_OK) return st;
+  v.segs = static_cast<const fg::Seg*>(a);
+  v.fix = static_cast<const fg::Fix*>(b);
+  v.slot_fix = static_cast<const int32_t*>(c);
+  v.slot_seg = static_cast<const int32_t*>(d);
+  v.num_segments = (int64_t)sc.segs.size();
+  v.num_split_rows = (int64_t)sc.fix.size();
+  v.num_slots = (int64_t)sc.slot_fix.size();
+  return FG_OK;
+}
+
+}  // namespace
+
+fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
+                         const int32_t* indices_host, int64_t max_width,
                          const fg_plan_options* opt, fg_plan** out, void* stream) {
   if (!out) return FG_ERR_INVALID_ARG;
   *out = nullptr;
   fg_status st = check_graph(g);
   if (st != FG_OK) return st;
   if (max_width < 1 || max_width > FG_MAX_WIDTH) return FG_ERR_INVALID_ARG;
-  int32_t S, cap;
-  if ((st = read_options(opt, &S, &cap)) != FG_OK) return st;
+  Options o;
+  if ((st = read_options(opt, max_width, &o)) != FG_OK) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
 
-  std::vector<int32_t> ip_copy;
+  std::vector<int32_t> ip_copy, ix_copy;
   const int32_t* ip = indptr_host;
+  const int32_t* ix = indices_host;
   try {
     if (!ip) {
       ip_copy.resize((size_t)g->num_rows + 1);
       if (hipMemcpyAsync(ip_copy.data(), g->indptr, sizeof(int32_t) * ip_copy.size(),
-                         hipMemcpyDeviceToHost, hs) != hipSuccess)
+                         hipMemcpyDeviceToHost, hs) != hipSuccess ||
+          hipStreamSynchronize(hs) != hipSuccess)
         return FG_ERR_HIP;
-      if (hipStreamSynchronize(hs) != hipSuccess) return FG_ERR_HIP;
       ip = ip_copy.data();
+    }
+    if (!indptr_valid(ip, g->num_rows, g->nnz)) return FG_ERR_INVALID_ARG;
+    if (!ix && o.slab > 0 && g->nnz > 0) {
+      ix_copy.resize((size_t)g->nnz);
+      if (hipMemcpyAsync(ix_copy.data(), g->indices, sizeof(int32_t) * ix_copy.size(),
+                         hipMemcpyDeviceToHost, hs) != hipSuccess ||
+          hipStreamSynchronize(hs) != hipSuccess)
+        return FG_ERR_HIP;
+      ix = ix_copy.data();
     }
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
   }
-  if (!indptr_valid(ip, g->num_rows, g->nnz)) return FG_ERR_INVALID_ARG;
+  if (ix && !indices_valid(ix, g->nnz, g->num_cols)) return FG_ERR_INVALID_ARG;
+  if (o.slab <= 0) ix = nullptr;
 
-  std::vector<fg::Seg> segs;
-  std::vector<fg::Fix> fix;
-  std::vector<int32_t> slot_fix;
+  Schedule gather, plain;
+  if ((st = make_schedules(ip, ix, g->num_rows, g->num_cols, o, gather, plain)) != FG_OK)
+    return st;
   fg_plan* p = nullptr;
   try {
-    build_schedule(ip, g->num_rows, S, cap, segs, fix, slot_fix);
     p = new fg_plan();
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
@@ -267,57 +450,49 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host, int64_t 
   p->nnz = g->nnz;
   p->max_width = max_width;
   p->indptr = g->indptr;
-  p->segment_edges = S;
-  p->max_row_segments = cap;
+  p->segment_edges = o.S;
+  p->max_row_segments = o.cap;
+  p->slab_rows = ix ? o.slab : 0;
+  p->partition_min_degree = o.min_deg;
+  p->num_partitioned_rows = gather.partitioned_rows;
   if (hipGetDevice(&p->device) != hipSuccess) {
     delete p;
     return FG_ERR_HIP;
   }
-  const int64_t nslots = (int64_t)slot_fix.size();
-  // workspace per slot: F partial values (sum / max) or 2*H softmax pairs
+  if ((st = upload(p, gather, p->gather, hs)) != FG_OK ||
+      (st = upload(p, plain, p->plain, hs)) != FG_OK) {
+    (void)hipStreamSynchronize(hs);
+    fg_plan_destroy(p);
+    return st;
+  }
+  // shared workspace: per slot F partial values (or 2H softmax pairs, or the
+  // fused kernel's F + 2H) and F argmax ids; per split row 2H merged pairs
+  const int64_t nslots = std::max(p->gather.num_slots, p->plain.num_slots);
+  const int64_t nsplit = std::max(p->gather.num_split_rows, p->plain.num_split_rows);
   const int64_t ws_width = 2 * max_width;
-  const int64_t nsplit = (int64_t)fix.size();
-  const size_t bytes[6] = {
-      sizeof(fg::Seg) * std::max<size_t>(segs.size(), 1),
-      sizeof(fg::Fix) * std::max<size_t>(fix.size(), 1),
-      sizeof(int32_t) * std::max<size_t>(slot_fix.size(), 1),
-      sizeof(float) * (size_t)std::max<int64_t>(nslots * ws_width, 1),
-      sizeof(int32_t) * (size_t)std::max<int64_t>(nslots * max_width, 1),
-      sizeof(float) * (size_t)std::max<int64_t>(nsplit * ws_width, 1),
-  };
-  for (int i = 0; i < 6; ++i) {
-    if (hipMalloc(&p->mem[i], bytes[i]) != hipSuccess) {
-      p->mem[i] = nullptr;
+  const size_t wb[3] = {sizeof(float) * (size_t)std::max<int64_t>(nslots * ws_width, 4),
+                        sizeof(int32_t) * (size_t)std::max<int64_t>(nslots * max_width, 4),
+                        sizeof(float) * (size_t)std::max<int64_t>(nsplit * ws_width, 4)};
+  void* w[3] = {nullptr, nullptr, nullptr};
+  for (int i = 0; i < 3; ++i) {
+    if (hipMalloc(&w[i], wb[i]) != hipSuccess) {
+      (void)hipStreamSynchronize(hs);
       fg_plan_destroy(p);
       return FG_ERR_NO_MEMORY;
     }
+    p->mem.push_back(w[i]);
   }
-  hipError_t e = hipSuccess;
-  if (!segs.empty())
-    e = hipMemcpyAsync(p->mem[0], segs.data(), sizeof(fg::Seg) * segs.size(),
-                       hipMemcpyHostToDevice, hs);
-  if (e == hipSuccess && !fix.empty())
-    e = hipMemcpyAsync(p->mem[1], fix.data(), sizeof(fg::Fix) * fix.size(),
-                       hipMemcpyHostToDevice, hs);
-  if (e == hipSuccess && !slot_fix.empty())
-    e = hipMemcpyAsync(p->mem[2], slot_fix.data(), sizeof(int32_t) * slot_fix.size(),
-                       hipMemcpyHostToDevice, hs);
-  if (e == hipSuccess) e = hipStreamSynchronize(hs);  // host vectors die on return
-  if (e != hipSuccess) {
+  for (fg::PlanView* v : {&p->gather, &p->plain}) {
+    v->ws_f = static_cast<float*>(w[0]);
+    v->ws_i = static_cast<int32_t*>(w[1]);
+    v->ws_row = static_cast<float*>(w[2]);
+    v->ws_width = ws_width;
+  }
+  p->workspace_bytes = (int64_t)(wb[0] + wb[1] + wb[2]);
+  if (hipStreamSynchronize(hs) != hipSuccess) {  // host schedules die on return
     fg_plan_destroy(p);
     return FG_ERR_HIP;
   }
-  p->view.segs = static_cast<const fg::Seg*>(p->mem[0]);
-  p->view.fix = static_cast<const fg::Fix*>(p->mem[1]);
-  p->view.slot_fix = static_cast<const int32_t*>(p->mem[2]);
-  p->view.ws_f = static_cast<float*>(p->mem[3]);
-  p->view.ws_i = static_cast<int32_t*>(p->mem[4]);
-  p->view.ws_row = static_cast<float*>(p->mem[5]);
-  p->view.num_segments = (int64_t)segs.size();
-  p->view.num_split_rows = (int64_t)fix.size();
-  p->view.num_slots = nslots;
-  p->view.ws_width = ws_width;
-  p->workspace_bytes = (int64_t)(bytes[3] + bytes[4] + bytes[5]);
   *out = p;
   return FG_OK;
 }
@@ -327,13 +502,19 @@ fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info) {
   std::memset(info, 0, sizeof(*info));
   info->num_rows = plan->num_rows;
   info->nnz = plan->nnz;
-  info->num_segments = plan->view.num_segments;
-  info->num_split_rows = plan->view.num_split_rows;
-  info->num_slots = plan->view.num_slots;
+  info->num_segments = plan->gather.num_segments;
+  info->num_split_rows = plan->gather.num_split_rows;
+  info->num_slots = plan->gather.num_slots;
+  info->num_partitioned_rows = plan->num_partitioned_rows;
+  info->plain_segments = plan->plain.num_segments;
+  info->plain_split_rows = plan->plain.num_split_rows;
+  info->plain_slots = plan->plain.num_slots;
   info->max_width = plan->max_width;
   info->workspace_bytes = plan->workspace_bytes;
   info->segment_edges = plan->segment_edges;
   info->max_row_segments = plan->max_row_segments;
+  info->source_slab_rows = plan->slab_rows;
+  info->partition_min_degree = plan->partition_min_degree;
   return FG_OK;
 }
 
@@ -360,7 +541,7 @@ fg_status fg_gspmm(const fg_graph* g, fg_msg_op msg, fg_reduce_op red, int32_t n
       overlaps(out, out_b, arg_eid, out_b))
     return FG_ERR_INVALID_ARG;
   const fg::GraphView gv = view_of(g);
-  return from_hip(fg::launch_gspmm(gv, plan ? &plan->view : nullptr, (int)msg, (int)red,
+  return from_hip(fg::launch_gspmm(gv, plan ? &plan->gather : nullptr, (int)msg, (int)red,
                                    num_heads, head_dim, x_src, edge_val, out, arg_eid,
                                    static_cast<hipStream_t>(stream)));
 }
@@ -380,7 +561,7 @@ fg_status fg_gsddmm(const fg_graph* g, fg_edge_op op, int32_t num_heads, int64_t
       overlaps(out, out_b, x_dst, g->num_rows * F * 4))
     return FG_ERR_INVALID_ARG;
   const fg::GraphView gv = view_of(g);
-  return from_hip(fg::launch_gsddmm(gv, plan ? &plan->view : nullptr, num_heads, head_dim, x_src,
+  return from_hip(fg::launch_gsddmm(gv, plan ? &plan->gather : nullptr, num_heads, head_dim, x_src,
                                     x_dst, out, static_cast<hipStream_t>(stream)));
 }
 
@@ -396,7 +577,7 @@ fg_status fg_edge_softmax(const fg_graph* g, int32_t num_heads, const float* sco
   const int64_t b = nnz_total_of(g) * num_heads * 4;
   if (out != scores && overlaps(out, b, scores, b)) return FG_ERR_INVALID_ARG;
   const fg::GraphView gv = view_of(g);
-  return from_hip(fg::launch_edge_softmax(gv, plan ? &plan->view : nullptr, num_heads, scores,
+  return from_hip(fg::launch_edge_softmax(gv, plan ? &plan->plain : nullptr, num_heads, scores,
                                           apply_leaky_relu != 0, negative_slope, out,
                                           static_cast<hipStream_t>(stream)));
 }
@@ -419,7 +600,7 @@ fg_status fg_gat_aggregate(const fg_graph* g, int32_t num_heads, int64_t head_di
                        reinterpret_cast<uintptr_t>(out);
   if (!fg::gat_fused_supported(num_heads, head_dim) || (al & 15u) != 0) return FG_ERR_UNSUPPORTED;
   const fg::GraphView gv = view_of(g);
-  return from_hip(fg::launch_gat_fused(gv, plan ? &plan->view : nullptr, num_heads, head_dim,
+  return from_hip(fg::launch_gat_fused(gv, plan ? &plan->gather : nullptr, num_heads, head_dim,
                                        x_src, x_dst, apply_leaky_relu != 0, negative_slope, out,
                                        static_cast<hipStream_t>(stream)));
 }

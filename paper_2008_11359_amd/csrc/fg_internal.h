@@ -19,9 +19,10 @@ struct Fix {
 
 // Device view of a plan (all pointers are device memory).
 struct PlanView {
-  const Seg* segs = nullptr;      // [num_segments]; segs[s].slot == s for s < num_slots
+  const Seg* segs = nullptr;      // [num_segments]; row == -1 marks an empty (padding) item
   const Fix* fix = nullptr;       // [num_split_rows]
   const int32_t* slot_fix = nullptr;  // [num_slots] -> index into fix
+  const int32_t* slot_seg = nullptr;  // [num_slots] -> index into segs
   float* ws_f = nullptr;          // [num_slots * ws_width] partial values
   int32_t* ws_i = nullptr;        // [num_slots * ws_width] partial argmax edge ids
   float* ws_row = nullptr;        // [num_split_rows * ws_width] merged per-row values

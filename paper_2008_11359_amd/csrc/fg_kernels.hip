@@ -202,6 +202,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;  // padding item of a partitioned schedule
   const int lane = lane_id();
   const int gid = lane / G;
   const int li = lane % G;
@@ -334,6 +335,7 @@ __global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;  // padding item of a partitioned schedule
   const int lane = lane_id();
   const int G = 1 << p.logG;
   const int ngroups = kWave >> p.logG;
@@ -536,6 +538,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;  // padding item of a partitioned schedule
   if (it.b >= it.e) return;
   const int lane = lane_id();
   const int gid = lane / G;
@@ -607,6 +610,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_headed_kernel(SddmmParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;  // padding item of a partitioned schedule
   if (it.b >= it.e) return;
   const int lane = lane_id();
   const int G = 1 << p.logG;
@@ -664,6 +668,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_scalar_kernel(SddmmParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;  // padding item of a partitioned schedule
   if (it.b >= it.e) return;
   const int lane = lane_id();
   const int G = 1 << p.logG;
@@ -735,6 +740,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_generic_kernel(SddmmParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;  // padding item of a partitioned schedule
   const int lane = lane_id();
   const int64_t H = p.H, dh = p.dh, F = p.F;
   const int64_t total = (it.e - it.b) * H;
@@ -763,6 +769,7 @@ struct SoftmaxParams {
   const Seg* segs;
   const Fix* fix;
   const int32_t* slot_fix;
+  const int32_t* slot_seg;
   float* ws;      // [slot][H][2]  per-segment (max, scaled sum)
   float* ws_row;  // [split row][H][2] merged per row
   int64_t n_items;
@@ -1077,6 +1084,7 @@ __global__ __launch_bounds__(kBlock) void softmax_kernel(SoftmaxParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;  // padding item of a partitioned schedule
   if (it.b >= it.e) return;
   const int lane = lane_id();
   const int H = p.H;
@@ -1204,7 +1212,7 @@ __global__ __launch_bounds__(kBlock) void softmax_rowstats_kernel(SoftmaxParams 
 __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, int64_t n_slots) {
   const int64_t slot = wave_item();
   if (slot >= n_slots) return;
-  const Seg s = p.segs[slot];
+  const Seg s = p.segs[p.slot_seg[slot]];
   const int64_t fi = p.slot_fix[slot];
   const int lane = lane_id();
   const int H = p.H;
@@ -1337,6 +1345,7 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;  // padding item of a partitioned schedule
   const int lane = lane_id();
   const int gid = lane / G;
   const int li = lane % G;
@@ -1664,6 +1673,7 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
   prm.segs = plan ? plan->segs : nullptr;
   prm.fix = plan ? plan->fix : nullptr;
   prm.slot_fix = plan ? plan->slot_fix : nullptr;
+  prm.slot_seg = plan ? plan->slot_seg : nullptr;
   prm.ws = plan ? plan->ws_f : nullptr;
   prm.ws_row = plan ? plan->ws_row : nullptr;
   prm.n_items = plan ? plan->num_segments : g.num_rows;

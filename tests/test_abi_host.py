@@ -151,26 +151,34 @@ def test_plan_create_rejects_invalid_arguments():
     g = _graph_struct()
     h = ctypes.c_void_p()
     opt = fg._PlanOptions()
-    assert L.fg_plan_create(ctypes.byref(g), None, 0, None, ctypes.byref(h), None) == -1
-    assert L.fg_plan_create(ctypes.byref(g), None, 8, None, None, None) == -1
+    assert L.fg_plan_create(ctypes.byref(g), None, None, 0, None, ctypes.byref(h), None) == -1
+    assert L.fg_plan_create(ctypes.byref(g), None, None, 8, None, None, None) == -1
     opt.reserved[2] = 1
-    assert L.fg_plan_create(ctypes.byref(g), None, 8, ctypes.byref(opt), ctypes.byref(h),
+    assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1
     opt.reserved[2] = 0
     opt.max_row_segments = 1  # a row must be allowed at least two pieces
-    assert L.fg_plan_create(ctypes.byref(g), None, 8, ctypes.byref(opt), ctypes.byref(h),
+    assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1
     opt.max_row_segments = 0
     opt.segment_edges = -5
-    assert L.fg_plan_create(ctypes.byref(g), None, 8, ctypes.byref(opt), ctypes.byref(h),
+    assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
+                            None) == -1
+    opt.segment_edges = 0
+    opt.partition_min_degree = -1
+    assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1
     # an inconsistent host indptr is rejected before any device allocation
     ip = np.array([0, 3, 2, 4, 7], np.int32)
-    assert L.fg_plan_create(ctypes.byref(g), ip.ctypes.data, 8, None, ctypes.byref(h),
+    assert L.fg_plan_create(ctypes.byref(g), ip.ctypes.data, None, 8, None, ctypes.byref(h),
                             None) == -1
     ip = np.array([0, 3, 4, 4, 6], np.int32)  # last entry != nnz
-    assert L.fg_plan_create(ctypes.byref(g), ip.ctypes.data, 8, None, ctypes.byref(h),
+    assert L.fg_plan_create(ctypes.byref(g), ip.ctypes.data, None, 8, None, ctypes.byref(h),
                             None) == -1
+    ip = np.array([0, 3, 4, 4, 7], np.int32)
+    ix = np.array([0, 1, 2, 3, 0, 4, 1], np.int32)  # source 4 >= num_cols
+    assert L.fg_plan_create(ctypes.byref(g), ip.ctypes.data, ix.ctypes.data, 8, None,
+                            ctypes.byref(h), None) == -1
     assert L.fg_plan_destroy(None) == -1
     assert L.fg_plan_get_info(None, None) == -1
 
@@ -184,39 +192,64 @@ def test_binding_refuses_cpu_tensors():
 # ---------------------------------------------------------------- schedule
 
 
-def _check_schedule(indptr, S, cap=128):
-    segs, n_split, n_slot = fg.schedule_host(indptr, S, cap)
+def _check_schedule(indptr, S, cap=128, indices=None, num_cols=0, slab=0, min_deg=0,
+                    which="plain", max_width=128):
+    segs, n_split, n_slot = fg.schedule_host(
+        indptr, indices, num_cols, max_width, which, segment_edges=S, max_row_segments=cap,
+        source_slab_rows=slab, partition_min_degree=min_deg)
     num_rows = indptr.size - 1
     deg = np.diff(indptr.astype(np.int64))
+    pad = segs[:, 0] < 0
+    assert np.all(segs[pad, 1:] == [0, 0, -1])  # padding items are empty
+    real = segs[~pad]
     # every edge covered exactly once, every row present
     cover = np.zeros(int(indptr[-1]), np.int32)
-    rows_seen = np.zeros(num_rows, np.int32)
-    for r, b, e, s in segs:
+    pieces = np.zeros(num_rows, np.int64)
+    for r, b, e, sl in real:
         assert indptr[r] <= b <= e <= indptr[r + 1]
         cover[b:e] += 1
-        rows_seen[r] += 1
+        pieces[r] += 1
     assert np.all(cover == 1)
-    assert np.all(rows_seen >= 1)
-    # k = min(ceil(deg / S), cap) pieces; split when k >= 2
-    k = np.minimum(np.maximum(-(-deg // S), 1), cap)
-    split = k >= 2
+    assert np.all(pieces >= 1)
+    # slots: rows with several pieces, numbered consecutively per row in edge order
+    split = pieces >= 2
     assert n_split == int(split.sum())
-    assert n_slot == int(k[split].sum())
-    assert np.all(rows_seen == k)
-    assert np.all(segs[:n_slot, 3] == np.arange(n_slot))
-    assert np.all(segs[n_slot:, 3] == -1)
-    lens = segs[:, 2] - segs[:, 1]
-    assert np.all(lens <= np.maximum(S, -(-deg[segs[:, 0]] // cap)))
-    for r in np.nonzero(split)[0]:
-        sl = np.nonzero(segs[:n_slot, 0] == r)[0]
-        assert np.all(np.diff(sl) == 1)  # a split row's slots are contiguous
-        ls = lens[sl]
-        assert ls.max() - ls.min() <= 1
-    # longest segments first among split rows, then whole rows by degree, empty last
-    if n_slot:
-        assert np.all(np.diff(deg[segs[:n_slot, 0]] / k[segs[:n_slot, 0]]) <= 1e-9)
-    tail = lens[n_slot:]
-    assert np.all(np.diff(tail) <= 0)
+    assert n_slot == int(pieces[split].sum())
+    slotted = real[real[:, 3] >= 0]
+    assert np.array_equal(np.sort(slotted[:, 3]), np.arange(n_slot))
+    assert np.all(split[slotted[:, 0]]) and np.all(~split[real[real[:, 3] < 0, 0]])
+    by_slot = slotted[np.argsort(slotted[:, 3])]
+    for r in np.nonzero(split)[0][:200]:
+        rs = by_slot[by_slot[:, 0] == r]
+        assert np.all(np.diff(rs[:, 3]) == 1)
+        assert rs[0, 1] == indptr[r] and rs[-1, 2] == indptr[r + 1]
+        assert np.all(rs[1:, 1] == rs[:-1, 2])  # slot order = edge order
+    lens = real[:, 2] - real[:, 1]
+    if which == "plain" or indices is None:
+        k = np.minimum(np.maximum(-(-deg // S), 1), cap)
+        assert np.array_equal(pieces, k)
+        assert np.all(lens <= np.maximum(S, -(-deg[real[:, 0]] // cap)))
+        assert not pad.any()
+        assert np.all(np.diff(lens) <= 0)  # longest first
+        return segs
+    # gather schedule with source slabs
+    nslab = -(-num_cols // slab)
+    thresh = max(min_deg, 32 * nslab)
+    part = deg >= thresh
+    for r in np.nonzero(part)[0]:
+        row = indices[indptr[r]:indptr[r + 1]]
+        part[r] = bool(np.all(np.diff(row) >= 0))
+    is_part = part[real[:, 0]]
+    lo_slab = indices[real[is_part, 1]] // slab
+    hi_slab = indices[real[is_part, 2] - 1] // slab
+    assert np.array_equal(lo_slab, hi_slab)  # a piece never crosses a slab boundary
+    assert np.all(lens[is_part] <= S)
+    # stream of die x = workgroups (4 items) w with w % 8 == x; slabs in order
+    die = (np.nonzero(~pad)[0] // 4) % 8
+    for x in range(8):
+        sl = lo_slab[die[is_part] == x]
+        assert np.all(sl % 8 == x)
+        assert np.all(np.diff(sl) >= 0)
     return segs
 
 
@@ -226,10 +259,36 @@ def test_schedule_covers_every_edge(S, cap):
     _check_schedule(w.csr.indptr, S, cap)
 
 
+@pytest.mark.parametrize("S,slab,min_deg", [(4096, 64, 0), (64, 16, 8), (7, 100, 1)])
+def test_partitioned_schedule(S, slab, min_deg):
+    w = synth.make_config("rmat_233k_115m", scale_down=128)
+    c = w.csr
+    segs = _check_schedule(c.indptr, S, indices=c.indices, num_cols=c.num_cols, slab=slab,
+                           min_deg=min_deg, which="gather")
+    assert (segs[:, 0] >= 0).sum() > c.num_rows  # some rows were cut
+    # the plain schedule of the same graph ignores the slabs
+    _check_schedule(c.indptr, S, indices=c.indices, num_cols=c.num_cols, slab=slab,
+                    min_deg=min_deg, which="plain")
+
+
+def test_partitioning_skips_unsorted_rows():
+    ip = np.array([0, 300, 300], np.int32)
+    ix = np.random.default_rng(0).integers(0, 1000, 300).astype(np.int32)  # unsorted hub
+    segs, n_split, n_slot = fg.schedule_host(ip, ix, 1000, 128, "gather", segment_edges=64,
+                                             source_slab_rows=250, partition_min_degree=1)
+    assert n_slot == 5 and not (segs[:, 0] < 0).any()  # plain cut: ceil(300 / 64)
+    ix.sort()
+    segs, n_split, n_slot = fg.schedule_host(ip, ix, 1000, 128, "gather", segment_edges=64,
+                                             source_slab_rows=250, partition_min_degree=1)
+    assert n_slot > 5  # now cut at slab boundaries too
+
+
 def test_schedule_edge_cases():
     _check_schedule(np.zeros(1, np.int32), 8)            # no rows
     _check_schedule(np.zeros(6, np.int32), 8)            # only empty rows
     _check_schedule(np.array([0, 100], np.int32), 8)     # one hub row
     _check_schedule(np.array([0, 8, 16, 17], np.int32), 8)
     with pytest.raises(fg.FgError):
-        fg.schedule_host(np.array([0, 5, 3], np.int32), 8)
+        fg.schedule_host(np.array([0, 5, 3], np.int32), segment_edges=8)
+    with pytest.raises(fg.FgError):  # a source id out of range
+        fg.schedule_host(np.array([0, 2], np.int32), np.array([0, 9], np.int32), 5)

@@ -175,6 +175,10 @@ def plans_for(G, width, sizes=(0, 1, 5, 64)):
     yield None
     for s in sizes:
         yield fg.Plan(G, max_width=width, segment_edges=s)
+    # rows cut at source-slab boundaries (8 slabs), pieces of at most 64 edges
+    slab = max(1, -(-G.num_cols // 8))
+    yield fg.Plan(G, max_width=width, segment_edges=64, source_slab_rows=slab,
+                  partition_min_degree=1)
 
 
 # ----------------------------------------------------------------------------
@@ -319,7 +323,8 @@ def test_determinism_and_plan_independence(small_rmat):
     csr, G = small_rmat
     x = np.random.default_rng(9).standard_normal((csr.num_cols, 128)).astype(np.float32)
     tx = dev(x)
-    plan = fg.Plan(G, 128, 32)
+    plan = fg.Plan(G, 128, 32, source_slab_rows=250, partition_min_degree=1)
+    assert plan.info()["num_partitioned_rows"] > 0
     a1 = host(fg.gspmm(G, tx, plan=plan))
     a2 = host(fg.gspmm(G, tx, plan=plan))
     np.testing.assert_array_equal(a1.view(np.uint32), a2.view(np.uint32))
@@ -378,11 +383,17 @@ def test_rmat_233k_full(rmat_full):
     info = plan.info()
     say("plan", info)
     assert info["num_split_rows"] > 0
+    # source-partitioned gather schedule of the same graph (automatic slab size)
+    pplan = fg.Plan(G, 128, source_slab_rows=-1)
+    assert pplan.info()["num_partitioned_rows"] > 0
     rows = sample_rows(csr, 2000, 3)
     check_spmm(csr, G, x, rows=rows, plan=plan, edge=wgt)
     check_spmm(csr, G, x, rows=rows, plan=plan, reduce="max")
     s = check_sddmm(csr, G, x, x, rows=rows, plan=plan)
     check_softmax(csr, G, host(s), rows=rows, plan=plan)
+    check_spmm(csr, G, x, rows=rows, plan=pplan, edge=wgt)
+    check_spmm(csr, G, x, rows=rows, plan=pplan, reduce="max")
+    check_sddmm(csr, G, x, x, rows=rows, plan=pplan)
     o = host(fg.gspmm(G, dev(np.ones((csr.num_cols, 128), np.float32)), plan=plan))
     np.testing.assert_array_equal(o[:, 0], csr.degrees().astype(np.float32))
     np.testing.assert_array_equal(o[:, 127], csr.degrees().astype(np.float32))
