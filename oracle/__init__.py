@@ -10,6 +10,8 @@ from .fgref import (  # noqa: F401
     gspmm,
     gsddmm,
     edge_softmax,
+    gspmm_max_backward,
+    edge_softmax_backward,
     max_threads,
     MSG_COPY_SRC,
     MSG_SRC_MUL_EDGE,

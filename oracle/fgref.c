@@ -26,6 +26,7 @@
  */
 #include <math.h>
 #include <stddef.h>
+#include <stdlib.h>
 #include <stdint.h>
 #include <omp.h>
 
@@ -210,6 +211,172 @@ FGREF_EXPORT int fgref_edge_softmax(int64_t num_rows, const int32_t* indptr,
         double s = scores[e * H + h];
         if (apply_leaky_relu && !(s > 0.0)) s = (double)slope * s;
         out[e * H + h] = (float)(exp(s - m) / z);
+      }
+    }
+  }
+  return bad ? -2 : 0;
+}
+
+/*
+ * Gradient of gSpMM with the max aggregator (Eq. 1 with (+) = max).  The
+ * output out[v,h,k] equals the message of one edge, the one the forward picks
+ * (largest message, smallest edge id among equal ones), so for a loss L with
+ * upstream gradient G = dL/dout only that edge receives G[v,h,k]:
+ *   copy_src     : dX[u,h,k] += G[v,h,k]
+ *   src_mul_edge : dX[u,h,k] += W[e,h] * G[v,h,k],  dW[e,h] += X[u,h,k] * G[v,h,k]
+ * where e is the selected edge and u its source.  Empty rows contribute
+ * nothing.  The argmax is recomputed here from x with fgref_gspmm (not taken
+ * from the caller), then the contributions of the selected rows are added in row order
+ * in fp64 and rounded to fp32 once.  grad_src [num_cols, F] and grad_edge
+ * [nnz_total, H] (src_mul_edge only) are fully overwritten; either may be
+ * NULL.  src_norm / edge_norm (optional, same shapes) receive
+ * sqrt(sum of squared contributions).  Edge ids must be distinct.
+ */
+FGREF_EXPORT int fgref_gspmm_max_backward(int64_t num_rows, int64_t num_cols,
+                                          const int32_t* indptr, const int32_t* indices,
+                                          const int32_t* edge_ids, int64_t nnz_total, int msg,
+                                          int64_t H, int64_t dh, const float* x,
+                                          const float* edge_val, const float* grad_out,
+                                          const int64_t* rows, int64_t num_sel, float* grad_src,
+                                          float* grad_edge, double* src_norm, double* edge_norm,
+                                          int num_threads) {
+  if (H < 1 || dh < 1 || num_rows < 0 || num_cols < 0 || nnz_total < 0 || !indptr) return -1;
+  if (msg != MSG_COPY_SRC && msg != MSG_SRC_MUL_EDGE) return -1;
+  if (msg == MSG_COPY_SRC && grad_edge) return -1;
+  if (msg == MSG_SRC_MUL_EDGE && !edge_val) return -1;
+  if (!x || !grad_out || (!rows && num_sel != num_rows)) return -1;
+  if (check_rows(rows, num_sel, num_rows)) return -1;
+  const int64_t F = H * dh;
+  const int64_t nnz = indptr[num_rows];
+  int rc = -3;
+  float* fwd = (float*)malloc(sizeof(float) * (size_t)(num_sel * F + 1));
+  int32_t* arg = (int32_t*)malloc(sizeof(int32_t) * (size_t)(num_sel * F + 1));
+  int64_t* pos = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nnz_total + 1));
+  double* gs = (double*)calloc((size_t)(num_cols * F + 1), sizeof(double));
+  double* gs2 = (double*)calloc((size_t)(num_cols * F + 1), sizeof(double));
+  double* ge = (double*)calloc((size_t)(nnz_total * H + 1), sizeof(double));
+  double* ge2 = (double*)calloc((size_t)(nnz_total * H + 1), sizeof(double));
+  if (!fwd || !arg || !pos || !gs || !gs2 || !ge || !ge2) goto done;
+
+  /* forward: the edge each output element takes its value from */
+  rc = fgref_gspmm(num_rows, num_cols, indptr, indices, edge_ids, nnz_total, msg, RED_MAX, H, dh,
+                   x, edge_val, rows, num_sel, fwd, arg, NULL, num_threads);
+  if (rc != 0) goto done;
+
+  /* storage position of every edge id */
+  for (int64_t e = 0; e < nnz_total; ++e) pos[e] = -1;
+  for (int64_t p = 0; p < nnz; ++p) {
+    const int64_t e = edge_ids ? edge_ids[p] : p;
+    if (e < 0 || e >= nnz_total || pos[e] != -1) { rc = -2; goto done; }
+    pos[e] = p;
+  }
+
+  for (int64_t i = 0; i < num_sel; ++i) {
+    const int64_t v = pick_row(rows, i);
+    for (int64_t h = 0; h < H; ++h) {
+      for (int64_t k = 0; k < dh; ++k) {
+        const int64_t f = h * dh + k;
+        const int64_t e = arg[i * F + f];
+        if (e < 0) continue;
+        const int64_t u = indices[pos[e]];
+        const double g = grad_out[v * F + f];
+        const double ts = msg == MSG_SRC_MUL_EDGE ? (double)edge_val[e * H + h] * g : g;
+        gs[u * F + f] += ts;
+        gs2[u * F + f] += ts * ts;
+        if (msg == MSG_SRC_MUL_EDGE) {
+          const double te = (double)x[u * F + f] * g;
+          ge[e * H + h] += te;
+          ge2[e * H + h] += te * te;
+        }
+      }
+    }
+  }
+  if (grad_src)
+    for (int64_t j = 0; j < num_cols * F; ++j) grad_src[j] = (float)gs[j];
+  if (src_norm)
+    for (int64_t j = 0; j < num_cols * F; ++j) src_norm[j] = sqrt(gs2[j]);
+  if (grad_edge)
+    for (int64_t j = 0; j < nnz_total * H; ++j) grad_edge[j] = (float)ge[j];
+  if (edge_norm && msg == MSG_SRC_MUL_EDGE)
+    for (int64_t j = 0; j < nnz_total * H; ++j) edge_norm[j] = sqrt(ge2[j]);
+  rc = 0;
+done:
+  free(fwd);
+  free(arg);
+  free(pos);
+  free(gs);
+  free(gs2);
+  free(ge);
+  free(ge2);
+  return rc;
+}
+
+/*
+ * Gradient of the edge softmax (with optional leaky ReLU) w.r.t. its input
+ * scores.  With a_e the softmax of row v (head h) and G = dL/da:
+ *   dL/ds'_e = a_e * (G_e - c),   c = sum_{p in row} a_p * G_p
+ * (the Jacobian of softmax is diag(a) - a a^T), and through the leaky ReLU
+ *   dL/ds_e = dL/ds'_e * (s_e > 0 ? 1 : slope)     (slope also at s_e = 0).
+ * a is recomputed here from the scores in fp64 exactly as fgref_edge_softmax
+ * defines it; the result is rounded to fp32 once.  scale (optional, indexed
+ * like grad_scores) receives a_e * (|G_e| + sum_p a_p |G_p|) times the leaky
+ * factor: the size of the terms the result is formed from.
+ */
+FGREF_EXPORT int fgref_edge_softmax_backward(int64_t num_rows, const int32_t* indptr,
+                                             const int32_t* edge_ids, int64_t nnz_total,
+                                             int64_t H, const float* scores,
+                                             const float* grad_out, int apply_leaky_relu,
+                                             float slope, const int64_t* rows, int64_t num_sel,
+                                             float* grad_scores, double* scale,
+                                             int num_threads) {
+  if (H < 1 || num_rows < 0 || !indptr || !scores || !grad_out || !grad_scores) return -1;
+  if (!rows && num_sel != num_rows) return -1;
+  if (check_rows(rows, num_sel, num_rows)) return -1;
+  set_threads(num_threads);
+  int bad = 0;
+
+#pragma omp parallel for schedule(dynamic, 64) reduction(| : bad)
+  for (int64_t i = 0; i < num_sel; ++i) {
+    const int64_t v = pick_row(rows, i);
+    const int64_t p0 = indptr[v], p1 = indptr[v + 1];
+    for (int64_t p = p0; p < p1; ++p) {
+      const int64_t e = edge_ids ? edge_ids[p] : p;
+      if (e < 0 || e >= nnz_total) bad |= 1;
+    }
+    if (bad) continue;
+    for (int64_t h = 0; h < H; ++h) {
+      double m = -INFINITY;
+      for (int64_t p = p0; p < p1; ++p) {
+        const int64_t e = edge_ids ? edge_ids[p] : p;
+        double s = scores[e * H + h];
+        if (apply_leaky_relu && !(s > 0.0)) s = (double)slope * s;
+        if (s > m) m = s;
+      }
+      double z = 0.0;
+      for (int64_t p = p0; p < p1; ++p) {
+        const int64_t e = edge_ids ? edge_ids[p] : p;
+        double s = scores[e * H + h];
+        if (apply_leaky_relu && !(s > 0.0)) s = (double)slope * s;
+        z += exp(s - m);
+      }
+      double c = 0.0, cabs = 0.0;
+      for (int64_t p = p0; p < p1; ++p) {
+        const int64_t e = edge_ids ? edge_ids[p] : p;
+        double s = scores[e * H + h];
+        if (apply_leaky_relu && !(s > 0.0)) s = (double)slope * s;
+        const double a = exp(s - m) / z;
+        c += a * (double)grad_out[e * H + h];
+        cabs += a * fabs((double)grad_out[e * H + h]);
+      }
+      for (int64_t p = p0; p < p1; ++p) {
+        const int64_t e = edge_ids ? edge_ids[p] : p;
+        const double s0 = scores[e * H + h];
+        const double s = (apply_leaky_relu && !(s0 > 0.0)) ? (double)slope * s0 : s0;
+        const double lf = (apply_leaky_relu && !(s0 > 0.0)) ? (double)slope : 1.0;
+        const double a = exp(s - m) / z;
+        const double g = grad_out[e * H + h];
+        grad_scores[e * H + h] = (float)(a * (g - c) * lf);
+        if (scale) scale[e * H + h] = a * (fabs(g) + cabs) * fabs(lf);
       }
     }
   }

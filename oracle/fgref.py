@@ -64,7 +64,12 @@ def _load():
                                  ctypes.c_int]
     lib.fgref_edge_softmax.argtypes = [i64, vp, vp, i64, i64, vp, ctypes.c_int, ctypes.c_float,
                                        vp, i64, vp, ctypes.c_int]
-    for f in (lib.fgref_gspmm, lib.fgref_gsddmm, lib.fgref_edge_softmax):
+    lib.fgref_gspmm_max_backward.argtypes = [i64, i64, vp, vp, vp, i64, ctypes.c_int, i64, i64,
+                                             vp, vp, vp, vp, i64, vp, vp, vp, vp, ctypes.c_int]
+    lib.fgref_edge_softmax_backward.argtypes = [i64, vp, vp, i64, i64, vp, vp, ctypes.c_int,
+                                                ctypes.c_float, vp, i64, vp, vp, ctypes.c_int]
+    for f in (lib.fgref_gspmm, lib.fgref_gsddmm, lib.fgref_edge_softmax,
+              lib.fgref_gspmm_max_backward, lib.fgref_edge_softmax_backward):
         f.restype = ctypes.c_int
     lib.fgref_max_threads.restype = ctypes.c_int
     del i32p
@@ -174,3 +179,65 @@ def edge_softmax(g, scores: np.ndarray, heads: int = 1, leaky: bool = True,
     if rc != 0:
         raise ValueError("fgref_edge_softmax failed (%d)" % rc)
     return out
+
+
+def gspmm_max_backward(g, x: np.ndarray, grad_out: np.ndarray, msg: int = MSG_COPY_SRC,
+                       heads: int = 1, edge_val: Optional[np.ndarray] = None,
+                       rows: Optional[Sequence[int]] = None, nnz_total: Optional[int] = None,
+                       want_edge: bool = False, with_norm: bool = False, threads: int = 0):
+    """Gradient of gSpMM-max w.r.t. the source features (and the edge values
+    for src_mul_edge when want_edge): returns grad_src [num_cols, F]
+    (, grad_edge [nnz_total, H]) (, src_norm (, edge_norm))."""
+    lib = _load()
+    indptr, indices, eids = _graph_args(g)
+    x = _c(x, np.float32).reshape(g.num_cols, -1)
+    F = x.shape[1]
+    if F % heads:
+        raise ValueError("feature width not divisible by heads")
+    dh = F // heads
+    go = _c(grad_out, np.float32).reshape(g.num_rows, F)
+    ev = _c(edge_val, np.float32)
+    nt = int(indptr[-1]) if nnz_total is None else nnz_total
+    r, nsel = _rows_arg(rows, g.num_rows)
+    gsrc = np.empty((g.num_cols, F), np.float32)
+    gedge = np.empty((nt, heads), np.float32) if want_edge else None
+    snorm = np.empty((g.num_cols, F), np.float64) if with_norm else None
+    enorm = np.empty((nt, heads), np.float64) if (with_norm and want_edge) else None
+    rc = lib.fgref_gspmm_max_backward(g.num_rows, g.num_cols, _ptr(indptr), _ptr(indices),
+                                      _ptr(eids), nt, msg, heads, dh, _ptr(x), _ptr(ev), _ptr(go),
+                                      _ptr(r), nsel, _ptr(gsrc), _ptr(gedge), _ptr(snorm),
+                                      _ptr(enorm), threads)
+    if rc != 0:
+        raise ValueError("fgref_gspmm_max_backward failed (%d)" % rc)
+    res = [gsrc]
+    if want_edge:
+        res.append(gedge)
+    if with_norm:
+        res.append(snorm)
+        if want_edge:
+            res.append(enorm)
+    return res[0] if len(res) == 1 else tuple(res)
+
+
+def edge_softmax_backward(g, scores: np.ndarray, grad_out: np.ndarray, heads: int = 1,
+                          leaky: bool = True, slope: float = 0.2,
+                          rows: Optional[Sequence[int]] = None, nnz_total: Optional[int] = None,
+                          out: Optional[np.ndarray] = None, with_scale: bool = False,
+                          threads: int = 0):
+    """Gradient of edge softmax w.r.t. the scores: [nnz_total, H] by edge id
+    (edges of unselected rows untouched) (, term scale)."""
+    lib = _load()
+    indptr, _, eids = _graph_args(g)
+    nt = int(indptr[-1]) if nnz_total is None else nnz_total
+    s = _c(scores, np.float32).reshape(nt, heads)
+    go = _c(grad_out, np.float32).reshape(nt, heads)
+    if out is None:
+        out = np.full((nt, heads), np.nan, np.float32)
+    sc = np.full((nt, heads), np.nan, np.float64) if with_scale else None
+    r, nsel = _rows_arg(rows, g.num_rows)
+    rc = lib.fgref_edge_softmax_backward(g.num_rows, _ptr(indptr), _ptr(eids), nt, heads, _ptr(s),
+                                         _ptr(go), int(bool(leaky)), float(slope), _ptr(r), nsel,
+                                         _ptr(out), _ptr(sc), threads)
+    if rc != 0:
+        raise ValueError("fgref_edge_softmax_backward failed (%d)" % rc)
+    return (out, sc) if with_scale else out

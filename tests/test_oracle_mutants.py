@@ -37,6 +37,17 @@ MUTANTS = [
     # stabilising shift, which leaves the result unchanged: not a mistake)
     ("softmax_leaky_condition_flipped", "if (apply_leaky_relu && !(s > 0.0))",
      "if (apply_leaky_relu && (s > 0.0))", "all"),
+    ("max_bwd_to_destination", "const int64_t u = indices[pos[e]];", "const int64_t u = v % num_cols;"),
+    ("max_bwd_source_by_id_not_position", "const int64_t u = indices[pos[e]];", "const int64_t u = indices[e];"),
+    ("max_bwd_weight_dropped", "? (double)edge_val[e * H + h] * g : g;", "? g : g;"),
+    ("max_bwd_edge_grad_without_x", "const double te = (double)x[u * F + f] * g;", "const double te = g;"),
+    ("max_bwd_grad_by_selection_index", "const double g = grad_out[v * F + f];", "const double g = grad_out[i * F + f];"),
+    ("softmax_bwd_not_centred", "grad_scores[e * H + h] = (float)(a * (g - c) * lf);",
+     "grad_scores[e * H + h] = (float)(a * g * lf);"),
+    ("softmax_bwd_leaky_factor_dropped", "grad_scores[e * H + h] = (float)(a * (g - c) * lf);",
+     "grad_scores[e * H + h] = (float)(a * (g - c));"),
+    ("softmax_bwd_centre_unweighted", "c += a * (double)grad_out[e * H + h];",
+     "c += (double)grad_out[e * H + h];"),
     ("softmax_off_normaliser", "out[e * H + h] = (float)(exp(s - m) / z);", "out[e * H + h] = (float)(exp(s - m) / (z + 1e-3));"),
 ]
 

@@ -383,3 +383,175 @@ def test_invalid_arguments_rejected(O):
     bad.indices[0] = g.num_cols  # source out of range
     with pytest.raises(ValueError):
         O.gspmm(bad, x)
+
+
+# ---------------------------------------------------------------- backward of max and softmax
+
+
+def test_golden_max_backward(O):
+    gd, g = _golden_graph()
+    x = np.array(gd["x"], np.float32)
+    w = np.array(gd["w"], np.float32)
+    c = gd["copy_src_max_backward"]
+    go = np.array(c["grad_out"], np.float32)
+    np.testing.assert_array_equal(O.gspmm_max_backward(g, x, go), np.array(c["grad_src"]))
+    m = gd["src_mul_edge_max_backward"]
+    dx, dw = O.gspmm_max_backward(g, x, go, msg=O.MSG_SRC_MUL_EDGE, edge_val=w.reshape(-1, 1),
+                                  want_edge=True)
+    np.testing.assert_array_equal(dx, np.array(m["grad_src"]))
+    np.testing.assert_array_equal(dw[:, 0], np.array(m["grad_edge"]))
+
+
+def test_golden_softmax_backward(O):
+    gd, g = _golden_graph()
+    b = gd["edge_softmax_backward"]
+    s = np.array(b["scores"], np.float32).reshape(-1, 1)
+    go = np.array(b["grad_out"], np.float32).reshape(-1, 1)
+    ds = O.edge_softmax_backward(g, s, go, leaky=False)[:, 0]
+    np.testing.assert_allclose(ds[:4], b["no_leaky_rows_0_1"]["value"], rtol=1e-6, atol=1e-12)
+    ds = O.edge_softmax_backward(g, s, go, leaky=True, slope=0.2)[:, 0]
+    np.testing.assert_allclose(ds[4:], b["leaky_0.2_row3"]["value"], rtol=1e-6, atol=1e-15)
+
+
+def _max_autograd(torch, g, x, go, w=None, heads=1):
+    """Reference gradient of sum(G * maxagg(messages)) by torch autograd (fp64):
+    the messages of each row are laid out by increasing edge id in a padded
+    [rows, slots, F] tensor, the kept edge is chosen by numpy's argmax on the
+    fp32 messages (documented to return the first of equal maxima, i.e. the
+    smallest edge id) and gathered, so autograd routes G to that edge."""
+    eids = _eids(g)
+    rows = csr_rows(g)
+    deg = g.degrees()
+    D = max(int(deg.max()), 1)
+    F = x.shape[1]
+    dh = F // heads
+    order = np.lexsort((eids, rows))  # by row, then edge id
+    slot = np.arange(g.nnz) - g.indptr[rows[order]]
+    m32 = np.full((g.num_rows, D, F), -np.inf, np.float32)
+    src = g.indices[order]
+    e_sorted = eids[order]
+    msg32 = x[src]
+    if w is not None:
+        msg32 = (np.repeat(w[e_sorted], dh, axis=1) * msg32).astype(np.float32)
+    m32[rows[order], slot] = msg32
+    pick = np.argmax(m32, axis=1)  # [rows, F]
+    tx = torch.from_numpy(x).double().requires_grad_(True)
+    tw = None if w is None else torch.from_numpy(w).double().requires_grad_(True)
+    m = torch.zeros((g.num_rows, D, F), dtype=torch.float64)
+    tmsg = tx[torch.from_numpy(src.astype(np.int64))]
+    if tw is not None:
+        tmsg = tw[torch.from_numpy(e_sorted.astype(np.int64))].repeat_interleave(dh, dim=1) * tmsg
+    m = m.index_put((torch.from_numpy(rows[order].astype(np.int64)),
+                     torch.from_numpy(slot.astype(np.int64))), tmsg)
+    out = m.gather(1, torch.from_numpy(pick.astype(np.int64))[:, None, :])[:, 0, :]
+    nonempty = torch.from_numpy((deg > 0).astype(np.float64))[:, None]
+    (out * nonempty * torch.from_numpy(go).double()).sum().backward()
+    return tx.grad.numpy(), (None if tw is None else tw.grad.numpy())
+
+
+@pytest.mark.parametrize("weighted,heads,transpose,ties", [
+    (False, 1, False, False), (False, 1, False, True), (True, 1, False, False),
+    (True, 2, False, True), (False, 1, True, True), (True, 2, True, False)])
+def test_max_backward_matches_torch_autograd(O, weighted, heads, transpose, ties):
+    torch = pytest.importorskip("torch")
+    g = _rand_graph(81, n_rows=120, n_cols=100, e=2400, empty_frac=0.2)
+    nnz_total = g.nnz
+    if transpose:
+        g = csr_to_csc(g)
+    rng = np.random.default_rng(82)
+    F = 6
+    if ties:  # small integers: many equal messages, the smallest edge id must win
+        x = rng.integers(-2, 3, (g.num_cols, F)).astype(np.float32)
+        w = rng.integers(1, 3, (nnz_total, heads)).astype(np.float32) if weighted else None
+    else:
+        x = rng.standard_normal((g.num_cols, F)).astype(np.float32)
+        w = rng.random((nnz_total, heads)).astype(np.float32) + 0.5 if weighted else None
+    go = rng.standard_normal((g.num_rows, F)).astype(np.float32)
+    ref_x, ref_w = _max_autograd(torch, g, x, go, w, heads)
+    if weighted:
+        dx, dw = O.gspmm_max_backward(g, x, go, msg=O.MSG_SRC_MUL_EDGE, edge_val=w, heads=heads,
+                                      nnz_total=nnz_total, want_edge=True)
+        np.testing.assert_allclose(dw, ref_w, rtol=1e-6, atol=1e-12)
+    else:
+        dx = O.gspmm_max_backward(g, x, go, nnz_total=nnz_total)
+    np.testing.assert_allclose(dx, ref_x, rtol=1e-6, atol=1e-12)
+
+
+def test_max_backward_conserves_gradient_and_threads(O):
+    """copy_src: every non-empty row sends each G[v, k] to exactly one source,
+    so column sums of dX equal those of G over non-empty rows; row selection
+    keeps only the selected rows' contributions; threads do not matter."""
+    g = _rand_graph(83, n_rows=400, e=9000, empty_frac=0.15)
+    rng = np.random.default_rng(84)
+    x = rng.standard_normal((g.num_cols, 5)).astype(np.float32)
+    go = rng.integers(-8, 9, (g.num_rows, 5)).astype(np.float32)
+    dx = O.gspmm_max_backward(g, x, go, threads=1)
+    np.testing.assert_array_equal(dx.sum(0), go[g.degrees() > 0].sum(0))
+    np.testing.assert_array_equal(dx, O.gspmm_max_backward(g, x, go, threads=8))
+    rows = np.flatnonzero(np.arange(g.num_rows) % 3 == 0)
+    go_sel = np.zeros_like(go)
+    go_sel[rows] = go[rows]
+    np.testing.assert_array_equal(O.gspmm_max_backward(g, x, go, rows=rows),
+                                  O.gspmm_max_backward(g, x, go_sel))
+
+
+@pytest.mark.parametrize("heads,leaky,transpose", [(1, True, False), (3, True, False),
+                                                   (2, False, False), (1, True, True)])
+def test_softmax_backward_matches_torch_autograd(O, heads, leaky, transpose):
+    torch = pytest.importorskip("torch")
+    g = _rand_graph(85, n_rows=150, e=3000, empty_frac=0.2)
+    nnz_total = g.nnz
+    if transpose:
+        g = csr_to_csc(g)
+    rng = np.random.default_rng(86)
+    s = (2 * rng.standard_normal((nnz_total, heads))).astype(np.float32)
+    s[rng.random((nnz_total, heads)) < 0.05] = 0.0  # the leaky kink: slope at exactly 0
+    go = rng.standard_normal((nnz_total, heads)).astype(np.float32)
+    ds = O.edge_softmax_backward(g, s, go, heads=heads, leaky=leaky, slope=0.2,
+                                 nnz_total=nnz_total)
+    ts = torch.from_numpy(s).double().requires_grad_(True)
+    t = torch.nn.functional.leaky_relu(ts, negative_slope=float(np.float32(0.2))) if leaky else ts
+    eids = _eids(g)
+    loss = 0
+    for v in range(g.num_rows):
+        a, b = g.indptr[v], g.indptr[v + 1]
+        if a == b:
+            continue
+        idx = torch.from_numpy(eids[a:b])
+        loss = loss + (torch.softmax(t[idx], dim=0) * torch.from_numpy(go).double()[idx]).sum()
+    loss.backward()
+    np.testing.assert_allclose(ds, ts.grad.numpy(), rtol=1e-5, atol=1e-9)
+
+
+def test_softmax_backward_invariants(O):
+    g = _rand_graph(87, n_rows=300, e=6000, empty_frac=0.2)
+    rng = np.random.default_rng(88)
+    s = (3 * rng.standard_normal((g.nnz, 2))).astype(np.float32)
+    go = rng.standard_normal((g.nnz, 2)).astype(np.float32)
+    ds = O.edge_softmax_backward(g, s, go, heads=2, leaky=False, threads=1)
+    nz = g.degrees() > 0
+    rs = np.add.reduceat(ds.astype(np.float64), g.indptr[:-1][nz], axis=0)
+    np.testing.assert_allclose(rs, 0.0, atol=1e-6)  # softmax outputs sum to one
+    # a gradient constant over each row changes nothing
+    const = np.repeat(rng.standard_normal(g.num_rows).astype(np.float32), g.degrees())
+    ds0 = O.edge_softmax_backward(g, s, np.stack([const, const], 1), heads=2, leaky=False)
+    np.testing.assert_allclose(ds0, 0.0, atol=1e-6)
+    np.testing.assert_array_equal(ds, O.edge_softmax_backward(g, s, go, heads=2, leaky=False,
+                                                              threads=8))
+    rows = rng.choice(g.num_rows, 40, replace=False)
+    part = O.edge_softmax_backward(g, s, go, heads=2, leaky=False, rows=rows)
+    sel = np.concatenate([np.arange(g.indptr[r], g.indptr[r + 1]) for r in rows])
+    np.testing.assert_array_equal(part[sel], ds[sel])
+
+
+def test_backward_invalid_arguments_rejected(O):
+    g = _rand_graph(89, n_rows=10, e=30)
+    x = np.ones((g.num_cols, 4), np.float32)
+    go = np.ones((g.num_rows, 4), np.float32)
+    with pytest.raises(ValueError):
+        O.gspmm_max_backward(g, x, go, want_edge=True)  # copy_src has no edge values
+    with pytest.raises(ValueError):
+        O.gspmm_max_backward(g, x, go, msg=O.MSG_SRC_MUL_EDGE)  # missing edge values
+    dup = CSR(g.num_rows, g.num_cols, g.indptr, g.indices, np.zeros(g.nnz, np.int32))
+    with pytest.raises(ValueError):
+        O.gspmm_max_backward(dup, x, go, nnz_total=g.nnz)  # edge ids not distinct
