@@ -9,6 +9,9 @@
  *                       template of Sec. III-B / Fig. 4, multi-head Fig. 4b)
  *   edge softmax       (per-destination normalisation of edge scores that
  *                       sits between the two in an attention layer)
+ *   backward of gSpMM-max and of edge softmax (training; the backward of
+ *                       gSpMM-sum and gSDDMM are themselves gSDDMM and gSpMM
+ *                       calls, Sec. II-A)
  *
  * The paper's user-defined message / edge functions become a closed set of
  * operators (the builtin message functions it supports, Sec. III-B): copy the
@@ -231,6 +234,57 @@ fg_status fg_edge_softmax(const fg_graph* g, int32_t num_heads, const float* sco
 fg_status fg_gat_aggregate(const fg_graph* g, int32_t num_heads, int64_t head_dim,
                            const float* x_src, const float* x_dst, int32_t apply_leaky_relu,
                            float negative_slope, float* out, fg_plan* plan, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Gradient of gSpMM with the max aggregator, for training with max
+ * aggregation (GraphSage, Sec. V-E).  Sec. II-A derives the backward of the
+ * templates by the chain rule; for (+) = max each output element took its
+ * value from one edge, so only that edge's message receives the upstream
+ * gradient.  For every (v, h, k) with e = arg_eid[v, h, k] >= 0 and u the
+ * source of edge e:
+ *   grad_src[u, h, k] += (src_mul_edge ? edge_val[e, h] : 1) * grad_out[v, h, k]
+ *   grad_edge[e, h]   += x_src[u, h, k] * grad_out[v, h, k]      (src_mul_edge)
+ * x_src     [num_cols, H, dh]; needed iff grad_edge != NULL
+ * edge_val  [nnz_total, H]; required iff msg = SRC_MUL_EDGE, else NULL
+ * arg_eid   [num_rows, H, dh] int32, as written by fg_gspmm(..., FG_REDUCE_MAX)
+ * grad_out  [num_rows, H, dh]
+ * grad_src  [num_cols, H, dh] or NULL; grad_edge [nnz_total, H] or NULL (must
+ *           be NULL for copy_src).  Both are fully overwritten (zeros where
+ *           nothing arrives).
+ * plan      required when g->edge_ids != NULL: a plan created for this graph
+ *           with these edge ids (it maps ids back to storage positions; ids
+ *           must be distinct); otherwise optional and unused.
+ * Entries of arg_eid that are not edge ids of g are skipped.  Contributions
+ * to one element are added with fp32 atomics in an unspecified order, so a
+ * sum of several contributions may differ in the last bits between calls;
+ * the atomic adds may flush subnormal results to zero.
+ * ------------------------------------------------------------------------- */
+fg_status fg_gspmm_max_backward(const fg_graph* g, fg_msg_op msg, int32_t num_heads,
+                                int64_t head_dim, const float* x_src, const float* edge_val,
+                                const int32_t* arg_eid, const float* grad_out, float* grad_src,
+                                float* grad_edge, fg_plan* plan, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Gradient of fg_edge_softmax w.r.t. its scores, for training attention
+ * layers (GAT, Sec. V-E).  With a = the forward's output and G = dL/da, per
+ * row v and head h:
+ *   c = sum_{edges p of v} a_p * G_p
+ *   grad_scores[e, h] = a_e * (G_e - c) * (leaky && !(s_e > 0) ? slope : 1)
+ * (softmax Jacobian diag(a) - a a^T; the leaky ReLU's derivative is the slope
+ * for s <= 0, as in its forward).
+ * out        [nnz_total, H] the forward's result a
+ * grad_out   [nnz_total, H] G
+ * scores     [nnz_total, H] the forward's input s; required iff
+ *            apply_leaky_relu, else ignored
+ * grad_scores [nnz_total, H]; entries of edges of g are written, others left
+ *            untouched.  It may be the same array as grad_out (in place); it
+ *            must not overlap out or scores.
+ * Sums are fp32 in a fixed order for a given plan (deterministic).
+ * ------------------------------------------------------------------------- */
+fg_status fg_edge_softmax_backward(const fg_graph* g, int32_t num_heads, const float* out,
+                                   const float* grad_out, const float* scores,
+                                   int32_t apply_leaky_relu, float negative_slope,
+                                   float* grad_scores, fg_plan* plan, void* stream);
 
 const char* fg_status_string(fg_status s); /* static storage, never NULL */
 int32_t fg_abi_version(void);              /* == FG_ABI_VERSION */

@@ -115,6 +115,11 @@ def _load():
     lib.fg_gat_aggregate.argtypes = [gp, i32, i64, vp, vp, i32, ctypes.c_float, vp, vp, vp]
     lib.fg_edge_softmax.restype = ctypes.c_int
     lib.fg_edge_softmax.argtypes = [gp, i32, vp, i32, ctypes.c_float, vp, vp, vp]
+    lib.fg_gspmm_max_backward.restype = ctypes.c_int
+    lib.fg_gspmm_max_backward.argtypes = [gp, ctypes.c_int, i32, i64, vp, vp, vp, vp, vp, vp, vp,
+                                          vp]
+    lib.fg_edge_softmax_backward.restype = ctypes.c_int
+    lib.fg_edge_softmax_backward.argtypes = [gp, i32, vp, vp, vp, i32, ctypes.c_float, vp, vp, vp]
     if lib.fg_abi_version() != ABI_VERSION:
         raise ImportError("ABI version mismatch: library %d, binding %d"
                           % (lib.fg_abi_version(), ABI_VERSION))
@@ -432,6 +437,107 @@ def gat_aggregate(g: Graph, x_src: torch.Tensor, x_dst: Optional[torch.Tensor] =
     return out
 
 
-__all__ = ["Graph", "Plan", "gspmm", "gsddmm", "edge_softmax", "gat_aggregate", "schedule_host",
-           "FgError",
+# ----------------------------------------------------------------------------
+# backward operators (the backward of gspmm-sum and gsddmm are gsddmm / gspmm
+# calls on the graph or its transpose)
+# ----------------------------------------------------------------------------
+
+
+def gspmm_max_backward(g: Graph, arg: torch.Tensor, grad_out: torch.Tensor,
+                       x: Optional[torch.Tensor] = None, edge: Optional[torch.Tensor] = None,
+                       msg: str = "copy_src", heads: int = 1, plan: Optional[Plan] = None,
+                       want_src: bool = True, want_edge: bool = False,
+                       grad_src: Optional[torch.Tensor] = None,
+                       grad_edge: Optional[torch.Tensor] = None):
+    """Gradient of gspmm(..., reduce='max'): grad_out [num_rows, F] (or
+    [num_rows, H, dh]) goes to the source of the edge each output element was
+    taken from (arg, the forward's edge ids).  Returns grad_src [num_cols, ...]
+    and/or grad_edge [nnz_total, H] (src_mul_edge only; needs x).  Graphs with
+    explicit edge ids need their plan."""
+    if msg not in MSG_OPS:
+        raise ValueError("unknown msg %r" % msg)
+    grad_out = _dev_tensor(grad_out, torch.float32, "grad_out")
+    arg = _dev_tensor(arg, torch.int32, "arg")
+    if grad_out.shape[0] != g.num_rows or arg.shape != grad_out.shape:
+        raise ValueError("grad_out and arg must be [num_rows, ...] of one shape")
+    F = int(np.prod(grad_out.shape[1:])) if grad_out.dim() > 1 else 1
+    if grad_out.dim() == 3:
+        heads = int(grad_out.shape[1])
+    if F % heads:
+        raise ValueError("feature width not divisible by heads")
+    if msg == "src_mul_edge":
+        if edge is None:
+            raise ValueError("src_mul_edge needs edge values")
+        edge = _dev_tensor(edge, torch.float32, "edge")
+        if edge.numel() != g.nnz_total * heads:
+            raise ValueError("edge must have nnz_total * heads values")
+    elif edge is not None or want_edge:
+        raise ValueError("copy_src has no edge values (and no edge gradient)")
+    if want_edge:
+        if x is None:
+            raise ValueError("the edge gradient needs the source features x")
+        x = _dev_tensor(x, torch.float32, "x")
+        if x.numel() != g.num_cols * F:
+            raise ValueError("x must be [num_cols, F]")
+    else:
+        x = None
+    dev = grad_out.device
+    if want_src:
+        shape = (g.num_cols,) + tuple(grad_out.shape[1:])
+        grad_src = torch.empty(shape, dtype=torch.float32, device=dev) if grad_src is None else \
+            _dev_tensor(grad_src, torch.float32, "grad_src")
+        if grad_src.numel() != g.num_cols * F:
+            raise ValueError("grad_src has the wrong size")
+    else:
+        grad_src = None
+    if want_edge:
+        grad_edge = torch.empty((g.nnz_total, heads), dtype=torch.float32, device=dev) \
+            if grad_edge is None else _dev_tensor(grad_edge, torch.float32, "grad_edge")
+        if grad_edge.numel() != g.nnz_total * heads:
+            raise ValueError("grad_edge has the wrong size")
+    else:
+        grad_edge = None
+    st = _lib.fg_gspmm_max_backward(ctypes.byref(g._c), MSG_OPS[msg], heads, F // heads,
+                                    _ptr(x), _ptr(edge), _ptr(arg), _ptr(grad_out),
+                                    _ptr(grad_src), _ptr(grad_edge), _plan_handle(plan),
+                                    _stream())
+    _check(st, "fg_gspmm_max_backward")
+    if want_src and want_edge:
+        return grad_src, grad_edge
+    return grad_src if want_src else grad_edge
+
+
+def edge_softmax_backward(g: Graph, out: torch.Tensor, grad_out: torch.Tensor,
+                          scores: Optional[torch.Tensor] = None, leaky: bool = True,
+                          slope: float = 0.2, plan: Optional[Plan] = None,
+                          grad_scores: Optional[torch.Tensor] = None):
+    """Gradient of edge_softmax w.r.t. its scores, from its output `out` (the
+    attention weights), the upstream gradient and (leaky ReLU only) the
+    forward's scores.  grad_scores may be grad_out itself (in place)."""
+    out = _dev_tensor(out, torch.float32, "out")
+    grad_out = _dev_tensor(grad_out, torch.float32, "grad_out")
+    if out.shape[0] != g.nnz_total or grad_out.shape != out.shape:
+        raise ValueError("out and grad_out must be [nnz_total(, H)] of one shape")
+    heads = int(out.shape[1]) if out.dim() == 2 else 1
+    if leaky:
+        if scores is None:
+            raise ValueError("the leaky ReLU's gradient needs the forward's scores")
+        scores = _dev_tensor(scores, torch.float32, "scores")
+        if scores.shape != out.shape:
+            raise ValueError("scores must have the shape of out")
+    else:
+        scores = None
+    grad_scores = torch.empty_like(out) if grad_scores is None else \
+        _dev_tensor(grad_scores, torch.float32, "grad_scores")
+    if grad_scores.numel() != out.numel():
+        raise ValueError("grad_scores has the wrong size")
+    st = _lib.fg_edge_softmax_backward(ctypes.byref(g._c), heads, _ptr(out), _ptr(grad_out),
+                                       _ptr(scores), 1 if leaky else 0, float(slope),
+                                       _ptr(grad_scores), _plan_handle(plan), _stream())
+    _check(st, "fg_edge_softmax_backward")
+    return grad_scores
+
+
+__all__ = ["Graph", "Plan", "gspmm", "gsddmm", "edge_softmax", "gat_aggregate",
+           "gspmm_max_backward", "edge_softmax_backward", "schedule_host", "FgError",
            "status_string", "LIB_PATH"]

@@ -6,6 +6,7 @@
 #include <cstdint>
 #include <cstring>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "featgraph_hip.h"
@@ -22,6 +23,11 @@ struct fg_plan {
   int64_t num_partitioned_rows = 0;
   int device = 0;
   fg::PlanView gather, plain;
+  // graphs with explicit edge ids: edge id -> storage position (the max
+  // gradient needs the source of an edge given its id)
+  const int32_t* edge_ids = nullptr;
+  int64_t nnz_total = 0;
+  int32_t* eid_pos = nullptr;
   std::vector<void*> mem;
   int64_t workspace_bytes = 0;
 };
@@ -489,6 +495,26 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
     v->ws_width = ws_width;
   }
   p->workspace_bytes = (int64_t)(wb[0] + wb[1] + wb[2]);
+  if (g->edge_ids) {
+    p->edge_ids = g->edge_ids;
+    p->nnz_total = nnz_total_of(g);
+    void* m = nullptr;
+    const size_t mb = sizeof(int32_t) * (size_t)std::max<int64_t>(p->nnz_total, 1);
+    if (hipMalloc(&m, mb) != hipSuccess) {
+      (void)hipStreamSynchronize(hs);
+      fg_plan_destroy(p);
+      return FG_ERR_NO_MEMORY;
+    }
+    p->mem.push_back(m);
+    p->eid_pos = static_cast<int32_t*>(m);
+    p->workspace_bytes += (int64_t)mb;
+    if (fg::launch_build_eid_pos(g->edge_ids, g->nnz, p->nnz_total, p->eid_pos, hs) !=
+        hipSuccess) {
+      (void)hipStreamSynchronize(hs);
+      fg_plan_destroy(p);
+      return FG_ERR_HIP;
+    }
+  }
   if (hipStreamSynchronize(hs) != hipSuccess) {  // host schedules die on return
     fg_plan_destroy(p);
     return FG_ERR_HIP;
@@ -603,6 +629,63 @@ fg_status fg_gat_aggregate(const fg_graph* g, int32_t num_heads, int64_t head_di
   return from_hip(fg::launch_gat_fused(gv, plan ? &plan->gather : nullptr, num_heads, head_dim,
                                        x_src, x_dst, apply_leaky_relu != 0, negative_slope, out,
                                        static_cast<hipStream_t>(stream)));
+}
+
+fg_status fg_gspmm_max_backward(const fg_graph* g, fg_msg_op msg, int32_t num_heads,
+                                int64_t head_dim, const float* x_src, const float* edge_val,
+                                const int32_t* arg_eid, const float* grad_out, float* grad_src,
+                                float* grad_edge, fg_plan* plan, void* stream) {
+  fg_status st = check_graph(g);
+  if (st != FG_OK) return st;
+  if ((st = check_width(num_heads, head_dim)) != FG_OK) return st;
+  if (msg != FG_MSG_COPY_SRC && msg != FG_MSG_SRC_MUL_EDGE) return FG_ERR_INVALID_ARG;
+  const bool mul = msg == FG_MSG_SRC_MUL_EDGE;
+  if (mul != (edge_val != nullptr)) return FG_ERR_INVALID_ARG;
+  if (!mul && grad_edge) return FG_ERR_INVALID_ARG;  // copy_src has no edge values
+  if (grad_edge && g->nnz > 0 && !x_src) return FG_ERR_INVALID_ARG;
+  if (g->num_rows > 0 && g->nnz > 0 && (grad_src || grad_edge) && (!arg_eid || !grad_out))
+    return FG_ERR_INVALID_ARG;
+  if ((st = check_plan(plan, g, 1)) != FG_OK) return st;
+  if (g->edge_ids && g->nnz > 0 &&
+      (!plan || plan->edge_ids != g->edge_ids || plan->nnz_total != nnz_total_of(g)))
+    return FG_ERR_INVALID_ARG;  // the plan of this graph holds the id -> position map
+  const int64_t F = (int64_t)num_heads * head_dim;
+  const int64_t src_b = g->num_cols * F * 4, edge_b = nnz_total_of(g) * num_heads * 4;
+  const int64_t row_b = g->num_rows * F * 4;
+  for (const auto& o : {std::make_pair((const void*)grad_src, src_b),
+                        std::make_pair((const void*)grad_edge, edge_b)}) {
+    if (overlaps(o.first, o.second, x_src, src_b) || overlaps(o.first, o.second, edge_val, edge_b) ||
+        overlaps(o.first, o.second, arg_eid, row_b) || overlaps(o.first, o.second, grad_out, row_b))
+      return FG_ERR_INVALID_ARG;
+  }
+  if (overlaps(grad_src, src_b, grad_edge, edge_b)) return FG_ERR_INVALID_ARG;
+  const fg::GraphView gv = view_of(g);
+  return from_hip(fg::launch_gspmm_max_backward(gv, plan ? plan->eid_pos : nullptr, (int)msg,
+                                                num_heads, head_dim, x_src, edge_val, arg_eid,
+                                                grad_out, grad_src, grad_edge,
+                                                static_cast<hipStream_t>(stream)));
+}
+
+fg_status fg_edge_softmax_backward(const fg_graph* g, int32_t num_heads, const float* out,
+                                   const float* grad_out, const float* scores,
+                                   int32_t apply_leaky_relu, float negative_slope,
+                                   float* grad_scores, fg_plan* plan, void* stream) {
+  fg_status st = check_graph(g);
+  if (st != FG_OK) return st;
+  if (num_heads < 1 || num_heads > FG_MAX_WIDTH) return FG_ERR_INVALID_ARG;
+  if (g->nnz > 0 && (!out || !grad_out || !grad_scores)) return FG_ERR_INVALID_ARG;
+  if (g->nnz > 0 && apply_leaky_relu && !scores) return FG_ERR_INVALID_ARG;
+  // the plan's workspace holds H floats per slot
+  if ((st = check_plan(plan, g, num_heads)) != FG_OK) return st;
+  const int64_t b = nnz_total_of(g) * num_heads * 4;
+  if (overlaps(grad_scores, b, out, b) || overlaps(grad_scores, b, apply_leaky_relu ? scores : nullptr, b))
+    return FG_ERR_INVALID_ARG;
+  if (grad_scores != grad_out && overlaps(grad_scores, b, grad_out, b)) return FG_ERR_INVALID_ARG;
+  const fg::GraphView gv = view_of(g);
+  return from_hip(fg::launch_edge_softmax_backward(
+      gv, plan ? &plan->plain : nullptr, num_heads, out, grad_out,
+      apply_leaky_relu ? scores : nullptr, apply_leaky_relu != 0, negative_slope, grad_scores,
+      static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -52,6 +52,22 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
                                const float* scores, bool leaky, float slope, float* out,
                                hipStream_t stream);
 
+// Backward of gSpMM-max: zero-fills gsrc / gedge (either may be null), then
+// sends each upstream gradient element to the source of the edge the forward
+// picked (fp32 atomics).  eid_pos maps edge id -> storage position and is
+// used only when g.edge_ids is set.
+hipError_t launch_gspmm_max_backward(const GraphView& g, const int32_t* eid_pos, int msg,
+                                     int64_t H, int64_t dh, const float* x, const float* ev,
+                                     const int32_t* arg, const float* go, float* gsrc,
+                                     float* gedge, hipStream_t stream);
+// Backward of edge softmax (leaky ReLU optional) on the plain schedule.
+hipError_t launch_edge_softmax_backward(const GraphView& g, const PlanView* plan, int64_t H,
+                                        const float* a, const float* go, const float* scores,
+                                        bool leaky, float slope, float* ds, hipStream_t stream);
+// pos[edge_ids[q]] = q for the nnz stored edges, -1 for ids not stored.
+hipError_t launch_build_eid_pos(const int32_t* eids, int64_t nnz, int64_t nnz_total, int32_t* pos,
+                                hipStream_t stream);
+
 // Fused SDDMM -> leaky ReLU -> edge softmax -> weighted gSpMM.  Supported
 // shapes: dh % 4 == 0, dh / 4 a power of two, H * dh <= 256; aligned inputs.
 bool gat_fused_supported(int64_t H, int64_t dh);

@@ -20,6 +20,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "fg_internal.h"
 
 namespace fg {
@@ -1273,6 +1275,194 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
 }
 
 // ----------------------------------------------------------------------------
+// backward of gSpMM-max and of edge softmax
+// ----------------------------------------------------------------------------
+
+// Zero fill (a kernel, not a memset, so that a caller may capture it in a
+// graph).  VEC4: the array is 16-byte aligned and n is a multiple of 4.
+template <bool VEC4>
+__global__ __launch_bounds__(kBlock) void zero_kernel(float* p, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if constexpr (VEC4) {
+    float4* q = reinterpret_cast<float4*>(p);
+    for (int64_t i = t; i < n / 4; i += stride) q[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  } else {
+    for (int64_t i = t; i < n; i += stride) p[i] = 0.0f;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+// pos[edge_ids[q]] = q for every stored edge q (ids outside [0, nnz_total)
+// are skipped; with distinct ids every write has its own address).
+__global__ __launch_bounds__(kBlock) void eid_pos_kernel(const int32_t* eids, int64_t nnz,
+                                                         int64_t nnz_total, int32_t* pos) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < nnz; q += stride) {
+    const int32_t e = eids[q];
+    if (e >= 0 && e < nnz_total) pos[e] = (int32_t)q;
+  }
+}
+
+struct MaxBwdParams {
+  const int32_t* indices;
+  const int32_t* eid_pos;  // edge id -> storage position; null: edge id == position
+  const int32_t* arg;      // [rows, F] edge id chosen by the forward, -1 for none
+  const float* go;         // [rows, F] upstream gradient
+  const float* x;          // [cols, F] source features (edge gradient only)
+  const float* ev;         // [nnz_total, H] edge values (src_mul_edge only)
+  float* gsrc;             // [cols, F] or null, zero-filled beforehand
+  float* gedge;            // [nnz_total, H] or null, zero-filled beforehand
+  int64_t num_rows, F, id_limit;  // ids >= id_limit are ignored
+  int32_t H, dh, mul;
+};
+
+// One wavefront per destination row, lanes over its F output elements (two
+// coalesced loads per element).  Each element's upstream gradient goes to the
+// source of the edge its forward value came from, by a hardware fp32 atomic
+// add in L2: about rows x F atomics in all, instead of re-reading every edge's
+// argmax through the transposed graph (rows x F << E x F).  The order of the
+// adds into one address is not fixed, so sums of several contributions may
+// differ in the last bits between runs.
+__global__ __launch_bounds__(kBlock) void spmm_max_bwd_kernel(MaxBwdParams p) {
+  const int64_t v = wave_item();
+  if (v >= p.num_rows) return;
+  const int lane = lane_id();
+  const int64_t base = v * p.F;
+  for (int64_t f = lane; f < p.F; f += kWave) {
+    const int32_t e = p.arg[base + f];
+    if (e < 0 || e >= p.id_limit) continue;
+    const int64_t q = p.eid_pos ? (int64_t)p.eid_pos[e] : (int64_t)e;
+    if (q < 0) continue;
+    const int64_t u = p.indices[q];
+    const float g = p.go[base + f];
+    const int64_t he = (int64_t)e * p.H + (p.H == 1 ? 0 : (int32_t)f / p.dh);
+    if (p.gsrc) unsafeAtomicAdd(&p.gsrc[u * p.F + f], p.mul ? p.ev[he] * g : g);
+    if (p.gedge) unsafeAtomicAdd(&p.gedge[he], p.x[u * p.F + f] * g);
+  }
+}
+
+struct SoftmaxBwdParams {
+  const int32_t* indptr;
+  const int32_t* eids;
+  const float* a;   // forward output (attention weights)
+  const float* go;  // upstream gradient w.r.t. a
+  const float* s;   // forward input scores (leaky ReLU only)
+  float* ds;        // gradient w.r.t. the scores
+  const Seg* segs;
+  const Fix* fix;
+  const int32_t* slot_fix;
+  const int32_t* slot_seg;
+  float* ws;  // [slot][H] partial sums of a * go
+  int64_t n_items;
+  int32_t H;
+  int32_t leaky;
+  float slope;
+};
+
+// ds_e = a_e * (go_e - c) * (leaky && s_e <= 0 ? slope : 1), c = sum_row a go.
+__device__ __forceinline__ void softmax_bwd_write(const SoftmaxBwdParams& p, int64_t b,
+                                                  int64_t e, int eo, int epw, int h, float c) {
+  const int H = p.H;
+  for (int64_t q0 = b + eo; q0 < e; q0 += (int64_t)kSoftmaxU * epw) {
+    float av[kSoftmaxU], gv[kSoftmaxU], lf[kSoftmaxU];
+    int64_t ix[kSoftmaxU];
+#pragma unroll
+    for (int k = 0; k < kSoftmaxU; ++k) {
+      const int64_t q = q0 + (int64_t)k * epw;
+      ix[k] = -1;
+      if (q < e) {
+        ix[k] = (p.eids ? (int64_t)p.eids[q] : q) * H + h;
+        av[k] = p.a[ix[k]];
+        gv[k] = p.go[ix[k]];
+        lf[k] = (p.leaky && !(p.s[ix[k]] > 0.0f)) ? p.slope : 1.0f;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kSoftmaxU; ++k)
+      if (ix[k] >= 0) p.ds[ix[k]] = av[k] * (gv[k] - c) * lf[k];
+  }
+}
+
+// One wavefront per item, lanes on (edge offset, head) pairs as in the
+// forward.  Pass 1 sums a * go per lane, lanes of one head combine in a fixed
+// tree; a whole row then writes its gradients (pass 2), a segment of a split
+// row leaves its partial sum in the workspace instead.
+template <bool SEG>
+__global__ __launch_bounds__(kBlock) void softmax_bwd_kernel(SoftmaxBwdParams p) {
+  const int64_t item = wave_item();
+  if (item >= p.n_items) return;
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0 || it.b >= it.e) return;
+  const int lane = lane_id();
+  const int H = p.H;
+  for (int h0 = 0; h0 < H; h0 += kWave) {
+    const int hc = min(H - h0, kWave);
+    const int epw = kWave / hc;
+    const int eo = lane / hc;
+    const int h = h0 + lane % hc;
+    const bool active = eo < epw;
+    float c = 0.0f;
+    if (active) {
+      for (int64_t q0 = it.b + eo; q0 < it.e; q0 += (int64_t)kSoftmaxU * epw) {
+        float av[kSoftmaxU], gv[kSoftmaxU];
+#pragma unroll
+        for (int k = 0; k < kSoftmaxU; ++k) {
+          const int64_t q = q0 + (int64_t)k * epw;
+          av[k] = 0.0f;
+          gv[k] = 0.0f;
+          if (q < it.e) {
+            const int64_t ix = (p.eids ? (int64_t)p.eids[q] : q) * H + h;
+            av[k] = p.a[ix];
+            gv[k] = p.go[ix];
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < kSoftmaxU; ++k) c = fmaf(av[k], gv[k], c);
+      }
+    }
+    for (int k = 1; k < epw; k <<= 1) {
+      const int partner = (lane + k * hc) & (kWave - 1);
+      const float oc = __shfl(c, partner);
+      if (active && (eo % (2 * k)) == 0 && eo + k < epw) c += oc;
+    }
+    c = __shfl(c, lane % hc);
+    if (SEG && it.slot >= 0) {
+      if (active && eo == 0) p.ws[(int64_t)it.slot * H + h] = c;
+      continue;
+    }
+    if (active) softmax_bwd_write(p, it.b, it.e, eo, epw, h, c);
+  }
+}
+
+// Segments of split rows: add the row's partial sums in slot order (every
+// segment of the row forms the same total), then write this segment's
+// gradients.  Item = slot.
+__global__ __launch_bounds__(kBlock) void softmax_bwd_split_kernel(SoftmaxBwdParams p,
+                                                                   int64_t n_slots) {
+  const int64_t slot = wave_item();
+  if (slot >= n_slots) return;
+  const Seg sg = p.segs[p.slot_seg[slot]];
+  const Fix fx = p.fix[p.slot_fix[slot]];
+  const int lane = lane_id();
+  const int H = p.H;
+  for (int h0 = 0; h0 < H; h0 += kWave) {
+    const int hc = min(H - h0, kWave);
+    const int epw = kWave / hc;
+    const int eo = lane / hc;
+    const int h = h0 + lane % hc;
+    if (eo >= epw) continue;
+    float c = 0.0f;
+    for (int t = fx.slot_begin; t < fx.slot_end; ++t) c += p.ws[(int64_t)t * H + h];
+    softmax_bwd_write(p, sg.begin, sg.end, eo, epw, h, c);
+  }
+}
+
+// ----------------------------------------------------------------------------
 // fused attention aggregation: SDDMM -> leaky ReLU -> edge softmax -> gSpMM
 // ----------------------------------------------------------------------------
 
@@ -1739,6 +1929,90 @@ hipError_t launch_gat_fused(const GraphView& g, const PlanView* plan, int64_t H,
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || !seg || plan->num_split_rows == 0) return err;
   FG_LAUNCH(gat_fixup_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, prm, plan->fix);
+  return hipGetLastError();
+}
+
+namespace {
+
+dim3 stride_grid(int64_t n) {
+  const int64_t b = (n + kBlock - 1) / kBlock;
+  return dim3((unsigned)std::max<int64_t>(1, std::min<int64_t>(b, 8192)), 1, 1);
+}
+
+hipError_t zero_fill(float* p, int64_t n, hipStream_t stream) {
+  if (!p || n <= 0) return hipSuccess;
+  if (aligned16(p) && n % 4 == 0)
+    FG_LAUNCH((zero_kernel<true>), stride_grid(n / 4), stream, p, n);
+  else
+    FG_LAUNCH((zero_kernel<false>), stride_grid(n), stream, p, n);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_build_eid_pos(const int32_t* eids, int64_t nnz, int64_t nnz_total, int32_t* pos,
+                                hipStream_t stream) {
+  if (nnz_total > 0) FG_LAUNCH(fill_i32_kernel, stride_grid(nnz_total), stream, pos, nnz_total, -1);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || nnz == 0) return err;
+  FG_LAUNCH(eid_pos_kernel, stride_grid(nnz), stream, eids, nnz, nnz_total, pos);
+  return hipGetLastError();
+}
+
+hipError_t launch_gspmm_max_backward(const GraphView& g, const int32_t* eid_pos, int msg,
+                                     int64_t H, int64_t dh, const float* x, const float* ev,
+                                     const int32_t* arg, const float* go, float* gsrc,
+                                     float* gedge, hipStream_t stream) {
+  const int64_t F = H * dh;
+  hipError_t err = zero_fill(gsrc, g.num_cols * F, stream);
+  if (err != hipSuccess) return err;
+  if ((err = zero_fill(gedge, g.nnz_total * H, stream)) != hipSuccess) return err;
+  if (g.num_rows == 0 || g.nnz == 0 || (!gsrc && !gedge)) return hipSuccess;
+  MaxBwdParams prm;
+  prm.indices = g.indices;
+  prm.eid_pos = g.edge_ids ? eid_pos : nullptr;
+  prm.arg = arg;
+  prm.go = go;
+  prm.x = x;
+  prm.ev = ev;
+  prm.gsrc = gsrc;
+  prm.gedge = gedge;
+  prm.num_rows = g.num_rows;
+  prm.F = F;
+  prm.id_limit = g.edge_ids ? g.nnz_total : g.nnz;
+  prm.H = (int32_t)H;
+  prm.dh = (int32_t)dh;
+  prm.mul = msg == kSrcMulEdge ? 1 : 0;
+  FG_LAUNCH(spmm_max_bwd_kernel, grid_for(g.num_rows, 1), stream, prm);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_softmax_backward(const GraphView& g, const PlanView* plan, int64_t H,
+                                        const float* a, const float* go, const float* scores,
+                                        bool leaky, float slope, float* ds, hipStream_t stream) {
+  if (g.num_rows == 0 || g.nnz == 0) return hipSuccess;
+  SoftmaxBwdParams prm;
+  prm.indptr = g.indptr;
+  prm.eids = g.edge_ids;
+  prm.a = a;
+  prm.go = go;
+  prm.s = scores;
+  prm.ds = ds;
+  prm.segs = plan ? plan->segs : nullptr;
+  prm.fix = plan ? plan->fix : nullptr;
+  prm.slot_fix = plan ? plan->slot_fix : nullptr;
+  prm.slot_seg = plan ? plan->slot_seg : nullptr;
+  prm.ws = plan ? plan->ws_f : nullptr;
+  prm.n_items = plan ? plan->num_segments : g.num_rows;
+  prm.H = (int32_t)H;
+  prm.leaky = leaky ? 1 : 0;
+  prm.slope = slope;
+  const dim3 grid = grid_for(prm.n_items, 1);
+  if (plan) FG_LAUNCH((softmax_bwd_kernel<true>), grid, stream, prm);
+  else FG_LAUNCH((softmax_bwd_kernel<false>), grid, stream, prm);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || !plan || plan->num_slots == 0) return err;
+  FG_LAUNCH(softmax_bwd_split_kernel, grid_for(plan->num_slots, 1), stream, prm, plan->num_slots);
   return hipGetLastError();
 }
 

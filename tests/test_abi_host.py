@@ -146,6 +146,50 @@ def test_gat_aggregate_rejects_invalid_or_unsupported_arguments():
     assert call(xs=FAKE_X + 4) == fg.FG_ERR_UNSUPPORTED  # not 16-byte aligned
 
 
+def test_gspmm_max_backward_rejects_invalid_arguments():
+    L = fg._lib
+    g = _graph_struct()
+    GS, GE, GO = 0x50000, 0x60000, 0x70000
+    ok = dict(msg=0, H=1, dh=4, x=FAKE_X, ev=None, arg=FAKE_ARG, go=GO, gs=GS, ge=None)
+
+    def call(graph=g, **kw):
+        a = dict(ok, **kw)
+        return L.fg_gspmm_max_backward(ctypes.byref(graph), a["msg"], a["H"], a["dh"], a["x"],
+                                       a["ev"], a["arg"], a["go"], a["gs"], a["ge"], None, None)
+
+    assert call(msg=2) == fg.FG_ERR_INVALID_ARG
+    assert call(H=0) == fg.FG_ERR_INVALID_ARG
+    assert call(ev=FAKE_EV) == fg.FG_ERR_INVALID_ARG           # copy_src takes no edge values
+    assert call(ge=GE) == fg.FG_ERR_INVALID_ARG                # ... and has no edge gradient
+    assert call(msg=1) == fg.FG_ERR_INVALID_ARG                # src_mul_edge without values
+    assert call(msg=1, ev=FAKE_EV, ge=GE, x=None) == fg.FG_ERR_INVALID_ARG  # edge grad needs x
+    assert call(arg=None) == fg.FG_ERR_INVALID_ARG
+    assert call(go=None) == fg.FG_ERR_INVALID_ARG
+    assert call(gs=FAKE_X + 4) == fg.FG_ERR_INVALID_ARG        # output overlaps x
+    assert call(gs=GO + 8) == fg.FG_ERR_INVALID_ARG            # output overlaps grad_out
+    assert call(msg=1, ev=FAKE_EV, ge=GS + 4) == fg.FG_ERR_INVALID_ARG  # the two outputs overlap
+    eg = fg._Graph(4, 4, 7, 7, 0x1000, 0x1100, 0x1200)
+    assert call(graph=eg) == fg.FG_ERR_INVALID_ARG             # edge ids need the graph's plan
+
+
+def test_edge_softmax_backward_rejects_invalid_arguments():
+    L = fg._lib
+    g = _graph_struct()
+    A, GO, S, DS = 0x10000, 0x20000, 0x30000, 0x40000
+
+    def call(H=1, a=A, go=GO, s=S, leaky=1, ds=DS):
+        return L.fg_edge_softmax_backward(ctypes.byref(g), H, a, go, s, leaky, 0.2, ds, None, None)
+
+    assert call(H=0) == fg.FG_ERR_INVALID_ARG
+    assert call(a=None) == fg.FG_ERR_INVALID_ARG
+    assert call(go=None) == fg.FG_ERR_INVALID_ARG
+    assert call(ds=None) == fg.FG_ERR_INVALID_ARG
+    assert call(s=None) == fg.FG_ERR_INVALID_ARG               # leaky needs the scores
+    assert call(ds=A + 4) == fg.FG_ERR_INVALID_ARG             # overlaps the weights
+    assert call(ds=S) == fg.FG_ERR_INVALID_ARG                 # overlaps the scores
+    assert call(ds=GO + 4) == fg.FG_ERR_INVALID_ARG            # partial overlap of grad_out
+
+
 def test_plan_create_rejects_invalid_arguments():
     L = fg._lib
     g = _graph_struct()

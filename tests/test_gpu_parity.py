@@ -171,6 +171,89 @@ def check_gat(csr, G, x, rows=None, plan=None, heads=1, leaky=True):
     return res
 
 
+def _sources_of_ids(csr, nnz_total):
+    """source vertex of every edge id (-1 for ids not stored)"""
+    src = np.full(nnz_total, -1, np.int64)
+    src[edge_ids_of(csr, np.arange(csr.nnz))] = csr.indices
+    return src
+
+
+def check_max_backward(csr, G, x, go, plan=None, edge=None, heads=1, nnz_total=None,
+                       exact=False, want_edge=False):
+    """gspmm(max) forward on the GPU, then its gradient, vs the oracle's
+    gradient (which recomputes the argmax itself).  Term counts for the
+    tolerance come from the oracle's own forward."""
+    F = int(np.prod(x.shape[1:]))
+    dh = F // heads
+    nt = csr.nnz if nnz_total is None else nnz_total
+    msg = "copy_src" if edge is None else "src_mul_edge"
+    say("gspmm_max_backward", msg, "rows=%d nnz=%d F=%d H=%d edge_grad=%s plan=%s" % (
+        csr.num_rows, csr.nnz, F, heads, want_edge,
+        None if plan is None else plan.info()["segment_edges"]))
+    tx, te = dev(x), (None if edge is None else dev(edge))
+    _, arg = fg.gspmm(G, tx, te, msg=msg, reduce="max", heads=heads, plan=plan)
+    res = fg.gspmm_max_backward(G, arg, dev(go), x=tx, edge=te, msg=msg, heads=heads, plan=plan,
+                                want_edge=want_edge)
+    gs, ge = (res if want_edge else (res, None))
+    gs = host(gs).reshape(csr.num_cols, F)
+    x2 = x.reshape(csr.num_cols, F)
+    go2 = go.reshape(csr.num_rows, F)
+    kw = dict(msg=O.MSG_COPY_SRC if edge is None else O.MSG_SRC_MUL_EDGE, heads=heads,
+              edge_val=None if edge is None else edge.reshape(-1, heads), nnz_total=nt)
+    if want_edge:
+        ge = host(ge).reshape(nt, heads)
+    if exact:  # integer-valued terms: any order of the atomic adds gives the same sum
+        ref = O.gspmm_max_backward(csr, x2, go2, want_edge=want_edge, **kw)
+        rs, re_ = ref if want_edge else (ref, None)
+        np.testing.assert_array_equal(gs, rs)
+        if want_edge:
+            np.testing.assert_array_equal(ge, re_)
+        return res
+    ref = O.gspmm_max_backward(csr, x2, go2, want_edge=want_edge, with_norm=True, **kw)
+    _, ra = O.gspmm(csr, x2, red=O.RED_MAX, **kw)
+    sel = ra >= 0
+    src = _sources_of_ids(csr, nt)
+    fcol = np.broadcast_to(np.arange(F), ra.shape)
+    cnt_s = np.zeros((csr.num_cols, F))
+    np.add.at(cnt_s, (src[ra[sel]], fcol[sel]), 1.0)
+    if want_edge:
+        rs, re_, ns, ne = ref
+        cnt_e = np.zeros((nt, heads))
+        np.add.at(cnt_e, (ra[sel], fcol[sel] // dh), 1.0)
+        assert_close_sum(ge, re_.astype(np.float64), ne, cnt_e)
+    else:
+        rs, ns = ref
+    assert_close_sum(gs, rs.astype(np.float64), ns, cnt_s)
+    return res
+
+
+def check_softmax_backward(csr, G, scores, go, rows=None, plan=None, heads=1, leaky=True,
+                           nnz_total=None, inplace=False):
+    """edge_softmax forward on the GPU, then its gradient from the GPU's
+    attention weights, vs the oracle's gradient from the scores.
+    Tolerance: |y - ref| <= 1e-5 * sqrt(n) * a (|G| + sum a|G|) + 1e-12."""
+    nt = csr.nnz if nnz_total is None else nnz_total
+    say("edge_softmax_backward rows=%d nnz=%d H=%d leaky=%s inplace=%s" % (
+        csr.num_rows, csr.nnz, heads, leaky, inplace))
+    ts, tg = dev(scores), dev(go)
+    a = fg.edge_softmax(G, ts, leaky=leaky, slope=0.2, plan=plan)
+    ds = fg.edge_softmax_backward(G, a, tg, scores=ts, leaky=leaky, slope=0.2, plan=plan,
+                                  grad_scores=tg if inplace else None)
+    out = host(ds).reshape(nt, heads)
+    ref, scale = O.edge_softmax_backward(csr, scores.reshape(nt, heads), go.reshape(nt, heads),
+                                         heads=heads, leaky=leaky, slope=0.2, rows=rows,
+                                         nnz_total=nt, with_scale=True)
+    sel = np.arange(csr.num_rows) if rows is None else rows
+    e = edge_ids_of(csr, row_edges(csr, sel))
+    n = np.repeat(csr.degrees()[sel], csr.degrees()[sel])[:, None]
+    bound = 1e-5 * np.sqrt(np.maximum(n, 1)) * scale[e] + 1e-12
+    err = np.abs(out[e].astype(np.float64) - ref[e])
+    bad = err > bound
+    assert not bad.any(), "softmax gradient mismatch at %s: %r vs %r (bound %r)" % (
+        np.argwhere(bad)[0], out[e][bad][0], ref[e][bad][0], bound[bad][0])
+    return ds
+
+
 def plans_for(G, width, sizes=(0, 1, 5, 64)):
     yield None
     for s in sizes:
@@ -258,6 +341,59 @@ def test_gat_fused(small_rmat, heads, dh):
         check_gat(csr, G, x, plan=plan, heads=heads, leaky=False)
 
 
+@pytest.mark.parametrize("d,heads,weighted", [(1, 1, False), (33, 1, False), (128, 1, False),
+                                              (128, 1, True), (48, 8, True), (20, 5, False)])
+def test_max_backward(small_rmat, d, heads, weighted):
+    csr, G = small_rmat
+    rng = np.random.default_rng(d * 10 + heads)
+    x = rng.standard_normal((csr.num_cols, d)).astype(np.float32)
+    go = rng.standard_normal((csr.num_rows, d)).astype(np.float32)
+    xi = rng.integers(-3, 4, (csr.num_cols, d)).astype(np.float32)  # ties
+    gi = rng.integers(-8, 9, (csr.num_rows, d)).astype(np.float32)  # exact sums
+    w = (rng.random((csr.nnz, heads)) + 0.5).astype(np.float32) if weighted else None
+    wi = rng.integers(1, 3, (csr.nnz, heads)).astype(np.float32) if weighted else None
+    for plan in (None, fg.Plan(G, max_width=d, segment_edges=64)):
+        check_max_backward(csr, G, x, go, plan=plan, edge=w, heads=heads, want_edge=weighted)
+        check_max_backward(csr, G, xi, gi, plan=plan, edge=wi, heads=heads, want_edge=weighted,
+                           exact=True)
+
+
+@pytest.mark.parametrize("heads,leaky", [(1, True), (1, False), (8, True), (3, True), (70, False)])
+def test_softmax_backward(small_rmat, heads, leaky):
+    csr, G = small_rmat
+    rng = np.random.default_rng(heads * 3 + leaky)
+    s = (4 * rng.standard_normal((csr.nnz, heads))).astype(np.float32)
+    s[rng.random(s.shape) < 0.02] = 0.0
+    go = rng.standard_normal((csr.nnz, heads)).astype(np.float32)
+    for plan in plans_for(G, heads, sizes=(1, 64)):
+        check_softmax_backward(csr, G, s, go, plan=plan, heads=heads, leaky=leaky)
+    check_softmax_backward(csr, G, s, go, plan=fg.Plan(G, max_width=heads, segment_edges=64),
+                           heads=heads, leaky=leaky, inplace=True)
+
+
+def test_backward_on_transposed_graph(small_rmat):
+    """Max aggregation over out-edges (the CSC with edge ids): the gradient
+    needs the plan's id -> position map; softmax gradient grouped by source."""
+    csr, _ = small_rmat
+    csc = csr_to_csc(csr)
+    Gt = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+    rng = np.random.default_rng(99)
+    x = rng.standard_normal((csc.num_cols, 16)).astype(np.float32)
+    go = rng.standard_normal((csc.num_rows, 16)).astype(np.float32)
+    w = (rng.random((csr.nnz, 2)) + 0.5).astype(np.float32)
+    for seg in (0, 64):
+        plan = fg.Plan(Gt, max_width=16, segment_edges=seg)
+        check_max_backward(csc, Gt, x, go, plan=plan, nnz_total=csr.nnz)
+        check_max_backward(csc, Gt, x, go, plan=plan, edge=w, heads=2, nnz_total=csr.nnz,
+                           want_edge=True)
+        s = (3 * rng.standard_normal((csr.nnz, 2))).astype(np.float32)
+        ge = rng.standard_normal((csr.nnz, 2)).astype(np.float32)
+        check_softmax_backward(csc, Gt, s, ge, plan=plan, heads=2, nnz_total=csr.nnz)
+    with pytest.raises(fg.FgError):  # no plan: no id -> position map
+        fg.gspmm_max_backward(Gt, torch.zeros((csc.num_rows, 16), dtype=torch.int32,
+                                              device="cuda"), dev(go))
+
+
 def test_gat_fused_unsupported_shape_raises(small_rmat):
     csr, G = small_rmat
     x = dev(np.ones((csr.num_cols, 3, 12), np.float32))
@@ -317,6 +453,24 @@ def test_edge_cases():
         a = host(fg.edge_softmax(G, dev(np.full(6, 3.0, np.float32)), plan=plan))
         np.testing.assert_allclose(a, [0.2] * 5 + [1.0], rtol=1e-6)
         del s
+        # gradients through duplicate edges and ties: the smallest edge id takes it
+        check_max_backward(dup, G, xi, np.arange(8, dtype=np.float32).reshape(2, 4), plan=plan,
+                           exact=True)
+        check_max_backward(dup, G, xi, np.ones((2, 4), np.float32), plan=plan,
+                           edge=np.array([1, 2, 1, 2, 1, 1], np.float32), want_edge=True,
+                           exact=True)
+        check_softmax_backward(dup, G, np.full(6, 3.0, np.float32),
+                               np.arange(6, dtype=np.float32), plan=plan)
+    # backward without edges: gradients all zero, softmax gradient writes nothing
+    G = fg.Graph.from_csr(noedge)
+    for plan in (None, fg.Plan(G, 8, 4)):
+        gs = fg.gspmm_max_backward(G, torch.full((3, 8), -1, dtype=torch.int32, device="cuda"),
+                                   dev(np.ones((3, 8), np.float32)), plan=plan)
+        assert gs.shape == (5, 8) and np.all(host(gs) == 0)
+        ds = fg.edge_softmax_backward(G, dev(np.zeros(0, np.float32)),
+                                      dev(np.zeros(0, np.float32)),
+                                      scores=dev(np.zeros(0, np.float32)), plan=plan)
+        assert ds.numel() == 0
 
 
 def test_determinism_and_plan_independence(small_rmat):
@@ -400,6 +554,18 @@ def test_rmat_233k_full(rmat_full):
 
 
 @pytest.mark.slow
+def test_rmat_233k_max_backward_full(rmat_full):
+    """GraphSage-max gradient on the whole power-law graph in the benchmark's
+    launch configuration; integer upstream gradients make the sums exact, so
+    the whole [N, 128] gradient must equal the oracle's bit for bit."""
+    w, G = rmat_full
+    csr = w.csr
+    plan = fg.Plan(G, 128)
+    go = np.random.default_rng(8).integers(-8, 9, (csr.num_rows, 128)).astype(np.float32)
+    check_max_backward(csr, G, w.arrays["x"], go, plan=plan, exact=True)
+
+
+@pytest.mark.slow
 def test_clustered_gat_layer_full():
     w = make_config("clustered_133k_deg300")
     csr = w.csr
@@ -415,6 +581,9 @@ def test_clustered_gat_layer_full():
     np.testing.assert_allclose(rs, 1.0, atol=1e-5 * math.sqrt(300))
     # the fused layer on the same graph
     check_gat(csr, G, x, rows=rows, plan=plan, heads=8)
+    # gradient of the softmax (upstream gradient of the attention weights)
+    ga = np.random.default_rng(9).standard_normal((csr.nnz, 8)).astype(np.float32)
+    check_softmax_backward(csr, G, host(s), ga, rows=rows, plan=plan, heads=8)
 
 
 @pytest.mark.slow
