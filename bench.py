@@ -37,7 +37,8 @@ HBM_PEAK_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_rmat_233k_d128.json")
 WORKLOADS = ("rmat_233k_115m", "uniform_deg100_100k", "clustered_133k_deg300",
-             "rmat_1m_33m_train", "tiny_uniform_1k")
+             "rmat_1m_33m_train", "tiny_uniform_1k", "sage_max_train_rmat_233k",
+             "gat_train_clustered_133k")
 
 
 def log(*a):
@@ -64,6 +65,17 @@ def bytes_softmax(n, e, H):
     return 4 * (n + 1) + 8 * e * H
 
 
+def bytes_max_bwd(n, c, F, H=1, weighted=False):
+    # zero-fill the gradient, read arg and grad_out, the picked edge's source
+    # index (and edge value) per element, one atomic read-modify-write
+    return 4 * c * F + 8 * n * F + 4 * n * F + (4 * n * F if weighted else 0) + 8 * n * F
+
+
+def bytes_softmax_bwd(n, e, H, leaky=True):
+    # row pointers, read a, grad_out (and scores), write the score gradient
+    return 4 * (n + 1) + (16 if leaky else 12) * e * H
+
+
 class Op:
     def __init__(self, name, fn, nbytes, flop, graded=False):
         self.name, self.fn, self.bytes, self.flop, self.graded = name, fn, nbytes, flop, graded
@@ -87,7 +99,9 @@ def setup(name, d, args, fg, torch, dev):
     import synth
 
     t0 = time.perf_counter()
-    wl = synth.make_config(name, d=d)
+    base = {"sage_max_train_rmat_233k": "rmat_233k_115m",
+            "gat_train_clustered_133k": "clustered_133k_deg300"}.get(name, name)
+    wl = synth.make_config(base, d=d)
     t_gen = time.perf_counter() - t0
     csr = wl.csr
     n, e = csr.num_rows, csr.nnz
@@ -99,6 +113,14 @@ def setup(name, d, args, fg, torch, dev):
     T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
     cfg = {"workload": name, "num_vertices": n, "num_edges": e}
     plans = []
+    plan_ms = []
+
+    def mkplan(g, **kw):  # plan construction is timed apart from the steps
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        p = fg.Plan(g, **kw)
+        plan_ms.append((time.perf_counter() - t) * 1e3)
+        return p
 
     if name in ("rmat_233k_115m", "tiny_uniform_1k"):
         x_h = wl.arrays["x"]
@@ -106,7 +128,7 @@ def setup(name, d, args, fg, torch, dev):
         w_h = wl.arrays["w"] if "w" in wl.arrays else \
             np.random.default_rng(7).random(e, dtype=np.float32)
         x, wt = T(x_h), T(w_h)
-        P = fg.Plan(G, max_width=F, **popt)
+        P = mkplan(G, max_width=F, **popt)
         plans.append(P)
         out_s, out_m = (torch.empty((n, F), device=dev) for _ in range(2))
         arg = torch.empty((n, F), dtype=torch.int32, device=dev)
@@ -143,7 +165,7 @@ def setup(name, d, args, fg, torch, dev):
         x_h = wl.arrays["x"]
         F = x_h.shape[1]
         x = T(x_h)
-        P = fg.Plan(G, max_width=F, **popt)
+        P = mkplan(G, max_width=F, **popt)
         plans.append(P)
         out_s = torch.empty((n, F), device=dev)
         sc = torch.empty((e,), device=dev)
@@ -170,7 +192,7 @@ def setup(name, d, args, fg, torch, dev):
         H, dh = x_h.shape[1], x_h.shape[2]
         F = H * dh
         x = T(x_h)
-        P = fg.Plan(G, max_width=F, **popt)
+        P = mkplan(G, max_width=F, **popt)
         plans.append(P)
         sc, at = (torch.empty((e, H), device=dev) for _ in range(2))
         out = torch.empty((n, H, dh), device=dev)
@@ -206,14 +228,116 @@ def setup(name, d, args, fg, torch, dev):
             return dt, 4 * ne * F + 4 * ne * H, "%d random rows (%d edges), attention layer" % (
                 rows.size, ne)
 
+    elif name == "sage_max_train_rmat_233k":
+        # GraphSage-style max aggregation, forward and backward (the layer's
+        # dense transform is outside the sparse path)
+        x_h = wl.arrays["x"]
+        F = x_h.shape[1]
+        x = T(x_h)
+        gy_h = np.random.default_rng(11).standard_normal((n, F), dtype=np.float32)
+        gy = T(gy_h)
+        P = mkplan(G, max_width=F, **popt)
+        plans.append(P)
+        out_m = torch.empty((n, F), device=dev)
+        arg = torch.empty((n, F), dtype=torch.int32, device=dev)
+        gx = torch.empty((csr.num_cols, F), device=dev)
+        ops = [
+            Op("spmm_max", lambda: fg.gspmm(G, x, reduce="max", plan=P, out=out_m, arg=arg),
+               bytes_spmm(n, e, F, 1, argmax=True), e * F, graded=True),
+            Op("spmm_max_bwd", lambda: fg.gspmm_max_backward(G, arg, gy, plan=P, grad_src=gx),
+               bytes_max_bwd(n, csr.num_cols, F), n * F),
+        ]
+        cfg.update(feature_dim=F, graph="R-MAT (.57,.19,.19,.05), self-loops removed, relabelled")
+
+        def oracle_sample(edges_target):
+            import oracle
+
+            rows, ne = _row_sample(csr, edges_target / 2, 12345)
+            t0 = time.perf_counter()
+            oracle.gspmm(csr, x_h, red=oracle.RED_MAX, rows=rows)
+            oracle.gspmm_max_backward(csr, x_h, gy_h, rows=rows)
+            dt = time.perf_counter() - t0
+            return dt, ne * F + rows.size * F, (
+                "%d random rows (%d edges), forward max and its gradient" % (rows.size, ne))
+
+    elif name == "gat_train_clustered_133k":
+        # one graph attention layer (8 heads of 16), forward and backward:
+        #   s = X[u].X[v] per head; a = softmax(leaky(s)); Y[v] = sum a X[u]
+        #   dX = A^T-side aggregation of a*dY + both SDDMM operand gradients
+        # (the three parts of dX are separate outputs; summing them is one
+        # elementwise add outside the sparse path)
+        csc = synth.csr_to_csc(csr)
+        Gt = fg.Graph.from_csr(csc, device=dev, nnz_total=e)
+        x_h = wl.arrays["x"]
+        H, dh = x_h.shape[1], x_h.shape[2]
+        F = H * dh
+        x = T(x_h)
+        gy = T(np.random.default_rng(12).standard_normal((n, H, dh), dtype=np.float32))
+        P = mkplan(G, max_width=F, **popt)
+        Pt = mkplan(Gt, max_width=F, **popt)
+        plans += [P, Pt]
+        sc, at, da = (torch.empty((e, H), device=dev) for _ in range(3))
+        y, dx_a, dx_s, dx_d = (torch.empty((n, H, dh), device=dev) for _ in range(4))
+        ops = [
+            Op("sddmm_heads", lambda: fg.gsddmm(G, x, x, plan=P, out=sc),
+               bytes_sddmm(n, e, F, H), 2 * e * F, graded=True),
+            Op("edge_softmax_heads", lambda: fg.edge_softmax(G, sc, leaky=True, slope=0.2,
+                                                             plan=P, out=at),
+               bytes_softmax(n, e, H), 4 * e * H),
+            Op("spmm_score_sum", lambda: fg.gspmm(G, x, at, msg="src_mul_edge", plan=P, out=y),
+               bytes_spmm(n, e, F, H, weighted=True), 2 * e * F, graded=True),
+            Op("bwd_spmm_csc_a", lambda: fg.gspmm(Gt, gy, at, msg="src_mul_edge", plan=Pt,
+                                                  out=dx_a),
+               bytes_spmm(n, e, F, H, weighted=True), 2 * e * F, graded=True),
+            Op("bwd_sddmm_da", lambda: fg.gsddmm(G, x, gy, plan=P, out=da),
+               bytes_sddmm(n, e, F, H), 2 * e * F, graded=True),
+            Op("bwd_edge_softmax", lambda: fg.edge_softmax_backward(
+                G, at, da, scores=sc, leaky=True, slope=0.2, plan=P, grad_scores=da),
+               bytes_softmax_bwd(n, e, H), 4 * e * H),
+            Op("bwd_spmm_csc_ds", lambda: fg.gspmm(Gt, x, da, msg="src_mul_edge", plan=Pt,
+                                                   out=dx_s),
+               bytes_spmm(n, e, F, H, weighted=True), 2 * e * F, graded=True),
+            Op("bwd_spmm_csr_ds", lambda: fg.gspmm(G, x, da, msg="src_mul_edge", plan=P,
+                                                   out=dx_d),
+               bytes_spmm(n, e, F, H, weighted=True), 2 * e * F, graded=True),
+        ]
+        cfg.update(feature_dim=F, heads=H, head_dim=dh,
+                   graph="100 communities, in-degree 300 (270 inside, 30 uniform), CSR + CSC")
+
+        def oracle_sample(edges_target):
+            import oracle
+
+            rows, ne = _row_sample(csr, edges_target / 8, 12345)
+            rows_b, ne_b = _row_sample(csc, edges_target / 8, 54321)
+            x2 = x_h.reshape(n, F)
+            g2 = gy.cpu().numpy().reshape(n, F)
+            t0 = time.perf_counter()
+            s = oracle.gsddmm(csr, x2, x2, heads=H, rows=rows)
+            a = oracle.edge_softmax(csr, s, heads=H, leaky=True, slope=0.2, rows=rows)
+            oracle.gspmm(csr, x2, msg=oracle.MSG_SRC_MUL_EDGE, edge_val=a, heads=H, rows=rows)
+            oracle.gspmm(csc, g2, msg=oracle.MSG_SRC_MUL_EDGE, edge_val=a, heads=H, rows=rows_b,
+                         nnz_total=e)
+            ga = oracle.gsddmm(csr, x2, g2, heads=H, rows=rows)
+            ds = oracle.edge_softmax_backward(csr, s, ga, heads=H, leaky=True, slope=0.2,
+                                              rows=rows)
+            oracle.gspmm(csc, x2, msg=oracle.MSG_SRC_MUL_EDGE, edge_val=ds, heads=H,
+                         rows=rows_b, nnz_total=e)
+            oracle.gspmm(csr, x2, msg=oracle.MSG_SRC_MUL_EDGE, edge_val=ds, heads=H, rows=rows)
+            dt = time.perf_counter() - t0
+            # six operators over the CSR rows' edges, two over the CSC rows' edges
+            flop = 8 * F * ne + 8 * H * ne + 4 * F * ne_b
+            return dt, flop, (
+                "%d CSR rows (%d edges) and %d CSC rows (%d edges), all eight operators"
+                % (rows.size, ne, rows_b.size, ne_b))
+
     elif name == "rmat_1m_33m_train":
         csc = wl.csc
         Gb = fg.Graph.from_csr(csc, device=dev, nnz_total=e)
         x_h, dy_h = wl.arrays["x"], wl.arrays["dy"]
         F = x_h.shape[1]
         x, dy = T(x_h), T(dy_h)
-        Pf = fg.Plan(G, max_width=F, **popt)
-        Pb = fg.Plan(Gb, max_width=F, **popt)
+        Pf = mkplan(G, max_width=F, **popt)
+        Pb = mkplan(Gb, max_width=F, **popt)
         plans += [Pf, Pb]
         y, dx = (torch.empty((n, F), device=dev) for _ in range(2))
         da = torch.empty((e,), device=dev)
@@ -247,16 +371,27 @@ def setup(name, d, args, fg, torch, dev):
     cfg.update(segment_edges=pinfo["segment_edges"], max_row_segments=pinfo["max_row_segments"],
                source_slab_rows=pinfo["source_slab_rows"],
                partition_min_degree=pinfo["partition_min_degree"], ops=[o.name for o in ops])
+    cfg["plan_build_ms"] = [round(t, 1) for t in plan_ms]
     return cfg, ops, plans, oracle_sample, e
 
 
-def cpu_baseline(oracle_sample, budget_s):
+def cpu_baseline(oracle_sample, budget_s, threads=0):
     """The oracle, as is, on a random row sample of the workload, repeated
-    until about `budget_s` seconds of host work have been timed."""
+    until about `budget_s` seconds of host work have been timed; `threads`
+    > 0 pins the OpenMP thread count for this measurement."""
     import oracle
 
     oracle.build(force=False)
-    threads = oracle.max_threads()
+    all_threads = oracle.max_threads()
+    if threads > 0:
+        oracle.set_num_threads(threads)
+    try:
+        return _cpu_baseline(oracle_sample, budget_s, oracle.max_threads())
+    finally:
+        oracle.set_num_threads(all_threads)
+
+
+def _cpu_baseline(oracle_sample, budget_s, threads):
     oracle_sample(200_000)  # warm-up: thread pool, page faults
     dt, flop, desc = oracle_sample(2_000_000)
     # size one pass for about a third of the budget (at most the whole graph)
@@ -274,6 +409,24 @@ def cpu_baseline(oracle_sample, budget_s):
 # ----------------------------------------------------------------------------
 # counter calibration and summary
 # ----------------------------------------------------------------------------
+
+
+def copy_bandwidth(torch, nbytes=1 << 30, reps=5):
+    """Attained HBM rate of a plain 1 GiB device copy (read + write bytes per
+    second, median of `reps`): the practical ceiling next to the 8 TB/s peak."""
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for e0, e1 in ev:
+        e0.record()
+        b.copy_(a)
+        e1.record()
+    torch.cuda.synchronize()
+    t = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev])) / 1e3
+    del a, b
+    return round(2 * nbytes / t / 1e9, 1)
 
 
 def copy_probe(nbytes=1 << 30, reps=4):
@@ -380,7 +533,12 @@ def main():
                     help="smallest row cut at slab boundaries (0: default)")
     ap.add_argument("--fused", action="store_true",
                     help="attention workload: one fused kernel instead of three operators")
+    ap.add_argument("--cold", action="store_true",
+                    help="overwrite a 1 GiB buffer before every operator (caches hold no "
+                         "inputs); the rate then comes from the operators' event times")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-1thread-budget", type=float, default=4.0,
+                    help="seconds of single-thread oracle work (0: skip)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration) and exit")
@@ -420,16 +578,23 @@ def main():
     K = args.steps
     ev = {op.name: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                     for _ in range(K)] for op in ops}
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev) if args.cold else None
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(K):
         for op in ops:
             a, b = ev[op.name][k]
+            if flush is not None:
+                flush.fill_(float(k))
             a.record()
             op.fn()
             b.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    if flush is not None:  # the flushes are not part of the work
+        del flush
+        elapsed = sum(a.elapsed_time(b) for op in ops for a, b in ev[op.name]) / 1e3
+        cfg["cold"] = True
 
     per_op = {}
     for op in ops:
@@ -480,9 +645,14 @@ def main():
                  "slots": pinfo["num_slots"],
                  "partitioned_rows": pinfo["num_partitioned_rows"]},
     }
+    result["hbm_copy_gbs"] = copy_bandwidth(torch)
     if not args.no_cpu_baseline:
         log("timing the oracle on a row sample")
         result["cpu_baseline"] = cpu_baseline(oracle_sample, args.cpu_budget)
+        if args.cpu_1thread_budget > 0:
+            log("timing the oracle on one thread")
+            result["cpu_baseline_1thread"] = cpu_baseline(oracle_sample,
+                                                          args.cpu_1thread_budget, threads=1)
     for p in plans:
         p.close()
     print(json.dumps(result), flush=True)

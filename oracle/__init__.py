@@ -13,6 +13,7 @@ from .fgref import (  # noqa: F401
     gspmm_max_backward,
     edge_softmax_backward,
     max_threads,
+    set_num_threads,
     MSG_COPY_SRC,
     MSG_SRC_MUL_EDGE,
     RED_SUM,

@@ -384,3 +384,8 @@ FGREF_EXPORT int fgref_edge_softmax_backward(int64_t num_rows, const int32_t* in
 }
 
 FGREF_EXPORT int fgref_max_threads(void) { return omp_get_max_threads(); }
+
+/* Sets the OpenMP thread count used by later calls that pass num_threads = 0. */
+FGREF_EXPORT void fgref_set_num_threads(int n) {
+  if (n > 0) omp_set_num_threads(n);
+}

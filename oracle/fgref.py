@@ -72,6 +72,8 @@ def _load():
               lib.fgref_gspmm_max_backward, lib.fgref_edge_softmax_backward):
         f.restype = ctypes.c_int
     lib.fgref_max_threads.restype = ctypes.c_int
+    lib.fgref_set_num_threads.argtypes = [ctypes.c_int]
+    lib.fgref_set_num_threads.restype = None
     del i32p
     _lib = lib
     return lib
@@ -79,6 +81,11 @@ def _load():
 
 def max_threads() -> int:
     return int(_load().fgref_max_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads for later calls made with threads=0."""
+    _load().fgref_set_num_threads(int(n))
 
 
 def _ptr(a: Optional[np.ndarray]):

@@ -1346,6 +1346,36 @@ __global__ __launch_bounds__(kBlock) void spmm_max_bwd_kernel(MaxBwdParams p) {
   }
 }
 
+// float4 k of a contiguous row's flat range of an [E, H] array; elements
+// outside the range read as `fill` / are not written.
+__device__ __forceinline__ void flat_load4(const float* base, const ContigRange& r, int64_t k,
+                                           float (&v)[4], float fill) {
+  const int64_t t0 = r.T0 + 4 * k;
+  if (t0 >= r.lo && t0 + 4 <= r.hi) {
+    load_vec<4>(base + t0, v);
+  } else {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int64_t t = t0 + c;
+      v[c] = (t >= r.lo && t < r.hi) ? base[t] : fill;
+    }
+  }
+}
+
+__device__ __forceinline__ void flat_store4(float* base, const ContigRange& r, int64_t k,
+                                            const float (&v)[4]) {
+  const int64_t t0 = r.T0 + 4 * k;
+  if (t0 >= r.lo && t0 + 4 <= r.hi) {
+    store_vec<4>(base + t0, v);
+  } else {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int64_t t = t0 + c;
+      if (t >= r.lo && t < r.hi) base[t] = v[c];
+    }
+  }
+}
+
 struct SoftmaxBwdParams {
   const int32_t* indptr;
   const int32_t* eids;
@@ -1362,7 +1392,80 @@ struct SoftmaxBwdParams {
   int32_t H;
   int32_t leaky;
   float slope;
+  int32_t contig;  // edge id == position, H a power of two <= 64, 16-byte aligned arrays
 };
+
+// ---- contiguous rows (same lane layout as the forward's float4 path: slot c
+// of every float4 a lane touches holds one fixed head)
+
+// Pass 2 over a range: ds = a * (go - c) * leaky factor, c per slot.
+__device__ __forceinline__ void softmax_bwd_contig_apply(const SoftmaxBwdParams& p,
+                                                         const ContigRange& r,
+                                                         const float (&c)[4]) {
+  const int lane = lane_id();
+  for (int64_t k0 = lane; k0 < r.K; k0 += 4 * kWave) {
+    float a[4][4], g[4][4], sv[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t k = k0 + (int64_t)kWave * i;
+      if (k < r.K) {
+        flat_load4(p.a, r, k, a[i], 0.0f);
+        flat_load4(p.go, r, k, g[i], 0.0f);
+        if (p.leaky) flat_load4(p.s, r, k, sv[i], 1.0f);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t k = k0 + (int64_t)kWave * i;
+      if (k < r.K) {
+        float o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          o[q] = a[i][q] * (g[i][q] - c[q]);
+          if (p.leaky && !(sv[i][q] > 0.0f)) o[q] *= p.slope;
+        }
+        flat_store4(p.ds, r, k, o);
+      }
+    }
+  }
+}
+
+// Pass 1 (sum of a * go per head, four float4 pairs in flight per lane), then
+// pass 2 for a whole row, or the partial sums published for a split row.
+__device__ __forceinline__ void softmax_bwd_contig(const SoftmaxBwdParams& p, const Item& it) {
+  const int lane = lane_id();
+  const int H = p.H;
+  const ContigRange r = contig_range(it.b, it.e, H);
+  float c[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int64_t k0 = lane; k0 < r.K; k0 += 4 * kWave) {
+    float a[4][4], g[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t k = k0 + (int64_t)kWave * i;
+      if (k < r.K) {
+        flat_load4(p.a, r, k, a[i], 0.0f);
+        flat_load4(p.go, r, k, g[i], 0.0f);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) a[i][q] = g[i][q] = 0.0f;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) c[q] = fmaf(a[i][q], g[i][q], c[q]);
+  }
+  contig_allsum(c, H);
+  if (it.slot >= 0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool pub = H >= 4 ? lane < H / 4 : (lane == 0 && q < H);
+      if (pub) p.ws[(int64_t)it.slot * H + contig_head(r, lane, q, H)] = c[q];
+    }
+    return;
+  }
+  softmax_bwd_contig_apply(p, r, c);
+}
 
 // ds_e = a_e * (go_e - c) * (leaky && s_e <= 0 ? slope : 1), c = sum_row a go.
 __device__ __forceinline__ void softmax_bwd_write(const SoftmaxBwdParams& p, int64_t b,
@@ -1400,6 +1503,11 @@ __global__ __launch_bounds__(kBlock) void softmax_bwd_kernel(SoftmaxBwdParams p)
   if (it.row < 0 || it.b >= it.e) return;
   const int lane = lane_id();
   const int H = p.H;
+  // float4 lanes once a row fills the wavefront or has >= 4 heads
+  if (p.contig && (H >= 4 || (it.e - it.b) * H > (int64_t)kWave * kSoftmaxU)) {
+    softmax_bwd_contig(p, it);
+    return;
+  }
   for (int h0 = 0; h0 < H; h0 += kWave) {
     const int hc = min(H - h0, kWave);
     const int epw = kWave / hc;
@@ -1450,6 +1558,18 @@ __global__ __launch_bounds__(kBlock) void softmax_bwd_split_kernel(SoftmaxBwdPar
   const Fix fx = p.fix[p.slot_fix[slot]];
   const int lane = lane_id();
   const int H = p.H;
+  if (p.contig) {
+    const ContigRange r = contig_range(sg.begin, sg.end, H);
+    float c[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int h = contig_head(r, lane, q, H);
+      c[q] = 0.0f;
+      for (int t = fx.slot_begin; t < fx.slot_end; ++t) c[q] += p.ws[(int64_t)t * H + h];
+    }
+    softmax_bwd_contig_apply(p, r, c);
+    return;
+  }
   for (int h0 = 0; h0 < H; h0 += kWave) {
     const int hc = min(H - h0, kWave);
     const int epw = kWave / hc;
@@ -2007,6 +2127,8 @@ hipError_t launch_edge_softmax_backward(const GraphView& g, const PlanView* plan
   prm.H = (int32_t)H;
   prm.leaky = leaky ? 1 : 0;
   prm.slope = slope;
+  prm.contig = (g.edge_ids == nullptr && H <= kWave && (H & (H - 1)) == 0 && aligned16(a) &&
+                aligned16(go) && aligned16(ds) && (!leaky || aligned16(scores))) ? 1 : 0;
   const dim3 grid = grid_for(prm.n_items, 1);
   if (plan) FG_LAUNCH((softmax_bwd_kernel<true>), grid, stream, prm);
   else FG_LAUNCH((softmax_bwd_kernel<false>), grid, stream, prm);
