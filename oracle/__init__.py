@@ -12,6 +12,8 @@ from .fgref import (  # noqa: F401
     edge_softmax,
     gspmm_max_backward,
     edge_softmax_backward,
+    mlp_aggregate,
+    dense_matmul,
     max_threads,
     set_num_threads,
     MSG_COPY_SRC,

@@ -383,6 +383,62 @@ FGREF_EXPORT int fgref_edge_softmax_backward(int64_t num_rows, const int32_t* in
   return bad ? -2 : 0;
 }
 
+/*
+ * MLP aggregation (Fig. 1, with the message function of Fig. 3b): for every
+ * stored edge (v <- u) with id e and every output feature i,
+ *   m_e[i] = relu( sum_k (Xs[u, k] + Xd[v, k]) * W[k, i] ),  relu(t) = t > 0 ? t : 0
+ * evaluated in fp64 (Xs [num_cols, d_in], Xd [num_rows, d_in], W [d_in, d_out]),
+ * and the destination keeps the maximum message:
+ *   out[v, i] = (float) max_e m_e[i],  arg[v, i] = the smallest edge id attaining it
+ * (empty row -> out 0, arg -1).  scale (optional) receives
+ * sum_k |Xs[u, k] + Xd[v, k]| * |W[k, i]| of the selected edge, the size of the
+ * terms its message is formed from.
+ */
+FGREF_EXPORT int fgref_mlp_aggregate(int64_t num_rows, int64_t num_cols, const int32_t* indptr,
+                                     const int32_t* indices, const int32_t* edge_ids,
+                                     int64_t nnz_total, int64_t d_in, int64_t d_out,
+                                     const float* xs, const float* xd, const float* w,
+                                     const int64_t* rows, int64_t num_sel, float* out,
+                                     int32_t* arg, double* scale, int num_threads) {
+  if (d_in < 1 || d_out < 1 || num_rows < 0 || num_cols < 0 || !indptr || !xs || !xd || !w ||
+      !out || !arg)
+    return -1;
+  if (!rows && num_sel != num_rows) return -1;
+  if (check_rows(rows, num_sel, num_rows)) return -1;
+  set_threads(num_threads);
+  int bad = 0;
+
+#pragma omp parallel for schedule(dynamic, 16) reduction(| : bad)
+  for (int64_t s = 0; s < num_sel; ++s) {
+    const int64_t v = pick_row(rows, s);
+    for (int64_t i = 0; i < d_out; ++i) {
+      double best = 0.0, best_scale = 0.0;
+      int32_t best_e = -1;
+      for (int64_t p = indptr[v]; p < indptr[v + 1]; ++p) {
+        const int64_t u = indices[p];
+        const int64_t e = edge_ids ? edge_ids[p] : p;
+        if (u < 0 || u >= num_cols || e < 0 || e >= nnz_total) { bad |= 1; continue; }
+        double t = 0.0, sc = 0.0;
+        for (int64_t k = 0; k < d_in; ++k) {
+          const double h = (double)xs[u * d_in + k] + (double)xd[v * d_in + k];
+          t += h * (double)w[k * d_out + i];
+          sc += fabs(h) * fabs((double)w[k * d_out + i]);
+        }
+        const double m = t > 0.0 ? t : 0.0;
+        if (best_e == -1 || m > best || (m == best && e < best_e)) {
+          best = m;
+          best_e = (int32_t)e;
+          best_scale = sc;
+        }
+      }
+      out[s * d_out + i] = best_e == -1 ? 0.0f : (float)best;
+      arg[s * d_out + i] = best_e;
+      if (scale) scale[s * d_out + i] = best_scale;
+    }
+  }
+  return bad ? -2 : 0;
+}
+
 FGREF_EXPORT int fgref_max_threads(void) { return omp_get_max_threads(); }
 
 /* Sets the OpenMP thread count used by later calls that pass num_threads = 0. */

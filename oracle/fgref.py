@@ -72,6 +72,9 @@ def _load():
               lib.fgref_gspmm_max_backward, lib.fgref_edge_softmax_backward):
         f.restype = ctypes.c_int
     lib.fgref_max_threads.restype = ctypes.c_int
+    lib.fgref_mlp_aggregate.argtypes = [i64, i64, vp, vp, vp, i64, i64, i64, vp, vp, vp, vp, i64,
+                                        vp, vp, vp, ctypes.c_int]
+    lib.fgref_mlp_aggregate.restype = ctypes.c_int
     lib.fgref_set_num_threads.argtypes = [ctypes.c_int]
     lib.fgref_set_num_threads.restype = None
     del i32p
@@ -248,3 +251,31 @@ def edge_softmax_backward(g, scores: np.ndarray, grad_out: np.ndarray, heads: in
     if rc != 0:
         raise ValueError("fgref_edge_softmax_backward failed (%d)" % rc)
     return (out, sc) if with_scale else out
+
+
+def mlp_aggregate(g, xs: np.ndarray, xd: np.ndarray, w: np.ndarray,
+                  rows: Optional[Sequence[int]] = None, nnz_total: Optional[int] = None,
+                  with_scale: bool = False, threads: int = 0):
+    """MLP aggregation: returns out [sel, d_out], arg [sel, d_out] (, scale)."""
+    lib = _load()
+    indptr, indices, eids = _graph_args(g)
+    w = _c(w, np.float32)
+    d_in, d_out = w.shape
+    xs = _c(xs, np.float32).reshape(g.num_cols, d_in)
+    xd = _c(xd, np.float32).reshape(g.num_rows, d_in)
+    nt = int(indptr[-1]) if nnz_total is None else nnz_total
+    r, nsel = _rows_arg(rows, g.num_rows)
+    out = np.empty((nsel, d_out), np.float32)
+    arg = np.empty((nsel, d_out), np.int32)
+    sc = np.empty((nsel, d_out), np.float64) if with_scale else None
+    rc = lib.fgref_mlp_aggregate(g.num_rows, g.num_cols, _ptr(indptr), _ptr(indices), _ptr(eids),
+                                 nt, d_in, d_out, _ptr(xs), _ptr(xd), _ptr(w), _ptr(r), nsel,
+                                 _ptr(out), _ptr(arg), _ptr(sc), threads)
+    if rc != 0:
+        raise ValueError("fgref_mlp_aggregate failed (%d)" % rc)
+    return (out, arg, sc) if with_scale else (out, arg)
+
+
+def dense_matmul(x: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """Y = X W in fp64 (numpy's matmul): the dense vertex transform."""
+    return np.asarray(x, np.float64) @ np.asarray(w, np.float64)

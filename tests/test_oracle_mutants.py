@@ -48,6 +48,12 @@ MUTANTS = [
      "grad_scores[e * H + h] = (float)(a * (g - c));"),
     ("softmax_bwd_centre_unweighted", "c += a * (double)grad_out[e * H + h];",
      "c += (double)grad_out[e * H + h];"),
+    ("mlp_dst_feature_dropped", "const double h = (double)xs[u * d_in + k] + (double)xd[v * d_in + k];",
+     "const double h = (double)xs[u * d_in + k];"),
+    ("mlp_weight_transposed", "w[k * d_out + i]", "w[i * d_in + k]", "all"),
+    ("mlp_relu_dropped", "const double m = t > 0.0 ? t : 0.0;", "const double m = t;"),
+    ("mlp_tie_to_largest_id", "(m == best && e < best_e)) {\n          best = m;\n          best_e = (int32_t)e;\n          best_scale",
+     "(m == best && e > best_e)) {\n          best = m;\n          best_e = (int32_t)e;\n          best_scale"),
     ("softmax_off_normaliser", "out[e * H + h] = (float)(exp(s - m) / z);", "out[e * H + h] = (float)(exp(s - m) / (z + 1e-3));"),
 ]
 

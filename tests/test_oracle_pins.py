@@ -555,3 +555,85 @@ def test_backward_invalid_arguments_rejected(O):
     dup = CSR(g.num_rows, g.num_cols, g.indptr, g.indices, np.zeros(g.nnz, np.int32))
     with pytest.raises(ValueError):
         O.gspmm_max_backward(dup, x, go, nnz_total=g.nnz)  # edge ids not distinct
+
+
+# ---------------------------------------------------------------- MLP aggregation
+
+
+def test_golden_mlp_aggregate(O):
+    gd, g = _golden_graph()
+    x = np.array(gd["x"], np.float32)
+    m = gd["mlp_aggregate"]
+    out, arg = O.mlp_aggregate(g, x, x, np.array(m["w"], np.float32))
+    np.testing.assert_array_equal(out, np.array(m["value"]))
+    np.testing.assert_array_equal(arg, np.array(m["arg"]))
+
+
+def _mlp_brute(g, xs, xd, w):
+    """Every message materialised with numpy (fp64 matmul), laid out per row by
+    increasing edge id, max by numpy's argmax (first of equal maxima)."""
+    eids = _eids(g)
+    rows = csr_rows(g)
+    msg = np.maximum((xs[g.indices].astype(np.float64) + xd[rows].astype(np.float64))
+                     @ w.astype(np.float64), 0.0)
+    D = max(int(g.degrees().max()), 1)
+    order = np.lexsort((eids, rows))
+    slot = np.arange(g.nnz) - g.indptr[rows[order]]
+    pad = np.full((g.num_rows, D, w.shape[1]), -np.inf)
+    ide = np.full((g.num_rows, D), -1, np.int64)
+    pad[rows[order], slot] = msg[order]
+    ide[rows[order], slot] = eids[order]
+    k = np.argmax(pad, axis=1)
+    out = np.take_along_axis(pad, k[:, None, :], 1)[:, 0, :]
+    arg = np.take_along_axis(ide, k, 1)
+    empty = g.degrees() == 0
+    out[empty] = 0.0
+    arg[empty] = -1
+    return out, arg
+
+
+@pytest.mark.parametrize("d_in,d_out,transpose", [(8, 16, False), (3, 5, False), (8, 7, True)])
+def test_mlp_aggregate_brute_force(O, d_in, d_out, transpose):
+    g = _rand_graph(91, n_rows=150, n_cols=130, e=2500, empty_frac=0.15)
+    nnz_total = g.nnz
+    if transpose:
+        g = csr_to_csc(g)
+    rng = np.random.default_rng(92)
+    xs = rng.standard_normal((g.num_cols, d_in)).astype(np.float32)
+    xd = rng.standard_normal((g.num_rows, d_in)).astype(np.float32)
+    w = rng.standard_normal((d_in, d_out)).astype(np.float32)
+    out, arg = O.mlp_aggregate(g, xs, xd, w, nnz_total=nnz_total)
+    ref, rarg = _mlp_brute(g, xs, xd, w)
+    np.testing.assert_allclose(out, ref, rtol=1e-6, atol=0)
+    np.testing.assert_array_equal(arg, rarg)  # ties only at exact zeros (ReLU)
+    assert (out == 0).any() and (arg[g.degrees() > 0] >= 0).all()
+
+
+def test_mlp_aggregate_identity_weight_is_shifted_max(O):
+    """W = I: m_e = relu(x_u + x_v), so out[v] = relu(max_u x_u + x_v) with the
+    gSpMM-max edge where that is positive."""
+    g = _rand_graph(93, n_rows=200, e=3000, empty_frac=0.1)
+    rng = np.random.default_rng(94)
+    x = rng.standard_normal((g.num_cols, 6)).astype(np.float32)
+    out, arg = O.mlp_aggregate(g, x, x[: g.num_rows], np.eye(6, dtype=np.float32))
+    mx, marg = O.gspmm(g, x, red=O.RED_MAX)
+    shifted = mx.astype(np.float64) + x[: g.num_rows].astype(np.float64)
+    ne = (g.degrees() > 0)[:, None]
+    np.testing.assert_array_equal(out, np.where(ne, np.maximum(shifted, 0), 0).astype(np.float32))
+    pos = ne & (shifted > 0)
+    np.testing.assert_array_equal(arg[pos], marg[pos])
+
+
+def test_mlp_aggregate_homogeneous_and_threads(O):
+    g = _rand_graph(95, n_rows=120, e=2000)
+    rng = np.random.default_rng(96)
+    x = rng.standard_normal((g.num_cols, 8)).astype(np.float32)
+    w = rng.standard_normal((8, 12)).astype(np.float32)
+    o1, a1 = O.mlp_aggregate(g, x, x[: g.num_rows], w, threads=1)
+    o2, a2 = O.mlp_aggregate(g, x, x[: g.num_rows], 2 * w, threads=8)
+    np.testing.assert_array_equal(o2, 2 * o1)  # relu is positively homogeneous
+    np.testing.assert_array_equal(a2, a1)
+    rows = np.array([0, 5, 17, 119])
+    o3, a3 = O.mlp_aggregate(g, x, x[: g.num_rows], w, rows=rows)
+    np.testing.assert_array_equal(o3, o1[rows])
+    np.testing.assert_array_equal(a3, a1[rows])
