@@ -12,6 +12,8 @@
  *   backward of gSpMM-max and of edge softmax (training; the backward of
  *                       gSpMM-sum and gSDDMM are themselves gSDDMM and gSpMM
  *                       calls, Sec. II-A)
+ *   MLP aggregation    (Fig. 1 / Fig. 3b: a dense vertex transform on the
+ *                       matrix cores, then a gSpMM with a relu(u + v) message)
  *
  * The paper's user-defined message / edge functions become a closed set of
  * operators (the builtin message functions it supports, Sec. III-B): copy the
@@ -285,6 +287,40 @@ fg_status fg_edge_softmax_backward(const fg_graph* g, int32_t num_heads, const f
                                    const float* grad_out, const float* scores,
                                    int32_t apply_leaky_relu, float negative_slope,
                                    float* grad_scores, fg_plan* plan, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Dense vertex transform y = x w (fp32 on the matrix cores): the vector-matrix
+ * product of the MLP aggregation's message function (Fig. 3b), applied once
+ * per vertex.  x [n, d_in], w [d_in, d_out], y [n, d_out] row-major; y must
+ * not overlap x or w.  fp32 products and sums (order fixed by the kernel).
+ * ------------------------------------------------------------------------- */
+fg_status fg_dense_matmul(int64_t n, int64_t d_in, int64_t d_out, const float* x, const float* w,
+                          float* y, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * MLP aggregation (Fig. 1, message function of Fig. 3b) with the max
+ * aggregator:
+ *   out[v, i]     = max over stored edges (u -> v, id e) of
+ *                   relu( sum_k (x_src[u, k] + x_dst[v, k]) * weight[k, i] )
+ *   arg_eid[v, i] = the smallest edge id attaining it;  empty row -> 0 / -1
+ * where relu(t) = t > 0 ? t : 0.  Computed as P_src = x_src weight and
+ * P_dst = x_dst weight (fg_dense_matmul) followed by a gSpMM whose message is
+ * relu(P_src[u] + P_dst[v]): equal to the per-edge form in exact arithmetic
+ * (the product distributes over the sum), without d_in * d_out multiply-adds
+ * per edge.  Rounding differs from the per-edge form, and so may the argmax
+ * between messages closer than that rounding.
+ * x_src     [num_cols, d_in];  x_dst [num_rows, d_in] (may be x_src itself
+ *           when num_rows == num_cols: one transform);  weight [d_in, d_out]
+ * out, arg_eid [num_rows, d_out]
+ * workspace caller-owned device scratch of (num_cols + num_rows) * d_out
+ *           floats (16-byte aligned for the vector path); clobbered
+ * plan      as for fg_gspmm, with max_width >= d_out
+ * Nothing is allocated; calls sharing a workspace must be ordered on one
+ * stream.
+ * ------------------------------------------------------------------------- */
+fg_status fg_mlp_aggregate(const fg_graph* g, int64_t d_in, int64_t d_out, const float* x_src,
+                           const float* x_dst, const float* weight, float* out, int32_t* arg_eid,
+                           float* workspace, fg_plan* plan, void* stream);
 
 const char* fg_status_string(fg_status s); /* static storage, never NULL */
 int32_t fg_abi_version(void);              /* == FG_ABI_VERSION */

@@ -120,6 +120,10 @@ def _load():
                                           vp]
     lib.fg_edge_softmax_backward.restype = ctypes.c_int
     lib.fg_edge_softmax_backward.argtypes = [gp, i32, vp, vp, vp, i32, ctypes.c_float, vp, vp, vp]
+    lib.fg_dense_matmul.restype = ctypes.c_int
+    lib.fg_dense_matmul.argtypes = [i64, i64, i64, vp, vp, vp, vp]
+    lib.fg_mlp_aggregate.restype = ctypes.c_int
+    lib.fg_mlp_aggregate.argtypes = [gp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp]
     if lib.fg_abi_version() != ABI_VERSION:
         raise ImportError("ABI version mismatch: library %d, binding %d"
                           % (lib.fg_abi_version(), ABI_VERSION))
@@ -538,6 +542,63 @@ def edge_softmax_backward(g: Graph, out: torch.Tensor, grad_out: torch.Tensor,
     return grad_scores
 
 
+# ----------------------------------------------------------------------------
+# MLP aggregation
+# ----------------------------------------------------------------------------
+
+
+def dense_matmul(x: torch.Tensor, w: torch.Tensor, out: Optional[torch.Tensor] = None):
+    """y = x w on the matrix cores: x [n, d_in], w [d_in, d_out] fp32."""
+    x = _dev_tensor(x, torch.float32, "x")
+    w = _dev_tensor(w, torch.float32, "w")
+    if x.dim() != 2 or w.dim() != 2 or x.shape[1] != w.shape[0]:
+        raise ValueError("x must be [n, d_in] and w [d_in, d_out]")
+    n, d_in = x.shape
+    d_out = w.shape[1]
+    out = torch.empty((n, d_out), dtype=torch.float32, device=x.device) if out is None else \
+        _dev_tensor(out, torch.float32, "out")
+    if out.numel() != n * d_out:
+        raise ValueError("out has the wrong size")
+    _check(_lib.fg_dense_matmul(n, d_in, d_out, _ptr(x), _ptr(w), _ptr(out), _stream()),
+           "fg_dense_matmul")
+    return out
+
+
+def mlp_aggregate(g: Graph, x_src: torch.Tensor, weight: torch.Tensor,
+                  x_dst: Optional[torch.Tensor] = None, plan: Optional[Plan] = None,
+                  out: Optional[torch.Tensor] = None, arg: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None):
+    """MLP aggregation: out[v, i] = max over in-edges of relu(((x_src[u] +
+    x_dst[v]) weight)[i]) and the edge id of each maximum.  x_dst defaults to
+    x_src (square graphs).  workspace: (num_cols + num_rows) * d_out floats
+    of scratch, allocated here when not given."""
+    x_src = _dev_tensor(x_src, torch.float32, "x_src")
+    x_dst = x_src if x_dst is None else _dev_tensor(x_dst, torch.float32, "x_dst")
+    weight = _dev_tensor(weight, torch.float32, "weight")
+    if weight.dim() != 2:
+        raise ValueError("weight must be [d_in, d_out]")
+    d_in, d_out = weight.shape
+    if x_src.shape != (g.num_cols, d_in) or x_dst.shape != (g.num_rows, d_in):
+        raise ValueError("x_src must be [num_cols, d_in] and x_dst [num_rows, d_in]")
+    dev = x_src.device
+    out = torch.empty((g.num_rows, d_out), dtype=torch.float32, device=dev) if out is None else \
+        _dev_tensor(out, torch.float32, "out")
+    arg = torch.empty((g.num_rows, d_out), dtype=torch.int32, device=dev) if arg is None else \
+        _dev_tensor(arg, torch.int32, "arg")
+    if out.numel() != g.num_rows * d_out or arg.numel() != g.num_rows * d_out:
+        raise ValueError("out / arg have the wrong size")
+    nws = (g.num_cols + g.num_rows) * d_out
+    workspace = torch.empty(max(nws, 1), dtype=torch.float32, device=dev) if workspace is None \
+        else _dev_tensor(workspace, torch.float32, "workspace")
+    if workspace.numel() < nws:
+        raise ValueError("workspace needs (num_cols + num_rows) * d_out floats")
+    st = _lib.fg_mlp_aggregate(ctypes.byref(g._c), d_in, d_out, _ptr(x_src), _ptr(x_dst),
+                               _ptr(weight), _ptr(out), _ptr(arg), _ptr(workspace),
+                               _plan_handle(plan), _stream())
+    _check(st, "fg_mlp_aggregate")
+    return out, arg
+
+
 __all__ = ["Graph", "Plan", "gspmm", "gsddmm", "edge_softmax", "gat_aggregate",
-           "gspmm_max_backward", "edge_softmax_backward", "schedule_host", "FgError",
-           "status_string", "LIB_PATH"]
+           "gspmm_max_backward", "edge_softmax_backward", "dense_matmul", "mlp_aggregate",
+           "schedule_host", "FgError", "status_string", "LIB_PATH"]

@@ -688,4 +688,48 @@ fg_status fg_edge_softmax_backward(const fg_graph* g, int32_t num_heads, const f
       static_cast<hipStream_t>(stream)));
 }
 
+fg_status fg_dense_matmul(int64_t n, int64_t d_in, int64_t d_out, const float* x, const float* w,
+                          float* y, void* stream) {
+  if (n < 0 || n > INT32_MAX || d_in < 1 || d_out < 1 || d_in > FG_MAX_WIDTH ||
+      d_out > FG_MAX_WIDTH)
+    return FG_ERR_INVALID_ARG;
+  if (n > 0 && (!x || !w || !y)) return FG_ERR_INVALID_ARG;
+  const int64_t yb = n * d_out * 4;
+  if (overlaps(y, yb, x, n * d_in * 4) || overlaps(y, yb, w, d_in * d_out * 4))
+    return FG_ERR_INVALID_ARG;
+  return from_hip(
+      fg::launch_dense_matmul(n, d_in, d_out, x, w, y, static_cast<hipStream_t>(stream)));
+}
+
+fg_status fg_mlp_aggregate(const fg_graph* g, int64_t d_in, int64_t d_out, const float* x_src,
+                           const float* x_dst, const float* weight, float* out, int32_t* arg_eid,
+                           float* workspace, fg_plan* plan, void* stream) {
+  fg_status st = check_graph(g);
+  if (st != FG_OK) return st;
+  if (d_in < 1 || d_out < 1 || d_in > FG_MAX_WIDTH || d_out > FG_MAX_WIDTH)
+    return FG_ERR_INVALID_ARG;
+  if (g->num_rows > 0 && (!out || !arg_eid)) return FG_ERR_INVALID_ARG;
+  if ((g->num_rows > 0 || g->num_cols > 0) && (!x_src || !x_dst || !weight || !workspace))
+    return FG_ERR_INVALID_ARG;
+  if (x_dst == x_src && g->num_rows != g->num_cols) return FG_ERR_INVALID_ARG;
+  if ((st = check_plan(plan, g, d_out)) != FG_OK) return st;
+  const int64_t out_b = g->num_rows * d_out * 4;
+  const int64_t xs_b = g->num_cols * d_in * 4, xd_b = g->num_rows * d_in * 4;
+  const int64_t w_b = d_in * d_out * 4, ws_b = (g->num_cols + g->num_rows) * d_out * 4;
+  for (const auto& o : {std::make_pair((const void*)out, out_b),
+                        std::make_pair((const void*)arg_eid, out_b),
+                        std::make_pair((const void*)workspace, ws_b)}) {
+    if (overlaps(o.first, o.second, x_src, xs_b) || overlaps(o.first, o.second, x_dst, xd_b) ||
+        overlaps(o.first, o.second, weight, w_b))
+      return FG_ERR_INVALID_ARG;
+  }
+  if (overlaps(out, out_b, arg_eid, out_b) || overlaps(out, out_b, workspace, ws_b) ||
+      overlaps(arg_eid, out_b, workspace, ws_b))
+    return FG_ERR_INVALID_ARG;
+  const fg::GraphView gv = view_of(g);
+  return from_hip(fg::launch_mlp_aggregate(gv, plan ? &plan->gather : nullptr, d_in, d_out, x_src,
+                                           x_dst, weight, out, arg_eid, workspace,
+                                           static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -68,6 +68,15 @@ hipError_t launch_edge_softmax_backward(const GraphView& g, const PlanView* plan
 hipError_t launch_build_eid_pos(const int32_t* eids, int64_t nnz, int64_t nnz_total, int32_t* pos,
                                 hipStream_t stream);
 
+// Y[n, M] = X[n, K] W[K, M] (fp32, matrix cores).
+hipError_t launch_dense_matmul(int64_t n, int64_t K, int64_t M, const float* x, const float* w,
+                               float* y, hipStream_t stream);
+// MLP aggregation: P = X W for sources (and destinations) into ws, then a
+// gSpMM with message relu(P_src[u] + P_dst[v]) and max/argmax.
+hipError_t launch_mlp_aggregate(const GraphView& g, const PlanView* plan, int64_t d_in,
+                                int64_t d_out, const float* xs, const float* xd, const float* w,
+                                float* out, int32_t* arg, float* ws, hipStream_t stream);
+
 // Fused SDDMM -> leaky ReLU -> edge softmax -> weighted gSpMM.  Supported
 // shapes: dh % 4 == 0, dh / 4 a power of two, H * dh <= 256; aligned inputs.
 bool gat_fused_supported(int64_t H, int64_t dh);

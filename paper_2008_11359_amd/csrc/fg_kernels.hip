@@ -133,6 +133,7 @@ struct SpmmParams {
   const int32_t* eids;
   const float* x;
   const float* ev;
+  const float* xd;  // destination features of the u_add_v message (ADD kernels only)
   float* out;
   int32_t* arg;
   const Seg* segs;
@@ -196,11 +197,14 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
 // smallest edge id among equal maxima; a group whose messages were all -inf
 // never replaces and takes its first edge afterwards.  Groups, segments and
 // slots are then merged with the full (value, edge id) order.
-template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool SEG>
+// ADD: the message is relu(x[u] + xd[v]) (MLP aggregation with the dense
+// transform applied to the vertices beforehand); requires MAX and !MUL.
+template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool SEG, bool ADD = false>
 __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
   constexpr int NG = kWave / G;
   constexpr bool POS = MAX && !EIDS;
   static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
+  static_assert(!ADD || (MAX && !MUL), "u_add_v messages are max-reduced copies");
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -229,6 +233,16 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
       acc[v][c] = MAX ? -INFINITY : 0.0f;
       am[v][c] = INT_MAX;
     }
+  float pd[NV][4];  // this row's destination features (ADD)
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    if (ADD && act[v]) {
+      load_vec<4>(p.xd + it.row * F + f[v], pd[v]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) pd[v][c] = 0.0f;
+    }
+  }
 
   for (int64_t base = it.b; base < it.e; base += kWave) {
     const int cnt = (int)min((int64_t)kWave, it.e - base);
@@ -260,6 +274,13 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         for (int v = 0; v < NV; ++v) {
           if (ok[u] && act[v]) {
             load_vec<4>(xr + f[v], val[u][v]);
+            if constexpr (ADD) {
+#pragma unroll
+              for (int c = 0; c < 4; ++c) {
+                const float t = val[u][v][c] + pd[v][c];
+                val[u][v][c] = t > 0.0f ? t : 0.0f;
+              }
+            }
             wv[u][v] = (MUL && p.H != 1) ? p.ev[(int64_t)eu[u] * p.H + hv[v]] : w1;
           } else {
 #pragma unroll
@@ -332,8 +353,9 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
 }
 
 // Generic path: any width (scalar lanes), runtime group width G = 2^logG.
-template <int NV, int U, bool MUL, bool MAX, bool SEG>
+template <int NV, int U, bool MUL, bool MAX, bool SEG, bool ADD = false>
 __global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
+  static_assert(!ADD || (MAX && !MUL), "u_add_v messages are max-reduced copies");
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -357,10 +379,12 @@ __global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
   }
   float acc[NV][1];
   int32_t am[NV][1];
+  float pd[NV];
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
     acc[v][0] = MAX ? -INFINITY : 0.0f;
     am[v][0] = INT_MAX;
+    pd[v] = (ADD && act[v]) ? p.xd[it.row * F + f[v]] : 0.0f;
   }
 
   for (int64_t base = it.b; base < it.e; base += kWave) {
@@ -392,6 +416,10 @@ __global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
         for (int v = 0; v < NV; ++v) {
           if (ok[u] && act[v]) {
             val[u][v] = xr[f[v]];
+            if constexpr (ADD) {
+              const float t = val[u][v] + pd[v];
+              val[u][v] = t > 0.0f ? t : 0.0f;
+            }
             wv[u][v] = (MUL && p.H != 1) ? p.ev[(int64_t)eu[u] * p.H + hv[v]] : w1;
           } else {
             val[u][v] = MAX ? -INFINITY : 0.0f;
@@ -1777,23 +1805,25 @@ dim3 grid_for(int64_t items, int64_t chunks) {
 #define FG_LAUNCH(kernel, grid, stream, ...) \
   hipLaunchKernelGGL((kernel), (grid), dim3(kBlock), 0, (stream), __VA_ARGS__)
 
-template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS>
+template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool ADD = false>
 void spmm_fast_seg(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
-  if (seg) FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, true>), grid, st, prm);
-  else FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, false>), grid, st, prm);
+  if (seg) FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, true, ADD>), grid, st, prm);
+  else FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, false, ADD>), grid, st, prm);
 }
 
-template <int G, int NV, int U, bool MUL, bool MAX>
+template <int G, int NV, int U, bool MUL, bool MAX, bool ADD = false>
 void spmm_fast_eids(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
   // copy + sum never looks at edge ids
-  if (prm.eids && (MUL || MAX)) spmm_fast_seg<G, NV, U, MUL, MAX, true>(prm, seg, grid, st);
-  else spmm_fast_seg<G, NV, U, MUL, MAX, false>(prm, seg, grid, st);
+  if (prm.eids && (MUL || MAX)) spmm_fast_seg<G, NV, U, MUL, MAX, true, ADD>(prm, seg, grid, st);
+  else spmm_fast_seg<G, NV, U, MUL, MAX, false, ADD>(prm, seg, grid, st);
 }
 
 template <int G, int NV, int U>
 void spmm_fast_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 grid,
                    hipStream_t st) {
-  if (mul) {
+  if (prm.xd) {
+    spmm_fast_eids<G, NV, U, false, true, true>(prm, seg, grid, st);
+  } else if (mul) {
     if (mx) spmm_fast_eids<G, NV, U, true, true>(prm, seg, grid, st);
     else spmm_fast_eids<G, NV, U, true, false>(prm, seg, grid, st);
   } else {
@@ -1802,16 +1832,18 @@ void spmm_fast_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 grid
   }
 }
 
-template <int NV, int U, bool MUL, bool MAX>
+template <int NV, int U, bool MUL, bool MAX, bool ADD = false>
 void spmm_generic_seg(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
-  if (seg) FG_LAUNCH((spmm_generic_kernel<NV, U, MUL, MAX, true>), grid, st, prm);
-  else FG_LAUNCH((spmm_generic_kernel<NV, U, MUL, MAX, false>), grid, st, prm);
+  if (seg) FG_LAUNCH((spmm_generic_kernel<NV, U, MUL, MAX, true, ADD>), grid, st, prm);
+  else FG_LAUNCH((spmm_generic_kernel<NV, U, MUL, MAX, false, ADD>), grid, st, prm);
 }
 
 template <int NV, int U>
 void spmm_generic_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 grid,
                       hipStream_t st) {
-  if (mul) {
+  if (prm.xd) {
+    spmm_generic_seg<NV, U, false, true, true>(prm, seg, grid, st);
+  } else if (mul) {
     if (mx) spmm_generic_seg<NV, U, true, true>(prm, seg, grid, st);
     else spmm_generic_seg<NV, U, true, false>(prm, seg, grid, st);
   } else {
@@ -1840,22 +1872,26 @@ void sddmm_scalar_go(const SddmmParams& prm, bool seg, dim3 grid, hipStream_t st
 
 }  // namespace
 
-hipError_t launch_gspmm(const GraphView& g, const PlanView* plan, int msg, int red, int64_t H,
-                        int64_t dh, const float* x, const float* ev, float* out, int32_t* arg,
-                        hipStream_t stream) {
+namespace {
+
+// gSpMM launch; xd != null selects the u_add_v + relu message (max only).
+hipError_t launch_spmm_core(const GraphView& g, const PlanView* plan, int msg, int red, int64_t H,
+                            int64_t dh, const float* x, const float* ev, const float* xd,
+                            float* out, int32_t* arg, hipStream_t stream) {
   if (g.num_rows == 0) return hipSuccess;
   const int64_t F = H * dh;
   const bool mul = msg == kSrcMulEdge;
   const bool mx = red == kMax;
   const bool seg = plan != nullptr;
   const bool vec4 = (F % 4 == 0) && (H == 1 || dh % 4 == 0) && aligned16(x) && aligned16(out) &&
-                    (!mx || aligned16(arg));
+                    (!mx || aligned16(arg)) && (!xd || aligned16(xd));
   SpmmParams prm;
   prm.indptr = g.indptr;
   prm.indices = g.indices;
   prm.eids = g.edge_ids;
   prm.x = x;
   prm.ev = ev;
+  prm.xd = xd;
   prm.out = out;
   prm.arg = arg;
   prm.segs = seg ? plan->segs : nullptr;
@@ -1903,6 +1939,83 @@ hipError_t launch_gspmm(const GraphView& g, const PlanView* plan, int msg, int r
     err = hipGetLastError();
   }
   return err;
+}
+
+// Y[n, M] = X[n, K] W[K, M] on the matrix cores (v_mfma_f32_16x16x4_f32,
+// fp32 in and out).  One wavefront per 16-row x 64-column tile of Y, four
+// 16x16 accumulators, K in steps of 4 (zero-padded).  Operand layout of the
+// instruction: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16] and
+// receives D[4 (l / 16) + r][l % 16], r = 0..3.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+constexpr int kMmTileCols = 64;
+
+__global__ __launch_bounds__(kBlock) void dense_matmul_kernel(const float* x, const float* w,
+                                                              float* y, int64_t n, int32_t K,
+                                                              int32_t M, int64_t n_tiles) {
+  const int64_t t = wave_item();
+  if (t >= n_tiles) return;
+  const int64_t col_tiles = (M + kMmTileCols - 1) / kMmTileCols;
+  const int64_t rt = t / col_tiles, ct = t % col_tiles;
+  const int lane = lane_id();
+  const int i = lane & 15, q = lane >> 4;
+  const int64_t arow = rt * 16 + i;
+  f32x4 acc[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) acc[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int k0 = 0; k0 < K; k0 += 4) {
+    const int k = k0 + q;
+    const float a = (arow < n && k < K) ? x[arow * K + k] : 0.0f;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int64_t col = ct * kMmTileCols + b * 16 + i;
+      const float bv = (k < K && col < M) ? w[(int64_t)k * M + col] : 0.0f;
+      acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv, acc[b], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int64_t col = ct * kMmTileCols + b * 16 + i;
+    if (col >= M) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t orow = rt * 16 + q * 4 + r;
+      if (orow < n) y[orow * M + col] = acc[b][r];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gspmm(const GraphView& g, const PlanView* plan, int msg, int red, int64_t H,
+                        int64_t dh, const float* x, const float* ev, float* out, int32_t* arg,
+                        hipStream_t stream) {
+  return launch_spmm_core(g, plan, msg, red, H, dh, x, ev, nullptr, out, arg, stream);
+}
+
+hipError_t launch_dense_matmul(int64_t n, int64_t K, int64_t M, const float* x, const float* w,
+                               float* y, hipStream_t stream) {
+  if (n == 0 || M == 0) return hipSuccess;
+  const int64_t tiles = ((n + 15) / 16) * ((M + kMmTileCols - 1) / kMmTileCols);
+  FG_LAUNCH(dense_matmul_kernel, grid_for(tiles, 1), stream, x, w, y, n, (int32_t)K, (int32_t)M,
+            tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_mlp_aggregate(const GraphView& g, const PlanView* plan, int64_t d_in,
+                                int64_t d_out, const float* xs, const float* xd, const float* w,
+                                float* out, int32_t* arg, float* ws, hipStream_t stream) {
+  // (x_u + x_v) W = x_u W + x_v W: transform the vertices once, then each
+  // edge's message is relu(P_src[u] + P_dst[v])
+  float* ps = ws;
+  float* pd = ws;
+  hipError_t err = launch_dense_matmul(g.num_cols, d_in, d_out, xs, w, ps, stream);
+  if (err != hipSuccess) return err;
+  if (!(xd == xs && g.num_rows == g.num_cols)) {
+    pd = ws + g.num_cols * d_out;
+    if ((err = launch_dense_matmul(g.num_rows, d_in, d_out, xd, w, pd, stream)) != hipSuccess)
+      return err;
+  }
+  return launch_spmm_core(g, plan, kCopySrc, kMax, 1, d_out, ps, nullptr, pd, out, arg, stream);
 }
 
 hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, int64_t dh,

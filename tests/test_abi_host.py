@@ -190,6 +190,41 @@ def test_edge_softmax_backward_rejects_invalid_arguments():
     assert call(ds=GO + 4) == fg.FG_ERR_INVALID_ARG            # partial overlap of grad_out
 
 
+def test_dense_matmul_rejects_invalid_arguments():
+    L = fg._lib
+    X, W, Y = 0x10000, 0x20000, 0x30000
+    assert L.fg_dense_matmul(-1, 8, 8, X, W, Y, None) == fg.FG_ERR_INVALID_ARG
+    assert L.fg_dense_matmul(4, 0, 8, X, W, Y, None) == fg.FG_ERR_INVALID_ARG
+    assert L.fg_dense_matmul(4, 8, 1 << 17, X, W, Y, None) == fg.FG_ERR_INVALID_ARG
+    assert L.fg_dense_matmul(4, 8, 8, None, W, Y, None) == fg.FG_ERR_INVALID_ARG
+    assert L.fg_dense_matmul(4, 8, 8, X, W, X + 16, None) == fg.FG_ERR_INVALID_ARG  # y overlaps x
+    assert L.fg_dense_matmul(0, 8, 8, None, None, None, None) == fg.FG_OK  # nothing to do
+
+
+def test_mlp_aggregate_rejects_invalid_arguments():
+    L = fg._lib
+    g = _graph_struct()
+    XS, XD, W, OUT, ARG, WS = 0x10000, 0x20000, 0x30000, 0x40000, 0x50000, 0x60000
+    ok = dict(di=8, do=16, xs=XS, xd=XD, w=W, out=OUT, arg=ARG, ws=WS)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return L.fg_mlp_aggregate(ctypes.byref(g), a["di"], a["do"], a["xs"], a["xd"], a["w"],
+                                  a["out"], a["arg"], a["ws"], None, None)
+
+    assert call(di=0) == fg.FG_ERR_INVALID_ARG
+    assert call(do=0) == fg.FG_ERR_INVALID_ARG
+    assert call(xs=None) == fg.FG_ERR_INVALID_ARG
+    assert call(w=None) == fg.FG_ERR_INVALID_ARG
+    assert call(arg=None) == fg.FG_ERR_INVALID_ARG
+    assert call(ws=None) == fg.FG_ERR_INVALID_ARG
+    assert call(out=XS + 8) == fg.FG_ERR_INVALID_ARG   # overlaps x_src
+    assert call(ws=OUT + 4) == fg.FG_ERR_INVALID_ARG   # workspace overlaps out
+    g2 = _graph_struct(num_rows=4, num_cols=5)
+    assert L.fg_mlp_aggregate(ctypes.byref(g2), 8, 16, XS, XS, W, OUT, ARG, WS, None, None) == \
+        fg.FG_ERR_INVALID_ARG  # x_dst = x_src needs a square graph
+
+
 def test_plan_create_rejects_invalid_arguments():
     L = fg._lib
     g = _graph_struct()

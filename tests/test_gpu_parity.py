@@ -254,6 +254,65 @@ def check_softmax_backward(csr, G, scores, go, rows=None, plan=None, heads=1, le
     return ds
 
 
+def check_dense_matmul(n, d_in, d_out, seed, exact=False):
+    rng = np.random.default_rng(seed)
+    if exact:
+        x = rng.integers(-4, 5, (n, d_in)).astype(np.float32)
+        w = rng.integers(-4, 5, (d_in, d_out)).astype(np.float32)
+    else:
+        x = rng.standard_normal((n, d_in)).astype(np.float32)
+        w = rng.standard_normal((d_in, d_out)).astype(np.float32)
+    say("dense_matmul n=%d d_in=%d d_out=%d exact=%s" % (n, d_in, d_out, exact))
+    y = host(fg.dense_matmul(dev(x), dev(w)))
+    ref = O.dense_matmul(x, w)
+    if exact:
+        np.testing.assert_array_equal(y, ref)
+    else:
+        tnorm = np.sqrt((x.astype(np.float64) ** 2) @ (w.astype(np.float64) ** 2))
+        assert_close_sum(y, ref, tnorm, d_in)
+
+
+def check_mlp(csr, G, xs, xd, w, rows=None, plan=None, exact=False, square=False):
+    """MLP aggregation vs the oracle's per-edge definition.  Values within the
+    rounding of the two forms; the GPU's edge must attain the oracle's maximum
+    within that tolerance (equal when the maximum is unique by more than it);
+    integer inputs: bit-exact values and edges."""
+    d_in, d_out = w.shape
+    say("mlp_aggregate rows=%d nnz=%d d_in=%d d_out=%d exact=%s plan=%s" % (
+        csr.num_rows, csr.nnz, d_in, d_out, exact,
+        None if plan is None else plan.info()["segment_edges"]))
+    txs = dev(xs)
+    out, arg = fg.mlp_aggregate(G, txs, dev(w), x_dst=txs if square else dev(xd), plan=plan)
+    out, arg = host(out), host(arg)
+    sel = np.arange(csr.num_rows) if rows is None else rows
+    ro, ra = O.mlp_aggregate(csr, xs, xd, w, rows=rows)
+    out, arg = out[sel], arg[sel]
+    if exact:
+        np.testing.assert_array_equal(out, ro)
+        np.testing.assert_array_equal(arg, ra)
+        return
+    deg = csr.degrees()[sel]
+    assert ((arg >= 0) == (deg > 0)[:, None]).all()
+    # the fp64 message of a given edge id for every (row, feature)
+    src = _sources_of_ids(csr, csr.nnz if csr.edge_ids is None else int(csr.edge_ids.max()) + 1)
+    w64 = w.astype(np.float64)
+
+    def msg(eids):
+        e = np.maximum(eids, 0)
+        h = xs[src[e]].astype(np.float64) + xd[sel][:, None, :].astype(np.float64)
+        return np.maximum(np.einsum("rik,ki->ri", h, w64), 0.0), \
+            np.einsum("rik,ki->ri", np.abs(xs[src[e]].astype(np.float64)) +
+                      np.abs(xd[sel][:, None, :].astype(np.float64)), np.abs(w64))
+
+    m_g, _ = msg(arg)
+    _, scale = msg(ra)
+    tol = 1e-5 * math.sqrt(2 * d_in) * np.maximum(np.abs(ro.astype(np.float64)), scale)
+    ne = deg[:, None] > 0
+    assert (np.abs(out.astype(np.float64) - ro) <= tol)[ne[:, 0]].all(), "mlp values differ"
+    assert (m_g >= ro - tol)[ne[:, 0]].all(), "mlp edge does not attain the maximum"
+    np.testing.assert_array_equal(out[~ne[:, 0]], 0)
+
+
 def plans_for(G, width, sizes=(0, 1, 5, 64)):
     yield None
     for s in sizes:
@@ -392,6 +451,44 @@ def test_backward_on_transposed_graph(small_rmat):
     with pytest.raises(fg.FgError):  # no plan: no id -> position map
         fg.gspmm_max_backward(Gt, torch.zeros((csc.num_rows, 16), dtype=torch.int32,
                                               device="cuda"), dev(go))
+
+
+@pytest.mark.parametrize("n,d_in,d_out", [(1, 1, 1), (17, 8, 128), (1000, 8, 33),
+                                           (4099, 3, 64), (333, 130, 70), (2, 8, 512)])
+def test_dense_matmul(n, d_in, d_out):
+    check_dense_matmul(n, d_in, d_out, n + d_in + d_out)
+    check_dense_matmul(n, d_in, d_out, n * 7 + d_out, exact=True)
+
+
+@pytest.mark.parametrize("d_in,d_out", [(8, 32), (8, 128), (8, 512), (8, 6), (3, 20)])
+def test_mlp_aggregate(small_rmat, d_in, d_out):
+    csr, G = small_rmat
+    rng = np.random.default_rng(d_in * 1000 + d_out)
+    x = rng.standard_normal((csr.num_cols, d_in)).astype(np.float32)
+    w = rng.standard_normal((d_in, d_out)).astype(np.float32)
+    xi = rng.integers(-3, 4, (csr.num_cols, d_in)).astype(np.float32)
+    wi = rng.integers(-2, 3, (d_in, d_out)).astype(np.float32)
+    for plan in plans_for(G, d_out, sizes=(64,)):
+        check_mlp(csr, G, x, x, w, plan=plan, square=True)
+        check_mlp(csr, G, xi, xi, wi, plan=plan, square=True, exact=True)
+    xd = rng.standard_normal((csr.num_rows, d_in)).astype(np.float32)
+    check_mlp(csr, G, x, xd, w, plan=fg.Plan(G, d_out, segment_edges=64))
+
+
+def test_mlp_aggregate_transposed_and_empty(small_rmat):
+    csr, _ = small_rmat
+    csc = csr_to_csc(csr)
+    Gt = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+    rng = np.random.default_rng(5)
+    x = rng.integers(-3, 4, (csc.num_cols, 8)).astype(np.float32)
+    w = rng.integers(-2, 3, (8, 16)).astype(np.float32)
+    for plan in (None, fg.Plan(Gt, 16, segment_edges=64)):
+        check_mlp(csc, Gt, x, x, w, plan=plan, exact=True, square=True)
+    noedge = synth.CSR(3, 5, np.zeros(4, np.int32), np.zeros(0, np.int32))
+    G0 = fg.Graph.from_csr(noedge)
+    o, a = fg.mlp_aggregate(G0, dev(np.ones((5, 8), np.float32)), dev(np.ones((8, 4), np.float32)),
+                            x_dst=dev(np.ones((3, 8), np.float32)))
+    assert np.all(host(o) == 0) and np.all(host(a) == -1)
 
 
 def test_gat_fused_unsupported_shape_raises(small_rmat):
@@ -563,6 +660,19 @@ def test_rmat_233k_max_backward_full(rmat_full):
     plan = fg.Plan(G, 128)
     go = np.random.default_rng(8).integers(-8, 9, (csr.num_rows, 128)).astype(np.float32)
     check_max_backward(csr, G, w.arrays["x"], go, plan=plan, exact=True)
+
+
+@pytest.mark.slow
+def test_rmat_233k_mlp_full(rmat_full):
+    """MLP aggregation (d_in 8 -> d_out 128) on the whole power-law graph in
+    the benchmark's configuration, checked on sampled rows."""
+    w_, G = rmat_full
+    csr = w_.csr
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((csr.num_cols, 8)).astype(np.float32)
+    w = rng.standard_normal((8, 128)).astype(np.float32)
+    rows = sample_rows(csr, 300, 22)
+    check_mlp(csr, G, x, x, w, rows=rows, plan=fg.Plan(G, 128), square=True)
 
 
 @pytest.mark.slow
