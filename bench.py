@@ -38,7 +38,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_rmat_233k_d128.json")
 WORKLOADS = ("rmat_233k_115m", "uniform_deg100_100k", "clustered_133k_deg300",
              "rmat_1m_33m_train", "tiny_uniform_1k", "sage_max_train_rmat_233k",
-             "gat_train_clustered_133k")
+             "gat_train_clustered_133k", "mlp_rmat_233k", "rand_100k_48m")
 
 
 def log(*a):
@@ -99,7 +99,7 @@ def setup(name, d, args, fg, torch, dev):
     import synth
 
     t0 = time.perf_counter()
-    base = {"sage_max_train_rmat_233k": "rmat_233k_115m",
+    base = {"sage_max_train_rmat_233k": "rmat_233k_115m", "mlp_rmat_233k": "rmat_233k_115m",
             "gat_train_clustered_133k": "clustered_133k_deg300"}.get(name, name)
     wl = synth.make_config(base, d=d)
     t_gen = time.perf_counter() - t0
@@ -161,7 +161,7 @@ def setup(name, d, args, fg, torch, dev):
             return dt, flop, "%d random rows (%d edges, %.1f%% of E), all four operators" % (
                 rows.size, ne, 100.0 * ne / e)
 
-    elif name == "uniform_deg100_100k":
+    elif name in ("uniform_deg100_100k", "rand_100k_48m"):
         x_h = wl.arrays["x"]
         F = x_h.shape[1]
         x = T(x_h)
@@ -175,7 +175,8 @@ def setup(name, d, args, fg, torch, dev):
             Op("sddmm_dot", lambda: fg.gsddmm(G, x, x, plan=P, out=sc),
                bytes_sddmm(n, e, F, 1), 2 * e * F, graded=True),
         ]
-        cfg.update(feature_dim=F, graph="uniform, in-degree 100")
+        cfg.update(feature_dim=F, graph="uniform, in-degree 100" if name.startswith("uniform")
+                   else "two degree classes: 20K vertices ~2000, 80K ~100 (in and out)")
 
         def oracle_sample(edges_target):
             import oracle
@@ -259,6 +260,44 @@ def setup(name, d, args, fg, torch, dev):
             dt = time.perf_counter() - t0
             return dt, ne * F + rows.size * F, (
                 "%d random rows (%d edges), forward max and its gradient" % (rows.size, ne))
+
+    elif name == "mlp_rmat_233k":
+        # MLP aggregation (d_in = 8 as in the paper's kernel study, d_out = --d):
+        # out[v] = max over in-edges of relu((x[u] + x[v]) W); one call = the
+        # vertex transform on the matrix cores + the relu(u + v) max gather
+        d_in, d_out = 8, (d or 128)
+        rng = np.random.default_rng(np.random.SeedSequence([3, d_in, d_out]))
+        x_h = rng.standard_normal((n, d_in), dtype=np.float32)
+        w_h = (rng.standard_normal((d_in, d_out), dtype=np.float32) / np.sqrt(d_in)).astype(
+            np.float32)
+        x, wt = T(x_h), T(w_h)
+        P = mkplan(G, max_width=d_out, **popt)
+        plans.append(P)
+        out_m = torch.empty((n, d_out), device=dev)
+        arg = torch.empty((n, d_out), dtype=torch.int32, device=dev)
+        ws = torch.empty((2 * n * d_out,), device=dev)
+        ops = [
+            Op("mlp_aggregate", lambda: fg.mlp_aggregate(G, x, wt, plan=P, out=out_m, arg=arg,
+                                                         workspace=ws),
+               # transform: read X, write P; gather: like gSpMM max over P with P[v] per row
+               4 * n * d_in + 4 * n * d_out + bytes_spmm(n, e, d_out, 1, argmax=True)
+               + 4 * n * d_out,
+               2 * n * d_in * d_out + 3 * e * d_out, graded=True),
+        ]
+        cfg.update(d_in=d_in, d_out=d_out,
+                   graph="R-MAT (.57,.19,.19,.05), self-loops removed, relabelled")
+
+        def oracle_sample(edges_target):
+            import oracle
+
+            rows, ne = _row_sample(csr, edges_target / 16, 12345)
+            t0 = time.perf_counter()
+            oracle.mlp_aggregate(csr, x_h, x_h, w_h, rows=rows)
+            dt = time.perf_counter() - t0
+            # the oracle evaluates the per-edge form; credited with the same
+            # executed-operation count as the GPU's factored form
+            return dt, 2 * rows.size * d_in * d_out + 3 * ne * d_out, (
+                "%d random rows (%d edges), per-edge definition" % (rows.size, ne))
 
     elif name == "gat_train_clustered_133k":
         # one graph attention layer (8 heads of 16), forward and backward:

@@ -113,11 +113,13 @@ typedef struct fg_graph {
  *    items first, rows without edges last;
  *  - gather (gSpMM, gSDDMM, fused attention): as plain by default.  With
  *    source partitioning (opt-in, source_slab_rows != 0), rows with at least
- *    max(partition_min_degree, 32 * slabs) edges and sorted source ids are cut
- *    where the source id crosses a multiple of source_slab_rows, then into
- *    pieces of at most S edges; slab p's pieces run on die p mod 8, slab after
- *    slab, so each die finds the slab's feature rows in its L2 (more L2 hits,
- *    more pieces to merge).
+ *    max(partition_min_degree, 32 * ceil(num_cols / source_slab_rows)) edges
+ *    and sorted source ids are cut where their sources change slab (slabs:
+ *    consecutive source ids, at most source_slab_rows of them and about equal
+ *    shares of these rows' edges), then into pieces of at most S edges; each
+ *    slab runs on one die (slabs dealt in order to the least-loaded die), so
+ *    the die finds the slab's feature rows in its L2 (more L2 hits, more
+ *    pieces to merge).
  * Items of rows cut in several pieces write partial results that a second
  * pass merges in a fixed order, so results are deterministic for a plan.
  * ------------------------------------------------------------------------- */

@@ -178,28 +178,62 @@ void build_plain(const int32_t* ip, int64_t num_rows, const Options& o, Schedule
 
 // Gather schedule with source partitioning (the paper's 1D graph partitioning
 // of source vertices, Sec. III-C, sized for one die's L2 instead of a CPU's
-// LLC).  Source ids are cut into slabs of o.slab vertices.  A row with at
-// least max(min_deg, kMinTileEdges * slabs) edges whose sources are sorted is
-// cut at slab boundaries (then into pieces of at most S edges); its pieces go
-// to the stream of die (slab mod 8), ordered by slab, so that each die works
-// through one slab of feature rows at a time and finds them in its L2.  The
-// remaining rows are cut as in the plain schedule and dealt to the streams,
-// longest first, to even out the edges per die.  The streams are interleaved
-// four items (one workgroup) at a time, following the round-robin order in
-// which workgroups reach the dies; exhausted streams are padded with empty
-// items (row = -1) that the kernels skip.
+// LLC).  A row with at least max(min_deg, kMinTileEdges * ceil(num_cols /
+// o.slab)) edges whose sources are sorted is partitioned.  Source ids are cut
+// into consecutive slabs of at most o.slab vertices that also hold about equal
+// shares of the partitioned rows' edges (so that labellings which put the
+// busy sources together still spread over the dies); partitioned rows are cut
+// where their sources change slab, then into pieces of at most S edges.  Each
+// slab goes, in slab order, to the die with the fewest partitioned edges so
+// far, and its pieces join that die's stream: each die works through its
+// slabs one at a time and finds their feature rows in its L2.  The remaining
+// rows are cut as in the plain schedule and dealt to the streams, longest
+// first, to even out the edges per die.  The streams are interleaved four
+// items (one workgroup) at a time, following the round-robin order in which
+// workgroups reach the dies; exhausted streams are padded with empty items
+// (row = -1) that the kernels skip.
 bool build_partitioned(const int32_t* ip, const int32_t* ix, int64_t num_rows, int64_t num_cols,
                        const Options& o, Schedule& sc) {
-  const int64_t slabs = (num_cols + o.slab - 1) / o.slab;
-  if (o.slab <= 0 || slabs < 2) return false;
-  const int64_t min_deg = std::max<int64_t>(o.min_deg, kMinTileEdges * slabs);
+  const int64_t id_slabs = (num_cols + o.slab - 1) / o.slab;
+  if (o.slab <= 0 || id_slabs < 2) return false;
+  const int64_t min_deg = std::max<int64_t>(o.min_deg, kMinTileEdges * id_slabs);
+  // partitioned rows and the edges each source contributes to them
+  std::vector<char> part_row((size_t)num_rows, 0);
+  std::vector<int64_t> work((size_t)num_cols, 0);
+  int64_t total = 0;
+  for (int64_t r = 0; r < num_rows; ++r) {
+    const int64_t b = ip[r], e = ip[r + 1];
+    bool part = e - b >= min_deg;
+    for (int64_t q = b + 1; part && q < e; ++q)
+      if (ix[q] < ix[q - 1]) part = false;  // unsorted row: no contiguous slab ranges
+    if (!part) continue;
+    part_row[(size_t)r] = 1;
+    for (int64_t q = b; q < e; ++q) ++work[(size_t)ix[q]];
+    total += e - b;
+  }
+  if (total == 0) return false;
+  // slab boundaries: at most o.slab ids and about total / max(id_slabs, dies) edges
+  const int64_t target = (total + std::max<int64_t>(id_slabs, kXcds) - 1) /
+                         std::max<int64_t>(id_slabs, kXcds);
+  std::vector<int32_t> slab_of((size_t)num_cols);
+  std::vector<int64_t> slab_work;
+  int64_t start = 0, acc = 0;
+  for (int64_t u = 0; u < num_cols; ++u) {
+    if (u > start && (u - start == o.slab || acc >= target)) {
+      slab_work.push_back(acc);
+      start = u;
+      acc = 0;
+    }
+    slab_of[(size_t)u] = (int32_t)slab_work.size();
+    acc += work[(size_t)u];
+  }
+  slab_work.push_back(acc);
+  const int64_t slabs = (int64_t)slab_work.size();
+
   std::vector<std::pair<fg::Seg, int32_t>> pieces;
   for (int64_t r = 0; r < num_rows; ++r) {
     const int64_t b = ip[r], e = ip[r + 1], deg = e - b;
-    bool part = deg >= min_deg;
-    for (int64_t q = b + 1; part && q < e; ++q)
-      if (ix[q] < ix[q - 1]) part = false;  // unsorted row: no contiguous slab ranges
-    if (!part) {
+    if (!part_row[(size_t)r]) {
       int64_t k = deg > o.S ? (deg + o.S - 1) / o.S : 1;
       if (k > o.cap) k = o.cap;
       cut_even((int32_t)r, b, e, k, -1, pieces);
@@ -208,10 +242,9 @@ bool build_partitioned(const int32_t* ip, const int32_t* ix, int64_t num_rows, i
     ++sc.partitioned_rows;
     int64_t q = b;
     while (q < e) {
-      const int32_t slab = (int32_t)(ix[q] / o.slab);
-      const int64_t lim = (int64_t)(slab + 1) * o.slab;
+      const int32_t slab = slab_of[(size_t)ix[q]];
       int64_t t = q;
-      while (t < e && ix[t] < lim) ++t;
+      while (t < e && slab_of[(size_t)ix[t]] == slab) ++t;
       cut_even((int32_t)r, q, t, (t - q + o.S - 1) / o.S, slab, pieces);
       q = t;
     }
@@ -229,7 +262,9 @@ bool build_partitioned(const int32_t* ip, const int32_t* ix, int64_t num_rows, i
     else rest.push_back(pc.first);
   }
   for (int64_t sl = 0; sl < slabs; ++sl) {
-    const int x = (int)(sl % kXcds);
+    int x = 0;
+    for (int y = 1; y < kXcds; ++y)
+      if (load[y] < load[x]) x = y;
     for (auto& sg : by_slab[(size_t)sl]) {
       stream[x].push_back(sg);
       load[x] += (int64_t)sg.end - sg.begin;

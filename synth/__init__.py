@@ -17,6 +17,7 @@ from .graphs import (  # noqa: F401
     fixed_indegree_graph,
     rmat_graph,
     clustered_graph,
+    two_class_graph,
     make_config,
     small_random_graph,
     CONFIG_NAMES,

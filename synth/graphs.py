@@ -245,6 +245,28 @@ def rmat_graph(seq: np.random.SeedSequence, perm_rng: Optional[np.random.Generat
     return coo_to_csr(dst, src, n, n)
 
 
+def two_class_graph(rng: np.random.Generator, perm_rng: Optional[np.random.Generator], n: int,
+                    n_hot: int, e: int, p_hot: float) -> CSR:
+    """Random multigraph with two degree classes: both ends of every edge are
+    drawn independently, from the n_hot "hot" vertices with probability p_hot
+    (uniformly inside the class) and from the other n - n_hot vertices
+    otherwise, so hot vertices average e * p_hot / n_hot in- and out-edges.
+    Duplicates and self-loops are kept; labels are then scrambled by a seeded
+    permutation of [0, n) (perm_rng None keeps the hot vertices first)."""
+    def ends():
+        hot = rng.random(e, dtype=np.float32) < np.float32(p_hot)
+        ids = rng.integers(0, n - n_hot, e, dtype=np.int64) + n_hot
+        ids[hot] = rng.integers(0, n_hot, int(hot.sum()), dtype=np.int64)
+        return ids
+
+    src = ends()
+    dst = ends()
+    if perm_rng is not None:
+        perm = perm_rng.permutation(n)
+        src, dst = perm[src], perm[dst]
+    return coo_to_csr(dst, src, n, n)
+
+
 def small_random_graph(rng: np.random.Generator, n_rows: int, n_cols: int, e: int,
                        empty_frac: float = 0.0) -> CSR:
     """Uniform random multigraph for pins and edge cases: destinations are
@@ -268,6 +290,7 @@ CONFIG_NAMES = (
     "rmat_233k_115m",       # R-MAT N=232,965, E=114.6M, d=128
     "clustered_133k_deg300",  # N=132,534, 100 communities, deg 300, H=8 x 16
     "rmat_1m_33m_train",    # R-MAT N=2^20, E=2^25, d=256, CSR + CSC
+    "rand_100k_48m",        # two degree classes: 20K at ~2000, 80K at ~100, E=48M, d in {32..512}
 )
 
 _SEEDS = {name: i + 1 for i, name in enumerate(CONFIG_NAMES)}
@@ -319,6 +342,13 @@ def make_config(name: str, d: Optional[int] = None, scale_down: int = 1) -> Work
         csr = clustered_graph(r_struct, n, 100, 300, 270)
         arrays["x"] = r_feat.standard_normal((n, 8, 16), dtype=np.float32)
         meta.update(heads=8, head_dim=16)
+    elif name == "rand_100k_48m":
+        d = 128 if d is None else d
+        n = 100_000 // scale_down
+        csr = two_class_graph(r_struct, r_perm, n, n // 5, 48_000_000 // scale_down, 40.0 / 48.0)
+        r_d = np.random.default_rng(np.random.SeedSequence([seed, d]))
+        arrays["x"] = r_d.standard_normal((n, d), dtype=np.float32)
+        meta.update(heads=1, head_dim=d)
     else:  # rmat_1m_33m_train
         d = 256 if d is None else d
         n = (1 << 20) // scale_down

@@ -319,16 +319,22 @@ def _check_schedule(indptr, S, cap=128, indices=None, num_cols=0, slab=0, min_de
         row = indices[indptr[r]:indptr[r + 1]]
         part[r] = bool(np.all(np.diff(row) >= 0))
     is_part = part[real[:, 0]]
-    lo_slab = indices[real[is_part, 1]] // slab
-    hi_slab = indices[real[is_part, 2] - 1] // slab
-    assert np.array_equal(lo_slab, hi_slab)  # a piece never crosses a slab boundary
+    lo = indices[real[is_part, 1]].astype(np.int64)       # smallest source of a piece
+    hi = indices[real[is_part, 2] - 1].astype(np.int64)   # largest source of a piece
+    assert np.all(hi - lo < slab)  # a piece lies inside one slab of at most `slab` ids
     assert np.all(lens[is_part] <= S)
-    # stream of die x = workgroups (4 items) w with w % 8 == x; slabs in order
-    die = (np.nonzero(~pad)[0] // 4) % 8
-    for x in range(8):
-        sl = lo_slab[die[is_part] == x]
-        assert np.all(sl % 8 == x)
-        assert np.all(np.diff(sl) >= 0)
+    # stream of die x = workgroups (4 items) w with w % 8 == x
+    die = ((np.nonzero(~pad)[0] // 4) % 8)[is_part]
+    for x in range(8):  # each die walks its slabs in source order
+        assert np.all(np.diff(lo[die == x]) >= -(slab - 1))
+        assert np.all(np.diff(hi[die == x]) >= -(slab - 1))
+    # pieces on different dies come from disjoint source ranges (a slab, and
+    # with it its feature rows, belongs to one die)
+    order = np.argsort(lo, kind="stable")
+    lo_s, hi_s, die_s = lo[order], hi[order], die[order]
+    run_hi = np.maximum.accumulate(hi_s)
+    cross = die_s[1:] != die_s[:-1]
+    assert np.all(lo_s[1:][cross] > run_hi[:-1][cross])
     return segs
 
 
@@ -348,6 +354,25 @@ def test_partitioned_schedule(S, slab, min_deg):
     # the plain schedule of the same graph ignores the slabs
     _check_schedule(c.indptr, S, indices=c.indices, num_cols=c.num_cols, slab=slab,
                     min_deg=min_deg, which="plain")
+
+
+def test_partition_slabs_balance_dies():
+    """Busy sources labelled first (one id slab would hold most edges): the
+    slabs follow the edges, so the partitioned work spreads over all dies."""
+    w = synth.make_config("rand_100k_48m", d=16, scale_down=20)
+    g = w.csr
+    outdeg = np.bincount(g.indices, minlength=g.num_cols)
+    order = np.argsort(-outdeg, kind="stable")
+    rank = np.empty_like(order)
+    rank[order] = np.arange(order.size)
+    hf = synth.coo_to_csr(rank[synth.csr_rows(g)], rank[g.indices], g.num_rows, g.num_cols)
+    segs = _check_schedule(hf.indptr, 4096, indices=hf.indices, num_cols=hf.num_cols,
+                           slab=1024, min_deg=500, which="gather")
+    real = segs[segs[:, 0] >= 0]
+    big = np.diff(hf.indptr.astype(np.int64))[real[:, 0]] >= 500
+    die = ((np.nonzero(segs[:, 0] >= 0)[0] // 4) % 8)[big]
+    per_die = np.bincount(die, weights=(real[big, 2] - real[big, 1]), minlength=8)
+    assert per_die.min() > 0.8 * per_die.mean()
 
 
 def test_partitioning_skips_unsorted_rows():

@@ -88,3 +88,19 @@ def test_check_csr_rejects_bad_graphs():
     bad.edge_ids[0] = g.nnz
     with pytest.raises(ValueError):
         check_csr(bad, nnz_total=g.nnz)
+
+
+def test_two_class_degrees():
+    """rand-100K shape: a fifth of the vertices hot with ~20x the degree of the
+    rest, both in and out; exact edge count; deterministic."""
+    w = synth.make_config("rand_100k_48m", d=16, scale_down=20)
+    g = w.csr
+    assert g.num_rows == 5000 and g.nnz == 2_400_000
+    indeg = g.degrees()
+    outdeg = np.bincount(g.indices, minlength=g.num_cols)
+    for deg in (indeg, outdeg):
+        top = np.sort(deg)[::-1]
+        assert abs(top[:1000].mean() - 2000) < 60 and abs(top[1000:].mean() - 100) < 5
+    w2 = synth.make_config("rand_100k_48m", d=16, scale_down=20)
+    np.testing.assert_array_equal(w2.csr.indices, g.indices)
+    np.testing.assert_array_equal(w2.arrays["x"], w.arrays["x"])
