@@ -165,7 +165,12 @@ __device__ __forceinline__ Item load_item(const Seg* segs, const int32_t* indptr
 
 // Writes one lane's accumulated vector: to the plan workspace for a split
 // row's segment, else to the output (max: empty -> 0 / -1).
-template <int VEC, bool MAX, bool SEG>
+// EPI (u_add_v max with positional edge ids): acc / am are the max and argmax
+// of the raw source values; the row's message max is relu(acc + xd[v]) (fp32
+// rounding of a sum is monotone in each operand, so this equals the max of
+// the rounded per-edge sums), taken by the argmax edge when positive, else
+// every message is 0 and the row's first edge id wins.
+template <int VEC, bool MAX, bool SEG, bool EPI = false>
 __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, int64_t f,
                                            const float (&acc)[VEC], const int32_t (&am)[VEC]) {
   if (SEG && it.slot >= 0) {
@@ -174,11 +179,20 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
   } else if constexpr (MAX) {
     float o[VEC];
     int32_t a[VEC];
+    float pdv[VEC];
+    if constexpr (EPI) load_vec<VEC>(p.xd + it.row * p.F + f, pdv);
 #pragma unroll
     for (int c = 0; c < VEC; ++c) {
       const bool none = am[c] == INT_MAX;
-      o[c] = none ? 0.0f : acc[c];
-      a[c] = none ? -1 : am[c];
+      if constexpr (EPI) {
+        const float t = acc[c] + pdv[c];
+        const bool pos = t > 0.0f;
+        o[c] = (none || !pos) ? 0.0f : t;
+        a[c] = none ? -1 : (pos ? am[c] : (int32_t)it.b);
+      } else {
+        o[c] = none ? 0.0f : acc[c];
+        a[c] = none ? -1 : am[c];
+      }
     }
     store_vec<VEC>(p.out + it.row * p.F + f, o);
     store_vec_i<VEC>(p.arg + it.row * p.F + f, a);
@@ -198,13 +212,17 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
 // never replaces and takes its first edge afterwards.  Groups, segments and
 // slots are then merged with the full (value, edge id) order.
 // ADD: the message is relu(x[u] + xd[v]) (MLP aggregation with the dense
-// transform applied to the vertices beforehand); requires MAX and !MUL.
+// transform applied to the vertices beforehand); requires MAX and !MUL.  With
+// positional edge ids the add and relu move to the store (EPI, see
+// spmm_store); with explicit edge ids each message is formed in the loop.
 template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool SEG, bool ADD = false>
 __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
   constexpr int NG = kWave / G;
   constexpr bool POS = MAX && !EIDS;
   static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
   static_assert(!ADD || (MAX && !MUL), "u_add_v messages are max-reduced copies");
+  constexpr bool EPI = ADD && POS;
+  constexpr bool ELEM = ADD && !POS;
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -233,10 +251,10 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
       acc[v][c] = MAX ? -INFINITY : 0.0f;
       am[v][c] = INT_MAX;
     }
-  float pd[NV][4];  // this row's destination features (ADD)
+  float pd[NV][4];  // this row's destination features (per-element messages)
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
-    if (ADD && act[v]) {
+    if (ELEM && act[v]) {
       load_vec<4>(p.xd + it.row * F + f[v], pd[v]);
     } else {
 #pragma unroll
@@ -274,7 +292,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         for (int v = 0; v < NV; ++v) {
           if (ok[u] && act[v]) {
             load_vec<4>(xr + f[v], val[u][v]);
-            if constexpr (ADD) {
+            if constexpr (ELEM) {
 #pragma unroll
               for (int c = 0; c < 4; ++c) {
                 const float t = val[u][v][c] + pd[v][c];
@@ -349,7 +367,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
   if (gid != 0) return;
 #pragma unroll
   for (int v = 0; v < NV; ++v)
-    if (act[v]) spmm_store<4, MAX, SEG>(p, it, f[v], acc[v], am[v]);
+    if (act[v]) spmm_store<4, MAX, SEG, EPI>(p, it, f[v], acc[v], am[v]);
 }
 
 // Generic path: any width (scalar lanes), runtime group width G = 2^logG.
@@ -470,10 +488,14 @@ __global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
 // tile of 64 feature columns (blockIdx.y); wavefront w takes slots
 // sb+w, sb+w+4, ... in increasing order (4 loads in flight), then the four
 // wavefront results are combined in order w = 0..3.
-template <bool MAX>
+// EPI: the partials are raw max / argmax of the source values of a u_add_v
+// max (see spmm_store); the merged result gets the same relu epilogue.
+template <bool MAX, bool EPI = false>
 __global__ __launch_bounds__(kBlock) void spmm_fixup_kernel(const Fix* fix, const float* ws_f,
                                                             const int32_t* ws_i, int64_t F,
-                                                            float* out, int32_t* arg) {
+                                                            float* out, int32_t* arg,
+                                                            const float* xd,
+                                                            const int32_t* indptr) {
   __shared__ float red_v[kWavesPerBlock][kWave];
   __shared__ int32_t red_a[kWavesPerBlock][kWave];
   const int w = threadIdx.x >> 6;
@@ -529,7 +551,13 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup_kernel(const Fix* fix, cons
     }
   }
   const int64_t o = (int64_t)fx.row * F + col;
-  if constexpr (MAX) {
+  if constexpr (EPI) {
+    const bool none = am == INT_MAX;
+    const float t = acc + xd[o];
+    const bool pos = t > 0.0f;
+    out[o] = (none || !pos) ? 0.0f : t;
+    arg[o] = none ? -1 : (pos ? am : indptr[fx.row]);
+  } else if constexpr (MAX) {
     const bool none = am == INT_MAX;
     out[o] = none ? 0.0f : acc;
     arg[o] = none ? -1 : am;
@@ -1930,12 +1958,17 @@ hipError_t launch_spmm_core(const GraphView& g, const PlanView* plan, int msg, i
   if (err != hipSuccess) return err;
   if (seg && plan->num_split_rows > 0) {
     const dim3 fgrid((unsigned)plan->num_split_rows, (unsigned)((F + kWave - 1) / kWave), 1);
-    if (mx)
+    // the float4 kernel with positional edge ids defers the u_add_v epilogue
+    const bool epi = xd && vec4 && !g.edge_ids;
+    if (epi)
+      FG_LAUNCH((spmm_fixup_kernel<true, true>), fgrid, stream, plan->fix, plan->ws_f,
+                plan->ws_i, F, out, arg, xd, g.indptr);
+    else if (mx)
       FG_LAUNCH((spmm_fixup_kernel<true>), fgrid, stream, plan->fix, plan->ws_f, plan->ws_i, F,
-                out, arg);
+                out, arg, nullptr, nullptr);
     else
       FG_LAUNCH((spmm_fixup_kernel<false>), fgrid, stream, plan->fix, plan->ws_f, plan->ws_i, F,
-                out, arg);
+                out, arg, nullptr, nullptr);
     err = hipGetLastError();
   }
   return err;
