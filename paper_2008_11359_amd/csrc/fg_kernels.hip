@@ -143,8 +143,21 @@ struct SpmmParams {
   int64_t F;
   int32_t H;
   int32_t dh;
-  int32_t logG;  // runtime group width (generic kernel only)
+  int32_t logG;     // runtime group width (generic kernel only)
+  int32_t ev_vec4;  // edge-value rows are 16-byte aligned float4s (H % 4 == 0)
 };
+
+// Largest head count whose per-batch edge values a wavefront stages in LDS.
+constexpr int kTabHeads = 16;
+
+// Orders one wavefront's LDS accesses around a cross-lane hand-off (the
+// hardware executes a wavefront's LDS operations in order; the fences keep
+// the compiler from moving accesses across).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 struct Item {
   int64_t row, b, e;
@@ -215,14 +228,23 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
 // transform applied to the vertices beforehand); requires MAX and !MUL.  With
 // positional edge ids the add and relu move to the store (EPI, see
 // spmm_store); with explicit edge ids each message is formed in the loop.
-template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool SEG, bool ADD = false>
+// TAB (per-head edge values, 2 <= H <= kTabHeads): each batch of 64 edges
+// stages its edge values in an LDS table, a few loads per lane, and every step
+// reads its weights from there; loading them per step would add one more
+// vector-memory instruction per gather, and the address unit is what bounds
+// these kernels.
+template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool SEG, bool ADD = false,
+          bool TAB = false>
 __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
   constexpr int NG = kWave / G;
   constexpr bool POS = MAX && !EIDS;
   static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
   static_assert(!ADD || (MAX && !MUL), "u_add_v messages are max-reduced copies");
+  static_assert(!TAB || MUL, "the table holds edge values");
   constexpr bool EPI = ADD && POS;
   constexpr bool ELEM = ADD && !POS;
+  __shared__ __align__(16) float tab_all[TAB ? kWavesPerBlock * kWave * kTabHeads : 1];
+  float* tab = tab_all + (TAB ? (threadIdx.x >> 6) * kWave * kTabHeads : 0);
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -274,6 +296,23 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         if (p.H == 1) my_w = p.ev[my_eid];
       }
     }
+    if constexpr (TAB) {
+      wave_lds_sync();  // the previous batch's table reads are done
+      if (lane < cnt) {
+        const float* er = p.ev + (int64_t)my_eid * p.H;
+        float* tr = tab + lane * p.H;
+        if (p.ev_vec4) {
+          for (int h = 0; h < p.H; h += 4) {
+            float q[4];
+            load_vec<4>(er + h, q);
+            store_vec<4>(tr + h, q);
+          }
+        } else {
+          for (int h = 0; h < p.H; ++h) tr[h] = er[h];
+        }
+      }
+      wave_lds_sync();
+    }
     for (int j0 = 0; j0 < cnt; j0 += NG * U) {
       float val[U][NV][4];
       float wv[U][NV];
@@ -299,7 +338,10 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
                 val[u][v][c] = t > 0.0f ? t : 0.0f;
               }
             }
-            wv[u][v] = (MUL && p.H != 1) ? p.ev[(int64_t)eu[u] * p.H + hv[v]] : w1;
+            if constexpr (TAB)
+              wv[u][v] = tab[(jb + gid) * p.H + hv[v]];
+            else
+              wv[u][v] = (MUL && p.H != 1) ? p.ev[(int64_t)eu[u] * p.H + hv[v]] : w1;
           } else {
 #pragma unroll
             for (int c = 0; c < 4; ++c) val[u][v][c] = MAX ? -INFINITY : 0.0f;
@@ -584,6 +626,7 @@ struct SddmmParams {
   int32_t dh;
   int32_t logG;  // lanes per feature row (runtime kernels)
   int32_t logS;  // lanes per head (runtime headed kernel)
+  int32_t out_vec4;  // output rows of H values are 16-byte aligned float4s
 };
 
 // Single head, float4 lanes, G lanes per feature row, NV float4 per lane.  The
@@ -673,9 +716,15 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
 
 // Several heads, float4 lanes, S lanes per head (compile time), G lanes per
 // feature row (runtime, <= 64, one float4 per lane).
+// Results of a batch are staged per edge in an LDS table (one row of H
+// values per edge) and leave in one pass of per-lane stores per batch, when
+// H <= kTabHeads; otherwise each step stores its heads directly.
 template <int S, bool SEG>
 __global__ __launch_bounds__(kBlock) void sddmm_headed_kernel(SddmmParams p) {
   constexpr int U = 4;
+  __shared__ __align__(16) float tab_all[kWavesPerBlock * kWave * kTabHeads];
+  float* tab = tab_all + (threadIdx.x >> 6) * kWave * kTabHeads;
+  const bool staged = p.H <= kTabHeads;
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -724,8 +773,30 @@ __global__ __launch_bounds__(kBlock) void sddmm_headed_kernel(SddmmParams p) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) part += val[u][c] * xd[c];
         part = group_sum<S>(part);
-        if (ok[u] && act && (li % S) == S - 1) p.out[(int64_t)eu[u] * p.H + h] = part;
+        if (ok[u] && act && (li % S) == S - 1) {
+          if (staged)
+            tab[(j0 + u * ngroups + gid) * p.H + h] = part;
+          else
+            p.out[(int64_t)eu[u] * p.H + h] = part;
+        }
       }
+    }
+    if (staged) {
+      wave_lds_sync();
+      if (lane < cnt) {
+        const float* tr = tab + lane * p.H;
+        float* orow = p.out + (int64_t)my_eid * p.H;
+        if (p.out_vec4) {
+          for (int hh = 0; hh < p.H; hh += 4) {
+            float q[4];
+            load_vec<4>(tr + hh, q);
+            store_vec<4>(orow + hh, q);
+          }
+        } else {
+          for (int hh = 0; hh < p.H; ++hh) orow[hh] = tr[hh];
+        }
+      }
+      wave_lds_sync();  // the table is rewritten by the next batch
     }
   }
 }
@@ -1844,10 +1915,22 @@ dim3 grid_for(int64_t items, int64_t chunks) {
 #define FG_LAUNCH(kernel, grid, stream, ...) \
   hipLaunchKernelGGL((kernel), (grid), dim3(kBlock), 0, (stream), __VA_ARGS__)
 
+template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool ADD, bool TAB>
+void spmm_fast_seg2(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+  if (seg) FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, true, ADD, TAB>), grid, st, prm);
+  else FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, false, ADD, TAB>), grid, st, prm);
+}
+
 template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool ADD = false>
 void spmm_fast_seg(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
-  if (seg) FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, true, ADD>), grid, st, prm);
-  else FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, false, ADD>), grid, st, prm);
+  // per-head edge values come from a per-batch LDS table
+  if constexpr (MUL) {
+    if (prm.H >= 2 && prm.H <= kTabHeads) {
+      spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, true>(prm, seg, grid, st);
+      return;
+    }
+  }
+  spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, false>(prm, seg, grid, st);
 }
 
 template <int G, int NV, int U, bool MUL, bool MAX, bool ADD = false>
@@ -1941,6 +2024,7 @@ hipError_t launch_spmm_core(const GraphView& g, const PlanView* plan, int msg, i
   prm.H = (int32_t)H;
   prm.dh = (int32_t)dh;
   prm.logG = 6;
+  prm.ev_vec4 = (ev && H % 4 == 0 && aligned16(ev)) ? 1 : 0;
   if (vec4) {
     const int64_t Q = F / 4;  // float4 per row
     if (Q <= 4) spmm_fast_ops<4, 1, 4>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
@@ -2081,6 +2165,7 @@ hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, in
   prm.dh = (int32_t)dh;
   prm.logG = 6;
   prm.logS = 0;
+  prm.out_vec4 = (H % 4 == 0 && aligned16(out)) ? 1 : 0;
   const dim3 grid = grid_for(prm.n_items, 1);
   const bool vec4 = (F % 4 == 0) && (H == 1 || dh % 4 == 0) && aligned16(xs) && aligned16(xd);
   if (vec4 && H == 1 && F <= 4 * 4 * kWave) {
