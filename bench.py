@@ -406,6 +406,10 @@ def setup(name, d, args, fg, torch, dev):
     else:
         raise SystemExit("unknown workload %r" % name)
 
+    # digests of the seeded inputs (short SHA-256 prefixes), so runs can be matched
+    digests = {"indptr": csr.indptr, "indices": csr.indices}
+    digests.update({k: v for k, v in wl.arrays.items() if isinstance(v, np.ndarray)})
+    cfg["inputs_sha256"] = {k: synth.sha256(v)[:16] for k, v in digests.items()}
     pinfo = plans[0].info()
     cfg.update(segment_edges=pinfo["segment_edges"], max_row_segments=pinfo["max_row_segments"],
                source_slab_rows=pinfo["source_slab_rows"],
@@ -442,7 +446,21 @@ def _cpu_baseline(oracle_sample, budget_s, threads):
         total_f += flop
         reps += 1
     return {"value": round(total_f / total_t / 1e9, 3), "unit": "GFLOP/s", "cores": threads,
-            "kind": "oracle", "sample": "%s; %d passes, %.1f s" % (desc, reps, total_t)}
+            "kind": "oracle", "sample": "%s; %d passes, %.1f s" % (desc, reps, total_t),
+            "host": _host()}
+
+
+def _host():
+    """CPU model and logical CPU count of the machine the oracle ran on."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "logical_cpus": os.cpu_count()}
 
 
 # ----------------------------------------------------------------------------
