@@ -1002,6 +1002,7 @@ __device__ __forceinline__ void softmax_row_in_registers(const SoftmaxParams& p,
 // (T0 + 4l + c) mod H.  Partial float4s at the ends (H < 4) use scalar access.
 
 constexpr int kContigRegs = 12;  // float4 per lane held in registers (3072 values)
+constexpr int kStreamDepth = 8;  // float4 loads in flight per lane when streaming a row
 
 struct ContigRange {
   int64_t lo, hi, T0, K;  // valid flat range, aligned start, number of float4
@@ -1170,10 +1171,10 @@ __device__ __forceinline__ void softmax_contig_stream(const SoftmaxParams& p, co
   const ContigRange r = contig_range(it.b, it.e, H);
   float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
   float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int64_t k0 = lane; k0 < r.K; k0 += 4 * kWave) {
-    float v[4][4];
+  for (int64_t k0 = lane; k0 < r.K; k0 += kStreamDepth * kWave) {
+    float v[kStreamDepth][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kStreamDepth; ++i) {
       const int64_t k = k0 + (int64_t)kWave * i;
       if (k < r.K) {
         contig_load(p, r, k, v[i]);
@@ -1183,7 +1184,7 @@ __device__ __forceinline__ void softmax_contig_stream(const SoftmaxParams& p, co
       }
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < kStreamDepth; ++i)
 #pragma unroll
       for (int c = 0; c < 4; ++c)
         if (v[i][c] != -INFINITY) lse_push(m[c], z[c], v[i][c]);
@@ -1205,15 +1206,15 @@ __device__ __forceinline__ void softmax_contig_stream(const SoftmaxParams& p, co
   float inv[4];
 #pragma unroll
   for (int c = 0; c < 4; ++c) inv[c] = 1.0f / z[c];
-  for (int64_t k0 = lane; k0 < r.K; k0 += 4 * kWave) {
-    float v[4][4];
+  for (int64_t k0 = lane; k0 < r.K; k0 += kStreamDepth * kWave) {
+    float v[kStreamDepth][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kStreamDepth; ++i) {
       const int64_t k = k0 + (int64_t)kWave * i;
       if (k < r.K) contig_load(p, r, k, v[i]);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kStreamDepth; ++i) {
       const int64_t k = k0 + (int64_t)kWave * i;
       if (k < r.K) {
         float o[4];
@@ -1375,15 +1376,15 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
       m[c] = p.ws_row[(fi * H + h) * 2 + 0];
       inv[c] = 1.0f / p.ws_row[(fi * H + h) * 2 + 1];
     }
-    for (int64_t k0 = lane; k0 < r.K; k0 += 4 * kWave) {
-      float v[4][4];
+    for (int64_t k0 = lane; k0 < r.K; k0 += kStreamDepth * kWave) {
+      float v[kStreamDepth][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < kStreamDepth; ++i) {
         const int64_t k = k0 + (int64_t)kWave * i;
         if (k < r.K) contig_load(p, r, k, v[i]);
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < kStreamDepth; ++i) {
         const int64_t k = k0 + (int64_t)kWave * i;
         if (k < r.K) {
           float o[4];
