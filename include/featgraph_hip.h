@@ -240,6 +240,21 @@ fg_status fg_gat_aggregate(const fg_graph* g, int32_t num_heads, int64_t head_di
                            float negative_slope, float* out, fg_plan* plan, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * SDDMM dot followed by edge softmax in one call (the attention scores of
+ * Eq. 4 and their normalisation, fused where the scores are produced, as the
+ * paper fuses UDFs into its templates, Sec. III-B):
+ *   scores[e, h] = fg_gsddmm's output;  out[e, h] = fg_edge_softmax(scores)
+ * One head with dh % 4 == 0, dh <= 1024 and 16-byte aligned features runs as
+ * one pass (plus the merge of split rows); other shapes run the two
+ * operators one after the other.  Both arrays are [nnz_total, H], written for
+ * the edges of g.  A plan must have max_width >= max(H * dh, H).
+ * ------------------------------------------------------------------------- */
+fg_status fg_gsddmm_edge_softmax(const fg_graph* g, int32_t num_heads, int64_t head_dim,
+                                 const float* x_src, const float* x_dst, int32_t apply_leaky_relu,
+                                 float negative_slope, float* scores, float* out, fg_plan* plan,
+                                 void* stream);
+
+/* ---------------------------------------------------------------------------
  * Gradient of gSpMM with the max aggregator, for training with max
  * aggregation (GraphSage, Sec. V-E).  Sec. II-A derives the backward of the
  * templates by the chain rule; for (+) = max each output element took its

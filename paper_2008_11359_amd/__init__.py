@@ -120,6 +120,9 @@ def _load():
                                           vp]
     lib.fg_edge_softmax_backward.restype = ctypes.c_int
     lib.fg_edge_softmax_backward.argtypes = [gp, i32, vp, vp, vp, i32, ctypes.c_float, vp, vp, vp]
+    lib.fg_gsddmm_edge_softmax.restype = ctypes.c_int
+    lib.fg_gsddmm_edge_softmax.argtypes = [gp, i32, i64, vp, vp, i32, ctypes.c_float, vp, vp, vp,
+                                           vp]
     lib.fg_dense_matmul.restype = ctypes.c_int
     lib.fg_dense_matmul.argtypes = [i64, i64, i64, vp, vp, vp, vp]
     lib.fg_mlp_aggregate.restype = ctypes.c_int
@@ -411,6 +414,39 @@ def edge_softmax(g: Graph, scores: torch.Tensor, leaky: bool = True, slope: floa
     return out
 
 
+def gsddmm_edge_softmax(g: Graph, x_src: torch.Tensor, x_dst: Optional[torch.Tensor] = None,
+                        heads: int = 1, leaky: bool = True, slope: float = 0.2,
+                        plan: Optional[Plan] = None, scores: Optional[torch.Tensor] = None,
+                        out: Optional[torch.Tensor] = None):
+    """gsddmm followed by edge_softmax, fused into one pass where the shape
+    allows: returns (scores, attention weights), each [nnz_total] or
+    [nnz_total, H]."""
+    x_src = _dev_tensor(x_src, torch.float32, "x_src")
+    x_dst = x_src if x_dst is None else _dev_tensor(x_dst, torch.float32, "x_dst")
+    if x_src.shape[0] != g.num_cols or x_dst.shape[0] != g.num_rows:
+        raise ValueError("x_src needs num_cols rows and x_dst num_rows rows")
+    if x_src.shape[1:] != x_dst.shape[1:]:
+        raise ValueError("x_src and x_dst must have the same feature shape")
+    if x_src.dim() == 3:
+        heads = int(x_src.shape[1])
+    F = int(np.prod(x_src.shape[1:])) if x_src.dim() > 1 else 1
+    if F % heads:
+        raise ValueError("feature width not divisible by heads")
+    shape = (g.nnz_total, heads) if (heads > 1 or x_src.dim() == 3) else (g.nnz_total,)
+    res = []
+    for name, t in (("scores", scores), ("out", out)):
+        t = torch.empty(shape, dtype=torch.float32, device=x_src.device) if t is None else \
+            _dev_tensor(t, torch.float32, name)
+        if t.numel() != g.nnz_total * heads:
+            raise ValueError("%s has the wrong size" % name)
+        res.append(t)
+    st = _lib.fg_gsddmm_edge_softmax(ctypes.byref(g._c), heads, F // heads, _ptr(x_src),
+                                     _ptr(x_dst), 1 if leaky else 0, float(slope), _ptr(res[0]),
+                                     _ptr(res[1]), _plan_handle(plan), _stream())
+    _check(st, "fg_gsddmm_edge_softmax")
+    return res[0], res[1]
+
+
 def gat_aggregate(g: Graph, x_src: torch.Tensor, x_dst: Optional[torch.Tensor] = None,
                   heads: int = 1, leaky: bool = True, slope: float = 0.2,
                   plan: Optional[Plan] = None, out: Optional[torch.Tensor] = None):
@@ -599,6 +635,7 @@ def mlp_aggregate(g: Graph, x_src: torch.Tensor, weight: torch.Tensor,
     return out, arg
 
 
-__all__ = ["Graph", "Plan", "gspmm", "gsddmm", "edge_softmax", "gat_aggregate",
+__all__ = ["Graph", "Plan", "gspmm", "gsddmm", "edge_softmax", "gsddmm_edge_softmax",
+           "gat_aggregate",
            "gspmm_max_backward", "edge_softmax_backward", "dense_matmul", "mlp_aggregate",
            "schedule_host", "FgError", "status_string", "LIB_PATH"]

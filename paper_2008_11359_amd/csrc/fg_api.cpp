@@ -666,6 +666,37 @@ fg_status fg_gat_aggregate(const fg_graph* g, int32_t num_heads, int64_t head_di
                                        static_cast<hipStream_t>(stream)));
 }
 
+fg_status fg_gsddmm_edge_softmax(const fg_graph* g, int32_t num_heads, int64_t head_dim,
+                                 const float* x_src, const float* x_dst, int32_t apply_leaky_relu,
+                                 float negative_slope, float* scores, float* out, fg_plan* plan,
+                                 void* stream) {
+  fg_status st = check_graph(g);
+  if (st != FG_OK) return st;
+  if ((st = check_width(num_heads, head_dim)) != FG_OK) return st;
+  const int64_t F = (int64_t)num_heads * head_dim;
+  if (g->nnz > 0 && (!x_src || !x_dst || !scores || !out)) return FG_ERR_INVALID_ARG;
+  // the plan holds F partial values per slot (SDDMM) and 2H per slot (softmax)
+  if ((st = check_plan(plan, g, std::max<int64_t>(F, num_heads))) != FG_OK) return st;
+  const int64_t eb = nnz_total_of(g) * num_heads * 4;
+  const int64_t xs_b = g->num_cols * F * 4, xd_b = g->num_rows * F * 4;
+  if (overlaps(scores, eb, out, eb) || overlaps(scores, eb, x_src, xs_b) ||
+      overlaps(scores, eb, x_dst, xd_b) || overlaps(out, eb, x_src, xs_b) ||
+      overlaps(out, eb, x_dst, xd_b))
+    return FG_ERR_INVALID_ARG;
+  const fg::GraphView gv = view_of(g);
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (fg::gsddmm_softmax_fused(num_heads, head_dim, x_src, x_dst))
+    return from_hip(fg::launch_gsddmm_softmax(gv, plan ? &plan->plain : nullptr, F, x_src, x_dst,
+                                              apply_leaky_relu != 0, negative_slope, scores, out,
+                                              hs));
+  // other shapes: the two operators one after the other
+  hipError_t e = fg::launch_gsddmm(gv, plan ? &plan->gather : nullptr, num_heads, head_dim, x_src,
+                                   x_dst, scores, hs);
+  if (e != hipSuccess) return FG_ERR_HIP;
+  return from_hip(fg::launch_edge_softmax(gv, plan ? &plan->plain : nullptr, num_heads, scores,
+                                          apply_leaky_relu != 0, negative_slope, out, hs));
+}
+
 fg_status fg_gspmm_max_backward(const fg_graph* g, fg_msg_op msg, int32_t num_heads,
                                 int64_t head_dim, const float* x_src, const float* edge_val,
                                 const int32_t* arg_eid, const float* grad_out, float* grad_src,

@@ -52,6 +52,13 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
                                const float* scores, bool leaky, float slope, float* out,
                                hipStream_t stream);
 
+// SDDMM dot with one head and the edge softmax of its scores in one pass
+// (writes both); covers F % 4 == 0, F <= 1024, 16-byte aligned features.
+bool gsddmm_softmax_fused(int64_t H, int64_t dh, const float* xs, const float* xd);
+hipError_t launch_gsddmm_softmax(const GraphView& g, const PlanView* plan, int64_t F,
+                                 const float* xs, const float* xd, bool leaky, float slope,
+                                 float* scores, float* att, hipStream_t stream);
+
 // Backward of gSpMM-max: zero-fills gsrc / gedge (either may be null), then
 // sends each upstream gradient element to the source of the edge the forward
 // picked (fp32 atomics).  eid_pos maps edge id -> storage position and is

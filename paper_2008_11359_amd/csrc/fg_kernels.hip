@@ -1424,6 +1424,127 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
 }
 
 // ----------------------------------------------------------------------------
+// SDDMM dot (one head) with the edge softmax of its scores fused in
+// ----------------------------------------------------------------------------
+
+// Scores are produced as in sddmm_fast_kernel (lane j collects the score of
+// edge j of each 64-edge batch) and written out; each lane also keeps a
+// running (max, sum) of the leaky scores it collected.  A wavefront merges
+// them in a fixed butterfly.  A whole row is then normalised: from registers
+// when it is a single batch, else by re-reading the scores this wavefront
+// just wrote (same lane, same address: program order).  A segment of a split
+// row publishes its (max, sum) for softmax_rowstats_kernel and
+// softmax_split_kernel.  The normalisation runs where the scores are made,
+// without a second launch re-reading them from memory.
+template <int G, int NV, int U, bool SEG>
+__global__ __launch_bounds__(kBlock) void sddmm_softmax_kernel(SddmmParams p, float* att,
+                                                               float* ws, int32_t leaky,
+                                                               float slope) {
+  constexpr int NG = kWave / G;
+  static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
+  const int64_t item = wave_item();
+  if (item >= p.n_items) return;
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;
+  if (it.b >= it.e) return;
+  const int lane = lane_id();
+  const int gid = lane / G;
+  const int li = lane % G;
+  const int64_t F = p.F;
+
+  int64_t f[NV];
+  bool act[NV];
+  float xd[NV][4];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    f[v] = (int64_t)(v * G + li) * 4;
+    act[v] = f[v] < F;
+    if (act[v]) {
+      load_vec<4>(p.xd + it.row * F + f[v], xd[v]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) xd[v][c] = 0.0f;
+    }
+  }
+
+  float m = -INFINITY, z = 0.0f;  // this lane's leaky scores so far
+  float res = 0.0f;
+  int cnt = 0, my_eid = 0;
+  for (int64_t base = it.b; base < it.e; base += kWave) {
+    cnt = (int)min((int64_t)kWave, it.e - base);
+    int my_src = 0;
+    my_eid = 0;
+    if (lane < cnt) {
+      my_src = __builtin_nontemporal_load(p.indices + base + lane);
+      my_eid = p.eids ? __builtin_nontemporal_load(p.eids + base + lane) : (int)(base + lane);
+    }
+    res = 0.0f;
+    for (int j0 = 0; j0 < cnt; j0 += NG * U) {
+      float val[U][NV][4];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int jb = j0 + u * NG;
+        ok[u] = jb + gid < cnt;
+        const int src = bcast_lane<NG>(my_src, jb, gid);
+        const float* xr = p.xs + (int64_t)src * F;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          if (ok[u] && act[v]) {
+            load_vec<4>(xr + f[v], val[u][v]);
+          } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) val[u][v][c] = 0.0f;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float part = 0.0f;
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) part += val[u][v][c] * xd[v][c];
+        part = group_sum<G>(part);
+        const int jb = j0 + u * NG;
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          if (jb + g < cnt) {
+            const int sum =
+                __builtin_amdgcn_readlane(__builtin_bit_cast(int, part), (g + 1) * G - 1);
+            if (lane == jb + g) res = __builtin_bit_cast(float, sum);
+          }
+        }
+      }
+    }
+    if (lane < cnt) {
+      p.out[my_eid] = res;
+      lse_push(m, z, leaky_relu(res, leaky, slope));
+    }
+  }
+  for (int off = 1; off < kWave; off <<= 1) {
+    const float om = __shfl_xor(m, off), oz = __shfl_xor(z, off);
+    lse_merge(m, z, om, oz);
+  }
+  if (SEG && it.slot >= 0) {
+    if (lane == 0) {
+      ws[(int64_t)it.slot * 2 + 0] = m;
+      ws[(int64_t)it.slot * 2 + 1] = z;
+    }
+    return;
+  }
+  const float inv = 1.0f / z;
+  if (it.e - it.b <= kWave) {
+    if (lane < cnt) att[my_eid] = expf(leaky_relu(res, leaky, slope) - m) * inv;
+    return;
+  }
+  for (int64_t q = it.b + lane; q < it.e; q += kWave) {
+    const int64_t e = p.eids ? (int64_t)p.eids[q] : q;
+    att[e] = expf(leaky_relu(p.out[e], leaky, slope) - m) * inv;
+  }
+}
+
+// ----------------------------------------------------------------------------
 // backward of gSpMM-max and of edge softmax
 // ----------------------------------------------------------------------------
 
@@ -2221,6 +2342,73 @@ hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, in
     else if (nv == 2) sddmm_scalar_go<2, 2, false>(prm, seg, grid, stream);
     else sddmm_scalar_go<4, 1, false>(prm, seg, grid, stream);
   }
+  return hipGetLastError();
+}
+
+bool gsddmm_softmax_fused(int64_t H, int64_t dh, const float* xs, const float* xd) {
+  const int64_t F = H * dh;
+  return H == 1 && F % 4 == 0 && F <= 4 * 4 * kWave && aligned16(xs) && aligned16(xd);
+}
+
+hipError_t launch_gsddmm_softmax(const GraphView& g, const PlanView* plan, int64_t F,
+                                 const float* xs, const float* xd, bool leaky, float slope,
+                                 float* scores, float* att, hipStream_t stream) {
+  if (g.num_rows == 0 || g.nnz == 0) return hipSuccess;
+  const bool seg = plan != nullptr;
+  SddmmParams prm;
+  prm.indptr = g.indptr;
+  prm.indices = g.indices;
+  prm.eids = g.edge_ids;
+  prm.xs = xs;
+  prm.xd = xd;
+  prm.out = scores;
+  prm.segs = seg ? plan->segs : nullptr;
+  prm.n_items = seg ? plan->num_segments : g.num_rows;
+  prm.F = F;
+  prm.H = 1;
+  prm.dh = (int32_t)F;
+  prm.logG = 6;
+  prm.logS = 0;
+  prm.out_vec4 = 0;
+  float* ws = seg ? plan->ws_f : nullptr;
+  const int32_t lk = leaky ? 1 : 0;
+  const dim3 grid = grid_for(prm.n_items, 1);
+  const int64_t Q = F / 4;
+#define FG_SDS(GG, NVV, UU)                                                                 \
+  if (seg) FG_LAUNCH((sddmm_softmax_kernel<GG, NVV, UU, true>), grid, stream, prm, att, ws, lk, \
+                     slope);                                                                \
+  else FG_LAUNCH((sddmm_softmax_kernel<GG, NVV, UU, false>), grid, stream, prm, att, ws, lk, slope);
+  if (Q <= 4) { FG_SDS(4, 1, 4) }
+  else if (Q <= 8) { FG_SDS(8, 1, 8) }
+  else if (Q <= 16) { FG_SDS(16, 1, 8) }
+  else if (Q <= 32) { FG_SDS(32, 1, 8) }
+  else if (Q <= 64) { FG_SDS(64, 1, 8) }
+  else if (Q <= 128) { FG_SDS(64, 2, 4) }
+  else { FG_SDS(64, 4, 2) }
+#undef FG_SDS
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || !seg || plan->num_slots == 0) return err;
+  // split rows: merge the segments' (max, sum), then normalise their edges
+  SoftmaxParams sp;
+  sp.indptr = g.indptr;
+  sp.eids = g.edge_ids;
+  sp.scores = scores;
+  sp.out = att;
+  sp.segs = plan->segs;
+  sp.fix = plan->fix;
+  sp.slot_fix = plan->slot_fix;
+  sp.slot_seg = plan->slot_seg;
+  sp.ws = plan->ws_f;
+  sp.ws_row = plan->ws_row;
+  sp.n_items = plan->num_segments;
+  sp.H = 1;
+  sp.leaky = lk;
+  sp.slope = slope;
+  sp.contig = (g.edge_ids == nullptr && aligned16(scores) && aligned16(att)) ? 1 : 0;
+  FG_LAUNCH(softmax_rowstats_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, sp);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  FG_LAUNCH(softmax_split_kernel, grid_for(plan->num_slots, 1), stream, sp, plan->num_slots);
   return hipGetLastError();
 }
 

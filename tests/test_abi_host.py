@@ -125,6 +125,24 @@ def test_edge_softmax_rejects_invalid_arguments():
     assert L.fg_edge_softmax(ctypes.byref(g), 1, FAKE_X, 1, 0.2, FAKE_X + 4, None, None) == -1
 
 
+def test_gsddmm_edge_softmax_rejects_invalid_arguments():
+    L = fg._lib
+    g = _graph_struct()
+    XS, XD, SC, OUT = 0x10000, 0x20000, 0x30000, 0x40000
+
+    def call(H=1, dh=8, xs=XS, xd=XD, sc=SC, out=OUT):
+        return L.fg_gsddmm_edge_softmax(ctypes.byref(g), H, dh, xs, xd, 1, 0.2, sc, out, None,
+                                        None)
+
+    assert call(H=0) == fg.FG_ERR_INVALID_ARG
+    assert call(dh=0) == fg.FG_ERR_INVALID_ARG
+    assert call(xs=None) == fg.FG_ERR_INVALID_ARG
+    assert call(sc=None) == fg.FG_ERR_INVALID_ARG
+    assert call(out=None) == fg.FG_ERR_INVALID_ARG
+    assert call(out=SC + 4) == fg.FG_ERR_INVALID_ARG   # weights overlap the scores
+    assert call(sc=XS + 16) == fg.FG_ERR_INVALID_ARG   # scores overlap x_src
+
+
 def test_gat_aggregate_rejects_invalid_or_unsupported_arguments():
     L = fg._lib
     g = _graph_struct()

@@ -152,6 +152,47 @@ def check_softmax(csr, G, scores, rows=None, plan=None, heads=1, leaky=True, nnz
     return res
 
 
+def check_sddmm_softmax(csr, G, xs, xd, rows=None, plan=None, heads=1, leaky=True,
+                        nnz_total=None):
+    """Fused SDDMM + edge softmax vs the oracle's gsddmm and edge_softmax of its
+    own scores.  Scores: the SDDMM tolerance.  Weights: the softmax tolerance
+    plus the first-order effect of the measured score difference,
+    2 * a * max over the row of |leaky(s_gpu) - leaky(s_ref)|."""
+    F = int(np.prod(xs.shape[1:]))
+    nt = csr.nnz if nnz_total is None else nnz_total
+    say("gsddmm_edge_softmax rows=%d nnz=%d F=%d H=%d leaky=%s plan=%s" % (
+        csr.num_rows, csr.nnz, F, heads, leaky,
+        None if plan is None else plan.info()["segment_edges"]))
+    sc, at = fg.gsddmm_edge_softmax(G, dev(xs), dev(xd), heads=heads, leaky=leaky, slope=0.2,
+                                    plan=plan)
+    sc, at = host(sc).reshape(nt, heads), host(at).reshape(nt, heads)
+    x2s, x2d = xs.reshape(csr.num_cols, F), xd.reshape(csr.num_rows, F)
+    s_ref, norm = O.gsddmm(csr, x2s, x2d, heads=heads, rows=rows, nnz_total=nt, with_norm=True)
+    a_ref = O.edge_softmax(csr, s_ref, heads=heads, leaky=leaky, slope=0.2, rows=rows,
+                           nnz_total=nt)
+    sel = np.arange(csr.num_rows) if rows is None else rows
+    pos = row_edges(csr, sel)
+    e = edge_ids_of(csr, pos)
+    assert_close_sum(sc[e], s_ref[e].astype(np.float64), norm[e], F // heads)
+
+    def lk(t):
+        t = t.astype(np.float64)
+        return np.where(t > 0, t, np.float64(np.float32(0.2)) * t) if leaky else t
+
+    d = np.abs(lk(sc[e]) - lk(s_ref[e]))
+    deg = csr.degrees()[sel]
+    starts = np.concatenate([[0], np.cumsum(deg)[:-1]])
+    nz = deg > 0
+    dmax = np.zeros((sel.size, heads))
+    dmax[nz] = np.maximum.reduceat(d, starts[nz], axis=0)
+    dm = np.repeat(dmax, deg, axis=0)
+    n = np.repeat(deg, deg)[:, None]
+    bound = 1e-5 * np.sqrt(np.maximum(n, 1)) * a_ref[e] + 2 * a_ref[e] * dm + 1e-12
+    bad = np.abs(at[e].astype(np.float64) - a_ref[e]) > bound
+    assert not bad.any(), "fused softmax mismatch at %s: %r vs %r" % (
+        np.argwhere(bad)[0], at[e][bad][0], a_ref[e][bad][0])
+
+
 def check_gat(csr, G, x, rows=None, plan=None, heads=1, leaky=True):
     """Fused attention aggregation vs the oracle's gsddmm -> edge_softmax ->
     gspmm(src_mul_edge, sum) on the selected rows."""
@@ -342,10 +383,11 @@ def test_tiny_uniform_all_ops():
         check_spmm(csr, G, xi, plan=plan, reduce="max")  # many ties
         check_spmm(csr, G, x, plan=plan, edge=wgt)
         check_spmm(csr, G, x, plan=plan, edge=wgt, reduce="max")
-        s = check_sddmm(csr, G, x, x, plan=plan)
+        check_sddmm(csr, G, x, x, plan=plan)
         check_sddmm(csr, G, xi, xi, plan=plan, exact=True)
-        check_softmax(csr, G, host(s), plan=plan)
-        check_softmax(csr, G, host(s), plan=plan, leaky=False)
+        s_ref = O.gsddmm(csr, x, x)  # the oracle's scores feed both sides
+        check_softmax(csr, G, s_ref, plan=plan)
+        check_softmax(csr, G, s_ref, plan=plan, leaky=False)
 
 
 # ----------------------------------------------------------------------------
@@ -382,11 +424,14 @@ def test_heads(small_rmat, heads, dh):
     csr, G = small_rmat
     rng = np.random.default_rng(heads * 100 + dh)
     x = rng.standard_normal((csr.num_cols, heads, dh)).astype(np.float32)
+    x2 = x.reshape(csr.num_cols, heads * dh)
+    s_ref = O.gsddmm(csr, x2, x2, heads=heads)  # oracle scores and weights feed both sides
+    a_ref = O.edge_softmax(csr, s_ref, heads=heads, leaky=True, slope=0.2)
     for plan in plans_for(G, heads * dh, sizes=(64,)):
-        s = check_sddmm(csr, G, x, x, plan=plan, heads=heads)
-        a = check_softmax(csr, G, host(s), plan=plan, heads=heads)
-        check_spmm(csr, G, x, plan=plan, edge=host(a), heads=heads)
-        check_spmm(csr, G, x, plan=plan, edge=host(a), heads=heads, reduce="max")
+        check_sddmm(csr, G, x, x, plan=plan, heads=heads)
+        check_softmax(csr, G, s_ref, plan=plan, heads=heads)
+        check_spmm(csr, G, x, plan=plan, edge=a_ref, heads=heads)
+        check_spmm(csr, G, x, plan=plan, edge=a_ref, heads=heads, reduce="max")
 
 
 @pytest.mark.parametrize("heads,dh", [(8, 16), (1, 128), (2, 32), (4, 8), (1, 4), (16, 16),
@@ -489,6 +534,30 @@ def test_mlp_aggregate_transposed_and_empty(small_rmat):
     o, a = fg.mlp_aggregate(G0, dev(np.ones((5, 8), np.float32)), dev(np.ones((8, 4), np.float32)),
                             x_dst=dev(np.ones((3, 8), np.float32)))
     assert np.all(host(o) == 0) and np.all(host(a) == -1)
+
+
+@pytest.mark.parametrize("d", [4, 16, 33, 64, 128, 512, 1024, 1040])
+def test_sddmm_edge_softmax(small_rmat, d):
+    csr, G = small_rmat
+    rng = np.random.default_rng(d + 5)
+    x = (rng.standard_normal((csr.num_cols, d)) / math.sqrt(d) * 3).astype(np.float32)
+    xd = (rng.standard_normal((csr.num_rows, d)) / math.sqrt(d) * 3).astype(np.float32)
+    for plan in plans_for(G, d, sizes=(1, 64)):
+        check_sddmm_softmax(csr, G, x, xd, plan=plan)
+    check_sddmm_softmax(csr, G, x, xd, plan=fg.Plan(G, d, segment_edges=64), leaky=False)
+
+
+def test_sddmm_edge_softmax_heads_and_transposed(small_rmat):
+    csr, G = small_rmat
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((csr.num_cols, 8, 16)).astype(np.float32) * 0.5
+    check_sddmm_softmax(csr, G, x, x, heads=8, plan=fg.Plan(G, 128, segment_edges=64))
+    csc = csr_to_csc(csr)
+    Gt = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+    y = rng.standard_normal((csc.num_cols, 32)).astype(np.float32) * 0.3
+    yd = rng.standard_normal((csc.num_rows, 32)).astype(np.float32) * 0.3
+    for plan in (None, fg.Plan(Gt, 32, segment_edges=64)):
+        check_sddmm_softmax(csc, Gt, y, yd, plan=plan, nnz_total=csr.nnz)
 
 
 def test_gat_fused_unsupported_shape_raises(small_rmat):
@@ -640,8 +709,13 @@ def test_rmat_233k_full(rmat_full):
     rows = sample_rows(csr, 2000, 3)
     check_spmm(csr, G, x, rows=rows, plan=plan, edge=wgt)
     check_spmm(csr, G, x, rows=rows, plan=plan, reduce="max")
-    s = check_sddmm(csr, G, x, x, rows=rows, plan=plan)
-    check_softmax(csr, G, host(s), rows=rows, plan=plan)
+    check_sddmm(csr, G, x, x, rows=rows, plan=plan)
+    # softmax on seeded scores of the SDDMM's scale (N(0, d)), the same array on both sides
+    s_syn = (np.random.default_rng(31).standard_normal(csr.nnz, dtype=np.float32)
+             * np.float32(math.sqrt(128)))
+    check_softmax(csr, G, s_syn, rows=rows, plan=plan)
+    # SDDMM and softmax fused, in the benchmark's launch configuration
+    check_sddmm_softmax(csr, G, x, x, rows=rows, plan=plan)
     check_spmm(csr, G, x, rows=rows, plan=pplan, edge=wgt)
     check_spmm(csr, G, x, rows=rows, plan=pplan, reduce="max")
     check_sddmm(csr, G, x, x, rows=rows, plan=pplan)
@@ -683,9 +757,14 @@ def test_clustered_gat_layer_full():
     x = w.arrays["x"]
     plan = fg.Plan(G, 128)
     rows = sample_rows(csr, 1500, 4)
-    s = check_sddmm(csr, G, x, x, rows=rows, plan=plan, heads=8)
-    a = check_softmax(csr, G, host(s), rows=rows, plan=plan, heads=8)
-    check_spmm(csr, G, x, rows=rows, plan=plan, edge=host(a), heads=8)
+    check_sddmm(csr, G, x, x, rows=rows, plan=plan, heads=8)
+    # softmax and weighted aggregation on seeded scores of the SDDMM's scale
+    # (N(0, dh)); the aggregation's weights are the oracle's softmax of them
+    s_syn = (np.random.default_rng(32).standard_normal((csr.nnz, 8), dtype=np.float32)
+             * np.float32(4.0))
+    a = check_softmax(csr, G, s_syn, rows=rows, plan=plan, heads=8)
+    a_ref = O.edge_softmax(csr, s_syn, heads=8, leaky=True, slope=0.2)
+    check_spmm(csr, G, x, rows=rows, plan=plan, edge=a_ref, heads=8)
     # softmax rows sum to one for every row and head
     rs = np.add.reduceat(host(a).astype(np.float64), csr.indptr[:-1], axis=0)
     np.testing.assert_allclose(rs, 1.0, atol=1e-5 * math.sqrt(300))
@@ -693,7 +772,7 @@ def test_clustered_gat_layer_full():
     check_gat(csr, G, x, rows=rows, plan=plan, heads=8)
     # gradient of the softmax (upstream gradient of the attention weights)
     ga = np.random.default_rng(9).standard_normal((csr.nnz, 8)).astype(np.float32)
-    check_softmax_backward(csr, G, host(s), ga, rows=rows, plan=plan, heads=8)
+    check_softmax_backward(csr, G, s_syn, ga, rows=rows, plan=plan, heads=8)
 
 
 @pytest.mark.slow
