@@ -619,8 +619,8 @@ def main():
         summarize_counters(*args.summarize_counters, TRAFFIC_FILE)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the path runs on a single MI355X and this build "
-              "has no multi-GPU mode (got --gpus %d)" % args.gpus, file=sys.stderr)
+        print("bench.py measures one GPU only: the library runs on a single MI355X and has no "
+              "multi-GPU mode (got --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     import torch
