@@ -3,6 +3,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <climits>
 #include <cstdint>
 #include <cstring>
 #include <new>
@@ -432,6 +433,21 @@ fg_status upload(fg_plan* p, const Schedule& sc, fg::PlanView& v, hipStream_t hs
   v.slot_fix = static_cast<const int32_t*>(c);
   v.slot_seg = static_cast<const int32_t*>(d);
   v.num_segments = (int64_t)sc.segs.size();
+  // leading long items, then short non-empty rows, then empty rows (the
+  // plain schedule's order); any other order keeps every item in the first class
+  int64_t nl = 0, nn = 0;
+  bool ordered = true, short_whole = true;
+  int64_t prev = INT64_MAX;
+  for (const fg::Seg& sg : sc.segs) {
+    const int64_t len = (int64_t)sg.end - sg.begin;
+    if (sg.row < 0 || len > prev) ordered = false;
+    prev = len;
+    if (len > fg::kShortRowEdges) ++nl;
+    else if (len > 0 && sg.slot >= 0) short_whole = false;  // a piece of a split row
+    if (len > 0) ++nn;
+  }
+  v.num_nonempty = ordered ? nn : v.num_segments;
+  v.num_long = (ordered && short_whole) ? nl : v.num_nonempty;
   v.num_split_rows = (int64_t)sc.fix.size();
   v.num_slots = (int64_t)sc.slot_fix.size();
   return FG_OK;

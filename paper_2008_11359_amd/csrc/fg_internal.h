@@ -28,7 +28,16 @@ struct PlanView {
   float* ws_row = nullptr;        // [num_split_rows * ws_width] merged per-row values
   int64_t num_segments = 0, num_split_rows = 0, num_slots = 0;
   int64_t ws_width = 0;           // floats per slot
+  // items are ordered longest first with empty rows last: [0, num_long) have
+  // more than kShortRowEdges edges, [num_long, num_nonempty) at most that
+  // many (whole rows), the rest none (a partitioned schedule sets both to
+  // num_segments)
+  int64_t num_long = 0, num_nonempty = 0;
 };
+
+// Rows of at most this many edges are short: the edge softmax packs four of
+// them into one wavefront.
+constexpr int kShortRowEdges = 64;
 
 struct GraphView {
   int64_t num_rows, num_cols, nnz, nnz_total;

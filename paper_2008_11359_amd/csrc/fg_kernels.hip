@@ -1852,6 +1852,54 @@ __global__ __launch_bounds__(kBlock) void softmax_bwd_split_kernel(SoftmaxBwdPar
   }
 }
 
+// Short single-head rows (at most kShortRowEdges edges, whole rows): four
+// per wavefront, a 16-lane quarter per row holding up to 4 scores per lane;
+// max and sum reduce within the quarter.  Items [first, last) of the plan.
+constexpr int kPackLanes = 16;
+static_assert(kShortRowEdges <= kPackLanes * 4, "a short row must fit one quarter");
+
+__global__ __launch_bounds__(kBlock) void softmax_pack_kernel(SoftmaxParams p, int64_t first,
+                                                              int64_t last) {
+  const int64_t w = wave_item();
+  const int64_t item0 = first + w * (kWave / kPackLanes);
+  if (item0 >= last) return;
+  const int lane = lane_id();
+  const int64_t item = item0 + lane / kPackLanes;
+  const int j = lane % kPackLanes;
+  int64_t b = 0, e = 0;
+  if (item < last) {
+    const Seg sg = p.segs[item];
+    b = sg.begin;
+    e = sg.end;
+  }
+  float v[4];
+  int64_t ev[4];
+  float m = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int64_t q = b + j + (int64_t)k * kPackLanes;
+    ev[k] = -1;
+    v[k] = -INFINITY;
+    if (q < e) {
+      ev[k] = p.eids ? p.eids[q] : q;
+      v[k] = leaky_relu(p.scores[ev[k]], p.leaky, p.slope);
+    }
+    m = fmaxf(m, v[k]);
+  }
+  for (int off = 1; off < kPackLanes; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
+  float z = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    v[k] = ev[k] >= 0 ? expf(v[k] - m) : 0.0f;
+    z += v[k];
+  }
+  for (int off = 1; off < kPackLanes; off <<= 1) z += __shfl_xor(z, off);
+  const float inv = 1.0f / z;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    if (ev[k] >= 0) p.out[ev[k]] = v[k] * inv;
+}
+
 // ----------------------------------------------------------------------------
 // fused attention aggregation: SDDMM -> leaky ReLU -> edge softmax -> gSpMM
 // ----------------------------------------------------------------------------
@@ -2291,7 +2339,7 @@ hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, in
   prm.xd = xd;
   prm.out = out;
   prm.segs = seg ? plan->segs : nullptr;
-  prm.n_items = seg ? plan->num_segments : g.num_rows;
+  prm.n_items = seg ? plan->num_nonempty : g.num_rows;  // empty rows (last) write nothing
   prm.F = F;
   prm.H = (int32_t)H;
   prm.dh = (int32_t)dh;
@@ -2363,7 +2411,7 @@ hipError_t launch_gsddmm_softmax(const GraphView& g, const PlanView* plan, int64
   prm.xd = xd;
   prm.out = scores;
   prm.segs = seg ? plan->segs : nullptr;
-  prm.n_items = seg ? plan->num_segments : g.num_rows;
+  prm.n_items = seg ? plan->num_nonempty : g.num_rows;  // empty rows write nothing
   prm.F = F;
   prm.H = 1;
   prm.dh = (int32_t)F;
@@ -2433,11 +2481,27 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
   prm.slope = slope;
   prm.contig = (g.edge_ids == nullptr && H <= kWave && (H & (H - 1)) == 0 && aligned16(scores) &&
                 aligned16(out)) ? 1 : 0;
-  const dim3 grid = grid_for(prm.n_items, 1);
-  if (plan) FG_LAUNCH((softmax_kernel<true>), grid, stream, prm);
-  else FG_LAUNCH((softmax_kernel<false>), grid, stream, prm);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess || !plan || plan->num_slots == 0) return err;
+  // with a plan: empty rows (last) need no work; short single-head rows go
+  // four to a wavefront
+  const bool pack = plan && H == 1 && plan->num_long < plan->num_nonempty;
+  if (plan) prm.n_items = pack ? plan->num_long : plan->num_nonempty;
+  hipError_t err = hipSuccess;
+  if (prm.n_items > 0) {
+    const dim3 grid = grid_for(prm.n_items, 1);
+    if (plan) FG_LAUNCH((softmax_kernel<true>), grid, stream, prm);
+    else FG_LAUNCH((softmax_kernel<false>), grid, stream, prm);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  if (pack) {
+    const int64_t rows = plan->num_nonempty - plan->num_long;
+    const int64_t per = kWave / kPackLanes;
+    FG_LAUNCH(softmax_pack_kernel, grid_for((rows + per - 1) / per, 1), stream, prm,
+              plan->num_long, plan->num_nonempty);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  if (!plan || plan->num_slots == 0) return err;
   FG_LAUNCH(softmax_rowstats_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, prm);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
@@ -2564,7 +2628,7 @@ hipError_t launch_edge_softmax_backward(const GraphView& g, const PlanView* plan
   prm.slot_fix = plan ? plan->slot_fix : nullptr;
   prm.slot_seg = plan ? plan->slot_seg : nullptr;
   prm.ws = plan ? plan->ws_f : nullptr;
-  prm.n_items = plan ? plan->num_segments : g.num_rows;
+  prm.n_items = plan ? plan->num_nonempty : g.num_rows;  // empty rows (last) need no work
   prm.H = (int32_t)H;
   prm.leaky = leaky ? 1 : 0;
   prm.slope = slope;
