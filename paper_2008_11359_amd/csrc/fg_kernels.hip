@@ -1966,10 +1966,16 @@ __device__ __forceinline__ void attn_merge(float& m, float& z, float (&acc)[4], 
 // leaky ReLU, then an online-softmax update of (max, exp-sum, weighted sum of
 // the same gathered source row).  The source row is read once per edge and no
 // per-edge score is written.
-template <int G, bool SEG>
+// SH: lanes per head (dh / 4), a compile-time constant so the per-edge head
+// reduction has no branches.  The running (max, sum, weighted sum) of a head
+// is rescaled only when a score exceeds the current maximum (a branch the
+// whole wavefront skips when no lane needs it); otherwise an edge costs one
+// exponential and a multiply-add per feature.
+template <int G, int SH, bool SEG>
 __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
   constexpr int NG = kWave / G;
   constexpr int U = NG * 4 <= kWave ? 4 : 1;
+  static_assert(SH <= G, "a head's lanes lie inside one lane group");
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -2008,24 +2014,20 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         float part = val[u][0] * xd[0] + val[u][1] * xd[1] + val[u][2] * xd[2] + val[u][3] * xd[3];
-        float sc;
-        switch (p.SH) {  // wave-uniform
-          case 1: sc = part; break;
-          case 2: sc = group_allsum<2>(part, gid); break;
-          case 4: sc = group_allsum<4>(part, gid); break;
-          case 8: sc = group_allsum<8>(part, gid); break;
-          case 16: sc = group_allsum<16>(part, gid); break;
-          case 32: sc = group_allsum<32>(part, gid); break;
-          default: sc = group_allsum<64>(part, gid); break;
-        }
+        float sc = SH == 1 ? part : group_allsum<SH>(part, gid);
         sc = leaky_relu(sc, p.leaky, p.slope);
         if (ok[u]) {
-          const float nm = fmaxf(m, sc);
-          const float a = expf(m - nm), b = expf(sc - nm);
-          z = z * a + b;
+          if (sc > m) {  // new maximum: move the state to it (m = -inf: a = 0)
+            const float a = expf(m - sc);
+            z *= a;
 #pragma unroll
-          for (int c = 0; c < 4; ++c) acc[c] = acc[c] * a + b * val[u][c];
-          m = nm;
+            for (int c = 0; c < 4; ++c) acc[c] *= a;
+            m = sc;
+          }
+          const float b = expf(sc - m);
+          z += b;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[c] = fmaf(b, val[u][c], acc[c]);
         }
       }
     }
@@ -2540,9 +2542,19 @@ hipError_t launch_gat_fused(const GraphView& g, const PlanView* plan, int64_t H,
   const int64_t Q = prm.F / 4;
   const int G = Q <= 4 ? 4 : Q <= 8 ? 8 : Q <= 16 ? 16 : Q <= 32 ? 32 : 64;
   // lanes of a head must not straddle the group (SH <= G always holds: dh <= F)
+#define FG_GAT2(GG, SS)                                                        \
+  if (seg) FG_LAUNCH((gat_fused_kernel<GG, SS, true>), grid, stream, prm);     \
+  else FG_LAUNCH((gat_fused_kernel<GG, SS, false>), grid, stream, prm);
 #define FG_GAT(GG)                                                             \
-  if (seg) FG_LAUNCH((gat_fused_kernel<GG, true>), grid, stream, prm);         \
-  else FG_LAUNCH((gat_fused_kernel<GG, false>), grid, stream, prm);
+  switch (prm.SH) {                                                            \
+    case 1: { FG_GAT2(GG, 1) } break;                                          \
+    case 2: { FG_GAT2(GG, (GG >= 2 ? 2 : 1)) } break;                          \
+    case 4: { FG_GAT2(GG, (GG >= 4 ? 4 : 1)) } break;                          \
+    case 8: { FG_GAT2(GG, (GG >= 8 ? 8 : 1)) } break;                          \
+    case 16: { FG_GAT2(GG, (GG >= 16 ? 16 : 1)) } break;                       \
+    case 32: { FG_GAT2(GG, (GG >= 32 ? 32 : 1)) } break;                       \
+    default: { FG_GAT2(GG, (GG >= 64 ? 64 : 1)) } break;                       \
+  }
   switch (G) {
     case 4: FG_GAT(4) break;
     case 8: FG_GAT(8) break;
@@ -2551,6 +2563,7 @@ hipError_t launch_gat_fused(const GraphView& g, const PlanView* plan, int64_t H,
     default: FG_GAT(64) break;
   }
 #undef FG_GAT
+#undef FG_GAT2
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || !seg || plan->num_split_rows == 0) return err;
   FG_LAUNCH(gat_fixup_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, prm, plan->fix);
