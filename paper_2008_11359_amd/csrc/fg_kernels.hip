@@ -284,19 +284,67 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
     }
   }
 
+  // TAB with edge ids: the edge values of batch k+1 are fetched into
+  // registers while batch k computes (ids two batches ahead)
+  constexpr bool PIPE = TAB && EIDS;
+  float qn[PIPE ? kTabHeads : 1];
+  int eid_n1 = 0, eid_n2 = 0;  // edge ids of the next batch and the one after
+  auto fetch_ids = [&](int64_t b0, int& e) {
+    e = 0;
+    const int c = (int)min((int64_t)kWave, it.e - b0);
+    if (b0 < it.e && lane < c) e = __builtin_nontemporal_load(p.eids + b0 + lane);
+  };
+  auto fetch_vals = [&](int64_t b0, int e) {
+    const int c = (int)min((int64_t)kWave, it.e - b0);
+    if (b0 < it.e && lane < c) {
+      const float* er = p.ev + (int64_t)e * p.H;
+#pragma unroll
+      for (int h = 0; h < kTabHeads; h += 4)
+        if (h < p.H) {
+          if (p.ev_vec4) {
+            float q4[4];
+            load_vec<4>(er + h, q4);
+#pragma unroll
+            for (int c4 = 0; c4 < 4; ++c4) qn[h + c4] = q4[c4];
+          } else {
+#pragma unroll
+            for (int c4 = 0; c4 < 4; ++c4)
+              if (h + c4 < p.H) qn[h + c4] = er[h + c4];
+          }
+        }
+    }
+  };
+  if constexpr (PIPE) {
+    fetch_ids(it.b, eid_n1);
+    fetch_vals(it.b, eid_n1);
+    fetch_ids(it.b + kWave, eid_n2);
+  }
   for (int64_t base = it.b; base < it.e; base += kWave) {
     const int cnt = (int)min((int64_t)kWave, it.e - base);
     int my_src = 0, my_eid = 0;
     float my_w = 0.0f;
     if (lane < cnt) {
       my_src = __builtin_nontemporal_load(p.indices + base + lane);
-      if constexpr (EIDS) my_eid = __builtin_nontemporal_load(p.eids + base + lane);
+      if constexpr (PIPE) my_eid = eid_n1;
+      else if constexpr (EIDS) my_eid = __builtin_nontemporal_load(p.eids + base + lane);
       else my_eid = (int)(base + lane);
       if constexpr (MUL) {
         if (p.H == 1) my_w = p.ev[my_eid];
       }
     }
-    if constexpr (TAB) {
+    if constexpr (PIPE) {
+      wave_lds_sync();
+      if (lane < cnt) {
+        float* tr = tab + lane * p.H;
+#pragma unroll
+        for (int h = 0; h < kTabHeads; ++h)
+          if (h < p.H) tr[h] = qn[h];
+      }
+      wave_lds_sync();
+      eid_n1 = eid_n2;
+      fetch_vals(base + kWave, eid_n1);       // next batch's values, in flight during this one
+      fetch_ids(base + 2 * kWave, eid_n2);
+    } else if constexpr (TAB) {
       wave_lds_sync();  // the previous batch's table reads are done
       if (lane < cnt) {
         const float* er = p.ev + (int64_t)my_eid * p.H;

@@ -584,6 +584,12 @@ def test_transposed_graph_with_edge_ids(small_rmat):
         check_sddmm(csc, G, y, x, plan=plan, nnz_total=csr.nnz)
         check_softmax(csc, G, rng.standard_normal(csr.nnz).astype(np.float32), plan=plan,
                       nnz_total=csr.nnz)
+    # per-head edge values through edge ids (staged a batch ahead), 4 heads of 8
+    y4 = rng.standard_normal((csc.num_cols, 4, 8)).astype(np.float32)
+    w4 = rng.random((csr.nnz, 4), dtype=np.float32)
+    for plan in plans_for(G, 32, sizes=(0, 16)):
+        check_spmm(csc, G, y4, plan=plan, edge=w4, heads=4, nnz_total=csr.nnz)
+        check_spmm(csc, G, y4, plan=plan, edge=w4, heads=4, reduce="max", nnz_total=csr.nnz)
 
 
 def test_edge_cases():
