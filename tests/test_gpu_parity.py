@@ -783,6 +783,55 @@ def test_clustered_gat_layer_full():
 
 
 @pytest.mark.slow
+def test_clustered_gat_backward_full():
+    """Backward of the attention layer on the whole clustered graph in the
+    benchmark's launch configuration: per-head aggregations on the transposed
+    graph, which read the edge values through edge ids, and the per-head
+    gradient SDDMM."""
+    w = make_config("clustered_133k_deg300")
+    csr = w.csr
+    csc = csr_to_csc(csr)
+    G = fg.Graph.from_csr(csr)
+    Gt = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+    x = w.arrays["x"]
+    n, H, dh = x.shape
+    gy = np.random.default_rng(12).standard_normal((n, H, dh)).astype(np.float32)
+    a = O.edge_softmax(csr, (np.random.default_rng(33).standard_normal((csr.nnz, H),
+                                                                       dtype=np.float32)
+                             * np.float32(4.0)), heads=H, leaky=True, slope=0.2)
+    ds = np.random.default_rng(34).standard_normal((csr.nnz, H)).astype(np.float32) * 1e-2
+    P, Pt = fg.Plan(G, H * dh), fg.Plan(Gt, H * dh)
+    rows = sample_rows(csr, 1000, 13)
+    rows_t = sample_rows(csc, 1000, 14)
+    check_spmm(csc, Gt, gy, rows=rows_t, plan=Pt, edge=a, heads=H, nnz_total=csr.nnz)
+    check_spmm(csc, Gt, x, rows=rows_t, plan=Pt, edge=ds, heads=H, nnz_total=csr.nnz)
+    check_spmm(csc, Gt, x, rows=rows_t, plan=None, edge=ds, heads=H, nnz_total=csr.nnz)
+    check_spmm(csr, G, x, rows=rows, plan=P, edge=ds, heads=H)
+    check_sddmm(csr, G, x, gy, rows=rows, plan=P, heads=H)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("d", [32, 128])
+def test_rand_100k_full(d):
+    """The two-degree-class graph (20K vertices at mean in-degree 2000, 80K
+    at 100) under the default and the source-partitioned schedules."""
+    w = make_config("rand_100k_48m", d=d)
+    csr = w.csr
+    G = fg.Graph.from_csr(csr)
+    x = w.arrays["x"]
+    rows = sample_rows(csr, 600, 15 + d)
+    plan = fg.Plan(G, d)
+    pplan = fg.Plan(G, d, source_slab_rows=-1)
+    assert pplan.info()["num_partitioned_rows"] > 0
+    for p in (plan, pplan):
+        check_spmm(csr, G, x, rows=rows, plan=p)
+        check_spmm(csr, G, x, rows=rows, plan=p, reduce="max")
+        check_sddmm(csr, G, x, x, rows=rows, plan=p)
+    o = host(fg.gspmm(G, dev(np.ones((csr.num_cols, d), np.float32)), plan=pplan))
+    np.testing.assert_array_equal(o[:, -1], csr.degrees().astype(np.float32))
+
+
+@pytest.mark.slow
 def test_rmat_train_step_full():
     w = make_config("rmat_1m_33m_train")
     csr, csc = w.csr, w.csc
