@@ -113,13 +113,18 @@ typedef struct fg_graph {
  *    items first, rows without edges last;
  *  - gather (gSpMM, gSDDMM, fused attention): as plain by default.  With
  *    source partitioning (opt-in, source_slab_rows != 0), rows with at least
- *    max(partition_min_degree, 32 * ceil(num_cols / source_slab_rows)) edges
- *    and sorted source ids are cut where their sources change slab (slabs:
+ *    partition_min_degree edges (if given; else max(64, 8 * ceil(num_cols /
+ *    source_slab_rows)), so that pieces average 8 edges or more) and sorted
+ *    source ids are cut where their sources change slab (slabs:
  *    consecutive source ids, at most source_slab_rows of them and about equal
  *    shares of these rows' edges), then into pieces of at most S edges; each
  *    slab runs on one die (slabs dealt in order to the least-loaded die), so
- *    the die finds the slab's feature rows in its L2 (more L2 hits, more
- *    pieces to merge).
+ *    each die gathers from a narrow band of the feature matrix at a time
+ *    (more hits in its L2 and the Infinity Cache, at the price of more
+ *    pieces to merge).  This pays on graphs whose gathers have no locality
+ *    of their own (sources spread uniformly, or features beyond the Infinity
+ *    Cache) and costs more than it saves on graphs with hubs or communities,
+ *    hence opt-in.
  * Items of rows cut in several pieces write partial results that a second
  * pass merges in a fixed order, so results are deterministic for a plan.
  * ------------------------------------------------------------------------- */
@@ -130,8 +135,12 @@ typedef struct fg_plan_options {
   int32_t max_row_segments;     /* cap on items per row (plain cut); 0 -> 128        */
   int32_t source_slab_rows;     /* source ids per slab of the gather schedule;
                                    0 -> no source partitioning (default);
-                                   negative -> 2 MiB of features at max_width        */
-  int32_t partition_min_degree; /* smallest row cut by slabs; 0 -> default (1024)    */
+                                   negative -> automatic: the larger of 8 MiB of
+                                   features at max_width and num_cols / 16, and
+                                   none if the num_cols x max_width features fit
+                                   in 32 MiB (the dies' L2s together)                */
+  int32_t partition_min_degree; /* smallest row cut by slabs; 0 -> max(64, 8 *
+                                   number of id slabs)                              */
   int32_t reserved[4];          /* must be zero                                      */
 } fg_plan_options;
 

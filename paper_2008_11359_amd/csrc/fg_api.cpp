@@ -39,7 +39,6 @@ constexpr int32_t kDefaultSegmentEdges = 4096;
 constexpr int32_t kMaxSegmentEdges = 1 << 24;
 constexpr int32_t kDefaultMaxRowSegments = 128;
 constexpr int32_t kMaxRowSegmentsLimit = 1 << 20;
-constexpr int32_t kDefaultPartitionMinDegree = 1024;
 
 fg_status check_graph(const fg_graph* g) {
   if (!g) return FG_ERR_INVALID_ARG;
@@ -100,11 +99,20 @@ bool indptr_valid(const int32_t* ip, int64_t num_rows, int64_t nnz) {
 
 constexpr int kXcds = 8;            // MI355X: 8 accelerator dies, workgroups dealt round-robin
 constexpr int kWavesPerGroup = 4;   // work items per workgroup (kernels launch 4 wavefronts)
-constexpr int64_t kSlabBytes = 2 << 20;  // source slab held in one die's L2 (4 MB) with room to spare
-constexpr int64_t kMinTileEdges = 32;    // partition a row only if tiles average this many edges
+// automatic slab width: the larger of 8 MiB of features and 1/16 of the
+// source feature matrix (measured best on graphs without gather locality)
+constexpr int64_t kAutoSlabBytes = 8 << 20;
+constexpr int64_t kAutoSlabsPerMatrix = 16;
+// automatic mode leaves feature matrices that the eight dies' L2s (4 MB
+// each) hold together unpartitioned: there the pieces cost more than they save
+constexpr int64_t kAutoMinMatrixBytes = int64_t(kXcds) * (4 << 20);
+// unless given, the smallest partitioned row has max(64, 8 * id slabs) edges:
+// its pieces average at least 8 edges
+constexpr int64_t kMinPartitionDegree = 64;
+constexpr int64_t kMinPieceEdges = 8;
 
 struct Options {
-  int32_t S, cap, slab, min_deg;
+  int32_t S, cap, slab, min_deg;  // slab 0: no source partitioning
 };
 
 struct Schedule {
@@ -179,8 +187,8 @@ void build_plain(const int32_t* ip, int64_t num_rows, const Options& o, Schedule
 
 // Gather schedule with source partitioning (the paper's 1D graph partitioning
 // of source vertices, Sec. III-C, sized for one die's L2 instead of a CPU's
-// LLC).  A row with at least max(min_deg, kMinTileEdges * ceil(num_cols /
-// o.slab)) edges whose sources are sorted is partitioned.  Source ids are cut
+// LLC).  A row with at least o.min_deg edges whose sources are sorted is
+// partitioned.  Source ids are cut
 // into consecutive slabs of at most o.slab vertices that also hold about equal
 // shares of the partitioned rows' edges (so that labellings which put the
 // busy sources together still spread over the dies); partitioned rows are cut
@@ -195,9 +203,10 @@ void build_plain(const int32_t* ip, int64_t num_rows, const Options& o, Schedule
 // (row = -1) that the kernels skip.
 bool build_partitioned(const int32_t* ip, const int32_t* ix, int64_t num_rows, int64_t num_cols,
                        const Options& o, Schedule& sc) {
+  if (o.slab <= 0) return false;
   const int64_t id_slabs = (num_cols + o.slab - 1) / o.slab;
-  if (o.slab <= 0 || id_slabs < 2) return false;
-  const int64_t min_deg = std::max<int64_t>(o.min_deg, kMinTileEdges * id_slabs);
+  if (id_slabs < 2) return false;
+  const int64_t min_deg = o.min_deg;
   // partitioned rows and the edges each source contributes to them
   std::vector<char> part_row((size_t)num_rows, 0);
   std::vector<int64_t> work((size_t)num_cols, 0);
@@ -297,11 +306,12 @@ bool build_partitioned(const int32_t* ip, const int32_t* ix, int64_t num_rows, i
   return true;
 }
 
-fg_status read_options(const fg_plan_options* opt, int64_t max_width, Options* o) {
+fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max_width,
+                       Options* o) {
   o->S = kDefaultSegmentEdges;
   o->cap = kDefaultMaxRowSegments;
   o->slab = 0;  // source partitioning is opt-in (see fg_plan_options)
-  o->min_deg = kDefaultPartitionMinDegree;
+  o->min_deg = 0;
   if (!opt) return FG_OK;
   for (int32_t r : opt->reserved)
     if (r != 0) return FG_ERR_INVALID_ARG;
@@ -313,10 +323,19 @@ fg_status read_options(const fg_plan_options* opt, int64_t max_width, Options* o
   if (opt->max_row_segments) o->cap = opt->max_row_segments;
   if (opt->source_slab_rows > 0) {
     o->slab = opt->source_slab_rows;
-  } else if (opt->source_slab_rows < 0) {  // automatic: 2 MiB of features per slab
-    o->slab = (int32_t)std::max<int64_t>(64, kSlabBytes / (4 * std::max<int64_t>(max_width, 1)));
+  } else if (opt->source_slab_rows < 0 &&
+             num_cols * 4 * std::max<int64_t>(max_width, 1) > kAutoMinMatrixBytes) {
+    const int64_t rows = std::max<int64_t>(kAutoSlabBytes / (4 * std::max<int64_t>(max_width, 1)),
+                                           (num_cols + kAutoSlabsPerMatrix - 1) / kAutoSlabsPerMatrix);
+    o->slab = (int32_t)std::min<int64_t>(std::max<int64_t>(64, rows), INT32_MAX);
   }
-  if (opt->partition_min_degree) o->min_deg = opt->partition_min_degree;
+  if (o->slab > 0) {
+    const int64_t id_slabs = (std::max<int64_t>(num_cols, 1) + o->slab - 1) / o->slab;
+    o->min_deg = opt->partition_min_degree
+                     ? opt->partition_min_degree
+                     : (int32_t)std::min<int64_t>(
+                           std::max(kMinPartitionDegree, kMinPieceEdges * id_slabs), INT32_MAX);
+  }
   if (o->cap < 2) return FG_ERR_INVALID_ARG;
   return FG_OK;
 }
@@ -369,7 +388,7 @@ fg_status fg_schedule_host(const int32_t* indptr_host, const int32_t* indices_ho
     return FG_ERR_INVALID_ARG;
   if (max_width < 1 || max_width > FG_MAX_WIDTH) return FG_ERR_INVALID_ARG;
   Options o;
-  fg_status st = read_options(opt, max_width, &o);
+  fg_status st = read_options(opt, num_cols, max_width, &o);
   if (st != FG_OK) return st;
   const int64_t nnz = indptr_host[num_rows];
   if (!indptr_valid(indptr_host, num_rows, nnz)) return FG_ERR_INVALID_ARG;
@@ -464,7 +483,7 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
   if (st != FG_OK) return st;
   if (max_width < 1 || max_width > FG_MAX_WIDTH) return FG_ERR_INVALID_ARG;
   Options o;
-  if ((st = read_options(opt, max_width, &o)) != FG_OK) return st;
+  if ((st = read_options(opt, g->num_cols, max_width, &o)) != FG_OK) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
 
   std::vector<int32_t> ip_copy, ix_copy;
@@ -510,7 +529,7 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
   p->segment_edges = o.S;
   p->max_row_segments = o.cap;
   p->slab_rows = ix ? o.slab : 0;
-  p->partition_min_degree = o.min_deg;
+  p->partition_min_degree = ix ? o.min_deg : 0;
   p->num_partitioned_rows = gather.partitioned_rows;
   if (hipGetDevice(&p->device) != hipSuccess) {
     delete p;

@@ -331,7 +331,7 @@ def _check_schedule(indptr, S, cap=128, indices=None, num_cols=0, slab=0, min_de
         return segs
     # gather schedule with source slabs
     nslab = -(-num_cols // slab)
-    thresh = max(min_deg, 32 * nslab)
+    thresh = min_deg if min_deg else max(64, 8 * nslab)
     part = deg >= thresh
     for r in np.nonzero(part)[0]:
         row = indices[indptr[r]:indptr[r + 1]]
@@ -374,6 +374,44 @@ def test_partitioned_schedule(S, slab, min_deg):
                     min_deg=min_deg, which="plain")
 
 
+def test_partition_min_degree_default_and_explicit():
+    """Rows of 100 edges over 16 id slabs: the default minimum (8 edges a
+    piece, 128) leaves them whole; an explicit minimum of 64 cuts them."""
+    w = synth.make_config("uniform_deg100_100k", d=8, scale_down=50)
+    c = w.csr
+    slab = -(-c.num_cols // 16)
+    segs, _, n_slot = fg.schedule_host(c.indptr, c.indices, c.num_cols, 128, "gather",
+                                       source_slab_rows=slab)
+    assert n_slot == 0
+    segs = _check_schedule(c.indptr, 4096, indices=c.indices, num_cols=c.num_cols, slab=slab,
+                           min_deg=64, which="gather")
+    assert (segs[:, 0] >= 0).sum() >= 12 * c.num_rows
+
+
+def test_partition_automatic_slabs():
+    """source_slab_rows < 0 picks slabs of max(8 MiB of features, num_cols /
+    16) ids and the default minimum row length for that many slabs."""
+    w = synth.make_config("uniform_deg100_100k", d=8, scale_down=5)
+    c = w.csr
+    # 20,000 sources x 256 floats = 20 MB: fits the dies' L2s, no partitioning
+    auto = fg.schedule_host(c.indptr, c.indices, c.num_cols, 256, "gather", source_slab_rows=-1)
+    assert auto[2] == 0 and auto[0].shape[0] == c.num_rows
+    for width in (512, 1024, 4096):
+        slab = max(64, (8 << 20) // (4 * width), -(-c.num_cols // 16))
+        auto = fg.schedule_host(c.indptr, c.indices, c.num_cols, width, "gather",
+                                source_slab_rows=-1)
+        same = fg.schedule_host(c.indptr, c.indices, c.num_cols, width, "gather",
+                                source_slab_rows=slab)
+        np.testing.assert_array_equal(auto[0], same[0])
+        nslab = -(-c.num_cols // slab)
+        segs = _check_schedule(c.indptr, 4096, indices=c.indices, num_cols=c.num_cols,
+                               slab=slab, which="gather")
+        if max(64, 8 * nslab) <= 100:  # rows of 100 edges are cut
+            assert (segs[:, 0] >= 0).sum() >= 7 * c.num_rows and auto[2] > 0
+        else:
+            assert (segs[:, 0] >= 0).sum() == c.num_rows and auto[2] == 0
+
+
 def test_partition_slabs_balance_dies():
     """Busy sources labelled first (one id slab would hold most edges): the
     slabs follow the edges, so the partitioned work spreads over all dies."""
@@ -391,6 +429,16 @@ def test_partition_slabs_balance_dies():
     die = ((np.nonzero(segs[:, 0] >= 0)[0] // 4) % 8)[big]
     per_die = np.bincount(die, weights=(real[big, 2] - real[big, 1]), minlength=8)
     assert per_die.min() > 0.8 * per_die.mean()
+
+
+def test_schedule_with_indices_but_no_slabs():
+    """Indices without source partitioning give the plain cut."""
+    w = synth.make_config("rmat_233k_115m", scale_down=512)
+    c = w.csr
+    a = fg.schedule_host(c.indptr, c.indices, c.num_cols, 128, "gather", segment_edges=64)
+    b = fg.schedule_host(c.indptr, None, c.num_cols, 128, "gather", segment_edges=64)
+    np.testing.assert_array_equal(a[0], b[0])
+    assert a[1:] == b[1:]
 
 
 def test_partitioning_skips_unsorted_rows():
