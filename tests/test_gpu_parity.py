@@ -821,14 +821,66 @@ def test_rand_100k_full(d):
     x = w.arrays["x"]
     rows = sample_rows(csr, 600, 15 + d)
     plan = fg.Plan(G, d)
-    pplan = fg.Plan(G, d, source_slab_rows=-1)
+    # automatic slabs at d = 128; at d = 32 the features fit the dies' L2s and
+    # the automatic rule leaves the graph whole, so slabs are given
+    pplan = fg.Plan(G, d, source_slab_rows=-1 if d >= 128 else 4096)
     assert pplan.info()["num_partitioned_rows"] > 0
+    assert fg.Plan(G, 32, source_slab_rows=-1).info()["num_partitioned_rows"] == 0
     for p in (plan, pplan):
         check_spmm(csr, G, x, rows=rows, plan=p)
         check_spmm(csr, G, x, rows=rows, plan=p, reduce="max")
         check_sddmm(csr, G, x, x, rows=rows, plan=p)
     o = host(fg.gspmm(G, dev(np.ones((csr.num_cols, d), np.float32)), plan=pplan))
     np.testing.assert_array_equal(o[:, -1], csr.degrees().astype(np.float32))
+
+
+@pytest.mark.slow
+def test_edge_arrays_past_int32_offsets():
+    """270M edges x 8 heads: [E, H] edge arrays hold 2.16e9 elements, so
+    their offsets pass 2^31.  Rows of 66,000 edges (split into segments)
+    sampled at the start, middle and end of the edge range; the oracle runs
+    on the sub-graph of the sampled rows, compared at their positions."""
+    n, deg, H, dh = 4096, 66_000, 8, 4
+    E = n * deg
+    assert E * H > 2**31
+    rng = np.random.default_rng(41)
+    ind = rng.integers(0, n, size=(n, deg), dtype=np.int32)
+    ind.sort(axis=1)
+    indptr = (np.arange(n + 1, dtype=np.int64) * deg).astype(np.int32)
+    csr = synth.CSR(n, n, indptr, ind.reshape(-1))
+    del ind
+    G = fg.Graph.from_csr(csr)
+    plan = fg.Plan(G, H * dh)
+    x = rng.standard_normal((n, H, dh)).astype(np.float32)
+    x2 = x.reshape(n, H * dh)
+    tx = dev(x)
+    rows = np.array([0, 2049, n - 1])
+    pos = row_edges(csr, rows)
+    sub = synth.CSR(rows.size, n, (np.arange(rows.size + 1) * deg).astype(np.int32),
+                    csr.indices[pos])
+    tpos = torch.from_numpy(pos).cuda()
+    say("edges", E, "sampled rows", rows.tolist(), "last position", int(pos[-1]))
+    # SDDMM per head
+    s = fg.gsddmm(G, tx, tx, heads=H, plan=plan).reshape(E, H)
+    rs, norm = O.gsddmm(sub, x2, x2[rows], heads=H, with_norm=True)
+    assert_close_sum(host(s[tpos]), rs.astype(np.float64), norm, dh)
+    # edge softmax, the sampled rows given the oracle's scores on both sides
+    s[tpos] = dev(rs)
+    a = fg.edge_softmax(G, s, leaky=True, slope=0.2, plan=plan).reshape(E, H)
+    ra = O.edge_softmax(sub, rs, heads=H, leaky=True, slope=0.2)
+    assert_close_softmax(host(a[tpos]), ra, deg)
+    del s
+    # weighted aggregation with the oracle's weights on the sampled rows
+    a[tpos] = dev(ra)
+    y = host(fg.gspmm(G, tx, a, msg="src_mul_edge", heads=H, plan=plan)).reshape(n, H * dh)
+    ry, rnorm = O.gspmm(sub, x2, msg=O.MSG_SRC_MUL_EDGE, heads=H, edge_val=ra, with_norm=True)
+    assert_close_sum(y[rows], ry.astype(np.float64), rnorm, deg)
+    del a
+    # max with argmax: edge ids near the end of the range
+    ym, am = fg.gspmm(G, tx, reduce="max", plan=plan)
+    rm, rarg = O.gspmm(sub, x2, red=O.RED_MAX)
+    np.testing.assert_array_equal(host(ym).reshape(n, -1)[rows].view(np.uint32), rm.view(np.uint32))
+    np.testing.assert_array_equal(host(am).reshape(n, -1)[rows], pos[rarg])
 
 
 @pytest.mark.slow
