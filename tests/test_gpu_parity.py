@@ -690,6 +690,12 @@ def test_uniform_deg100_full(d):
     plan = fg.Plan(G, d)
     check_spmm(csr, G, x, rows=rows, plan=plan)
     check_sddmm(csr, G, x, x, rows=rows, plan=plan)
+    # automatic source slabs: every row cut at d = 128, none at the other widths
+    aplan = fg.Plan(G, d, source_slab_rows=-1)
+    assert (aplan.info()["num_partitioned_rows"] == csr.num_rows) == (d == 128)
+    if d == 128:
+        check_spmm(csr, G, x, rows=rows, plan=aplan)
+        check_sddmm(csr, G, x, x, rows=rows, plan=aplan)
     # property over every row: all-ones features sum to the in-degree (100)
     o = host(fg.gspmm(G, dev(np.ones((csr.num_cols, d), np.float32)), plan=plan))
     assert np.all(o == 100.0)
@@ -903,3 +909,9 @@ def test_rmat_train_step_full():
     c = float(da.double().sum())
     scale = float((tdy.abs() * fg.gspmm(Gf, dev(np.abs(x)), plan=pf).double()).sum())
     assert abs(a - b) <= 1e-5 * scale and abs(a - c) <= 1e-5 * scale
+    # the same three with automatic source slabs on both orientations
+    af, ab = fg.Plan(Gf, 256, source_slab_rows=-1), fg.Plan(Gb, 256, source_slab_rows=-1)
+    assert af.info()["num_partitioned_rows"] > 0 and ab.info()["num_partitioned_rows"] > 0
+    check_spmm(csr, Gf, x, rows=rows_f, plan=af)
+    check_spmm(csc, Gb, dy, rows=rows_b, plan=ab, nnz_total=csr.nnz)
+    check_sddmm(csr, Gf, x, dy, rows=rows_f, plan=af)
