@@ -111,8 +111,10 @@ typedef struct fg_graph {
  *  - plain (edge softmax): rows with more than S = segment_edges edges are
  *    cut into k = min(ceil(deg / S), max_row_segments) equal segments; long
  *    items first, rows without edges last;
- *  - gather (gSpMM, gSDDMM, fused attention): as plain by default.  With
- *    source partitioning (opt-in, source_slab_rows != 0), rows with at least
+ *  - gather (gSpMM, gSDDMM, fused attention): as plain, unless source
+ *    partitioning applies (by default once the num_cols x max_width source
+ *    features exceed 128 MiB, half the Infinity Cache; see
+ *    fg_plan_options.source_slab_rows).  With it, rows with at least
  *    partition_min_degree edges (if given; else max(64, 8 * ceil(num_cols /
  *    source_slab_rows)), so that pieces average 8 edges or more) and sorted
  *    source ids are cut where their sources change slab (slabs:
@@ -123,8 +125,8 @@ typedef struct fg_graph {
  *    (more hits in its L2 and the Infinity Cache, at the price of more
  *    pieces to merge).  This pays on graphs whose gathers have no locality
  *    of their own (sources spread uniformly, or features beyond the Infinity
- *    Cache) and costs more than it saves on graphs with hubs or communities,
- *    hence opt-in.
+ *    Cache) and costs more than it saves on graphs with hubs or communities
+ *    whose features the caches hold, hence the size threshold.
  * Items of rows cut in several pieces write partial results that a second
  * pass merges in a fixed order, so results are deterministic for a plan.
  * ------------------------------------------------------------------------- */
@@ -134,11 +136,13 @@ typedef struct fg_plan_options {
   int32_t segment_edges;        /* S: target edges per item; 0 -> default (4096)     */
   int32_t max_row_segments;     /* cap on items per row (plain cut); 0 -> 128        */
   int32_t source_slab_rows;     /* source ids per slab of the gather schedule;
-                                   0 -> no source partitioning (default);
-                                   negative -> automatic: the larger of 8 MiB of
-                                   features at max_width and num_cols / 16, and
-                                   none if the num_cols x max_width features fit
-                                   in 32 MiB (the dies' L2s together)                */
+                                   0 -> automatic slabs if the num_cols x
+                                   max_width features exceed 128 MiB, else none
+                                   (default); -1 -> automatic slabs if they
+                                   exceed 32 MiB (the dies' L2s together);
+                                   -2 -> no source partitioning; automatic
+                                   slabs: the larger of 8 MiB of features at
+                                   max_width and num_cols / 16 ids              */
   int32_t partition_min_degree; /* smallest row cut by slabs; 0 -> max(64, 8 *
                                    number of id slabs)                              */
   int32_t reserved[4];          /* must be zero                                      */

@@ -241,11 +241,13 @@ def _check_host_csr(num_rows, num_cols, indptr, indices, eids, nnz_total):
 class Plan:
     """Degree-aware schedules of one graph (see fg_plan_create): rows longer
     than ``segment_edges`` are cut into equal pieces (at most
-    ``max_row_segments``); with ``source_slab_rows`` != 0 (negative: automatic
-    size) long rows of the gather schedule are also cut at source-slab
-    boundaries for L2 reuse on each die; partial-result workspace for features up to
-    ``max_width`` floats.  Zero selects the library defaults.  Owns device
-    memory until ``close()``."""
+    ``max_row_segments``); long rows of the gather schedule may also be cut
+    at source-slab boundaries, so that each die gathers from a narrow band of
+    the features.  ``source_slab_rows``: 0 (default) automatic slabs once the
+    num_cols x max_width features exceed 128 MiB, -1 once they exceed 32 MiB,
+    -2 never, > 0 that many source ids per slab.  Partial-result workspace
+    for features up to ``max_width`` floats.  Zero selects the library
+    defaults.  Owns device memory until ``close()``."""
 
     def __init__(self, g: Graph, max_width: int, segment_edges: int = 0,
                  max_row_segments: int = 0, source_slab_rows: int = 0,

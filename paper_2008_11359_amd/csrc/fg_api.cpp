@@ -106,6 +106,12 @@ constexpr int64_t kAutoSlabsPerMatrix = 16;
 // automatic mode leaves feature matrices that the eight dies' L2s (4 MB
 // each) hold together unpartitioned: there the pieces cost more than they save
 constexpr int64_t kAutoMinMatrixBytes = int64_t(kXcds) * (4 << 20);
+// by default (source_slab_rows == 0) automatic slabs are used once the source
+// features exceed half the 256 MB Infinity Cache; below that the caches serve
+// graphs with hubs or communities better than the pieces would
+constexpr int64_t kDefaultPartitionBytes = int64_t(128) << 20;
+constexpr int32_t kSlabsAuto = -1;  // source_slab_rows: automatic above 32 MiB
+constexpr int32_t kSlabsOff = -2;   // source_slab_rows: never partition
 // unless given, the smallest partitioned row has max(64, 8 * id slabs) edges:
 // its pieces average at least 8 edges
 constexpr int64_t kMinPartitionDegree = 64;
@@ -310,33 +316,38 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
                        Options* o) {
   o->S = kDefaultSegmentEdges;
   o->cap = kDefaultMaxRowSegments;
-  o->slab = 0;  // source partitioning is opt-in (see fg_plan_options)
+  o->slab = 0;
   o->min_deg = 0;
-  if (!opt) return FG_OK;
-  for (int32_t r : opt->reserved)
-    if (r != 0) return FG_ERR_INVALID_ARG;
-  if (opt->segment_edges < 0 || opt->segment_edges > kMaxSegmentEdges) return FG_ERR_INVALID_ARG;
-  if (opt->max_row_segments < 0 || opt->max_row_segments > kMaxRowSegmentsLimit)
-    return FG_ERR_INVALID_ARG;
-  if (opt->partition_min_degree < 0) return FG_ERR_INVALID_ARG;
-  if (opt->segment_edges) o->S = opt->segment_edges;
-  if (opt->max_row_segments) o->cap = opt->max_row_segments;
-  if (opt->source_slab_rows > 0) {
-    o->slab = opt->source_slab_rows;
-  } else if (opt->source_slab_rows < 0 &&
-             num_cols * 4 * std::max<int64_t>(max_width, 1) > kAutoMinMatrixBytes) {
+  int32_t slab_opt = 0, min_opt = 0;
+  if (opt) {
+    for (int32_t r : opt->reserved)
+      if (r != 0) return FG_ERR_INVALID_ARG;
+    if (opt->segment_edges < 0 || opt->segment_edges > kMaxSegmentEdges) return FG_ERR_INVALID_ARG;
+    if (opt->max_row_segments < 0 || opt->max_row_segments > kMaxRowSegmentsLimit)
+      return FG_ERR_INVALID_ARG;
+    if (opt->partition_min_degree < 0) return FG_ERR_INVALID_ARG;
+    if (opt->source_slab_rows < kSlabsOff) return FG_ERR_INVALID_ARG;
+    if (opt->segment_edges) o->S = opt->segment_edges;
+    if (opt->max_row_segments) o->cap = opt->max_row_segments;
+    slab_opt = opt->source_slab_rows;
+    min_opt = opt->partition_min_degree;
+  }
+  if (o->cap < 2) return FG_ERR_INVALID_ARG;
+  const int64_t feature_bytes = num_cols * 4 * std::max<int64_t>(max_width, 1);
+  if (slab_opt > 0) {
+    o->slab = slab_opt;
+  } else if ((slab_opt == 0 && feature_bytes > kDefaultPartitionBytes) ||
+             (slab_opt == kSlabsAuto && feature_bytes > kAutoMinMatrixBytes)) {
     const int64_t rows = std::max<int64_t>(kAutoSlabBytes / (4 * std::max<int64_t>(max_width, 1)),
                                            (num_cols + kAutoSlabsPerMatrix - 1) / kAutoSlabsPerMatrix);
     o->slab = (int32_t)std::min<int64_t>(std::max<int64_t>(64, rows), INT32_MAX);
   }
   if (o->slab > 0) {
     const int64_t id_slabs = (std::max<int64_t>(num_cols, 1) + o->slab - 1) / o->slab;
-    o->min_deg = opt->partition_min_degree
-                     ? opt->partition_min_degree
-                     : (int32_t)std::min<int64_t>(
-                           std::max(kMinPartitionDegree, kMinPieceEdges * id_slabs), INT32_MAX);
+    o->min_deg = min_opt ? min_opt
+                         : (int32_t)std::min<int64_t>(
+                               std::max(kMinPartitionDegree, kMinPieceEdges * id_slabs), INT32_MAX);
   }
-  if (o->cap < 2) return FG_ERR_INVALID_ARG;
   return FG_OK;
 }
 

@@ -412,6 +412,28 @@ def test_partition_automatic_slabs():
             assert (segs[:, 0] >= 0).sum() == c.num_rows and auto[2] == 0
 
 
+def test_partition_default_rule():
+    """By default the gather schedule uses automatic slabs once the num_cols x
+    max_width features exceed 128 MiB; -2 switches slabs off, below -2 is an
+    error."""
+    w = synth.make_config("rand_100k_48m", d=16, scale_down=5)  # 20,000 ids, hot rows ~2000 edges
+    c = w.csr
+    plain = fg.schedule_host(c.indptr, None, c.num_cols, 4096, "gather")
+    # 20,000 x 1024 floats = 82 MB: no slabs
+    below = fg.schedule_host(c.indptr, c.indices, c.num_cols, 1024, "gather")
+    np.testing.assert_array_equal(below[0], fg.schedule_host(c.indptr, None, c.num_cols, 1024,
+                                                             "gather")[0])
+    # 20,000 x 4096 floats = 328 MB: the automatic slabs of source_slab_rows=-1
+    above = fg.schedule_host(c.indptr, c.indices, c.num_cols, 4096, "gather")
+    auto = fg.schedule_host(c.indptr, c.indices, c.num_cols, 4096, "gather", source_slab_rows=-1)
+    np.testing.assert_array_equal(above[0], auto[0])
+    assert above[0].shape[0] > plain[0].shape[0]
+    off = fg.schedule_host(c.indptr, c.indices, c.num_cols, 4096, "gather", source_slab_rows=-2)
+    np.testing.assert_array_equal(off[0], plain[0])
+    with pytest.raises(fg.FgError):
+        fg.schedule_host(c.indptr, c.indices, c.num_cols, 4096, "gather", source_slab_rows=-3)
+
+
 def test_partition_slabs_balance_dies():
     """Busy sources labelled first (one id slab would hold most edges): the
     slabs follow the edges, so the partitioned work spreads over all dies."""

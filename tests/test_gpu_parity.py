@@ -909,9 +909,11 @@ def test_rmat_train_step_full():
     c = float(da.double().sum())
     scale = float((tdy.abs() * fg.gspmm(Gf, dev(np.abs(x)), plan=pf).double()).sum())
     assert abs(a - b) <= 1e-5 * scale and abs(a - c) <= 1e-5 * scale
-    # the same three with automatic source slabs on both orientations
-    af, ab = fg.Plan(Gf, 256, source_slab_rows=-1), fg.Plan(Gb, 256, source_slab_rows=-1)
-    assert af.info()["num_partitioned_rows"] > 0 and ab.info()["num_partitioned_rows"] > 0
+    # the default plans of this 1 GiB feature matrix use source slabs; the
+    # same three without them
+    assert pf.info()["num_partitioned_rows"] > 0 and pb.info()["num_partitioned_rows"] > 0
+    af, ab = fg.Plan(Gf, 256, source_slab_rows=-2), fg.Plan(Gb, 256, source_slab_rows=-2)
+    assert af.info()["num_partitioned_rows"] == 0 and ab.info()["num_partitioned_rows"] == 0
     check_spmm(csr, Gf, x, rows=rows_f, plan=af)
     check_spmm(csc, Gb, dy, rows=rows_b, plan=ab, nnz_total=csr.nnz)
     check_sddmm(csr, Gf, x, dy, rows=rows_f, plan=af)
