@@ -646,6 +646,74 @@ def test_edge_cases():
         assert ds.numel() == 0
 
 
+def _odd(a=None, shape=None, dtype=torch.float32):
+    """A contiguous device tensor that starts 4 bytes past a 16-byte boundary."""
+    shape = a.shape if a is not None else shape
+    n = int(np.prod(shape))
+    buf = torch.zeros(n + 4, dtype=dtype, device="cuda")
+    t = buf[1:1 + n].view(shape)
+    assert t.data_ptr() % 16 == 4
+    if a is not None:
+        t.copy_(torch.from_numpy(np.ascontiguousarray(a)))
+    return t
+
+
+def test_misaligned_pointers(small_rmat):
+    """Every array 4 bytes off a 16-byte boundary: the kernels' float4 paths
+    must step aside for the scalar ones and give the oracle's results."""
+    csr, G = small_rmat
+    n, e = csr.num_rows, csr.nnz
+    rng = np.random.default_rng(23)
+    plan = fg.Plan(G, 128)
+    x = rng.standard_normal((n, 128)).astype(np.float32)
+    x8 = x.reshape(n, 8, 16)
+    w8 = rng.random((e, 8), dtype=np.float32)
+    deg = csr.degrees()[:, None]
+    # gSpMM: copy + sum, per-head weights, max + argmax
+    out = _odd(shape=(n, 128))
+    fg.gspmm(G, _odd(x), plan=plan, out=out)
+    ro, nrm = O.gspmm(csr, x, with_norm=True)
+    assert_close_sum(host(out), ro.astype(np.float64), nrm, deg)
+    out8 = _odd(shape=(n, 8, 16))
+    fg.gspmm(G, _odd(x8), _odd(w8), msg="src_mul_edge", plan=plan, out=out8)
+    ro, nrm = O.gspmm(csr, x, msg=O.MSG_SRC_MUL_EDGE, heads=8, edge_val=w8, with_norm=True)
+    assert_close_sum(host(out8).reshape(n, 128), ro.astype(np.float64), nrm, deg)
+    arg = _odd(shape=(n, 128), dtype=torch.int32)
+    fg.gspmm(G, _odd(x), reduce="max", plan=plan, out=out, arg=arg)
+    rm, ra = O.gspmm(csr, x, red=O.RED_MAX)
+    np.testing.assert_array_equal(host(out).view(np.uint32), rm.view(np.uint32))
+    np.testing.assert_array_equal(host(arg), ra)
+    # gSDDMM per head
+    sc = _odd(shape=(e, 8))
+    fg.gsddmm(G, _odd(x8), _odd(x8), plan=plan, out=sc)
+    rs, nrm = O.gsddmm(csr, x, x, heads=8, with_norm=True)
+    assert_close_sum(host(sc), rs.astype(np.float64), nrm, 16)
+    # edge softmax and its gradient, on the oracle's scores
+    a = _odd(shape=(e, 8))
+    fg.edge_softmax(G, _odd(rs), leaky=True, slope=0.2, plan=plan, out=a)
+    ra = O.edge_softmax(csr, rs, heads=8, leaky=True, slope=0.2)
+    assert_close_softmax(host(a), ra, np.repeat(csr.degrees(), csr.degrees())[:, None])
+    ga = rng.standard_normal((e, 8)).astype(np.float32)
+    ds = _odd(shape=(e, 8))
+    fg.edge_softmax_backward(G, _odd(ra), _odd(ga), scores=_odd(rs), leaky=True, slope=0.2,
+                             plan=plan, grad_scores=ds)
+    rd, scale = O.edge_softmax_backward(csr, rs, ga, heads=8, leaky=True, slope=0.2,
+                                        with_scale=True)
+    bound = 1e-5 * np.sqrt(np.repeat(np.maximum(csr.degrees(), 1), csr.degrees()))[:, None] * scale
+    assert (np.abs(host(ds).astype(np.float64) - rd) <= bound + 1e-12).all()
+    # fused SDDMM + softmax, one head
+    s1, a1 = _odd(shape=(e,)), _odd(shape=(e,))
+    fg.gsddmm_edge_softmax(G, _odd(x), _odd(x), plan=plan, scores=s1, out=a1)
+    r1, nrm = O.gsddmm(csr, x, x, with_norm=True)
+    assert_close_sum(host(s1)[:, None], r1.astype(np.float64), nrm, 128)
+    nz = csr.degrees() > 0
+    rsum = np.add.reduceat(host(a1).astype(np.float64), csr.indptr[:-1][nz])
+    np.testing.assert_allclose(rsum, 1.0, atol=1e-5 * math.sqrt(csr.degrees().max()))
+    # the fused attention layer needs 16-byte aligned rows and says so
+    with pytest.raises(fg.FgError):
+        fg.gat_aggregate(G, _odd(x8), _odd(x8), plan=plan, out=_odd(shape=(n, 8, 16)))
+
+
 def test_determinism_and_plan_independence(small_rmat):
     csr, G = small_rmat
     x = np.random.default_rng(9).standard_normal((csr.num_cols, 128)).astype(np.float32)
