@@ -713,12 +713,21 @@ def main():
     }
     result["hbm_copy_gbs"] = copy_bandwidth(torch)
     if not args.no_cpu_baseline:
+        # the oracle's rate also as edges/s and algorithmic GB/s of the same
+        # step: its FLOP rate times the step's edges and bytes per FLOP
+        bytes_step = sum(op.bytes for op in ops)
+
+        def also_per_edge(cb):
+            cb["edges_per_s"] = round(cb["value"] * 1e9 * e / flop_step, 1)
+            cb["gbs_alg"] = round(cb["value"] * bytes_step / flop_step, 3)
+            return cb
+
         log("timing the oracle on a row sample")
-        result["cpu_baseline"] = cpu_baseline(oracle_sample, args.cpu_budget)
+        result["cpu_baseline"] = also_per_edge(cpu_baseline(oracle_sample, args.cpu_budget))
         if args.cpu_1thread_budget > 0:
             log("timing the oracle on one thread")
-            result["cpu_baseline_1thread"] = cpu_baseline(oracle_sample,
-                                                          args.cpu_1thread_budget, threads=1)
+            result["cpu_baseline_1thread"] = also_per_edge(
+                cpu_baseline(oracle_sample, args.cpu_1thread_budget, threads=1))
     for p in plans:
         p.close()
     print(json.dumps(result), flush=True)
