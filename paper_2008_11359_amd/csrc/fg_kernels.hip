@@ -39,6 +39,16 @@ __device__ __forceinline__ int64_t wave_item() {
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
 
+// Offset of source row `src` in a [rows, F] array.  Both factors are
+// non-negative and below 2^32 (src < 2^31, F <= 65536), so one unsigned
+// 32 x 32 -> 64-bit multiply replaces the signed 64-bit product, which costs
+// two 32-bit multiplies, a 64-bit multiply-add and a sign extension.  Used by
+// the SDDMM and fused attention kernels; the gSpMM kernels keep the signed
+// product, with which they measured 2-4% faster.
+__device__ __forceinline__ uint64_t row_off(int32_t src, int64_t F) {
+  return (uint64_t)(uint32_t)src * (uint32_t)F;
+}
+
 template <int VEC>
 __device__ __forceinline__ void load_vec(const float* p, float (&r)[VEC]) {
   if constexpr (VEC == 4) {
@@ -733,7 +743,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
         ok[u] = jb + gid < cnt;
         const int src = bcast_lane<NG>(my_src, jb, gid);
         eu[u] = COLLECT ? 0 : bcast_lane<NG>(my_eid, jb, gid);
-        const float* xr = p.xs + (int64_t)src * F;
+        const float* xr = p.xs + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
           if (ok[u] && act[v]) {
@@ -819,7 +829,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_headed_kernel(SddmmParams p) {
         const int src = __shfl(my_src, jl);
         eu[u] = __shfl(my_eid, jl);
         if (ok[u] && act) {
-          load_vec<4>(p.xs + (int64_t)src * F + f, val[u]);
+          load_vec<4>(p.xs + row_off(src, F) + f, val[u]);
         } else {
 #pragma unroll
           for (int c = 0; c < 4; ++c) val[u][c] = 0.0f;
@@ -906,7 +916,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_scalar_kernel(SddmmParams p) {
         eu[u] = __shfl(my_eid, jl);
 #pragma unroll
         for (int v = 0; v < NV; ++v)
-          val[u][v] = (ok[u] && act[v]) ? p.xs[(int64_t)src * F + f[v]] : 0.0f;
+          val[u][v] = (ok[u] && act[v]) ? p.xs[row_off(src, F) + f[v]] : 0.0f;
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -1535,7 +1545,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_softmax_kernel(SddmmParams p, fl
         const int jb = j0 + u * NG;
         ok[u] = jb + gid < cnt;
         const int src = bcast_lane<NG>(my_src, jb, gid);
-        const float* xr = p.xs + (int64_t)src * F;
+        const float* xr = p.xs + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
           if (ok[u] && act[v]) {
@@ -2061,7 +2071,7 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
         ok[u] = jb + gid < cnt;
         const int src = bcast_lane<NG>(my_src, jb, gid);
         if (ok[u] && act) {
-          load_vec<4>(p.xs + (int64_t)src * F + f, val[u]);
+          load_vec<4>(p.xs + row_off(src, F) + f, val[u]);
         } else {
 #pragma unroll
           for (int c = 0; c < 4; ++c) val[u][c] = 0.0f;
