@@ -991,6 +991,16 @@ __device__ __forceinline__ float leaky_relu(float s, int on, float slope) {
   return (on && !(s > 0.0f)) ? slope * s : s;
 }
 
+// e^x for x <= 0 through the hardware 2^x instruction: the rounding of
+// x * log2(e) gives a relative error of about |x| * 2^-23 (2e-6 at x = -20,
+// below which a term weighs less than 2e-9 of the row's largest), in two
+// instructions instead of the ten or so of the correctly rounded expf.  Used
+// for the running (max, sum) statistics and the fused attention weights; the
+// softmax outputs themselves are written with expf.
+__device__ __forceinline__ float exp_nonpos(float x) {
+  return __builtin_amdgcn_exp2f(x * 1.44269504088896341f);
+}
+
 // (m, z) stands for sum_i exp(x_i - m) = z.  Merging two such pairs.
 __device__ __forceinline__ void lse_merge(float& m, float& z, float om, float oz) {
   if (om == -INFINITY) return;
@@ -1000,16 +1010,16 @@ __device__ __forceinline__ void lse_merge(float& m, float& z, float om, float oz
     return;
   }
   const float nm = fmaxf(m, om);
-  z = z * expf(m - nm) + oz * expf(om - nm);
+  z = z * exp_nonpos(m - nm) + oz * exp_nonpos(om - nm);
   m = nm;
 }
 
 __device__ __forceinline__ void lse_push(float& m, float& z, float s) {
   if (s > m) {
-    z = z * expf(m - s) + 1.0f;
+    z = z * exp_nonpos(m - s) + 1.0f;
     m = s;
   } else {
-    z += expf(s - m);
+    z += exp_nonpos(s - m);
   }
 }
 
@@ -2029,14 +2039,6 @@ __device__ __forceinline__ void attn_merge(float& m, float& z, float (&acc)[4], 
 // is rescaled only when a score exceeds the current maximum (a branch the
 // whole wavefront skips when no lane needs it); otherwise an edge costs one
 // exponential and a multiply-add per feature.
-// e^x for x <= 0 through the hardware 2^x instruction: the rounding of
-// x * log2(e) gives a relative error of about |x| * 2^-23 (2e-6 at x = -20,
-// below which a term weighs less than 2e-9 of the row's largest), in two
-// instructions instead of the ten or so of the correctly rounded expf.
-__device__ __forceinline__ float exp_nonpos(float x) {
-  return __builtin_amdgcn_exp2f(x * 1.44269504088896341f);
-}
-
 template <int G, int SH, bool SEG>
 __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
   constexpr int NG = kWave / G;
