@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define FG_ABI_VERSION 1
+#define FG_ABI_VERSION 2
 #define FG_MAX_WIDTH (1 << 16) /* largest supported F = H*dh */
 
 typedef enum fg_status {
@@ -145,7 +145,13 @@ typedef struct fg_plan_options {
                                    max_width and num_cols / 16 ids              */
   int32_t partition_min_degree; /* smallest row cut by slabs; 0 -> max(64, 8 *
                                    number of id slabs)                              */
-  int32_t reserved[4];          /* must be zero                                      */
+  int32_t item_order;           /* order of the work items: 0 -> automatic (2 if rows
+                                   with neighbouring ids share sources, judged on
+                                   64 windows of 32 rows, else 1; 1 without
+                                   indices); 1 -> longest first; 2 -> by
+                                   power-of-two length class, longest first, rows
+                                   in id order within a class                       */
+  int32_t reserved[3];          /* must be zero                                      */
 } fg_plan_options;
 
 typedef struct fg_plan_info {
@@ -158,6 +164,8 @@ typedef struct fg_plan_info {
   int64_t max_width;            /* largest F the workspace holds                     */
   int64_t workspace_bytes;
   int32_t segment_edges, max_row_segments, source_slab_rows, partition_min_degree;
+  int32_t item_order;           /* the order used: 1 or 2 (see fg_plan_options)      */
+  int32_t reserved;
 } fg_plan_info;
 
 /* One work item of a schedule (host view; the device tables hold the same). */

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert fg._lib.fg_abi_version() == fg.ABI_VERSION == 1
+    assert fg._lib.fg_abi_version() == fg.ABI_VERSION == 2
     for s in (0, -1, -2, -3, -4):
         assert fg.status_string(s) and fg.status_string(s) != "unknown status"
     assert fg.status_string(7) == "unknown status"
@@ -327,7 +327,15 @@ def _check_schedule(indptr, S, cap=128, indices=None, num_cols=0, slab=0, min_de
         assert np.array_equal(pieces, k)
         assert np.all(lens <= np.maximum(S, -(-deg[real[:, 0]] // cap)))
         assert not pad.any()
-        assert np.all(np.diff(lens) <= 0)  # longest first
+        # longest first (rows without edges last), or by power-of-two length
+        # class (ceil(log2(len))) with rows in id order within a class;
+        # without indices always the former
+        cls = np.where(lens > 0, np.ceil(np.log2(np.maximum(lens, 1))), -1).astype(np.int64)
+        assert np.all(np.diff(cls) <= 0)
+        by_len = bool(np.all(np.diff(lens) <= 0))
+        by_id = bool(np.all(np.diff(real[:, 0])[np.diff(cls) == 0] >= 0))
+        assert by_len or by_id
+        assert by_len or indices is not None
         return segs
     # gather schedule with source slabs
     nslab = -(-num_cols // slab)
@@ -432,6 +440,28 @@ def test_partition_default_rule():
     np.testing.assert_array_equal(off[0], plain[0])
     with pytest.raises(fg.FgError):
         fg.schedule_host(c.indptr, c.indices, c.num_cols, 4096, "gather", source_slab_rows=-3)
+
+
+@pytest.mark.parametrize("name,transpose,expect", [
+    ("clustered_133k_deg300", True, 2),   # neighbouring ids share sources (communities)
+    ("rmat_233k_115m", False, 1),
+    ("uniform_deg100_100k", False, 1),
+    ("rand_100k_48m", False, 1),
+])
+def test_item_order_follows_id_locality(name, transpose, expect):
+    """Automatic item order: rows in id order within length classes when rows
+    with neighbouring ids share sources, longest first otherwise."""
+    w = synth.make_config(name, d=8 if name in ("uniform_deg100_100k", "rand_100k_48m") else None,
+                          scale_down=10)
+    g = synth.csr_to_csc(w.csr) if transpose else w.csr
+    sched = {o: fg.schedule_host(g.indptr, g.indices, g.num_cols, 128, "plain", item_order=o)[0]
+             for o in (0, 1, 2)}
+    if np.unique(g.degrees()).size > 1:  # equal degrees: both orders are the id order
+        assert not np.array_equal(sched[1], sched[2])
+    np.testing.assert_array_equal(sched[0], sched[expect])
+    _check_schedule(g.indptr, 4096, indices=g.indices, num_cols=g.num_cols, which="plain")
+    with pytest.raises(fg.FgError):
+        fg.schedule_host(g.indptr, g.indices, g.num_cols, 128, "plain", item_order=3)
 
 
 def test_partition_slabs_balance_dies():

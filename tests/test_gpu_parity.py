@@ -358,6 +358,8 @@ def plans_for(G, width, sizes=(0, 1, 5, 64)):
     yield None
     for s in sizes:
         yield fg.Plan(G, max_width=width, segment_edges=s)
+    # items by length class, rows in id order within a class
+    yield fg.Plan(G, max_width=width, segment_edges=64, item_order=2)
     # rows cut at source-slab boundaries (8 slabs), pieces of at most 64 edges
     slab = max(1, -(-G.num_cols // 8))
     yield fg.Plan(G, max_width=width, segment_edges=64, source_slab_rows=slab,
