@@ -37,6 +37,24 @@ struct Graph {
 
 // Row degrees: mostly small, some empty, a few hubs; sources sorted per row
 // unless `unsorted`.
+// Rows in blocks of 40 that draw their sources from one block of 64 ids
+// (neighbouring ids share sources), with degrees 20-60.
+Graph make_blocked_graph(int64_t rows, int64_t cols) {
+  Graph g;
+  g.rows = rows;
+  g.cols = cols;
+  g.indptr.assign((size_t)rows + 1, 0);
+  for (int64_t r = 0; r < rows; ++r) g.indptr[(size_t)r + 1] = g.indptr[(size_t)r] + 20 + (int32_t)below(41);
+  g.indices.resize((size_t)g.indptr[(size_t)rows]);
+  for (int64_t r = 0; r < rows; ++r) {
+    const int64_t base = ((r / 40) * 64) % std::max<int64_t>(cols - 64, 1);
+    auto b = g.indices.begin() + g.indptr[(size_t)r], e = g.indices.begin() + g.indptr[(size_t)r + 1];
+    for (auto it = b; it != e; ++it) *it = (int32_t)std::min<int64_t>(base + below(64), cols - 1);
+    std::sort(b, e);
+  }
+  return g;
+}
+
 Graph make_graph(int64_t rows, int64_t cols, int64_t hub_deg, bool unsorted) {
   Graph g;
   g.rows = rows;
@@ -145,6 +163,10 @@ void invalid_arguments() {
   CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
         FG_ERR_INVALID_ARG);
   bad = o;
+  bad.item_order = 3;
+  CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
+        FG_ERR_INVALID_ARG);
+  bad = o;
   bad.reserved[2] = 1;
   CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
         FG_ERR_INVALID_ARG);
@@ -202,13 +224,15 @@ int main() {
   for (int rep = 0; rep < 30; ++rep) {
     const int64_t rows = rep < 3 ? rep : below(3000);
     const int64_t cols = 1 + below(rep % 2 ? 50000 : 300);
-    const Graph g = make_graph(rows, cols, rep % 3 ? 20000 : 0, rep % 7 == 5);
+    const Graph g = rep % 5 == 4 ? make_blocked_graph(rows, cols + 64)
+                                 : make_graph(rows, cols, rep % 3 ? 20000 : 0, rep % 7 == 5);
     for (int t = 0; t < 6; ++t) {
       fg_plan_options o{};
       o.segment_edges = seg_opts[below(5)];
       o.max_row_segments = cap_opts[below(4)];
       o.source_slab_rows = slab_opts[below(5)];
       o.partition_min_degree = min_opts[below(4)];
+      o.item_order = (int32_t)below(3);
       const int64_t w = widths[below(4)];
       for (int which = 0; which < 2; ++which)
         for (int ind = 0; ind < 2; ++ind) {
