@@ -592,8 +592,8 @@ def main():
                     help="cap on segments per row (0: default)")
     ap.add_argument("--source-slab-rows", type=int, default=0,
                     help="source ids per slab of the gather schedule (0: library default, "
-                         "automatic above 128 MiB of features; -1: automatic above 32 MiB; "
-                         "-2: off)")
+                         "automatic above 128 MiB of features, or 32 MiB with spread gathers; "
+                         "-1: automatic above 32 MiB; -2: off)")
     ap.add_argument("--partition-min-degree", type=int, default=0,
                     help="smallest row cut at slab boundaries (0: default)")
     ap.add_argument("--fused", action="store_true",

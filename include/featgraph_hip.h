@@ -113,8 +113,9 @@ typedef struct fg_graph {
  *    items first, rows without edges last;
  *  - gather (gSpMM, gSDDMM, fused attention): as plain, unless source
  *    partitioning applies (by default once the num_cols x max_width source
- *    features exceed 128 MiB, half the Infinity Cache; see
- *    fg_plan_options.source_slab_rows).  With it, rows with at least
+ *    features exceed 128 MiB, half the Infinity Cache, or 32 MiB when the
+ *    gathers are spread; see fg_plan_options.source_slab_rows).  With it,
+ *    rows with at least
  *    partition_min_degree edges (if given; else max(64, 8 * ceil(num_cols /
  *    source_slab_rows)), so that pieces average 8 edges or more) and sorted
  *    source ids are cut where their sources change slab (slabs:
@@ -137,9 +138,13 @@ typedef struct fg_plan_options {
   int32_t max_row_segments;     /* cap on items per row (plain cut); 0 -> 128        */
   int32_t source_slab_rows;     /* source ids per slab of the gather schedule;
                                    0 -> automatic slabs if the num_cols x
-                                   max_width features exceed 128 MiB, else none
-                                   (default); -1 -> automatic slabs if they
-                                   exceed 32 MiB (the dies' L2s together);
+                                   max_width features exceed 128 MiB, or exceed
+                                   32 MiB with spread gathers (the most used 4 MB
+                                   of source rows take under 45% of the edges,
+                                   and rows with neighbouring ids do not share
+                                   sources), else none (default); -1 ->
+                                   automatic slabs if they exceed 32 MiB (the
+                                   dies' L2s together);
                                    -2 -> no source partitioning; automatic
                                    slabs: the larger of 8 MiB of features at
                                    max_width and num_cols / 16 ids              */

@@ -246,8 +246,9 @@ class Plan:
     ``max_row_segments``); long rows of the gather schedule may also be cut
     at source-slab boundaries, so that each die gathers from a narrow band of
     the features.  ``source_slab_rows``: 0 (default) automatic slabs once the
-    num_cols x max_width features exceed 128 MiB, -1 once they exceed 32 MiB,
-    -2 never, > 0 that many source ids per slab.  ``item_order``: 1 longest
+    num_cols x max_width features exceed 128 MiB, or 32 MiB when the gathers
+    are spread (no dominant hot sources, no locality along row ids); -1 once
+    they exceed 32 MiB; -2 never; > 0 that many source ids per slab.  ``item_order``: 1 longest
     item first, 2 by power-of-two length class with rows in id order (keeps
     the locality of graphs whose neighbouring ids share sources), 0
     (default) picks 2 for such graphs and 1 otherwise.  Partial-result

@@ -188,20 +188,58 @@ bool ids_share_sources(const int32_t* ip, const std::vector<std::pair<int64_t, i
   return adj >= 0.02 && adj >= 8.0 * far;
 }
 
-// Resolves an automatic item order from host indices (none: by length).
-int32_t resolve_order(int32_t order, const int32_t* ip, const int32_t* ix, int64_t num_rows) {
-  if (order != kOrderAuto) return order;
-  if (!ix) return kOrderByLength;
+// ids_share_sources() on host indices.
+bool ids_share_sources_host(const int32_t* ip, const int32_t* ix, int64_t num_rows) {
   const auto wins = order_windows(ip, num_rows);
   std::vector<std::vector<int32_t>> win_ix;
   for (const auto& w : wins) win_ix.emplace_back(ix + ip[w.first], ix + ip[w.second]);
-  return ids_share_sources(ip, wins, win_ix) ? kOrderById : kOrderByLength;
+  return ids_share_sources(ip, wins, win_ix);
 }
+
+// Share of the edges whose source is among the `rows` most used sources: the
+// hit rate an L2 holding that many feature rows could at best reach.
+double hot_source_share(const int32_t* ix, int64_t nnz, int64_t num_cols, int64_t rows) {
+  if (nnz <= 0) return 1.0;
+  std::vector<int32_t> cnt((size_t)num_cols, 0);
+  for (int64_t q = 0; q < nnz; ++q) ++cnt[(size_t)ix[q]];
+  if (rows < num_cols) {
+    std::nth_element(cnt.begin(), cnt.begin() + rows, cnt.end(), std::greater<int32_t>());
+    cnt.resize((size_t)rows);
+  }
+  int64_t top = 0;
+  for (int32_t c : cnt) top += c;
+  return (double)top / (double)nnz;
+}
+
+// Below the default threshold, features of more than kAutoMinMatrixBytes get
+// slabs if the gathers are spread: the hottest 4 MB of source rows (one die's
+// L2) take less than this share of the edges, and rows with neighbouring ids
+// do not share sources.  (The power-law graph at d = 128: 66%, kept whole;
+// rand-100K and uniform graphs at d = 128: 35% and 10%, cut.)
+constexpr double kSpreadShare = 0.45;
+constexpr int64_t kDieL2Bytes = 4 << 20;
 
 struct Options {
   int32_t S, cap, slab, min_deg;  // slab 0: no source partitioning
   int32_t order;                  // item order: 0 automatic, 1 by length, 2 by class + id
+  bool slab_if_spread;            // keep the slabs only if the gathers are spread
 };
+
+// Settles the automatic choices that depend on the graph: the item order and
+// conditional slabs.  ix: host indices (all of them) or null; id_local: the
+// result of ids_share_sources() if already known (-1: not known).
+void settle_options(Options& o, const int32_t* ip, const int32_t* ix, int64_t num_rows,
+                    int64_t num_cols, int64_t max_width, int id_local) {
+  if (id_local < 0 && ix && (o.order == kOrderAuto || o.slab_if_spread))
+    id_local = ids_share_sources_host(ip, ix, num_rows) ? 1 : 0;
+  if (o.order == kOrderAuto) o.order = id_local == 1 ? kOrderById : kOrderByLength;
+  if (o.slab_if_spread) {
+    const int64_t rows = kDieL2Bytes / (4 * std::max<int64_t>(max_width, 1));
+    if (!ix || id_local != 0 || hot_source_share(ix, ip[num_rows], num_cols, rows) >= kSpreadShare)
+      o.slab = 0;
+    o.slab_if_spread = false;
+  }
+}
 
 struct Schedule {
   std::vector<fg::Seg> segs;
@@ -428,6 +466,7 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
   o->min_deg = 0;
   int32_t slab_opt = 0, min_opt = 0;
   o->order = kOrderAuto;
+  o->slab_if_spread = false;
   if (opt) {
     for (int32_t r : opt->reserved)
       if (r != 0) return FG_ERR_INVALID_ARG;
@@ -447,8 +486,9 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
   const int64_t feature_bytes = num_cols * 4 * std::max<int64_t>(max_width, 1);
   if (slab_opt > 0) {
     o->slab = slab_opt;
-  } else if ((slab_opt == 0 && feature_bytes > kDefaultPartitionBytes) ||
+  } else if ((slab_opt == 0 && feature_bytes > kAutoMinMatrixBytes) ||
              (slab_opt == kSlabsAuto && feature_bytes > kAutoMinMatrixBytes)) {
+    o->slab_if_spread = slab_opt == 0 && feature_bytes <= kDefaultPartitionBytes;
     const int64_t rows = std::max<int64_t>(kAutoSlabBytes / (4 * std::max<int64_t>(max_width, 1)),
                                            (num_cols + kAutoSlabsPerMatrix - 1) / kAutoSlabsPerMatrix);
     o->slab = (int32_t)std::min<int64_t>(std::max<int64_t>(64, rows), INT32_MAX);
@@ -516,7 +556,7 @@ fg_status fg_schedule_host(const int32_t* indptr_host, const int32_t* indices_ho
   if (!indptr_valid(indptr_host, num_rows, nnz)) return FG_ERR_INVALID_ARG;
   if (indices_host && !indices_valid(indices_host, nnz, num_cols)) return FG_ERR_INVALID_ARG;
   try {
-    o.order = resolve_order(o.order, indptr_host, indices_host, num_rows);
+    settle_options(o, indptr_host, indices_host, num_rows, num_cols, max_width, -1);
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
   }
@@ -641,8 +681,8 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
   }
   if (ix && !indices_valid(ix, g->nnz, g->num_cols)) return FG_ERR_INVALID_ARG;
   try {
-    if (o.order == kOrderAuto && ix) {
-      o.order = resolve_order(o.order, ip, ix, g->num_rows);
+    if (ix) {
+      settle_options(o, ip, ix, g->num_rows, g->num_cols, max_width, -1);
     } else if (o.order == kOrderAuto) {  // sample windows of the device indices
       const auto wins = order_windows(ip, g->num_rows);
       std::vector<std::vector<int32_t>> win_ix;
@@ -660,6 +700,7 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
   }
+  if (o.slab_if_spread) o.slab = 0;  // (conditional slabs always come with host indices)
   if (o.slab <= 0) ix = nullptr;
 
   Schedule gather, plain;

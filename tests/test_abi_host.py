@@ -422,46 +422,48 @@ def test_partition_automatic_slabs():
 
 def test_partition_default_rule():
     """By default the gather schedule uses automatic slabs once the num_cols x
-    max_width features exceed 128 MiB; -2 switches slabs off, below -2 is an
-    error."""
+    max_width features exceed 128 MiB, or 32 MiB when the gathers are spread
+    (the most used 4 MB of source rows take under 45% of the edges and rows
+    with neighbouring ids do not share sources); -2 switches slabs off, below
+    -2 is an error."""
     w = synth.make_config("rand_100k_48m", d=16, scale_down=5)  # 20,000 ids, hot rows ~2000 edges
     c = w.csr
-    plain = fg.schedule_host(c.indptr, None, c.num_cols, 4096, "gather")
-    # 20,000 x 1024 floats = 82 MB: no slabs
-    below = fg.schedule_host(c.indptr, c.indices, c.num_cols, 1024, "gather")
-    np.testing.assert_array_equal(below[0], fg.schedule_host(c.indptr, None, c.num_cols, 1024,
-                                                             "gather")[0])
-    # 20,000 x 4096 floats = 328 MB: the automatic slabs of source_slab_rows=-1
+    plain = {wd: fg.schedule_host(c.indptr, None, c.num_cols, wd, "gather") for wd in (256, 1024, 4096)}
+    # 20,000 x 256 floats = 20 MB: no slabs
+    np.testing.assert_array_equal(
+        fg.schedule_host(c.indptr, c.indices, c.num_cols, 256, "gather")[0], plain[256][0])
+    # 82 MB and spread (the top 1,024 sources take 22% of the edges): slabs
+    spread = fg.schedule_host(c.indptr, c.indices, c.num_cols, 1024, "gather")
+    np.testing.assert_array_equal(
+        spread[0], fg.schedule_host(c.indptr, c.indices, c.num_cols, 1024, "gather",
+                                    source_slab_rows=-1)[0])
+    assert spread[0].shape[0] > plain[1024][0].shape[0]
+    # 328 MB: the automatic slabs of source_slab_rows=-1, unconditionally
     above = fg.schedule_host(c.indptr, c.indices, c.num_cols, 4096, "gather")
     auto = fg.schedule_host(c.indptr, c.indices, c.num_cols, 4096, "gather", source_slab_rows=-1)
     np.testing.assert_array_equal(above[0], auto[0])
-    assert above[0].shape[0] > plain[0].shape[0]
+    assert above[0].shape[0] > plain[4096][0].shape[0]
     off = fg.schedule_host(c.indptr, c.indices, c.num_cols, 4096, "gather", source_slab_rows=-2)
-    np.testing.assert_array_equal(off[0], plain[0])
+    np.testing.assert_array_equal(off[0], plain[4096][0])
     with pytest.raises(fg.FgError):
         fg.schedule_host(c.indptr, c.indices, c.num_cols, 4096, "gather", source_slab_rows=-3)
 
 
-@pytest.mark.parametrize("name,transpose,expect", [
-    ("clustered_133k_deg300", True, 2),   # neighbouring ids share sources (communities)
-    ("rmat_233k_115m", False, 1),
-    ("uniform_deg100_100k", False, 1),
-    ("rand_100k_48m", False, 1),
+@pytest.mark.parametrize("name,cut", [
+    ("rmat_233k_115m", False),        # hubs: the top 1,024 sources take 60% of the edges
+    ("clustered_133k_deg300", False),  # spread, but neighbouring ids share sources
+    ("uniform_deg100_100k", True),     # spread: 6%
 ])
-def test_item_order_follows_id_locality(name, transpose, expect):
-    """Automatic item order: rows in id order within length classes when rows
-    with neighbouring ids share sources, longest first otherwise."""
-    w = synth.make_config(name, d=8 if name in ("uniform_deg100_100k", "rand_100k_48m") else None,
-                          scale_down=10)
-    g = synth.csr_to_csc(w.csr) if transpose else w.csr
-    sched = {o: fg.schedule_host(g.indptr, g.indices, g.num_cols, 128, "plain", item_order=o)[0]
-             for o in (0, 1, 2)}
-    if np.unique(g.degrees()).size > 1:  # equal degrees: both orders are the id order
-        assert not np.array_equal(sched[1], sched[2])
-    np.testing.assert_array_equal(sched[0], sched[expect])
-    _check_schedule(g.indptr, 4096, indices=g.indices, num_cols=g.num_cols, which="plain")
-    with pytest.raises(fg.FgError):
-        fg.schedule_host(g.indptr, g.indices, g.num_cols, 128, "plain", item_order=3)
+def test_partition_spread_gathers(name, cut):
+    """Between 32 and 128 MiB of features (width 1,024 on a tenth- or
+    fifth-size graph), slabs only for spread gathers without id locality."""
+    sd = 5 if name == "uniform_deg100_100k" else 10
+    w = synth.make_config(name, d=16 if name == "uniform_deg100_100k" else None, scale_down=sd)
+    c = w.csr
+    assert 32 << 20 < c.num_cols * 1024 * 4 <= 128 << 20
+    d = fg.schedule_host(c.indptr, c.indices, c.num_cols, 1024, "gather")
+    plain = fg.schedule_host(c.indptr, None, c.num_cols, 1024, "gather")
+    assert (d[0].shape[0] != plain[0].shape[0] or d[2] != plain[2]) == cut
 
 
 def test_partition_slabs_balance_dies():
