@@ -760,12 +760,16 @@ def test_uniform_deg100_full(d):
     plan = fg.Plan(G, d)
     check_spmm(csr, G, x, rows=rows, plan=plan)
     check_sddmm(csr, G, x, x, rows=rows, plan=plan)
-    # automatic source slabs: every row cut at d = 128, none at the other widths
+    # source slabs: at d = 128 every row is cut by default (spread gathers) and
+    # with -1; at the other widths rows of 100 edges stay whole
     aplan = fg.Plan(G, d, source_slab_rows=-1)
     assert (aplan.info()["num_partitioned_rows"] == csr.num_rows) == (d == 128)
+    assert plan.info()["num_partitioned_rows"] == aplan.info()["num_partitioned_rows"]
     if d == 128:
-        check_spmm(csr, G, x, rows=rows, plan=aplan)
-        check_sddmm(csr, G, x, x, rows=rows, plan=aplan)
+        nplan = fg.Plan(G, d, source_slab_rows=-2)
+        assert nplan.info()["num_partitioned_rows"] == 0
+        check_spmm(csr, G, x, rows=rows, plan=nplan)
+        check_sddmm(csr, G, x, x, rows=rows, plan=nplan)
     # property over every row: all-ones features sum to the in-degree (100)
     o = host(fg.gspmm(G, dev(np.ones((csr.num_cols, d), np.float32)), plan=plan))
     assert np.all(o == 100.0)
