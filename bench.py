@@ -109,7 +109,7 @@ def setup(name, d, args, fg, torch, dev):
     G = fg.Graph.from_csr(csr, device=dev)
     popt = dict(segment_edges=args.segment_edges, max_row_segments=args.max_row_segments,
                 source_slab_rows=args.source_slab_rows,
-                partition_min_degree=args.partition_min_degree)
+                partition_min_degree=args.partition_min_degree, item_order=args.item_order)
     T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
     cfg = {"workload": name, "num_vertices": n, "num_edges": e}
     plans = []
@@ -419,7 +419,8 @@ def setup(name, d, args, fg, torch, dev):
     pinfo = plans[0].info()
     cfg.update(segment_edges=pinfo["segment_edges"], max_row_segments=pinfo["max_row_segments"],
                source_slab_rows=pinfo["source_slab_rows"],
-               partition_min_degree=pinfo["partition_min_degree"], ops=[o.name for o in ops])
+               partition_min_degree=pinfo["partition_min_degree"],
+               item_order=[p.info()["item_order"] for p in plans], ops=[o.name for o in ops])
     cfg["plan_build_ms"] = [round(t, 1) for t in plan_ms]
     return cfg, ops, plans, oracle_sample, e
 
@@ -594,6 +595,9 @@ def main():
                     help="source ids per slab of the gather schedule (0: library default, "
                          "automatic above 128 MiB of features, or 32 MiB with spread gathers; "
                          "-1: automatic above 32 MiB; -2: off)")
+    ap.add_argument("--item-order", type=int, default=0,
+                    help="plan item order (0: library default, 1: longest first, "
+                         "2: length classes with rows in id order)")
     ap.add_argument("--partition-min-degree", type=int, default=0,
                     help="smallest row cut at slab boundaries (0: default)")
     ap.add_argument("--fused", action="store_true",
