@@ -964,6 +964,59 @@ def test_edge_arrays_past_int32_offsets():
 
 
 @pytest.mark.slow
+def test_features_past_int32_offsets():
+    """2.2M vertices x 1,024 features: [N, F] arrays hold 2.25e9 elements, so
+    row offsets pass 2^31.  Features come from a seeded torch generator on the
+    device; the oracle sees the sampled rows' own sources, relabelled into a
+    small sub-graph, and is compared at those rows (sum, max/argmax, SDDMM,
+    and the max gradient, fed only at the sampled rows)."""
+    n, deg, F = 2_200_000, 4, 1024
+    assert n * F > 2**31
+    rng = np.random.default_rng(43)
+    ind = np.sort(rng.integers(0, n, size=(n, deg), dtype=np.int32), axis=1).reshape(-1)
+    indptr = (np.arange(n + 1, dtype=np.int64) * deg).astype(np.int32)
+    csr = synth.CSR(n, n, indptr, ind)
+    G = fg.Graph.from_csr(csr)
+    gen = torch.Generator(device="cuda").manual_seed(44)
+    x = torch.randn((n, F), generator=gen, device="cuda")
+    rows = np.concatenate([np.arange(n - 40, n), rng.choice(n, 40, replace=False)])
+    rows = np.unique(rows).astype(np.int64)
+    pos = row_edges(csr, rows)
+    uniq, local = np.unique(csr.indices[pos], return_inverse=True)
+    sub = synth.CSR(rows.size, uniq.size, (np.arange(rows.size + 1) * deg).astype(np.int32),
+                    local.astype(np.int32))
+    xs = host(x[torch.from_numpy(uniq.astype(np.int64)).cuda()])
+    xd = host(x[torch.from_numpy(rows).cuda()])
+    trows = torch.from_numpy(rows).cuda()
+    say("rows", n, "features", F, "largest sampled offset", int(rows.max()) * F)
+    for plan in (None, fg.Plan(G, F)):
+        y = fg.gspmm(G, x, plan=plan)
+        ro, norm = O.gspmm(sub, xs, with_norm=True)
+        assert_close_sum(host(y[trows]), ro.astype(np.float64), norm, deg)
+        del y
+        ym, am = fg.gspmm(G, x, reduce="max", plan=plan)
+        rm, ra = O.gspmm(sub, xs, red=O.RED_MAX)
+        np.testing.assert_array_equal(host(ym[trows]).view(np.uint32), rm.view(np.uint32))
+        np.testing.assert_array_equal(host(am[trows]), pos[ra])
+        del ym
+        sc = fg.gsddmm(G, x, x, plan=plan)
+        rs, snorm = O.gsddmm(sub, xs, xd, with_norm=True)
+        assert_close_sum(host(sc[torch.from_numpy(pos).cuda()])[:, None], rs.astype(np.float64),
+                         snorm, F)
+        del sc
+        # gradient of max with the upstream gradient nonzero only at the sampled rows
+        go = torch.zeros((n, F), device="cuda")
+        go_s = np.random.default_rng(45).integers(-4, 5, (rows.size, F)).astype(np.float32)
+        go[trows] = dev(go_s)
+        gs = fg.gspmm_max_backward(G, am, go, x=x, plan=plan)
+        del go, am
+        rg = O.gspmm_max_backward(sub, xs, go_s)
+        np.testing.assert_array_equal(host(gs[torch.from_numpy(uniq.astype(np.int64)).cuda()]), rg)
+        assert float(gs.abs().sum()) == float(np.abs(rg).astype(np.float64).sum())
+        del gs
+
+
+@pytest.mark.slow
 def test_rmat_train_step_full():
     w = make_config("rmat_1m_33m_train")
     csr, csc = w.csr, w.csc
