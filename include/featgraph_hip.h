@@ -105,12 +105,12 @@ typedef struct fg_graph {
  * epochs (Sec. IV-B).  It replaces the paper's per-block row assignment
  * (Sec. III-C, adaptive parallelization) with one that stays balanced on
  * power-law graphs, and revives its 1D source partitioning (Sec. III-C, graph
- * partitioning) for the L2 of each MI355X die.
+ * partitioning) for the caches of each MI355X die.
  *
  * A plan holds two schedules over one workspace:
  *  - plain (edge softmax): rows with more than S = segment_edges edges are
  *    cut into k = min(ceil(deg / S), max_row_segments) equal segments; long
- *    items first, rows without edges last;
+ *    items first (fg_plan_options.item_order), rows without edges last;
  *  - gather (gSpMM, gSDDMM, fused attention): as plain, unless source
  *    partitioning applies (by default once the num_cols x max_width source
  *    features exceed 128 MiB, half the Infinity Cache, or 32 MiB when the
@@ -194,9 +194,11 @@ fg_status fg_schedule_host(const int32_t* indptr_host, const int32_t* indices_ho
 
 /* Creates a plan for graph `g` and features up to `max_width` = H*dh floats.
  * indptr_host / indices_host: optional HOST copies of g->indptr / g->indices
- * (without them the plan copies what it needs from the device).  opt may be
- * NULL.  Validates indptr and indices (FG_ERR_INVALID_ARG), allocates device
- * memory, synchronises `stream`.  The plan is bound to g->indptr, num_rows and
+ * (without them the plan copies what it needs from the device: indptr, the
+ * indices when source slabs may apply, else 64 windows of them for the item
+ * order).  opt may be NULL.  Validates indptr, and the indices whenever it
+ * holds them all on the host (FG_ERR_INVALID_ARG), allocates device memory,
+ * synchronises `stream`.  The plan is bound to g->indptr, num_rows and
  * nnz: calls with another graph are rejected with FG_ERR_INVALID_ARG.  Its
  * workspace is mutable: calls that share a plan must be ordered on one
  * stream. */
