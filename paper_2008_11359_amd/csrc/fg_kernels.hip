@@ -1996,13 +1996,15 @@ struct GatParams {
 };
 
 // Sum over aligned groups of W lanes, returned in every lane of the group.
+// For W = 32 a lane takes the total of its own half of the wavefront (a
+// feature row of 64 lanes holds two such heads).
 template <int W>
-__device__ __forceinline__ float group_allsum(float v, int gid) {
+__device__ __forceinline__ float group_allsum(float v) {
   v = group_sum<W>(v);
   if constexpr (W == 32) {
     const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 31));
     const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
-    v = gid ? b : a;
+    v = (lane_id() & 32) ? b : a;
   } else if constexpr (W == 64) {
     v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
   }
@@ -2082,7 +2084,7 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         float part = val[u][0] * xd[0] + val[u][1] * xd[1] + val[u][2] * xd[2] + val[u][3] * xd[3];
-        float sc = SH == 1 ? part : group_allsum<SH>(part, gid);
+        float sc = SH == 1 ? part : group_allsum<SH>(part);
         sc = leaky_relu(sc, p.leaky, p.slope);
         if (ok[u]) {
           if (sc > m) {  // new maximum: move the state to it (m = -inf: a = 0)

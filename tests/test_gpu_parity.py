@@ -437,7 +437,7 @@ def test_heads(small_rmat, heads, dh):
 
 
 @pytest.mark.parametrize("heads,dh", [(8, 16), (1, 128), (2, 32), (4, 8), (1, 4), (16, 16),
-                                      (1, 256), (4, 64)])
+                                      (1, 256), (4, 64), (2, 128), (2, 64), (4, 32), (64, 4)])
 def test_gat_fused(small_rmat, heads, dh):
     csr, G = small_rmat
     x = np.random.default_rng(heads * 7 + dh).standard_normal(
@@ -646,6 +646,94 @@ def test_edge_cases():
                                       dev(np.zeros(0, np.float32)),
                                       scores=dev(np.zeros(0, np.float32)), plan=plan)
         assert ds.numel() == 0
+
+
+def _blocked_graph(rng, n, deg_hi):
+    """Rows in blocks of 40 drawing sources from one block of 64 ids
+    (neighbouring rows share sources), degrees 1..deg_hi."""
+    deg = rng.integers(1, deg_hi + 1, n)
+    dst = np.repeat(np.arange(n), deg)
+    base = (dst // 40 * 64) % max(n - 64, 1)
+    src = np.minimum(base + rng.integers(0, 64, dst.size), n - 1)
+    return synth.coo_to_csr(dst, src, n, n)
+
+
+_WIDTHS = (1, 2, 3, 4, 8, 12, 16, 20, 32, 48, 64, 96, 128, 160, 256, 300, 512)
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_random_configurations(seed):
+    """Seeded sweep over graph shapes (uniform, power-law with hubs, blocked
+    communities, sometimes transposed with edge ids), widths, heads, operators
+    and plan options (segment length, source slabs, item order): each case
+    against the oracle on every row."""
+    rng = np.random.default_rng(1000 + seed)
+    kind = ("uniform", "rmat", "blocked")[seed % 3]
+    n = int(rng.integers(2, 2500))
+    if kind == "uniform":
+        csr = synth.uniform_graph(rng, n, int(rng.integers(0, 40 * n)))
+    elif kind == "rmat":
+        scale = max(1, int(np.ceil(np.log2(n))))
+        csr = synth.rmat_graph(np.random.SeedSequence(seed), rng, scale, n,
+                               int(rng.integers(1, 30 * n)), workers=1)
+    else:
+        csr = _blocked_graph(rng, n, int(rng.integers(1, 120)))
+    F = int(rng.choice(_WIDTHS))
+    heads = int(rng.choice([h for h in (1, 2, 4, 8) if F % h == 0]))
+    x = rng.standard_normal((n, F)).astype(np.float32)
+    if heads > 1:
+        x = x.reshape(n, heads, F // heads)
+    nnz_total = None
+    g = csr
+    if seed % 4 == 3:  # the transposed graph with edge ids
+        g, nnz_total = csr_to_csc(csr), csr.nnz
+    G = fg.Graph.from_csr(g, nnz_total=nnz_total or 0)
+    if rng.random() < 0.2:
+        plan = None
+    else:
+        plan = fg.Plan(G, max(F, heads, 1), segment_edges=int(rng.choice([0, 1, 7, 64, 512])),
+                       source_slab_rows=int(rng.choice([0, -1, -2, 37, 500])),
+                       partition_min_degree=int(rng.choice([0, 1, 16])),
+                       item_order=int(rng.integers(0, 3)))
+        say("plan", plan.info())
+    nt = nnz_total or g.nnz
+    ops = rng.choice(["sum", "mul", "max", "sddmm", "softmax", "softmax_bwd", "max_bwd", "gat",
+                      "mlp", "sddmm_softmax"], size=3, replace=False)
+    say("seed", seed, kind, "n", n, "nnz", g.nnz, "F", F, "heads", heads, "ops", list(ops))
+    for op in ops:
+        if op == "sum":
+            check_spmm(g, G, x, plan=plan, heads=heads, nnz_total=nnz_total)
+        elif op == "mul":
+            w = rng.random((nt, heads), dtype=np.float32)
+            check_spmm(g, G, x, plan=plan, edge=w, heads=heads, nnz_total=nnz_total)
+        elif op == "max":
+            check_spmm(g, G, x, plan=plan, reduce="max", heads=heads, nnz_total=nnz_total)
+        elif op == "sddmm":
+            check_sddmm(g, G, x, x, plan=plan, heads=heads, nnz_total=nnz_total)
+        elif op == "softmax":
+            sc = (rng.standard_normal((nt, heads)) * 3).astype(np.float32)
+            check_softmax(g, G, sc, plan=plan, heads=heads, nnz_total=nnz_total)
+        elif op == "softmax_bwd":
+            sc = (rng.standard_normal((nt, heads)) * 3).astype(np.float32)
+            go = rng.standard_normal((nt, heads)).astype(np.float32)
+            check_softmax_backward(g, G, sc, go, plan=plan, heads=heads, nnz_total=nnz_total)
+        elif op == "max_bwd" and nnz_total is None:
+            go = rng.integers(-4, 5, (n, F)).astype(np.float32).reshape(x.shape)
+            check_max_backward(g, G, x, go, plan=plan, heads=heads, exact=True)
+        elif op == "gat" and nnz_total is None:
+            dh = F // heads
+            if dh % 4 == 0 and (dh // 4) & (dh // 4 - 1) == 0 and F <= 256:
+                check_gat(g, G, x.reshape(n, heads, dh), plan=plan, heads=heads)
+            else:
+                with pytest.raises(fg.FgError):
+                    fg.gat_aggregate(G, dev(x.reshape(n, heads, dh)), plan=plan)
+        elif op == "mlp" and nnz_total is None:
+            d_in = int(rng.choice([1, 3, 8]))
+            xi = rng.integers(-3, 4, (n, d_in)).astype(np.float32)
+            wi = rng.integers(-2, 3, (d_in, F)).astype(np.float32)
+            check_mlp(g, G, xi, xi, wi, plan=plan, exact=True, square=True)
+        elif op == "sddmm_softmax":
+            check_sddmm_softmax(g, G, x, x, plan=plan, heads=heads, nnz_total=nnz_total)
 
 
 def _odd(a=None, shape=None, dtype=torch.float32):
