@@ -658,20 +658,24 @@ def _blocked_graph(rng, n, deg_hi):
     return synth.coo_to_csr(dst, src, n, n)
 
 
-_WIDTHS = (1, 2, 3, 4, 8, 12, 16, 20, 32, 48, 64, 96, 128, 160, 256, 300, 512)
+_WIDTHS = (1, 2, 3, 4, 8, 12, 16, 20, 32, 48, 64, 96, 128, 160, 256, 300, 512, 1024, 1040)
 
 
-@pytest.mark.parametrize("seed", range(30))
+@pytest.mark.parametrize("seed", range(160))
 def test_random_configurations(seed):
     """Seeded sweep over graph shapes (uniform, power-law with hubs, blocked
-    communities, sometimes transposed with edge ids), widths, heads, operators
-    and plan options (segment length, source slabs, item order): each case
-    against the oracle on every row."""
+    communities, bipartite; sometimes transposed with edge ids), widths,
+    heads, operators and plan options (segment length, source slabs, item
+    order): each case against the oracle on every row."""
     rng = np.random.default_rng(1000 + seed)
-    kind = ("uniform", "rmat", "blocked")[seed % 3]
+    kind = ("uniform", "rmat", "blocked", "bipartite")[seed % 4]
     n = int(rng.integers(2, 2500))
     if kind == "uniform":
         csr = synth.uniform_graph(rng, n, int(rng.integers(0, 40 * n)))
+    elif kind == "bipartite":  # sources and destinations of different counts
+        m = int(rng.integers(1, 3000))
+        e = int(rng.integers(0, 40 * n))
+        csr = synth.coo_to_csr(rng.integers(0, n, e), rng.integers(0, m, e), n, m)
     elif kind == "rmat":
         scale = max(1, int(np.ceil(np.log2(n))))
         csr = synth.rmat_graph(np.random.SeedSequence(seed), rng, scale, n,
@@ -679,14 +683,17 @@ def test_random_configurations(seed):
     else:
         csr = _blocked_graph(rng, n, int(rng.integers(1, 120)))
     F = int(rng.choice(_WIDTHS))
-    heads = int(rng.choice([h for h in (1, 2, 4, 8) if F % h == 0]))
-    x = rng.standard_normal((n, F)).astype(np.float32)
-    if heads > 1:
-        x = x.reshape(n, heads, F // heads)
+    heads = int(rng.choice([h for h in (1, 2, 4, 8, 16) if F % h == 0]))
     nnz_total = None
     g = csr
-    if seed % 4 == 3:  # the transposed graph with edge ids
+    if seed % 5 == 3:  # the transposed graph with edge ids
         g, nnz_total = csr_to_csc(csr), csr.nnz
+    square = g.num_rows == g.num_cols
+    x = rng.standard_normal((g.num_cols, F)).astype(np.float32)
+    xd = rng.standard_normal((g.num_rows, F)).astype(np.float32)
+    if heads > 1:
+        x = x.reshape(g.num_cols, heads, F // heads)
+        xd = xd.reshape(g.num_rows, heads, F // heads)
     G = fg.Graph.from_csr(g, nnz_total=nnz_total or 0)
     if rng.random() < 0.2:
         plan = None
@@ -709,7 +716,7 @@ def test_random_configurations(seed):
         elif op == "max":
             check_spmm(g, G, x, plan=plan, reduce="max", heads=heads, nnz_total=nnz_total)
         elif op == "sddmm":
-            check_sddmm(g, G, x, x, plan=plan, heads=heads, nnz_total=nnz_total)
+            check_sddmm(g, G, x, xd, plan=plan, heads=heads, nnz_total=nnz_total)
         elif op == "softmax":
             sc = (rng.standard_normal((nt, heads)) * 3).astype(np.float32)
             check_softmax(g, G, sc, plan=plan, heads=heads, nnz_total=nnz_total)
@@ -718,9 +725,10 @@ def test_random_configurations(seed):
             go = rng.standard_normal((nt, heads)).astype(np.float32)
             check_softmax_backward(g, G, sc, go, plan=plan, heads=heads, nnz_total=nnz_total)
         elif op == "max_bwd" and nnz_total is None:
-            go = rng.integers(-4, 5, (n, F)).astype(np.float32).reshape(x.shape)
+            go = rng.integers(-4, 5, (g.num_rows, F)).astype(np.float32).reshape(
+                (g.num_rows,) + x.shape[1:])
             check_max_backward(g, G, x, go, plan=plan, heads=heads, exact=True)
-        elif op == "gat" and nnz_total is None:
+        elif op == "gat" and nnz_total is None and square:
             dh = F // heads
             if dh % 4 == 0 and (dh // 4) & (dh // 4 - 1) == 0 and F <= 256:
                 check_gat(g, G, x.reshape(n, heads, dh), plan=plan, heads=heads)
@@ -729,11 +737,12 @@ def test_random_configurations(seed):
                     fg.gat_aggregate(G, dev(x.reshape(n, heads, dh)), plan=plan)
         elif op == "mlp" and nnz_total is None:
             d_in = int(rng.choice([1, 3, 8]))
-            xi = rng.integers(-3, 4, (n, d_in)).astype(np.float32)
+            xi = rng.integers(-3, 4, (g.num_cols, d_in)).astype(np.float32)
+            xj = rng.integers(-3, 4, (g.num_rows, d_in)).astype(np.float32)
             wi = rng.integers(-2, 3, (d_in, F)).astype(np.float32)
-            check_mlp(g, G, xi, xi, wi, plan=plan, exact=True, square=True)
+            check_mlp(g, G, xi, xj, wi, plan=plan, exact=True, square=False)
         elif op == "sddmm_softmax":
-            check_sddmm_softmax(g, G, x, x, plan=plan, heads=heads, nnz_total=nnz_total)
+            check_sddmm_softmax(g, G, x, xd, plan=plan, heads=heads, nnz_total=nnz_total)
 
 
 def _odd(a=None, shape=None, dtype=torch.float32):
