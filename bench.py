@@ -243,7 +243,8 @@ def setup(name, d, args, fg, torch, dev):
         x = T(x_h)
         gy_h = np.random.default_rng(11).standard_normal((n, F), dtype=np.float32)
         gy = T(gy_h)
-        P = mkplan(G, max_width=F, **popt)
+        # the plan also holds the workspace of the binned max backward
+        P = mkplan(G, max_width=F, max_backward=not args.atomic_max_backward, **popt)
         plans.append(P)
         out_m = torch.empty((n, F), device=dev)
         arg = torch.empty((n, F), dtype=torch.int32, device=dev)
@@ -420,7 +421,8 @@ def setup(name, d, args, fg, torch, dev):
     cfg.update(segment_edges=pinfo["segment_edges"], max_row_segments=pinfo["max_row_segments"],
                source_slab_rows=pinfo["source_slab_rows"],
                partition_min_degree=pinfo["partition_min_degree"],
-               item_order=[p.info()["item_order"] for p in plans], ops=[o.name for o in ops])
+               item_order=[p.info()["item_order"] for p in plans], ops=[o.name for o in ops],
+               max_backward=[p.info()["max_backward"] for p in plans])
     cfg["plan_build_ms"] = [round(t, 1) for t in plan_ms]
     return cfg, ops, plans, oracle_sample, e
 
@@ -606,6 +608,9 @@ def main():
     ap.add_argument("--cold", action="store_true",
                     help="overwrite a 1 GiB buffer before every operator (caches hold no "
                          "inputs); the rate then comes from the operators' event times")
+    ap.add_argument("--atomic-max-backward", action="store_true",
+                    help="sage_max workload: plan without the binned max-backward workspace "
+                         "(the gradient goes through fp32 atomics)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-1thread-budget", type=float, default=4.0,
                     help="seconds of single-thread oracle work (0: skip)")

@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define FG_ABI_VERSION 2
+#define FG_ABI_VERSION 3
 #define FG_MAX_WIDTH (1 << 16) /* largest supported F = H*dh */
 
 typedef enum fg_status {
@@ -156,7 +156,13 @@ typedef struct fg_plan_options {
                                    indices); 1 -> longest first; 2 -> by
                                    power-of-two length class, longest first, rows
                                    in id order within a class                       */
-  int32_t reserved[3];          /* must be zero                                      */
+  int32_t max_backward;         /* 1 -> also reserve the workspace of the binned
+                                   gSpMM-max backward: 8 bytes per element of a
+                                   num_rows x max_width gradient (that product must
+                                   not exceed 2^31 - 1, else FG_ERR_UNSUPPORTED)
+                                   plus bin tables (128 KiB, and 4 KiB per source
+                                   tile, at most 32 MiB); 0 -> none (default)      */
+  int32_t reserved[2];          /* must be zero                                      */
 } fg_plan_options;
 
 typedef struct fg_plan_info {
@@ -170,7 +176,7 @@ typedef struct fg_plan_info {
   int64_t workspace_bytes;
   int32_t segment_edges, max_row_segments, source_slab_rows, partition_min_degree;
   int32_t item_order;           /* the order used: 1 or 2 (see fg_plan_options)      */
-  int32_t reserved;
+  int32_t max_backward;         /* 1 if the binned max-backward workspace is held    */
 } fg_plan_info;
 
 /* One work item of a schedule (host view; the device tables hold the same). */
@@ -301,10 +307,17 @@ fg_status fg_gsddmm_edge_softmax(const fg_graph* g, int32_t num_heads, int64_t h
  * plan      required when g->edge_ids != NULL: a plan created for this graph
  *           with these edge ids (it maps ids back to storage positions; ids
  *           must be distinct); otherwise optional and unused.
- * Entries of arg_eid that are not edge ids of g are skipped.  Contributions
- * to one element are added with fp32 atomics in an unspecified order, so a
- * sum of several contributions may differ in the last bits between calls;
- * the atomic adds may flush subnormal results to zero.
+ * Entries of arg_eid that are not edge ids of g are skipped.
+ * With a plan that holds the binned workspace (fg_plan_options.max_backward)
+ * and H * dh <= max_width, <= 16384, and num_cols / (source rows per 64 KiB
+ * tile) <= 8192 tiles, grad_src is built by binning: every element becomes
+ * an 8-byte record in the bin of its source tile (a counting sort), and one
+ * workgroup per piece of up to 16384 records sums a bin in LDS and writes the
+ * tile's rows.  Otherwise, and for grad_edge always, contributions go to
+ * zero-filled arrays with fp32 atomics.  Either way the order of the adds
+ * into one element is not fixed, so a sum of several contributions may
+ * differ in the last bits between calls, and the adds may flush subnormal
+ * results to zero.
  * ------------------------------------------------------------------------- */
 fg_status fg_gspmm_max_backward(const fg_graph* g, fg_msg_op msg, int32_t num_heads,
                                 int64_t head_dim, const float* x_src, const float* edge_val,

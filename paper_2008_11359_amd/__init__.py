@@ -33,7 +33,7 @@ FG_OK, FG_ERR_INVALID_ARG, FG_ERR_UNSUPPORTED, FG_ERR_HIP, FG_ERR_NO_MEMORY = 0,
 MSG_OPS = {"copy_src": 0, "src_mul_edge": 1}
 REDUCE_OPS = {"sum": 0, "max": 1}
 EDGE_OPS = {"dot": 0}
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 
 class FgError(RuntimeError):
@@ -57,7 +57,8 @@ class _Graph(ctypes.Structure):
 class _PlanOptions(ctypes.Structure):
     _fields_ = [("segment_edges", ctypes.c_int32), ("max_row_segments", ctypes.c_int32),
                 ("source_slab_rows", ctypes.c_int32), ("partition_min_degree", ctypes.c_int32),
-                ("item_order", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
+                ("item_order", ctypes.c_int32), ("max_backward", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 2)]
 
 
 class _PlanInfo(ctypes.Structure):
@@ -78,7 +79,7 @@ class _PlanInfo(ctypes.Structure):
         ("source_slab_rows", ctypes.c_int32),
         ("partition_min_degree", ctypes.c_int32),
         ("item_order", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("max_backward", ctypes.c_int32),
     ]
 
 
@@ -252,14 +253,18 @@ class Plan:
     item first, 2 by power-of-two length class with rows in id order (keeps
     the locality of graphs whose neighbouring ids share sources), 0
     (default) picks 2 for such graphs and 1 otherwise.  Partial-result
-    workspace for features up to ``max_width`` floats.  Zero selects the
-    library defaults.  Owns device memory until ``close()``."""
+    workspace for features up to ``max_width`` floats.  ``max_backward``:
+    also hold the workspace with which gspmm_max_backward bins the gradient
+    per source tile instead of adding it with atomics (8 bytes per element of
+    a num_rows x max_width gradient).  Zero selects the library defaults.
+    Owns device memory until ``close()``."""
 
     def __init__(self, g: Graph, max_width: int, segment_edges: int = 0,
                  max_row_segments: int = 0, source_slab_rows: int = 0,
-                 partition_min_degree: int = 0, item_order: int = 0):
+                 partition_min_degree: int = 0, item_order: int = 0,
+                 max_backward: bool = False):
         opt = _options(segment_edges, max_row_segments, source_slab_rows, partition_min_degree,
-                       item_order)
+                       item_order, max_backward)
         h = ctypes.c_void_p()
         ip, ix = g.indptr_host, g.indices_host
         st = _lib.fg_plan_create(ctypes.byref(g._c), None if ip is None else ip.ctypes.data,
@@ -294,13 +299,15 @@ class Plan:
 
 
 def _options(segment_edges: int = 0, max_row_segments: int = 0, source_slab_rows: int = 0,
-             partition_min_degree: int = 0, item_order: int = 0) -> _PlanOptions:
+             partition_min_degree: int = 0, item_order: int = 0,
+             max_backward: bool = False) -> _PlanOptions:
     opt = _PlanOptions()
     opt.segment_edges = int(segment_edges)
     opt.max_row_segments = int(max_row_segments)
     opt.source_slab_rows = int(source_slab_rows)
     opt.partition_min_degree = int(partition_min_degree)
     opt.item_order = int(item_order)
+    opt.max_backward = int(max_backward)
     return opt
 
 

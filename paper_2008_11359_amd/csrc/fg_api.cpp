@@ -30,6 +30,7 @@ struct fg_plan {
   const int32_t* edge_ids = nullptr;
   int64_t nnz_total = 0;
   int32_t* eid_pos = nullptr;
+  fg::BinWorkspace bin;  // binned max backward (plan option), else empty
   std::vector<void*> mem;
   int64_t workspace_bytes = 0;
 };
@@ -223,6 +224,7 @@ struct Options {
   int32_t S, cap, slab, min_deg;  // slab 0: no source partitioning
   int32_t order;                  // item order: 0 automatic, 1 by length, 2 by class + id
   bool slab_if_spread;            // keep the slabs only if the gathers are spread
+  bool max_backward;              // reserve the binned max-backward workspace
 };
 
 // Settles the automatic choices that depend on the graph: the item order and
@@ -467,9 +469,12 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
   int32_t slab_opt = 0, min_opt = 0;
   o->order = kOrderAuto;
   o->slab_if_spread = false;
+  o->max_backward = false;
   if (opt) {
     for (int32_t r : opt->reserved)
       if (r != 0) return FG_ERR_INVALID_ARG;
+    if (opt->max_backward < 0 || opt->max_backward > 1) return FG_ERR_INVALID_ARG;
+    o->max_backward = opt->max_backward == 1;
     if (opt->item_order < kOrderAuto || opt->item_order > kOrderById) return FG_ERR_INVALID_ARG;
     o->order = opt->item_order;
     if (opt->segment_edges < 0 || opt->segment_edges > kMaxSegmentEdges) return FG_ERR_INVALID_ARG;
@@ -653,6 +658,8 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
   if (max_width < 1 || max_width > FG_MAX_WIDTH) return FG_ERR_INVALID_ARG;
   Options o;
   if ((st = read_options(opt, g->num_cols, max_width, &o)) != FG_OK) return st;
+  // binned max-backward records are addressed with int32 offsets
+  if (o.max_backward && g->num_rows * max_width > INT32_MAX) return FG_ERR_UNSUPPORTED;
   hipStream_t hs = static_cast<hipStream_t>(stream);
 
   std::vector<int32_t> ip_copy, ix_copy;
@@ -776,6 +783,33 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
       return FG_ERR_HIP;
     }
   }
+  if (o.max_backward) {
+    // one 8-byte record per gradient element; bin tables; per-group runs
+    // for the most tiles any width up to max_width needs (narrower rows put
+    // more sources in a tile)
+    const int64_t cap = std::max<int64_t>(g->num_rows * max_width, 1);
+    const int64_t bins = std::max<int64_t>(
+        1, std::min<int64_t>(fg::kMaxBins,
+                             fg::bin_tiles(g->num_cols, std::min<int64_t>(max_width,
+                                                                          fg::kBinTileFloats))));
+    const size_t sz[3] = {8 * (size_t)cap, sizeof(int32_t) * 4 * (size_t)(fg::kMaxBins + 1),
+                          sizeof(int32_t) * (size_t)fg::kBinGroups * (size_t)bins};
+    void* m[3] = {nullptr, nullptr, nullptr};
+    for (int i = 0; i < 3; ++i) {
+      if (hipMalloc(&m[i], sz[i]) != hipSuccess) {
+        (void)hipStreamSynchronize(hs);
+        fg_plan_destroy(p);
+        return FG_ERR_NO_MEMORY;
+      }
+      p->mem.push_back(m[i]);
+      p->workspace_bytes += (int64_t)sz[i];
+    }
+    p->bin.rec = m[0];
+    p->bin.rec_capacity = cap;
+    p->bin.tables = static_cast<int32_t*>(m[1]);
+    p->bin.runs = static_cast<int32_t*>(m[2]);
+    p->bin.max_bins = bins;
+  }
   if (hipStreamSynchronize(hs) != hipSuccess) {  // host schedules die on return
     fg_plan_destroy(p);
     return FG_ERR_HIP;
@@ -803,6 +837,7 @@ fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info) {
   info->source_slab_rows = plan->slab_rows;
   info->partition_min_degree = plan->partition_min_degree;
   info->item_order = plan->item_order;
+  info->max_backward = plan->bin.rec ? 1 : 0;
   return FG_OK;
 }
 
@@ -956,6 +991,7 @@ fg_status fg_gspmm_max_backward(const fg_graph* g, fg_msg_op msg, int32_t num_he
   return from_hip(fg::launch_gspmm_max_backward(gv, plan ? plan->eid_pos : nullptr, (int)msg,
                                                 num_heads, head_dim, x_src, edge_val, arg_eid,
                                                 grad_out, grad_src, grad_edge,
+                                                plan ? &plan->bin : nullptr,
                                                 static_cast<hipStream_t>(stream)));
 }
 

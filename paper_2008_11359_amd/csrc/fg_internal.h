@@ -68,14 +68,48 @@ hipError_t launch_gsddmm_softmax(const GraphView& g, const PlanView* plan, int64
                                  const float* xs, const float* xd, bool leaky, float slope,
                                  float* scores, float* att, hipStream_t stream);
 
-// Backward of gSpMM-max: zero-fills gsrc / gedge (either may be null), then
-// sends each upstream gradient element to the source of the edge the forward
-// picked (fp32 atomics).  eid_pos maps edge id -> storage position and is
-// used only when g.edge_ids is set.
+// Binned gSpMM-max backward: a source tile holds 2^logR source rows of F
+// floats, at most kBinTileFloats (64 KiB of LDS); at most kMaxBins tiles;
+// kBinGroups row groups in the counting and scatter kernels.
+constexpr int kBinTileFloats = 16384;
+constexpr int kMaxBins = 8192;
+constexpr int kBinGroups = 1024;
+
+// log2 of the source rows per tile at width F (1 <= F <= kBinTileFloats).
+inline int bin_log_rows(int64_t F) {
+  int l = 0;
+  while (((int64_t)2 << l) * F <= kBinTileFloats) ++l;
+  return l;
+}
+
+// Tiles needed for num_cols sources at width F.
+inline int64_t bin_tiles(int64_t num_cols, int64_t F) {
+  const int l = bin_log_rows(F);
+  return (num_cols + ((int64_t)1 << l) - 1) >> l;
+}
+
+// Its workspace, owned by a plan: 8-byte records (one per gradient element),
+// four tables of kMaxBins + 1 int32 (bin sizes, first records, first
+// pieces, cursors) and kBinGroups x max_bins int32 (per-group counts).
+struct BinWorkspace {
+  void* rec = nullptr;
+  int64_t rec_capacity = 0;  // records
+  int32_t* tables = nullptr;
+  int32_t* runs = nullptr;
+  int64_t max_bins = 0;
+};
+
+// Backward of gSpMM-max: sends each upstream gradient element to the source
+// of the edge the forward picked; gsrc / gedge (either may be null) are fully
+// overwritten.  With a workspace whose capacity covers rows x F records (and
+// widths and source counts its tables fit), grad_src is built by binning the
+// elements per source tile and summing each tile in LDS; otherwise, and for
+// gedge always, with fp32 atomics into zero-filled arrays.  eid_pos maps
+// edge id -> storage position and is used only when g.edge_ids is set.
 hipError_t launch_gspmm_max_backward(const GraphView& g, const int32_t* eid_pos, int msg,
                                      int64_t H, int64_t dh, const float* x, const float* ev,
                                      const int32_t* arg, const float* go, float* gsrc,
-                                     float* gedge, hipStream_t stream);
+                                     float* gedge, const BinWorkspace* ws, hipStream_t stream);
 // Backward of edge softmax (leaky ReLU optional) on the plain schedule.
 hipError_t launch_edge_softmax_backward(const GraphView& g, const PlanView* plan, int64_t H,
                                         const float* a, const float* go, const float* scores,

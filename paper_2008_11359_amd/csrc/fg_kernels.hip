@@ -1684,6 +1684,238 @@ __global__ __launch_bounds__(kBlock) void spmm_max_bwd_kernel(MaxBwdParams p) {
   }
 }
 
+// ---- binned gSpMM-max backward
+//
+// The same sums as spmm_max_bwd_kernel without global atomics: a counting
+// sort moves every gradient element, as an 8-byte (slot, value) record, into
+// the bin of its source tile (2^logR consecutive source rows, at most
+// kBinTileFloats values), and then one workgroup per piece of a bin adds its
+// records in LDS and writes the tile's rows with coalesced stores.  Device
+// fp32 atomics at scattered addresses run at about 2e10 per second on MI355X
+// whatever their contention (measured with the real target addresses and
+// with random ones), so the atomic kernel is bound by their rate; the binned
+// form streams arg, grad_out and the records instead.  Bins with more than
+// kBinPiece records are split over several workgroups, which add their
+// partial tiles with atomics into rows zeroed beforehand.
+//
+// Kernels, in stream order: counts per (group, bin) and per bin; prefix sums
+// over bins; the scatter of the records (each group reserves one run per bin
+// with an atomic add on the bin's cursor); the per-tile sums.  A group of the
+// counting and scatter kernels owns a range of whole rows, the same in both.
+
+constexpr int kBinPiece = 16384;       // records per accumulating workgroup
+constexpr int kBinBlock = 512;         // threads of an accumulating workgroup
+constexpr int kBinUnroll = 4;          // elements in flight per thread
+
+struct BinParams {
+  const int32_t* indices;
+  const int32_t* eid_pos;  // edge id -> storage position; null: edge id == position
+  const int32_t* arg;      // [rows, F]
+  const float* go;         // [rows, F]
+  const float* ev;         // [nnz_total, H] edge values (src_mul_edge only)
+  float* gsrc;             // [cols, F]
+  int32_t* total;          // [nb] records per bin (zeroed beforehand)
+  int32_t* start;          // [nb + 1] first record of each bin
+  int32_t* piece;          // [nb + 1] first accumulating workgroup of each bin
+  int32_t* cursor;         // [nb] next free record of each bin
+  int32_t* runs;           // [groups, nb] records per group and bin
+  int2* rec;               // records (slot in the tile, value bits)
+  int64_t num_rows, num_cols, id_limit;
+  int32_t F, H, dh, mul, logR, nb, rows_per_group;
+};
+
+// Source of the element whose forward took edge id e; -1 if e is not an edge
+// of this graph.
+__device__ __forceinline__ int32_t bin_source(const BinParams& p, int32_t e) {
+  if (e < 0 || e >= p.id_limit) return -1;
+  const int32_t q = p.eid_pos ? p.eid_pos[e] : e;
+  return q < 0 ? -1 : p.indices[q];
+}
+
+__device__ __forceinline__ int32_t bin_pieces(int32_t records) {
+  return records <= kBinPiece ? 1 : (records + kBinPiece - 1) / kBinPiece;
+}
+
+// Elements [first, first + n) of the flat [rows, F] arrays that this group
+// of the counting and scatter kernels owns (whole rows).
+__device__ __forceinline__ void bin_range(const BinParams& p, int64_t& first, int32_t& n) {
+  const int64_t r0 = (int64_t)blockIdx.x * p.rows_per_group;
+  const int64_t r1 = min(p.num_rows, r0 + p.rows_per_group);
+  first = r0 * p.F;
+  n = r1 > r0 ? (int32_t)((r1 - r0) * p.F) : 0;
+}
+
+// Records per (group, bin), counted in LDS; per bin also one global add.
+__global__ __launch_bounds__(kBlock) void bin_count_kernel(BinParams p) {
+  extern __shared__ int32_t bin_lds[];
+  int32_t* cnt = bin_lds;  // [nb]
+  for (int b = threadIdx.x; b < p.nb; b += kBlock) cnt[b] = 0;
+  __syncthreads();
+  int64_t first;
+  int32_t n;
+  bin_range(p, first, n);
+  for (int32_t t0 = threadIdx.x; t0 < n; t0 += kBlock * kBinUnroll) {
+    int32_t e[kBinUnroll];
+#pragma unroll
+    for (int k = 0; k < kBinUnroll; ++k) {
+      const int32_t t = t0 + k * kBlock;
+      e[k] = t < n ? p.arg[first + t] : -1;
+    }
+    int32_t u[kBinUnroll];
+#pragma unroll
+    for (int k = 0; k < kBinUnroll; ++k) u[k] = bin_source(p, e[k]);
+#pragma unroll
+    for (int k = 0; k < kBinUnroll; ++k)
+      if (u[k] >= 0) atomicAdd(&cnt[u[k] >> p.logR], 1);
+  }
+  __syncthreads();
+  int32_t* mine = p.runs + (int64_t)blockIdx.x * p.nb;
+  for (int b = threadIdx.x; b < p.nb; b += kBlock) {
+    const int32_t c = cnt[b];
+    mine[b] = c;
+    if (c) atomicAdd(&p.total[b], c);
+  }
+}
+
+// Exclusive prefix sums of the bin sizes (record offsets) and of their piece
+// counts (accumulating workgroups); one workgroup of 1024 threads.
+constexpr int kBinScanThreads = 1024;
+__global__ __launch_bounds__(kBinScanThreads) void bin_scan_kernel(BinParams p) {
+  __shared__ int32_t s_rec[kBinScanThreads];
+  __shared__ int32_t s_pc[kBinScanThreads];
+  const int t = threadIdx.x;
+  const int per = (p.nb + kBinScanThreads - 1) / kBinScanThreads;
+  const int b0 = min(p.nb, t * per), b1 = min(p.nb, b0 + per);
+  int32_t rec = 0, pc = 0;
+  for (int b = b0; b < b1; ++b) {
+    rec += p.total[b];
+    pc += bin_pieces(p.total[b]);
+  }
+  s_rec[t] = rec;
+  s_pc[t] = pc;
+  __syncthreads();
+  for (int off = 1; off < kBinScanThreads; off <<= 1) {
+    const int32_t a = t >= off ? s_rec[t - off] : 0;
+    const int32_t c = t >= off ? s_pc[t - off] : 0;
+    __syncthreads();
+    s_rec[t] += a;
+    s_pc[t] += c;
+    __syncthreads();
+  }
+  rec = s_rec[t] - rec;
+  pc = s_pc[t] - pc;
+  for (int b = b0; b < b1; ++b) {
+    p.start[b] = rec;
+    p.cursor[b] = rec;
+    p.piece[b] = pc;
+    rec += p.total[b];
+    pc += bin_pieces(p.total[b]);
+  }
+  if (t == kBinScanThreads - 1) {
+    p.start[p.nb] = s_rec[t];
+    p.piece[p.nb] = s_pc[t];
+  }
+}
+
+// Zeroes the rows of every split bin (their pieces add with atomics), then
+// reserves this group's run in each bin it feeds and writes each element's
+// record into it, ranked inside the run through LDS.
+__global__ __launch_bounds__(kBlock) void bin_scatter_kernel(BinParams p) {
+  extern __shared__ int32_t bin_lds[];
+  int32_t* cnt = bin_lds;          // [nb]
+  int32_t* run = bin_lds + p.nb;   // [nb]
+  const int64_t tile = ((int64_t)1 << p.logR) * p.F;
+  for (int b = blockIdx.x; b < p.nb; b += gridDim.x) {
+    if (p.piece[b + 1] - p.piece[b] == 1) continue;
+    const int64_t lo = (int64_t)b * tile;
+    const int64_t hi = min(p.num_cols * p.F, lo + tile);
+    for (int64_t t = lo + threadIdx.x; t < hi; t += kBlock) p.gsrc[t] = 0.0f;
+  }
+  const int32_t* mine = p.runs + (int64_t)blockIdx.x * p.nb;
+  for (int b = threadIdx.x; b < p.nb; b += kBlock) {
+    const int32_t c = mine[b];
+    cnt[b] = 0;
+    run[b] = c ? atomicAdd(&p.cursor[b], c) : 0;
+  }
+  __syncthreads();
+  int64_t first;
+  int32_t n;
+  bin_range(p, first, n);
+  for (int32_t t0 = threadIdx.x; t0 < n; t0 += kBlock * kBinUnroll) {
+    int32_t e[kBinUnroll];
+    float g[kBinUnroll];
+#pragma unroll
+    for (int k = 0; k < kBinUnroll; ++k) {
+      const int32_t t = t0 + k * kBlock;
+      e[k] = -1;
+      g[k] = 0.0f;
+      if (t < n) {
+        e[k] = p.arg[first + t];
+        g[k] = p.go[first + t];
+      }
+    }
+    int32_t u[kBinUnroll];
+#pragma unroll
+    for (int k = 0; k < kBinUnroll; ++k) u[k] = bin_source(p, e[k]);
+#pragma unroll
+    for (int k = 0; k < kBinUnroll; ++k) {
+      if (u[k] < 0) continue;
+      const int32_t t = t0 + k * kBlock;
+      const int32_t b = u[k] >> p.logR;
+      const int32_t r = atomicAdd(&cnt[b], 1);
+      const int32_t f = t % p.F;
+      float v = g[k];
+      if (p.mul) v = p.ev[(int64_t)e[k] * p.H + (p.H == 1 ? 0 : f / p.dh)] * v;
+      const int32_t slot = (u[k] - (b << p.logR)) * p.F + f;
+      p.rec[run[b] + r] = make_int2(slot, __float_as_int(v));
+    }
+  }
+}
+
+// One piece of one bin: adds its records into an LDS tile and writes the
+// tile's rows (plain stores for a whole bin, atomics for a split one).
+__global__ __launch_bounds__(kBinBlock) void bin_accumulate_kernel(BinParams p) {
+  __shared__ float tile[kBinTileFloats];
+  const int32_t i = (int32_t)blockIdx.x;
+  if (i >= p.piece[p.nb]) return;
+  int lo = 0, hi = p.nb - 1;  // the last bin whose first piece is <= i
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (p.piece[mid] <= i) lo = mid;
+    else hi = mid - 1;
+  }
+  const int b = lo;
+  const int32_t k = i - p.piece[b];
+  const bool whole = p.piece[b + 1] - p.piece[b] == 1;
+  const int64_t r0 = (int64_t)p.start[b] + (int64_t)k * kBinPiece;
+  const int64_t r1 = min((int64_t)p.start[b + 1], r0 + kBinPiece);
+  const int64_t row0 = (int64_t)b << p.logR;
+  const int32_t n_el = (int32_t)(min((int64_t)1 << p.logR, p.num_cols - row0) * p.F);
+  for (int32_t t = threadIdx.x; t < n_el; t += kBinBlock) tile[t] = 0.0f;
+  __syncthreads();
+  for (int64_t j0 = r0 + threadIdx.x; j0 < r1; j0 += kBinBlock * kBinUnroll) {
+    int2 q[kBinUnroll];
+#pragma unroll
+    for (int k2 = 0; k2 < kBinUnroll; ++k2) {
+      const int64_t j = j0 + k2 * kBinBlock;
+      q[k2] = j < r1 ? p.rec[j] : make_int2(-1, 0);
+    }
+#pragma unroll
+    for (int k2 = 0; k2 < kBinUnroll; ++k2)
+      if (q[k2].x >= 0) atomicAdd(&tile[q[k2].x], __int_as_float(q[k2].y));
+  }
+  __syncthreads();
+  float* dst = p.gsrc + row0 * p.F;
+  if (whole) {
+    for (int32_t t = threadIdx.x; t < n_el; t += kBinBlock) dst[t] = tile[t];
+  } else {
+    for (int32_t t = threadIdx.x; t < n_el; t += kBinBlock) {
+      const float v = tile[t];
+      if (v != 0.0f) unsafeAtomicAdd(&dst[t], v);
+    }
+  }
+}
+
 // float4 k of a contiguous row's flat range of an [E, H] array; elements
 // outside the range read as `fill` / are not written.
 __device__ __forceinline__ void flat_load4(const float* base, const ContigRange& r, int64_t k,
@@ -2667,11 +2899,70 @@ hipError_t launch_build_eid_pos(const int32_t* eids, int64_t nnz, int64_t nnz_to
   return hipGetLastError();
 }
 
+// Tile rows (log2) and bin count of the binned max backward for width F;
+// false if the shape does not fit its LDS tables or int32 record offsets.
+// Tile rows (log2) and bin count of the binned max backward for width F;
+// false if the shape does not fit the workspace, its LDS tables or int32
+// record offsets.
+static bool bin_shape(const GraphView& g, int64_t F, const BinWorkspace* ws, int& logR, int& nb) {
+  if (!ws || !ws->rec || F < 1 || F > kBinTileFloats) return false;
+  if (g.num_rows * F > INT32_MAX || g.num_rows * F > ws->rec_capacity) return false;
+  const int64_t bins = bin_tiles(g.num_cols, F);
+  if (bins < 1 || bins > kMaxBins || bins > ws->max_bins) return false;
+  logR = bin_log_rows(F);
+  nb = (int)bins;
+  return true;
+}
+
 hipError_t launch_gspmm_max_backward(const GraphView& g, const int32_t* eid_pos, int msg,
                                      int64_t H, int64_t dh, const float* x, const float* ev,
                                      const int32_t* arg, const float* go, float* gsrc,
-                                     float* gedge, hipStream_t stream) {
+                                     float* gedge, const BinWorkspace* ws, hipStream_t stream) {
   const int64_t F = H * dh;
+  int logR = 0, nb = 0;
+  if (gsrc && g.num_rows > 0 && g.nnz > 0 && bin_shape(g, F, ws, logR, nb)) {
+    // the edge gradient (if asked) still goes through the atomic kernel
+    hipError_t err = hipSuccess;
+    if (gedge) {
+      err = launch_gspmm_max_backward(g, eid_pos, msg, H, dh, x, ev, arg, go, nullptr, gedge,
+                                      nullptr, stream);
+      if (err != hipSuccess) return err;
+    }
+    BinParams bp;
+    bp.indices = g.indices;
+    bp.eid_pos = g.edge_ids ? eid_pos : nullptr;
+    bp.arg = arg;
+    bp.go = go;
+    bp.ev = ev;
+    bp.gsrc = gsrc;
+    bp.total = ws->tables;
+    bp.start = ws->tables + (kMaxBins + 1);
+    bp.piece = ws->tables + 2 * (kMaxBins + 1);
+    bp.cursor = ws->tables + 3 * (kMaxBins + 1);
+    bp.runs = ws->runs;
+    bp.rec = static_cast<int2*>(ws->rec);
+    bp.num_rows = g.num_rows;
+    bp.num_cols = g.num_cols;
+    bp.id_limit = g.edge_ids ? g.nnz_total : g.nnz;
+    bp.F = (int32_t)F;
+    bp.H = (int32_t)H;
+    bp.dh = (int32_t)dh;
+    bp.mul = msg == kSrcMulEdge ? 1 : 0;
+    bp.logR = logR;
+    bp.nb = nb;
+    bp.rows_per_group = (int32_t)((g.num_rows + kBinGroups - 1) / kBinGroups);
+    const int32_t groups = (int32_t)((g.num_rows + bp.rows_per_group - 1) / bp.rows_per_group);
+    FG_LAUNCH(fill_i32_kernel, stride_grid(nb), stream, bp.total, (int64_t)nb, 0);
+    hipLaunchKernelGGL(bin_count_kernel, dim3((unsigned)groups), dim3(kBlock), (size_t)nb * 4,
+                       stream, bp);
+    hipLaunchKernelGGL(bin_scan_kernel, dim3(1), dim3(kBinScanThreads), 0, stream, bp);
+    hipLaunchKernelGGL(bin_scatter_kernel, dim3((unsigned)groups), dim3(kBlock), (size_t)nb * 8,
+                       stream, bp);
+    const int64_t pieces = nb + (g.num_rows * F + kBinPiece - 1) / kBinPiece;
+    hipLaunchKernelGGL(bin_accumulate_kernel, dim3((unsigned)pieces), dim3(kBinBlock), 0, stream,
+                       bp);
+    return hipGetLastError();
+  }
   hipError_t err = zero_fill(gsrc, g.num_cols * F, stream);
   if (err != hipSuccess) return err;
   if ((err = zero_fill(gedge, g.nnz_total * H, stream)) != hipSuccess) return err;

@@ -25,7 +25,7 @@ hipError_t launch_gsddmm_softmax(const GraphView&, const PlanView*, int64_t, con
 }
 hipError_t launch_gspmm_max_backward(const GraphView&, const int32_t*, int, int64_t, int64_t,
                                      const float*, const float*, const int32_t*, const float*, float*,
-                                     float*, hipStream_t) {
+                                     float*, const BinWorkspace*, hipStream_t) {
   return hipErrorNotSupported;
 }
 hipError_t launch_edge_softmax_backward(const GraphView&, const PlanView*, int64_t, const float*,

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert fg._lib.fg_abi_version() == fg.ABI_VERSION == 2
+    assert fg._lib.fg_abi_version() == fg.ABI_VERSION == 3
     for s in (0, -1, -2, -3, -4):
         assert fg.status_string(s) and fg.status_string(s) != "unknown status"
     assert fg.status_string(7) == "unknown status"
@@ -250,10 +250,14 @@ def test_plan_create_rejects_invalid_arguments():
     opt = fg._PlanOptions()
     assert L.fg_plan_create(ctypes.byref(g), None, None, 0, None, ctypes.byref(h), None) == -1
     assert L.fg_plan_create(ctypes.byref(g), None, None, 8, None, None, None) == -1
-    opt.reserved[2] = 1
+    opt.reserved[1] = 1
     assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1
-    opt.reserved[2] = 0
+    opt.reserved[1] = 0
+    opt.max_backward = 2  # 0 or 1
+    assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
+                            None) == -1
+    opt.max_backward = 0
     opt.max_row_segments = 1  # a row must be allowed at least two pieces
     assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1

@@ -220,10 +220,11 @@ def _sources_of_ids(csr, nnz_total):
 
 
 def check_max_backward(csr, G, x, go, plan=None, edge=None, heads=1, nnz_total=None,
-                       exact=False, want_edge=False):
+                       exact=False, want_edge=False, bwd_plan=None):
     """gspmm(max) forward on the GPU, then its gradient, vs the oracle's
     gradient (which recomputes the argmax itself).  Term counts for the
-    tolerance come from the oracle's own forward."""
+    tolerance come from the oracle's own forward.  bwd_plan: a different plan
+    for the backward call."""
     F = int(np.prod(x.shape[1:]))
     dh = F // heads
     nt = csr.nnz if nnz_total is None else nnz_total
@@ -233,8 +234,8 @@ def check_max_backward(csr, G, x, go, plan=None, edge=None, heads=1, nnz_total=N
         None if plan is None else plan.info()["segment_edges"]))
     tx, te = dev(x), (None if edge is None else dev(edge))
     _, arg = fg.gspmm(G, tx, te, msg=msg, reduce="max", heads=heads, plan=plan)
-    res = fg.gspmm_max_backward(G, arg, dev(go), x=tx, edge=te, msg=msg, heads=heads, plan=plan,
-                                want_edge=want_edge)
+    res = fg.gspmm_max_backward(G, arg, dev(go), x=tx, edge=te, msg=msg, heads=heads,
+                                plan=plan if bwd_plan is None else bwd_plan, want_edge=want_edge)
     gs, ge = (res if want_edge else (res, None))
     gs = host(gs).reshape(csr.num_cols, F)
     x2 = x.reshape(csr.num_cols, F)
@@ -458,7 +459,8 @@ def test_max_backward(small_rmat, d, heads, weighted):
     gi = rng.integers(-8, 9, (csr.num_rows, d)).astype(np.float32)  # exact sums
     w = (rng.random((csr.nnz, heads)) + 0.5).astype(np.float32) if weighted else None
     wi = rng.integers(1, 3, (csr.nnz, heads)).astype(np.float32) if weighted else None
-    for plan in (None, fg.Plan(G, max_width=d, segment_edges=64)):
+    for plan in (None, fg.Plan(G, max_width=d, segment_edges=64),
+                 fg.Plan(G, max_width=d, max_backward=True)):
         check_max_backward(csr, G, x, go, plan=plan, edge=w, heads=heads, want_edge=weighted)
         check_max_backward(csr, G, xi, gi, plan=plan, edge=wi, heads=heads, want_edge=weighted,
                            exact=True)
@@ -488,7 +490,7 @@ def test_backward_on_transposed_graph(small_rmat):
     go = rng.standard_normal((csc.num_rows, 16)).astype(np.float32)
     w = (rng.random((csr.nnz, 2)) + 0.5).astype(np.float32)
     for seg in (0, 64):
-        plan = fg.Plan(Gt, max_width=16, segment_edges=seg)
+        plan = fg.Plan(Gt, max_width=16, segment_edges=seg, max_backward=seg == 64)
         check_max_backward(csc, Gt, x, go, plan=plan, nnz_total=csr.nnz)
         check_max_backward(csc, Gt, x, go, plan=plan, edge=w, heads=2, nnz_total=csr.nnz,
                            want_edge=True)
@@ -498,6 +500,50 @@ def test_backward_on_transposed_graph(small_rmat):
     with pytest.raises(fg.FgError):  # no plan: no id -> position map
         fg.gspmm_max_backward(Gt, torch.zeros((csc.num_rows, 16), dtype=torch.int32,
                                               device="cuda"), dev(go))
+
+
+def test_max_backward_binned_shapes():
+    """The binned max backward (plan option) at the shapes that decide its
+    tables: bins split over several workgroups (one hot source takes every
+    row's maximum), a last tile cut short by the source count, and the shapes
+    that fall back to atomics (width above the plan's, a row wider than one
+    LDS tile, more tiles than the bin tables hold)."""
+    rng = np.random.default_rng(2024)
+    # hot source 0: 3000 rows x 16 features = 48,000 records in one bin
+    n, C, F = 3000, 301, 16
+    src = np.concatenate([np.zeros((n, 1), np.int64), rng.integers(1, C, (n, 4))], axis=1)
+    dst = np.repeat(np.arange(n), 5)
+    csr = synth.coo_to_csr(dst, src.reshape(-1), n, C)
+    G = fg.Graph.from_csr(csr)
+    x = rng.standard_normal((C, F)).astype(np.float32)
+    x[0] = 10.0  # source 0 wins every row and feature
+    go = rng.integers(-8, 9, (n, F)).astype(np.float32)
+    plan = fg.Plan(G, F, max_backward=True)
+    info = plan.info()
+    assert info["max_backward"] == 1
+    assert info["workspace_bytes"] >= 8 * n * F
+    check_max_backward(csr, G, x, go, plan=plan, exact=True)
+    check_max_backward(csr, G, x, rng.standard_normal((n, F)).astype(np.float32), plan=plan)
+    w = rng.integers(1, 4, (csr.nnz, 1)).astype(np.float32)
+    check_max_backward(csr, G, x, go, plan=plan, edge=w, want_edge=True, exact=True)
+    # width above the plan's: atomics
+    plan8 = fg.Plan(G, 8, max_backward=True)
+    check_max_backward(csr, G, x, go, plan=plan, bwd_plan=plan8, exact=True)
+    # a row wider than one LDS tile (16,384 floats): atomics
+    g2 = synth.small_random_graph(np.random.default_rng(5), 12, 9, 60)
+    G2 = fg.Graph.from_csr(g2)
+    F2 = 16400
+    x2 = rng.standard_normal((g2.num_cols, F2)).astype(np.float32)
+    go2 = rng.integers(-4, 5, (g2.num_rows, F2)).astype(np.float32)
+    check_max_backward(g2, G2, x2, go2, plan=fg.Plan(G2, F2, max_backward=True), exact=True)
+    # 8 source rows per tile at width 2048: 70,000 sources need 8,750 tiles
+    # (more than the 8,192 the tables hold): atomics; 59,999 need 7,500: binned
+    for cols in (70000, 59999):
+        g3 = synth.small_random_graph(np.random.default_rng(cols), 40, cols, 400)
+        G3 = fg.Graph.from_csr(g3)
+        x3 = rng.standard_normal((cols, 2048)).astype(np.float32)
+        go3 = rng.integers(-4, 5, (40, 2048)).astype(np.float32)
+        check_max_backward(g3, G3, x3, go3, plan=fg.Plan(G3, 2048, max_backward=True), exact=True)
 
 
 @pytest.mark.parametrize("n,d_in,d_out", [(1, 1, 1), (17, 8, 128), (1000, 8, 33),
@@ -621,7 +667,7 @@ def test_edge_cases():
     dup = synth.CSR(2, 3, np.array([0, 5, 6], np.int32), np.array([1, 1, 1, 2, 2, 0], np.int32))
     G = fg.Graph.from_csr(dup)
     xi = np.array([[1, 2, 3, 4], [5, 5, 5, 5], [5, 0, 5, 0]], np.float32)
-    for plan in (None, fg.Plan(G, 4, 2)):
+    for plan in (None, fg.Plan(G, 4, 2), fg.Plan(G, 4, 2, max_backward=True)):
         check_spmm(dup, G, xi, plan=plan, reduce="max")
         check_spmm(dup, G, xi, plan=plan, exact=True)
         s = check_sddmm(dup, G, xi, xi[:2], plan=plan, exact=True)
@@ -638,7 +684,7 @@ def test_edge_cases():
                                np.arange(6, dtype=np.float32), plan=plan)
     # backward without edges: gradients all zero, softmax gradient writes nothing
     G = fg.Graph.from_csr(noedge)
-    for plan in (None, fg.Plan(G, 8, 4)):
+    for plan in (None, fg.Plan(G, 8, 4), fg.Plan(G, 8, 4, max_backward=True)):
         gs = fg.gspmm_max_backward(G, torch.full((3, 8), -1, dtype=torch.int32, device="cuda"),
                                    dev(np.ones((3, 8), np.float32)), plan=plan)
         assert gs.shape == (5, 8) and np.all(host(gs) == 0)
@@ -701,7 +747,7 @@ def test_random_configurations(seed):
         plan = fg.Plan(G, max(F, heads, 1), segment_edges=int(rng.choice([0, 1, 7, 64, 512])),
                        source_slab_rows=int(rng.choice([0, -1, -2, 37, 500])),
                        partition_min_degree=int(rng.choice([0, 1, 16])),
-                       item_order=int(rng.integers(0, 3)))
+                       item_order=int(rng.integers(0, 3)), max_backward=seed % 2 == 1)
         say("plan", plan.info())
     nt = nnz_total or g.nnz
     ops = rng.choice(["sum", "mul", "max", "sddmm", "softmax", "softmax_bwd", "max_bwd", "gat",
@@ -915,9 +961,12 @@ def test_rmat_233k_max_backward_full(rmat_full):
     the whole [N, 128] gradient must equal the oracle's bit for bit."""
     w, G = rmat_full
     csr = w.csr
-    plan = fg.Plan(G, 128)
     go = np.random.default_rng(8).integers(-8, 9, (csr.num_rows, 128)).astype(np.float32)
-    check_max_backward(csr, G, w.arrays["x"], go, plan=plan, exact=True)
+    for binned in (False, True):
+        plan = fg.Plan(G, 128, max_backward=binned)
+        assert plan.info()["max_backward"] == int(binned)
+        check_max_backward(csr, G, w.arrays["x"], go, plan=plan, exact=True)
+        plan.close()
 
 
 @pytest.mark.slow
