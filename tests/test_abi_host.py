@@ -257,6 +257,13 @@ def test_plan_create_rejects_invalid_arguments():
     opt.max_backward = 2  # 0 or 1
     assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1
+    # the binned max-backward records need rows x max_width <= 2^31 - 1 (int32
+    # offsets): refused before any device work
+    opt.max_backward = 1
+    big = _graph_struct(num_rows=1 << 20, num_cols=8, nnz=7)
+    assert L.fg_plan_create(ctypes.byref(big), None, None, 4096, ctypes.byref(opt),
+                            ctypes.byref(h), None) == fg.FG_ERR_UNSUPPORTED
+    assert not h.value
     opt.max_backward = 0
     opt.max_row_segments = 1  # a row must be allowed at least two pieces
     assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
