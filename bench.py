@@ -351,11 +351,21 @@ def setup(name, d, args, fg, torch, dev):
             Op("bwd_spmm_csc_a", lambda: fg.gspmm(Gt, gy, at, msg="src_mul_edge", plan=Pt,
                                                   out=dx_a),
                bytes_spmm(n, e, F, H, weighted=True), 2 * e * F, graded=True),
-            Op("bwd_sddmm_da", lambda: fg.gsddmm(G, x, gy, plan=P, out=da),
-               bytes_sddmm(n, e, F, H), 2 * e * F, graded=True),
-            Op("bwd_edge_softmax", lambda: fg.edge_softmax_backward(
-                G, at, da, scores=sc, leaky=True, slope=0.2, plan=P, grad_scores=da),
-               bytes_softmax_bwd(n, e, H), 4 * e * H),
+        ]
+        if args.fused:  # score gradient in one call: SDDMM dY.X fused with the softmax backward
+            ops.append(Op("bwd_sddmm_softmax", lambda: fg.gsddmm_edge_softmax_backward(
+                G, x, gy, at, scores=sc, leaky=True, slope=0.2, plan=P, grad_scores=da),
+                bytes_sddmm(n, e, F, H) + bytes_softmax_bwd(n, e, H) - 4 * (n + 1) - 8 * e * H,
+                2 * e * F + 4 * e * H))
+        else:
+            ops += [
+                Op("bwd_sddmm_da", lambda: fg.gsddmm(G, x, gy, plan=P, out=da),
+                   bytes_sddmm(n, e, F, H), 2 * e * F, graded=True),
+                Op("bwd_edge_softmax", lambda: fg.edge_softmax_backward(
+                    G, at, da, scores=sc, leaky=True, slope=0.2, plan=P, grad_scores=da),
+                   bytes_softmax_bwd(n, e, H), 4 * e * H),
+            ]
+        ops += [
             Op("bwd_spmm_csc_ds", lambda: fg.gspmm(Gt, x, da, msg="src_mul_edge", plan=Pt,
                                                    out=dx_s),
                bytes_spmm(n, e, F, H, weighted=True), 2 * e * F, graded=True),

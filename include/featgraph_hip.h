@@ -347,6 +347,33 @@ fg_status fg_edge_softmax_backward(const fg_graph* g, int32_t num_heads, const f
                                    float* grad_scores, fg_plan* plan, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * The score gradient of an attention layer in one call: the gSDDMM dot of
+ * x_src and x_dst per head (Sec. II-A: the gradient of the SpMM y = A(s) x
+ * w.r.t. its edge values is an SDDMM of the upstream gradient with x), fed
+ * straight into fg_edge_softmax_backward.  Per row v and head h:
+ *   g_e = sum_k x_src[u_e, h, k] * x_dst[v, h, k]
+ *   c   = sum_{edges p of v} out_p * g_p
+ *   grad_scores[e, h] = out_e * (g_e - c) * (leaky && !(s_e > 0) ? slope : 1)
+ * x_src      [num_cols, H, dh] (the layer's source features)
+ * x_dst      [num_rows, H, dh] (the upstream gradient of the aggregation)
+ * out        [nnz_total, H] the forward softmax's result
+ * scores     [nnz_total, H] the forward softmax's input; required iff
+ *            apply_leaky_relu
+ * grad_scores [nnz_total, H]; entries of edges of g are written.  It must not
+ *            overlap any input.
+ * One fused pass when 2 <= H <= 16, head_dim is 16, 32 or 64, H * head_dim
+ * <= 256, the feature arrays are 16-byte aligned and the plan (if any) cuts
+ * no row of its softmax schedule; otherwise the same results through
+ * fg_gsddmm into grad_scores followed by fg_edge_softmax_backward in place.
+ * Sums are fp32 in a fixed order for a given plan (deterministic).
+ * ------------------------------------------------------------------------- */
+fg_status fg_gsddmm_edge_softmax_backward(const fg_graph* g, int32_t num_heads, int64_t head_dim,
+                                          const float* x_src, const float* x_dst,
+                                          const float* out, const float* scores,
+                                          int32_t apply_leaky_relu, float negative_slope,
+                                          float* grad_scores, fg_plan* plan, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Dense vertex transform y = x w (fp32 on the matrix cores): the vector-matrix
  * product of the MLP aggregation's message function (Fig. 3b), applied once
  * per vertex.  x [n, d_in], w [d_in, d_out], y [n, d_out] row-major; y must

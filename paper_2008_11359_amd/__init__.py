@@ -123,6 +123,9 @@ def _load():
                                           vp]
     lib.fg_edge_softmax_backward.restype = ctypes.c_int
     lib.fg_edge_softmax_backward.argtypes = [gp, i32, vp, vp, vp, i32, ctypes.c_float, vp, vp, vp]
+    lib.fg_gsddmm_edge_softmax_backward.restype = ctypes.c_int
+    lib.fg_gsddmm_edge_softmax_backward.argtypes = [gp, i32, i64, vp, vp, vp, vp, i32,
+                                                    ctypes.c_float, vp, vp, vp]
     lib.fg_gsddmm_edge_softmax.restype = ctypes.c_int
     lib.fg_gsddmm_edge_softmax.argtypes = [gp, i32, i64, vp, vp, i32, ctypes.c_float, vp, vp, vp,
                                            vp]
@@ -592,6 +595,46 @@ def edge_softmax_backward(g: Graph, out: torch.Tensor, grad_out: torch.Tensor,
                                        _ptr(scores), 1 if leaky else 0, float(slope),
                                        _ptr(grad_scores), _plan_handle(plan), _stream())
     _check(st, "fg_edge_softmax_backward")
+    return grad_scores
+
+
+def gsddmm_edge_softmax_backward(g: Graph, x_src: torch.Tensor, x_dst: torch.Tensor,
+                                 out: torch.Tensor, scores: Optional[torch.Tensor] = None,
+                                 leaky: bool = True, slope: float = 0.2,
+                                 plan: Optional[Plan] = None,
+                                 grad_scores: Optional[torch.Tensor] = None):
+    """The score gradient of an attention layer in one call: the per-head
+    gsddmm of x_src [num_cols, H, dh] and x_dst [num_rows, H, dh] (the
+    aggregation's upstream gradient), fed into edge_softmax_backward with the
+    forward's attention weights `out` [nnz_total, H] (and scores for the
+    leaky ReLU).  Returns grad_scores [nnz_total, H]."""
+    x_src = _dev_tensor(x_src, torch.float32, "x_src")
+    x_dst = _dev_tensor(x_dst, torch.float32, "x_dst")
+    out = _dev_tensor(out, torch.float32, "out")
+    if x_src.dim() != 3 or x_dst.dim() != 3 or x_src.shape[1:] != x_dst.shape[1:]:
+        raise ValueError("x_src and x_dst must be [n, H, dh] with the same H and dh")
+    if x_src.shape[0] != g.num_cols or x_dst.shape[0] != g.num_rows:
+        raise ValueError("x_src must have num_cols rows and x_dst num_rows rows")
+    heads, dh = int(x_src.shape[1]), int(x_src.shape[2])
+    if out.numel() != g.nnz_total * heads:
+        raise ValueError("out must be [nnz_total, H]")
+    if leaky:
+        if scores is None:
+            raise ValueError("the leaky ReLU's gradient needs the forward's scores")
+        scores = _dev_tensor(scores, torch.float32, "scores")
+        if scores.numel() != out.numel():
+            raise ValueError("scores must have the size of out")
+    else:
+        scores = None
+    grad_scores = torch.empty((g.nnz_total, heads), dtype=torch.float32, device=out.device) \
+        if grad_scores is None else _dev_tensor(grad_scores, torch.float32, "grad_scores")
+    if grad_scores.numel() != out.numel():
+        raise ValueError("grad_scores has the wrong size")
+    st = _lib.fg_gsddmm_edge_softmax_backward(ctypes.byref(g._c), heads, dh, _ptr(x_src),
+                                              _ptr(x_dst), _ptr(out), _ptr(scores),
+                                              1 if leaky else 0, float(slope),
+                                              _ptr(grad_scores), _plan_handle(plan), _stream())
+    _check(st, "fg_gsddmm_edge_softmax_backward")
     return grad_scores
 
 

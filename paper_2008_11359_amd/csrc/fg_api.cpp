@@ -1017,6 +1017,32 @@ fg_status fg_edge_softmax_backward(const fg_graph* g, int32_t num_heads, const f
       static_cast<hipStream_t>(stream)));
 }
 
+fg_status fg_gsddmm_edge_softmax_backward(const fg_graph* g, int32_t num_heads, int64_t head_dim,
+                                          const float* x_src, const float* x_dst,
+                                          const float* out, const float* scores,
+                                          int32_t apply_leaky_relu, float negative_slope,
+                                          float* grad_scores, fg_plan* plan, void* stream) {
+  fg_status st = check_graph(g);
+  if (st != FG_OK) return st;
+  if ((st = check_width(num_heads, head_dim)) != FG_OK) return st;
+  const int64_t F = (int64_t)num_heads * head_dim;
+  if (g->nnz > 0 && (!x_src || !x_dst || !out || !grad_scores)) return FG_ERR_INVALID_ARG;
+  if (g->nnz > 0 && apply_leaky_relu && !scores) return FG_ERR_INVALID_ARG;
+  // the SDDMM may run on the gather schedule (F wide) and the softmax
+  // backward keeps H floats per slot
+  if ((st = check_plan(plan, g, F)) != FG_OK) return st;
+  const int64_t b = nnz_total_of(g) * num_heads * 4;
+  if (overlaps(grad_scores, b, x_src, g->num_cols * F * 4) ||
+      overlaps(grad_scores, b, x_dst, g->num_rows * F * 4) || overlaps(grad_scores, b, out, b) ||
+      overlaps(grad_scores, b, apply_leaky_relu ? scores : nullptr, b))
+    return FG_ERR_INVALID_ARG;
+  const fg::GraphView gv = view_of(g);
+  return from_hip(fg::launch_gsddmm_softmax_backward(
+      gv, plan ? &plan->gather : nullptr, plan ? &plan->plain : nullptr, num_heads, head_dim,
+      x_src, x_dst, out, apply_leaky_relu ? scores : nullptr, apply_leaky_relu != 0,
+      negative_slope, grad_scores, static_cast<hipStream_t>(stream)));
+}
+
 fg_status fg_dense_matmul(int64_t n, int64_t d_in, int64_t d_out, const float* x, const float* w,
                           float* y, void* stream) {
   if (n < 0 || n > INT32_MAX || d_in < 1 || d_out < 1 || d_in > FG_MAX_WIDTH ||

@@ -110,6 +110,16 @@ hipError_t launch_gspmm_max_backward(const GraphView& g, const int32_t* eid_pos,
                                      int64_t H, int64_t dh, const float* x, const float* ev,
                                      const int32_t* arg, const float* go, float* gsrc,
                                      float* gedge, const BinWorkspace* ws, hipStream_t stream);
+// Score gradient of an attention layer: SDDMM x_src . x_dst per head, then
+// the edge-softmax backward of its results, written to ds.  One fused kernel
+// on the plain schedule when it cuts no row (2 <= H <= 16, dh in {16, 32,
+// 64}, H * dh <= 256, aligned features); otherwise the two operators (the
+// SDDMM on the gather schedule into ds, then the softmax backward in place).
+hipError_t launch_gsddmm_softmax_backward(const GraphView& g, const PlanView* gather,
+                                          const PlanView* plain, int64_t H, int64_t dh,
+                                          const float* xs, const float* xd, const float* a,
+                                          const float* scores, bool leaky, float slope, float* ds,
+                                          hipStream_t stream);
 // Backward of edge softmax (leaky ReLU optional) on the plain schedule.
 hipError_t launch_edge_softmax_backward(const GraphView& g, const PlanView* plan, int64_t H,
                                         const float* a, const float* go, const float* scores,

@@ -2037,6 +2037,159 @@ __device__ __forceinline__ void softmax_bwd_contig(const SoftmaxBwdParams& p, co
   softmax_bwd_contig_apply(p, r, c);
 }
 
+// Multi-head SDDMM with the edge-softmax backward of its results fused in: the
+// score gradient of an attention layer.  Per row v and head h, with a the
+// forward's attention weights and s its scores:
+//   g_e = <x_src[u_e, h, :], x_dst[v, h, :]>      (the SDDMM: dL/da)
+//   c   = sum_e a_e g_e,   ds_e = a_e (g_e - c) * (leaky && !(s_e > 0) ? slope : 1)
+// Pass 1 computes g as sddmm_headed_kernel does (staged per 64-edge batch in
+// LDS), writes it to ds and accumulates c; pass 2 re-reads g (just written by
+// this wavefront, so mostly from L2), a and s and writes ds.  This replaces
+// the softmax backward's separate pass over the [E, H] arrays.
+// FLAT (edge id = position, H in {4, 8, 16}, aligned [E, H] arrays): a batch's
+// [cnt, H] block of a / g is a flat range handled as float4s, lane l always on
+// the heads (4l + q) mod H, exactly as softmax_bwd_contig lays out a row, so
+// pass 2 is softmax_bwd_contig_apply with g in place of the upstream
+// gradient; the batch's a loads are issued before its gathers.  Otherwise
+// lane j takes edge j of a batch and loops over its heads.  Whole rows only:
+// the launcher uses this kernel when no row is split (H <= kTabHeads).
+template <int S, bool SEG, bool FLAT>
+__global__ __launch_bounds__(kBlock) void sddmm_softmax_bwd_kernel(SddmmParams p, const float* a,
+                                                                   const float* sc, int leaky,
+                                                                   float slope) {
+  constexpr int U = 4;
+  constexpr int NC = FLAT ? 4 : kTabHeads;
+  __shared__ __align__(16) float tab_all[kWavesPerBlock * kWave * kTabHeads];
+  float* tab = tab_all + (threadIdx.x >> 6) * kWave * kTabHeads;
+  const int64_t item = wave_item();
+  if (item >= p.n_items) return;
+  const Item it = load_item<SEG>(p.segs, p.indptr, item);
+  if (it.row < 0) return;  // padding item of a partitioned schedule
+  if (it.b >= it.e) return;
+  const int lane = lane_id();
+  const int H = p.H;
+  const int G = 1 << p.logG;
+  const int ngroups = kWave >> p.logG;
+  const int gid = lane >> p.logG;
+  const int li = lane & (G - 1);
+  const int64_t F = p.F;
+  const int64_t f = (int64_t)li * 4;
+  const bool act = f < F;
+  const int64_t h = act ? f / p.dh : 0;
+  float xd[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (act) load_vec<4>(p.xd + it.row * F + f, xd);
+  float c[NC];  // FLAT: per float4 slot (fixed head); else per head
+#pragma unroll
+  for (int k = 0; k < NC; ++k) c[k] = 0.0f;
+
+  for (int64_t base = it.b; base < it.e; base += kWave) {
+    const int cnt = (int)min((int64_t)kWave, it.e - base);
+    int my_src = 0, my_eid = 0;
+    if (lane < cnt) {
+      my_src = __builtin_nontemporal_load(p.indices + base + lane);
+      my_eid = p.eids ? __builtin_nontemporal_load(p.eids + base + lane) : (int)(base + lane);
+    }
+    const int n4 = cnt * H / 4;  // FLAT: float4s of the batch's [cnt, H] block
+    float a4[4][4];
+    if constexpr (FLAT) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k = lane + kWave * i;
+        if (k < n4) {
+          load_vec<4>(a + base * H + 4 * k, a4[i]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) a4[i][q] = 0.0f;
+        }
+      }
+    }
+    for (int j0 = 0; j0 < cnt; j0 += ngroups * U) {
+      float val[U][4];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = j0 + u * ngroups + gid;
+        ok[u] = j < cnt;
+        const int src = __shfl(my_src, j & (kWave - 1));
+        if (ok[u] && act) {
+          load_vec<4>(p.xs + row_off(src, F) + f, val[u]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) val[u][k] = 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float part = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) part += val[u][k] * xd[k];
+        part = group_sum<S>(part);
+        if (ok[u] && act && (li % S) == S - 1) tab[(j0 + u * ngroups + gid) * H + h] = part;
+      }
+    }
+    wave_lds_sync();
+    if constexpr (FLAT) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k = lane + kWave * i;
+        if (k < n4) {
+          float g4[4];
+          load_vec<4>(tab + 4 * k, g4);
+          store_vec<4>(p.out + base * H + 4 * k, g4);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) c[q] = fmaf(a4[i][q], g4[q], c[q]);
+        }
+      }
+    } else if (lane < cnt) {  // lane j: edge base + j, its H values of g
+      const float* tr = tab + lane * H;
+      float* orow = p.out + (int64_t)my_eid * H;
+      const float* arow = a + (int64_t)my_eid * H;
+#pragma unroll
+      for (int hh = 0; hh < kTabHeads; ++hh)
+        if (hh < H) {
+          const float q = tr[hh];
+          orow[hh] = q;
+          c[hh] = fmaf(arow[hh], q, c[hh]);
+        }
+    }
+    wave_lds_sync();  // the table is rewritten by the next batch
+  }
+
+  if constexpr (FLAT) {
+    contig_allsum(c, H);
+    SoftmaxBwdParams q;
+    q.a = a;
+    q.go = p.out;
+    q.s = sc;
+    q.ds = p.out;
+    q.H = H;
+    q.leaky = leaky;
+    q.slope = slope;
+    softmax_bwd_contig_apply(q, contig_range(it.b, it.e, H), c);
+    return;
+  } else {
+    // c per head over the row: the lanes' shares, in a fixed butterfly
+#pragma unroll
+    for (int hh = 0; hh < kTabHeads; ++hh)
+      if (hh < H)
+        for (int off = 1; off < kWave; off <<= 1) c[hh] += __shfl_xor(c[hh], off);
+    for (int64_t base = it.b; base < it.e; base += kWave) {
+      const int cnt = (int)min((int64_t)kWave, it.e - base);
+      if (lane >= cnt) continue;
+      const int64_t e = p.eids ? (int64_t)p.eids[base + lane] : base + lane;
+      float* orow = p.out + e * H;
+      const float* arow = a + e * H;
+#pragma unroll
+      for (int hh = 0; hh < kTabHeads; ++hh)
+        if (hh < H) {
+          float o = arow[hh] * (orow[hh] - c[hh]);
+          if (leaky && !(sc[e * H + hh] > 0.0f)) o *= slope;
+          orow[hh] = o;
+        }
+    }
+  }
+}
+
 // ds_e = a_e * (go_e - c) * (leaky && s_e <= 0 ? slope : 1), c = sum_row a go.
 __device__ __forceinline__ void softmax_bwd_write(const SoftmaxBwdParams& p, int64_t b,
                                                   int64_t e, int eo, int epw, int h, float c) {
@@ -2694,6 +2847,64 @@ hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, in
     else if (nv == 2) sddmm_scalar_go<2, 2, false>(prm, seg, grid, stream);
     else sddmm_scalar_go<4, 1, false>(prm, seg, grid, stream);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_gsddmm_softmax_backward(const GraphView& g, const PlanView* gather,
+                                          const PlanView* plain, int64_t H, int64_t dh,
+                                          const float* xs, const float* xd, const float* a,
+                                          const float* scores, bool leaky, float slope, float* ds,
+                                          hipStream_t stream) {
+  if (g.num_rows == 0 || g.nnz == 0) return hipSuccess;
+  const int64_t F = H * dh;
+  const bool fused = H >= 2 && H <= kTabHeads && (dh == 16 || dh == 32 || dh == 64) &&
+                     F <= 4 * kWave && aligned16(xs) && aligned16(xd) &&
+                     (!plain || plain->num_slots == 0);
+  if (!fused) {  // the two operators, the second in place
+    hipError_t err = launch_gsddmm(g, gather, H, dh, xs, xd, ds, stream);
+    if (err != hipSuccess) return err;
+    return launch_edge_softmax_backward(g, plain, H, a, ds, scores, leaky, slope, ds, stream);
+  }
+  const bool seg = plain != nullptr;
+  SddmmParams prm;
+  prm.indptr = g.indptr;
+  prm.indices = g.indices;
+  prm.eids = g.edge_ids;
+  prm.xs = xs;
+  prm.xd = xd;
+  prm.out = ds;
+  prm.segs = seg ? plain->segs : nullptr;
+  prm.n_items = seg ? plain->num_nonempty : g.num_rows;
+  prm.F = F;
+  prm.H = (int32_t)H;
+  prm.dh = (int32_t)dh;
+  prm.logG = ilog2_ceil(F / 4);
+  prm.logS = 0;
+  prm.out_vec4 = 0;
+  const bool flat = g.edge_ids == nullptr && H % 4 == 0 && aligned16(ds) && aligned16(a) &&
+                    (!leaky || aligned16(scores));
+  const dim3 grid = grid_for(prm.n_items, 1);
+  const int lk = leaky ? 1 : 0;
+#define FG_SSB3(SS, SG, FL) \
+  FG_LAUNCH((sddmm_softmax_bwd_kernel<SS, SG, FL>), grid, stream, prm, a, scores, lk, slope)
+#define FG_SSB(SS)                 \
+  if (seg && flat)                 \
+    FG_SSB3(SS, true, true);       \
+  else if (seg)                    \
+    FG_SSB3(SS, true, false);      \
+  else if (flat)                   \
+    FG_SSB3(SS, false, true);      \
+  else                             \
+    FG_SSB3(SS, false, false);
+  if (dh == 16) {
+    FG_SSB(4)
+  } else if (dh == 32) {
+    FG_SSB(8)
+  } else {
+    FG_SSB(16)
+  }
+#undef FG_SSB3
+#undef FG_SSB
   return hipGetLastError();
 }
 

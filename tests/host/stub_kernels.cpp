@@ -33,6 +33,12 @@ hipError_t launch_edge_softmax_backward(const GraphView&, const PlanView*, int64
                                         hipStream_t) {
   return hipErrorNotSupported;
 }
+hipError_t launch_gsddmm_softmax_backward(const GraphView&, const PlanView*, const PlanView*,
+                                          int64_t, int64_t, const float*, const float*,
+                                          const float*, const float*, bool, float, float*,
+                                          hipStream_t) {
+  return hipErrorNotSupported;
+}
 hipError_t launch_build_eid_pos(const int32_t*, int64_t, int64_t, int32_t*, hipStream_t) {
   return hipErrorNotSupported;
 }

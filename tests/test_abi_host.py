@@ -208,6 +208,26 @@ def test_edge_softmax_backward_rejects_invalid_arguments():
     assert call(ds=GO + 4) == fg.FG_ERR_INVALID_ARG            # partial overlap of grad_out
 
 
+def test_gsddmm_edge_softmax_backward_rejects_invalid_arguments():
+    L = fg._lib
+    g = _graph_struct()  # 4 x 4, 7 edges
+    XS, XD, A, S, DS = 0x10000, 0x20000, 0x30000, 0x40000, 0x50000
+
+    def call(H=2, dh=16, xs=XS, xd=XD, a=A, s=S, leaky=1, ds=DS):
+        return L.fg_gsddmm_edge_softmax_backward(ctypes.byref(g), H, dh, xs, xd, a, s, leaky, 0.2,
+                                                 ds, None, None)
+
+    assert call(H=0) == fg.FG_ERR_INVALID_ARG
+    assert call(dh=0) == fg.FG_ERR_INVALID_ARG
+    for k in ("xs", "xd", "a", "ds"):
+        assert call(**{k: None}) == fg.FG_ERR_INVALID_ARG
+    assert call(s=None) == fg.FG_ERR_INVALID_ARG               # leaky needs the scores
+    assert call(ds=A + 4) == fg.FG_ERR_INVALID_ARG             # overlaps the weights
+    assert call(ds=S) == fg.FG_ERR_INVALID_ARG                 # overlaps the scores
+    assert call(ds=XS + 8) == fg.FG_ERR_INVALID_ARG            # overlaps the source features
+    assert call(ds=XD) == fg.FG_ERR_INVALID_ARG                # overlaps the destination features
+
+
 def test_dense_matmul_rejects_invalid_arguments():
     L = fg._lib
     X, W, Y = 0x10000, 0x20000, 0x30000

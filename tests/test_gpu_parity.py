@@ -296,6 +296,36 @@ def check_softmax_backward(csr, G, scores, go, rows=None, plan=None, heads=1, le
     return ds
 
 
+def check_sddmm_softmax_backward(csr, G, x, dy, scores, plan=None, leaky=True, nnz_total=None):
+    """Score gradient of an attention layer in one call (per-head SDDMM of x
+    and dy, then the softmax backward) vs the oracle's SDDMM followed by the
+    oracle's softmax backward.  x and dy hold small integers, so the dot
+    products are exact on both sides and the softmax-gradient tolerance
+    applies: |y - ref| <= 1e-5 * sqrt(n) * a (|G| + sum a|G|) + 1e-12."""
+    nt = csr.nnz if nnz_total is None else nnz_total
+    heads, dh = x.shape[1], x.shape[2]
+    say("gsddmm_edge_softmax_backward rows=%d nnz=%d H=%d dh=%d leaky=%s plan=%s" % (
+        csr.num_rows, csr.nnz, heads, dh, leaky,
+        None if plan is None else plan.info()["segment_edges"]))
+    ts = dev(scores.reshape(nt, heads))
+    a = fg.edge_softmax(G, ts, leaky=leaky, slope=0.2, plan=plan)
+    ds = host(fg.gsddmm_edge_softmax_backward(G, dev(x), dev(dy), a, scores=ts, leaky=leaky,
+                                              slope=0.2, plan=plan)).reshape(nt, heads)
+    F = heads * dh
+    g_ref = O.gsddmm(csr, x.reshape(csr.num_cols, F), dy.reshape(csr.num_rows, F), heads=heads,
+                     nnz_total=nt)
+    ref, scale = O.edge_softmax_backward(csr, scores.reshape(nt, heads), g_ref, heads=heads,
+                                         leaky=leaky, slope=0.2, nnz_total=nt, with_scale=True)
+    e = edge_ids_of(csr, np.arange(csr.nnz))
+    n = np.repeat(csr.degrees(), csr.degrees())[:, None]
+    bound = 1e-5 * np.sqrt(np.maximum(n, 1)) * scale[e] + 1e-12
+    err = np.abs(ds[e].astype(np.float64) - ref[e])
+    bad = err > bound
+    assert not bad.any(), "attention score gradient mismatch at %s: %r vs %r (bound %r)" % (
+        np.argwhere(bad)[0], ds[e][bad][0], ref[e][bad][0], bound[bad][0])
+    return ds
+
+
 def check_dense_matmul(n, d_in, d_out, seed, exact=False):
     rng = np.random.default_rng(seed)
     if exact:
@@ -477,6 +507,47 @@ def test_softmax_backward(small_rmat, heads, leaky):
         check_softmax_backward(csr, G, s, go, plan=plan, heads=heads, leaky=leaky)
     check_softmax_backward(csr, G, s, go, plan=fg.Plan(G, max_width=heads, segment_edges=64),
                            heads=heads, leaky=leaky, inplace=True)
+
+
+@pytest.mark.parametrize("heads,dh", [(8, 16), (4, 32), (2, 64), (16, 16), (3, 16), (2, 16),
+                                      (5, 20), (1, 32)])
+def test_sddmm_softmax_backward(small_rmat, heads, dh):
+    """The fused score gradient: one kernel for whole rows (2-16 heads of 16,
+    32 or 64 features, no row cut), else the two operators; on the CSR and on
+    the transposed graph with edge ids."""
+    csr, G = small_rmat
+    rng = np.random.default_rng(heads * 100 + dh)
+    x = rng.integers(-3, 4, (csr.num_cols, heads, dh)).astype(np.float32)
+    dy = rng.integers(-3, 4, (csr.num_rows, heads, dh)).astype(np.float32)
+    s = (3 * rng.standard_normal((csr.nnz, heads))).astype(np.float32)
+    s[rng.random(s.shape) < 0.02] = 0.0
+    F = heads * dh
+    for plan in (None, fg.Plan(G, F), fg.Plan(G, F, segment_edges=64)):
+        for leaky in (True, False):
+            check_sddmm_softmax_backward(csr, G, x, dy, s, plan=plan, leaky=leaky)
+    csc = csr_to_csc(csr)
+    Gt = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+    xt = rng.integers(-3, 4, (csc.num_cols, heads, dh)).astype(np.float32)
+    dyt = rng.integers(-3, 4, (csc.num_rows, heads, dh)).astype(np.float32)
+    check_sddmm_softmax_backward(csc, Gt, xt, dyt, s, plan=fg.Plan(Gt, F), nnz_total=csr.nnz)
+
+
+def test_sddmm_softmax_backward_matches_two_calls(small_rmat):
+    """With float features the fused kernel and the two separate operators
+    agree closely (the same products, the sums in another order)."""
+    csr, G = small_rmat
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((csr.num_cols, 8, 16)).astype(np.float32)
+    dy = rng.standard_normal((csr.num_rows, 8, 16)).astype(np.float32)
+    ts = dev((2 * rng.standard_normal((csr.nnz, 8))).astype(np.float32))
+    plan = fg.Plan(G, 128)
+    a = fg.edge_softmax(G, ts, plan=plan)
+    fused = host(fg.gsddmm_edge_softmax_backward(G, dev(x), dev(dy), a, scores=ts, plan=plan))
+    g = fg.gsddmm(G, dev(x), dev(dy), plan=plan)
+    two = host(fg.edge_softmax_backward(G, a, g, scores=ts, plan=plan))
+    np.testing.assert_allclose(fused, two, rtol=1e-4, atol=1e-6)
+    again = host(fg.gsddmm_edge_softmax_backward(G, dev(x), dev(dy), a, scores=ts, plan=plan))
+    np.testing.assert_array_equal(fused, again)  # deterministic
 
 
 def test_backward_on_transposed_graph(small_rmat):
