@@ -822,7 +822,7 @@ def test_random_configurations(seed):
         say("plan", plan.info())
     nt = nnz_total or g.nnz
     ops = rng.choice(["sum", "mul", "max", "sddmm", "softmax", "softmax_bwd", "max_bwd", "gat",
-                      "mlp", "sddmm_softmax"], size=3, replace=False)
+                      "mlp", "sddmm_softmax", "sddmm_softmax_bwd"], size=3, replace=False)
     say("seed", seed, kind, "n", n, "nnz", g.nnz, "F", F, "heads", heads, "ops", list(ops))
     for op in ops:
         if op == "sum":
@@ -860,6 +860,12 @@ def test_random_configurations(seed):
             check_mlp(g, G, xi, xj, wi, plan=plan, exact=True, square=False)
         elif op == "sddmm_softmax":
             check_sddmm_softmax(g, G, x, xd, plan=plan, heads=heads, nnz_total=nnz_total)
+        elif op == "sddmm_softmax_bwd":
+            dh = F // heads
+            xi = rng.integers(-3, 4, (g.num_cols, heads, dh)).astype(np.float32)
+            di = rng.integers(-3, 4, (g.num_rows, heads, dh)).astype(np.float32)
+            sc = (rng.standard_normal((nt, heads)) * 3).astype(np.float32)
+            check_sddmm_softmax_backward(g, G, xi, di, sc, plan=plan, nnz_total=nnz_total)
 
 
 def _odd(a=None, shape=None, dtype=torch.float32):
