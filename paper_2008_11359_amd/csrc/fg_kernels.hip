@@ -666,6 +666,116 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup_kernel(const Fix* fix, cons
   }
 }
 
+// The same merge with float4 lanes (F % 4 == 0, 16-byte aligned out / arg):
+// a wavefront covers 256 columns, so each slot costs one 1 KiB load per
+// wavefront instead of four.  Same slot order and combination order.
+template <bool MAX, bool EPI = false>
+__global__ __launch_bounds__(kBlock) void spmm_fixup4_kernel(const Fix* fix, const float* ws_f,
+                                                             const int32_t* ws_i, int64_t F,
+                                                             float* out, int32_t* arg,
+                                                             const float* xd,
+                                                             const int32_t* indptr) {
+  __shared__ float red_v[kWavesPerBlock][kWave][4];
+  __shared__ int32_t red_a[kWavesPerBlock][kWave][4];
+  const int w = threadIdx.x >> 6;
+  const int lane = lane_id();
+  const int64_t col = ((int64_t)blockIdx.y * kWave + lane) * 4;
+  const bool valid = col < F;
+  const Fix fx = fix[blockIdx.x];
+  constexpr int kStride = kWavesPerBlock;
+  float acc[4];
+  int32_t am[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    acc[c] = MAX ? -INFINITY : 0.0f;
+    am[c] = INT_MAX;
+  }
+  if (valid) {
+    for (int s0 = fx.slot_begin + w; s0 < fx.slot_end; s0 += 4 * kStride) {
+      float v[4][4];
+      int32_t a[4][4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int s = s0 + k * kStride;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          v[k][c] = MAX ? -INFINITY : 0.0f;
+          a[k][c] = INT_MAX;
+        }
+        if (s < fx.slot_end) {
+          load_vec<4>(ws_f + (int64_t)s * F + col, v[k]);
+          if constexpr (MAX) {
+            const int4 t = *reinterpret_cast<const int4*>(ws_i + (int64_t)s * F + col);
+            a[k][0] = t.x; a[k][1] = t.y; a[k][2] = t.z; a[k][3] = t.w;
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          if constexpr (MAX) {
+            if (takes_over(v[k][c], a[k][c], acc[c], am[c])) {
+              acc[c] = v[k][c];
+              am[c] = a[k][c];
+            }
+          } else {
+            acc[c] += v[k][c];
+          }
+        }
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    red_v[w][lane][c] = acc[c];
+    red_a[w][lane][c] = am[c];
+  }
+  __syncthreads();
+  if (w != 0 || !valid) return;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    acc[c] = red_v[0][lane][c];
+    am[c] = red_a[0][lane][c];
+  }
+#pragma unroll
+  for (int k = 1; k < kWavesPerBlock; ++k)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      if constexpr (MAX) {
+        if (takes_over(red_v[k][lane][c], red_a[k][lane][c], acc[c], am[c])) {
+          acc[c] = red_v[k][lane][c];
+          am[c] = red_a[k][lane][c];
+        }
+      } else {
+        acc[c] += red_v[k][lane][c];
+      }
+    }
+  const int64_t o = (int64_t)fx.row * F + col;
+  if constexpr (EPI || MAX) {
+    float ov[4];
+    int32_t oa[4];
+    float xv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if constexpr (EPI) load_vec<4>(xd + o, xv);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const bool none = am[c] == INT_MAX;
+      if constexpr (EPI) {
+        const float t = acc[c] + xv[c];
+        const bool pos = t > 0.0f;
+        ov[c] = (none || !pos) ? 0.0f : t;
+        oa[c] = none ? -1 : (pos ? am[c] : indptr[fx.row]);
+      } else {
+        ov[c] = none ? 0.0f : acc[c];
+        oa[c] = none ? -1 : am[c];
+      }
+    }
+    store_vec<4>(out + o, ov);
+    store_vec_i<4>(arg + o, oa);
+  } else {
+    store_vec<4>(out + o, acc);
+  }
+}
+
 // ----------------------------------------------------------------------------
 // generalized SDDMM (dot, per head)
 // ----------------------------------------------------------------------------
@@ -2689,9 +2799,24 @@ hipError_t launch_spmm_core(const GraphView& g, const PlanView* plan, int msg, i
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (seg && plan->num_split_rows > 0) {
-    const dim3 fgrid((unsigned)plan->num_split_rows, (unsigned)((F + kWave - 1) / kWave), 1);
     // the float4 kernel with positional edge ids defers the u_add_v epilogue
     const bool epi = xd && vec4 && !g.edge_ids;
+    // float4 merge: vec4 already checked F % 4, out (and arg, xd) alignment
+    if (vec4) {
+      const dim3 fgrid((unsigned)plan->num_split_rows, (unsigned)((F + 4 * kWave - 1) / (4 * kWave)),
+                       1);
+      if (epi)
+        FG_LAUNCH((spmm_fixup4_kernel<true, true>), fgrid, stream, plan->fix, plan->ws_f,
+                  plan->ws_i, F, out, arg, xd, g.indptr);
+      else if (mx)
+        FG_LAUNCH((spmm_fixup4_kernel<true>), fgrid, stream, plan->fix, plan->ws_f, plan->ws_i,
+                  F, out, arg, nullptr, nullptr);
+      else
+        FG_LAUNCH((spmm_fixup4_kernel<false>), fgrid, stream, plan->fix, plan->ws_f, plan->ws_i,
+                  F, out, arg, nullptr, nullptr);
+      return hipGetLastError();
+    }
+    const dim3 fgrid((unsigned)plan->num_split_rows, (unsigned)((F + kWave - 1) / kWave), 1);
     if (epi)
       FG_LAUNCH((spmm_fixup_kernel<true, true>), fgrid, stream, plan->fix, plan->ws_f,
                 plan->ws_i, F, out, arg, xd, g.indptr);
