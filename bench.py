@@ -536,8 +536,8 @@ def copy_probe(nbytes=1 << 30, reps=4):
 
 
 KERNEL_OPS = {  # regular expressions over kernel names; template args <G, NV, U, MUL, MAX, ...>
-    "spmm_mul_sum": (r"spmm_fast_kernel<\d+, \d+, \d+, true, false", r"spmm_fixup_kernel<false>"),
-    "spmm_max": (r"spmm_fast_kernel<\d+, \d+, \d+, false, true", r"spmm_fixup_kernel<true>"),
+    "spmm_mul_sum": (r"spmm_fast_kernel<\d+, \d+, \d+, true, false", r"spmm_fixup4?_kernel<false"),
+    "spmm_max": (r"spmm_fast_kernel<\d+, \d+, \d+, false, true", r"spmm_fixup4?_kernel<true"),
     "sddmm_dot": (r"sddmm_fast_kernel<",),
     "edge_softmax": (r"softmax_kernel<", r"softmax_rowstats_kernel", r"softmax_split_kernel"),
 }
