@@ -753,6 +753,12 @@ def test_edge_cases():
                            exact=True)
         check_softmax_backward(dup, G, np.full(6, 3.0, np.float32),
                                np.arange(6, dtype=np.float32), plan=plan)
+        # fused score gradient (2 heads of 16) through duplicates and equal scores
+        xh = np.arange(96, dtype=np.float32).reshape(3, 2, 16) % 5 - 2
+        dyh = np.arange(64, dtype=np.float32).reshape(2, 2, 16) % 3 - 1
+        check_sddmm_softmax_backward(dup, G, xh, dyh, np.full((6, 2), 3.0, np.float32),
+                                     plan=None if plan is None else fg.Plan(
+                                         G, 32, 2 if plan.info()["max_backward"] else 0))
     # backward without edges: gradients all zero, softmax gradient writes nothing
     G = fg.Graph.from_csr(noedge)
     for plan in (None, fg.Plan(G, 8, 4), fg.Plan(G, 8, 4, max_backward=True)):
@@ -762,6 +768,10 @@ def test_edge_cases():
         ds = fg.edge_softmax_backward(G, dev(np.zeros(0, np.float32)),
                                       dev(np.zeros(0, np.float32)),
                                       scores=dev(np.zeros(0, np.float32)), plan=plan)
+        assert ds.numel() == 0
+        ds = fg.gsddmm_edge_softmax_backward(
+            G, dev(np.ones((5, 2, 4), np.float32)), dev(np.ones((3, 2, 4), np.float32)),
+            dev(np.zeros((0, 2), np.float32)), scores=dev(np.zeros((0, 2), np.float32)))
         assert ds.numel() == 0
 
 
