@@ -296,7 +296,8 @@ def check_softmax_backward(csr, G, scores, go, rows=None, plan=None, heads=1, le
     return ds
 
 
-def check_sddmm_softmax_backward(csr, G, x, dy, scores, plan=None, leaky=True, nnz_total=None):
+def check_sddmm_softmax_backward(csr, G, x, dy, scores, plan=None, leaky=True, nnz_total=None,
+                                 rows=None):
     """Score gradient of an attention layer in one call (per-head SDDMM of x
     and dy, then the softmax backward) vs the oracle's SDDMM followed by the
     oracle's softmax backward.  x and dy hold small integers, so the dot
@@ -313,11 +314,13 @@ def check_sddmm_softmax_backward(csr, G, x, dy, scores, plan=None, leaky=True, n
                                               slope=0.2, plan=plan)).reshape(nt, heads)
     F = heads * dh
     g_ref = O.gsddmm(csr, x.reshape(csr.num_cols, F), dy.reshape(csr.num_rows, F), heads=heads,
-                     nnz_total=nt)
+                     nnz_total=nt, rows=rows)
     ref, scale = O.edge_softmax_backward(csr, scores.reshape(nt, heads), g_ref, heads=heads,
-                                         leaky=leaky, slope=0.2, nnz_total=nt, with_scale=True)
-    e = edge_ids_of(csr, np.arange(csr.nnz))
-    n = np.repeat(csr.degrees(), csr.degrees())[:, None]
+                                         leaky=leaky, slope=0.2, nnz_total=nt, with_scale=True,
+                                         rows=rows)
+    sel = np.arange(csr.num_rows) if rows is None else rows
+    e = edge_ids_of(csr, row_edges(csr, sel))
+    n = np.repeat(csr.degrees()[sel], csr.degrees()[sel])[:, None]
     bound = 1e-5 * np.sqrt(np.maximum(n, 1)) * scale[e] + 1e-12
     err = np.abs(ds[e].astype(np.float64) - ref[e])
     bad = err > bound
@@ -1121,6 +1124,13 @@ def test_clustered_gat_backward_full():
     check_spmm(csc, Gt, x, rows=rows_t, plan=None, edge=ds, heads=H, nnz_total=csr.nnz)
     check_spmm(csr, G, x, rows=rows, plan=P, edge=ds, heads=H)
     check_sddmm(csr, G, x, gy, rows=rows, plan=P, heads=H)
+    # the score gradient in one call (fused kernel: no row of this graph is
+    # cut), with small-integer features so that the dot products are exact
+    rng = np.random.default_rng(35)
+    xi = rng.integers(-3, 4, x.shape).astype(np.float32)
+    gi = rng.integers(-3, 4, gy.shape).astype(np.float32)
+    s = (4 * rng.standard_normal((csr.nnz, H))).astype(np.float32)
+    check_sddmm_softmax_backward(csr, G, xi, gi, s, plan=P, rows=rows)
 
 
 @pytest.mark.slow
