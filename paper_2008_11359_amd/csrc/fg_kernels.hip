@@ -1095,6 +1095,7 @@ struct SoftmaxParams {
   int32_t leaky;
   float slope;
   int32_t contig;  // edge id == position, H a power of two <= 64, 16-byte aligned arrays
+  int32_t self_merge;  // contig and H == 1: the split kernel merges its row's (m, z) itself
 };
 
 __device__ __forceinline__ float leaky_relu(float s, int on, float slope) {
@@ -1548,11 +1549,31 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
   if (p.contig) {
     const ContigRange r = contig_range(s.begin, s.end, H);
     float m[4], inv[4];
+    if (p.self_merge) {
+      // one head: every wavefront of the row merges the row's segment
+      // statistics itself (lane l takes slots l, l + 64, ... in order, then a
+      // fixed butterfly; lse_merge is symmetric, so all lanes agree bitwise)
+      const Fix fx = p.fix[fi];
+      float mm = -INFINITY, zz = 0.0f;
+      for (int t = fx.slot_begin + lane; t < fx.slot_end; t += kWave)
+        lse_merge(mm, zz, p.ws[(int64_t)t * 2 + 0], p.ws[(int64_t)t * 2 + 1]);
+      for (int off = 1; off < kWave; off <<= 1) {
+        const float om = __shfl_xor(mm, off);
+        const float oz = __shfl_xor(zz, off);
+        lse_merge(mm, zz, om, oz);
+      }
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int h = contig_head(r, lane, c, H);
-      m[c] = p.ws_row[(fi * H + h) * 2 + 0];
-      inv[c] = 1.0f / p.ws_row[(fi * H + h) * 2 + 1];
+      for (int c = 0; c < 4; ++c) {
+        m[c] = mm;
+        inv[c] = 1.0f / zz;
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int h = contig_head(r, lane, c, H);
+        m[c] = p.ws_row[(fi * H + h) * 2 + 0];
+        inv[c] = 1.0f / p.ws_row[(fi * H + h) * 2 + 1];
+      }
     }
     for (int64_t k0 = lane; k0 < r.K; k0 += kStreamDepth * kWave) {
       float v[kStreamDepth][4];
@@ -3093,9 +3114,12 @@ hipError_t launch_gsddmm_softmax(const GraphView& g, const PlanView* plan, int64
   sp.leaky = lk;
   sp.slope = slope;
   sp.contig = (g.edge_ids == nullptr && aligned16(scores) && aligned16(att)) ? 1 : 0;
-  FG_LAUNCH(softmax_rowstats_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, sp);
-  err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  sp.self_merge = sp.contig;
+  if (!sp.self_merge) {
+    FG_LAUNCH(softmax_rowstats_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, sp);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
   FG_LAUNCH(softmax_split_kernel, grid_for(plan->num_slots, 1), stream, sp, plan->num_slots);
   return hipGetLastError();
 }
@@ -3121,6 +3145,7 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
   prm.slope = slope;
   prm.contig = (g.edge_ids == nullptr && H <= kWave && (H & (H - 1)) == 0 && aligned16(scores) &&
                 aligned16(out)) ? 1 : 0;
+  prm.self_merge = (prm.contig && H == 1) ? 1 : 0;
   // with a plan: empty rows (last) need no work; short single-head rows go
   // four to a wavefront
   const bool pack = plan && H == 1 && plan->num_long < plan->num_nonempty;
@@ -3142,9 +3167,11 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
     if (err != hipSuccess) return err;
   }
   if (!plan || plan->num_slots == 0) return err;
-  FG_LAUNCH(softmax_rowstats_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, prm);
-  err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  if (!prm.self_merge) {
+    FG_LAUNCH(softmax_rowstats_kernel, dim3((unsigned)plan->num_split_rows, 1, 1), stream, prm);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
   FG_LAUNCH(softmax_split_kernel, grid_for(plan->num_slots, 1), stream, prm, plan->num_slots);
   return hipGetLastError();
 }
