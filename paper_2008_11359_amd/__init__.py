@@ -513,7 +513,9 @@ def gspmm_max_backward(g: Graph, arg: torch.Tensor, grad_out: torch.Tensor,
     [num_rows, H, dh]) goes to the source of the edge each output element was
     taken from (arg, the forward's edge ids).  Returns grad_src [num_cols, ...]
     and/or grad_edge [nnz_total, H] (src_mul_edge only; needs x).  Graphs with
-    explicit edge ids need their plan."""
+    explicit edge ids need their plan.  With a plan created with
+    ``max_backward=True`` grad_src is summed per source tile in LDS after a
+    counting sort instead of with fp32 atomics."""
     if msg not in MSG_OPS:
         raise ValueError("unknown msg %r" % msg)
     grad_out = _dev_tensor(grad_out, torch.float32, "grad_out")
