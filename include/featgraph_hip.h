@@ -160,8 +160,8 @@ typedef struct fg_plan_options {
                                    gSpMM-max backward: 8 bytes per element of a
                                    num_rows x max_width gradient (that product must
                                    not exceed 2^31 - 1, else FG_ERR_UNSUPPORTED)
-                                   plus bin tables (128 KiB, and 4 KiB per source
-                                   tile, at most 32 MiB); 0 -> none (default)      */
+                                   plus bin tables (128 KiB, and 1 KiB per source
+                                   tile, at most 8 MiB); 0 -> none (default)       */
   int32_t reserved[2];          /* must be zero                                      */
 } fg_plan_options;
 

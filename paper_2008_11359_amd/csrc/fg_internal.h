@@ -73,7 +73,7 @@ hipError_t launch_gsddmm_softmax(const GraphView& g, const PlanView* plan, int64
 // kBinGroups row groups in the counting and scatter kernels.
 constexpr int kBinTileFloats = 16384;
 constexpr int kMaxBins = 8192;
-constexpr int kBinGroups = 1024;
+constexpr int kBinGroups = 256;
 
 // log2 of the source rows per tile at width F (1 <= F <= kBinTileFloats).
 inline int bin_log_rows(int64_t F) {

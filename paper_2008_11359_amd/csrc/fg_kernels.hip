@@ -1836,6 +1836,7 @@ __global__ __launch_bounds__(kBlock) void spmm_max_bwd_kernel(MaxBwdParams p) {
 
 constexpr int kBinPiece = 16384;       // records per accumulating workgroup
 constexpr int kBinBlock = 512;         // threads of an accumulating workgroup
+constexpr int kBinThreads = 1024;      // threads of a counting / scatter group
 constexpr int kBinUnroll = 4;          // elements in flight per thread
 
 struct BinParams {
@@ -1877,19 +1878,19 @@ __device__ __forceinline__ void bin_range(const BinParams& p, int64_t& first, in
 }
 
 // Records per (group, bin), counted in LDS; per bin also one global add.
-__global__ __launch_bounds__(kBlock) void bin_count_kernel(BinParams p) {
+__global__ __launch_bounds__(kBinThreads) void bin_count_kernel(BinParams p) {
   extern __shared__ int32_t bin_lds[];
   int32_t* cnt = bin_lds;  // [nb]
-  for (int b = threadIdx.x; b < p.nb; b += kBlock) cnt[b] = 0;
+  for (int b = threadIdx.x; b < p.nb; b += kBinThreads) cnt[b] = 0;
   __syncthreads();
   int64_t first;
   int32_t n;
   bin_range(p, first, n);
-  for (int32_t t0 = threadIdx.x; t0 < n; t0 += kBlock * kBinUnroll) {
+  for (int32_t t0 = threadIdx.x; t0 < n; t0 += kBinThreads * kBinUnroll) {
     int32_t e[kBinUnroll];
 #pragma unroll
     for (int k = 0; k < kBinUnroll; ++k) {
-      const int32_t t = t0 + k * kBlock;
+      const int32_t t = t0 + k * kBinThreads;
       e[k] = t < n ? p.arg[first + t] : -1;
     }
     int32_t u[kBinUnroll];
@@ -1901,7 +1902,7 @@ __global__ __launch_bounds__(kBlock) void bin_count_kernel(BinParams p) {
   }
   __syncthreads();
   int32_t* mine = p.runs + (int64_t)blockIdx.x * p.nb;
-  for (int b = threadIdx.x; b < p.nb; b += kBlock) {
+  for (int b = threadIdx.x; b < p.nb; b += kBinThreads) {
     const int32_t c = cnt[b];
     mine[b] = c;
     if (c) atomicAdd(&p.total[b], c);
@@ -1951,7 +1952,7 @@ __global__ __launch_bounds__(kBinScanThreads) void bin_scan_kernel(BinParams p) 
 // Zeroes the rows of every split bin (their pieces add with atomics), then
 // reserves this group's run in each bin it feeds and writes each element's
 // record into it, ranked inside the run through LDS.
-__global__ __launch_bounds__(kBlock) void bin_scatter_kernel(BinParams p) {
+__global__ __launch_bounds__(kBinThreads) void bin_scatter_kernel(BinParams p) {
   extern __shared__ int32_t bin_lds[];
   int32_t* cnt = bin_lds;          // [nb]
   int32_t* run = bin_lds + p.nb;   // [nb]
@@ -1960,10 +1961,10 @@ __global__ __launch_bounds__(kBlock) void bin_scatter_kernel(BinParams p) {
     if (p.piece[b + 1] - p.piece[b] == 1) continue;
     const int64_t lo = (int64_t)b * tile;
     const int64_t hi = min(p.num_cols * p.F, lo + tile);
-    for (int64_t t = lo + threadIdx.x; t < hi; t += kBlock) p.gsrc[t] = 0.0f;
+    for (int64_t t = lo + threadIdx.x; t < hi; t += kBinThreads) p.gsrc[t] = 0.0f;
   }
   const int32_t* mine = p.runs + (int64_t)blockIdx.x * p.nb;
-  for (int b = threadIdx.x; b < p.nb; b += kBlock) {
+  for (int b = threadIdx.x; b < p.nb; b += kBinThreads) {
     const int32_t c = mine[b];
     cnt[b] = 0;
     run[b] = c ? atomicAdd(&p.cursor[b], c) : 0;
@@ -1972,12 +1973,12 @@ __global__ __launch_bounds__(kBlock) void bin_scatter_kernel(BinParams p) {
   int64_t first;
   int32_t n;
   bin_range(p, first, n);
-  for (int32_t t0 = threadIdx.x; t0 < n; t0 += kBlock * kBinUnroll) {
+  for (int32_t t0 = threadIdx.x; t0 < n; t0 += kBinThreads * kBinUnroll) {
     int32_t e[kBinUnroll];
     float g[kBinUnroll];
 #pragma unroll
     for (int k = 0; k < kBinUnroll; ++k) {
-      const int32_t t = t0 + k * kBlock;
+      const int32_t t = t0 + k * kBinThreads;
       e[k] = -1;
       g[k] = 0.0f;
       if (t < n) {
@@ -1991,7 +1992,7 @@ __global__ __launch_bounds__(kBlock) void bin_scatter_kernel(BinParams p) {
 #pragma unroll
     for (int k = 0; k < kBinUnroll; ++k) {
       if (u[k] < 0) continue;
-      const int32_t t = t0 + k * kBlock;
+      const int32_t t = t0 + k * kBinThreads;
       const int32_t b = u[k] >> p.logR;
       const int32_t r = atomicAdd(&cnt[b], 1);
       const int32_t f = t % p.F;
@@ -3316,11 +3317,11 @@ hipError_t launch_gspmm_max_backward(const GraphView& g, const int32_t* eid_pos,
     bp.rows_per_group = (int32_t)((g.num_rows + kBinGroups - 1) / kBinGroups);
     const int32_t groups = (int32_t)((g.num_rows + bp.rows_per_group - 1) / bp.rows_per_group);
     FG_LAUNCH(fill_i32_kernel, stride_grid(nb), stream, bp.total, (int64_t)nb, 0);
-    hipLaunchKernelGGL(bin_count_kernel, dim3((unsigned)groups), dim3(kBlock), (size_t)nb * 4,
-                       stream, bp);
+    hipLaunchKernelGGL(bin_count_kernel, dim3((unsigned)groups), dim3(kBinThreads),
+                       (size_t)nb * 4, stream, bp);
     hipLaunchKernelGGL(bin_scan_kernel, dim3(1), dim3(kBinScanThreads), 0, stream, bp);
-    hipLaunchKernelGGL(bin_scatter_kernel, dim3((unsigned)groups), dim3(kBlock), (size_t)nb * 8,
-                       stream, bp);
+    hipLaunchKernelGGL(bin_scatter_kernel, dim3((unsigned)groups), dim3(kBinThreads),
+                       (size_t)nb * 8, stream, bp);
     const int64_t pieces = nb + (g.num_rows * F + kBinPiece - 1) / kBinPiece;
     hipLaunchKernelGGL(bin_accumulate_kernel, dim3((unsigned)pieces), dim3(kBinBlock), 0, stream,
                        bp);
