@@ -95,6 +95,21 @@ def _row_sample(csr, edges_target, seed):
     return rows, int(deg[rows].sum())
 
 
+def simple_graph(csr):
+    """One edge of every (destination, source) pair of a CSR sorted by (dst,
+    src), where repeats follow their first copy.  Returns the new CSR and the
+    mask of the kept positions."""
+    import synth
+
+    rows = np.repeat(np.arange(csr.num_rows), np.diff(csr.indptr.astype(np.int64)))
+    keep = np.ones(csr.nnz, bool)
+    keep[1:] = (csr.indices[1:] != csr.indices[:-1]) | (rows[1:] != rows[:-1])
+    ip = np.zeros(csr.num_rows + 1, np.int64)
+    np.cumsum(np.bincount(rows[keep], minlength=csr.num_rows), out=ip[1:])
+    return synth.CSR(csr.num_rows, csr.num_cols, ip.astype(np.int32),
+                     np.ascontiguousarray(csr.indices[keep])), keep
+
+
 def setup(name, d, args, fg, torch, dev):
     import synth
 
@@ -105,17 +120,9 @@ def setup(name, d, args, fg, torch, dev):
     t_gen = time.perf_counter() - t0
     csr = wl.csr
     if args.simple_graph:
-        # keep one edge of every (destination, source) pair: the CSR is sorted
-        # by (dst, src), so repeats follow their first copy
         if base != "rmat_233k_115m":
             raise SystemExit("--simple-graph applies to the power-law graph workloads")
-        rows = np.repeat(np.arange(csr.num_rows), np.diff(csr.indptr.astype(np.int64)))
-        keep = np.ones(csr.nnz, bool)
-        keep[1:] = (csr.indices[1:] != csr.indices[:-1]) | (rows[1:] != rows[:-1])
-        ip = np.zeros(csr.num_rows + 1, np.int64)
-        np.cumsum(np.bincount(rows[keep], minlength=csr.num_rows), out=ip[1:])
-        csr = synth.CSR(csr.num_rows, csr.num_cols, ip.astype(np.int32),
-                        np.ascontiguousarray(csr.indices[keep]))
+        csr, keep = simple_graph(csr)
         if "w" in wl.arrays:
             wl.arrays["w"] = np.ascontiguousarray(wl.arrays["w"][keep])
     n, e = csr.num_rows, csr.nnz

@@ -77,3 +77,25 @@ def test_cpu_baseline_record(bench):
     assert rec["value"] == pytest.approx(1e8 / 0.05 / 1e9)
     assert calls[0] == 200_000 and calls[1] == 2_000_000 and len(calls) >= 6
     assert "passes" in rec["sample"] and rec["host"]["logical_cpus"] == os.cpu_count()
+
+
+def test_simple_graph_keeps_one_edge_per_pair(bench):
+    """--simple-graph: every (destination, source) pair once, first copies
+    kept, rows and their order otherwise unchanged."""
+    rng = np.random.default_rng(3)
+    dst = rng.integers(0, 50, 3000)
+    src = rng.integers(0, 20, 3000)
+    csr = synth.coo_to_csr(dst, src, 60, 20)
+    simple, keep = bench.simple_graph(csr)
+    synth.check_csr(simple)
+    rows = synth.csr_rows(csr)
+    pairs = set(zip(rows.tolist(), csr.indices.tolist()))
+    srows = synth.csr_rows(simple)
+    spairs = list(zip(srows.tolist(), simple.indices.tolist()))
+    assert len(spairs) == len(set(spairs)) == len(pairs) and set(spairs) == pairs
+    # the kept positions are the first copy of each pair, in storage order
+    first = {}
+    for q, pr in enumerate(zip(rows.tolist(), csr.indices.tolist())):
+        first.setdefault(pr, q)
+    assert np.array_equal(np.nonzero(keep)[0], np.array(sorted(first.values())))
+    assert simple.num_rows == csr.num_rows and simple.num_cols == csr.num_cols
