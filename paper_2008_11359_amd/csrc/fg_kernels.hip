@@ -836,23 +836,20 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
       my_src = __builtin_nontemporal_load(p.indices + base + lane);
       my_eid = p.eids ? __builtin_nontemporal_load(p.eids + base + lane) : (int)(base + lane);
     }
-    // wide rows (one or two lane groups): lane j collects the dot product of
-    // edge base + j, so the batch's results leave in one store instead of one
-    // one- or two-lane store per step, which would cost the address unit as
-    // much as the gathers; narrow rows (four or more groups) finish enough
-    // edges per step for a direct store, and collecting would cost more VALU
-    constexpr bool COLLECT = NG <= 2;
+    // lane j collects the dot product of edge base + j, so the batch's
+    // results leave in one store instead of one store per step with one lane
+    // per group active, which would cost the address unit as much as a
+    // gather: one or two groups hand their sums over with scalar readlanes,
+    // more groups with one cross-lane permute per step
     float res = 0.0f;
     for (int j0 = 0; j0 < cnt; j0 += NG * U) {
       float val[U][NV][4];
-      int32_t eu[U];
       bool ok[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
         ok[u] = jb + gid < cnt;
         const int src = bcast_lane<NG>(my_src, jb, gid);
-        eu[u] = COLLECT ? 0 : bcast_lane<NG>(my_eid, jb, gid);
         const float* xr = p.xs + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
@@ -873,10 +870,10 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
           for (int c = 0; c < 4; ++c) part += val[u][v][c] * xd[v][c];
         part = group_sum<G>(part);
         const int jb = j0 + u * NG;
-        if constexpr (COLLECT) {
+        // the last lane of group g holds the sum of edge jb + g
+        if constexpr (NG <= 2) {
 #pragma unroll
           for (int g = 0; g < NG; ++g) {
-            // the last lane of group g holds the sum of edge jb + g
             if (jb + g < cnt) {
               const int sum =
                   __builtin_amdgcn_readlane(__builtin_bit_cast(int, part), (g + 1) * G - 1);
@@ -884,11 +881,14 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
             }
           }
         } else {
-          if (ok[u] && li == G - 1) p.out[eu[u]] = part;
+          const int rel = lane - jb;
+          const bool mine = rel >= 0 && rel < NG && lane < cnt;
+          const float got = __shfl(part, mine ? rel * G + (G - 1) : lane);
+          if (mine) res = got;
         }
       }
     }
-    if (COLLECT && lane < cnt) p.out[my_eid] = res;
+    if (lane < cnt) p.out[my_eid] = res;
   }
 }
 
