@@ -30,10 +30,12 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "_build", "libfeatgraph_hip.so")
 
 FG_OK, FG_ERR_INVALID_ARG, FG_ERR_UNSUPPORTED, FG_ERR_HIP, FG_ERR_NO_MEMORY = 0, -1, -2, -3, -4
+FG_ERR_SCRATCH_LIMIT = -5
+NOALLOC_SCRATCH_BYTES = 32 << 20  # fixed scratch of gspmm_noalloc (per device)
 MSG_OPS = {"copy_src": 0, "src_mul_edge": 1}
 REDUCE_OPS = {"sum": 0, "max": 1}
 EDGE_OPS = {"dot": 0}
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 
 class FgError(RuntimeError):
@@ -112,6 +114,9 @@ def _load():
     lib.fg_plan_get_info.argtypes = [vp, ctypes.POINTER(_PlanInfo)]
     lib.fg_gspmm.restype = ctypes.c_int
     lib.fg_gspmm.argtypes = [gp, ctypes.c_int, ctypes.c_int, i32, i64, vp, vp, vp, vp, vp, vp]
+    lib.fg_gspmm_noalloc.restype = ctypes.c_int
+    lib.fg_gspmm_noalloc.argtypes = [gp, ctypes.c_int, ctypes.c_int, i32, i64, vp, vp, vp, vp, vp,
+                                     vp]
     lib.fg_gsddmm.restype = ctypes.c_int
     lib.fg_gsddmm.argtypes = [gp, ctypes.c_int, i32, i64, vp, vp, vp, vp, vp]
     lib.fg_gat_aggregate.restype = ctypes.c_int
@@ -385,6 +390,53 @@ def gspmm(g: Graph, x: torch.Tensor, edge: Optional[torch.Tensor] = None, msg: s
     st = _lib.fg_gspmm(ctypes.byref(g._c), MSG_OPS[msg], REDUCE_OPS[reduce], heads, dh,
                        _ptr(x), _ptr(edge), _ptr(out), _ptr(arg), _plan_handle(plan), _stream())
     _check(st, "fg_gspmm")
+    return (out, arg) if reduce == "max" else out
+
+
+def gspmm_noalloc(g: Graph, x: torch.Tensor, out: torch.Tensor,
+                  arg: Optional[torch.Tensor] = None, edge: Optional[torch.Tensor] = None,
+                  msg: str = "copy_src", reduce: str = "sum", heads: int = 1,
+                  plan: Optional[Plan] = None):
+    """gspmm through fg_gspmm_noalloc: nothing is allocated, neither by the
+    library (split-row partials go to its fixed per-device scratch of
+    NOALLOC_SCRATCH_BYTES) nor here, so the caller passes ``out`` (and
+    ``arg`` for reduce='max').  Same results as gspmm with the same plan.
+    Raises FgError (status FG_ERR_SCRATCH_LIMIT) when the plan's partials do
+    not fit the scratch.  Calls on one device share the scratch: order them
+    on one stream."""
+    if msg not in MSG_OPS or reduce not in REDUCE_OPS:
+        raise ValueError("unknown msg %r or reduce %r" % (msg, reduce))
+    x = _dev_tensor(x, torch.float32, "x")
+    if x.shape[0] != g.num_cols:
+        raise ValueError("x must have num_cols rows")
+    F = int(np.prod(x.shape[1:])) if x.dim() > 1 else 1
+    if x.dim() == 3:
+        heads = int(x.shape[1])
+    if F % heads:
+        raise ValueError("feature width not divisible by heads")
+    if msg == "src_mul_edge":
+        if edge is None:
+            raise ValueError("src_mul_edge needs edge values")
+        edge = _dev_tensor(edge, torch.float32, "edge")
+        if edge.numel() != g.nnz_total * heads:
+            raise ValueError("edge must have nnz_total * heads values")
+    elif edge is not None:
+        raise ValueError("copy_src takes no edge values")
+    out = _dev_tensor(out, torch.float32, "out")
+    if out.numel() != g.num_rows * F:
+        raise ValueError("out has the wrong size")
+    if reduce == "max":
+        if arg is None:
+            raise ValueError("reduce='max' needs arg (nothing is allocated here)")
+        arg = _dev_tensor(arg, torch.int32, "arg")
+        if arg.numel() != g.num_rows * F:
+            raise ValueError("arg has the wrong size")
+    elif arg is not None:
+        raise ValueError("arg is only written for reduce='max'")
+    st = _lib.fg_gspmm_noalloc(ctypes.byref(g._c), MSG_OPS[msg], REDUCE_OPS[reduce], heads,
+                               F // heads, _ptr(x), _ptr(edge), _ptr(out), _ptr(arg),
+                               _plan_handle(plan), _stream())
+    _check(st, "fg_gspmm_noalloc")
     return (out, arg) if reduce == "max" else out
 
 

@@ -35,6 +35,9 @@ struct fg_plan {
   int64_t workspace_bytes = 0;
 };
 
+static_assert(fg::kNoAllocScratchBytes == FG_NOALLOC_SCRATCH_BYTES,
+              "the fixed scratch size is part of the ABI");
+
 namespace {
 
 constexpr int32_t kDefaultSegmentEdges = 4096;
@@ -539,6 +542,8 @@ const char* fg_status_string(fg_status s) {
     case FG_ERR_UNSUPPORTED: return "unsupported combination";
     case FG_ERR_HIP: return "HIP runtime error";
     case FG_ERR_NO_MEMORY: return "out of memory";
+    case FG_ERR_SCRATCH_LIMIT:
+      return "the split-row partials exceed the fixed scratch of the allocation-free entry point";
   }
   return "unknown status";
 }
@@ -841,9 +846,14 @@ fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info) {
   return FG_OK;
 }
 
-fg_status fg_gspmm(const fg_graph* g, fg_msg_op msg, fg_reduce_op red, int32_t num_heads,
-                   int64_t head_dim, const float* x_src, const float* edge_val, float* out,
-                   int32_t* arg_eid, fg_plan* plan, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Host-side checks shared by fg_gspmm and fg_gspmm_noalloc.
+fg_status check_gspmm(const fg_graph* g, fg_msg_op msg, fg_reduce_op red, int32_t num_heads,
+                      int64_t head_dim, const float* x_src, const float* edge_val,
+                      const float* out, const int32_t* arg_eid, const fg_plan* plan) {
   fg_status st = check_graph(g);
   if (st != FG_OK) return st;
   if ((st = check_width(num_heads, head_dim)) != FG_OK) return st;
@@ -863,10 +873,53 @@ fg_status fg_gspmm(const fg_graph* g, fg_msg_op msg, fg_reduce_op red, int32_t n
       overlaps(arg_eid, out_b, x_src, x_b) || overlaps(arg_eid, out_b, edge_val, ev_b) ||
       overlaps(out, out_b, arg_eid, out_b))
     return FG_ERR_INVALID_ARG;
+  return FG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+fg_status fg_gspmm(const fg_graph* g, fg_msg_op msg, fg_reduce_op red, int32_t num_heads,
+                   int64_t head_dim, const float* x_src, const float* edge_val, float* out,
+                   int32_t* arg_eid, fg_plan* plan, void* stream) {
+  const fg_status st =
+      check_gspmm(g, msg, red, num_heads, head_dim, x_src, edge_val, out, arg_eid, plan);
+  if (st != FG_OK) return st;
   const fg::GraphView gv = view_of(g);
   return from_hip(fg::launch_gspmm(gv, plan ? &plan->gather : nullptr, (int)msg, (int)red,
                                    num_heads, head_dim, x_src, edge_val, out, arg_eid,
                                    static_cast<hipStream_t>(stream)));
+}
+
+fg_status fg_gspmm_noalloc(const fg_graph* g, fg_msg_op msg, fg_reduce_op red, int32_t num_heads,
+                           int64_t head_dim, const float* x_src, const float* edge_val,
+                           float* out, int32_t* arg_eid, fg_plan* plan, void* stream) {
+  fg_status st =
+      check_gspmm(g, msg, red, num_heads, head_dim, x_src, edge_val, out, arg_eid, plan);
+  if (st != FG_OK) return st;
+  void* base = nullptr;  // this device's copy of the fixed scratch
+  if (fg::noalloc_scratch(&base) != hipSuccess) return FG_ERR_HIP;
+  const int64_t F = (int64_t)num_heads * head_dim;
+  const bool mx = red == FG_REDUCE_MAX;
+  const fg::GraphView gv = view_of(g);
+  if (!plan || plan->gather.num_split_rows == 0)  // no partial results to keep
+    return from_hip(fg::launch_gspmm(gv, plan ? &plan->gather : nullptr, (int)msg, (int)red,
+                                     num_heads, head_dim, x_src, edge_val, out, arg_eid,
+                                     static_cast<hipStream_t>(stream)));
+  const int64_t slots = plan->gather.num_slots;
+  if (fg::noalloc_bytes(slots, F, mx) > fg::kNoAllocScratchBytes) return FG_ERR_SCRATCH_LIMIT;
+  // the plan's schedule with the fixed scratch in place of its workspace;
+  // every slot is written before the merge reads it, so nothing is cleared
+  fg::PlanView v = plan->gather;
+  v.ws_f = static_cast<float*>(base);
+  v.ws_i = mx ? reinterpret_cast<int32_t*>(static_cast<char*>(base) +
+                                           fg::noalloc_ids_offset(slots, F))
+              : nullptr;
+  v.ws_row = nullptr;
+  v.ws_width = F;
+  return from_hip(fg::launch_gspmm(gv, &v, (int)msg, (int)red, num_heads, head_dim, x_src,
+                                   edge_val, out, arg_eid, static_cast<hipStream_t>(stream)));
 }
 
 fg_status fg_gsddmm(const fg_graph* g, fg_edge_op op, int32_t num_heads, int64_t head_dim,

@@ -137,6 +137,26 @@ hipError_t launch_mlp_aggregate(const GraphView& g, const PlanView* plan, int64_
                                 int64_t d_out, const float* xs, const float* xd, const float* w,
                                 float* out, int32_t* arg, float* ws, hipStream_t stream);
 
+// Fixed device scratch of the allocation-free gSpMM (fg_gspmm_noalloc): a
+// file-scope device array of this many bytes in fg_kernels.hip.  It holds
+// the split-row partial values and, for max, their edge ids.
+constexpr int64_t kNoAllocScratchBytes = int64_t(32) << 20;
+
+// Byte offset of the edge-id partials in the scratch (after the values,
+// rounded up to 256 bytes) and the bytes a schedule with `slots` partial
+// slots of F floats needs.
+inline int64_t noalloc_ids_offset(int64_t slots, int64_t F) {
+  return (slots * F * 4 + 255) / 256 * 256;
+}
+inline int64_t noalloc_bytes(int64_t slots, int64_t F, bool with_ids) {
+  return with_ids ? noalloc_ids_offset(slots, F) + slots * F * 4 : slots * F * 4;
+}
+
+// Device address of that array on the current device.  The first call on a
+// device looks it up with hipGetSymbolAddress (once per device, under a
+// lock); later calls return the kept address.
+hipError_t noalloc_scratch(void** ptr);
+
 // Fused SDDMM -> leaky ReLU -> edge softmax -> weighted gSpMM.  Supported
 // shapes: dh % 4 == 0, dh / 4 a power of two, H * dh <= 256; aligned inputs.
 bool gat_fused_supported(int64_t H, int64_t dh);

@@ -21,6 +21,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "fg_internal.h"
 
@@ -3379,6 +3380,40 @@ hipError_t launch_edge_softmax_backward(const GraphView& g, const PlanView* plan
   if (err != hipSuccess || !plan || plan->num_slots == 0) return err;
   FG_LAUNCH(softmax_bwd_split_kernel, grid_for(plan->num_slots, 1), stream, prm, plan->num_slots);
   return hipGetLastError();
+}
+
+}  // namespace fg
+
+// Scratch of fg_gspmm_noalloc, for callers that cannot allocate device
+// memory: the split-row partial values (and argmax edge ids) of one call.
+// Every device holds its own copy from the library's load until the process
+// ends; calls on one device share it, so calls that overlap in time on one
+// device race.  Host code never passes this name to a kernel: on the host it
+// is a stand-in, and the device address comes from noalloc_scratch().
+static __device__ __align__(256) unsigned char scratch[fg::kNoAllocScratchBytes];
+
+namespace fg {
+namespace {
+constexpr int kScratchDevices = 256;
+std::mutex scratch_mu;
+void* scratch_addr[kScratchDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    scratch_addr[dev] = p;
+  }
+  *ptr = scratch_addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace fg

@@ -36,8 +36,8 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert fg._lib.fg_abi_version() == fg.ABI_VERSION == 3
-    for s in (0, -1, -2, -3, -4):
+    assert fg._lib.fg_abi_version() == fg.ABI_VERSION == 4
+    for s in (0, -1, -2, -3, -4, -5):
         assert fg.status_string(s) and fg.status_string(s) != "unknown status"
     assert fg.status_string(7) == "unknown status"
 
@@ -54,7 +54,10 @@ FAKE_X, FAKE_OUT, FAKE_ARG, FAKE_EV = 0x10000, 0x20000, 0x30000, 0x40000
     "null_graph", "neg_rows", "huge_nnz", "no_indptr", "zero_heads", "zero_dh", "too_wide",
     "bad_msg", "bad_red", "mul_without_edge", "copy_with_edge", "max_without_arg",
     "sum_with_arg", "no_x", "no_out", "out_aliases_x", "nnz_total_too_small"])
-def test_gspmm_rejects_invalid_arguments(case):
+@pytest.mark.parametrize("entry", ["fg_gspmm", "fg_gspmm_noalloc"])
+def test_gspmm_rejects_invalid_arguments(case, entry):
+    """Both gSpMM entry points share their host checks; the allocation-free
+    one must reject before it touches the device (there is none here)."""
     L = fg._lib
     g = _graph_struct()
     args = dict(msg=0, red=0, H=1, dh=4, x=FAKE_X, ev=None, out=FAKE_OUT, arg=None)
@@ -93,8 +96,8 @@ def test_gspmm_rejects_invalid_arguments(case):
         args["out"] = FAKE_X + 8
     elif case == "nnz_total_too_small":
         g.nnz_total = 3
-    st = L.fg_gspmm(gp, args["msg"], args["red"], args["H"], args["dh"], args["x"], args["ev"],
-                    args["out"], args["arg"], None, None)
+    st = getattr(L, entry)(gp, args["msg"], args["red"], args["H"], args["dh"], args["x"],
+                           args["ev"], args["out"], args["arg"], None, None)
     assert st == fg.FG_ERR_INVALID_ARG
 
 
