@@ -61,7 +61,10 @@ static int check_rows(const int64_t* rows, int64_t num_sel, int64_t num_rows) {
  * sum : out[v,h,k] = (float) sum_p (double) m            (empty row -> 0)
  * max : out[v,h,k] = max_p m, arg[v,h,k] = the smallest edge id attaining it;
  *       empty row -> out 0, arg -1.  Equality is IEEE equality, so -0 == +0
- *       and the edge id decides between them.
+ *       and the edge id decides between them.  A NaN message takes part as
+ *       -inf (the paper leaves NaN undefined; this is the library's reading),
+ *       so it never beats a number and a row of NaN / -inf messages gives
+ *       -inf with its smallest edge id.
  *
  * Output i (0 <= i < num_sel) is row pick_row(rows, i); with rows == NULL all
  * num_rows rows are computed (num_sel must then equal num_rows).
@@ -99,6 +102,7 @@ FGREF_EXPORT int fgref_gspmm(int64_t num_rows, int64_t num_cols, const int32_t* 
           if (u < 0 || u >= num_cols || e < 0 || e >= nnz_total) { bad |= 1; continue; }
           float m = x[u * F + f];
           if (msg == MSG_SRC_MUL_EDGE) m = edge_val[e * H + h] * m;
+          if (red == RED_MAX && isnan(m)) m = -INFINITY;
           if (red == RED_SUM) {
             acc += (double)m;
             sq += (double)m * (double)m;
@@ -437,6 +441,28 @@ FGREF_EXPORT int fgref_mlp_aggregate(int64_t num_rows, int64_t num_cols, const i
     }
   }
   return bad ? -2 : 0;
+}
+
+/*
+ * Dense vertex transform of MLP aggregation (the vector-matrix product inside
+ * the message function of Fig. 3b, applied to every vertex's features):
+ *   Y[i, j] = sum_k X[i, k] * W[k, j]
+ * with X [n, d_in] and W [d_in, d_out] row-major fp32, Y [n, d_out] fp64 (the
+ * products and their sum in fp64, k in increasing order, no rounding to fp32).
+ */
+FGREF_EXPORT int fgref_dense_matmul(int64_t n, int64_t d_in, int64_t d_out, const float* x,
+                                    const float* w, double* y, int num_threads) {
+  if (n < 0 || d_in < 1 || d_out < 1 || (n > 0 && (!x || !w || !y))) return -1;
+  set_threads(num_threads);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    for (int64_t j = 0; j < d_out; ++j) {
+      double acc = 0.0;
+      for (int64_t k = 0; k < d_in; ++k) acc += (double)x[i * d_in + k] * (double)w[k * d_out + j];
+      y[i * d_out + j] = acc;
+    }
+  }
+  return 0;
 }
 
 FGREF_EXPORT int fgref_max_threads(void) { return omp_get_max_threads(); }

@@ -75,6 +75,8 @@ def _load():
     lib.fgref_mlp_aggregate.argtypes = [i64, i64, vp, vp, vp, i64, i64, i64, vp, vp, vp, vp, i64,
                                         vp, vp, vp, ctypes.c_int]
     lib.fgref_mlp_aggregate.restype = ctypes.c_int
+    lib.fgref_dense_matmul.argtypes = [i64, i64, i64, vp, vp, vp, ctypes.c_int]
+    lib.fgref_dense_matmul.restype = ctypes.c_int
     lib.fgref_set_num_threads.argtypes = [ctypes.c_int]
     lib.fgref_set_num_threads.restype = None
     del i32p
@@ -276,6 +278,18 @@ def mlp_aggregate(g, xs: np.ndarray, xd: np.ndarray, w: np.ndarray,
     return (out, arg, sc) if with_scale else (out, arg)
 
 
-def dense_matmul(x: np.ndarray, w: np.ndarray) -> np.ndarray:
-    """Y = X W in fp64 (numpy's matmul): the dense vertex transform."""
-    return np.asarray(x, np.float64) @ np.asarray(w, np.float64)
+def dense_matmul(x: np.ndarray, w: np.ndarray, threads: int = 0) -> np.ndarray:
+    """Y = X W, the dense vertex transform of MLP aggregation (Fig. 3b's
+    vector-matrix product applied per vertex): fp32 inputs, fp64 products,
+    sums and result (fgref_dense_matmul)."""
+    lib = _load()
+    w = _c(w, np.float32)
+    if w.ndim != 2:
+        raise ValueError("w must be [d_in, d_out]")
+    d_in, d_out = w.shape
+    x = _c(x, np.float32).reshape(-1, d_in)
+    y = np.empty((x.shape[0], d_out), np.float64)
+    rc = lib.fgref_dense_matmul(x.shape[0], d_in, d_out, _ptr(x), _ptr(w), _ptr(y), threads)
+    if rc != 0:
+        raise ValueError("fgref_dense_matmul failed (%d)" % rc)
+    return y

@@ -54,6 +54,10 @@ MUTANTS = [
     ("mlp_relu_dropped", "const double m = t > 0.0 ? t : 0.0;", "const double m = t;"),
     ("mlp_tie_to_largest_id", "(m == best && e < best_e)) {\n          best = m;\n          best_e = (int32_t)e;\n          best_scale",
      "(m == best && e > best_e)) {\n          best = m;\n          best_e = (int32_t)e;\n          best_scale"),
+    ("dense_matmul_weight_transposed", "(double)w[k * d_out + j]", "(double)w[j * d_in + k]"),
+    ("dense_matmul_last_term_dropped", "for (int64_t k = 0; k < d_in; ++k) acc +=",
+     "for (int64_t k = 0; k < d_in - 1; ++k) acc +="),
+    ("max_nan_not_minus_inf", "if (red == RED_MAX && isnan(m)) m = -INFINITY;", ""),
     ("softmax_off_normaliser", "out[e * H + h] = (float)(exp(s - m) / z);", "out[e * H + h] = (float)(exp(s - m) / (z + 1e-3));"),
 ]
 

@@ -637,3 +637,61 @@ def test_mlp_aggregate_homogeneous_and_threads(O):
     o3, a3 = O.mlp_aggregate(g, x, x[: g.num_rows], w, rows=rows)
     np.testing.assert_array_equal(o3, o1[rows])
     np.testing.assert_array_equal(a3, a1[rows])
+
+
+# ---------------------------------------------------------------- dense transform
+
+
+def test_golden_dense_matmul(O):
+    """Hand-worked product with a square, non-symmetric W (a transposed W is
+    a different, also hand-worked, result)."""
+    gd = json.load(open(os.path.join(GOLDEN, "dense_matmul_2x3x3.json")))
+    x, w = np.array(gd["x"], np.float32), np.array(gd["w"], np.float32)
+    y = O.dense_matmul(x, w)
+    assert y.dtype == np.float64 and y.shape == (2, 3)
+    np.testing.assert_array_equal(y, np.array(gd["y"]))
+    assert not np.array_equal(y, np.array(gd["y_with_w_transposed"]))
+
+
+def test_dense_matmul_against_library_and_special_cases(O):
+    rng = np.random.default_rng(97)
+    x = rng.standard_normal((37, 8)).astype(np.float32)
+    w = rng.standard_normal((8, 13)).astype(np.float32)
+    y = O.dense_matmul(x, w, threads=3)
+    # a library product of the same fp32 inputs in fp64 (fp32 x fp32 products
+    # are exact in fp64, so only the order of 8 additions may differ)
+    np.testing.assert_allclose(y, x.astype(np.float64) @ w.astype(np.float64), rtol=1e-14,
+                               atol=1e-14)
+    np.testing.assert_array_equal(O.dense_matmul(x, np.eye(8, dtype=np.float32)), x)
+    # a one-hot weight column picks one input column
+    e3 = np.zeros((8, 1), np.float32)
+    e3[3, 0] = 1.0
+    np.testing.assert_array_equal(O.dense_matmul(x, e3)[:, 0], x[:, 3])
+    # linearity in x: rows are independent
+    np.testing.assert_array_equal(O.dense_matmul(x[5:9], w), y[5:9])
+    assert O.dense_matmul(np.zeros((0, 8), np.float32), w).shape == (0, 13)
+
+
+# ---------------------------------------------------------------- NaN in max
+
+
+def test_max_nan_message_counts_as_minus_inf(O):
+    """The library's reading for NaN messages (the paper defines none): a NaN
+    competes as -inf, so it never beats a number, and a row of NaN / -inf
+    messages reports -inf with its smallest edge id.  Worked by hand."""
+    nan, inf = np.float32(np.nan), np.float32(np.inf)
+    x = np.array([[nan], [5.0], [-inf]], np.float32)
+    # row 0: NaN, 5 | row 1: NaN, NaN | row 2: NaN, -inf | row 3: -inf, NaN
+    g = CSR(4, 3, np.array([0, 2, 4, 6, 8], np.int32),
+            np.array([0, 1, 0, 0, 0, 2, 2, 0], np.int32))
+    out, arg = O.gspmm(g, x, red=O.RED_MAX)
+    np.testing.assert_array_equal(out[:, 0], [5.0, -inf, -inf, -inf])
+    np.testing.assert_array_equal(arg[:, 0], [1, 2, 4, 6])
+    # a weighted message 0 * inf is NaN as well
+    xw = np.array([[inf], [1.0], [-2.0]], np.float32)
+    w = np.array([0.0, 1.0, 0.0, 3.0, 1.0, 1.0, 1.0, 1.0], np.float32)
+    out, arg = O.gspmm(g, xw, msg=O.MSG_SRC_MUL_EDGE, edge_val=w, red=O.RED_MAX)
+    # row 0: NaN, 1 -> 1 (e1) | row 1: NaN, 3*inf -> inf (e3) | row 2: inf, -2 -> inf (e4)
+    # row 3: -2, inf -> inf (e7)
+    np.testing.assert_array_equal(out[:, 0], [1.0, inf, inf, inf])
+    np.testing.assert_array_equal(arg[:, 0], [1, 3, 4, 7])
