@@ -227,7 +227,9 @@ fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info);
  * plan     NULL -> one wavefront per row (no load balancing); else a plan of
  *          this graph with max_width >= H*dh
  * Sums are fp32 in an order that depends on the schedule (deterministic for a
- * given plan).  Max/argmax is exact and schedule-independent.
+ * given plan).  Max/argmax is exact and schedule-independent.  A NaN message
+ * competes as -inf: it never beats a number, and a row whose messages are all
+ * NaN or -inf gives -inf with its smallest edge id.
  * ------------------------------------------------------------------------- */
 fg_status fg_gspmm(const fg_graph* g, fg_msg_op msg, fg_reduce_op red, int32_t num_heads,
                    int64_t head_dim, const float* x_src, const float* edge_val, float* out,
@@ -422,12 +424,18 @@ fg_status fg_dense_matmul(int64_t n, int64_t d_in, int64_t d_out, const float* x
  * aggregator:
  *   out[v, i]     = max over stored edges (u -> v, id e) of
  *                   relu( sum_k (x_src[u, k] + x_dst[v, k]) * weight[k, i] )
- *   arg_eid[v, i] = the smallest edge id attaining it;  empty row -> 0 / -1
+ *   arg_eid[v, i] = the edge that supplies it;  empty row -> 0 / -1
  * where relu(t) = t > 0 ? t : 0.  Computed as P_src = x_src weight and
  * P_dst = x_dst weight (fg_dense_matmul) followed by a gSpMM whose message is
  * relu(P_src[u] + P_dst[v]): equal to the per-edge form in exact arithmetic
  * (the product distributes over the sum), without d_in * d_out multiply-adds
- * per edge.  Rounding differs from the per-edge form, and so may the argmax
+ * per edge.  The edges compete by their fp32 P_src[u, i]: arg_eid is the
+ * smallest edge id among the edges with the largest P_src[u, i], and out is
+ * relu(that P_src + P_dst[v, i]) rounded once (fp32 rounding is monotone, so
+ * this is the largest rounded message); when that is not positive every
+ * message is 0 and arg_eid is the row's smallest edge id.  Every schedule,
+ * width and edge-id layout follows this rule, so results do not depend on
+ * the plan.  Rounding differs from the per-edge form, and so may the argmax
  * between messages closer than that rounding.
  * x_src     [num_cols, d_in];  x_dst [num_rows, d_in] (may be x_src itself
  *           when num_rows == num_cols: one transform);  weight [d_in, d_out]

@@ -84,6 +84,11 @@ __device__ __forceinline__ bool takes_over(float m, int32_t e, float best, int32
   return m > best || (m == best && e < best_e);
 }
 
+// A NaN message competes as -inf: it never beats a number, and a row whose
+// messages are all NaN or -inf reports -inf with its smallest edge id.  (The
+// positional-id comparison "strictly greater replaces" behaves so by itself.)
+__device__ __forceinline__ float max_key(float m) { return m != m ? -INFINITY : m; }
+
 // ---- cross-lane primitives --------------------------------------------------
 
 // DPP controls (GFX9 encoding, valid on gfx950).
@@ -187,14 +192,23 @@ __device__ __forceinline__ Item load_item(const Seg* segs, const int32_t* indptr
   return it;
 }
 
+// Epilogues of the u_add_v max (MLP aggregation).  Its edges are compared by
+// their transformed source value P_src[u] (raw: before adding P_dst[v]); fp32
+// rounding of a sum is monotone in each operand, so the edge with the largest
+// raw value also has the largest rounded message relu(P_src[u] + P_dst[v]),
+// and the row's output is relu(acc + xd[v]).  When that is not positive every
+// message is 0 and the row's smallest edge id is reported.
+//  kEpiFirst  (positional edge ids): acc / am are the max and smallest argmax
+//             of the raw values; the smallest id of the row is its first
+//             position.
+//  kEpiMasked (any edge ids): edges whose rounded sum is not positive compete
+//             as -inf, so am already is the smallest id of the row when
+//             nothing is positive.
+constexpr int kEpiNone = 0, kEpiFirst = 1, kEpiMasked = 2;
+
 // Writes one lane's accumulated vector: to the plan workspace for a split
-// row's segment, else to the output (max: empty -> 0 / -1).
-// EPI (u_add_v max with positional edge ids): acc / am are the max and argmax
-// of the raw source values; the row's message max is relu(acc + xd[v]) (fp32
-// rounding of a sum is monotone in each operand, so this equals the max of
-// the rounded per-edge sums), taken by the argmax edge when positive, else
-// every message is 0 and the row's first edge id wins.
-template <int VEC, bool MAX, bool SEG, bool EPI = false>
+// row's segment, else to the output (max: empty -> 0 / -1; EPI: see above).
+template <int VEC, bool MAX, bool SEG, int EPI = kEpiNone>
 __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, int64_t f,
                                            const float (&acc)[VEC], const int32_t (&am)[VEC]) {
   if (SEG && it.slot >= 0) {
@@ -204,15 +218,15 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
     float o[VEC];
     int32_t a[VEC];
     float pdv[VEC];
-    if constexpr (EPI) load_vec<VEC>(p.xd + it.row * p.F + f, pdv);
+    if constexpr (EPI != kEpiNone) load_vec<VEC>(p.xd + it.row * p.F + f, pdv);
 #pragma unroll
     for (int c = 0; c < VEC; ++c) {
       const bool none = am[c] == INT_MAX;
-      if constexpr (EPI) {
+      if constexpr (EPI != kEpiNone) {
         const float t = acc[c] + pdv[c];
         const bool pos = t > 0.0f;
         o[c] = (none || !pos) ? 0.0f : t;
-        a[c] = none ? -1 : (pos ? am[c] : (int32_t)it.b);
+        a[c] = none ? -1 : ((pos || EPI == kEpiMasked) ? am[c] : (int32_t)it.b);
       } else {
         o[c] = none ? 0.0f : acc[c];
         a[c] = none ? -1 : am[c];
@@ -236,9 +250,11 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
 // never replaces and takes its first edge afterwards.  Groups, segments and
 // slots are then merged with the full (value, edge id) order.
 // ADD: the message is relu(x[u] + xd[v]) (MLP aggregation with the dense
-// transform applied to the vertices beforehand); requires MAX and !MUL.  With
-// positional edge ids the add and relu move to the store (EPI, see
-// spmm_store); with explicit edge ids each message is formed in the loop.
+// transform applied to the vertices beforehand); requires MAX and !MUL.  Edges
+// compete by their raw x[u] (see the epilogues above spmm_store).  With
+// positional edge ids the add and relu move to the store (kEpiFirst); with
+// explicit edge ids each edge's sum is formed in the loop to mask the edges
+// whose message is 0 (kEpiMasked).
 // TAB (per-head edge values, 2 <= H <= kTabHeads): each batch of 64 edges
 // stages its edge values in an LDS table, a few loads per lane, and every step
 // reads its weights from there; loading them per step would add one more
@@ -254,6 +270,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
   static_assert(!TAB || MUL, "the table holds edge values");
   constexpr bool EPI = ADD && POS;
   constexpr bool ELEM = ADD && !POS;
+  constexpr int EPK = EPI ? kEpiFirst : (ELEM ? kEpiMasked : kEpiNone);
   __shared__ __align__(16) float tab_all[TAB ? kWavesPerBlock * kWave * kTabHeads : 1];
   float* tab = tab_all + (TAB ? (threadIdx.x >> 6) * kWave * kTabHeads : 0);
   const int64_t item = wave_item();
@@ -394,7 +411,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
 #pragma unroll
               for (int c = 0; c < 4; ++c) {
                 const float t = val[u][v][c] + pd[v][c];
-                val[u][v][c] = t > 0.0f ? t : 0.0f;
+                val[u][v][c] = t > 0.0f ? val[u][v][c] : -INFINITY;
               }
             }
             if constexpr (TAB)
@@ -422,7 +439,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
                 am[v][c] = eu[u];
               }
             } else if constexpr (MAX) {
-              const float m = MUL ? wv[u][v] * val[u][v][c] : val[u][v][c];
+              const float m = max_key(MUL ? wv[u][v] * val[u][v][c] : val[u][v][c]);
               if (ok[u] && takes_over(m, eu[u], acc[v][c], am[v][c])) {
                 acc[v][c] = m;
                 am[v][c] = eu[u];
@@ -468,7 +485,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
   if (gid != 0) return;
 #pragma unroll
   for (int v = 0; v < NV; ++v)
-    if (act[v]) spmm_store<4, MAX, SEG, EPI>(p, it, f[v], acc[v], am[v]);
+    if (act[v]) spmm_store<4, MAX, SEG, EPK>(p, it, f[v], acc[v], am[v]);
 }
 
 // Generic path: any width (scalar lanes), runtime group width G = 2^logG.
@@ -535,9 +552,9 @@ __global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
         for (int v = 0; v < NV; ++v) {
           if (ok[u] && act[v]) {
             val[u][v] = xr[f[v]];
-            if constexpr (ADD) {
+            if constexpr (ADD) {  // raw value; edges with a zero message compete as -inf
               const float t = val[u][v] + pd[v];
-              val[u][v] = t > 0.0f ? t : 0.0f;
+              val[u][v] = t > 0.0f ? val[u][v] : -INFINITY;
             }
             wv[u][v] = (MUL && p.H != 1) ? p.ev[(int64_t)eu[u] * p.H + hv[v]] : w1;
           } else {
@@ -551,7 +568,7 @@ __global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
           if constexpr (MAX) {
-            const float m = MUL ? wv[u][v] * val[u][v] : val[u][v];
+            const float m = max_key(MUL ? wv[u][v] * val[u][v] : val[u][v]);
             if (ok[u] && takes_over(m, eu[u], acc[v][0], am[v][0])) {
               acc[v][0] = m;
               am[v][0] = eu[u];
@@ -582,7 +599,7 @@ __global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
   if (gid != 0) return;
 #pragma unroll
   for (int v = 0; v < NV; ++v)
-    if (act[v]) spmm_store<1, MAX, SEG>(p, it, f[v], acc[v], am[v]);
+    if (act[v]) spmm_store<1, MAX, SEG, ADD ? kEpiMasked : kEpiNone>(p, it, f[v], acc[v], am[v]);
 }
 
 // Merges the partial results of each split row.  Block = 4 wavefronts over a
@@ -591,7 +608,7 @@ __global__ __launch_bounds__(kBlock) void spmm_generic_kernel(SpmmParams p) {
 // wavefront results are combined in order w = 0..3.
 // EPI: the partials are raw max / argmax of the source values of a u_add_v
 // max (see spmm_store); the merged result gets the same relu epilogue.
-template <bool MAX, bool EPI = false>
+template <bool MAX, int EPI = kEpiNone>
 __global__ __launch_bounds__(kBlock) void spmm_fixup_kernel(const Fix* fix, const float* ws_f,
                                                             const int32_t* ws_i, int64_t F,
                                                             float* out, int32_t* arg,
@@ -652,12 +669,12 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup_kernel(const Fix* fix, cons
     }
   }
   const int64_t o = (int64_t)fx.row * F + col;
-  if constexpr (EPI) {
+  if constexpr (EPI != kEpiNone) {
     const bool none = am == INT_MAX;
     const float t = acc + xd[o];
     const bool pos = t > 0.0f;
     out[o] = (none || !pos) ? 0.0f : t;
-    arg[o] = none ? -1 : (pos ? am : indptr[fx.row]);
+    arg[o] = none ? -1 : ((pos || EPI == kEpiMasked) ? am : indptr[fx.row]);
   } else if constexpr (MAX) {
     const bool none = am == INT_MAX;
     out[o] = none ? 0.0f : acc;
@@ -670,7 +687,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup_kernel(const Fix* fix, cons
 // The same merge with float4 lanes (F % 4 == 0, 16-byte aligned out / arg):
 // a wavefront covers 256 columns, so each slot costs one 1 KiB load per
 // wavefront instead of four.  Same slot order and combination order.
-template <bool MAX, bool EPI = false>
+template <bool MAX, int EPI = kEpiNone>
 __global__ __launch_bounds__(kBlock) void spmm_fixup4_kernel(const Fix* fix, const float* ws_f,
                                                              const int32_t* ws_i, int64_t F,
                                                              float* out, int32_t* arg,
@@ -752,19 +769,19 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup4_kernel(const Fix* fix, con
       }
     }
   const int64_t o = (int64_t)fx.row * F + col;
-  if constexpr (EPI || MAX) {
+  if constexpr (EPI != kEpiNone || MAX) {
     float ov[4];
     int32_t oa[4];
     float xv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    if constexpr (EPI) load_vec<4>(xd + o, xv);
+    if constexpr (EPI != kEpiNone) load_vec<4>(xd + o, xv);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const bool none = am[c] == INT_MAX;
-      if constexpr (EPI) {
+      if constexpr (EPI != kEpiNone) {
         const float t = acc[c] + xv[c];
         const bool pos = t > 0.0f;
         ov[c] = (none || !pos) ? 0.0f : t;
-        oa[c] = none ? -1 : (pos ? am[c] : indptr[fx.row]);
+        oa[c] = none ? -1 : ((pos || EPI == kEpiMasked) ? am[c] : indptr[fx.row]);
       } else {
         ov[c] = none ? 0.0f : acc[c];
         oa[c] = none ? -1 : am[c];
@@ -2822,14 +2839,18 @@ hipError_t launch_spmm_core(const GraphView& g, const PlanView* plan, int msg, i
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (seg && plan->num_split_rows > 0) {
-    // the float4 kernel with positional edge ids defers the u_add_v epilogue
-    const bool epi = xd && vec4 && !g.edge_ids;
+    // u_add_v partials are raw values: the merge applies the epilogue (the
+    // float4 kernel with positional edge ids keeps them unmasked)
+    const int epi = !xd ? kEpiNone : ((vec4 && !g.edge_ids) ? kEpiFirst : kEpiMasked);
     // float4 merge: vec4 already checked F % 4, out (and arg, xd) alignment
     if (vec4) {
       const dim3 fgrid((unsigned)plan->num_split_rows, (unsigned)((F + 4 * kWave - 1) / (4 * kWave)),
                        1);
-      if (epi)
-        FG_LAUNCH((spmm_fixup4_kernel<true, true>), fgrid, stream, plan->fix, plan->ws_f,
+      if (epi == kEpiFirst)
+        FG_LAUNCH((spmm_fixup4_kernel<true, kEpiFirst>), fgrid, stream, plan->fix, plan->ws_f,
+                  plan->ws_i, F, out, arg, xd, g.indptr);
+      else if (epi == kEpiMasked)
+        FG_LAUNCH((spmm_fixup4_kernel<true, kEpiMasked>), fgrid, stream, plan->fix, plan->ws_f,
                   plan->ws_i, F, out, arg, xd, g.indptr);
       else if (mx)
         FG_LAUNCH((spmm_fixup4_kernel<true>), fgrid, stream, plan->fix, plan->ws_f, plan->ws_i,
@@ -2840,8 +2861,11 @@ hipError_t launch_spmm_core(const GraphView& g, const PlanView* plan, int msg, i
       return hipGetLastError();
     }
     const dim3 fgrid((unsigned)plan->num_split_rows, (unsigned)((F + kWave - 1) / kWave), 1);
-    if (epi)
-      FG_LAUNCH((spmm_fixup_kernel<true, true>), fgrid, stream, plan->fix, plan->ws_f,
+    if (epi == kEpiFirst)
+      FG_LAUNCH((spmm_fixup_kernel<true, kEpiFirst>), fgrid, stream, plan->fix, plan->ws_f,
+                plan->ws_i, F, out, arg, xd, g.indptr);
+    else if (epi == kEpiMasked)
+      FG_LAUNCH((spmm_fixup_kernel<true, kEpiMasked>), fgrid, stream, plan->fix, plan->ws_f,
                 plan->ws_i, F, out, arg, xd, g.indptr);
     else if (mx)
       FG_LAUNCH((spmm_fixup_kernel<true>), fgrid, stream, plan->fix, plan->ws_f, plan->ws_i, F,

@@ -347,11 +347,42 @@ def check_dense_matmul(n, d_in, d_out, seed, exact=False):
         assert_close_sum(y, ref, tnorm, d_in)
 
 
+def check_mlp_edges(csr, sel, out, arg):
+    """Rules every MLP-aggregation edge must satisfy, whatever the rounding:
+    the edge is one of row v's own edges; among duplicate edges (same source,
+    so the same message in every rounding) it is the one with the smallest
+    id; and where the output is 0 (no positive message, so every message is
+    0) it is the row's smallest edge id.  Rows without edges report -1."""
+    for i, v in enumerate(sel):
+        p0, p1 = int(csr.indptr[v]), int(csr.indptr[v + 1])
+        a = arg[i].astype(np.int64)
+        if p0 == p1:
+            assert (a == -1).all() and (out[i] == 0).all(), "row %d has no edges" % v
+            continue
+        ids = edge_ids_of(csr, np.arange(p0, p1))
+        srcs = csr.indices[p0:p1].astype(np.int64)
+        order = np.lexsort((ids, srcs))  # by source, then id
+        u_sorted, first = np.unique(srcs[order], return_index=True)
+        min_id_of_src = ids[order][first]
+        # membership: a's position in this row
+        pos_sorted = np.argsort(ids, kind="stable")
+        k = np.searchsorted(ids[pos_sorted], a)
+        k = np.minimum(k, len(ids) - 1)
+        assert (ids[pos_sorted][k] == a).all(), \
+            "row %d: edge %r is not an edge of the row" % (v, a[ids[pos_sorted][k] != a][:4])
+        src_a = srcs[pos_sorted][k]
+        j = np.searchsorted(u_sorted, src_a)
+        assert (min_id_of_src[j] == a).all(), \
+            "row %d: a duplicate with a smaller id exists for %r" % (v, a[min_id_of_src[j] != a][:4])
+        zero = out[i] == 0
+        assert (a[zero] == ids.min()).all(), "row %d: zero output must report the smallest id" % v
+
+
 def check_mlp(csr, G, xs, xd, w, rows=None, plan=None, exact=False, square=False):
     """MLP aggregation vs the oracle's per-edge definition.  Values within the
-    rounding of the two forms; the GPU's edge must attain the oracle's maximum
-    within that tolerance (equal when the maximum is unique by more than it);
-    integer inputs: bit-exact values and edges."""
+    rounding of the two forms; the GPU's edge must be an edge of its row,
+    attain the oracle's maximum within that tolerance and obey the rules of
+    check_mlp_edges; integer inputs: bit-exact values and edges."""
     d_in, d_out = w.shape
     say("mlp_aggregate rows=%d nnz=%d d_in=%d d_out=%d exact=%s plan=%s" % (
         csr.num_rows, csr.nnz, d_in, d_out, exact,
@@ -368,6 +399,7 @@ def check_mlp(csr, G, xs, xd, w, rows=None, plan=None, exact=False, square=False
         return
     deg = csr.degrees()[sel]
     assert ((arg >= 0) == (deg > 0)[:, None]).all()
+    check_mlp_edges(csr, sel, out, arg)
     # the fp64 message of a given edge id for every (row, feature)
     src = _sources_of_ids(csr, csr.nnz if csr.edge_ids is None else int(csr.edge_ids.max()) + 1)
     w64 = w.astype(np.float64)
@@ -642,6 +674,103 @@ def test_mlp_aggregate(small_rmat, d_in, d_out):
     check_mlp(csr, G, x, xd, w, plan=fg.Plan(G, d_out, segment_edges=64))
 
 
+def _mlp_tie_graph(ids):
+    """Rows whose messages tie only after fp32 rounding, rows whose messages
+    are all 0 (ReLU), duplicate edges, an empty row.  ids: 'positions' or
+    'reversed' (edge id = nnz - 1 - position, so a row's smallest id is its
+    last stored edge)."""
+    a, b = 2.0 ** -25, 2.0 ** -24
+    xs = np.array([[a], [b], [0.5], [0.25], [2.0], [1.0]], np.float32)
+    xd = np.array([[1.0], [-1.0], [0.0], [0.0], [-1.0]], np.float32)
+    dst = np.array([0, 0, 1, 1, 2, 2, 2, 4, 4])
+    src = np.array([0, 1, 2, 3, 1, 4, 4, 5, 2])
+    csr = synth.coo_to_csr(dst, src, 5, 6)
+    if ids == "reversed":
+        csr = synth.CSR(5, 6, csr.indptr, csr.indices,
+                        (csr.nnz - 1 - np.arange(csr.nnz)).astype(np.int32))
+    return csr, xs, xd
+
+
+def _mlp_rule(csr, xs, xd, w):
+    """The library's rule in fp32: edges compete by P_src[u] = x_u W (raw,
+    before adding P_dst[v]); the output is relu(max P_src + P_dst), taken by
+    the smallest id among the edges with that largest raw value, or, when no
+    message is positive (all are 0), by the row's smallest edge id."""
+    ps = (xs.astype(np.float64) @ w.astype(np.float64)).astype(np.float32)
+    pd = (xd.astype(np.float64) @ w.astype(np.float64)).astype(np.float32)
+    out = np.zeros((csr.num_rows, w.shape[1]), np.float32)
+    arg = np.full((csr.num_rows, w.shape[1]), -1, np.int32)
+    for v in range(csr.num_rows):
+        p = np.arange(csr.indptr[v], csr.indptr[v + 1])
+        if p.size == 0:
+            continue
+        ids = edge_ids_of(csr, p)
+        for i in range(w.shape[1]):
+            raw = ps[csr.indices[p], i]
+            t = raw + pd[v, i]  # fp32 sums
+            if (t > 0).any():
+                m = raw[t > 0].max()
+                out[v, i] = np.float32(m + pd[v, i])
+                arg[v, i] = ids[raw == m].min()
+            else:
+                arg[v, i] = ids.min()
+    return out, arg
+
+
+@pytest.mark.parametrize("ids", ["positions", "reversed"])
+@pytest.mark.parametrize("w_row", [[1.0, 2.0, 0.5, -1.0], [1.0, 2.0, -1.0]])
+def test_mlp_rounding_ties(ids, w_row):
+    """One argmax rule on every path (float4 lanes with positional ids, scalar
+    lanes, explicit edge ids, and the split-row merges): messages
+    relu(P_src[u] + P_dst[v]) that differ only before rounding go to the
+    larger P_src, and a row without a positive message reports its smallest
+    edge id.  On this graph the oracle's fp64 per-edge messages pick the same
+    edges, so the GPU must equal both bitwise."""
+    csr, xs, xd = _mlp_tie_graph(ids)
+    w = np.array([w_row], np.float32)
+    G = fg.Graph.from_csr(csr)
+    ro, ra = _mlp_rule(csr, xs, xd, w)
+    oo, oa = O.mlp_aggregate(csr, xs, xd, w)
+    np.testing.assert_array_equal(ro, oo)
+    np.testing.assert_array_equal(ra, oa)
+    for plan in (None, fg.Plan(G, w.shape[1], segment_edges=1)):
+        say("mlp rounding ties ids=%s d_out=%d plan=%s" % (ids, w.shape[1], plan is not None))
+        out, arg = fg.mlp_aggregate(G, dev(xs), dev(w), x_dst=dev(xd), plan=plan)
+        np.testing.assert_array_equal(host(out).view(np.uint32), ro.view(np.uint32))
+        np.testing.assert_array_equal(host(arg), ra)
+
+
+def test_max_nan_messages():
+    """NaN messages compete as -inf (value bits and edge ids against the
+    oracle) on every max path: float4 lanes with positional ids, scalar
+    lanes, explicit edge ids, weighted messages, and split rows."""
+    rng = np.random.default_rng(41)
+    n_rows, n_cols = 300, 200
+    base = synth.small_random_graph(rng, n_rows, n_cols, 6000, 0.1)
+    # rows 0..2: only NaN sources; NaN and -inf; -inf, NaN and numbers
+    dst = np.concatenate([synth.csr_rows(base), [0, 0, 0, 1, 1, 2, 2, 2]])
+    src = np.concatenate([base.indices, [0, 1, 2, 0, 20, 20, 0, 50]])
+    csr = synth.coo_to_csr(dst, src, n_rows, n_cols)
+    G = fg.Graph.from_csr(csr)
+    csc = csr_to_csc(csr)
+    Gt = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+    for F in (8, 5):
+        x = rng.standard_normal((n_cols, F)).astype(np.float32)
+        x[rng.random((n_cols, F)) < 0.3] = np.nan
+        x[:20] = np.nan
+        x[20:25] = -np.inf
+        xt = rng.standard_normal((n_rows, F)).astype(np.float32)
+        xt[rng.random((n_rows, F)) < 0.3] = np.nan
+        w = rng.random(csr.nnz, dtype=np.float32)
+        w[rng.random(csr.nnz) < 0.2] = 0.0  # 0 * (-inf) is NaN
+        for plan in plans_for(G, F, sizes=(0, 5)):
+            check_spmm(csr, G, x, plan=plan, reduce="max")
+            check_spmm(csr, G, x, plan=plan, reduce="max", edge=w)
+        for plan in (None, fg.Plan(Gt, F, segment_edges=5)):
+            check_spmm(csc, Gt, xt, plan=plan, reduce="max", nnz_total=csr.nnz)
+            check_spmm(csc, Gt, xt, plan=plan, reduce="max", edge=w, nnz_total=csr.nnz)
+
+
 def test_mlp_aggregate_transposed_and_empty(small_rmat):
     csr, _ = small_rmat
     csc = csr_to_csc(csr)
@@ -649,8 +778,14 @@ def test_mlp_aggregate_transposed_and_empty(small_rmat):
     rng = np.random.default_rng(5)
     x = rng.integers(-3, 4, (csc.num_cols, 8)).astype(np.float32)
     w = rng.integers(-2, 3, (8, 16)).astype(np.float32)
+    xf = rng.standard_normal((csc.num_cols, 8)).astype(np.float32)
+    wf = rng.standard_normal((8, 16)).astype(np.float32)
     for plan in (None, fg.Plan(Gt, 16, segment_edges=64)):
         check_mlp(csc, Gt, x, x, w, plan=plan, exact=True, square=True)
+        # float inputs through explicit edge ids (messages masked in the loop)
+        check_mlp(csc, Gt, xf, xf, wf, plan=plan, square=True)
+        check_mlp(csc, Gt, xf[:, :7].copy(), xf[:, :7].copy(), wf[:7, :7].copy(), plan=None,
+                  square=True)  # odd width: scalar lanes
     noedge = synth.CSR(3, 5, np.zeros(4, np.int32), np.zeros(0, np.int32))
     G0 = fg.Graph.from_csr(noedge)
     o, a = fg.mlp_aggregate(G0, dev(np.ones((5, 8), np.float32)), dev(np.ones((8, 4), np.float32)),
