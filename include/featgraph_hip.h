@@ -180,6 +180,7 @@ typedef struct fg_plan_info {
   int32_t segment_edges, max_row_segments, source_slab_rows, partition_min_degree;
   int32_t item_order;           /* the order used: 1 or 2 (see fg_plan_options)      */
   int32_t max_backward;         /* 1 if the binned max-backward workspace is held    */
+  uint64_t indptr_checksum;     /* fg_indptr_checksum of the indptr it was built for */
 } fg_plan_info;
 
 /* One work item of a schedule (host view; the device tables hold the same). */
@@ -208,7 +209,8 @@ fg_status fg_schedule_host(const int32_t* indptr_host, const int32_t* indices_ho
  * order).  opt may be NULL.  Validates indptr, and the indices whenever it
  * holds them all on the host (FG_ERR_INVALID_ARG), allocates device memory,
  * synchronises `stream`.  The plan is bound to g->indptr, num_rows and
- * nnz: calls with another graph are rejected with FG_ERR_INVALID_ARG.  Its
+ * nnz: calls with another graph are rejected with FG_ERR_INVALID_ARG; it
+ * also keeps the checksum of indptr (fg_plan_validate re-checks it).  Its
  * workspace is mutable: calls that share a plan must be ordered on one
  * stream. */
 fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
@@ -216,6 +218,23 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
                          const fg_plan_options* opt, fg_plan** out, void* stream);
 fg_status fg_plan_destroy(fg_plan* plan);
 fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info);
+
+/* Checksum of a HOST indptr array [num_rows + 1]: 64-bit FNV-1a over the
+ * little-endian bytes of its int32 entries (offset basis 14695981039346656037,
+ * prime 1099511628211).  Pure host function: no HIP call. */
+fg_status fg_indptr_checksum(const int32_t* indptr_host, int64_t num_rows, uint64_t* out);
+
+/* Re-validates a plan against graph `g`: the bindings every call checks
+ * (indptr pointer, num_rows, nnz) and the checksum of indptr's current
+ * contents against the one taken when the plan was built, so that a plan is
+ * not reused after indptr was edited in place or another graph of the same
+ * shape was placed at the same address.  indptr_host: an optional HOST copy
+ * of g->indptr; without it indptr is copied from the device on `stream`,
+ * which is synchronised.  FG_OK if the plan fits, FG_ERR_INVALID_ARG if not.
+ * (The compute calls check only the pointer and sizes: the checksum costs a
+ * pass over indptr, so callers that edit graphs in place call this.) */
+fg_status fg_plan_validate(const fg_plan* plan, const fg_graph* g, const int32_t* indptr_host,
+                           void* stream);
 
 /* ---------------------------------------------------------------------------
  * Generalized SpMM (Sec. II-A Eq. 1; Sec. III-B featgraph.spmm):

@@ -82,6 +82,7 @@ class _PlanInfo(ctypes.Structure):
         ("partition_min_degree", ctypes.c_int32),
         ("item_order", ctypes.c_int32),
         ("max_backward", ctypes.c_int32),
+        ("indptr_checksum", ctypes.c_uint64),
     ]
 
 
@@ -112,6 +113,10 @@ def _load():
     lib.fg_plan_destroy.argtypes = [vp]
     lib.fg_plan_get_info.restype = ctypes.c_int
     lib.fg_plan_get_info.argtypes = [vp, ctypes.POINTER(_PlanInfo)]
+    lib.fg_indptr_checksum.restype = ctypes.c_int
+    lib.fg_indptr_checksum.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_uint64)]
+    lib.fg_plan_validate.restype = ctypes.c_int
+    lib.fg_plan_validate.argtypes = [vp, gp, vp, vp]
     lib.fg_gspmm.restype = ctypes.c_int
     lib.fg_gspmm.argtypes = [gp, ctypes.c_int, ctypes.c_int, i32, i64, vp, vp, vp, vp, vp, vp]
     lib.fg_gspmm_noalloc.restype = ctypes.c_int
@@ -281,12 +286,32 @@ class Plan:
         _check(st, "fg_plan_create")
         self._h = h
         self.graph = g
+        self._versions = _graph_versions(g)
 
     @property
     def handle(self):
         if self._h is None:
             raise ValueError("plan is closed")
         return self._h
+
+    def validate(self) -> None:
+        """Re-checks the plan against its graph's current indptr on the device
+        (fg_plan_validate: the checksum taken at creation); raises FgError if
+        indptr no longer matches.  Afterwards in-place edits that kept indptr
+        (and a re-sorted indices of an unpartitioned plan) are accepted."""
+        g = self.graph
+        _check(_lib.fg_plan_validate(self.handle, ctypes.byref(g._c), None, _stream()),
+               "fg_plan_validate")
+        self._versions = _graph_versions(g)
+
+    def check_current(self) -> None:
+        """Raises ValueError when the graph's device arrays were modified in
+        place since the plan was built (or last validated): the plan's
+        schedules describe the old rows."""
+        if _graph_versions(self.graph) != self._versions:
+            raise ValueError(
+                "the graph's indptr / indices / edge_ids were modified in place after this plan "
+                "was built; build a new plan, or call plan.validate() if indptr is unchanged")
 
     def info(self) -> dict:
         inf = _PlanInfo()
@@ -339,8 +364,27 @@ def schedule_host(indptr: np.ndarray, indices: Optional[np.ndarray] = None, num_
     return segs, n_split.value, n_slot.value
 
 
+def _graph_versions(g: Graph):
+    """In-place modification counters of a graph's device arrays."""
+    return tuple(None if t is None else t._version for t in (g.indptr, g.indices, g.edge_ids))
+
+
+def indptr_checksum(indptr: np.ndarray) -> int:
+    """fg_indptr_checksum of a host indptr (64-bit FNV-1a over its int32 bytes)."""
+    ip = np.ascontiguousarray(indptr, dtype=np.int32)
+    if ip.ndim != 1 or ip.size < 1:
+        raise ValueError("indptr must be a non-empty 1-D array")
+    out = ctypes.c_uint64()
+    _check(_lib.fg_indptr_checksum(ip.ctypes.data, ip.size - 1, ctypes.byref(out)),
+           "fg_indptr_checksum")
+    return out.value
+
+
 def _plan_handle(plan: Optional[Plan]):
-    return None if plan is None else plan.handle
+    if plan is None:
+        return None
+    plan.check_current()
+    return plan.handle
 
 
 # ----------------------------------------------------------------------------

@@ -33,6 +33,7 @@ struct fg_plan {
   fg::BinWorkspace bin;  // binned max backward (plan option), else empty
   std::vector<void*> mem;
   int64_t workspace_bytes = 0;
+  uint64_t indptr_sum = 0;  // checksum of the indptr the schedules were built from
 };
 
 static_assert(fg::kNoAllocScratchBytes == FG_NOALLOC_SCRATCH_BYTES,
@@ -94,6 +95,19 @@ fg::GraphView view_of(const fg_graph* g) {
 }
 
 fg_status from_hip(hipError_t e) { return e == hipSuccess ? FG_OK : FG_ERR_HIP; }
+
+// 64-bit FNV-1a over the bytes of the int32 entries (little endian).
+uint64_t checksum_of(const int32_t* ip, int64_t n) {
+  uint64_t h = 14695981039346656037ull;
+  for (int64_t i = 0; i < n; ++i) {
+    const uint32_t v = (uint32_t)ip[i];
+    for (int b = 0; b < 4; ++b) {
+      h ^= (v >> (8 * b)) & 0xFFu;
+      h *= 1099511628211ull;
+    }
+  }
+  return h;
+}
 
 bool indptr_valid(const int32_t* ip, int64_t num_rows, int64_t nnz) {
   if (ip[0] != 0 || ip[num_rows] != nnz) return false;
@@ -728,6 +742,7 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
   p->nnz = g->nnz;
   p->max_width = max_width;
   p->indptr = g->indptr;
+  p->indptr_sum = checksum_of(ip, g->num_rows + 1);
   p->segment_edges = o.S;
   p->max_row_segments = o.cap;
   p->slab_rows = ix ? o.slab : 0;
@@ -843,7 +858,38 @@ fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info) {
   info->partition_min_degree = plan->partition_min_degree;
   info->item_order = plan->item_order;
   info->max_backward = plan->bin.rec ? 1 : 0;
+  info->indptr_checksum = plan->indptr_sum;
   return FG_OK;
+}
+
+fg_status fg_indptr_checksum(const int32_t* indptr_host, int64_t num_rows, uint64_t* out) {
+  if (!indptr_host || !out || num_rows < 0 || num_rows >= INT32_MAX) return FG_ERR_INVALID_ARG;
+  *out = checksum_of(indptr_host, num_rows + 1);
+  return FG_OK;
+}
+
+fg_status fg_plan_validate(const fg_plan* plan, const fg_graph* g, const int32_t* indptr_host,
+                           void* stream) {
+  if (!plan) return FG_ERR_INVALID_ARG;
+  fg_status st = check_graph(g);
+  if (st != FG_OK) return st;
+  if ((st = check_plan(plan, g, 1)) != FG_OK) return st;
+  std::vector<int32_t> copy;
+  const int32_t* ip = indptr_host;
+  if (!ip) {
+    try {
+      copy.resize((size_t)g->num_rows + 1);
+    } catch (const std::bad_alloc&) {
+      return FG_ERR_NO_MEMORY;
+    }
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    if (hipMemcpyAsync(copy.data(), g->indptr, sizeof(int32_t) * copy.size(),
+                       hipMemcpyDeviceToHost, hs) != hipSuccess ||
+        hipStreamSynchronize(hs) != hipSuccess)
+      return FG_ERR_HIP;
+    ip = copy.data();
+  }
+  return checksum_of(ip, g->num_rows + 1) == plan->indptr_sum ? FG_OK : FG_ERR_INVALID_ARG;
 }
 
 }  // extern "C"

@@ -550,3 +550,46 @@ def test_schedule_edge_cases():
         fg.schedule_host(np.array([0, 5, 3], np.int32), segment_edges=8)
     with pytest.raises(fg.FgError):  # a source id out of range
         fg.schedule_host(np.array([0, 2], np.int32), np.array([0, 9], np.int32), 5)
+
+
+def _fnv1a64(ip):
+    h = 14695981039346656037
+    for b in np.ascontiguousarray(ip, dtype="<i4").tobytes():
+        h = ((h ^ b) * 1099511628211) & 0xFFFFFFFFFFFFFFFF
+    return h
+
+
+def test_indptr_checksum_is_fnv1a_and_sees_in_place_edits():
+    ip = np.array([0, 3, 4, 4, 7], np.int32)
+    assert fg.indptr_checksum(ip) == _fnv1a64(ip)
+    moved = ip.copy()
+    moved[1] = 2  # one edge moved from row 0 to row 1: same shape and nnz
+    assert fg.indptr_checksum(moved) != fg.indptr_checksum(ip)
+    big = synth.make_config("tiny_uniform_1k").csr.indptr
+    assert fg.indptr_checksum(big) == _fnv1a64(big)
+    out = ctypes.c_uint64()
+    assert fg._lib.fg_indptr_checksum(None, 4, ctypes.byref(out)) == fg.FG_ERR_INVALID_ARG
+    assert fg._lib.fg_indptr_checksum(ip.ctypes.data, -1, ctypes.byref(out)) == \
+        fg.FG_ERR_INVALID_ARG
+    assert fg._lib.fg_plan_validate(None, None, None, None) == fg.FG_ERR_INVALID_ARG
+
+
+def test_plan_refuses_a_graph_edited_in_place():
+    """The binding records the in-place modification counters of the graph's
+    arrays when a plan is built and refuses the plan once any of them moved
+    (the kernels take row ranges from the plan, not from indptr)."""
+    from types import SimpleNamespace
+
+    p = fg.Plan.__new__(fg.Plan)
+    p._h = None
+    p.graph = SimpleNamespace(indptr=torch.tensor([0, 3, 4, 4, 7], dtype=torch.int32),
+                              indices=torch.zeros(7, dtype=torch.int32), edge_ids=None)
+    p._versions = fg._graph_versions(p.graph)
+    p.check_current()
+    p.graph.indices[2] = 1
+    with pytest.raises(ValueError, match="modified in place"):
+        p.check_current()
+    p._versions = fg._graph_versions(p.graph)
+    p.graph.indptr[1] = 2
+    with pytest.raises(ValueError, match="modified in place"):
+        fg._plan_handle(p)

@@ -6,6 +6,7 @@ softmax, d or dh for dots) and ||t||_2 the L2 norm of the n fp64 terms from the
 oracle.  Softmax: |y - ref| <= 1e-5 * sqrt(n) * |ref| + 1e-12.  Max/argmax and
 integer-valued inputs: bit-exact.
 """
+import ctypes
 import math
 
 import numpy as np
@@ -1111,6 +1112,35 @@ def test_plan_bound_to_its_graph(small_rmat):
         fg.gspmm(other, x, plan=plan)
     with pytest.raises(fg.FgError):
         fg.gspmm(G, dev(np.ones((csr.num_cols, 32), np.float32)), plan=plan)  # too wide
+
+
+def test_plan_checksum_after_in_place_edit():
+    """A plan is not reused after its graph's indptr was edited in place: the
+    binding refuses it (modification counters), fg_plan_validate sees the
+    changed checksum, and restoring indptr makes the plan valid again."""
+    csr = make_config("tiny_uniform_1k").csr
+    G = fg.Graph.from_csr(csr)
+    plan = fg.Plan(G, 32, segment_edges=5)
+    assert plan.info()["indptr_checksum"] == fg.indptr_checksum(csr.indptr)
+    x = np.random.default_rng(9).standard_normal((csr.num_cols, 32)).astype(np.float32)
+    plan.validate()
+    say("plan checksum: edit indptr in place")
+    old = int(csr.indptr[1])
+    G.indptr[1] = old - 1  # one edge moves from row 0 to row 1: same shape, same nnz
+    with pytest.raises(ValueError, match="modified in place"):
+        fg.gspmm(G, dev(x), plan=plan)
+    with pytest.raises(fg.FgError):
+        plan.validate()
+    st = fg._lib.fg_plan_validate(plan.handle, ctypes.byref(G._c), None, fg._stream())
+    assert st == fg.FG_ERR_INVALID_ARG
+    G.indptr[1] = old
+    plan.validate()  # contents match again: accepted, counters re-recorded
+    check_spmm(csr, G, x, plan=plan)
+    # another graph of the same shape at another address is refused by pointer
+    other = fg.Graph.from_csr(csr)
+    assert fg._lib.fg_plan_validate(plan.handle, ctypes.byref(other._c), None,
+                                    fg._stream()) == fg.FG_ERR_INVALID_ARG
+    plan.close()
 
 
 # ----------------------------------------------------------------------------
