@@ -155,10 +155,18 @@ typedef struct fg_plan_options {
                                    number of id slabs)                              */
   int32_t item_order;           /* order of the work items: 0 -> automatic (2 if rows
                                    with neighbouring ids share sources, judged on
-                                   64 windows of 32 rows, else 1; 1 without
-                                   indices); 1 -> longest first; 2 -> by
+                                   64 windows of 32 rows, else 1, and then 3 if
+                                   some row is cut into 8 or more pieces; 1 or 3
+                                   without indices); 1 -> longest first; 2 -> by
                                    power-of-two length class, longest first, rows
-                                   in id order within a class                       */
+                                   in id order within a class; 3 -> die-banded
+                                   gather schedule (unless source slabs apply):
+                                   the same items as 1, but piece k of a row cut
+                                   into K >= 8 pieces runs on die
+                                   floor(8 (k + 1/2) / K), so each die gathers from
+                                   one eighth of those rows' sources; the other
+                                   items balance the dies' edges (edge softmax
+                                   keeps order 1); results equal those of 1   */
   int32_t max_backward;         /* 1 -> also reserve the workspace of the binned
                                    gSpMM-max backward: 8 bytes per element of a
                                    num_rows x max_width gradient (that product must
@@ -178,7 +186,7 @@ typedef struct fg_plan_info {
   int64_t max_width;            /* largest F the workspace holds                     */
   int64_t workspace_bytes;
   int32_t segment_edges, max_row_segments, source_slab_rows, partition_min_degree;
-  int32_t item_order;           /* the order used: 1 or 2 (see fg_plan_options)      */
+  int32_t item_order;           /* the order used: 1, 2 or 3 (see fg_plan_options)   */
   int32_t max_backward;         /* 1 if the binned max-backward workspace is held    */
   uint64_t indptr_checksum;     /* fg_indptr_checksum of the indptr it was built for */
 } fg_plan_info;

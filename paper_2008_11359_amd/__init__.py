@@ -264,8 +264,11 @@ class Plan:
     are spread (no dominant hot sources, no locality along row ids); -1 once
     they exceed 32 MiB; -2 never; > 0 that many source ids per slab.  ``item_order``: 1 longest
     item first, 2 by power-of-two length class with rows in id order (keeps
-    the locality of graphs whose neighbouring ids share sources), 0
-    (default) picks 2 for such graphs and 1 otherwise.  Partial-result
+    the locality of graphs whose neighbouring ids share sources), 3 the items
+    of 1 with the pieces of rows cut into 8 or more dealt to the dies by
+    position in the row (each die gathers from one eighth of their sources;
+    same results as 1), 0 (default) picks 2 for such graphs and otherwise 3
+    if some row is cut into 8 or more pieces, else 1.  Partial-result
     workspace for features up to ``max_width`` floats.  ``max_backward``:
     also hold the workspace with which gspmm_max_backward bins the gradient
     per source tile instead of adding it with atomics (8 bytes per element of

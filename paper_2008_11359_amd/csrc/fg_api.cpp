@@ -136,7 +136,7 @@ constexpr int32_t kSlabsOff = -2;   // source_slab_rows: never partition
 constexpr int64_t kMinPartitionDegree = 64;
 constexpr int64_t kMinPieceEdges = 8;
 
-constexpr int32_t kOrderAuto = 0, kOrderByLength = 1, kOrderById = 2;
+constexpr int32_t kOrderAuto = 0, kOrderByLength = 1, kOrderById = 2, kOrderDieBanded = 3;
 constexpr int64_t kOrderWindows = 64, kOrderWindowRows = 32, kOrderWindowEdges = 1 << 16;
 
 // Windows of up to kOrderWindowRows consecutive rows (at most
@@ -239,7 +239,10 @@ constexpr int64_t kDieL2Bytes = 4 << 20;
 
 struct Options {
   int32_t S, cap, slab, min_deg;  // slab 0: no source partitioning
-  int32_t order;                  // item order: 0 automatic, 1 by length, 2 by class + id
+  int32_t order;                  // item order: 0 automatic, 1 by length, 2 by class + id,
+                                  // 3 die-banded gather schedule
+  bool band_auto;                 // automatic order settled on 1: band the gather schedule
+                                  // if some row has kXcds or more pieces
   bool slab_if_spread;            // keep the slabs only if the gathers are spread
   bool max_backward;              // reserve the binned max-backward workspace
 };
@@ -251,7 +254,10 @@ void settle_options(Options& o, const int32_t* ip, const int32_t* ix, int64_t nu
                     int64_t num_cols, int64_t max_width, int id_local) {
   if (id_local < 0 && ix && (o.order == kOrderAuto || o.slab_if_spread))
     id_local = ids_share_sources_host(ip, ix, num_rows) ? 1 : 0;
-  if (o.order == kOrderAuto) o.order = id_local == 1 ? kOrderById : kOrderByLength;
+  if (o.order == kOrderAuto) {
+    o.order = id_local == 1 ? kOrderById : kOrderByLength;
+    o.band_auto = o.order == kOrderByLength;
+  }
   if (o.slab_if_spread) {
     const int64_t rows = kDieL2Bytes / (4 * std::max<int64_t>(max_width, 1));
     if (!ix || id_local != 0 || hot_source_share(ix, ip[num_rows], num_cols, rows) >= kSpreadShare)
@@ -261,6 +267,7 @@ void settle_options(Options& o, const int32_t* ip, const int32_t* ix, int64_t nu
 }
 
 struct Schedule {
+  bool banded = false;  // die-banded order (band_by_die)
   std::vector<fg::Seg> segs;
   std::vector<fg::Fix> fix;
   std::vector<int32_t> slot_fix;  // slot -> index into fix
@@ -352,6 +359,26 @@ void build_plain(const int32_t* ip, int64_t num_rows, const Options& o, Schedule
   for (auto& pc : pieces) sc.segs.push_back(pc.first);
   if (o.order == kOrderById) std::stable_sort(sc.segs.begin(), sc.segs.end(), longer_class);
   else std::stable_sort(sc.segs.begin(), sc.segs.end(), longer);
+  for (size_t i = 0; i < sc.segs.size(); ++i)
+    if (sc.segs[i].slot >= 0) sc.slot_seg[sc.segs[i].slot] = (int32_t)i;
+}
+
+// Deals per-die item streams into one item list: workgroup i (four items)
+// runs on die i mod 8, so round r holds four items of die 0, then four of die
+// 1, and so on; exhausted streams are padded with empty items (row = -1)
+// that the kernels skip.  Fills slot -> item.
+void interleave_streams(const std::vector<std::vector<fg::Seg>>& stream, Schedule& sc) {
+  size_t longest = 0;
+  for (auto& st : stream) longest = std::max(longest, st.size());
+  const size_t rounds = (longest + kWavesPerGroup - 1) / kWavesPerGroup;
+  sc.segs.reserve(rounds * kXcds * kWavesPerGroup);
+  const fg::Seg none{-1, 0, 0, -1};
+  for (size_t rd = 0; rd < rounds; ++rd)
+    for (int x = 0; x < kXcds; ++x)
+      for (int w = 0; w < kWavesPerGroup; ++w) {
+        const size_t i = rd * kWavesPerGroup + w;
+        sc.segs.push_back(i < stream[x].size() ? stream[x][i] : none);
+      }
   for (size_t i = 0; i < sc.segs.size(); ++i)
     if (sc.segs[i].slot >= 0) sc.slot_seg[sc.segs[i].slot] = (int32_t)i;
 }
@@ -461,20 +488,53 @@ bool build_partitioned(const int32_t* ip, const int32_t* ix, int64_t num_rows, i
     stream[x].push_back(sg);
     load[x] += (int64_t)sg.end - sg.begin;
   }
-  size_t longest = 0;
-  for (auto& st : stream) longest = std::max(longest, st.size());
-  const size_t rounds = (longest + kWavesPerGroup - 1) / kWavesPerGroup;
-  sc.segs.reserve(rounds * kXcds * kWavesPerGroup);
-  const fg::Seg none{-1, 0, 0, -1};
-  for (size_t rd = 0; rd < rounds; ++rd)
-    for (int x = 0; x < kXcds; ++x)
-      for (int w = 0; w < kWavesPerGroup; ++w) {
-        const size_t i = rd * kWavesPerGroup + w;
-        sc.segs.push_back(i < stream[x].size() ? stream[x][i] : none);
-      }
-  for (size_t i = 0; i < sc.segs.size(); ++i)
-    if (sc.segs[i].slot >= 0) sc.slot_seg[sc.segs[i].slot] = (int32_t)i;
+  interleave_streams(stream, sc);
   return true;
+}
+
+// Die-banded order of a plain schedule (item_order 3, gather schedule only):
+// piece k of a row cut into K pieces goes to die floor(8 (k + 1/2) / K), the
+// eighth of the row its midpoint falls in, if K >= 8; pieces of rows cut
+// into fewer go with the whole rows.  A row's
+// sources are sorted, so the pieces of the long rows that one die runs draw
+// on about one eighth of their source id range, instead of every die
+// gathering from the whole feature matrix at once.  The pieces and their
+// slots are unchanged (so are the results).  Whole rows (and the pieces of
+// rows cut into fewer than 8) go, longest first, to the die with the fewest
+// edges so far; each die runs its items longest first.
+void band_by_die(Schedule& sc) {
+  std::vector<std::vector<fg::Seg>> stream(kXcds);
+  std::vector<int64_t> load(kXcds, 0);
+  std::vector<fg::Seg> rest;
+  for (const fg::Seg& sg : sc.segs) {
+    if (sg.slot < 0) {
+      rest.push_back(sg);
+      continue;
+    }
+    const fg::Fix& fx = sc.fix[(size_t)sc.slot_fix[(size_t)sg.slot]];
+    const int64_t k = sg.slot - fx.slot_begin, K = (int64_t)fx.slot_end - fx.slot_begin;
+    if (K < kXcds) {  // too few pieces to band: balanced with the whole rows
+      rest.push_back(sg);
+      continue;
+    }
+    const int x = (int)((2 * kXcds * k + kXcds) / (2 * K));  // die of the piece's midpoint
+    stream[x].push_back(sg);
+    load[x] += (int64_t)sg.end - sg.begin;
+  }
+  std::stable_sort(rest.begin(), rest.end(), longer);
+  for (auto& sg : rest) {
+    int x = 0;
+    for (int y = 1; y < kXcds; ++y) {
+      const int64_t len = (int64_t)sg.end - sg.begin;
+      if (len > 0 ? load[y] < load[x] : stream[y].size() < stream[x].size()) x = y;
+    }
+    stream[x].push_back(sg);
+    load[x] += (int64_t)sg.end - sg.begin;
+  }
+  for (auto& st : stream) std::stable_sort(st.begin(), st.end(), longer);
+  sc.segs.clear();
+  interleave_streams(stream, sc);
+  sc.banded = true;
 }
 
 fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max_width,
@@ -485,6 +545,7 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
   o->min_deg = 0;
   int32_t slab_opt = 0, min_opt = 0;
   o->order = kOrderAuto;
+  o->band_auto = false;
   o->slab_if_spread = false;
   o->max_backward = false;
   if (opt) {
@@ -492,7 +553,8 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
       if (r != 0) return FG_ERR_INVALID_ARG;
     if (opt->max_backward < 0 || opt->max_backward > 1) return FG_ERR_INVALID_ARG;
     o->max_backward = opt->max_backward == 1;
-    if (opt->item_order < kOrderAuto || opt->item_order > kOrderById) return FG_ERR_INVALID_ARG;
+    if (opt->item_order < kOrderAuto || opt->item_order > kOrderDieBanded)
+      return FG_ERR_INVALID_ARG;
     o->order = opt->item_order;
     if (opt->segment_edges < 0 || opt->segment_edges > kMaxSegmentEdges) return FG_ERR_INVALID_ARG;
     if (opt->max_row_segments < 0 || opt->max_row_segments > kMaxRowSegmentsLimit)
@@ -532,6 +594,11 @@ fg_status make_schedules(const int32_t* ip, const int32_t* ix, int64_t num_rows,
     if (!ix || !build_partitioned(ip, ix, num_rows, num_cols, o, gather)) {
       gather = plain;
       gather.partitioned_rows = 0;
+      bool band = o.order == kOrderDieBanded;
+      if (o.band_auto)
+        for (const fg::Fix& fx : plain.fix)
+          if (fx.slot_end - fx.slot_begin >= kXcds) band = true;
+      if (band) band_by_die(gather);
     }
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
@@ -722,6 +789,7 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
       }
       if (!wins.empty() && hipStreamSynchronize(hs) != hipSuccess) return FG_ERR_HIP;
       o.order = ids_share_sources(ip, wins, win_ix) ? kOrderById : kOrderByLength;
+      o.band_auto = o.order == kOrderByLength;
     }
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
@@ -748,7 +816,7 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
   p->slab_rows = ix ? o.slab : 0;
   p->partition_min_degree = ix ? o.min_deg : 0;
   p->num_partitioned_rows = gather.partitioned_rows;
-  p->item_order = o.order;
+  p->item_order = gather.banded ? kOrderDieBanded : o.order;
   if (hipGetDevice(&p->device) != hipSuccess) {
     delete p;
     return FG_ERR_HIP;

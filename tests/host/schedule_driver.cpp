@@ -163,7 +163,7 @@ void invalid_arguments() {
   CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
         FG_ERR_INVALID_ARG);
   bad = o;
-  bad.item_order = 3;
+  bad.item_order = 4;
   CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
         FG_ERR_INVALID_ARG);
   bad = o;
@@ -211,6 +211,13 @@ void invalid_arguments() {
   CHECK(fg_plan_destroy(nullptr) == FG_ERR_INVALID_ARG);
   fg_plan_info info;
   CHECK(fg_plan_get_info(nullptr, &info) == FG_ERR_INVALID_ARG);
+  uint64_t h1 = 0, h2 = 0;
+  CHECK(fg_indptr_checksum(ip_ok, 2, &h1) == FG_OK);
+  CHECK(fg_indptr_checksum(ip_bad, 2, &h2) == FG_OK && h1 != h2);
+  CHECK(fg_indptr_checksum(nullptr, 2, &h1) == FG_ERR_INVALID_ARG);
+  CHECK(fg_plan_validate(nullptr, &g, ip_ok, nullptr) == FG_ERR_INVALID_ARG);
+  CHECK(fg_gspmm_noalloc(&g, FG_MSG_COPY_SRC, FG_REDUCE_MAX, 1, 4, buf, nullptr, buf + 32,
+                         nullptr, nullptr, nullptr) == FG_ERR_INVALID_ARG);  // max needs arg_eid
   for (int s = -5; s <= 1; ++s) CHECK(fg_status_string((fg_status)s) != nullptr);
   CHECK(fg_abi_version() == FG_ABI_VERSION);
 }
@@ -236,7 +243,7 @@ int main() {
       o.max_row_segments = cap_opts[below(4)];
       o.source_slab_rows = slab_opts[below(5)];
       o.partition_min_degree = min_opts[below(4)];
-      o.item_order = (int32_t)below(3);
+      o.item_order = (int32_t)below(4);
       const int64_t w = widths[below(4)];
       for (int which = 0; which < 2; ++which)
         for (int ind = 0; ind < 2; ++ind) {

@@ -39,6 +39,7 @@ hipError_t launch_gsddmm_softmax_backward(const GraphView&, const PlanView*, con
                                           hipStream_t) {
   return hipErrorNotSupported;
 }
+hipError_t noalloc_scratch(void**) { return hipErrorNotSupported; }
 hipError_t launch_build_eid_pos(const int32_t*, int64_t, int64_t, int32_t*, hipStream_t) {
   return hipErrorNotSupported;
 }

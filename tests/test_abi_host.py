@@ -593,3 +593,42 @@ def test_plan_refuses_a_graph_edited_in_place():
     p.graph.indptr[1] = 2
     with pytest.raises(ValueError, match="modified in place"):
         fg._plan_handle(p)
+
+
+@pytest.mark.parametrize("S", [64, 4096])
+def test_die_banded_schedule(S):
+    """item_order 3: the gather schedule holds the plain schedule's items
+    (same pieces, same slots), piece k of a row cut into K >= 8 runs on die
+    floor(8 (k + 1/2) / K) (workgroup w = item // 4 runs on die w % 8), other
+    items
+    balance the dies' edges, and each die runs its items longest first."""
+    c = synth.make_config("rmat_233k_115m", scale_down=64).csr
+    kw = dict(segment_edges=S)
+    plain, n_split, n_slot = fg.schedule_host(c.indptr, None, c.num_cols, 128, "plain", **kw)
+    band, b_split, b_slot = fg.schedule_host(c.indptr, None, c.num_cols, 128, "gather",
+                                             item_order=3, **kw)
+    assert (n_split, n_slot) == (b_split, b_slot) and n_split > 0
+    pad = band[:, 0] < 0
+    assert np.all(band[pad, 1:] == [0, 0, -1])
+    real = band[~pad]
+    key = lambda a: a[np.lexsort((a[:, 3], a[:, 2], a[:, 1], a[:, 0]))]
+    np.testing.assert_array_equal(key(real), key(plain))
+    die = (np.nonzero(~pad)[0] // 4) % 8
+    # slot ranges per split row: piece k of K
+    slotted = real[:, 3] >= 0
+    rows = real[slotted, 0]
+    first = {}
+    count = {}
+    for r, sl in zip(rows, real[slotted, 3]):
+        first[r] = min(first.get(r, sl), sl)
+        count[r] = count.get(r, 0) + 1
+    k = np.array([sl - first[r] for r, sl in zip(rows, real[slotted, 3])])
+    K = np.array([count[r] for r in rows])
+    banded = K >= 8  # rows of fewer pieces are balanced with the whole rows
+    np.testing.assert_array_equal(die[slotted][banded], ((16 * k + 8) // (2 * K))[banded])
+    lens = real[:, 2] - real[:, 1]
+    load = np.bincount(die, weights=lens, minlength=8)
+    print("die loads", load)
+    assert load.max() - load.min() <= max(lens.max(), 0.02 * load.sum())
+    for x in range(8):
+        assert np.all(np.diff(lens[die == x]) <= 0)

@@ -427,6 +427,8 @@ def plans_for(G, width, sizes=(0, 1, 5, 64)):
         yield fg.Plan(G, max_width=width, segment_edges=s)
     # items by length class, rows in id order within a class
     yield fg.Plan(G, max_width=width, segment_edges=64, item_order=2)
+    # die-banded pieces of long rows (rows of 8+ pieces at 16-edge pieces)
+    yield fg.Plan(G, max_width=width, segment_edges=16, item_order=3)
     # rows cut at source-slab boundaries (8 slabs), pieces of at most 64 edges
     slab = max(1, -(-G.num_cols // 8))
     yield fg.Plan(G, max_width=width, segment_edges=64, source_slab_rows=slab,
@@ -964,10 +966,15 @@ def test_random_configurations(seed):
     if rng.random() < 0.2:
         plan = None
     else:
-        plan = fg.Plan(G, max(F, heads, 1), segment_edges=int(rng.choice([0, 1, 7, 64, 512])),
-                       source_slab_rows=int(rng.choice([0, -1, -2, 37, 500])),
-                       partition_min_degree=int(rng.choice([0, 1, 16])),
-                       item_order=int(rng.integers(0, 3)), max_backward=seed % 2 == 1)
+        seg = int(rng.choice([0, 1, 7, 64, 512]))
+        slab = int(rng.choice([0, -1, -2, 37, 500]))
+        min_deg = int(rng.choice([0, 1, 16]))
+        order = int(rng.integers(0, 3))
+        if order == 1 and seed % 3 == 0:
+            order = 3  # die-banded (drawn this way to keep every seed's other draws)
+        plan = fg.Plan(G, max(F, heads, 1), segment_edges=seg, source_slab_rows=slab,
+                       partition_min_degree=min_deg, item_order=order,
+                       max_backward=seed % 2 == 1)
         say("plan", plan.info())
     nt = nnz_total or g.nnz
     ops = rng.choice(["sum", "mul", "max", "sddmm", "softmax", "softmax_bwd", "max_bwd", "gat",
@@ -1101,6 +1108,25 @@ def test_determinism_and_plan_independence(small_rmat):
     s1 = host(fg.gsddmm(G, tx, tx[: csr.num_rows].contiguous(), plan=plan))
     s2 = host(fg.gsddmm(G, tx, tx[: csr.num_rows].contiguous()))
     np.testing.assert_array_equal(s1.view(np.uint32), s2.view(np.uint32))
+
+
+def test_die_banded_order_gives_identical_results(small_rmat):
+    """The die-banded gather order runs the same pieces with the same slots
+    as longest-first order, so every result is bitwise the same."""
+    csr, G = small_rmat
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((csr.num_cols, 64)).astype(np.float32)
+    w = rng.random(csr.nnz, dtype=np.float32)
+    p1 = fg.Plan(G, 64, segment_edges=16, item_order=1)
+    p3 = fg.Plan(G, 64, segment_edges=16, item_order=3)
+    assert p3.info()["item_order"] == 3 and p3.info()["num_segments"] > p1.info()["num_segments"]
+    tx, tw = dev(x), dev(w)
+    for name, f in (("mul_sum", lambda p: fg.gspmm(G, tx, tw, msg="src_mul_edge", plan=p)),
+                    ("max", lambda p: fg.gspmm(G, tx, reduce="max", plan=p)[0]),
+                    ("sddmm", lambda p: fg.gsddmm(G, tx, tx, plan=p))):
+        say("die-banded vs longest first:", name)
+        np.testing.assert_array_equal(host(f(p3)).view(np.uint32), host(f(p1)).view(np.uint32))
+    check_spmm(csr, G, x, plan=p3, edge=w)
 
 
 def test_plan_bound_to_its_graph(small_rmat):
