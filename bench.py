@@ -36,6 +36,8 @@ METRIC = "gSpMM/SDDMM GFLOP/s and achieved HBM GB/s (% peak), d=128, one MI355X"
 HBM_PEAK_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_rmat_233k_d128.json")
+FLOOR_FILE = os.path.join(ROOT, "profiles", "gather_floor_mi355x.json")
+NUM_CUS = 256
 WORKLOADS = ("rmat_233k_115m", "uniform_deg100_100k", "clustered_133k_deg300",
              "rmat_1m_33m_train", "tiny_uniform_1k", "sage_max_train_rmat_233k",
              "gat_train_clustered_133k", "mlp_rmat_233k", "rand_100k_48m")
@@ -550,6 +552,48 @@ KERNEL_OPS = {  # regular expressions over kernel names; template args <G, NV, U
 }
 
 
+def gather_floor(reps=5):
+    """Cost of one vector-memory gather instruction per compute unit on a
+    cache-resident table (the probe library's fgp_gather_floor): 8 loads in
+    flight per wavefront, 2048 workgroups of 4 wavefronts, 2048 loads each;
+    tables of 32 KiB and 2 MiB; 1 to 64 active lanes.  Prints one JSON line;
+    `floor_ns_per_instruction_per_cu` is the best full-wavefront figure."""
+    import ctypes
+
+    from paper_2008_11359_amd.build import PROBE_LIB
+
+    lib = ctypes.CDLL(PROBE_LIB)
+    f = lib.fgp_gather_floor
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_int] * 5 + [ctypes.POINTER(ctypes.c_float),
+                                       ctypes.POINTER(ctypes.c_ulonglong),
+                                       ctypes.POINTER(ctypes.c_ulonglong)]
+    blocks, iters = 8 * NUM_CUS, 2048
+    runs = []
+    for rows in (64, 4096):
+        for active in (1, 16, 32, 64):
+            ms, ct, rt = ctypes.c_float(), ctypes.c_ulonglong(), ctypes.c_ulonglong()
+            rc = f(rows, blocks, iters, active, reps, ctypes.byref(ms), ctypes.byref(ct),
+                   ctypes.byref(rt))
+            if rc != 0:
+                raise SystemExit("fgp_gather_floor failed (%d)" % rc)
+            instr = blocks * 4 * iters
+            ns = ms.value * 1e6 / (instr / NUM_CUS)
+            ghz = ct.value / (rt.value / 100e6) / 1e9 if rt.value else None
+            runs.append({"table_bytes": rows * 512, "active_lanes": active,
+                         "ms": round(ms.value, 4), "instructions": instr,
+                         "ns_per_instruction_per_cu": round(ns, 4),
+                         "clock_ghz": None if ghz is None else round(ghz, 3),
+                         "cycles_per_instruction": None if ghz is None else round(ns * ghz, 2)})
+            log("gather floor: table %d B, %d lanes: %.3f ns/instr/CU" % (rows * 512, active, ns))
+    full = [r for r in runs if r["active_lanes"] == 64]
+    best = min(full, key=lambda r: r["ns_per_instruction_per_cu"])
+    print(json.dumps({"probe": "fgp_gather_floor (float4 gathers, 1 KiB per instruction)",
+                      "floor_ns_per_instruction_per_cu": best["ns_per_instruction_per_cu"],
+                      "floor_cycles_per_instruction": best["cycles_per_instruction"],
+                      "runs": runs}), flush=True)
+
+
 def _counter_means(csv_dir, counter):
     """Mean value of `counter` per dispatch for each kernel name."""
     import csv
@@ -566,10 +610,13 @@ def _counter_means(csv_dir, counter):
     return {k: sums[k] / counts[k] for k in sums}
 
 
-def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out_json):
+def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out_json,
+                       vmem_dir=None):
     """Per-launch fabric/HBM traffic of each operator of the headline workload
     from FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by the
-    reading of the same counter for the 1 GiB copy of `--copy-probe`."""
+    reading of the same counter for the 1 GiB copy of `--copy-probe`; with
+    `vmem_dir` (a run of TA_FLAT_READ_WAVEFRONTS_sum, TA_TA_BUSY_sum and
+    GRBM_GUI_ACTIVE) also the vector-memory read instructions per launch."""
     from paper_2008_11359_amd.build import source_digest
 
     nbytes = 1 << 30
@@ -591,6 +638,11 @@ def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out
         wb = sel(write) * 1024.0 * w_fac
         ops[op] = {"fetch_bytes": round(fb), "write_bytes": round(wb),
                    "hbm_bytes_per_launch": round(fb + wb)}
+        if vmem_dir:
+            ops[op]["read_instructions"] = round(sel(_counter_means(vmem_dir,
+                                                                    "TA_FLAT_READ_WAVEFRONTS_sum")))
+            ops[op]["ta_busy_cycles"] = round(sel(_counter_means(vmem_dir, "TA_TA_BUSY_sum")))
+            ops[op]["gui_active_cycles"] = round(sel(_counter_means(vmem_dir, "GRBM_GUI_ACTIVE")))
     res = {"source_digest": source_digest(), "fetch_scale": f_fac, "write_scale": w_fac,
            "copy_probe_bytes": nbytes, "ops": ops}
     with open(out_json, "w") as f:
@@ -598,7 +650,10 @@ def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out
     print(json.dumps(res, indent=1))
 
 
-def traffic_for(op_name):
+def counters_for(op_name):
+    """The counter summary of one operator of the headline workload (traffic
+    per launch, and read instructions if taken), or None when the file is
+    missing or was taken with other kernel sources."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     try:
@@ -606,14 +661,106 @@ def traffic_for(op_name):
         from paper_2008_11359_amd.build import source_digest
 
         if tf.get("source_digest") == source_digest() and op_name in tf.get("ops", {}):
-            return tf["ops"][op_name]["hbm_bytes_per_launch"]
+            return tf["ops"][op_name]
         log("traffic file is for other kernel sources: traffic not reported")
     except Exception as exc:  # a stale or malformed file means "not measured"
         log("traffic file ignored:", exc)
     return None
 
 
+def gather_floor_cycles():
+    """Measured gather floor (cycles per instruction per compute unit), or None."""
+    try:
+        return float(json.load(open(FLOOR_FILE))["floor_cycles_per_instruction"])
+    except Exception:
+        return None
+
+
+# the gather path binds when the texture addresser is busy (issuing or
+# stalled on the L1/L2) at least this share of the kernel's cycles
+VMEM_BUSY_BINDS = 0.8
+
+
+def roofline_extras(per_op, op_name, ctr, floor_cycles):
+    """Counter-grounded figures next to the algorithmic roofline of one
+    operator: the rate of the bytes leaving the L2s (an upper bound on its
+    HBM traffic: the counters do not tell Infinity Cache hits from HBM reads)
+    and the vector-memory ceiling: read instructions per launch times the
+    measured per-CU gather floor (cycles), over 256 CUs, against the kernel's
+    own cycles per CU (GRBM_GUI_ACTIVE is summed over the 8 dies)."""
+    t = per_op[op_name]["ms_mean"] / 1e3
+    out = {}
+    if ctr is None:
+        return out
+    tr = ctr["hbm_bytes_per_launch"]
+    out["traffic_gbs"] = round(tr / t / 1e9, 1)
+    out["traffic_frac"] = round(tr / t / 1e9 / HBM_PEAK_GBS, 4)
+    if floor_cycles is not None and ctr.get("read_instructions") and ctr.get("gui_active_cycles"):
+        cyc = ctr["gui_active_cycles"] / 8.0
+        need = ctr["read_instructions"] / NUM_CUS * floor_cycles
+        out["vmem"] = {"read_instructions": ctr["read_instructions"],
+                       "floor_cycles_per_instruction": floor_cycles,
+                       "kernel_cycles_per_cu": round(cyc),
+                       "ceiling_ms": round(t * 1e3 * need / cyc, 4),
+                       "frac": round(need / cyc, 4),
+                       "ta_busy": round(ctr["ta_busy_cycles"] / (NUM_CUS * cyc), 4)}
+    return out
+
+
 # ----------------------------------------------------------------------------
+
+
+def time_ops(torch, dev, ops, K, warmup, cold=False):
+    """`warmup` untimed steps, then K timed steps of every operator in order,
+    each bracketed by HIP events on the launch stream.  Returns the per-op
+    event times (ms) and the wall time of the K steps (with `cold`, a 1 GiB
+    buffer is overwritten before every operator and the wall time is the sum
+    of the operators' event times instead)."""
+    for _ in range(warmup):
+        for op in ops:
+            op.fn()
+    torch.cuda.synchronize()
+    ev = {op.name: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    for _ in range(K)] for op in ops}
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev) if cold else None
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        for op in ops:
+            a, b = ev[op.name][k]
+            if flush is not None:
+                flush.fill_(float(k))
+            a.record()
+            op.fn()
+            b.record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_of = {op.name: [a.elapsed_time(b) for a, b in ev[op.name]] for op in ops}
+    if flush is not None:  # the flushes are not part of the work
+        del flush
+        elapsed = sum(sum(v) for v in ms_of.values()) / 1e3
+    return ms_of, elapsed
+
+
+def simple_graph_rates(args, fg, torch, dev, K):
+    """The headline step on the power-law graph with one copy of each
+    repeated (destination, source) pair: the distinct-edge rate next to the
+    multigraph headline (whose repeats gather rows the caches just served)."""
+    import copy
+
+    a2 = copy.copy(args)
+    a2.simple_graph = True
+    cfg, ops, plans, _, e = setup(args.workload, args.d, a2, fg, torch, dev)
+    ms_of, elapsed = time_ops(torch, dev, ops, K, args.warmup)
+    for p in plans:
+        p.close()
+    res = {"num_edges": e, "ms_per_step": round(elapsed / K * 1e3, 4),
+           "edges_per_s_step": round(e * K / elapsed, 1), "ops": {}}
+    for op in ops:
+        t = float(np.mean(ms_of[op.name])) / 1e3
+        res["ops"][op.name] = {"ms_mean": round(t * 1e3, 4), "edges_per_s": round(e / t, 1),
+                               "gflops": round(op.flop / t / 1e9, 1)}
+    return res
 
 
 def main():
@@ -648,22 +795,36 @@ def main():
                     help="power-law graph workloads: drop the repeated (destination, source) "
                          "pairs of the R-MAT multigraph (31.6%% of its edges) before timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-simple-graph-rate", action="store_true",
+                    help="power-law workload: skip the extra timing on the graph without its "
+                         "repeated edges (reported as simple_graph)")
     ap.add_argument("--cpu-1thread-budget", type=float, default=4.0,
                     help="seconds of single-thread oracle work (0: skip)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration) and exit")
-    ap.add_argument("--summarize-counters", nargs=4,
-                    metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
-                    help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE outputs of the headline "
-                         "workload and of --copy-probe into the traffic file, then exit")
+    ap.add_argument("--summarize-counters", nargs="+",
+                    metavar="DIR",
+                    help="FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR [VMEM_DIR]: turn "
+                         "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE outputs of the headline "
+                         "workload and of --copy-probe (and a TA_FLAT_READ_WAVEFRONTS_sum "
+                         "TA_TA_BUSY_sum GRBM_GUI_ACTIVE run) into the traffic file, then exit")
+    ap.add_argument("--gather-floor", action="store_true",
+                    help="only run the gather-floor probe (cache-resident float4 gathers) and "
+                         "print its JSON line")
     args = ap.parse_args()
     sys.path.insert(0, ROOT)
     if args.copy_probe:
         copy_probe()
         return
     if args.summarize_counters:
-        summarize_counters(*args.summarize_counters, TRAFFIC_FILE)
+        d = args.summarize_counters
+        if len(d) not in (4, 5):
+            raise SystemExit("--summarize-counters takes 4 or 5 directories")
+        summarize_counters(*d[:4], TRAFFIC_FILE, vmem_dir=d[4] if len(d) == 5 else None)
+        return
+    if args.gather_floor:
+        gather_floor()
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library runs on a single MI355X and has no "
@@ -681,42 +842,21 @@ def main():
     torch.cuda.synchronize()
     log("setup %.1fs; plan" % (time.perf_counter() - t0), plans[0].info())
 
-    for _ in range(args.warmup):
-        for op in ops:
-            op.fn()
-    torch.cuda.synchronize()
-
     K = args.steps
-    ev = {op.name: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                    for _ in range(K)] for op in ops}
-    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev) if args.cold else None
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(K):
-        for op in ops:
-            a, b = ev[op.name][k]
-            if flush is not None:
-                flush.fill_(float(k))
-            a.record()
-            op.fn()
-            b.record()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    if flush is not None:  # the flushes are not part of the work
-        del flush
-        elapsed = sum(a.elapsed_time(b) for op in ops for a, b in ev[op.name]) / 1e3
+    ms_of, elapsed = time_ops(torch, dev, ops, K, args.warmup, args.cold)
+    if args.cold:
         cfg["cold"] = True
 
     per_op = {}
     for op in ops:
-        ms = [a.elapsed_time(b) for a, b in ev[op.name]]
+        ms = ms_of[op.name]
         t = float(np.mean(ms)) / 1e3
         per_op[op.name] = {
             "ms_mean": round(float(np.mean(ms)), 4),
             "ms_median": round(float(np.median(ms)), 4),
             "gflops": round(op.flop / t / 1e9, 1),
             "gbs_alg": round(op.bytes / t / 1e9, 1),
-            "frac_hbm": round(op.bytes / t / 1e9 / HBM_PEAK_GBS, 4),
+            "frac_alg": round(op.bytes / t / 1e9 / HBM_PEAK_GBS, 4),
             "bytes_alg": int(op.bytes),
             "edges_per_s": round(e / t, 1),
         }
@@ -725,7 +865,12 @@ def main():
     # dominant kernel: the slowest of the graded operators
     dom = max((op for op in ops if op.graded), key=lambda o: per_op[o.name]["ms_mean"]).name
     ach = per_op[dom]["gbs_alg"]
-    traffic = traffic_for(dom) if args.workload == "rmat_233k_115m" else None
+    headline = args.workload == "rmat_233k_115m" and not args.simple_graph
+    floor_cyc = gather_floor_cycles()
+    ctrs = {o.name: (counters_for(o.name) if headline else None) for o in ops}
+    for name, ctr in ctrs.items():  # counter-grounded figures per operator
+        per_op[name].update(roofline_extras(per_op, name, ctr, floor_cyc))
+    traffic = ctrs[dom]["hbm_bytes_per_launch"] if ctrs[dom] else None
     pinfo = plans[0].info()
     result = {
         "metric": METRIC,
@@ -756,11 +901,42 @@ def main():
                  "slots": pinfo["num_slots"],
                  "partitioned_rows": pinfo["num_partitioned_rows"]},
     }
+    # what `achieved` counts, and the counter-grounded figures beside it
+    rl = result["roofline"]
+    rl["achieved_counts"] = ("algorithmic bytes: one gathered source row per edge plus indices, "
+                             "edge values, destination rows and outputs once; gathers the L2s "
+                             "and the Infinity Cache serve count too, so frac can exceed 1")
+    extra = roofline_extras(per_op, dom, ctrs[dom], floor_cyc)
+    if "traffic_gbs" in extra:
+        rl["traffic_gbs"] = extra["traffic_gbs"]
+        rl["traffic_frac"] = extra["traffic_frac"]
+        rl["traffic_counts"] = ("bytes leaving the L2s per launch (FETCH_SIZE + WRITE_SIZE, "
+                                "scaled by a 1 GiB copy): an upper bound on HBM bytes, as the "
+                                "counters do not separate Infinity Cache hits")
+    if "vmem" in extra:
+        rl["vmem"] = extra["vmem"]
+        rl["binds"] = "vmem" if extra["vmem"]["ta_busy"] >= VMEM_BUSY_BINDS else "hbm"
+        rl["binds_rule"] = ("vmem when the texture addresser is busy (issuing, or stalled on "
+                            "the L1 / L2) at least %.0f%% of the kernel's cycles, else hbm"
+                            % (100 * VMEM_BUSY_BINDS))
     result["hbm_copy_gbs"] = copy_bandwidth(torch)
+    bytes_step = sum(op.bytes for op in ops)
+    if args.workload == "rmat_233k_115m" and not args.simple_graph and \
+            not args.no_simple_graph_rate and not args.cold:
+        # distinct-edge rate: the same step on the graph without repeated pairs
+        del ops
+        for p in plans:
+            p.close()
+        plans = []
+        log("timing the step on the graph without repeated edges")
+        sg = simple_graph_rates(args, fg, torch, dev, min(K, 20))
+        sg["duplicate_share"] = round(1.0 - sg["num_edges"] / e, 4)
+        sg["note"] = ("one copy of each (destination, source) pair of the same R-MAT draw; "
+                      "duplicate_share = stored edges that repeat a pair")
+        result["simple_graph"] = sg
     if not args.no_cpu_baseline:
         # the oracle's rate also as edges/s and algorithmic GB/s of the same
         # step: its FLOP rate times the step's edges and bytes per FLOP
-        bytes_step = sum(op.bytes for op in ops)
 
         def also_per_edge(cb):
             cb["edges_per_s"] = round(cb["value"] * 1e9 * e / flop_step, 1)

@@ -1,4 +1,5 @@
-"""Builds the gfx950 shared library ``_build/libfeatgraph_hip.so`` in-tree.
+"""Builds the gfx950 shared library ``_build/libfeatgraph_hip.so`` in-tree,
+and the measurement probe ``_build/libfg_probe.so`` (bench.py --gather-floor).
 
 Run ``python paper_2008_11359_amd/build.py`` (by path: importing the package
 would load the library it is about to rebuild).  hipcc
@@ -17,6 +18,9 @@ INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(BUILD, "libfeatgraph_hip.so")
 SOURCES = ["fg_kernels.hip", "fg_api.cpp"]
+# measurement probe (bench.py --gather-floor), a library of its own
+PROBE_SOURCE = "fg_probe.hip"
+PROBE_LIB = os.path.join(BUILD, "libfg_probe.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -38,6 +42,8 @@ def source_digest() -> str:
 
     h = hashlib.sha256()
     for name in sorted(os.listdir(CSRC)):
+        if name == PROBE_SOURCE:
+            continue
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
@@ -59,6 +65,12 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    tmp = PROBE_LIB + ".tmp%d" % os.getpid()
+    cmd = [HIPCC] + COMMON + DEVICE + ["-shared", os.path.join(CSRC, PROBE_SOURCE), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 

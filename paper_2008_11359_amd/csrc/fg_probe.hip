@@ -1,0 +1,110 @@
+// fg_probe.hip -- measurement probe, not part of the library's ABI: the
+// per-compute-unit cost of one vector-memory gather instruction when the data
+// is cache-resident, i.e. the floor that the gather path (texture addresser
+// and data return) sets under the sparse kernels whatever the memory
+// hierarchy behind it delivers.  Built into its own shared library
+// (_build/libfg_probe.so) and run by `bench.py --gather-floor`.
+//
+// Each wavefront issues `iters` float4 loads in batches of 8 independent
+// loads; lane l of a wavefront reads float4 (l % 32) of a 512-byte row, so one
+// instruction fetches two rows (1 KiB), the lane layout of the gSpMM / gSDDMM
+// kernels at 128 features.  Rows come from a register hash (no dependent index
+// loads) over a table of `rows` rows that the caches hold.  Only the first
+// `active` lanes load (the rest are masked off), which shows whether the cost
+// is per instruction or per lane.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kBatch = 8;
+
+__global__ __launch_bounds__(kBlock) void gather_floor_kernel(const float4* __restrict__ x,
+                                                              uint32_t row_mask,
+                                                              float4* __restrict__ out,
+                                                              int iters, int active,
+                                                              unsigned long long* clocks) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t wave = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  uint64_t t0 = 0, r0 = 0;
+  const bool timer = blockIdx.x == 0 && threadIdx.x == 0;
+  if (timer) {
+    t0 = __builtin_amdgcn_s_memtime();
+    r0 = __builtin_amdgcn_s_memrealtime();
+  }
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int it = 0; it < iters; it += kBatch) {
+    float4 v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const uint32_t h = (uint32_t)(it + j) * 2654435761u ^ (wave * 2246822519u) ^
+                         ((uint32_t)(lane >> 5) * 3266489917u);
+      const uint32_t row = (h ^ (h >> 15)) & row_mask;
+      v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (lane < active) v[j] = x[(size_t)row * 32 + (lane & 31)];
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      acc.x += v[j].x;
+      acc.y += v[j].y;
+      acc.z += v[j].z;
+      acc.w += v[j].w;
+    }
+  }
+  out[(size_t)blockIdx.x * kBlock + threadIdx.x] = acc;
+  if (timer) {
+    clocks[0] = __builtin_amdgcn_s_memtime() - t0;
+    clocks[1] = __builtin_amdgcn_s_memrealtime() - r0;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+// Runs the probe `reps` times after one warm-up launch: `blocks` workgroups
+// of 4 wavefronts, `iters` loads per wavefront (a multiple of 8), a table of
+// `rows` (a power of two) 512-byte rows.  Writes the mean launch time (ms)
+// and the shader-clock and 100 MHz real-time ticks that wavefront 0 counted
+// during its last launch.  Allocates and frees its own buffers.  0 on success.
+int fgp_gather_floor(int rows, int blocks, int iters, int active, int reps, float* ms_out,
+                     unsigned long long* clock_ticks, unsigned long long* real_ticks) {
+  if (rows < 1 || (rows & (rows - 1)) != 0 || blocks < 1 || iters < kBatch ||
+      iters % kBatch != 0 || active < 1 || active > 64 || reps < 1 || !ms_out)
+    return -1;
+  float4 *x = nullptr, *out = nullptr;
+  unsigned long long* clocks = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = -2;
+  if (hipMalloc(&x, (size_t)rows * 512) != hipSuccess ||
+      hipMalloc(&out, (size_t)blocks * kBlock * sizeof(float4)) != hipSuccess ||
+      hipMalloc(&clocks, 2 * sizeof(unsigned long long)) != hipSuccess ||
+      hipMemset(x, 0, (size_t)rows * 512) != hipSuccess ||
+      hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess)
+    goto done;
+  gather_floor_kernel<<<blocks, kBlock>>>(x, (uint32_t)(rows - 1), out, iters, active, clocks);
+  if (hipEventRecord(e0) != hipSuccess) goto done;
+  for (int r = 0; r < reps; ++r)
+    gather_floor_kernel<<<blocks, kBlock>>>(x, (uint32_t)(rows - 1), out, iters, active, clocks);
+  if (hipEventRecord(e1) != hipSuccess || hipEventSynchronize(e1) != hipSuccess) goto done;
+  {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) goto done;
+    *ms_out = ms / (float)reps;
+    unsigned long long h[2] = {0, 0};
+    if (hipMemcpy(h, clocks, sizeof(h), hipMemcpyDeviceToHost) != hipSuccess) goto done;
+    if (clock_ticks) *clock_ticks = h[0];
+    if (real_ticks) *real_ticks = h[1];
+    rc = hipGetLastError() == hipSuccess ? 0 : -3;
+  }
+done:
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (clocks) (void)hipFree(clocks);
+  if (out) (void)hipFree(out);
+  if (x) (void)hipFree(x);
+  return rc;
+}
+
+}  // extern "C"

@@ -99,3 +99,20 @@ def test_simple_graph_keeps_one_edge_per_pair(bench):
         first.setdefault(pr, q)
     assert np.array_equal(np.nonzero(keep)[0], np.array(sorted(first.values())))
     assert simple.num_rows == csr.num_rows and simple.num_cols == csr.num_cols
+
+
+def test_roofline_extras_from_counters(bench):
+    """Counter-grounded roofline figures: traffic rate and fraction of 8 TB/s,
+    and the vector-memory ceiling from read instructions, the gather floor in
+    cycles and the kernel's cycles per CU."""
+    per_op = {"k": {"ms_mean": 2.0}}
+    # 51.2M instructions / 256 CUs * 16 cycles = 3.2M of the kernel's 4M cycles
+    ctr = {"hbm_bytes_per_launch": 12_000_000_000, "read_instructions": 51_200_000,
+           "gui_active_cycles": 32_000_000, "ta_busy_cycles": 921_600_000}
+    ex = bench.roofline_extras(per_op, "k", ctr, 16.0)
+    assert ex["traffic_gbs"] == 6000.0 and ex["traffic_frac"] == 0.75
+    v = ex["vmem"]
+    assert v["kernel_cycles_per_cu"] == 4_000_000 and v["frac"] == 0.8
+    assert v["ceiling_ms"] == 1.6 and v["ta_busy"] == 0.9
+    assert bench.roofline_extras(per_op, "k", None, 16.0) == {}
+    assert "vmem" not in bench.roofline_extras(per_op, "k", ctr, None)
