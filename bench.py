@@ -588,10 +588,34 @@ def gather_floor(reps=5):
             log("gather floor: table %d B, %d lanes: %.3f ns/instr/CU" % (rows * 512, active, ns))
     full = [r for r in runs if r["active_lanes"] == 64]
     best = min(full, key=lambda r: r["ns_per_instruction_per_cu"])
+    # reads alone: 1 GiB, four times the Infinity Cache, grid-stride
+    rs = lib.fgp_read_stream
+    rs.restype = ctypes.c_int
+    rs.argtypes = [ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
+    reads = []
+    for blk in (2048, 8192, 32768):
+        ms = ctypes.c_float()
+        if rs(1 << 30, blk, reps, ctypes.byref(ms)) != 0:
+            raise SystemExit("fgp_read_stream failed")
+        reads.append({"blocks": blk, "ms": round(ms.value, 4),
+                      "gbs": round((1 << 30) / (ms.value / 1e3) / 1e9, 1)})
+        log("read stream, %d workgroups: %.1f GB/s" % (blk, reads[-1]["gbs"]))
+    rc_ = lib.fgp_read_chunks
+    rc_.restype = ctypes.c_int
+    rc_.argtypes = [ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
+    chunks = []
+    for cb in (4 << 10, 16 << 10, 64 << 10, 256 << 10):
+        ms = ctypes.c_float()
+        if rc_(1 << 30, cb, reps, ctypes.byref(ms)) != 0:
+            raise SystemExit("fgp_read_chunks failed")
+        chunks.append({"chunk_bytes": cb, "ms": round(ms.value, 4),
+                       "gbs": round((1 << 30) / (ms.value / 1e3) / 1e9, 1)})
+        log("read in %d KiB chunks per wavefront: %.1f GB/s" % (cb >> 10, chunks[-1]["gbs"]))
     print(json.dumps({"probe": "fgp_gather_floor (float4 gathers, 1 KiB per instruction)",
                       "floor_ns_per_instruction_per_cu": best["ns_per_instruction_per_cu"],
                       "floor_cycles_per_instruction": best["cycles_per_instruction"],
-                      "runs": runs}), flush=True)
+                      "runs": runs, "read_stream_1gib": reads, "read_chunks_1gib": chunks,
+                      "read_stream_gbs": max(r["gbs"] for r in reads)}), flush=True)
 
 
 def _counter_means(csv_dir, counter):

@@ -713,20 +713,25 @@ fg_status upload(fg_plan* p, const Schedule& sc, fg::PlanView& v, hipStream_t hs
   // leading long items, then short non-empty rows, then empty rows (the
   // plain schedule's order by length class); any other order keeps every item
   // in the first group
-  int64_t nl = 0, nn = 0;
-  bool ordered = true, short_whole = true;
+  int64_t nl = 0, nn = 0, nm = 0;
+  bool ordered = true, short_whole = true, medium_whole = true;
   int prev = INT32_MAX;
   for (const fg::Seg& sg : sc.segs) {
     const int64_t len = (int64_t)sg.end - sg.begin;
     const int cls = len_class(len);
     if (sg.row < 0 || cls > prev) ordered = false;
     prev = cls;
+    if (len > fg::kMediumRowEdges) ++nm;
+    else if (len > fg::kShortRowEdges && sg.slot >= 0) medium_whole = false;
     if (len > fg::kShortRowEdges) ++nl;
     else if (len > 0 && sg.slot >= 0) short_whole = false;  // a piece of a split row
     if (len > 0) ++nn;
   }
+  // (kMediumRowEdges and kShortRowEdges are powers of two, so the length
+  // classes that order the items separate the three groups)
   v.num_nonempty = ordered ? nn : v.num_segments;
   v.num_long = (ordered && short_whole) ? nl : v.num_nonempty;
+  v.num_medium = (ordered && short_whole && medium_whole) ? nm : v.num_long;
   v.num_split_rows = (int64_t)sc.fix.size();
   v.num_slots = (int64_t)sc.slot_fix.size();
   return FG_OK;

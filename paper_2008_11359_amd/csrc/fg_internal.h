@@ -31,13 +31,18 @@ struct PlanView {
   // items are ordered longest first with empty rows last: [0, num_long) have
   // more than kShortRowEdges edges, [num_long, num_nonempty) at most that
   // many (whole rows), the rest none (a partitioned schedule sets both to
-  // num_segments)
-  int64_t num_long = 0, num_nonempty = 0;
+  // num_segments); [num_medium, num_long) are whole rows of more than
+  // kShortRowEdges and at most kMediumRowEdges edges (num_medium == num_long
+  // when the order does not guarantee it)
+  int64_t num_long = 0, num_nonempty = 0, num_medium = 0;
 };
 
 // Rows of at most this many edges are short: the edge softmax packs four of
 // them into one wavefront.
 constexpr int kShortRowEdges = 64;
+// Rows of at most this many edges (and more than kShortRowEdges) also go
+// several to a wavefront: four, with float4 lanes.
+constexpr int kMediumRowEdges = 256;
 
 struct GraphView {
   int64_t num_rows, num_cols, nnz, nnz_total;

@@ -1214,20 +1214,34 @@ __device__ __forceinline__ ContigRange contig_range(int64_t b, int64_t e, int H)
   return r;
 }
 
-// Loads float4 k of the range (leaky ReLU applied); invalid elements get -inf.
+// Loads float4 k of the range as stored (a 16-byte load when it lies inside
+// the range, else element loads); elements outside the range get -inf.  The
+// leaky ReLU is applied apart (contig_leaky), after every load of a batch is
+// issued: applied inside the load's branch, it made the compiler wait for
+// each load before issuing the next, one load in flight per wavefront.
 __device__ __forceinline__ void contig_load(const SoftmaxParams& p, const ContigRange& r,
                                             int64_t k, float (&v)[4]) {
   const int64_t t0 = r.T0 + 4 * k;
   if (t0 >= r.lo && t0 + 4 <= r.hi) {
     load_vec<4>(p.scores + t0, v);
-#pragma unroll
-    for (int c = 0; c < 4; ++c) v[c] = leaky_relu(v[c], p.leaky, p.slope);
   } else {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const int64_t t = t0 + c;
-      v[c] = (t >= r.lo && t < r.hi) ? leaky_relu(p.scores[t], p.leaky, p.slope) : -INFINITY;
+      v[c] = (t >= r.lo && t < r.hi) ? p.scores[t] : -INFINITY;
     }
+  }
+}
+
+// Leaky ReLU of the elements of float4 k that lie inside the range.
+__device__ __forceinline__ void contig_leaky(const SoftmaxParams& p, const ContigRange& r,
+                                             int64_t k, float (&v)[4]) {
+  if (!p.leaky) return;
+  const int64_t t0 = r.T0 + 4 * k;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int64_t t = t0 + c;
+    if (t >= r.lo && t < r.hi) v[c] = leaky_relu(v[c], 1, p.slope);
   }
 }
 
@@ -1321,12 +1335,17 @@ __device__ __forceinline__ void softmax_contig_regs(const SoftmaxParams& p, cons
   float v[kContigRegs][4];
   float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
-  for (int i = 0; i < kContigRegs; ++i) {
+  for (int i = 0; i < kContigRegs; ++i) {  // every load first, then their use
     const int64_t k = lane + (int64_t)kWave * i;
 #pragma unroll
     for (int c = 0; c < 4; ++c) v[i][c] = -INFINITY;
+    if (i < rounds && k < r.K) contig_load(p, r, k, v[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < kContigRegs; ++i) {
+    const int64_t k = lane + (int64_t)kWave * i;
     if (i < rounds) {
-      if (k < r.K) contig_load(p, r, k, v[i]);
+      if (k < r.K) contig_leaky(p, r, k, v[i]);
 #pragma unroll
       for (int c = 0; c < 4; ++c) m[c] = fmaxf(m[c], v[i][c]);
     }
@@ -1360,8 +1379,11 @@ __device__ __forceinline__ void softmax_contig_regs(const SoftmaxParams& p, cons
 }
 
 // Longer rows and segments of split rows: running (max, sum) per slot over the
-// float4s, four in flight; then either publish per-segment statistics or
-// re-read and normalise.
+// float4s, kStreamDepth in flight; then either publish per-segment
+// statistics or re-read and normalise.  Each batch first takes its maximum,
+// rescales the running sum once to it and adds its exponentials: one
+// exponential per value and no divergent branch (a value-by-value running
+// update would take a data-dependent branch per value).
 __device__ __forceinline__ void softmax_contig_stream(const SoftmaxParams& p, const Item& it) {
   const int lane = lane_id();
   const int H = p.H;
@@ -1381,10 +1403,24 @@ __device__ __forceinline__ void softmax_contig_stream(const SoftmaxParams& p, co
       }
     }
 #pragma unroll
-    for (int i = 0; i < kStreamDepth; ++i)
+    for (int i = 0; i < kStreamDepth; ++i) {
+      const int64_t k = k0 + (int64_t)kWave * i;
+      if (k < r.K) contig_leaky(p, r, k, v[i]);
+    }
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (v[i][c] != -INFINITY) lse_push(m[c], z[c], v[i][c]);
+    for (int c = 0; c < 4; ++c) {
+      float bm = v[0][c];
+#pragma unroll
+      for (int i = 1; i < kStreamDepth; ++i) bm = fmaxf(bm, v[i][c]);
+      const float nm = fmaxf(m[c], bm);
+      if (nm == -INFINITY) continue;  // nothing but padding so far
+      // exp(-inf) = 0 covers an empty running sum and padded values
+      float acc = z[c] * exp_nonpos(m[c] - nm);
+#pragma unroll
+      for (int i = 0; i < kStreamDepth; ++i) acc += exp_nonpos(v[i][c] - nm);
+      z[c] = acc;
+      m[c] = nm;
+    }
   }
   contig_alllse(m, z, H);
   if (it.slot >= 0) {
@@ -1414,6 +1450,7 @@ __device__ __forceinline__ void softmax_contig_stream(const SoftmaxParams& p, co
     for (int i = 0; i < kStreamDepth; ++i) {
       const int64_t k = k0 + (int64_t)kWave * i;
       if (k < r.K) {
+        contig_leaky(p, r, k, v[i]);
         float o[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) o[c] = expf(v[i][c] - m[c]) * inv[c];
@@ -1604,6 +1641,7 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
       for (int i = 0; i < kStreamDepth; ++i) {
         const int64_t k = k0 + (int64_t)kWave * i;
         if (k < r.K) {
+          contig_leaky(p, r, k, v[i]);
           float o[4];
 #pragma unroll
           for (int c = 0; c < 4; ++c) o[c] = expf(v[i][c] - m[c]) * inv[c];
@@ -2503,6 +2541,73 @@ __global__ __launch_bounds__(kBlock) void softmax_pack_kernel(SoftmaxParams p, i
     if (ev[k] >= 0) p.out[ev[k]] = v[k] * inv;
 }
 
+// Whole rows of kShortRowEdges + 1 .. kMediumRowEdges edges, one head, scores
+// contiguous (edge id = position): four rows per wavefront, kPackLanes lanes
+// each; lane j of a row's group holds float4 j, j + 16, ... of the row's
+// range aligned down to 16 bytes (at most 66 float4 for 256 edges, so
+// kPack4Vec = 5 per lane covers it).  Exact maximum, one expf per value, one
+// read and one write, like the register path of one row per wavefront.
+constexpr int kPack4Vec = 5;
+static_assert(kMediumRowEdges + 6 <= kPackLanes * kPack4Vec * 4,
+              "a medium row's aligned float4 range must fit one quarter");
+
+__global__ __launch_bounds__(kBlock) void softmax_pack4_kernel(SoftmaxParams p, int64_t first,
+                                                               int64_t last) {
+  const int64_t w = wave_item();
+  const int64_t item0 = first + w * (kWave / kPackLanes);
+  if (item0 >= last) return;
+  const int lane = lane_id();
+  const int64_t item = item0 + lane / kPackLanes;
+  const int j = lane % kPackLanes;
+  int64_t b = 0, e = 0;
+  if (item < last) {
+    const Seg sg = p.segs[item];
+    b = sg.begin;
+    e = sg.end;
+  }
+  const ContigRange r = contig_range(b, e, 1);
+  float v[kPack4Vec][4];
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kPack4Vec; ++i) {
+    const int64_t k = j + (int64_t)kPackLanes * i;
+    if (k < r.K) {
+      contig_load(p, r, k, v[i]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) v[i][c] = -INFINITY;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kPack4Vec; ++i) {
+    const int64_t k = j + (int64_t)kPackLanes * i;
+    if (k < r.K) contig_leaky(p, r, k, v[i]);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) m = fmaxf(m, v[i][c]);
+  }
+  for (int off = 1; off < kPackLanes; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
+  float z = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kPack4Vec; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      v[i][c] = v[i][c] == -INFINITY ? 0.0f : expf(v[i][c] - m);
+      z += v[i][c];
+    }
+  for (int off = 1; off < kPackLanes; off <<= 1) z += __shfl_xor(z, off);
+  const float inv = 1.0f / z;
+#pragma unroll
+  for (int i = 0; i < kPack4Vec; ++i) {
+    const int64_t k = j + (int64_t)kPackLanes * i;
+    if (k < r.K) {
+      float o[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) o[c] = v[i][c] * inv;
+      contig_store(p, r, k, o);
+    }
+  }
+}
+
 // ----------------------------------------------------------------------------
 // fused attention aggregation: SDDMM -> leaky ReLU -> edge softmax -> gSpMM
 // ----------------------------------------------------------------------------
@@ -3173,14 +3278,24 @@ hipError_t launch_edge_softmax(const GraphView& g, const PlanView* plan, int64_t
                 aligned16(out)) ? 1 : 0;
   prm.self_merge = (prm.contig && H == 1) ? 1 : 0;
   // with a plan: empty rows (last) need no work; short single-head rows go
-  // four to a wavefront
+  // four to a wavefront, and so do medium rows with contiguous scores
   const bool pack = plan && H == 1 && plan->num_long < plan->num_nonempty;
-  if (plan) prm.n_items = pack ? plan->num_long : plan->num_nonempty;
+  const bool pack4 = plan && H == 1 && prm.contig && plan->num_medium < plan->num_long;
+  if (plan)
+    prm.n_items = pack4 ? plan->num_medium : (pack ? plan->num_long : plan->num_nonempty);
   hipError_t err = hipSuccess;
   if (prm.n_items > 0) {
     const dim3 grid = grid_for(prm.n_items, 1);
     if (plan) FG_LAUNCH((softmax_kernel<true>), grid, stream, prm);
     else FG_LAUNCH((softmax_kernel<false>), grid, stream, prm);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  if (pack4) {
+    const int64_t rows = plan->num_long - plan->num_medium;
+    const int64_t per = kWave / kPackLanes;
+    FG_LAUNCH(softmax_pack4_kernel, grid_for((rows + per - 1) / per, 1), stream, prm,
+              plan->num_medium, plan->num_long);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
   }

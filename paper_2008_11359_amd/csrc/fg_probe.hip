@@ -3,7 +3,8 @@
 // is cache-resident, i.e. the floor that the gather path (texture addresser
 // and data return) sets under the sparse kernels whatever the memory
 // hierarchy behind it delivers.  Built into its own shared library
-// (_build/libfg_probe.so) and run by `bench.py --gather-floor`.
+// (_build/libfg_probe.so) and run by `bench.py --gather-floor`, which also
+// times a read-only stream over a buffer four times the Infinity Cache.
 //
 // Each wavefront issues `iters` float4 loads in batches of 8 independent
 // loads; lane l of a wavefront reads float4 (l % 32) of a 512-byte row, so one
@@ -13,6 +14,7 @@
 // `active` lanes load (the rest are masked off), which shows whether the cost
 // is per instruction or per lane.
 #include <hip/hip_runtime.h>
+#include <limits.h>
 #include <stdint.h>
 
 namespace {
@@ -59,9 +61,136 @@ __global__ __launch_bounds__(kBlock) void gather_floor_kernel(const float4* __re
   }
 }
 
+// Read-only stream: every thread sums its float4s of a large buffer
+// (grid-stride, 8 loads in flight); the attainable rate of reads alone.
+__global__ __launch_bounds__(kBlock) void read_stream_kernel(const float4* __restrict__ x,
+                                                             size_t n, float4* __restrict__ out) {
+  const size_t stride = (size_t)gridDim.x * kBlock;
+  size_t i = (size_t)blockIdx.x * kBlock + threadIdx.x;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (; i + (kBatch - 1) * stride < n; i += kBatch * stride) {
+    float4 v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) v[j] = x[i + j * stride];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      acc.x += v[j].x;
+      acc.y += v[j].y;
+      acc.z += v[j].z;
+      acc.w += v[j].w;
+    }
+  }
+  for (; i < n; i += stride) {
+    const float4 v = x[i];
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  out[(size_t)blockIdx.x * kBlock + threadIdx.x] = acc;
+}
+
+// Chunked read: wavefront w reads float4s [w * chunk, (w + 1) * chunk) of the
+// buffer, 8 per lane in flight, then exits (the access pattern of a kernel
+// that gives each wavefront one contiguous range).
+__global__ __launch_bounds__(kBlock) void read_chunks_kernel(const float4* __restrict__ x,
+                                                             size_t n, size_t chunk,
+                                                             float4* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const size_t wave = (size_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  const size_t b = wave * chunk;
+  const size_t e = b + chunk < n ? b + chunk : n;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (size_t k0 = b + lane; k0 < e; k0 += kBatch * 64) {
+    float4 v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const size_t k = k0 + (size_t)j * 64;
+      v[j] = k < e ? x[k] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      acc.x += v[j].x;
+      acc.y += v[j].y;
+      acc.z += v[j].z;
+      acc.w += v[j].w;
+    }
+  }
+  out[(size_t)blockIdx.x * kBlock + threadIdx.x] = acc;
+}
+
 }  // namespace
 
 extern "C" {
+
+// Reads a buffer of `bytes` in contiguous chunks of `chunk_bytes` (both
+// multiples of 16), one per wavefront, `reps` times after a warm-up; writes
+// the mean time per pass (ms).  Allocates and frees its own buffers.
+int fgp_read_chunks(size_t bytes, size_t chunk_bytes, int reps, float* ms_out) {
+  if (bytes < 16 || bytes % 16 != 0 || chunk_bytes < 16 || chunk_bytes % 16 != 0 || reps < 1 ||
+      !ms_out)
+    return -1;
+  const size_t n = bytes / 16, chunk = chunk_bytes / 16;
+  const size_t waves = (n + chunk - 1) / chunk;
+  const size_t blocks = (waves + 3) / 4;
+  if (blocks > (size_t)INT32_MAX) return -1;
+  float4 *x = nullptr, *out = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = -2;
+  if (hipMalloc(&x, bytes) != hipSuccess ||
+      hipMalloc(&out, blocks * kBlock * sizeof(float4)) != hipSuccess ||
+      hipMemset(x, 0, bytes) != hipSuccess || hipEventCreate(&e0) != hipSuccess ||
+      hipEventCreate(&e1) != hipSuccess)
+    goto done;
+  read_chunks_kernel<<<(unsigned)blocks, kBlock>>>(x, n, chunk, out);
+  if (hipEventRecord(e0) != hipSuccess) goto done;
+  for (int r = 0; r < reps; ++r) read_chunks_kernel<<<(unsigned)blocks, kBlock>>>(x, n, chunk, out);
+  if (hipEventRecord(e1) != hipSuccess || hipEventSynchronize(e1) != hipSuccess) goto done;
+  {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) goto done;
+    *ms_out = ms / (float)reps;
+    rc = hipGetLastError() == hipSuccess ? 0 : -3;
+  }
+done:
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (out) (void)hipFree(out);
+  if (x) (void)hipFree(x);
+  return rc;
+}
+
+// Reads a buffer of `bytes` (a multiple of 16) `reps` times after one
+// warm-up pass with `blocks` workgroups; writes the mean time per pass (ms).
+// Allocates and frees its own buffers.  0 on success.
+int fgp_read_stream(size_t bytes, int blocks, int reps, float* ms_out) {
+  if (bytes < 16 || bytes % 16 != 0 || blocks < 1 || reps < 1 || !ms_out) return -1;
+  float4 *x = nullptr, *out = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = -2;
+  const size_t n = bytes / 16;
+  if (hipMalloc(&x, bytes) != hipSuccess ||
+      hipMalloc(&out, (size_t)blocks * kBlock * sizeof(float4)) != hipSuccess ||
+      hipMemset(x, 0, bytes) != hipSuccess || hipEventCreate(&e0) != hipSuccess ||
+      hipEventCreate(&e1) != hipSuccess)
+    goto done;
+  read_stream_kernel<<<blocks, kBlock>>>(x, n, out);
+  if (hipEventRecord(e0) != hipSuccess) goto done;
+  for (int r = 0; r < reps; ++r) read_stream_kernel<<<blocks, kBlock>>>(x, n, out);
+  if (hipEventRecord(e1) != hipSuccess || hipEventSynchronize(e1) != hipSuccess) goto done;
+  {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) goto done;
+    *ms_out = ms / (float)reps;
+    rc = hipGetLastError() == hipSuccess ? 0 : -3;
+  }
+done:
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (out) (void)hipFree(out);
+  if (x) (void)hipFree(x);
+  return rc;
+}
 
 // Runs the probe `reps` times after one warm-up launch: `blocks` workgroups
 // of 4 wavefronts, `iters` loads per wavefront (a multiple of 8), a table of
