@@ -611,10 +611,23 @@ def gather_floor(reps=5):
         chunks.append({"chunk_bytes": cb, "ms": round(ms.value, 4),
                        "gbs": round((1 << 30) / (ms.value / 1e3) / 1e9, 1)})
         log("read in %d KiB chunks per wavefront: %.1f GB/s" % (cb >> 10, chunks[-1]["gbs"]))
+    sr = lib.fgp_scatter_runs
+    sr.restype = ctypes.c_int
+    sr.argtypes = [ctypes.c_int] * 5 + [ctypes.POINTER(ctypes.c_float)]
+    scat = []
+    total = 28_000_000  # the records of the power-law graph's max backward at d = 128
+    for bins in (64, 256, 1820):
+        per = total // 256
+        ms = ctypes.c_float()
+        if sr(256, per, bins, int(per / bins * 1.3) + 64, reps, ctypes.byref(ms)) != 0:
+            raise SystemExit("fgp_scatter_runs failed")
+        scat.append({"groups": 256, "bins": bins, "records": per * 256, "ms": round(ms.value, 4)})
+        log("scatter of 8-byte records from 256 groups into %d bins: %.3f ms" % (bins, ms.value))
     print(json.dumps({"probe": "fgp_gather_floor (float4 gathers, 1 KiB per instruction)",
                       "floor_ns_per_instruction_per_cu": best["ns_per_instruction_per_cu"],
                       "floor_cycles_per_instruction": best["cycles_per_instruction"],
                       "runs": runs, "read_stream_1gib": reads, "read_chunks_1gib": chunks,
+                      "scatter_runs": scat,
                       "read_stream_gbs": max(r["gbs"] for r in reads)}), flush=True)
 
 

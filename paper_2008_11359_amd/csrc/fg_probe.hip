@@ -119,9 +119,64 @@ __global__ __launch_bounds__(kBlock) void read_chunks_kernel(const float4* __res
   out[(size_t)blockIdx.x * kBlock + threadIdx.x] = acc;
 }
 
+// Scattered 8-byte record writes, the pattern of a counting-sort scatter:
+// `groups` workgroups of 1024 threads each own `per_group` consecutive
+// elements; element i goes to bin hash(i) % bins, at the next position of its
+// group's run in that bin (ranked by an LDS atomic).  Runs have a fixed
+// capacity `cap` (records beyond it are dropped), laid out bin-major, so the
+// runs of one bin are adjacent as in the real sort.
+__global__ __launch_bounds__(1024) void scatter_runs_kernel(int2* __restrict__ rec, int per_group,
+                                                            int bins, int cap) {
+  extern __shared__ int32_t cnt[];
+  for (int b = threadIdx.x; b < bins; b += 1024) cnt[b] = 0;
+  __syncthreads();
+  const int64_t first = (int64_t)blockIdx.x * per_group;
+  for (int t = threadIdx.x; t < per_group; t += 1024) {
+    const uint32_t i = (uint32_t)(first + t);
+    uint32_t h = i * 2654435761u;
+    h ^= h >> 16;
+    h *= 2246822519u;
+    h ^= h >> 13;
+    const int b = (int)(h % (uint32_t)bins);
+    const int r = atomicAdd(&cnt[b], 1);
+    if (r < cap)
+      rec[((int64_t)b * gridDim.x + blockIdx.x) * cap + r] = make_int2((int)i, (int)h);
+  }
+}
+
 }  // namespace
 
 extern "C" {
+
+// Times scatter_runs_kernel (`reps` launches after one warm-up); the record
+// array holds groups * bins * cap records.  Allocates and frees its buffers.
+int fgp_scatter_runs(int groups, int per_group, int bins, int cap, int reps, float* ms_out) {
+  if (groups < 1 || per_group < 1 || bins < 1 || bins > 16384 || cap < 1 || reps < 1 || !ms_out)
+    return -1;
+  int2* rec = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = -2;
+  const size_t n = (size_t)groups * bins * cap;
+  if (hipMalloc(&rec, n * sizeof(int2)) != hipSuccess || hipEventCreate(&e0) != hipSuccess ||
+      hipEventCreate(&e1) != hipSuccess)
+    goto done;
+  scatter_runs_kernel<<<groups, 1024, (size_t)bins * 4>>>(rec, per_group, bins, cap);
+  if (hipEventRecord(e0) != hipSuccess) goto done;
+  for (int r = 0; r < reps; ++r)
+    scatter_runs_kernel<<<groups, 1024, (size_t)bins * 4>>>(rec, per_group, bins, cap);
+  if (hipEventRecord(e1) != hipSuccess || hipEventSynchronize(e1) != hipSuccess) goto done;
+  {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) goto done;
+    *ms_out = ms / (float)reps;
+    rc = hipGetLastError() == hipSuccess ? 0 : -3;
+  }
+done:
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (rec) (void)hipFree(rec);
+  return rc;
+}
 
 // Reads a buffer of `bytes` in contiguous chunks of `chunk_bytes` (both
 // multiples of 16), one per wavefront, `reps` times after a warm-up; writes
