@@ -489,9 +489,11 @@ def _cpu_baseline(oracle_sample, budget_s, threads):
         total_t += dt
         total_f += flop
         reps += 1
+    import oracle.fgref as fgref
+
     return {"value": round(total_f / total_t / 1e9, 3), "unit": "GFLOP/s", "cores": threads,
             "kind": "oracle", "sample": "%s; %d passes, %.1f s" % (desc, reps, total_t),
-            "host": _host()}
+            "host": _host(), "build": "gcc " + " ".join(fgref.BUILD_FLAGS)}
 
 
 def _host():

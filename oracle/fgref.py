@@ -30,13 +30,17 @@ def lib_path() -> str:
     return _LIB
 
 
+# Portable flags (no -march=native): the library is built once and may run
+# on a host with another CPU model.
+BUILD_FLAGS = ["-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math"]
+
+
 def compile_oracle(src: str, out: str) -> str:
     """gcc build of an oracle source file into a shared library."""
     os.makedirs(os.path.dirname(out), exist_ok=True)
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
-           "-fno-fast-math", "-Wall", "-Wextra", "-Wno-unused-parameter",
-           "-o", tmp, src, "-lm"]
+    cmd = ["gcc"] + BUILD_FLAGS + ["-fPIC", "-shared", "-Wall", "-Wextra",
+                                   "-Wno-unused-parameter", "-o", tmp, src, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
     return out
