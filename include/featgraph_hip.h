@@ -111,9 +111,12 @@ typedef struct fg_graph {
  * partitioning) for the caches of each MI355X die.
  *
  * A plan holds two schedules over one workspace:
- *  - plain (edge softmax): rows with more than S = segment_edges edges are
- *    cut into k = min(ceil(deg / S), max_row_segments) equal segments; long
- *    items first (fg_plan_options.item_order), rows without edges last;
+ *  - plain (edge softmax): rows with more than S edges are cut into
+ *    k = min(ceil(deg / S), max_row_segments) equal segments, S =
+ *    segment_edges if given, else 16384 (a whole row of up to 16384 scores
+ *    is streamed by one wavefront; a cut row is read once more by a merge
+ *    pass); long items first (fg_plan_options.item_order), rows without
+ *    edges last;
  *  - gather (gSpMM, gSDDMM, fused attention): as plain, unless source
  *    partitioning applies (by default once the num_cols x max_width source
  *    features exceed 128 MiB, half the Infinity Cache, or 32 MiB when the
@@ -137,7 +140,8 @@ typedef struct fg_graph {
 typedef struct fg_plan fg_plan; /* opaque; owns device schedules + workspace */
 
 typedef struct fg_plan_options {
-  int32_t segment_edges;        /* S: target edges per item; 0 -> default (4096)     */
+  int32_t segment_edges;        /* S: target edges per item; 0 -> default (4096 for
+                                   the gather schedule, 16384 for the plain one)    */
   int32_t max_row_segments;     /* cap on items per row (plain cut); 0 -> 128        */
   int32_t source_slab_rows;     /* source ids per slab of the gather schedule;
                                    0 -> automatic slabs if the num_cols x

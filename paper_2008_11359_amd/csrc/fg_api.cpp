@@ -42,6 +42,11 @@ static_assert(fg::kNoAllocScratchBytes == FG_NOALLOC_SCRATCH_BYTES,
 namespace {
 
 constexpr int32_t kDefaultSegmentEdges = 4096;
+// The plain schedule (edge softmax) cuts only rows longer than this by
+// default: a whole row of up to 16,384 scores is streamed by one wavefront
+// (read twice, the second time mostly from the L2), while a cut row passes
+// its statistics to a second kernel that reads it again from memory.
+constexpr int32_t kDefaultPlainSegmentEdges = 16384;
 constexpr int32_t kMaxSegmentEdges = 1 << 24;
 constexpr int32_t kDefaultMaxRowSegments = 128;
 constexpr int32_t kMaxRowSegmentsLimit = 1 << 20;
@@ -239,6 +244,7 @@ constexpr int64_t kDieL2Bytes = 4 << 20;
 
 struct Options {
   int32_t S, cap, slab, min_deg;  // slab 0: no source partitioning
+  int32_t S_plain;                // segment length of the plain (edge softmax) schedule
   int32_t order;                  // item order: 0 automatic, 1 by length, 2 by class + id,
                                   // 3 die-banded gather schedule
   bool band_auto;                 // automatic order settled on 1: band the gather schedule
@@ -540,6 +546,7 @@ void band_by_die(Schedule& sc) {
 fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max_width,
                        Options* o) {
   o->S = kDefaultSegmentEdges;
+  o->S_plain = kDefaultPlainSegmentEdges;
   o->cap = kDefaultMaxRowSegments;
   o->slab = 0;
   o->min_deg = 0;
@@ -561,7 +568,7 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
       return FG_ERR_INVALID_ARG;
     if (opt->partition_min_degree < 0) return FG_ERR_INVALID_ARG;
     if (opt->source_slab_rows < kSlabsOff) return FG_ERR_INVALID_ARG;
-    if (opt->segment_edges) o->S = opt->segment_edges;
+    if (opt->segment_edges) o->S = o->S_plain = opt->segment_edges;
     if (opt->max_row_segments) o->cap = opt->max_row_segments;
     slab_opt = opt->source_slab_rows;
     min_opt = opt->partition_min_degree;
@@ -590,13 +597,20 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
 fg_status make_schedules(const int32_t* ip, const int32_t* ix, int64_t num_rows, int64_t num_cols,
                          const Options& o, Schedule& gather, Schedule& plain) {
   try {
-    build_plain(ip, num_rows, o, plain);
+    Options op = o;
+    op.S = o.S_plain;
+    build_plain(ip, num_rows, op, plain);
     if (!ix || !build_partitioned(ip, ix, num_rows, num_cols, o, gather)) {
-      gather = plain;
+      if (o.S_plain == o.S) {
+        gather = plain;
+      } else {
+        gather = Schedule();
+        build_plain(ip, num_rows, o, gather);
+      }
       gather.partitioned_rows = 0;
       bool band = o.order == kOrderDieBanded;
       if (o.band_auto)
-        for (const fg::Fix& fx : plain.fix)
+        for (const fg::Fix& fx : gather.fix)
           if (fx.slot_end - fx.slot_begin >= kXcds) band = true;
       if (band) band_by_die(gather);
     }
