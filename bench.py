@@ -130,7 +130,9 @@ def setup(name, d, args, fg, torch, dev):
     n, e = csr.num_rows, csr.nnz
     log("workload %s: N=%d E=%d generated in %.1fs" % (name, n, e, t_gen))
     G = fg.Graph.from_csr(csr, device=dev)
-    popt = dict(segment_edges=args.segment_edges, max_row_segments=args.max_row_segments,
+    popt = dict(segment_edges=args.segment_edges,
+                softmax_segment_edges=args.softmax_segment_edges,
+                max_row_segments=args.max_row_segments,
                 source_slab_rows=args.source_slab_rows,
                 partition_min_degree=args.partition_min_degree, item_order=args.item_order)
     T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
@@ -810,6 +812,9 @@ def main():
     ap.add_argument("--workload", default="rmat_233k_115m", choices=WORKLOADS)
     ap.add_argument("--d", type=int, default=None, help="feature width (uniform workload)")
     ap.add_argument("--segment-edges", type=int, default=0, help="plan segment length (0: default)")
+    ap.add_argument("--softmax-segment-edges", type=int, default=0,
+                    help="segment length of the edge-softmax schedule (0: --segment-edges if "
+                         "given, else the library default)")
     ap.add_argument("--max-row-segments", type=int, default=0,
                     help="cap on segments per row (0: default)")
     ap.add_argument("--source-slab-rows", type=int, default=0,

@@ -113,11 +113,12 @@ typedef struct fg_graph {
  * A plan holds two schedules over one workspace:
  *  - plain (edge softmax): rows with more than S edges are cut into
  *    k = min(ceil(deg / S), max_row_segments) equal segments, S =
- *    segment_edges if given, else 16384 (a whole row of up to 16384 scores
- *    is streamed by one wavefront; a cut row is read once more by a merge
- *    pass); long items first (fg_plan_options.item_order), rows without
- *    edges last;
- *  - gather (gSpMM, gSDDMM, fused attention): as plain, unless source
+ *    softmax_segment_edges if given, else segment_edges if given, else 16384
+ *    (a whole row of up to 16384 scores is streamed by one wavefront; a cut
+ *    row is read once more by a merge pass); long items first
+ *    (fg_plan_options.item_order), rows without edges last;
+ *  - gather (gSpMM, gSDDMM, fused attention): as plain with S =
+ *    segment_edges if given, else 2048, unless source
  *    partitioning applies (by default once the num_cols x max_width source
  *    features exceed 128 MiB, half the Infinity Cache, or 32 MiB when the
  *    gathers are spread; see fg_plan_options.source_slab_rows).  With it,
@@ -140,7 +141,7 @@ typedef struct fg_graph {
 typedef struct fg_plan fg_plan; /* opaque; owns device schedules + workspace */
 
 typedef struct fg_plan_options {
-  int32_t segment_edges;        /* S: target edges per item; 0 -> default (4096 for
+  int32_t segment_edges;        /* S: target edges per item; 0 -> default (2048 for
                                    the gather schedule, 16384 for the plain one)    */
   int32_t max_row_segments;     /* cap on items per row (plain cut); 0 -> 128        */
   int32_t source_slab_rows;     /* source ids per slab of the gather schedule;
@@ -166,18 +167,23 @@ typedef struct fg_plan_options {
                                    in id order within a class; 3 -> die-banded
                                    gather schedule (unless source slabs apply):
                                    the same items as 1, but piece k of a row cut
-                                   into K >= 8 pieces runs on die
-                                   floor(8 (k + 1/2) / K), so each die gathers from
-                                   one eighth of those rows' sources; the other
-                                   items balance the dies' edges (edge softmax
-                                   keeps order 1); results equal those of 1   */
+                                   into K pieces runs on die floor(8 (k + 1/2) /
+                                   K) if K >= 8, else on one of the dies
+                                   [floor(8k / K), ceil(8(k + 1) / K)) (the
+                                   pieces sharing such a span take its dies in
+                                   turn), so each die gathers from one eighth
+                                   of those rows' sources; whole rows balance
+                                   the dies' edges (edge softmax keeps order
+                                   1); results equal those of 1               */
   int32_t max_backward;         /* 1 -> also reserve the workspace of the binned
                                    gSpMM-max backward: 8 bytes per element of a
                                    num_rows x max_width gradient (that product must
                                    not exceed 2^31 - 1, else FG_ERR_UNSUPPORTED)
                                    plus bin tables (128 KiB, and 1 KiB per source
                                    tile, at most 8 MiB); 0 -> none (default)       */
-  int32_t reserved[2];          /* must be zero                                      */
+  int32_t softmax_segment_edges;/* S of the plain schedule; 0 -> segment_edges if that
+                                   is given, else 16384                             */
+  int32_t reserved[1];          /* must be zero                                      */
 } fg_plan_options;
 
 typedef struct fg_plan_info {

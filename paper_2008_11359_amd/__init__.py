@@ -60,7 +60,7 @@ class _PlanOptions(ctypes.Structure):
     _fields_ = [("segment_edges", ctypes.c_int32), ("max_row_segments", ctypes.c_int32),
                 ("source_slab_rows", ctypes.c_int32), ("partition_min_degree", ctypes.c_int32),
                 ("item_order", ctypes.c_int32), ("max_backward", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 2)]
+                ("softmax_segment_edges", ctypes.c_int32), ("reserved", ctypes.c_int32 * 1)]
 
 
 class _PlanInfo(ctypes.Structure):
@@ -256,7 +256,9 @@ def _check_host_csr(num_rows, num_cols, indptr, indices, eids, nnz_total):
 
 class Plan:
     """Degree-aware schedules of one graph (see fg_plan_create): rows longer
-    than ``segment_edges`` are cut into equal pieces (at most
+    than ``segment_edges`` (default 2048 edges in the gather schedule of
+    gSpMM / gSDDMM, 16,384 in the edge-softmax schedule, which
+    ``softmax_segment_edges`` sets apart) are cut into equal pieces (at most
     ``max_row_segments``); long rows of the gather schedule may also be cut
     at source-slab boundaries, so that each die gathers from a narrow band of
     the features.  ``source_slab_rows``: 0 (default) automatic slabs once the
@@ -265,9 +267,9 @@ class Plan:
     they exceed 32 MiB; -2 never; > 0 that many source ids per slab.  ``item_order``: 1 longest
     item first, 2 by power-of-two length class with rows in id order (keeps
     the locality of graphs whose neighbouring ids share sources), 3 the items
-    of 1 with the pieces of rows cut into 8 or more dealt to the dies by
-    position in the row (each die gathers from one eighth of their sources;
-    same results as 1), 0 (default) picks 2 for such graphs and otherwise 3
+    of 1 with the pieces of split rows dealt to the dies by position in the
+    row (each die gathers from about one eighth of their sources; same
+    results as 1), 0 (default) picks 2 for such graphs and otherwise 3
     if some row is cut into 8 or more pieces, else 1.  Partial-result
     workspace for features up to ``max_width`` floats.  ``max_backward``:
     also hold the workspace with which gspmm_max_backward bins the gradient
@@ -278,9 +280,9 @@ class Plan:
     def __init__(self, g: Graph, max_width: int, segment_edges: int = 0,
                  max_row_segments: int = 0, source_slab_rows: int = 0,
                  partition_min_degree: int = 0, item_order: int = 0,
-                 max_backward: bool = False):
+                 max_backward: bool = False, softmax_segment_edges: int = 0):
         opt = _options(segment_edges, max_row_segments, source_slab_rows, partition_min_degree,
-                       item_order, max_backward)
+                       item_order, max_backward, softmax_segment_edges)
         h = ctypes.c_void_p()
         ip, ix = g.indptr_host, g.indices_host
         st = _lib.fg_plan_create(ctypes.byref(g._c), None if ip is None else ip.ctypes.data,
@@ -336,7 +338,7 @@ class Plan:
 
 def _options(segment_edges: int = 0, max_row_segments: int = 0, source_slab_rows: int = 0,
              partition_min_degree: int = 0, item_order: int = 0,
-             max_backward: bool = False) -> _PlanOptions:
+             max_backward: bool = False, softmax_segment_edges: int = 0) -> _PlanOptions:
     opt = _PlanOptions()
     opt.segment_edges = int(segment_edges)
     opt.max_row_segments = int(max_row_segments)
@@ -344,6 +346,7 @@ def _options(segment_edges: int = 0, max_row_segments: int = 0, source_slab_rows
     opt.partition_min_degree = int(partition_min_degree)
     opt.item_order = int(item_order)
     opt.max_backward = int(max_backward)
+    opt.softmax_segment_edges = int(softmax_segment_edges)
     return opt
 
 

@@ -41,7 +41,11 @@ static_assert(fg::kNoAllocScratchBytes == FG_NOALLOC_SCRATCH_BYTES,
 
 namespace {
 
-constexpr int32_t kDefaultSegmentEdges = 4096;
+// The gather schedule cuts rows into pieces of at most 2,048 edges by
+// default: the pieces of the long rows are what spreads them over the dies
+// (die-banded order), and at this length a piece's partial result is still
+// small next to the features it gathers.
+constexpr int32_t kDefaultSegmentEdges = 2048;
 // The plain schedule (edge softmax) cuts only rows longer than this by
 // default: a whole row of up to 16,384 scores is streamed by one wavefront
 // (read twice, the second time mostly from the L2), while a cut row passes
@@ -498,20 +502,22 @@ bool build_partitioned(const int32_t* ip, const int32_t* ix, int64_t num_rows, i
   return true;
 }
 
-// Die-banded order of a plain schedule (item_order 3, gather schedule only):
-// piece k of a row cut into K pieces goes to die floor(8 (k + 1/2) / K), the
-// eighth of the row its midpoint falls in, if K >= 8; pieces of rows cut
-// into fewer go with the whole rows.  A row's
-// sources are sorted, so the pieces of the long rows that one die runs draw
-// on about one eighth of their source id range, instead of every die
-// gathering from the whole feature matrix at once.  The pieces and their
-// slots are unchanged (so are the results).  Whole rows (and the pieces of
-// rows cut into fewer than 8) go, longest first, to the die with the fewest
-// edges so far; each die runs its items longest first.
+// Die-banded order of a plain schedule (item_order 3, gather schedule only).
+// Piece k of a row cut into K pieces covers the fraction [k/K, (k+1)/K) of
+// the row.  With K >= 8 it goes to die floor(8 (k + 1/2) / K), the eighth of
+// the row its midpoint falls in; with fewer pieces it spans the dies
+// [floor(8k/K), ceil(8(k+1)/K)), and the pieces of all rows that share one
+// span take its dies in turn.  A row's sources are sorted, so the pieces
+// that one die runs draw on about one eighth of their rows' source id range,
+// instead of every die gathering from the whole feature matrix at once.  The
+// pieces and their slots are unchanged (so are the results).  Whole rows go,
+// longest first, to the die with the fewest edges so far; each die runs its
+// items longest first.
 void band_by_die(Schedule& sc) {
   std::vector<std::vector<fg::Seg>> stream(kXcds);
   std::vector<int64_t> load(kXcds, 0);
   std::vector<fg::Seg> rest;
+  int64_t turn[kXcds][kXcds + 1] = {};
   for (const fg::Seg& sg : sc.segs) {
     if (sg.slot < 0) {
       rest.push_back(sg);
@@ -519,11 +525,15 @@ void band_by_die(Schedule& sc) {
     }
     const fg::Fix& fx = sc.fix[(size_t)sc.slot_fix[(size_t)sg.slot]];
     const int64_t k = sg.slot - fx.slot_begin, K = (int64_t)fx.slot_end - fx.slot_begin;
-    if (K < kXcds) {  // too few pieces to band: balanced with the whole rows
-      rest.push_back(sg);
-      continue;
+    int x;
+    if (K >= kXcds) {
+      x = (int)((2 * kXcds * k + kXcds) / (2 * K));  // die of the piece's midpoint
+    } else {
+      // fewer pieces than dies: the piece spans dies [lo, hi) of the row;
+      // successive pieces of that span take them in turn
+      const int lo = (int)(kXcds * k / K), hi = (int)((kXcds * (k + 1) + K - 1) / K);
+      x = lo + (int)(turn[lo][hi]++ % (hi - lo));
     }
-    const int x = (int)((2 * kXcds * k + kXcds) / (2 * K));  // die of the piece's midpoint
     stream[x].push_back(sg);
     load[x] += (int64_t)sg.end - sg.begin;
   }
@@ -569,6 +579,9 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
     if (opt->partition_min_degree < 0) return FG_ERR_INVALID_ARG;
     if (opt->source_slab_rows < kSlabsOff) return FG_ERR_INVALID_ARG;
     if (opt->segment_edges) o->S = o->S_plain = opt->segment_edges;
+    if (opt->softmax_segment_edges < 0 || opt->softmax_segment_edges > kMaxSegmentEdges)
+      return FG_ERR_INVALID_ARG;
+    if (opt->softmax_segment_edges) o->S_plain = opt->softmax_segment_edges;
     if (opt->max_row_segments) o->cap = opt->max_row_segments;
     slab_opt = opt->source_slab_rows;
     min_opt = opt->partition_min_degree;

@@ -167,7 +167,7 @@ void invalid_arguments() {
   CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
         FG_ERR_INVALID_ARG);
   bad = o;
-  bad.reserved[1] = 1;
+  bad.reserved[0] = 1;
   CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
         FG_ERR_INVALID_ARG);
   bad = o;

@@ -273,10 +273,10 @@ def test_plan_create_rejects_invalid_arguments():
     opt = fg._PlanOptions()
     assert L.fg_plan_create(ctypes.byref(g), None, None, 0, None, ctypes.byref(h), None) == -1
     assert L.fg_plan_create(ctypes.byref(g), None, None, 8, None, None, None) == -1
-    opt.reserved[1] = 1
+    opt.reserved[0] = 1
     assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1
-    opt.reserved[1] = 0
+    opt.reserved[0] = 0
     opt.max_backward = 2  # 0 or 1
     assert L.fg_plan_create(ctypes.byref(g), None, None, 8, ctypes.byref(opt), ctypes.byref(h),
                             None) == -1
@@ -599,8 +599,9 @@ def test_plan_refuses_a_graph_edited_in_place():
 def test_die_banded_schedule(S):
     """item_order 3: the gather schedule holds the plain schedule's items
     (same pieces, same slots), piece k of a row cut into K >= 8 runs on die
-    floor(8 (k + 1/2) / K) (workgroup w = item // 4 runs on die w % 8), other
-    items
+    floor(8 (k + 1/2) / K) (workgroup w = item // 4 runs on die w % 8), one
+    of a row cut into fewer on a die of [floor(8k / K), ceil(8(k + 1) / K)),
+    the pieces of one such span spread evenly over its dies; whole rows
     balance the dies' edges, and each die runs its items longest first."""
     c = synth.make_config("rmat_233k_115m", scale_down=64).csr
     kw = dict(segment_edges=S)
@@ -624,8 +625,17 @@ def test_die_banded_schedule(S):
         count[r] = count.get(r, 0) + 1
     k = np.array([sl - first[r] for r, sl in zip(rows, real[slotted, 3])])
     K = np.array([count[r] for r in rows])
-    banded = K >= 8  # rows of fewer pieces are balanced with the whole rows
+    banded = K >= 8
     np.testing.assert_array_equal(die[slotted][banded], ((16 * k + 8) // (2 * K))[banded])
+    lo, hi = (8 * k) // K, -((-8 * (k + 1)) // K)
+    d = die[slotted]
+    assert np.all((d >= lo) & (d < hi))
+    spans = set(zip(lo[~banded].tolist(), hi[~banded].tolist()))
+    assert spans or S == 4096
+    for a, b in spans:
+        on = (lo == a) & (hi == b) & ~banded
+        per = np.bincount(d[on] - a, minlength=b - a)
+        assert per.max() - per.min() <= 1, (a, b, per)
     lens = real[:, 2] - real[:, 1]
     load = np.bincount(die, weights=lens, minlength=8)
     print("die loads", load)
