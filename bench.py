@@ -132,6 +132,7 @@ def setup(name, d, args, fg, torch, dev):
     G = fg.Graph.from_csr(csr, device=dev)
     popt = dict(segment_edges=args.segment_edges,
                 softmax_segment_edges=args.softmax_segment_edges,
+                band_row_edges=args.band_row_edges,
                 max_row_segments=args.max_row_segments,
                 source_slab_rows=args.source_slab_rows,
                 partition_min_degree=args.partition_min_degree, item_order=args.item_order)
@@ -815,6 +816,9 @@ def main():
     ap.add_argument("--softmax-segment-edges", type=int, default=0,
                     help="segment length of the edge-softmax schedule (0: --segment-edges if "
                          "given, else the library default)")
+    ap.add_argument("--band-row-edges", type=int, default=0,
+                    help="die-banded gather schedule: rows of more edges get at least 8 pieces "
+                         "(0: library default, -1: none)")
     ap.add_argument("--max-row-segments", type=int, default=0,
                     help="cap on segments per row (0: default)")
     ap.add_argument("--source-slab-rows", type=int, default=0,

@@ -166,15 +166,17 @@ typedef struct fg_plan_options {
                                    power-of-two length class, longest first, rows
                                    in id order within a class; 3 -> die-banded
                                    gather schedule (unless source slabs apply):
-                                   the same items as 1, but piece k of a row cut
-                                   into K pieces runs on die floor(8 (k + 1/2) /
-                                   K) if K >= 8, else on one of the dies
-                                   [floor(8k / K), ceil(8(k + 1) / K)) (the
-                                   pieces sharing such a span take its dies in
-                                   turn), so each die gathers from one eighth
-                                   of those rows' sources; whole rows balance
-                                   the dies' edges (edge softmax keeps order
-                                   1); results equal those of 1               */
+                                   the items of 1, except that rows of more than
+                                   band_row_edges edges are cut into at least 8
+                                   pieces; piece k of a row cut into K pieces
+                                   runs on die floor(8 (k + 1/2) / K) if K >= 8,
+                                   else on one of the dies [floor(8k / K),
+                                   ceil(8(k + 1) / K)) (the pieces sharing such
+                                   a span take its dies in turn), so each die
+                                   gathers from one eighth of those rows'
+                                   sources; whole rows balance the dies' edges
+                                   (edge softmax keeps order 1); with
+                                   band_row_edges = -1 results equal those of 1 */
   int32_t max_backward;         /* 1 -> also reserve the workspace of the binned
                                    gSpMM-max backward: 8 bytes per element of a
                                    num_rows x max_width gradient (that product must
@@ -183,7 +185,12 @@ typedef struct fg_plan_options {
                                    tile, at most 8 MiB); 0 -> none (default)       */
   int32_t softmax_segment_edges;/* S of the plain schedule; 0 -> segment_edges if that
                                    is given, else 16384                             */
-  int32_t reserved[1];          /* must be zero                                      */
+  int32_t band_row_edges;       /* die-banded gather schedule (item_order 3): rows
+                                   of more edges are cut into at least
+                                   min(8, max_row_segments) pieces, so that every
+                                   die takes a share of them; 0 -> 512; -1 -> no
+                                   such cut (the items of order 1)                  */
+  int32_t reserved[2];          /* must be zero                                      */
 } fg_plan_options;
 
 typedef struct fg_plan_info {

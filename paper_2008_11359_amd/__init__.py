@@ -60,7 +60,8 @@ class _PlanOptions(ctypes.Structure):
     _fields_ = [("segment_edges", ctypes.c_int32), ("max_row_segments", ctypes.c_int32),
                 ("source_slab_rows", ctypes.c_int32), ("partition_min_degree", ctypes.c_int32),
                 ("item_order", ctypes.c_int32), ("max_backward", ctypes.c_int32),
-                ("softmax_segment_edges", ctypes.c_int32), ("reserved", ctypes.c_int32 * 1)]
+                ("softmax_segment_edges", ctypes.c_int32), ("band_row_edges", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 2)]
 
 
 class _PlanInfo(ctypes.Structure):
@@ -267,10 +268,12 @@ class Plan:
     they exceed 32 MiB; -2 never; > 0 that many source ids per slab.  ``item_order``: 1 longest
     item first, 2 by power-of-two length class with rows in id order (keeps
     the locality of graphs whose neighbouring ids share sources), 3 the items
-    of 1 with the pieces of split rows dealt to the dies by position in the
-    row (each die gathers from about one eighth of their sources; same
-    results as 1), 0 (default) picks 2 for such graphs and otherwise 3
-    if some row is cut into 8 or more pieces, else 1.  Partial-result
+    of 1 with rows of more than ``band_row_edges`` edges (default 512; -1:
+    none) cut into at least 8 pieces and the pieces of split rows dealt to
+    the dies by position in the row (each die gathers from about one eighth
+    of their sources; with ``band_row_edges=-1`` the results equal those of
+    1), 0 (default) picks 2 for such graphs and otherwise 3 if some row is
+    cut into 8 or more pieces by length, else 1.  Partial-result
     workspace for features up to ``max_width`` floats.  ``max_backward``:
     also hold the workspace with which gspmm_max_backward bins the gradient
     per source tile instead of adding it with atomics (8 bytes per element of
@@ -280,9 +283,10 @@ class Plan:
     def __init__(self, g: Graph, max_width: int, segment_edges: int = 0,
                  max_row_segments: int = 0, source_slab_rows: int = 0,
                  partition_min_degree: int = 0, item_order: int = 0,
-                 max_backward: bool = False, softmax_segment_edges: int = 0):
+                 max_backward: bool = False, softmax_segment_edges: int = 0,
+                 band_row_edges: int = 0):
         opt = _options(segment_edges, max_row_segments, source_slab_rows, partition_min_degree,
-                       item_order, max_backward, softmax_segment_edges)
+                       item_order, max_backward, softmax_segment_edges, band_row_edges)
         h = ctypes.c_void_p()
         ip, ix = g.indptr_host, g.indices_host
         st = _lib.fg_plan_create(ctypes.byref(g._c), None if ip is None else ip.ctypes.data,
@@ -338,7 +342,8 @@ class Plan:
 
 def _options(segment_edges: int = 0, max_row_segments: int = 0, source_slab_rows: int = 0,
              partition_min_degree: int = 0, item_order: int = 0,
-             max_backward: bool = False, softmax_segment_edges: int = 0) -> _PlanOptions:
+             max_backward: bool = False, softmax_segment_edges: int = 0,
+             band_row_edges: int = 0) -> _PlanOptions:
     opt = _PlanOptions()
     opt.segment_edges = int(segment_edges)
     opt.max_row_segments = int(max_row_segments)
@@ -347,6 +352,7 @@ def _options(segment_edges: int = 0, max_row_segments: int = 0, source_slab_rows
     opt.item_order = int(item_order)
     opt.max_backward = int(max_backward)
     opt.softmax_segment_edges = int(softmax_segment_edges)
+    opt.band_row_edges = int(band_row_edges)
     return opt
 
 

@@ -171,6 +171,10 @@ void invalid_arguments() {
   CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
         FG_ERR_INVALID_ARG);
   bad = o;
+  bad.band_row_edges = -2;
+  CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
+        FG_ERR_INVALID_ARG);
+  bad = o;
   bad.max_backward = 2;
   CHECK(fg_schedule_host(ip_ok, ix, 2, 5, 8, &bad, 0, nullptr, 0, &n, nullptr, nullptr) ==
         FG_ERR_INVALID_ARG);
@@ -232,6 +236,7 @@ int main() {
   const int32_t slab_opts[] = {0, -1, 1, 64, 1000};
   const int32_t min_opts[] = {0, 1, 10, 1000};
   const int64_t widths[] = {1, 32, 128, 1024};
+  const int32_t band_opts[] = {0, -1, 1, 9};
   for (int rep = 0; rep < 30; ++rep) {
     const int64_t rows = rep < 3 ? rep : below(3000);
     const int64_t cols = 1 + below(rep % 2 ? 50000 : 300);
@@ -244,6 +249,7 @@ int main() {
       o.source_slab_rows = slab_opts[below(5)];
       o.partition_min_degree = min_opts[below(4)];
       o.item_order = (int32_t)below(4);
+      o.band_row_edges = band_opts[below(4)];
       const int64_t w = widths[below(4)];
       for (int which = 0; which < 2; ++which)
         for (int ind = 0; ind < 2; ++ind) {

@@ -597,8 +597,8 @@ def test_plan_refuses_a_graph_edited_in_place():
 
 @pytest.mark.parametrize("S", [64, 4096])
 def test_die_banded_schedule(S):
-    """item_order 3: the gather schedule holds the plain schedule's items
-    (same pieces, same slots), piece k of a row cut into K >= 8 runs on die
+    """item_order 3 with band_row_edges = -1: the gather schedule holds the
+    plain schedule's items (same pieces, same slots), piece k of a row cut into K >= 8 runs on die
     floor(8 (k + 1/2) / K) (workgroup w = item // 4 runs on die w % 8), one
     of a row cut into fewer on a die of [floor(8k / K), ceil(8(k + 1) / K)),
     the pieces of one such span spread evenly over its dies; whole rows
@@ -607,7 +607,7 @@ def test_die_banded_schedule(S):
     kw = dict(segment_edges=S)
     plain, n_split, n_slot = fg.schedule_host(c.indptr, None, c.num_cols, 128, "plain", **kw)
     band, b_split, b_slot = fg.schedule_host(c.indptr, None, c.num_cols, 128, "gather",
-                                             item_order=3, **kw)
+                                             item_order=3, band_row_edges=-1, **kw)
     assert (n_split, n_slot) == (b_split, b_slot) and n_split > 0
     pad = band[:, 0] < 0
     assert np.all(band[pad, 1:] == [0, 0, -1])
@@ -642,3 +642,42 @@ def test_die_banded_schedule(S):
     assert load.max() - load.min() <= max(lens.max(), 0.02 * load.sum())
     for x in range(8):
         assert np.all(np.diff(lens[die == x]) <= 0)
+
+
+@pytest.mark.parametrize("T,cap", [(0, 0), (40, 0), (40, 5)])
+def test_die_banded_cuts_mid_length_rows(T, cap):
+    """item_order 3 cuts every row of more than band_row_edges edges (default
+    512) into at least min(8, max_row_segments) even pieces, longer rows as
+    before; with 8 pieces each goes to its own die.  The edge-softmax
+    schedule is not affected."""
+    c = synth.make_config("rmat_233k_115m", scale_down=64).csr
+    S = 256
+    kw = dict(segment_edges=S, max_row_segments=cap, band_row_edges=T)
+    band, n_split, n_slot = fg.schedule_host(c.indptr, None, c.num_cols, 128, "gather",
+                                             item_order=3, **kw)
+    plain, *_ = fg.schedule_host(c.indptr, None, c.num_cols, 128, "plain", item_order=3, **kw)
+    deg = np.diff(c.indptr)
+    thr, cap_ = (T or 512), (cap or 128)
+    base = np.minimum(np.maximum(-(-deg // S), 1), cap_)
+    want = np.where(deg > thr, np.maximum(base, np.minimum(np.minimum(8, cap_), deg)), base)
+    want[deg == 0] = 1
+    pad = band[:, 0] < 0
+    real = band[~pad]
+    got = np.bincount(real[:, 0], minlength=len(deg))
+    np.testing.assert_array_equal(got, want)
+    assert np.sum(want[want > 1]) == n_slot and np.sum(want > 1) == n_split
+    # pieces tile each row evenly: lengths differ by at most one
+    order = np.lexsort((real[:, 1], real[:, 0]))
+    r = real[order]
+    lens = r[:, 2] - r[:, 1]
+    for row in np.nonzero(want > 1)[0][:200]:
+        L = lens[r[:, 0] == row]
+        assert L.sum() == deg[row] and L.max() - L.min() <= 1
+    # the plain schedule (same S here) keeps the length-only cut
+    base[deg == 0] = 1
+    np.testing.assert_array_equal(np.bincount(plain[plain[:, 0] >= 0, 0], minlength=len(deg)),
+                                  base)
+    # rows of exactly 8 pieces: one piece per die
+    die = (np.nonzero(~pad)[0] // 4) % 8
+    for row in np.nonzero(want == 8)[0][:200]:
+        assert sorted(die[real[:, 0] == row].tolist()) == list(range(8))

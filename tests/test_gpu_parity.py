@@ -429,6 +429,8 @@ def plans_for(G, width, sizes=(0, 1, 5, 64)):
     yield fg.Plan(G, max_width=width, segment_edges=64, item_order=2)
     # die-banded pieces of long rows (rows of 8+ pieces at 16-edge pieces)
     yield fg.Plan(G, max_width=width, segment_edges=16, item_order=3)
+    # die-banded, every row of more than 20 edges cut into at least 8 pieces
+    yield fg.Plan(G, max_width=width, segment_edges=64, item_order=3, band_row_edges=20)
     # rows cut at source-slab boundaries (8 slabs), pieces of at most 64 edges
     slab = max(1, -(-G.num_cols // 8))
     yield fg.Plan(G, max_width=width, segment_edges=64, source_slab_rows=slab,
@@ -1111,14 +1113,15 @@ def test_determinism_and_plan_independence(small_rmat):
 
 
 def test_die_banded_order_gives_identical_results(small_rmat):
-    """The die-banded gather order runs the same pieces with the same slots
-    as longest-first order, so every result is bitwise the same."""
+    """Without the extra cut of mid-length rows (band_row_edges = -1) the
+    die-banded gather order runs the same pieces with the same slots as
+    longest-first order, so every result is bitwise the same."""
     csr, G = small_rmat
     rng = np.random.default_rng(12)
     x = rng.standard_normal((csr.num_cols, 64)).astype(np.float32)
     w = rng.random(csr.nnz, dtype=np.float32)
     p1 = fg.Plan(G, 64, segment_edges=16, item_order=1)
-    p3 = fg.Plan(G, 64, segment_edges=16, item_order=3)
+    p3 = fg.Plan(G, 64, segment_edges=16, item_order=3, band_row_edges=-1)
     assert p3.info()["item_order"] == 3 and p3.info()["num_segments"] > p1.info()["num_segments"]
     tx, tw = dev(x), dev(w)
     for name, f in (("mul_sum", lambda p: fg.gspmm(G, tx, tw, msg="src_mul_edge", plan=p)),
