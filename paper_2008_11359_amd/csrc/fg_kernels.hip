@@ -3404,8 +3404,6 @@ hipError_t launch_build_eid_pos(const int32_t* eids, int64_t nnz, int64_t nnz_to
 }
 
 // Tile rows (log2) and bin count of the binned max backward for width F;
-// false if the shape does not fit its LDS tables or int32 record offsets.
-// Tile rows (log2) and bin count of the binned max backward for width F;
 // false if the shape does not fit the workspace, its LDS tables or int32
 // record offsets.
 static bool bin_shape(const GraphView& g, int64_t F, const BinWorkspace* ws, int& logR, int& nb) {
