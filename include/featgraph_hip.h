@@ -117,7 +117,8 @@ typedef struct fg_graph {
  *    (a whole row of up to 16384 scores is streamed by one wavefront; a cut
  *    row is read once more by a merge pass); long items first
  *    (fg_plan_options.item_order), rows without edges last;
- *  - gather (gSpMM, gSDDMM, fused attention): as plain with S =
+ *  - gather (gSpMM, gSDDMM, the fused SDDMM + edge softmax, fused
+ *    attention): as plain with S =
  *    segment_edges if given, else 2048, unless source
  *    partitioning applies (by default once the num_cols x max_width source
  *    features exceed 128 MiB, half the Infinity Cache, or 32 MiB when the

@@ -1162,8 +1162,10 @@ fg_status fg_gsddmm_edge_softmax(const fg_graph* g, int32_t num_heads, int64_t h
     return FG_ERR_INVALID_ARG;
   const fg::GraphView gv = view_of(g);
   hipStream_t hs = static_cast<hipStream_t>(stream);
+  // the fused kernel gathers like the SDDMM, so it takes the gather schedule
+  // (die-banded on power-law graphs: 3.26 -> 3.06 ms against the plain one)
   if (fg::gsddmm_softmax_fused(num_heads, head_dim, x_src, x_dst))
-    return from_hip(fg::launch_gsddmm_softmax(gv, plan ? &plan->plain : nullptr, F, x_src, x_dst,
+    return from_hip(fg::launch_gsddmm_softmax(gv, plan ? &plan->gather : nullptr, F, x_src, x_dst,
                                               apply_leaky_relu != 0, negative_slope, scores, out,
                                               hs));
   // other shapes: the two operators one after the other
