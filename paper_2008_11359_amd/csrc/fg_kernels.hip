@@ -139,6 +139,84 @@ __device__ __forceinline__ float bcast_lane_f(float v, int jb, int gid) {
   return __builtin_bit_cast(float, bcast_lane<NG>(__builtin_bit_cast(int, v), jb, gid));
 }
 
+// Wide batches of Q * 64 edges (the SDDMM on long items): lane l holds edges
+// Q*l .. Q*l + Q - 1 of the batch (Q = 4 for one or two lane groups, else 1),
+// so the ids of 256 edges arrive in one 16-byte load per lane and their
+// results leave in one 16-byte store: the address unit that bounds the
+// gather kernels spends one instruction on each instead of four.  (The
+// gSpMM kernels keep 64-edge batches: the extra registers cost them more
+// occupancy than the instructions save.)
+template <int NG, int U>
+constexpr int ids_per_lane() { return NG <= 2 && (NG * U) % 4 == 0 ? 4 : 1; }
+
+// Plans whose items average at least this many edges use the wide batches.
+constexpr int64_t kWideItemEdges = 128;
+
+template <int Q, typename T>
+__device__ __forceinline__ T pick(const T (&v)[Q], int c) {
+  if constexpr (Q == 1) {
+    return v[0];
+  } else {
+    return c == 0 ? v[0] : c == 1 ? v[1] : c == 2 ? v[2] : v[3];
+  }
+}
+
+typedef int32_t int4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+typedef float float4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+
+// v[c] = x for a c known after unrolling (no indexed register access).
+template <int Q>
+__device__ __forceinline__ void put(float (&v)[Q], int c, float x) {
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+    if (q == c) v[q] = x;
+}
+
+// Edges base + Q*lane + q (q < Q) of a batch of `cnt` edges from a streamed
+// int32 array of `len` elements (non-temporal); 0 past cnt.  A lane with
+// edges in the batch takes its Q with one 16-byte load (4-byte aligned:
+// gfx950 loads it unaligned) when they lie inside the array, else (only at
+// its very end) one by one, so nothing past the array is read.
+template <int Q>
+__device__ __forceinline__ void load_ids(const int32_t* ptr, int64_t len, int64_t base, int lane,
+                                         int cnt, int32_t (&out)[Q]) {
+  const int k0 = lane * Q;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) out[q] = 0;
+  if (k0 >= cnt) return;
+  if constexpr (Q == 1) {
+    out[0] = __builtin_nontemporal_load(ptr + base + k0);
+  } else if (base + k0 + Q <= len) {
+    const int4_a4 v = __builtin_nontemporal_load(reinterpret_cast<const int4_a4*>(ptr + base + k0));
+    out[0] = v.x;
+    out[1] = k0 + 1 < cnt ? v.y : 0;
+    out[2] = k0 + 2 < cnt ? v.z : 0;
+    out[3] = k0 + 3 < cnt ? v.w : 0;
+  } else {
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+      if (k0 + q < cnt) out[q] = __builtin_nontemporal_load(ptr + base + k0 + q);
+  }
+}
+
+// Value of edge (jb + gid) of the batch (jb wave-uniform, gid < NG the
+// caller's lane group) when each lane holds Q consecutive edges; jb % Q is
+// c0, known after unrolling.
+template <int NG, int Q>
+__device__ __forceinline__ int bcast_q(const int32_t (&v)[Q], int jb, int c0, int gid) {
+  if constexpr (Q == 1) {
+    return bcast_lane<NG>(v[0], jb, gid);
+  } else if constexpr (NG == 1) {
+    return __builtin_amdgcn_readlane(pick<Q>(v, c0), jb / Q);
+  } else {
+    static_assert(NG == 2, "four ids per lane serve one or two lane groups");
+    // c0 is even, so edges jb and jb + 1 sit in the same lane
+    const int a = __builtin_amdgcn_readlane(pick<Q>(v, c0), jb / Q);
+    const int b = __builtin_amdgcn_readlane(pick<Q>(v, c0 + 1), jb / Q);
+    return gid ? b : a;
+  }
+}
+
 // ----------------------------------------------------------------------------
 // generalized SpMM
 // ----------------------------------------------------------------------------
@@ -807,6 +885,7 @@ struct SddmmParams {
   float* out;
   const Seg* segs;
   int64_t n_items;
+  int64_t nnz;  // stored edges: elements of indices and eids
   int64_t F;
   int32_t H;
   int32_t dh;
@@ -818,7 +897,7 @@ struct SddmmParams {
 // Single head, float4 lanes, G lanes per feature row, NV float4 per lane.  The
 // destination row stays in registers for the whole item; each edge gathers
 // its source row, multiplies, and reduces across its G lanes with DPP.
-template <int G, int NV, int U, bool SEG>
+template <int G, int NV, int U, bool SEG, bool WIDE = false>
 __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
   constexpr int NG = kWave / G;
   static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
@@ -847,19 +926,26 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
     }
   }
 
-  for (int64_t base = it.b; base < it.e; base += kWave) {
-    const int cnt = (int)min((int64_t)kWave, it.e - base);
-    int my_src = 0, my_eid = 0;
-    if (lane < cnt) {
-      my_src = __builtin_nontemporal_load(p.indices + base + lane);
-      my_eid = p.eids ? __builtin_nontemporal_load(p.eids + base + lane) : (int)(base + lane);
+  constexpr int Q = WIDE ? ids_per_lane<NG, U>() : 1;
+  static_assert((NG * U) % Q == 0, "every step starts on a lane's first edge");
+  for (int64_t base = it.b; base < it.e; base += Q * kWave) {
+    const int cnt = (int)min((int64_t)(Q * kWave), it.e - base);
+    int32_t my_src[Q], my_eid[Q];
+    load_ids<Q>(p.indices, p.nnz, base, lane, cnt, my_src);
+    if (p.eids) {
+      load_ids<Q>(p.eids, p.nnz, base, lane, cnt, my_eid);
+    } else {
+#pragma unroll
+      for (int q = 0; q < Q; ++q) my_eid[q] = (int)(base + lane * Q + q);
     }
-    // lane j collects the dot product of edge base + j, so the batch's
+    // lane j collects the dot products of edges base + Q*j + q, so the batch's
     // results leave in one store instead of one store per step with one lane
     // per group active, which would cost the address unit as much as a
     // gather: one or two groups hand their sums over with scalar readlanes,
     // more groups with one cross-lane permute per step
-    float res = 0.0f;
+    float res[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) res[q] = 0.0f;
     for (int j0 = 0; j0 < cnt; j0 += NG * U) {
       float val[U][NV][4];
       bool ok[U];
@@ -867,7 +953,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
         ok[u] = jb + gid < cnt;
-        const int src = bcast_lane<NG>(my_src, jb, gid);
+        const int src = bcast_q<NG, Q>(my_src, jb, (u * NG) % Q, gid);
         const float* xr = p.xs + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
@@ -895,18 +981,30 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
             if (jb + g < cnt) {
               const int sum =
                   __builtin_amdgcn_readlane(__builtin_bit_cast(int, part), (g + 1) * G - 1);
-              if (lane == jb + g) res = __builtin_bit_cast(float, sum);
+              if (lane == (jb + g) / Q) put<Q>(res, (u * NG + g) % Q, __builtin_bit_cast(float, sum));
             }
           }
         } else {
           const int rel = lane - jb;
           const bool mine = rel >= 0 && rel < NG && lane < cnt;
           const float got = __shfl(part, mine ? rel * G + (G - 1) : lane);
-          if (mine) res = got;
+          if (mine) res[0] = got;  // Q == 1 for more than two groups
         }
       }
     }
-    if (lane < cnt) p.out[my_eid] = res;
+    bool stored = false;
+    if constexpr (Q == 4) {
+      if (!p.eids && lane * Q + Q <= cnt) {  // four positional results: one 16-byte store
+        *reinterpret_cast<float4_a4*>(p.out + base + lane * Q) =
+            float4_a4{res[0], res[1], res[2], res[3]};
+        stored = true;
+      }
+    }
+    if (!stored) {
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+        if (lane * Q + q < cnt) p.out[my_eid[q]] = res[q];
+    }
   }
 }
 
@@ -2866,8 +2964,16 @@ void spmm_generic_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 g
   }
 }
 
+// wide: batches of four ids per lane where the lane layout allows it
 template <int G, int NV, int U>
-void sddmm_fast_go(const SddmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+void sddmm_fast_go(const SddmmParams& prm, bool seg, bool wide, dim3 grid, hipStream_t st) {
+  if constexpr (ids_per_lane<kWave / G, U>() > 1) {
+    if (wide) {
+      if (seg) FG_LAUNCH((sddmm_fast_kernel<G, NV, U, true, true>), grid, st, prm);
+      else FG_LAUNCH((sddmm_fast_kernel<G, NV, U, false, true>), grid, st, prm);
+      return;
+    }
+  }
   if (seg) FG_LAUNCH((sddmm_fast_kernel<G, NV, U, true>), grid, st, prm);
   else FG_LAUNCH((sddmm_fast_kernel<G, NV, U, false>), grid, st, prm);
 }
@@ -3066,6 +3172,7 @@ hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, in
   const int64_t F = H * dh;
   const bool seg = plan != nullptr;
   SddmmParams prm;
+  prm.nnz = g.nnz;
   prm.indptr = g.indptr;
   prm.indices = g.indices;
   prm.eids = g.edge_ids;
@@ -3084,13 +3191,17 @@ hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, in
   const bool vec4 = (F % 4 == 0) && (H == 1 || dh % 4 == 0) && aligned16(xs) && aligned16(xd);
   if (vec4 && H == 1 && F <= 4 * 4 * kWave) {
     const int64_t Q = F / 4;
-    if (Q <= 4) sddmm_fast_go<4, 1, 4>(prm, seg, grid, stream);
-    else if (Q <= 8) sddmm_fast_go<8, 1, 8>(prm, seg, grid, stream);
-    else if (Q <= 16) sddmm_fast_go<16, 1, 8>(prm, seg, grid, stream);
-    else if (Q <= 32) sddmm_fast_go<32, 1, 8>(prm, seg, grid, stream);
-    else if (Q <= 64) sddmm_fast_go<64, 1, 8>(prm, seg, grid, stream);
-    else if (Q <= 128) sddmm_fast_go<64, 2, 4>(prm, seg, grid, stream);
-    else sddmm_fast_go<64, 4, 2>(prm, seg, grid, stream);
+    // items of kWideItemEdges edges or more on average take the 256-edge
+    // batches; short items (source-slab pieces) keep 64-edge batches
+    const int64_t items = seg ? plan->num_segments : g.num_rows;
+    const bool wide = g.nnz >= kWideItemEdges * std::max<int64_t>(items, 1);
+    if (Q <= 4) sddmm_fast_go<4, 1, 4>(prm, seg, wide, grid, stream);
+    else if (Q <= 8) sddmm_fast_go<8, 1, 8>(prm, seg, wide, grid, stream);
+    else if (Q <= 16) sddmm_fast_go<16, 1, 8>(prm, seg, wide, grid, stream);
+    else if (Q <= 32) sddmm_fast_go<32, 1, 8>(prm, seg, wide, grid, stream);
+    else if (Q <= 64) sddmm_fast_go<64, 1, 8>(prm, seg, wide, grid, stream);
+    else if (Q <= 128) sddmm_fast_go<64, 2, 4>(prm, seg, wide, grid, stream);
+    else sddmm_fast_go<64, 4, 2>(prm, seg, wide, grid, stream);
     return hipGetLastError();
   }
   if (vec4 && H > 1 && F <= 4 * kWave && (dh == 16 || dh == 32 || dh == 64)) {
@@ -3144,6 +3255,7 @@ hipError_t launch_gsddmm_softmax_backward(const GraphView& g, const PlanView* ga
   }
   const bool seg = plain != nullptr;
   SddmmParams prm;
+  prm.nnz = g.nnz;
   prm.indptr = g.indptr;
   prm.indices = g.indices;
   prm.eids = g.edge_ids;
@@ -3196,6 +3308,7 @@ hipError_t launch_gsddmm_softmax(const GraphView& g, const PlanView* plan, int64
   if (g.num_rows == 0 || g.nnz == 0) return hipSuccess;
   const bool seg = plan != nullptr;
   SddmmParams prm;
+  prm.nnz = g.nnz;
   prm.indptr = g.indptr;
   prm.indices = g.indices;
   prm.eids = g.edge_ids;
