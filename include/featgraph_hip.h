@@ -361,8 +361,10 @@ fg_status fg_gat_aggregate(const fg_graph* g, int32_t num_heads, int64_t head_di
  * paper fuses UDFs into its templates, Sec. III-B):
  *   scores[e, h] = fg_gsddmm's output;  out[e, h] = fg_edge_softmax(scores)
  * One head with dh % 4 == 0, dh <= 1024 and 16-byte aligned features runs as
- * one pass (plus the merge of split rows); other shapes run the two
- * operators one after the other.  Both arrays are [nnz_total, H], written for
+ * one pass (plus the merge of split rows), unless the plan's items average
+ * 128 edges or more: there, and for other shapes, the two operators run one
+ * after the other (the SDDMM's batches of 256 edges and the streaming softmax
+ * are faster on such plans than the fused pass).  Both arrays are [nnz_total, H], written for
  * the edges of g.  A plan must have max_width >= max(H * dh, H).
  * ------------------------------------------------------------------------- */
 fg_status fg_gsddmm_edge_softmax(const fg_graph* g, int32_t num_heads, int64_t head_dim,

@@ -1162,13 +1162,18 @@ fg_status fg_gsddmm_edge_softmax(const fg_graph* g, int32_t num_heads, int64_t h
     return FG_ERR_INVALID_ARG;
   const fg::GraphView gv = view_of(g);
   hipStream_t hs = static_cast<hipStream_t>(stream);
-  // the fused kernel gathers like the SDDMM, so it takes the gather schedule
-  // (die-banded on power-law graphs: 3.26 -> 3.06 ms against the plain one)
-  if (fg::gsddmm_softmax_fused(num_heads, head_dim, x_src, x_dst))
+  // The fused kernel gathers like the SDDMM, so it takes the gather schedule
+  // (die-banded on power-law graphs: 3.26 -> 3.06 ms against the plain one).
+  // On plans of long items the SDDMM's wide batches and the streaming
+  // softmax are faster than its one-value-per-lane passes (2.82 against
+  // 3.06 ms on the power-law graph), so those run the two kernels.
+  const bool long_items =
+      plan && g->nnz >= fg::kWideItemEdges * std::max<int64_t>(plan->gather.num_segments, 1);
+  if (!long_items && fg::gsddmm_softmax_fused(num_heads, head_dim, x_src, x_dst))
     return from_hip(fg::launch_gsddmm_softmax(gv, plan ? &plan->gather : nullptr, F, x_src, x_dst,
                                               apply_leaky_relu != 0, negative_slope, scores, out,
                                               hs));
-  // other shapes: the two operators one after the other
+  // long items and other shapes: the two operators one after the other
   hipError_t e = fg::launch_gsddmm(gv, plan ? &plan->gather : nullptr, num_heads, head_dim, x_src,
                                    x_dst, scores, hs);
   if (e != hipSuccess) return FG_ERR_HIP;

@@ -40,6 +40,10 @@ struct PlanView {
 // Rows of at most this many edges are short: the edge softmax packs four of
 // them into one wavefront.
 constexpr int kShortRowEdges = 64;
+// Plans whose items average at least this many edges take the SDDMM's wide
+// (256-edge) batches, and the SDDMM + softmax call runs as two kernels there.
+constexpr int64_t kWideItemEdges = 128;
+
 // Rows of at most this many edges (and more than kShortRowEdges) also go
 // several to a wavefront: four, with float4 lanes.
 constexpr int kMediumRowEdges = 256;

@@ -149,8 +149,6 @@ __device__ __forceinline__ float bcast_lane_f(float v, int jb, int gid) {
 template <int NG, int U>
 constexpr int ids_per_lane() { return NG <= 2 && (NG * U) % 4 == 0 ? 4 : 1; }
 
-// Plans whose items average at least this many edges use the wide batches.
-constexpr int64_t kWideItemEdges = 128;
 
 template <int Q, typename T>
 __device__ __forceinline__ T pick(const T (&v)[Q], int c) {

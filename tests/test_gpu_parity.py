@@ -1228,8 +1228,10 @@ def test_rmat_233k_full(rmat_full):
     s_syn = (np.random.default_rng(31).standard_normal(csr.nnz, dtype=np.float32)
              * np.float32(math.sqrt(128)))
     check_softmax(csr, G, s_syn, rows=rows, plan=plan)
-    # SDDMM and softmax fused, in the benchmark's launch configuration
+    # SDDMM and softmax in one call, in the benchmark's launch configuration
+    # (long items: the two kernels), and as the fused kernel (64-edge items)
     check_sddmm_softmax(csr, G, x, x, rows=rows, plan=plan)
+    check_sddmm_softmax(csr, G, x, x, rows=rows, plan=fg.Plan(G, 128, segment_edges=64))
     check_spmm(csr, G, x, rows=rows, plan=pplan, edge=wgt)
     check_spmm(csr, G, x, rows=rows, plan=pplan, reduce="max")
     check_sddmm(csr, G, x, x, rows=rows, plan=pplan)
