@@ -40,6 +40,12 @@ __device__ __forceinline__ int64_t wave_item() {
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
 
+// Compile-time flag passed to generic lambdas (decltype(tag)::value).
+template <bool B>
+struct BoolTag {
+  static constexpr bool value = B;
+};
+
 // Offset of source row `src` in a [rows, F] array.  Both factors are
 // non-negative and below 2^32 (src < 2^31, F <= 65536), so one unsigned
 // 32 x 32 -> 64-bit multiply replaces the signed 64-bit product, which costs
@@ -465,7 +471,10 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
       }
       wave_lds_sync();
     }
-    for (int j0 = 0; j0 < cnt; j0 += NG * U) {
+    // one step of U edges per lane group; FULL: every edge of the step is in
+    // the batch and every feature chunk in the row (no per-edge masking)
+    auto step = [&](int j0, auto full_tag) {
+      constexpr bool FULL = decltype(full_tag)::value;
       float val[U][NV][4];
       float wv[U][NV];
       int32_t eu[U];
@@ -473,7 +482,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
-        ok[u] = jb + gid < cnt;
+        ok[u] = FULL || jb + gid < cnt;
         const int src = bcast_lane<NG>(my_src, jb, gid);
         if constexpr (EIDS) eu[u] = bcast_lane<NG>(my_eid, jb, gid);
         else eu[u] = (int)(base + jb + gid);
@@ -481,7 +490,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         const float* xr = p.x + (int64_t)src * F;
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
-          if (ok[u] && act[v]) {
+          if (FULL || (ok[u] && act[v])) {
             load_vec<4>(xr + f[v], val[u][v]);
             if constexpr (ELEM) {
 #pragma unroll
@@ -516,7 +525,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
               }
             } else if constexpr (MAX) {
               const float m = max_key(MUL ? wv[u][v] * val[u][v][c] : val[u][v][c]);
-              if (ok[u] && takes_over(m, eu[u], acc[v][c], am[v][c])) {
+              if ((FULL || ok[u]) && takes_over(m, eu[u], acc[v][c], am[v][c])) {
                 acc[v][c] = m;
                 am[v][c] = eu[u];
               }
@@ -526,7 +535,13 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
               acc[v][c] += val[u][v][c];
             }
           }
-    }
+    };
+    // full steps (wave-uniform test) take the unmasked body
+    const bool all_feat = c0 + (int64_t)G * 4 * NV <= F;
+    int j0 = 0;
+    if (all_feat)
+      for (; j0 + NG * U <= cnt; j0 += NG * U) step(j0, BoolTag<true>{});
+    for (; j0 < cnt; j0 += NG * U) step(j0, BoolTag<false>{});
   }
   if constexpr (POS) {
     const int64_t first = it.b + gid;  // this group's first edge
