@@ -486,7 +486,9 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         const int src = bcast_lane<NG>(my_src, jb, gid);
         if constexpr (EIDS) eu[u] = bcast_lane<NG>(my_eid, jb, gid);
         else eu[u] = (int)(base + jb + gid);
-        const float w1 = MUL ? bcast_lane_f<NG>(my_w, jb, gid) : 1.0f;
+        // the weight via the LDS crossbar (one permute) rather than two
+        // readlanes and a select on the vector unit
+        const float w1 = MUL ? __shfl(my_w, jb + gid) : 1.0f;
         const float* xr = p.x + (int64_t)src * F;
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
