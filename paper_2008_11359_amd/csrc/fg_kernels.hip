@@ -483,7 +483,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
         ok[u] = FULL || jb + gid < cnt;
-        const int src = bcast_lane<NG>(my_src, jb, gid);
+        const int src = __shfl(my_src, jb + gid);
         if constexpr (EIDS) eu[u] = bcast_lane<NG>(my_eid, jb, gid);
         else eu[u] = (int)(base + jb + gid);
         // the weight via the LDS crossbar (one permute) rather than two
