@@ -206,18 +206,26 @@ __device__ __forceinline__ void load_ids(const int32_t* ptr, int64_t len, int64_
 // Value of edge (jb + gid) of the batch (jb wave-uniform, gid < NG the
 // caller's lane group) when each lane holds Q consecutive edges; jb % Q is
 // c0, known after unrolling.
+// Two groups take their ids through one cross-lane permute (the vector unit,
+// which partly bounds the gather kernels, then only forms the lane index);
+// one group reads its id into a scalar register.
 template <int NG, int Q>
 __device__ __forceinline__ int bcast_q(const int32_t (&v)[Q], int jb, int c0, int gid) {
-  if constexpr (Q == 1) {
-    return bcast_lane<NG>(v[0], jb, gid);
-  } else if constexpr (NG == 1) {
+  if constexpr (NG == 1) {
     return __builtin_amdgcn_readlane(pick<Q>(v, c0), jb / Q);
+  } else if constexpr (NG == 2) {
+    if constexpr (Q == 1) {
+      return __shfl(v[0], jb + gid);
+    } else {
+      // c0 is even, so edges jb and jb + 1 sit in the same lane, as two of
+      // its registers: one permute each (the source lane supplies the value)
+      const int a = __shfl(pick<Q>(v, c0), jb / Q);
+      const int b = __shfl(pick<Q>(v, c0 + 1), jb / Q);
+      return gid ? b : a;
+    }
   } else {
-    static_assert(NG == 2, "four ids per lane serve one or two lane groups");
-    // c0 is even, so edges jb and jb + 1 sit in the same lane
-    const int a = __builtin_amdgcn_readlane(pick<Q>(v, c0), jb / Q);
-    const int b = __builtin_amdgcn_readlane(pick<Q>(v, c0 + 1), jb / Q);
-    return gid ? b : a;
+    static_assert(Q == 1, "four ids per lane serve one or two lane groups");
+    return bcast_lane<NG>(v[0], jb, gid);
   }
 }
 
