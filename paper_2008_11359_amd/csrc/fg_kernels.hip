@@ -49,9 +49,8 @@ struct BoolTag {
 // Offset of source row `src` in a [rows, F] array.  Both factors are
 // non-negative and below 2^32 (src < 2^31, F <= 65536), so one unsigned
 // 32 x 32 -> 64-bit multiply replaces the signed 64-bit product, which costs
-// two 32-bit multiplies, a 64-bit multiply-add and a sign extension.  Used by
-// the SDDMM and fused attention kernels; the gSpMM kernels keep the signed
-// product, with which they measured 2-4% faster.
+// two 32-bit multiplies, a 64-bit multiply-add and a sign extension (the
+// gather kernels are partly bound by vector instruction issue).
 __device__ __forceinline__ uint64_t row_off(int32_t src, int64_t F) {
   return (uint64_t)(uint32_t)src * (uint32_t)F;
 }
@@ -497,7 +496,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         // the weight via the LDS crossbar (one permute) rather than two
         // readlanes and a select on the vector unit
         const float w1 = MUL ? __shfl(my_w, jb + gid) : 1.0f;
-        const float* xr = p.x + (int64_t)src * F;
+        const float* xr = p.x + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
           if (FULL || (ok[u] && act[v])) {
