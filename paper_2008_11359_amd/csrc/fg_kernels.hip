@@ -167,13 +167,6 @@ __device__ __forceinline__ T pick(const T (&v)[Q], int c) {
 typedef int32_t int4_a4 __attribute__((ext_vector_type(4), aligned(4)));
 typedef float float4_a4 __attribute__((ext_vector_type(4), aligned(4)));
 
-// v[c] = x for a c known after unrolling (no indexed register access).
-template <int Q>
-__device__ __forceinline__ void put(float (&v)[Q], int c, float x) {
-#pragma unroll
-  for (int q = 0; q < Q; ++q)
-    if (q == c) v[q] = x;
-}
 
 // Edges base + Q*lane + q (q < Q) of a batch of `cnt` edges from a streamed
 // int32 array of `len` elements (non-temporal); 0 past cnt.  A lane with
@@ -923,6 +916,12 @@ template <int G, int NV, int U, bool SEG, bool WIDE = false>
 __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
   constexpr int NG = kWave / G;
   static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
+  constexpr int QB = WIDE ? ids_per_lane<NG, U>() : 1;
+  // one or two groups hand each edge's dot product over through this
+  // per-wavefront table (the group's last lane writes it; each lane reads
+  // its QB results after the batch) instead of readlanes and selects
+  __shared__ __align__(16) float res_all[NG <= 2 ? kWavesPerBlock * kWave * QB : 1];
+  float* res_tab = res_all + (NG <= 2 ? (threadIdx.x >> 6) * kWave * QB : 0);
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -963,7 +962,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
     // lane j collects the dot products of edges base + Q*j + q, so the batch's
     // results leave in one store instead of one store per step with one lane
     // per group active, which would cost the address unit as much as a
-    // gather: one or two groups hand their sums over with scalar readlanes,
+    // gather: one or two groups hand their sums over through the LDS table,
     // more groups with one cross-lane permute per step
     float res[Q];
 #pragma unroll
@@ -998,14 +997,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
         const int jb = j0 + u * NG;
         // the last lane of group g holds the sum of edge jb + g
         if constexpr (NG <= 2) {
-#pragma unroll
-          for (int g = 0; g < NG; ++g) {
-            if (jb + g < cnt) {
-              const int sum =
-                  __builtin_amdgcn_readlane(__builtin_bit_cast(int, part), (g + 1) * G - 1);
-              if (lane == (jb + g) / Q) put<Q>(res, (u * NG + g) % Q, __builtin_bit_cast(float, sum));
-            }
-          }
+          if (li == G - 1 && jb + gid < cnt) res_tab[jb + gid] = part;
         } else {
           const int rel = lane - jb;
           const bool mine = rel >= 0 && rel < NG && lane < cnt;
@@ -1013,6 +1005,19 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
           if (mine) res[0] = got;  // Q == 1 for more than two groups
         }
       }
+    }
+    if constexpr (NG <= 2) {
+      wave_lds_sync();  // the table holds the batch's results
+      if constexpr (Q == 4) {
+        const float4 t = *reinterpret_cast<const float4*>(res_tab + lane * Q);
+        res[0] = t.x;
+        res[1] = t.y;
+        res[2] = t.z;
+        res[3] = t.w;
+      } else {
+        res[0] = res_tab[lane];
+      }
+      wave_lds_sync();  // read before the next batch writes
     }
     bool stored = false;
     if constexpr (Q == 4) {
