@@ -473,8 +473,10 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
     }
     // one step of U edges per lane group; FULL: every edge of the step is in
     // the batch and every feature chunk in the row (no per-edge masking)
-    auto step = [&](int j0, auto full_tag) {
+    // H1: one head (weights broadcast from the batch; else loaded per edge)
+    auto step = [&](int j0, auto full_tag, auto h1_tag) {
       constexpr bool FULL = decltype(full_tag)::value;
+      constexpr bool H1 = decltype(h1_tag)::value;
       float val[U][NV][4];
       float wv[U][NV];
       int32_t eu[U];
@@ -488,7 +490,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         else eu[u] = (int)(base + jb + gid);
         // the weight via the LDS crossbar (one permute) rather than two
         // readlanes and a select on the vector unit
-        const float w1 = MUL ? __shfl(my_w, jb + gid) : 1.0f;
+        const float w1 = (MUL && H1) ? __shfl(my_w, jb + gid) : 1.0f;
         const float* xr = p.x + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
@@ -504,7 +506,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
             if constexpr (TAB)
               wv[u][v] = tab[(jb + gid) * p.H + hv[v]];
             else
-              wv[u][v] = (MUL && p.H != 1) ? p.ev[(int64_t)eu[u] * p.H + hv[v]] : w1;
+              wv[u][v] = (MUL && !H1) ? p.ev[(int64_t)eu[u] * p.H + hv[v]] : w1;
           } else {
 #pragma unroll
             for (int c = 0; c < 4; ++c) val[u][v][c] = MAX ? -INFINITY : 0.0f;
@@ -540,10 +542,15 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
     };
     // full steps (wave-uniform test) take the unmasked body
     const bool all_feat = c0 + (int64_t)G * 4 * NV <= F;
-    int j0 = 0;
-    if (all_feat)
-      for (; j0 + NG * U <= cnt; j0 += NG * U) step(j0, BoolTag<true>{});
-    for (; j0 < cnt; j0 += NG * U) step(j0, BoolTag<false>{});
+    auto steps = [&](auto h1_tag) {
+      int j0 = 0;
+      if (all_feat)
+        for (; j0 + NG * U <= cnt; j0 += NG * U) step(j0, BoolTag<true>{}, h1_tag);
+      for (; j0 < cnt; j0 += NG * U) step(j0, BoolTag<false>{}, h1_tag);
+    };
+    // (without weights, or with a table, the head count plays no part)
+    if (!MUL || TAB || p.H == 1) steps(BoolTag<true>{});
+    else steps(BoolTag<false>{});
   }
   if constexpr (POS) {
     const int64_t first = it.b + gid;  // this group's first edge
