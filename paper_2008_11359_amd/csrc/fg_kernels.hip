@@ -954,6 +954,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
     }
   }
 
+  const bool all_feat = (int64_t)G * 4 * NV <= F;
   constexpr int Q = WIDE ? ids_per_lane<NG, U>() : 1;
   static_assert((NG * U) % Q == 0, "every step starts on a lane's first edge");
   for (int64_t base = it.b; base < it.e; base += Q * kWave) {
@@ -974,18 +975,21 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
     float res[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) res[q] = 0.0f;
-    for (int j0 = 0; j0 < cnt; j0 += NG * U) {
+    // one step of U edges per lane group; FULL: every edge of the step is in
+    // the batch and every feature chunk in the row (no per-edge masking)
+    auto step = [&](int j0, auto full_tag) {
+      constexpr bool FULL = decltype(full_tag)::value;
       float val[U][NV][4];
       bool ok[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
-        ok[u] = jb + gid < cnt;
+        ok[u] = FULL || jb + gid < cnt;
         const int src = bcast_q<NG, Q>(my_src, jb, (u * NG) % Q, gid);
         const float* xr = p.xs + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
-          if (ok[u] && act[v]) {
+          if (FULL || (ok[u] && act[v])) {
             load_vec<4>(xr + f[v], val[u][v]);
           } else {
 #pragma unroll
@@ -1004,7 +1008,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
         const int jb = j0 + u * NG;
         // the last lane of group g holds the sum of edge jb + g
         if constexpr (NG <= 2) {
-          if (li == G - 1 && jb + gid < cnt) res_tab[jb + gid] = part;
+          if (li == G - 1 && (FULL || jb + gid < cnt)) res_tab[jb + gid] = part;
         } else {
           const int rel = lane - jb;
           const bool mine = rel >= 0 && rel < NG && lane < cnt;
@@ -1012,7 +1016,12 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
           if (mine) res[0] = got;  // Q == 1 for more than two groups
         }
       }
-    }
+    };
+    // full steps (wave-uniform test) take the unmasked body
+    int j0 = 0;
+    if (all_feat)
+      for (; j0 + NG * U <= cnt; j0 += NG * U) step(j0, BoolTag<true>{});
+    for (; j0 < cnt; j0 += NG * U) step(j0, BoolTag<false>{});
     if constexpr (NG <= 2) {
       wave_lds_sync();  // the table holds the batch's results
       if constexpr (Q == 4) {
