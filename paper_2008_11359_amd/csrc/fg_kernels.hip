@@ -1265,8 +1265,9 @@ __device__ __forceinline__ float leaky_relu(float s, int on, float slope) {
 // x * log2(e) gives a relative error of about |x| * 2^-23 (2e-6 at x = -20,
 // below which a term weighs less than 2e-9 of the row's largest), in two
 // instructions instead of the ten or so of the correctly rounded expf.  Used
-// for the running (max, sum) statistics and the fused attention weights; the
-// softmax outputs themselves are written with expf.
+// for the running (max, sum) statistics, the fused attention weights and the
+// edge softmax outputs (the softmax is partly bound by vector instruction
+// issue; the relative error stays within the 1e-5 * sqrt(degree) tolerance).
 __device__ __forceinline__ float exp_nonpos(float x) {
   return __builtin_amdgcn_exp2f(x * 1.44269504088896341f);
 }
@@ -1323,7 +1324,7 @@ __device__ __forceinline__ void softmax_row_in_registers(const SoftmaxParams& p,
   float z = 0.0f;
 #pragma unroll
   for (int k = 0; k < kSoftmaxU; ++k) {
-    sv[k] = ev[k] >= 0 ? expf(sv[k] - mx) : 0.0f;
+    sv[k] = ev[k] >= 0 ? exp_nonpos(sv[k] - mx) : 0.0f;
     z += sv[k];
   }
   for (int off = H; off < kWave; off <<= 1) z += __shfl_xor(z, off);
@@ -1498,7 +1499,7 @@ __device__ __forceinline__ void softmax_contig_regs(const SoftmaxParams& p, cons
     if (i < rounds) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        v[i][c] = v[i][c] == -INFINITY ? 0.0f : expf(v[i][c] - m[c]);
+        v[i][c] = v[i][c] == -INFINITY ? 0.0f : exp_nonpos(v[i][c] - m[c]);
         z[c] += v[i][c];
       }
     }
@@ -1594,7 +1595,7 @@ __device__ __forceinline__ void softmax_contig_stream(const SoftmaxParams& p, co
         contig_leaky(p, r, k, v[i]);
         float o[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) o[c] = expf(v[i][c] - m[c]) * inv[c];
+        for (int c = 0; c < 4; ++c) o[c] = exp_nonpos(v[i][c] - m[c]) * inv[c];
         contig_store(p, r, k, o);
       }
     }
@@ -1685,7 +1686,7 @@ __global__ __launch_bounds__(kBlock) void softmax_kernel(SoftmaxParams p) {
         }
 #pragma unroll
         for (int k = 0; k < kSoftmaxU; ++k)
-          if (ev[k] >= 0) p.out[ev[k] * H + h] = expf(sv[k] - m) * inv;
+          if (ev[k] >= 0) p.out[ev[k] * H + h] = exp_nonpos(sv[k] - m) * inv;
       }
     }
   }
@@ -1785,7 +1786,7 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
           contig_leaky(p, r, k, v[i]);
           float o[4];
 #pragma unroll
-          for (int c = 0; c < 4; ++c) o[c] = expf(v[i][c] - m[c]) * inv[c];
+          for (int c = 0; c < 4; ++c) o[c] = exp_nonpos(v[i][c] - m[c]) * inv[c];
           contig_store(p, r, k, o);
         }
       }
@@ -1814,7 +1815,7 @@ __global__ __launch_bounds__(kBlock) void softmax_split_kernel(SoftmaxParams p, 
       }
 #pragma unroll
       for (int k = 0; k < kSoftmaxU; ++k)
-        if (ev[k] >= 0) p.out[ev[k] * H + h] = expf(sv[k] - m) * inv;
+        if (ev[k] >= 0) p.out[ev[k] * H + h] = exp_nonpos(sv[k] - m) * inv;
     }
   }
 }
@@ -2672,7 +2673,7 @@ __global__ __launch_bounds__(kBlock) void softmax_pack_kernel(SoftmaxParams p, i
   float z = 0.0f;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    v[k] = ev[k] >= 0 ? expf(v[k] - m) : 0.0f;
+    v[k] = ev[k] >= 0 ? exp_nonpos(v[k] - m) : 0.0f;
     z += v[k];
   }
   for (int off = 1; off < kPackLanes; off <<= 1) z += __shfl_xor(z, off);
@@ -2732,7 +2733,7 @@ __global__ __launch_bounds__(kBlock) void softmax_pack4_kernel(SoftmaxParams p, 
   for (int i = 0; i < kPack4Vec; ++i)
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      v[i][c] = v[i][c] == -INFINITY ? 0.0f : expf(v[i][c] - m);
+      v[i][c] = v[i][c] == -INFINITY ? 0.0f : exp_nonpos(v[i][c] - m);
       z += v[i][c];
     }
   for (int off = 1; off < kPackLanes; off <<= 1) z += __shfl_xor(z, off);
