@@ -2841,6 +2841,7 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
   const int h = act ? (int)(f / p.dh) : 0;
   float xd[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (act) load_vec<4>(p.xd + it.row * F + f, xd);
+  const bool all_act = (int64_t)G * 4 <= F;  // every lane holds a feature chunk
   float m = -INFINITY, z = 0.0f;
   float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 
@@ -2848,15 +2849,19 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
     const int cnt = (int)min((int64_t)kWave, it.e - base);
     int my_src = 0;
     if (lane < cnt) my_src = __builtin_nontemporal_load(p.indices + base + lane);
-    for (int j0 = 0; j0 < cnt; j0 += NG * U) {
+    // one step of U edges per lane group; FULL: all of them in the batch and
+    // every lane active (no masking)
+    auto step = [&](int j0, auto full_tag) {
+      constexpr bool FULL = decltype(full_tag)::value;
       float val[U][4];
       bool ok[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
-        ok[u] = jb + gid < cnt;
-        const int src = bcast_lane<NG>(my_src, jb, gid);
-        if (ok[u] && act) {
+        ok[u] = FULL || jb + gid < cnt;
+        // (two or fewer groups: one cross-lane permute, off the vector ALU)
+        const int src = NG <= 2 ? __shfl(my_src, jb + gid) : bcast_lane<NG>(my_src, jb, gid);
+        if (FULL || (ok[u] && act)) {
           load_vec<4>(p.xs + row_off(src, F) + f, val[u]);
         } else {
 #pragma unroll
@@ -2868,7 +2873,7 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
         float part = val[u][0] * xd[0] + val[u][1] * xd[1] + val[u][2] * xd[2] + val[u][3] * xd[3];
         float sc = SH == 1 ? part : group_allsum<SH>(part);
         sc = leaky_relu(sc, p.leaky, p.slope);
-        if (ok[u]) {
+        if (FULL || ok[u]) {
           if (sc > m) {  // new maximum: move the state to it (m = -inf: a = 0)
             const float a = exp_nonpos(m - sc);
             z *= a;
@@ -2882,7 +2887,11 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
           for (int c = 0; c < 4; ++c) acc[c] = fmaf(b, val[u][c], acc[c]);
         }
       }
-    }
+    };
+    int j0 = 0;
+    if (all_act)
+      for (; j0 + NG * U <= cnt; j0 += NG * U) step(j0, BoolTag<true>{});
+    for (; j0 < cnt; j0 += NG * U) step(j0, BoolTag<false>{});
   }
   // merge the lane groups
   for (int s = G; s < kWave; s <<= 1) {
