@@ -1483,3 +1483,35 @@ def test_rmat_train_step_full():
     check_spmm(csr, Gf, x, rows=rows_f, plan=af)
     check_spmm(csc, Gb, dy, rows=rows_b, plan=ab, nnz_total=csr.nnz)
     check_sddmm(csr, Gf, x, dy, rows=rows_f, plan=af)
+
+
+def test_sddmm_wide_batches_with_edge_ids_and_ragged_ends():
+    """The SDDMM's 256-edge batches (items of 128 edges or more on average)
+    on a transposed graph with explicit edge ids (ids loaded four per lane,
+    scores stored one by one through them) and on its CSR (positional
+    16-byte stores): row lengths that are not multiples of 4 or of 256, and
+    a stored-edge count that is not a multiple of 4, so the last lane of the
+    last item reads its ids one by one.  Also the plain one-edge batches on
+    the same graphs (short items), and the sum and max gSpMM on them."""
+    rng = np.random.default_rng(77)
+    n, m = 700, 900
+    deg = rng.integers(150, 420, size=n)
+    deg[-1] = 389  # a long last row whose end is not 4-aligned
+    dst = np.repeat(np.arange(n), deg)
+    src = rng.integers(0, m, size=dst.size)
+    assert dst.size % 4 != 0
+    csr = synth.coo_to_csr(dst.astype(np.int64), src.astype(np.int64), n, m)
+    csc = csr_to_csc(csr)
+    for d in (128, 256):
+        xs = rng.standard_normal((m, d)).astype(np.float32)
+        xd = rng.standard_normal((n, d)).astype(np.float32)
+        G = fg.Graph.from_csr(csr)
+        for plan in (fg.Plan(G, d), fg.Plan(G, d, segment_edges=64)):
+            say("wide-batch SDDMM CSR d=%d items=%d" % (d, plan.info()["num_segments"]))
+            check_sddmm(csr, G, xs, xd, plan=plan)
+            check_spmm(csr, G, xs, plan=plan)
+            check_spmm(csr, G, xs, plan=plan, reduce="max")
+        Gt = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+        for plan in (fg.Plan(Gt, d), fg.Plan(Gt, d, segment_edges=64)):
+            say("wide-batch SDDMM CSC d=%d items=%d" % (d, plan.info()["num_segments"]))
+            check_sddmm(csc, Gt, xd, xs, plan=plan, nnz_total=csr.nnz)
