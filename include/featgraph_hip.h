@@ -110,7 +110,8 @@ typedef struct fg_graph {
  * power-law graphs, and revives its 1D source partitioning (Sec. III-C, graph
  * partitioning) for the caches of each MI355X die.
  *
- * A plan holds two schedules over one workspace:
+ * A plan holds two schedules over one workspace, and a third for the SDDMM
+ * on some graphs:
  *  - plain (edge softmax): rows with more than S edges are cut into
  *    k = min(ceil(deg / S), max_row_segments) equal segments, S =
  *    softmax_segment_edges if given, else segment_edges if given, else 16384
@@ -136,6 +137,12 @@ typedef struct fg_graph {
  *    of their own (sources spread uniformly, or features beyond the Infinity
  *    Cache) and costs more than it saves on graphs with hubs or communities
  *    whose features the caches hold, hence the size threshold.
+ *  - the SDDMM's own (only on spread graphs with source slabs, a max_width
+ *    of 256 floats or more and num_cols x max_width features of at most
+ *    256 MiB, the Infinity Cache): every row cut where its sources change
+ *    slab (16 slabs of about equal edge shares), no partial-result slots;
+ *    fg_gsddmm runs it for H * head_dim >= 256, the gather schedule
+ *    otherwise.
  * Items of rows cut in several pieces write partial results that a second
  * pass merges in a fixed order, so results are deterministic for a plan.
  * ------------------------------------------------------------------------- */
@@ -207,6 +214,8 @@ typedef struct fg_plan_info {
   int32_t item_order;           /* the order used: 1, 2 or 3 (see fg_plan_options)   */
   int32_t max_backward;         /* 1 if the binned max-backward workspace is held    */
   uint64_t indptr_checksum;     /* fg_indptr_checksum of the indptr it was built for */
+  int64_t sddmm_segments;       /* the SDDMM's own schedule: work items; 0: none (the
+                                   gather schedule serves it)                       */
 } fg_plan_info;
 
 /* One work item of a schedule (host view; the device tables hold the same). */
@@ -218,7 +227,9 @@ typedef struct fg_segment {
                     >= 0: partial-result slot of a row cut in several pieces   */
 } fg_segment;
 
-/* Builds a schedule on the host (which = 0: gather, 1: plain) from HOST
+/* Builds a schedule on the host (which = 0: gather, 1: plain, 2: the SDDMM's,
+ * which is the gather schedule where the plan has no schedule of its own for
+ * it) from HOST
  * copies of indptr and (optional; NULL: no source partitioning) indices.
  * Writes at most `capacity` items to `segs` (may be NULL to only count) and
  * the counts to the optional out-pointers.  Pure host function: no HIP call. */

@@ -84,6 +84,7 @@ class _PlanInfo(ctypes.Structure):
         ("item_order", ctypes.c_int32),
         ("max_backward", ctypes.c_int32),
         ("indptr_checksum", ctypes.c_uint64),
+        ("sddmm_segments", ctypes.c_int64),
     ]
 
 
@@ -364,7 +365,7 @@ def schedule_host(indptr: np.ndarray, indices: Optional[np.ndarray] = None, num_
     ip = np.ascontiguousarray(indptr, dtype=np.int32)
     ix = None if indices is None else np.ascontiguousarray(indices, dtype=np.int32)
     opt = _options(**options)
-    w = {"gather": 0, "plain": 1}[which]
+    w = {"gather": 0, "plain": 1, "sddmm": 2}[which]
     args = (ip.ctypes.data, None if ix is None else ix.ctypes.data, ip.size - 1, int(num_cols),
             int(max_width), ctypes.byref(opt), w)
     n_seg, n_split, n_slot = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()

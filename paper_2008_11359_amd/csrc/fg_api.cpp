@@ -25,6 +25,7 @@ struct fg_plan {
   int32_t item_order = 0;  // 1: longest first, 2: length classes, rows in id order
   int device = 0;
   fg::PlanView gather, plain;
+  fg::PlanView edge;  // the SDDMM's own schedule on spread graphs (num_segments 0: none)
   // graphs with explicit edge ids: edge id -> storage position (the max
   // gradient needs the source of an edge given its id)
   const int32_t* edge_ids = nullptr;
@@ -249,6 +250,17 @@ double hot_source_share(const int32_t* ix, int64_t nnz, int64_t num_cols, int64_
 // rand-100K and uniform graphs at d = 128: 35% and 10%, cut.)
 constexpr double kSpreadShare = 0.45;
 constexpr int64_t kDieL2Bytes = 4 << 20;
+// Spread graphs with source slabs at widths of this many floats or more, and
+// features that the Infinity Cache holds, get a schedule of their own for
+// the SDDMM: every row cut where its sources change slab (kEdgeSlabs slabs of
+// about equal edge shares), with no merge to pay since the SDDMM writes
+// per-edge results.  (The uniform graph's SDDMM: 1.36 -> 0.89 ms at d = 256,
+// 2.76 -> 2.43 ms at d = 512; rand-100K's 5.62 -> 4.55 ms at d = 512.  At
+// d = 128 the cut costs more than it gains, 0.40 -> 0.56 ms, and so it does
+// on the 1M-vertex R-MAT graph's 1 GiB of features, 2.39 -> 2.90 ms.)
+constexpr int64_t kEdgeScheduleMinWidth = 256;
+constexpr int64_t kEdgeSlabs = 16;
+constexpr int64_t kInfinityCacheBytes = int64_t(256) << 20;
 
 struct Options {
   int32_t S, cap, slab, min_deg;  // slab 0: no source partitioning
@@ -260,6 +272,8 @@ struct Options {
   bool slab_if_spread;            // keep the slabs only if the gathers are spread
   bool max_backward;              // reserve the binned max-backward workspace
   int32_t band_rows;              // die-banded: rows of more edges get >= kXcds pieces (-1: off)
+  bool spread = false;            // slabs on spread gathers at a wide max_width whose features
+                                  // the Infinity Cache holds: the SDDMM gets its own schedule
 };
 
 // Settles the automatic choices that depend on the graph: the item order and
@@ -273,11 +287,21 @@ void settle_options(Options& o, const int32_t* ip, const int32_t* ix, int64_t nu
     o.order = id_local == 1 ? kOrderById : kOrderByLength;
     o.band_auto = o.order == kOrderByLength;
   }
+  const int64_t rows = kDieL2Bytes / (4 * std::max<int64_t>(max_width, 1));
+  double share = -1.0;  // hot_source_share, computed once if needed
   if (o.slab_if_spread) {
-    const int64_t rows = kDieL2Bytes / (4 * std::max<int64_t>(max_width, 1));
-    if (!ix || id_local != 0 || hot_source_share(ix, ip[num_rows], num_cols, rows) >= kSpreadShare)
+    if (!ix || id_local != 0 || (share = hot_source_share(ix, ip[num_rows], num_cols, rows)) >= kSpreadShare)
       o.slab = 0;
     o.slab_if_spread = false;
+  }
+  o.spread = false;
+  if (ix && o.slab > 0 && max_width >= kEdgeScheduleMinWidth &&
+      num_cols * max_width * 4 <= kInfinityCacheBytes) {
+    if (id_local < 0) id_local = ids_share_sources_host(ip, ix, num_rows) ? 1 : 0;
+    if (id_local == 0) {
+      if (share < 0.0) share = hot_source_share(ix, ip[num_rows], num_cols, rows);
+      o.spread = share < kSpreadShare;
+    }
   }
 }
 
@@ -621,7 +645,8 @@ fg_status read_options(const fg_plan_options* opt, int64_t num_cols, int64_t max
 
 // Both schedules of a graph.  indices may be null: no source partitioning.
 fg_status make_schedules(const int32_t* ip, const int32_t* ix, int64_t num_rows, int64_t num_cols,
-                         const Options& o, Schedule& gather, Schedule& plain) {
+                         const Options& o, Schedule& gather, Schedule& plain,
+                         Schedule* edge = nullptr) {
   try {
     Options op = o;
     op.S = o.S_plain;
@@ -642,6 +667,22 @@ fg_status make_schedules(const int32_t* ip, const int32_t* ix, int64_t num_rows,
       }
       gather.partitioned_rows = 0;
       if (band) band_by_die(gather);
+    }
+    if (edge) {
+      // the SDDMM's schedule on spread graphs: every row cut at slab
+      // boundaries; its per-edge results need no slots
+      *edge = Schedule();
+      Options oe = o;
+      oe.slab = (int32_t)std::max<int64_t>(1, (num_cols + kEdgeSlabs - 1) / kEdgeSlabs);
+      oe.min_deg = 1;
+      if (ix && o.spread && build_partitioned(ip, ix, num_rows, num_cols, oe, *edge)) {
+        for (fg::Seg& sg : edge->segs) sg.slot = -1;
+        edge->fix.clear();
+        edge->slot_fix.clear();
+        edge->slot_seg.clear();
+      } else {
+        *edge = Schedule();
+      }
     }
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
@@ -680,7 +721,7 @@ fg_status fg_schedule_host(const int32_t* indptr_host, const int32_t* indices_ho
                            int64_t capacity, int64_t* num_segments, int64_t* num_split_rows,
                            int64_t* num_slots) {
   if (!indptr_host || num_rows < 0 || num_rows >= INT32_MAX || num_cols < 0 ||
-      num_cols > INT32_MAX || capacity < 0 || (which != 0 && which != 1))
+      num_cols > INT32_MAX || capacity < 0 || which < 0 || which > 2)
     return FG_ERR_INVALID_ARG;
   if (max_width < 1 || max_width > FG_MAX_WIDTH) return FG_ERR_INVALID_ARG;
   Options o;
@@ -694,11 +735,12 @@ fg_status fg_schedule_host(const int32_t* indptr_host, const int32_t* indices_ho
   } catch (const std::bad_alloc&) {
     return FG_ERR_NO_MEMORY;
   }
-  Schedule gather, plain;
-  if ((st = make_schedules(indptr_host, indices_host, num_rows, num_cols, o, gather, plain)) !=
-      FG_OK)
+  Schedule gather, plain, edge;
+  if ((st = make_schedules(indptr_host, indices_host, num_rows, num_cols, o, gather, plain,
+                           &edge)) != FG_OK)
     return st;
-  const Schedule& sc = which == 0 ? gather : plain;
+  // which 2: the SDDMM's schedule (the gather schedule where it has none)
+  const Schedule& sc = which == 1 ? plain : (which == 2 && !edge.segs.empty() ? edge : gather);
   if (num_segments) *num_segments = (int64_t)sc.segs.size();
   if (num_split_rows) *num_split_rows = (int64_t)sc.fix.size();
   if (num_slots) *num_slots = (int64_t)sc.slot_fix.size();
@@ -845,8 +887,8 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
   if (o.slab_if_spread) o.slab = 0;  // (conditional slabs always come with host indices)
   if (o.slab <= 0) ix = nullptr;
 
-  Schedule gather, plain;
-  if ((st = make_schedules(ip, ix, g->num_rows, g->num_cols, o, gather, plain)) != FG_OK)
+  Schedule gather, plain, edge;
+  if ((st = make_schedules(ip, ix, g->num_rows, g->num_cols, o, gather, plain, &edge)) != FG_OK)
     return st;
   fg_plan* p = nullptr;
   try {
@@ -870,7 +912,8 @@ fg_status fg_plan_create(const fg_graph* g, const int32_t* indptr_host,
     return FG_ERR_HIP;
   }
   if ((st = upload(p, gather, p->gather, hs)) != FG_OK ||
-      (st = upload(p, plain, p->plain, hs)) != FG_OK) {
+      (st = upload(p, plain, p->plain, hs)) != FG_OK ||
+      (!edge.segs.empty() && (st = upload(p, edge, p->edge, hs)) != FG_OK)) {
     (void)hipStreamSynchronize(hs);
     fg_plan_destroy(p);
     return st;
@@ -975,6 +1018,7 @@ fg_status fg_plan_get_info(const fg_plan* plan, fg_plan_info* info) {
   info->item_order = plan->item_order;
   info->max_backward = plan->bin.rec ? 1 : 0;
   info->indptr_checksum = plan->indptr_sum;
+  info->sddmm_segments = plan->edge.num_segments;
   return FG_OK;
 }
 
@@ -1099,8 +1143,12 @@ fg_status fg_gsddmm(const fg_graph* g, fg_edge_op op, int32_t num_heads, int64_t
       overlaps(out, out_b, x_dst, g->num_rows * F * 4))
     return FG_ERR_INVALID_ARG;
   const fg::GraphView gv = view_of(g);
-  return from_hip(fg::launch_gsddmm(gv, plan ? &plan->gather : nullptr, num_heads, head_dim, x_src,
-                                    x_dst, out, static_cast<hipStream_t>(stream)));
+  // wide rows of a spread graph: the plan's SDDMM schedule, if it has one
+  const fg::PlanView* v = nullptr;
+  if (plan)
+    v = (plan->edge.num_segments > 0 && F >= kEdgeScheduleMinWidth) ? &plan->edge : &plan->gather;
+  return from_hip(fg::launch_gsddmm(gv, v, num_heads, head_dim, x_src, x_dst, out,
+                                    static_cast<hipStream_t>(stream)));
 }
 
 fg_status fg_edge_softmax(const fg_graph* g, int32_t num_heads, const float* scores,

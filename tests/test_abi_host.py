@@ -681,3 +681,40 @@ def test_die_banded_cuts_mid_length_rows(T, cap):
     die = (np.nonzero(~pad)[0] // 4) % 8
     for row in np.nonzero(want == 8)[0][:200]:
         assert sorted(die[real[:, 0] == row].tolist()) == list(range(8))
+
+
+def test_sddmm_schedule_on_spread_graphs():
+    """With source slabs, a spread graph (no hot sources, no locality along
+    row ids) and max_width >= 256, the plan's SDDMM schedule cuts every row
+    where its sources change slab (slabs of at most ceil(num_cols / 16) ids),
+    with no partial-result slots; otherwise it is the gather schedule."""
+    rng = np.random.default_rng(5)
+    n, m, d = 3000, 30000, 100
+    dst = np.repeat(np.arange(n), d)
+    src = rng.integers(0, m, size=n * d)
+    c = synth.coo_to_csr(dst.astype(np.int64), src.astype(np.int64), n, m)
+    kw = dict(source_slab_rows=4096)
+    edge, e_split, e_slot = fg.schedule_host(c.indptr, c.indices, m, 256, "sddmm", **kw)
+    gather, *_ = fg.schedule_host(c.indptr, c.indices, m, 256, "gather", **kw)
+    assert e_split == 0 and e_slot == 0
+    real = edge[edge[:, 0] >= 0]
+    assert np.all(real[:, 3] == -1)
+    cover = np.zeros(c.nnz, np.int32)
+    for r, b, e, _ in real:
+        assert c.indptr[r] <= b < e <= c.indptr[r + 1]
+        cover[b:e] += 1
+        s = c.indices[b:e]
+        assert s.max() - s.min() < -(-m // 16)  # inside one slab
+    assert np.all(cover == 1)
+    pieces = np.bincount(real[:, 0], minlength=n)
+    assert pieces.mean() > 8 and real.shape[0] > gather[gather[:, 0] >= 0].shape[0]
+    # below 256 floats, or without slabs: the gather schedule serves the SDDMM
+    for width, opts in ((128, kw), (256, {})):
+        a, *_ = fg.schedule_host(c.indptr, c.indices, m, width, "sddmm", **opts)
+        b, *_ = fg.schedule_host(c.indptr, c.indices, m, width, "gather", **opts)
+        np.testing.assert_array_equal(a, b)
+    # a power-law graph (hot sources) keeps the gather schedule too
+    p = synth.make_config("rmat_233k_115m", scale_down=64).csr
+    a, *_ = fg.schedule_host(p.indptr, p.indices, p.num_cols, 256, "sddmm", source_slab_rows=64)
+    b, *_ = fg.schedule_host(p.indptr, p.indices, p.num_cols, 256, "gather", source_slab_rows=64)
+    np.testing.assert_array_equal(a, b)

@@ -1515,3 +1515,30 @@ def test_sddmm_wide_batches_with_edge_ids_and_ragged_ends():
         for plan in (fg.Plan(Gt, d), fg.Plan(Gt, d, segment_edges=64)):
             say("wide-batch SDDMM CSC d=%d items=%d" % (d, plan.info()["num_segments"]))
             check_sddmm(csc, Gt, xd, xs, plan=plan, nnz_total=csr.nnz)
+
+
+def test_sddmm_own_schedule_on_spread_graph():
+    """A spread graph with source slabs at d >= 256: the plan holds a schedule
+    of its own for the SDDMM (every row cut at slab boundaries, no slots),
+    which fg_gsddmm runs; checked on every row, on the CSR and on the CSC
+    with explicit edge ids, and the gSpMM of the same plan alongside."""
+    rng = np.random.default_rng(9)
+    n, m, deg = 3000, 30000, 100
+    dst = np.repeat(np.arange(n), deg)
+    src = rng.integers(0, m, size=n * deg)
+    csr = synth.coo_to_csr(dst.astype(np.int64), src.astype(np.int64), n, m)
+    csc = csr_to_csc(csr)
+    for d in (256, 512):
+        xs = rng.standard_normal((m, d)).astype(np.float32)
+        xd = rng.standard_normal((n, d)).astype(np.float32)
+        G = fg.Graph.from_csr(csr)
+        plan = fg.Plan(G, d, source_slab_rows=4096)
+        info = plan.info()
+        say("SDDMM schedule d=%d: %d items (gather %d)" % (d, info["sddmm_segments"],
+                                                          info["num_segments"]))
+        assert info["sddmm_segments"] > info["num_segments"]
+        check_sddmm(csr, G, xs, xd, plan=plan)
+        check_spmm(csr, G, xs, plan=plan)
+        Gt = fg.Graph.from_csr(csc, nnz_total=csr.nnz)
+        pt = fg.Plan(Gt, d, source_slab_rows=4096)
+        check_sddmm(csc, Gt, xd, xs, plan=pt, nnz_total=csr.nnz)
