@@ -144,13 +144,11 @@ __device__ __forceinline__ float bcast_lane_f(float v, int jb, int gid) {
   return __builtin_bit_cast(float, bcast_lane<NG>(__builtin_bit_cast(int, v), jb, gid));
 }
 
-// Wide batches of Q * 64 edges (the SDDMM on long items): lane l holds edges
-// Q*l .. Q*l + Q - 1 of the batch (Q = 4 for one or two lane groups, else 1),
-// so the ids of 256 edges arrive in one 16-byte load per lane and their
-// results leave in one 16-byte store: the address unit that bounds the
-// gather kernels spends one instruction on each instead of four.  (The
-// gSpMM kernels keep 64-edge batches: the extra registers cost them more
-// occupancy than the instructions save.)
+// Wide batches of Q * 64 edges (gather kernels on long items): lane l holds
+// edges Q*l .. Q*l + Q - 1 of the batch (Q = 4 for one or two lane groups,
+// else 1), so the ids of 256 edges arrive in one 16-byte load per lane (and
+// the SDDMM's results leave in one 16-byte store): the address unit that
+// bounds the gather kernels spends one instruction on each instead of four.
 template <int NG, int U>
 constexpr int ids_per_lane() { return NG <= 2 && (NG * U) % 4 == 0 ? 4 : 1; }
 
@@ -197,27 +195,54 @@ __device__ __forceinline__ void load_ids(const int32_t* ptr, int64_t len, int64_
 
 // Value of edge (jb + gid) of the batch (jb wave-uniform, gid < NG the
 // caller's lane group) when each lane holds Q consecutive edges; jb % Q is
-// c0, known after unrolling.
-// Two groups take their ids through one cross-lane permute (the vector unit,
-// which partly bounds the gather kernels, then only forms the lane index);
-// one group reads its id into a scalar register.
+// c0, known after unrolling.  One group reads its id into a scalar
+// register; two groups take theirs through one cross-lane permute (the
+// vector unit, which partly bounds the gather kernels, then only forms the
+// lane index).  Two groups with four ids per lane use the LDS table below.
 template <int NG, int Q>
 __device__ __forceinline__ int bcast_q(const int32_t (&v)[Q], int jb, int c0, int gid) {
   if constexpr (NG == 1) {
     return __builtin_amdgcn_readlane(pick<Q>(v, c0), jb / Q);
-  } else if constexpr (NG == 2) {
-    if constexpr (Q == 1) {
-      return __shfl(v[0], jb + gid);
-    } else {
-      // c0 is even, so edges jb and jb + 1 sit in the same lane, as two of
-      // its registers: one permute each (the source lane supplies the value)
-      const int a = __shfl(pick<Q>(v, c0), jb / Q);
-      const int b = __shfl(pick<Q>(v, c0 + 1), jb / Q);
-      return gid ? b : a;
-    }
   } else {
-    static_assert(Q == 1, "four ids per lane serve one or two lane groups");
-    return bcast_lane<NG>(v[0], jb, gid);
+    static_assert(Q == 1, "four ids per lane: one group, or the LDS table for two");
+    if constexpr (NG == 2) return __shfl(v[0], jb + gid);
+    else return bcast_lane<NG>(v[0], jb, gid);
+  }
+}
+
+// Wide batches of two lane groups keep their 256 ids (or weights) in a
+// per-wavefront LDS table, group by group: edge k of the batch at
+// (k & 1) * kWideHalf + k / 2, so that group g's edges of a step (j0 + 2u + g,
+// u < U) are U consecutive entries, read with U / 4 16-byte LDS reads instead
+// of one cross-lane permute (and a select) per edge.  The 4-entry pad between
+// the halves puts the two groups' reads of one step in different banks.
+constexpr int kWideHalf = 2 * kWave + 4;
+constexpr int kWideTab = 2 * kWideHalf;
+
+// Lane l holds edges 4l .. 4l + 3 of the batch: 4l and 4l + 2 go to group
+// 0's half, 4l + 1 and 4l + 3 to group 1's.
+template <typename T>
+__device__ __forceinline__ void wide_put(T* tab, int lane, const int32_t (&q)[4]) {
+  static_assert(sizeof(T) == 4, "4-byte entries");
+  int32_t* t = reinterpret_cast<int32_t*>(tab);
+  *reinterpret_cast<int2*>(t + 2 * lane) = make_int2(q[0], q[2]);
+  *reinterpret_cast<int2*>(t + kWideHalf + 2 * lane) = make_int2(q[1], q[3]);
+}
+
+// Group gid's U entries of the step that starts at batch edge j0 (a multiple
+// of 2U, so the reads are 16-byte aligned).
+template <int U, typename T>
+__device__ __forceinline__ void wide_get(const T* tab, int gid, int j0, T (&out)[U]) {
+  static_assert(U % 4 == 0, "whole 16-byte reads");
+  const T* t = tab + gid * kWideHalf + j0 / 2;
+#pragma unroll
+  for (int k = 0; k < U; k += 4) {
+    typedef T T4 __attribute__((ext_vector_type(4)));
+    const T4 v = *reinterpret_cast<const T4*>(t + k);
+    out[k] = v.x;
+    out[k + 1] = v.y;
+    out[k + 2] = v.z;
+    out[k + 3] = v.w;
   }
 }
 
@@ -238,6 +263,7 @@ struct SpmmParams {
   float* ws_f;
   int32_t* ws_i;
   int64_t n_items;
+  int64_t nnz;      // length of indices (and of ev with one head and positional ids)
   int64_t F;
   int32_t H;
   int32_t dh;
@@ -342,12 +368,25 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
 // reads its weights from there; loading them per step would add one more
 // vector-memory instruction per gather, and the address unit is what bounds
 // these kernels.
+//
+// WIDE (two lane groups, positional ids, one head): 256-edge batches whose
+// ids (and weights) arrive four per lane in one 16-byte load (a quarter of
+// the id loads for the address unit) and go to the group-major LDS table.
+// Without weights they are held to 7 wavefronts per SIMD (72 registers): the
+// max kernel otherwise takes 85 (5 wavefronts), with no spill either way.
 template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool SEG, bool ADD = false,
-          bool TAB = false>
-__global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
+          bool TAB = false, bool WIDE = false>
+__global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kernel(SpmmParams p) {
   constexpr int NG = kWave / G;
   constexpr bool POS = MAX && !EIDS;
   static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
+  static_assert(!WIDE || (NG == 2 && U % 4 == 0 && !EIDS && !TAB),
+                "wide batches serve two lane groups with positional ids");
+  constexpr int BATCH = WIDE ? 4 * kWave : kWave;
+  __shared__ __align__(16) int32_t wid_all[WIDE ? kWavesPerBlock * kWideTab : 1];
+  __shared__ __align__(16) float wwt_all[WIDE && MUL ? kWavesPerBlock * kWideTab : 1];
+  int32_t* wid = wid_all + (WIDE ? (threadIdx.x >> 6) * kWideTab : 0);
+  float* wwt = wwt_all + (WIDE && MUL ? (threadIdx.x >> 6) * kWideTab : 0);
   static_assert(!ADD || (MAX && !MUL), "u_add_v messages are max-reduced copies");
   static_assert(!TAB || MUL, "the table holds edge values");
   constexpr bool EPI = ADD && POS;
@@ -429,11 +468,20 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
     fetch_vals(it.b, eid_n1);
     fetch_ids(it.b + kWave, eid_n2);
   }
-  for (int64_t base = it.b; base < it.e; base += kWave) {
-    const int cnt = (int)min((int64_t)kWave, it.e - base);
+  for (int64_t base = it.b; base < it.e; base += BATCH) {
+    const int cnt = (int)min((int64_t)BATCH, it.e - base);
     int my_src = 0, my_eid = 0;
     float my_w = 0.0f;
-    if (lane < cnt) {
+    if constexpr (WIDE) {
+      int32_t qs[4], qw[4];
+      load_ids<4>(p.indices, p.nnz, base, lane, cnt, qs);
+      if constexpr (MUL)  // the weights' bits (0.0f past the batch)
+        load_ids<4>(reinterpret_cast<const int32_t*>(p.ev), p.nnz, base, lane, cnt, qw);
+      wave_lds_sync();  // the previous batch's table reads are done
+      wide_put(wid, lane, qs);
+      if constexpr (MUL) wide_put(wwt, lane, qw);
+      wave_lds_sync();
+    } else if (lane < cnt) {
       my_src = __builtin_nontemporal_load(p.indices + base + lane);
       if constexpr (PIPE) my_eid = eid_n1;
       else if constexpr (EIDS) my_eid = __builtin_nontemporal_load(p.eids + base + lane);
@@ -481,16 +529,29 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
       float wv[U][NV];
       int32_t eu[U];
       bool ok[U];
+      // wide batches: this group's U ids (and weights) of the step
+      int32_t tsrc[WIDE ? U : 1];
+      float tw[WIDE && MUL ? U : 1];
+      if constexpr (WIDE) {
+        wide_get<U>(wid, gid, j0, tsrc);
+        if constexpr (MUL) wide_get<U>(wwt, gid, j0, tw);
+      }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
         ok[u] = FULL || jb + gid < cnt;
-        const int src = __shfl(my_src, jb + gid);
+        int src;
+        if constexpr (WIDE) src = tsrc[u];
+        else src = __shfl(my_src, jb + gid);
         if constexpr (EIDS) eu[u] = bcast_lane<NG>(my_eid, jb, gid);
         else eu[u] = (int)(base + jb + gid);
         // the weight via the LDS crossbar (one permute) rather than two
         // readlanes and a select on the vector unit
-        const float w1 = (MUL && H1) ? __shfl(my_w, jb + gid) : 1.0f;
+        float w1 = 1.0f;
+        if constexpr (MUL && H1) {
+          if constexpr (WIDE) w1 = tw[u];
+          else w1 = __shfl(my_w, jb + gid);
+        }
         const float* xr = p.x + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
@@ -548,8 +609,9 @@ __global__ __launch_bounds__(kBlock) void spmm_fast_kernel(SpmmParams p) {
         for (; j0 + NG * U <= cnt; j0 += NG * U) step(j0, BoolTag<true>{}, h1_tag);
       for (; j0 < cnt; j0 += NG * U) step(j0, BoolTag<false>{}, h1_tag);
     };
-    // (without weights, or with a table, the head count plays no part)
-    if (!MUL || TAB || p.H == 1) steps(BoolTag<true>{});
+    // (without weights, or with a table, the head count plays no part; wide
+    // batches are launched for one head only)
+    if (!MUL || TAB || WIDE || p.H == 1) steps(BoolTag<true>{});
     else steps(BoolTag<false>{});
   }
   if constexpr (POS) {
@@ -929,6 +991,10 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
   // its QB results after the batch) instead of readlanes and selects
   __shared__ __align__(16) float res_all[NG <= 2 ? kWavesPerBlock * kWave * QB : 1];
   float* res_tab = res_all + (NG <= 2 ? (threadIdx.x >> 6) * kWave * QB : 0);
+  // wide batches of two groups take their ids from the group-major table
+  constexpr bool IDTAB = WIDE && NG == 2;
+  __shared__ __align__(16) int32_t sid_all[IDTAB ? kWavesPerBlock * kWideTab : 1];
+  int32_t* sid = sid_all + (IDTAB ? (threadIdx.x >> 6) * kWideTab : 0);
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -961,6 +1027,11 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
     const int cnt = (int)min((int64_t)(Q * kWave), it.e - base);
     int32_t my_src[Q], my_eid[Q];
     load_ids<Q>(p.indices, p.nnz, base, lane, cnt, my_src);
+    if constexpr (IDTAB) {
+      wave_lds_sync();  // the previous batch's table reads are done
+      wide_put(sid, lane, my_src);
+      wave_lds_sync();
+    }
     if (p.eids) {
       load_ids<Q>(p.eids, p.nnz, base, lane, cnt, my_eid);
     } else {
@@ -981,11 +1052,15 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
       constexpr bool FULL = decltype(full_tag)::value;
       float val[U][NV][4];
       bool ok[U];
+      int32_t tsrc[IDTAB ? U : 1];
+      if constexpr (IDTAB) wide_get<U>(sid, gid, j0, tsrc);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
         ok[u] = FULL || jb + gid < cnt;
-        const int src = bcast_q<NG, Q>(my_src, jb, (u * NG) % Q, gid);
+        int src;
+        if constexpr (IDTAB) src = tsrc[u];
+        else src = bcast_q<NG, Q>(my_src, jb, (u * NG) % Q, gid);
         const float* xr = p.xs + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
@@ -2958,42 +3033,57 @@ dim3 grid_for(int64_t items, int64_t chunks) {
 #define FG_LAUNCH(kernel, grid, stream, ...) \
   hipLaunchKernelGGL((kernel), (grid), dim3(kBlock), 0, (stream), __VA_ARGS__)
 
+// wide: items average kWideItemEdges edges or more (256-edge batches where
+// the lane layout allows them)
 template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool ADD, bool TAB>
-void spmm_fast_seg2(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+void spmm_fast_seg2(const SpmmParams& prm, bool seg, bool wide, dim3 grid, hipStream_t st) {
+  if constexpr (kWave / G == 2 && U % 4 == 0 && !EIDS && !TAB) {
+    if (wide && (!MUL || prm.H == 1)) {
+      if (seg)
+        FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, true, ADD, TAB, true>), grid, st,
+                  prm);
+      else
+        FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, false, ADD, TAB, true>), grid, st,
+                  prm);
+      return;
+    }
+  }
   if (seg) FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, true, ADD, TAB>), grid, st, prm);
   else FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, false, ADD, TAB>), grid, st, prm);
 }
 
 template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool ADD = false>
-void spmm_fast_seg(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+void spmm_fast_seg(const SpmmParams& prm, bool seg, bool wide, dim3 grid, hipStream_t st) {
   // per-head edge values come from a per-batch LDS table
   if constexpr (MUL) {
     if (prm.H >= 2 && prm.H <= kTabHeads) {
-      spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, true>(prm, seg, grid, st);
+      spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, true>(prm, seg, wide, grid, st);
       return;
     }
   }
-  spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, false>(prm, seg, grid, st);
+  spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, false>(prm, seg, wide, grid, st);
 }
 
 template <int G, int NV, int U, bool MUL, bool MAX, bool ADD = false>
-void spmm_fast_eids(const SpmmParams& prm, bool seg, dim3 grid, hipStream_t st) {
+void spmm_fast_eids(const SpmmParams& prm, bool seg, bool wide, dim3 grid, hipStream_t st) {
   // copy + sum never looks at edge ids
-  if (prm.eids && (MUL || MAX)) spmm_fast_seg<G, NV, U, MUL, MAX, true, ADD>(prm, seg, grid, st);
-  else spmm_fast_seg<G, NV, U, MUL, MAX, false, ADD>(prm, seg, grid, st);
+  if (prm.eids && (MUL || MAX))
+    spmm_fast_seg<G, NV, U, MUL, MAX, true, ADD>(prm, seg, wide, grid, st);
+  else
+    spmm_fast_seg<G, NV, U, MUL, MAX, false, ADD>(prm, seg, wide, grid, st);
 }
 
 template <int G, int NV, int U>
-void spmm_fast_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 grid,
+void spmm_fast_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, bool wide, dim3 grid,
                    hipStream_t st) {
   if (prm.xd) {
-    spmm_fast_eids<G, NV, U, false, true, true>(prm, seg, grid, st);
+    spmm_fast_eids<G, NV, U, false, true, true>(prm, seg, wide, grid, st);
   } else if (mul) {
-    if (mx) spmm_fast_eids<G, NV, U, true, true>(prm, seg, grid, st);
-    else spmm_fast_eids<G, NV, U, true, false>(prm, seg, grid, st);
+    if (mx) spmm_fast_eids<G, NV, U, true, true>(prm, seg, wide, grid, st);
+    else spmm_fast_eids<G, NV, U, true, false>(prm, seg, wide, grid, st);
   } else {
-    if (mx) spmm_fast_eids<G, NV, U, false, true>(prm, seg, grid, st);
-    else spmm_fast_eids<G, NV, U, false, false>(prm, seg, grid, st);
+    if (mx) spmm_fast_eids<G, NV, U, false, true>(prm, seg, wide, grid, st);
+    else spmm_fast_eids<G, NV, U, false, false>(prm, seg, wide, grid, st);
   }
 }
 
@@ -3071,6 +3161,7 @@ hipError_t launch_spmm_core(const GraphView& g, const PlanView* plan, int msg, i
   prm.ws_f = seg ? plan->ws_f : nullptr;
   prm.ws_i = seg ? plan->ws_i : nullptr;
   prm.n_items = seg ? plan->num_segments : g.num_rows;
+  prm.nnz = g.nnz;
   prm.F = F;
   prm.H = (int32_t)H;
   prm.dh = (int32_t)dh;
@@ -3078,13 +3169,17 @@ hipError_t launch_spmm_core(const GraphView& g, const PlanView* plan, int msg, i
   prm.ev_vec4 = (ev && H % 4 == 0 && aligned16(ev)) ? 1 : 0;
   if (vec4) {
     const int64_t Q = F / 4;  // float4 per row
-    if (Q <= 4) spmm_fast_ops<4, 1, 4>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
-    else if (Q <= 8) spmm_fast_ops<8, 1, 8>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
-    else if (Q <= 16) spmm_fast_ops<16, 1, 8>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
-    else if (Q <= 32) spmm_fast_ops<32, 1, 8>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
-    else if (Q <= 64) spmm_fast_ops<64, 1, 8>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
-    else if (Q <= 128) spmm_fast_ops<64, 2, 4>(prm, mul, mx, seg, grid_for(prm.n_items, 1), stream);
-    else spmm_fast_ops<64, 4, 2>(prm, mul, mx, seg, grid_for(prm.n_items, (Q + 255) / 256), stream);
+    const bool wide = g.nnz >= kWideItemEdges * std::max<int64_t>(prm.n_items, 1);
+    const dim3 grid1 = grid_for(prm.n_items, 1);
+    if (Q <= 4) spmm_fast_ops<4, 1, 4>(prm, mul, mx, seg, wide, grid1, stream);
+    else if (Q <= 8) spmm_fast_ops<8, 1, 8>(prm, mul, mx, seg, wide, grid1, stream);
+    else if (Q <= 16) spmm_fast_ops<16, 1, 8>(prm, mul, mx, seg, wide, grid1, stream);
+    else if (Q <= 32) spmm_fast_ops<32, 1, 8>(prm, mul, mx, seg, wide, grid1, stream);
+    else if (Q <= 64) spmm_fast_ops<64, 1, 8>(prm, mul, mx, seg, wide, grid1, stream);
+    else if (Q <= 128) spmm_fast_ops<64, 2, 4>(prm, mul, mx, seg, wide, grid1, stream);
+    else
+      spmm_fast_ops<64, 4, 2>(prm, mul, mx, seg, wide, grid_for(prm.n_items, (Q + 255) / 256),
+                              stream);
   } else {
     // scalar lanes: G = 2^ceil(log2 F) up to 64, then NV values per lane
     int nv = 1;

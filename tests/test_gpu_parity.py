@@ -1517,6 +1517,49 @@ def test_sddmm_wide_batches_with_edge_ids_and_ragged_ends():
             check_sddmm(csc, Gt, xd, xs, plan=plan, nnz_total=csr.nnz)
 
 
+def test_gspmm_wide_batches_ragged_ends():
+    """The gSpMM's 256-edge batches (two lane groups, d = 65..128, items of 128
+    edges or more on average): ids and weights four per lane through the
+    group-major LDS table.  Copy and weighted sum, max with and without
+    weights and the MLP's u_add_v max, at d = 128 (unmasked steps) and
+    d = 100 (every step masked), on rows whose lengths are not multiples of
+    4 or 256 and a stored-edge count that is not a multiple of 4 (the last
+    lane of the last item loads its ids and weights one by one); then the
+    same graph with short items (64-edge batches) and with split rows."""
+    rng = np.random.default_rng(78)
+    n, m = 600, 1000
+    deg = rng.integers(130, 700, size=n)
+    deg[5] = 0
+    deg[-1] = 517  # a long last row whose end is not 4-aligned
+    dst = np.repeat(np.arange(n), deg)
+    src = rng.integers(0, m, size=dst.size)
+    src[:40] = src[0]  # a run of duplicate edges: ties go to the smallest id
+    assert dst.size % 4 != 0
+    csr = synth.coo_to_csr(dst.astype(np.int64), src.astype(np.int64), n, m)
+    G = fg.Graph.from_csr(csr)
+    ew = rng.uniform(0.0, 1.0, csr.nnz).astype(np.float32) + np.float32(1e-3)
+    for d in (128, 100):
+        x = rng.standard_normal((m, d)).astype(np.float32)
+        xi = rng.integers(-4, 5, (m, d)).astype(np.float32)
+        ewi = rng.integers(1, 4, csr.nnz).astype(np.float32)
+        for plan in (fg.Plan(G, d), fg.Plan(G, d, segment_edges=64),
+                     fg.Plan(G, d, segment_edges=300)):
+            info = plan.info()
+            say("wide-batch gSpMM d=%d items=%d split=%d" % (d, info["num_segments"],
+                                                             info["num_split_rows"]))
+            check_spmm(csr, G, x, plan=plan)
+            check_spmm(csr, G, x, plan=plan, edge=ew)
+            check_spmm(csr, G, xi, plan=plan, edge=ewi, exact=True)
+            check_spmm(csr, G, x, plan=plan, reduce="max")
+            check_spmm(csr, G, xi, plan=plan, reduce="max")
+            check_spmm(csr, G, x, plan=plan, edge=ew, reduce="max")
+    w = rng.standard_normal((8, 128)).astype(np.float32)
+    xm = rng.standard_normal((m, 8)).astype(np.float32)
+    xdm = rng.standard_normal((n, 8)).astype(np.float32)
+    for plan in (fg.Plan(G, 128), fg.Plan(G, 128, segment_edges=300)):
+        check_mlp(csr, G, xm, xdm, w, plan=plan)
+
+
 def test_sddmm_own_schedule_on_spread_graph():
     """A spread graph with source slabs at d >= 256: the plan holds a schedule
     of its own for the SDDMM (every row cut at slab boundaries, no slots),
