@@ -55,6 +55,14 @@ __device__ __forceinline__ uint64_t row_off(int32_t src, int64_t F) {
   return (uint64_t)(uint32_t)src * (uint32_t)F;
 }
 
+// The same for a lane's element pointer xl (the array plus the lane's
+// element offset) and the row size in bytes (F * 4 <= 2^18): one unsigned
+// 32 x 32 + 64-bit multiply-add per gather, where p + row_off(src, F) + f
+// takes a multiply, a shift and a 64-bit add.
+__device__ __forceinline__ const float* row_at(const char* xl, int32_t src, uint32_t rb) {
+  return reinterpret_cast<const float*>(xl + (uint64_t)(uint32_t)src * rb);
+}
+
 template <int VEC>
 __device__ __forceinline__ void load_vec(const float* p, float (&r)[VEC]) {
   if constexpr (VEC == 4) {
@@ -407,11 +415,14 @@ __global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kern
   int64_t f[NV];
   bool act[NV];
   int hv[NV];
+  const char* xl[NV];  // this lane's elements of source row 0
+  const uint32_t rb = (uint32_t)F * 4u;
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
     f[v] = c0 + (int64_t)(v * G + li) * 4;
     act[v] = f[v] < F;
     hv[v] = (MUL && act[v]) ? (int)(f[v] / p.dh) : 0;
+    xl[v] = reinterpret_cast<const char*>(p.x) + f[v] * 4;
   }
   float acc[NV][4];
   int32_t am[NV][4];
@@ -552,11 +563,10 @@ __global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kern
           if constexpr (WIDE) w1 = tw[u];
           else w1 = __shfl(my_w, jb + gid);
         }
-        const float* xr = p.x + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
           if (FULL || (ok[u] && act[v])) {
-            load_vec<4>(xr + f[v], val[u][v]);
+            load_vec<4>(row_at(xl[v], src, rb), val[u][v]);
             if constexpr (ELEM) {
 #pragma unroll
               for (int c = 0; c < 4; ++c) {
@@ -1008,10 +1018,13 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
   int64_t f[NV];
   bool act[NV];
   float xd[NV][4];
+  const char* xl[NV];  // this lane's elements of source row 0
+  const uint32_t rb = (uint32_t)F * 4u;
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
     f[v] = (int64_t)(v * G + li) * 4;
     act[v] = f[v] < F;
+    xl[v] = reinterpret_cast<const char*>(p.xs) + f[v] * 4;
     if (act[v]) {
       load_vec<4>(p.xd + it.row * F + f[v], xd[v]);
     } else {
@@ -1061,11 +1074,10 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
         int src;
         if constexpr (IDTAB) src = tsrc[u];
         else src = bcast_q<NG, Q>(my_src, jb, (u * NG) % Q, gid);
-        const float* xr = p.xs + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
           if (FULL || (ok[u] && act[v])) {
-            load_vec<4>(xr + f[v], val[u][v]);
+            load_vec<4>(row_at(xl[v], src, rb), val[u][v]);
           } else {
 #pragma unroll
             for (int c = 0; c < 4; ++c) val[u][v][c] = 0.0f;
@@ -1153,6 +1165,8 @@ __global__ __launch_bounds__(kBlock) void sddmm_headed_kernel(SddmmParams p) {
   const int64_t h = act ? f / p.dh : 0;
   float xd[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (act) load_vec<4>(p.xd + it.row * F + f, xd);
+  const char* xl = reinterpret_cast<const char*>(p.xs) + f * 4;  // lane's elements of row 0
+  const uint32_t rb = (uint32_t)F * 4u;
 
   for (int64_t base = it.b; base < it.e; base += kWave) {
     const int cnt = (int)min((int64_t)kWave, it.e - base);
@@ -1173,7 +1187,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_headed_kernel(SddmmParams p) {
         const int src = __shfl(my_src, jl);
         eu[u] = __shfl(my_eid, jl);
         if (ok[u] && act) {
-          load_vec<4>(p.xs + row_off(src, F) + f, val[u]);
+          load_vec<4>(row_at(xl, src, rb), val[u]);
         } else {
 #pragma unroll
           for (int c = 0; c < 4; ++c) val[u][c] = 0.0f;
@@ -1927,10 +1941,13 @@ __global__ __launch_bounds__(kBlock) void sddmm_softmax_kernel(SddmmParams p, fl
   int64_t f[NV];
   bool act[NV];
   float xd[NV][4];
+  const char* xl[NV];  // this lane's elements of source row 0
+  const uint32_t rb = (uint32_t)F * 4u;
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
     f[v] = (int64_t)(v * G + li) * 4;
     act[v] = f[v] < F;
+    xl[v] = reinterpret_cast<const char*>(p.xs) + f[v] * 4;
     if (act[v]) {
       load_vec<4>(p.xd + it.row * F + f[v], xd[v]);
     } else {
@@ -1959,11 +1976,10 @@ __global__ __launch_bounds__(kBlock) void sddmm_softmax_kernel(SddmmParams p, fl
         const int jb = j0 + u * NG;
         ok[u] = jb + gid < cnt;
         const int src = bcast_lane<NG>(my_src, jb, gid);
-        const float* xr = p.xs + row_off(src, F);
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
           if (ok[u] && act[v]) {
-            load_vec<4>(xr + f[v], val[u][v]);
+            load_vec<4>(row_at(xl[v], src, rb), val[u][v]);
           } else {
 #pragma unroll
             for (int c = 0; c < 4; ++c) val[u][v][c] = 0.0f;
@@ -2483,6 +2499,8 @@ __global__ __launch_bounds__(kBlock) void sddmm_softmax_bwd_kernel(SddmmParams p
   const int64_t h = act ? f / p.dh : 0;
   float xd[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (act) load_vec<4>(p.xd + it.row * F + f, xd);
+  const char* xl = reinterpret_cast<const char*>(p.xs) + f * 4;  // lane's elements of row 0
+  const uint32_t rb = (uint32_t)F * 4u;
   float c[NC];  // FLAT: per float4 slot (fixed head); else per head
 #pragma unroll
   for (int k = 0; k < NC; ++k) c[k] = 0.0f;
@@ -2517,7 +2535,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_softmax_bwd_kernel(SddmmParams p
         ok[u] = j < cnt;
         const int src = __shfl(my_src, j & (kWave - 1));
         if (ok[u] && act) {
-          load_vec<4>(p.xs + row_off(src, F) + f, val[u]);
+          load_vec<4>(row_at(xl, src, rb), val[u]);
         } else {
 #pragma unroll
           for (int k = 0; k < 4; ++k) val[u][k] = 0.0f;
@@ -2916,6 +2934,8 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
   const int h = act ? (int)(f / p.dh) : 0;
   float xd[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (act) load_vec<4>(p.xd + it.row * F + f, xd);
+  const char* xl = reinterpret_cast<const char*>(p.xs) + f * 4;  // lane's elements of row 0
+  const uint32_t rb = (uint32_t)F * 4u;
   const bool all_act = (int64_t)G * 4 <= F;  // every lane holds a feature chunk
   float m = -INFINITY, z = 0.0f;
   float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -2937,7 +2957,7 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
         // (two or fewer groups: one cross-lane permute, off the vector ALU)
         const int src = NG <= 2 ? __shfl(my_src, jb + gid) : bcast_lane<NG>(my_src, jb, gid);
         if (FULL || (ok[u] && act)) {
-          load_vec<4>(p.xs + row_off(src, F) + f, val[u]);
+          load_vec<4>(row_at(xl, src, rb), val[u]);
         } else {
 #pragma unroll
           for (int c = 0; c < 4; ++c) val[u][c] = 0.0f;
