@@ -2862,6 +2862,7 @@ struct GatParams {
   const Seg* segs;
   float* ws;  // per slot: [F] scaled partial sum, [H] running max, [H] scaled exp-sum
   int64_t n_items;
+  int64_t nnz;  // length of indices
   int64_t F;
   int32_t H;
   int32_t dh;
@@ -2916,11 +2917,17 @@ __device__ __forceinline__ void attn_merge(float& m, float& z, float (&acc)[4], 
 // is rescaled only when a score exceeds the current maximum (a branch the
 // whole wavefront skips when no lane needs it); otherwise an edge costs one
 // exponential and a multiply-add per feature.
-template <int G, int SH, bool SEG>
+// WIDE (two lane groups): 256-edge batches, ids four per lane in one load
+// and through the group-major LDS table.
+template <int G, int SH, bool SEG, bool WIDE = false>
 __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
   constexpr int NG = kWave / G;
   constexpr int U = NG * 4 <= kWave ? 4 : 1;
   static_assert(SH <= G, "a head's lanes lie inside one lane group");
+  static_assert(!WIDE || (NG == 2 && U % 4 == 0), "wide batches serve two lane groups");
+  constexpr int BATCH = WIDE ? 4 * kWave : kWave;
+  __shared__ __align__(16) int32_t wid_all[WIDE ? kWavesPerBlock * kWideTab : 1];
+  int32_t* wid = wid_all + (WIDE ? (threadIdx.x >> 6) * kWideTab : 0);
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -2940,22 +2947,34 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
   float m = -INFINITY, z = 0.0f;
   float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 
-  for (int64_t base = it.b; base < it.e; base += kWave) {
-    const int cnt = (int)min((int64_t)kWave, it.e - base);
+  for (int64_t base = it.b; base < it.e; base += BATCH) {
+    const int cnt = (int)min((int64_t)BATCH, it.e - base);
     int my_src = 0;
-    if (lane < cnt) my_src = __builtin_nontemporal_load(p.indices + base + lane);
+    if constexpr (WIDE) {
+      int32_t q[4];
+      load_ids<4>(p.indices, p.nnz, base, lane, cnt, q);
+      wave_lds_sync();  // the previous batch's table reads are done
+      wide_put(wid, lane, q);
+      wave_lds_sync();
+    } else if (lane < cnt) {
+      my_src = __builtin_nontemporal_load(p.indices + base + lane);
+    }
     // one step of U edges per lane group; FULL: all of them in the batch and
     // every lane active (no masking)
     auto step = [&](int j0, auto full_tag) {
       constexpr bool FULL = decltype(full_tag)::value;
       float val[U][4];
       bool ok[U];
+      int32_t tsrc[WIDE ? U : 1];
+      if constexpr (WIDE) wide_get<U>(wid, gid, j0, tsrc);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
         ok[u] = FULL || jb + gid < cnt;
         // (two or fewer groups: one cross-lane permute, off the vector ALU)
-        const int src = NG <= 2 ? __shfl(my_src, jb + gid) : bcast_lane<NG>(my_src, jb, gid);
+        int src;
+        if constexpr (WIDE) src = tsrc[u];
+        else src = NG <= 2 ? __shfl(my_src, jb + gid) : bcast_lane<NG>(my_src, jb, gid);
         if (FULL || (ok[u] && act)) {
           load_vec<4>(row_at(xl, src, rb), val[u]);
         } else {
@@ -3619,6 +3638,7 @@ hipError_t launch_gat_fused(const GraphView& g, const PlanView* plan, int64_t H,
   prm.segs = seg ? plan->segs : nullptr;
   prm.ws = seg ? plan->ws_f : nullptr;
   prm.n_items = seg ? plan->num_segments : g.num_rows;
+  prm.nnz = g.nnz;
   prm.F = H * dh;
   prm.H = (int32_t)H;
   prm.dh = (int32_t)dh;
@@ -3628,10 +3648,19 @@ hipError_t launch_gat_fused(const GraphView& g, const PlanView* plan, int64_t H,
   const dim3 grid = grid_for(prm.n_items, 1);
   const int64_t Q = prm.F / 4;
   const int G = Q <= 4 ? 4 : Q <= 8 ? 8 : Q <= 16 ? 16 : Q <= 32 ? 32 : 64;
-  // lanes of a head must not straddle the group (SH <= G always holds: dh <= F)
-#define FG_GAT2(GG, SS)                                                        \
-  if (seg) FG_LAUNCH((gat_fused_kernel<GG, SS, true>), grid, stream, prm);     \
-  else FG_LAUNCH((gat_fused_kernel<GG, SS, false>), grid, stream, prm);
+  // lanes of a head must not straddle the group (SH <= G always holds: dh <= F);
+  // two lane groups on items of kWideItemEdges edges or more on average take
+  // 256-edge batches
+  const bool wide = g.nnz >= kWideItemEdges * std::max<int64_t>(prm.n_items, 1);
+#define FG_GAT2(GG, SS)                                                              \
+  if (GG == 32 && wide) {                                                            \
+    if (seg) FG_LAUNCH((gat_fused_kernel<GG, SS, true, GG == 32>), grid, stream, prm); \
+    else FG_LAUNCH((gat_fused_kernel<GG, SS, false, GG == 32>), grid, stream, prm);    \
+  } else if (seg) {                                                                  \
+    FG_LAUNCH((gat_fused_kernel<GG, SS, true>), grid, stream, prm);                  \
+  } else {                                                                           \
+    FG_LAUNCH((gat_fused_kernel<GG, SS, false>), grid, stream, prm);                 \
+  }
 #define FG_GAT(GG)                                                             \
   switch (prm.SH) {                                                            \
     case 1: { FG_GAT2(GG, 1) } break;                                          \

@@ -1560,6 +1560,31 @@ def test_gspmm_wide_batches_ragged_ends():
         check_mlp(csr, G, xm, xdm, w, plan=plan)
 
 
+def test_gat_fused_wide_batches_ragged_ends():
+    """The fused attention kernel's 256-edge batches (two lane groups, F = 128,
+    items of 128 edges or more on average) with ids through the group-major
+    LDS table: heads of 16, 64 and 128 features, rows whose lengths are not
+    multiples of 4 or 256, a stored-edge count that is not a multiple of 4,
+    an empty row; whole rows and split rows."""
+    rng = np.random.default_rng(79)
+    n = 800
+    deg = rng.integers(130, 600, size=n)
+    deg[7] = 0
+    deg[-1] = 301
+    dst = np.repeat(np.arange(n), deg)
+    src = rng.integers(0, n, size=dst.size)
+    assert dst.size % 4 != 0
+    csr = synth.coo_to_csr(dst.astype(np.int64), src.astype(np.int64), n, n)
+    G = fg.Graph.from_csr(csr)
+    for heads, dh in ((8, 16), (2, 64), (1, 128)):
+        x = (rng.standard_normal((n, heads, dh)) * 0.25).astype(np.float32)
+        for plan in (fg.Plan(G, heads * dh), fg.Plan(G, heads * dh, segment_edges=1000)):
+            info = plan.info()
+            say("wide-batch attention H=%d dh=%d items=%d split=%d" % (
+                heads, dh, info["num_segments"], info["num_split_rows"]))
+            check_gat(csr, G, x, plan=plan, heads=heads)
+
+
 def test_sddmm_own_schedule_on_spread_graph():
     """A spread graph with source slabs at d >= 256: the plan holds a schedule
     of its own for the SDDMM (every row cut at slab boundaries, no slots),
