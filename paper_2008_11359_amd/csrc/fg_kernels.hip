@@ -82,6 +82,29 @@ __device__ __forceinline__ void store_vec(float* p, const float (&r)[VEC]) {
   }
 }
 
+// Non-temporal forms for results no later step of the kernel reads: they
+// should not displace the gathered rows from the L2.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+template <int VEC>
+__device__ __forceinline__ void store_vec_nt(float* p, const float (&r)[VEC]) {
+  if constexpr (VEC == 4) {
+    __builtin_nontemporal_store(f32x4{r[0], r[1], r[2], r[3]}, reinterpret_cast<f32x4*>(p));
+  } else {
+    __builtin_nontemporal_store(r[0], p);
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_vec_i_nt(int32_t* p, const int32_t (&r)[VEC]) {
+  if constexpr (VEC == 4) {
+    __builtin_nontemporal_store(i32x4{r[0], r[1], r[2], r[3]}, reinterpret_cast<i32x4*>(p));
+  } else {
+    __builtin_nontemporal_store(r[0], p);
+  }
+}
+
 template <int VEC>
 __device__ __forceinline__ void store_vec_i(int32_t* p, const int32_t (&r)[VEC]) {
   if constexpr (VEC == 4) {
@@ -328,8 +351,8 @@ template <int VEC, bool MAX, bool SEG, int EPI = kEpiNone>
 __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, int64_t f,
                                            const float (&acc)[VEC], const int32_t (&am)[VEC]) {
   if (SEG && it.slot >= 0) {
-    store_vec<VEC>(p.ws_f + (int64_t)it.slot * p.F + f, acc);
-    if constexpr (MAX) store_vec_i<VEC>(p.ws_i + (int64_t)it.slot * p.F + f, am);
+    store_vec_nt<VEC>(p.ws_f + (int64_t)it.slot * p.F + f, acc);
+    if constexpr (MAX) store_vec_i_nt<VEC>(p.ws_i + (int64_t)it.slot * p.F + f, am);
   } else if constexpr (MAX) {
     float o[VEC];
     int32_t a[VEC];
@@ -348,10 +371,10 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
         a[c] = none ? -1 : am[c];
       }
     }
-    store_vec<VEC>(p.out + it.row * p.F + f, o);
-    store_vec_i<VEC>(p.arg + it.row * p.F + f, a);
+    store_vec_nt<VEC>(p.out + it.row * p.F + f, o);
+    store_vec_i_nt<VEC>(p.arg + it.row * p.F + f, a);
   } else {
-    store_vec<VEC>(p.out + it.row * p.F + f, acc);
+    store_vec_nt<VEC>(p.out + it.row * p.F + f, acc);
   }
 }
 
@@ -1125,15 +1148,15 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
     bool stored = false;
     if constexpr (Q == 4) {
       if (!p.eids && lane * Q + Q <= cnt) {  // four positional results: one 16-byte store
-        *reinterpret_cast<float4_a4*>(p.out + base + lane * Q) =
-            float4_a4{res[0], res[1], res[2], res[3]};
+        __builtin_nontemporal_store(float4_a4{res[0], res[1], res[2], res[3]},
+                                    reinterpret_cast<float4_a4*>(p.out + base + lane * Q));
         stored = true;
       }
     }
     if (!stored) {
 #pragma unroll
       for (int q = 0; q < Q; ++q)
-        if (lane * Q + q < cnt) p.out[my_eid[q]] = res[q];
+        if (lane * Q + q < cnt) __builtin_nontemporal_store(res[q], p.out + my_eid[q]);
     }
   }
 }
