@@ -472,6 +472,14 @@ __global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kern
   constexpr bool PIPE = TAB && EIDS;
   float qn[PIPE ? kTabHeads : 1];
   int eid_n1 = 0, eid_n2 = 0;  // edge ids of the next batch and the one after
+  // The table's loads: with 4, 8 or 16 heads (16-byte aligned rows) lpe =
+  // H / 4 lanes share an edge, one float4 each, so that an instruction reads
+  // 64 / lpe whole edge rows (one 64-byte cache tag each for 8 heads) rather
+  // than one float4 of 64 different edges; load i of a lane holds part
+  // lane % lpe of edge i * 64 / lpe + lane / lpe.
+  const int lpe = (TAB && p.ev_vec4 && (p.H == 4 || p.H == 8 || p.H == 16)) ? p.H >> 2 : 0;
+  const int lpe_part = lpe ? lane % lpe : 0;
+  const int lpe_sub = lpe ? lane / lpe : 0;
   auto fetch_ids = [&](int64_t b0, int& e) {
     e = 0;
     const int c = (int)min((int64_t)kWave, it.e - b0);
@@ -479,6 +487,21 @@ __global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kern
   };
   auto fetch_vals = [&](int64_t b0, int e) {
     const int c = (int)min((int64_t)kWave, it.e - b0);
+    if (lpe) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < lpe) {
+          const int k = i * (kWave / lpe) + lpe_sub;
+          const int ek = __shfl(e, k);
+          if (b0 < it.e && k < c) {
+            float q4[4];
+            load_vec<4>(p.ev + (int64_t)ek * p.H + lpe_part * 4, q4);
+#pragma unroll
+            for (int c4 = 0; c4 < 4; ++c4) qn[4 * i + c4] = q4[c4];
+          }
+        }
+      return;
+    }
     if (b0 < it.e && lane < c) {
       const float* er = p.ev + (int64_t)e * p.H;
 #pragma unroll
@@ -526,7 +549,17 @@ __global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kern
     }
     if constexpr (PIPE) {
       wave_lds_sync();
-      if (lane < cnt) {
+      if (lpe) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (i < lpe) {
+            const int k = i * (kWave / lpe) + lpe_sub;
+            if (k < cnt) {
+              const float q4[4] = {qn[4 * i], qn[4 * i + 1], qn[4 * i + 2], qn[4 * i + 3]};
+              store_vec<4>(tab + k * p.H + lpe_part * 4, q4);
+            }
+          }
+      } else if (lane < cnt) {
         float* tr = tab + lane * p.H;
 #pragma unroll
         for (int h = 0; h < kTabHeads; ++h)
@@ -538,7 +571,19 @@ __global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kern
       fetch_ids(base + 2 * kWave, eid_n2);
     } else if constexpr (TAB) {
       wave_lds_sync();  // the previous batch's table reads are done
-      if (lane < cnt) {
+      if (lpe) {  // positional edge ids (explicit ones take the PIPE path)
+        float q4[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int k = i * (kWave / lpe) + lpe_sub;
+          if (i < lpe && k < cnt) load_vec<4>(p.ev + (base + k) * p.H + lpe_part * 4, q4[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int k = i * (kWave / lpe) + lpe_sub;
+          if (i < lpe && k < cnt) store_vec<4>(tab + k * p.H + lpe_part * 4, q4[i]);
+        }
+      } else if (lane < cnt) {
         const float* er = p.ev + (int64_t)my_eid * p.H;
         float* tr = tab + lane * p.H;
         if (p.ev_vec4) {
