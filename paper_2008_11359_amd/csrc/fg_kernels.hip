@@ -1223,6 +1223,9 @@ __global__ __launch_bounds__(kBlock) void sddmm_headed_kernel(SddmmParams p) {
   if (it.row < 0) return;  // padding item of a partitioned schedule
   if (it.b >= it.e) return;
   const int lane = lane_id();
+  const int lpe = (p.out_vec4 && (p.H == 4 || p.H == 8 || p.H == 16)) ? p.H >> 2 : 0;
+  const int lpe_part = lpe ? lane % lpe : 0;
+  const int lpe_sub = lpe ? lane / lpe : 0;
   const int G = 1 << p.logG;
   const int ngroups = kWave >> p.logG;
   const int gid = lane >> p.logG;
@@ -1277,7 +1280,21 @@ __global__ __launch_bounds__(kBlock) void sddmm_headed_kernel(SddmmParams p) {
     }
     if (staged) {
       wave_lds_sync();
-      if (lane < cnt) {
+      if (lpe) {
+        // lpe = H / 4 lanes share an edge (one float4 each), so that a store
+        // instruction writes 64 / lpe whole edge rows
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (i < lpe) {
+            const int k = i * (kWave / lpe) + lpe_sub;
+            const int ek = __shfl(my_eid, k);
+            if (k < cnt) {
+              float q[4];
+              load_vec<4>(tab + k * p.H + lpe_part * 4, q);
+              store_vec<4>(p.out + (int64_t)ek * p.H + lpe_part * 4, q);
+            }
+          }
+      } else if (lane < cnt) {
         const float* tr = tab + lane * p.H;
         float* orow = p.out + (int64_t)my_eid * p.H;
         if (p.out_vec4) {
