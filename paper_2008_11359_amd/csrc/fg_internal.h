@@ -40,9 +40,12 @@ struct PlanView {
 // Rows of at most this many edges are short: the edge softmax packs four of
 // them into one wavefront.
 constexpr int kShortRowEdges = 64;
-// Plans whose items average at least this many edges take the SDDMM's wide
-// (256-edge) batches, and the SDDMM + softmax call runs as two kernels there.
+// Plans whose items average at least this many edges take the gather
+// kernels' wide (256-edge) batches with two lane groups (rows of 65-128
+// floats), and the SDDMM + softmax call runs as two kernels there.
 constexpr int64_t kWideItemEdges = 128;
+// The same for four or more lane groups (rows of at most 64 floats).
+constexpr int64_t kWideItemEdgesMany = 64;
 
 // Rows of at most this many edges (and more than kShortRowEdges) also go
 // several to a wavefront: four, with float4 lanes.

@@ -176,12 +176,20 @@ __device__ __forceinline__ float bcast_lane_f(float v, int jb, int gid) {
 }
 
 // Wide batches of Q * 64 edges (gather kernels on long items): lane l holds
-// edges Q*l .. Q*l + Q - 1 of the batch (Q = 4 for one or two lane groups,
-// else 1), so the ids of 256 edges arrive in one 16-byte load per lane (and
-// the SDDMM's results leave in one 16-byte store): the address unit that
-// bounds the gather kernels spends one instruction on each instead of four.
+// edges Q*l .. Q*l + Q - 1 of the batch (Q = 4 when a step covers whole
+// lanes, else 1), so the ids of 256 edges arrive in one 16-byte load per lane
+// (and the SDDMM's results leave in one 16-byte store): the address unit that
+// bounds the gather kernels spends one instruction on each instead of four,
+// and an item of up to 256 edges waits for one id load instead of several.
 template <int NG, int U>
-constexpr int ids_per_lane() { return NG <= 2 && (NG * U) % 4 == 0 ? 4 : 1; }
+constexpr int ids_per_lane() { return (NG * U) % 4 == 0 && (NG == 1 || U % 4 == 0) ? 4 : 1; }
+
+// Average item length from which wide batches pay: two lane groups (rows of
+// 65-128 floats) gain from the quarter of the id loads on long items only;
+// four or more groups (narrower rows, where a step of U edges per group
+// spans 64 or more edges) also gain from waiting for one id load per item.
+template <int NG>
+constexpr int64_t wide_item_edges() { return NG >= 4 ? kWideItemEdgesMany : kWideItemEdges; }
 
 
 template <int Q, typename T>
@@ -229,7 +237,7 @@ __device__ __forceinline__ void load_ids(const int32_t* ptr, int64_t len, int64_
 // c0, known after unrolling.  One group reads its id into a scalar
 // register; two groups take theirs through one cross-lane permute (the
 // vector unit, which partly bounds the gather kernels, then only forms the
-// lane index).  Two groups with four ids per lane use the LDS table below.
+// lane index).  Several groups with four ids per lane use the LDS table below.
 template <int NG, int Q>
 __device__ __forceinline__ int bcast_q(const int32_t (&v)[Q], int jb, int c0, int gid) {
   if constexpr (NG == 1) {
@@ -241,31 +249,44 @@ __device__ __forceinline__ int bcast_q(const int32_t (&v)[Q], int jb, int c0, in
   }
 }
 
-// Wide batches of two lane groups keep their 256 ids (or weights) in a
+// Wide batches of NG >= 2 lane groups keep their 256 ids (or weights) in a
 // per-wavefront LDS table, group by group: edge k of the batch at
-// (k & 1) * kWideHalf + k / 2, so that group g's edges of a step (j0 + 2u + g,
-// u < U) are U consecutive entries, read with U / 4 16-byte LDS reads instead
-// of one cross-lane permute (and a select) per edge.  The 4-entry pad between
-// the halves puts the two groups' reads of one step in different banks.
-constexpr int kWideHalf = 2 * kWave + 4;
-constexpr int kWideTab = 2 * kWideHalf;
+// (k % NG) * wide_half<NG>() + k / NG, so that group g's edges of a step
+// (j0 + NG u + g, u < U) are U consecutive entries, read with U / 4 16-byte
+// LDS reads instead of one cross-lane permute (and a select) per edge.  The
+// 4-entry pad after each group's 256 / NG entries puts the groups' reads of
+// one step in different banks.
+template <int NG>
+constexpr int wide_half() { return 4 * kWave / NG + 4; }
+template <int NG>
+constexpr int wide_tab() { return NG * wide_half<NG>(); }
 
-// Lane l holds edges 4l .. 4l + 3 of the batch: 4l and 4l + 2 go to group
-// 0's half, 4l + 1 and 4l + 3 to group 1's.
-template <typename T>
+// Lane l holds edges 4l .. 4l + 3 of the batch.  Two groups: 4l and 4l + 2
+// go to group 0's entries 2l and 2l + 1, 4l + 1 and 4l + 3 to group 1's.
+// NG = 4m groups: edge 4l + q goes to group 4 (l % m) + q, entry l / m.
+template <int NG, typename T>
 __device__ __forceinline__ void wide_put(T* tab, int lane, const int32_t (&q)[4]) {
   static_assert(sizeof(T) == 4, "4-byte entries");
+  static_assert(NG == 2 || NG % 4 == 0, "two lane groups or a multiple of four");
   int32_t* t = reinterpret_cast<int32_t*>(tab);
-  *reinterpret_cast<int2*>(t + 2 * lane) = make_int2(q[0], q[2]);
-  *reinterpret_cast<int2*>(t + kWideHalf + 2 * lane) = make_int2(q[1], q[3]);
+  constexpr int H = wide_half<NG>();
+  if constexpr (NG == 2) {
+    *reinterpret_cast<int2*>(t + 2 * lane) = make_int2(q[0], q[2]);
+    *reinterpret_cast<int2*>(t + H + 2 * lane) = make_int2(q[1], q[3]);
+  } else {
+    constexpr int M = NG / 4;
+    const int g0 = 4 * (lane % M), pos = lane / M;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) t[(g0 + c) * H + pos] = q[c];
+  }
 }
 
 // Group gid's U entries of the step that starts at batch edge j0 (a multiple
-// of 2U, so the reads are 16-byte aligned).
-template <int U, typename T>
+// of NG U, so the reads are 16-byte aligned).
+template <int NG, int U, typename T>
 __device__ __forceinline__ void wide_get(const T* tab, int gid, int j0, T (&out)[U]) {
   static_assert(U % 4 == 0, "whole 16-byte reads");
-  const T* t = tab + gid * kWideHalf + j0 / 2;
+  const T* t = tab + gid * wide_half<NG>() + j0 / NG;
 #pragma unroll
   for (int k = 0; k < U; k += 4) {
     typedef T T4 __attribute__((ext_vector_type(4)));
@@ -400,9 +421,9 @@ __device__ __forceinline__ void spmm_store(const SpmmParams& p, const Item& it, 
 // vector-memory instruction per gather, and the address unit is what bounds
 // these kernels.
 //
-// WIDE (two lane groups, positional ids, one head): 256-edge batches whose
-// ids (and weights) arrive four per lane in one 16-byte load (a quarter of
-// the id loads for the address unit) and go to the group-major LDS table.
+// WIDE (two or more lane groups, positional ids, one head): 256-edge batches
+// whose ids (and weights) arrive four per lane in one 16-byte load (a quarter
+// of the id loads for the address unit) and go to the group-major LDS table.
 // Without weights they are held to 7 wavefronts per SIMD (72 registers): the
 // max kernel otherwise takes 85 (5 wavefronts), with no spill either way.
 template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool SEG, bool ADD = false,
@@ -411,13 +432,14 @@ __global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kern
   constexpr int NG = kWave / G;
   constexpr bool POS = MAX && !EIDS;
   static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
-  static_assert(!WIDE || (NG == 2 && U % 4 == 0 && !EIDS && !TAB),
-                "wide batches serve two lane groups with positional ids");
+  static_assert(!WIDE || (NG >= 2 && U % 4 == 0 && !EIDS && !TAB),
+                "wide batches serve several lane groups with positional ids");
   constexpr int BATCH = WIDE ? 4 * kWave : kWave;
-  __shared__ __align__(16) int32_t wid_all[WIDE ? kWavesPerBlock * kWideTab : 1];
-  __shared__ __align__(16) float wwt_all[WIDE && MUL ? kWavesPerBlock * kWideTab : 1];
-  int32_t* wid = wid_all + (WIDE ? (threadIdx.x >> 6) * kWideTab : 0);
-  float* wwt = wwt_all + (WIDE && MUL ? (threadIdx.x >> 6) * kWideTab : 0);
+  constexpr int WT = WIDE ? wide_tab<NG>() : 1;
+  __shared__ __align__(16) int32_t wid_all[WIDE ? kWavesPerBlock * WT : 1];
+  __shared__ __align__(16) float wwt_all[WIDE && MUL ? kWavesPerBlock * WT : 1];
+  int32_t* wid = wid_all + (WIDE ? (threadIdx.x >> 6) * WT : 0);
+  float* wwt = wwt_all + (WIDE && MUL ? (threadIdx.x >> 6) * WT : 0);
   static_assert(!ADD || (MAX && !MUL), "u_add_v messages are max-reduced copies");
   static_assert(!TAB || MUL, "the table holds edge values");
   constexpr bool EPI = ADD && POS;
@@ -535,8 +557,8 @@ __global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kern
       if constexpr (MUL)  // the weights' bits (0.0f past the batch)
         load_ids<4>(reinterpret_cast<const int32_t*>(p.ev), p.nnz, base, lane, cnt, qw);
       wave_lds_sync();  // the previous batch's table reads are done
-      wide_put(wid, lane, qs);
-      if constexpr (MUL) wide_put(wwt, lane, qw);
+      wide_put<NG>(wid, lane, qs);
+      if constexpr (MUL) wide_put<NG>(wwt, lane, qw);
       wave_lds_sync();
     } else if (lane < cnt) {
       my_src = __builtin_nontemporal_load(p.indices + base + lane);
@@ -612,8 +634,8 @@ __global__ __launch_bounds__(kBlock, (WIDE && !MUL) ? 7 : 1) void spmm_fast_kern
       int32_t tsrc[WIDE ? U : 1];
       float tw[WIDE && MUL ? U : 1];
       if constexpr (WIDE) {
-        wide_get<U>(wid, gid, j0, tsrc);
-        if constexpr (MUL) wide_get<U>(wwt, gid, j0, tw);
+        wide_get<NG, U>(wid, gid, j0, tsrc);
+        if constexpr (MUL) wide_get<NG, U>(wwt, gid, j0, tw);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -1064,15 +1086,18 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
   constexpr int NG = kWave / G;
   static_assert(NG * U <= kWave, "one batch of 64 edges must cover whole steps");
   constexpr int QB = WIDE ? ids_per_lane<NG, U>() : 1;
-  // one or two groups hand each edge's dot product over through this
-  // per-wavefront table (the group's last lane writes it; each lane reads
-  // its QB results after the batch) instead of readlanes and selects
-  __shared__ __align__(16) float res_all[NG <= 2 ? kWavesPerBlock * kWave * QB : 1];
-  float* res_tab = res_all + (NG <= 2 ? (threadIdx.x >> 6) * kWave * QB : 0);
-  // wide batches of two groups take their ids from the group-major table
-  constexpr bool IDTAB = WIDE && NG == 2;
-  __shared__ __align__(16) int32_t sid_all[IDTAB ? kWavesPerBlock * kWideTab : 1];
-  int32_t* sid = sid_all + (IDTAB ? (threadIdx.x >> 6) * kWideTab : 0);
+  // one or two groups, and wide batches, hand each edge's dot product over
+  // through this per-wavefront table (the group's last lane writes it; each
+  // lane reads its QB results after the batch) instead of readlanes and
+  // selects, or a cross-lane permute per step
+  constexpr bool RTAB = NG <= 2 || WIDE;
+  __shared__ __align__(16) float res_all[RTAB ? kWavesPerBlock * kWave * QB : 1];
+  float* res_tab = res_all + (RTAB ? (threadIdx.x >> 6) * kWave * QB : 0);
+  // wide batches of several groups take their ids from the group-major table
+  constexpr bool IDTAB = WIDE && NG >= 2;
+  constexpr int WT = IDTAB ? wide_tab<NG>() : 1;
+  __shared__ __align__(16) int32_t sid_all[IDTAB ? kWavesPerBlock * WT : 1];
+  int32_t* sid = sid_all + (IDTAB ? (threadIdx.x >> 6) * WT : 0);
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -1110,7 +1135,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
     load_ids<Q>(p.indices, p.nnz, base, lane, cnt, my_src);
     if constexpr (IDTAB) {
       wave_lds_sync();  // the previous batch's table reads are done
-      wide_put(sid, lane, my_src);
+      wide_put<NG>(sid, lane, my_src);
       wave_lds_sync();
     }
     if (p.eids) {
@@ -1122,8 +1147,8 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
     // lane j collects the dot products of edges base + Q*j + q, so the batch's
     // results leave in one store instead of one store per step with one lane
     // per group active, which would cost the address unit as much as a
-    // gather: one or two groups hand their sums over through the LDS table,
-    // more groups with one cross-lane permute per step
+    // gather: one or two groups, and wide batches, hand their sums over
+    // through the LDS table, more groups with one cross-lane permute per step
     float res[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) res[q] = 0.0f;
@@ -1134,7 +1159,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
       float val[U][NV][4];
       bool ok[U];
       int32_t tsrc[IDTAB ? U : 1];
-      if constexpr (IDTAB) wide_get<U>(sid, gid, j0, tsrc);
+      if constexpr (IDTAB) wide_get<NG, U>(sid, gid, j0, tsrc);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
@@ -1162,13 +1187,13 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
         part = group_sum<G>(part);
         const int jb = j0 + u * NG;
         // the last lane of group g holds the sum of edge jb + g
-        if constexpr (NG <= 2) {
+        if constexpr (RTAB) {
           if (li == G - 1 && (FULL || jb + gid < cnt)) res_tab[jb + gid] = part;
         } else {
           const int rel = lane - jb;
           const bool mine = rel >= 0 && rel < NG && lane < cnt;
           const float got = __shfl(part, mine ? rel * G + (G - 1) : lane);
-          if (mine) res[0] = got;  // Q == 1 for more than two groups
+          if (mine) res[0] = got;  // Q == 1 without the table
         }
       }
     };
@@ -1177,7 +1202,7 @@ __global__ __launch_bounds__(kBlock) void sddmm_fast_kernel(SddmmParams p) {
     if (all_feat)
       for (; j0 + NG * U <= cnt; j0 += NG * U) step(j0, BoolTag<true>{});
     for (; j0 < cnt; j0 += NG * U) step(j0, BoolTag<false>{});
-    if constexpr (NG <= 2) {
+    if constexpr (RTAB) {
       wave_lds_sync();  // the table holds the batch's results
       if constexpr (Q == 4) {
         const float4 t = *reinterpret_cast<const float4*>(res_tab + lane * Q);
@@ -3011,8 +3036,9 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
   static_assert(SH <= G, "a head's lanes lie inside one lane group");
   static_assert(!WIDE || (NG == 2 && U % 4 == 0), "wide batches serve two lane groups");
   constexpr int BATCH = WIDE ? 4 * kWave : kWave;
-  __shared__ __align__(16) int32_t wid_all[WIDE ? kWavesPerBlock * kWideTab : 1];
-  int32_t* wid = wid_all + (WIDE ? (threadIdx.x >> 6) * kWideTab : 0);
+  constexpr int WT = WIDE ? wide_tab<NG>() : 1;
+  __shared__ __align__(16) int32_t wid_all[WIDE ? kWavesPerBlock * WT : 1];
+  int32_t* wid = wid_all + (WIDE ? (threadIdx.x >> 6) * WT : 0);
   const int64_t item = wave_item();
   if (item >= p.n_items) return;
   const Item it = load_item<SEG>(p.segs, p.indptr, item);
@@ -3039,7 +3065,7 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
       int32_t q[4];
       load_ids<4>(p.indices, p.nnz, base, lane, cnt, q);
       wave_lds_sync();  // the previous batch's table reads are done
-      wide_put(wid, lane, q);
+      wide_put<NG>(wid, lane, q);
       wave_lds_sync();
     } else if (lane < cnt) {
       my_src = __builtin_nontemporal_load(p.indices + base + lane);
@@ -3051,7 +3077,7 @@ __global__ __launch_bounds__(kBlock) void gat_fused_kernel(GatParams p) {
       float val[U][4];
       bool ok[U];
       int32_t tsrc[WIDE ? U : 1];
-      if constexpr (WIDE) wide_get<U>(wid, gid, j0, tsrc);
+      if constexpr (WIDE) wide_get<NG, U>(wid, gid, j0, tsrc);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int jb = j0 + u * NG;
@@ -3157,12 +3183,12 @@ dim3 grid_for(int64_t items, int64_t chunks) {
 #define FG_LAUNCH(kernel, grid, stream, ...) \
   hipLaunchKernelGGL((kernel), (grid), dim3(kBlock), 0, (stream), __VA_ARGS__)
 
-// wide: items average kWideItemEdges edges or more (256-edge batches where
-// the lane layout allows them)
+// avg: the items' average edge count (256-edge batches where the lane layout
+// allows them and the items are long enough, wide_item_edges)
 template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool ADD, bool TAB>
-void spmm_fast_seg2(const SpmmParams& prm, bool seg, bool wide, dim3 grid, hipStream_t st) {
-  if constexpr (kWave / G == 2 && U % 4 == 0 && !EIDS && !TAB) {
-    if (wide && (!MUL || prm.H == 1)) {
+void spmm_fast_seg2(const SpmmParams& prm, bool seg, int64_t avg, dim3 grid, hipStream_t st) {
+  if constexpr (kWave / G >= 2 && U % 4 == 0 && !EIDS && !TAB) {
+    if (avg >= wide_item_edges<kWave / G>() && (!MUL || prm.H == 1)) {
       if (seg)
         FG_LAUNCH((spmm_fast_kernel<G, NV, U, MUL, MAX, EIDS, true, ADD, TAB, true>), grid, st,
                   prm);
@@ -3177,37 +3203,37 @@ void spmm_fast_seg2(const SpmmParams& prm, bool seg, bool wide, dim3 grid, hipSt
 }
 
 template <int G, int NV, int U, bool MUL, bool MAX, bool EIDS, bool ADD = false>
-void spmm_fast_seg(const SpmmParams& prm, bool seg, bool wide, dim3 grid, hipStream_t st) {
+void spmm_fast_seg(const SpmmParams& prm, bool seg, int64_t avg, dim3 grid, hipStream_t st) {
   // per-head edge values come from a per-batch LDS table
   if constexpr (MUL) {
     if (prm.H >= 2 && prm.H <= kTabHeads) {
-      spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, true>(prm, seg, wide, grid, st);
+      spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, true>(prm, seg, avg, grid, st);
       return;
     }
   }
-  spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, false>(prm, seg, wide, grid, st);
+  spmm_fast_seg2<G, NV, U, MUL, MAX, EIDS, ADD, false>(prm, seg, avg, grid, st);
 }
 
 template <int G, int NV, int U, bool MUL, bool MAX, bool ADD = false>
-void spmm_fast_eids(const SpmmParams& prm, bool seg, bool wide, dim3 grid, hipStream_t st) {
+void spmm_fast_eids(const SpmmParams& prm, bool seg, int64_t avg, dim3 grid, hipStream_t st) {
   // copy + sum never looks at edge ids
   if (prm.eids && (MUL || MAX))
-    spmm_fast_seg<G, NV, U, MUL, MAX, true, ADD>(prm, seg, wide, grid, st);
+    spmm_fast_seg<G, NV, U, MUL, MAX, true, ADD>(prm, seg, avg, grid, st);
   else
-    spmm_fast_seg<G, NV, U, MUL, MAX, false, ADD>(prm, seg, wide, grid, st);
+    spmm_fast_seg<G, NV, U, MUL, MAX, false, ADD>(prm, seg, avg, grid, st);
 }
 
 template <int G, int NV, int U>
-void spmm_fast_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, bool wide, dim3 grid,
+void spmm_fast_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, int64_t avg, dim3 grid,
                    hipStream_t st) {
   if (prm.xd) {
-    spmm_fast_eids<G, NV, U, false, true, true>(prm, seg, wide, grid, st);
+    spmm_fast_eids<G, NV, U, false, true, true>(prm, seg, avg, grid, st);
   } else if (mul) {
-    if (mx) spmm_fast_eids<G, NV, U, true, true>(prm, seg, wide, grid, st);
-    else spmm_fast_eids<G, NV, U, true, false>(prm, seg, wide, grid, st);
+    if (mx) spmm_fast_eids<G, NV, U, true, true>(prm, seg, avg, grid, st);
+    else spmm_fast_eids<G, NV, U, true, false>(prm, seg, avg, grid, st);
   } else {
-    if (mx) spmm_fast_eids<G, NV, U, false, true>(prm, seg, wide, grid, st);
-    else spmm_fast_eids<G, NV, U, false, false>(prm, seg, wide, grid, st);
+    if (mx) spmm_fast_eids<G, NV, U, false, true>(prm, seg, avg, grid, st);
+    else spmm_fast_eids<G, NV, U, false, false>(prm, seg, avg, grid, st);
   }
 }
 
@@ -3231,11 +3257,12 @@ void spmm_generic_ops(const SpmmParams& prm, bool mul, bool mx, bool seg, dim3 g
   }
 }
 
-// wide: batches of four ids per lane where the lane layout allows it
+// avg: the items' average edge count (batches of four ids per lane where the
+// lane layout allows it and the items are long enough, wide_item_edges)
 template <int G, int NV, int U>
-void sddmm_fast_go(const SddmmParams& prm, bool seg, bool wide, dim3 grid, hipStream_t st) {
+void sddmm_fast_go(const SddmmParams& prm, bool seg, int64_t avg, dim3 grid, hipStream_t st) {
   if constexpr (ids_per_lane<kWave / G, U>() > 1) {
-    if (wide) {
+    if (avg >= wide_item_edges<kWave / G>()) {
       if (seg) FG_LAUNCH((sddmm_fast_kernel<G, NV, U, true, true>), grid, st, prm);
       else FG_LAUNCH((sddmm_fast_kernel<G, NV, U, false, true>), grid, st, prm);
       return;
@@ -3293,16 +3320,16 @@ hipError_t launch_spmm_core(const GraphView& g, const PlanView* plan, int msg, i
   prm.ev_vec4 = (ev && H % 4 == 0 && aligned16(ev)) ? 1 : 0;
   if (vec4) {
     const int64_t Q = F / 4;  // float4 per row
-    const bool wide = g.nnz >= kWideItemEdges * std::max<int64_t>(prm.n_items, 1);
+    const int64_t avg = g.nnz / std::max<int64_t>(prm.n_items, 1);
     const dim3 grid1 = grid_for(prm.n_items, 1);
-    if (Q <= 4) spmm_fast_ops<4, 1, 4>(prm, mul, mx, seg, wide, grid1, stream);
-    else if (Q <= 8) spmm_fast_ops<8, 1, 8>(prm, mul, mx, seg, wide, grid1, stream);
-    else if (Q <= 16) spmm_fast_ops<16, 1, 8>(prm, mul, mx, seg, wide, grid1, stream);
-    else if (Q <= 32) spmm_fast_ops<32, 1, 8>(prm, mul, mx, seg, wide, grid1, stream);
-    else if (Q <= 64) spmm_fast_ops<64, 1, 8>(prm, mul, mx, seg, wide, grid1, stream);
-    else if (Q <= 128) spmm_fast_ops<64, 2, 4>(prm, mul, mx, seg, wide, grid1, stream);
+    if (Q <= 4) spmm_fast_ops<4, 1, 4>(prm, mul, mx, seg, avg, grid1, stream);
+    else if (Q <= 8) spmm_fast_ops<8, 1, 8>(prm, mul, mx, seg, avg, grid1, stream);
+    else if (Q <= 16) spmm_fast_ops<16, 1, 8>(prm, mul, mx, seg, avg, grid1, stream);
+    else if (Q <= 32) spmm_fast_ops<32, 1, 8>(prm, mul, mx, seg, avg, grid1, stream);
+    else if (Q <= 64) spmm_fast_ops<64, 1, 8>(prm, mul, mx, seg, avg, grid1, stream);
+    else if (Q <= 128) spmm_fast_ops<64, 2, 4>(prm, mul, mx, seg, avg, grid1, stream);
     else
-      spmm_fast_ops<64, 4, 2>(prm, mul, mx, seg, wide, grid_for(prm.n_items, (Q + 255) / 256),
+      spmm_fast_ops<64, 4, 2>(prm, mul, mx, seg, avg, grid_for(prm.n_items, (Q + 255) / 256),
                               stream);
   } else {
     // scalar lanes: G = 2^ceil(log2 F) up to 64, then NV values per lane
@@ -3463,17 +3490,17 @@ hipError_t launch_gsddmm(const GraphView& g, const PlanView* plan, int64_t H, in
   const bool vec4 = (F % 4 == 0) && (H == 1 || dh % 4 == 0) && aligned16(xs) && aligned16(xd);
   if (vec4 && H == 1 && F <= 4 * 4 * kWave) {
     const int64_t Q = F / 4;
-    // items of kWideItemEdges edges or more on average take the 256-edge
+    // items long enough on average (wide_item_edges) take the 256-edge
     // batches; short items (source-slab pieces) keep 64-edge batches
     const int64_t items = seg ? plan->num_segments : g.num_rows;
-    const bool wide = g.nnz >= kWideItemEdges * std::max<int64_t>(items, 1);
-    if (Q <= 4) sddmm_fast_go<4, 1, 4>(prm, seg, wide, grid, stream);
-    else if (Q <= 8) sddmm_fast_go<8, 1, 8>(prm, seg, wide, grid, stream);
-    else if (Q <= 16) sddmm_fast_go<16, 1, 8>(prm, seg, wide, grid, stream);
-    else if (Q <= 32) sddmm_fast_go<32, 1, 8>(prm, seg, wide, grid, stream);
-    else if (Q <= 64) sddmm_fast_go<64, 1, 8>(prm, seg, wide, grid, stream);
-    else if (Q <= 128) sddmm_fast_go<64, 2, 4>(prm, seg, wide, grid, stream);
-    else sddmm_fast_go<64, 4, 2>(prm, seg, wide, grid, stream);
+    const int64_t avg = g.nnz / std::max<int64_t>(items, 1);
+    if (Q <= 4) sddmm_fast_go<4, 1, 4>(prm, seg, avg, grid, stream);
+    else if (Q <= 8) sddmm_fast_go<8, 1, 8>(prm, seg, avg, grid, stream);
+    else if (Q <= 16) sddmm_fast_go<16, 1, 8>(prm, seg, avg, grid, stream);
+    else if (Q <= 32) sddmm_fast_go<32, 1, 8>(prm, seg, avg, grid, stream);
+    else if (Q <= 64) sddmm_fast_go<64, 1, 8>(prm, seg, avg, grid, stream);
+    else if (Q <= 128) sddmm_fast_go<64, 2, 4>(prm, seg, avg, grid, stream);
+    else sddmm_fast_go<64, 4, 2>(prm, seg, avg, grid, stream);
     return hipGetLastError();
   }
   if (vec4 && H > 1 && F <= 4 * kWave && (dh == 16 || dh == 32 || dh == 64)) {

@@ -1502,7 +1502,7 @@ def test_sddmm_wide_batches_with_edge_ids_and_ragged_ends():
     assert dst.size % 4 != 0
     csr = synth.coo_to_csr(dst.astype(np.int64), src.astype(np.int64), n, m)
     csc = csr_to_csc(csr)
-    for d in (128, 256):
+    for d in (128, 256, 64, 32, 16):
         xs = rng.standard_normal((m, d)).astype(np.float32)
         xd = rng.standard_normal((n, d)).astype(np.float32)
         G = fg.Graph.from_csr(csr)
@@ -1518,14 +1518,15 @@ def test_sddmm_wide_batches_with_edge_ids_and_ragged_ends():
 
 
 def test_gspmm_wide_batches_ragged_ends():
-    """The gSpMM's 256-edge batches (two lane groups, d = 65..128, items of 128
-    edges or more on average): ids and weights four per lane through the
-    group-major LDS table.  Copy and weighted sum, max with and without
-    weights and the MLP's u_add_v max, at d = 128 (unmasked steps) and
-    d = 100 (every step masked), on rows whose lengths are not multiples of
-    4 or 256 and a stored-edge count that is not a multiple of 4 (the last
-    lane of the last item loads its ids and weights one by one); then the
-    same graph with short items (64-edge batches) and with split rows."""
+    """The gSpMM's 256-edge batches (two or more lane groups, long items):
+    ids and weights four per lane through the group-major LDS table.  Copy
+    and weighted sum, max with and without weights and the MLP's u_add_v
+    max, with 2 lane groups at d = 128 (unmasked steps) and d = 100 (every
+    step masked), 4 at d = 64, 8 at d = 32 and d = 20 (masked), 16 at
+    d = 16, on rows whose lengths are not multiples of 4 or 256 and a
+    stored-edge count that is not a multiple of 4 (the last lane of the last
+    item loads its ids and weights one by one); then the same graph with
+    short items (64-edge batches) and with split rows."""
     rng = np.random.default_rng(78)
     n, m = 600, 1000
     deg = rng.integers(130, 700, size=n)
@@ -1538,7 +1539,7 @@ def test_gspmm_wide_batches_ragged_ends():
     csr = synth.coo_to_csr(dst.astype(np.int64), src.astype(np.int64), n, m)
     G = fg.Graph.from_csr(csr)
     ew = rng.uniform(0.0, 1.0, csr.nnz).astype(np.float32) + np.float32(1e-3)
-    for d in (128, 100):
+    for d in (128, 100, 64, 32, 20, 16):
         x = rng.standard_normal((m, d)).astype(np.float32)
         xi = rng.integers(-4, 5, (m, d)).astype(np.float32)
         ewi = rng.integers(1, 4, csr.nnz).astype(np.float32)
@@ -1558,6 +1559,36 @@ def test_gspmm_wide_batches_ragged_ends():
     xdm = rng.standard_normal((n, 8)).astype(np.float32)
     for plan in (fg.Plan(G, 128), fg.Plan(G, 128, segment_edges=300)):
         check_mlp(csr, G, xm, xdm, w, plan=plan)
+
+
+def test_wide_batches_for_many_lane_groups_on_mid_length_rows():
+    """Items of 64 to 127 edges on average: kernels with four or more lane
+    groups (d <= 64) take the wide batches, two groups (d = 128) keep 64-edge
+    batches.  Rows of 60-130 edges (one or two 64-edge batches, never more
+    than one wide batch), an empty row and a last row that ends off a
+    4-edge boundary."""
+    rng = np.random.default_rng(80)
+    n, m = 900, 700
+    deg = rng.integers(60, 131, size=n)
+    deg[11] = 0
+    deg[-1] = 83
+    dst = np.repeat(np.arange(n), deg)
+    src = rng.integers(0, m, size=dst.size)
+    if dst.size % 4 == 0:
+        dst, src = dst[:-1], src[:-1]
+    csr = synth.coo_to_csr(dst.astype(np.int64), src.astype(np.int64), n, m)
+    G = fg.Graph.from_csr(csr)
+    ew = rng.uniform(0.0, 1.0, csr.nnz).astype(np.float32) + np.float32(1e-3)
+    for d in (16, 32, 48, 64, 128):
+        xs = rng.standard_normal((m, d)).astype(np.float32)
+        xd = rng.standard_normal((n, d)).astype(np.float32)
+        plan = fg.Plan(G, d)
+        say("mid-length rows d=%d items=%d" % (d, plan.info()["num_segments"]))
+        for pl in (plan, None):
+            check_spmm(csr, G, xs, plan=pl)
+            check_spmm(csr, G, xs, plan=pl, edge=ew)
+            check_spmm(csr, G, xs, plan=pl, reduce="max")
+            check_sddmm(csr, G, xs, xd, plan=pl)
 
 
 def test_gat_fused_wide_batches_ragged_ends():
