@@ -1554,11 +1554,12 @@ def test_gspmm_wide_batches_ragged_ends():
             check_spmm(csr, G, x, plan=plan, reduce="max")
             check_spmm(csr, G, xi, plan=plan, reduce="max")
             check_spmm(csr, G, x, plan=plan, edge=ew, reduce="max")
-    w = rng.standard_normal((8, 128)).astype(np.float32)
     xm = rng.standard_normal((m, 8)).astype(np.float32)
     xdm = rng.standard_normal((n, 8)).astype(np.float32)
-    for plan in (fg.Plan(G, 128), fg.Plan(G, 128, segment_edges=300)):
-        check_mlp(csr, G, xm, xdm, w, plan=plan)
+    for d_out in (128, 32, 16):
+        w = rng.standard_normal((8, d_out)).astype(np.float32)
+        for plan in (fg.Plan(G, d_out), fg.Plan(G, d_out, segment_edges=300)):
+            check_mlp(csr, G, xm, xdm, w, plan=plan)
 
 
 def test_wide_batches_for_many_lane_groups_on_mid_length_rows():
