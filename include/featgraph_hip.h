@@ -120,7 +120,7 @@ typedef struct fg_graph {
  *    (fg_plan_options.item_order), rows without edges last;
  *  - gather (gSpMM, gSDDMM, the fused SDDMM + edge softmax, fused
  *    attention): as plain with S =
- *    segment_edges if given, else 2048, unless source
+ *    segment_edges if given, else 1536, unless source
  *    partitioning applies (by default once the num_cols x max_width source
  *    features exceed 128 MiB, half the Infinity Cache, or 32 MiB when the
  *    gathers are spread; see fg_plan_options.source_slab_rows).  With it,
@@ -149,7 +149,7 @@ typedef struct fg_graph {
 typedef struct fg_plan fg_plan; /* opaque; owns device schedules + workspace */
 
 typedef struct fg_plan_options {
-  int32_t segment_edges;        /* S: target edges per item; 0 -> default (2048 for
+  int32_t segment_edges;        /* S: target edges per item; 0 -> default (1536 for
                                    the gather schedule, 16384 for the plain one)    */
   int32_t max_row_segments;     /* cap on items per row (plain cut); 0 -> 128        */
   int32_t source_slab_rows;     /* source ids per slab of the gather schedule;
@@ -196,7 +196,7 @@ typedef struct fg_plan_options {
   int32_t band_row_edges;       /* die-banded gather schedule (item_order 3): rows
                                    of more edges are cut into at least
                                    min(8, max_row_segments) pieces, so that every
-                                   die takes a share of them; 0 -> 512; -1 -> no
+                                   die takes a share of them; 0 -> 256; -1 -> no
                                    such cut (the items of order 1)                  */
   int32_t reserved[2];          /* must be zero                                      */
 } fg_plan_options;

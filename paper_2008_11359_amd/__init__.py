@@ -258,7 +258,7 @@ def _check_host_csr(num_rows, num_cols, indptr, indices, eids, nnz_total):
 
 class Plan:
     """Degree-aware schedules of one graph (see fg_plan_create): rows longer
-    than ``segment_edges`` (default 2048 edges in the gather schedule of
+    than ``segment_edges`` (default 1536 edges in the gather schedule of
     gSpMM / gSDDMM, 16,384 in the edge-softmax schedule, which
     ``softmax_segment_edges`` sets apart) are cut into equal pieces (at most
     ``max_row_segments``); long rows of the gather schedule may also be cut
@@ -269,7 +269,7 @@ class Plan:
     they exceed 32 MiB; -2 never; > 0 that many source ids per slab.  ``item_order``: 1 longest
     item first, 2 by power-of-two length class with rows in id order (keeps
     the locality of graphs whose neighbouring ids share sources), 3 the items
-    of 1 with rows of more than ``band_row_edges`` edges (default 512; -1:
+    of 1 with rows of more than ``band_row_edges`` edges (default 256; -1:
     none) cut into at least 8 pieces and the pieces of split rows dealt to
     the dies by position in the row (each die gathers from about one eighth
     of their sources; with ``band_row_edges=-1`` the results equal those of

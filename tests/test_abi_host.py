@@ -647,7 +647,7 @@ def test_die_banded_schedule(S):
 @pytest.mark.parametrize("T,cap", [(0, 0), (40, 0), (40, 5)])
 def test_die_banded_cuts_mid_length_rows(T, cap):
     """item_order 3 cuts every row of more than band_row_edges edges (default
-    512) into at least min(8, max_row_segments) even pieces, longer rows as
+    256) into at least min(8, max_row_segments) even pieces, longer rows as
     before; with 8 pieces each goes to its own die.  The edge-softmax
     schedule is not affected."""
     c = synth.make_config("rmat_233k_115m", scale_down=64).csr
@@ -657,7 +657,7 @@ def test_die_banded_cuts_mid_length_rows(T, cap):
                                              item_order=3, **kw)
     plain, *_ = fg.schedule_host(c.indptr, None, c.num_cols, 128, "plain", item_order=3, **kw)
     deg = np.diff(c.indptr)
-    thr, cap_ = (T or 512), (cap or 128)
+    thr, cap_ = (T or 256), (cap or 128)
     base = np.minimum(np.maximum(-(-deg // S), 1), cap_)
     want = np.where(deg > thr, np.maximum(base, np.minimum(np.minimum(8, cap_), deg)), base)
     want[deg == 0] = 1
