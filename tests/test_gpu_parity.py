@@ -978,10 +978,64 @@ def test_random_configurations(seed):
                        partition_min_degree=min_deg, item_order=order,
                        max_backward=seed % 2 == 1)
         say("plan", plan.info())
-    nt = nnz_total or g.nnz
     ops = rng.choice(["sum", "mul", "max", "sddmm", "softmax", "softmax_bwd", "max_bwd", "gat",
                       "mlp", "sddmm_softmax", "sddmm_softmax_bwd"], size=3, replace=False)
     say("seed", seed, kind, "n", n, "nnz", g.nnz, "F", F, "heads", heads, "ops", list(ops))
+    _check_ops(rng, ops, g, G, x, xd, plan, heads, nnz_total)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_configurations_long_rows(seed):
+    """Seeded sweep over graphs whose rows average 64 to 400 edges (uniform,
+    power-law with hubs, blocked communities; sometimes transposed with edge
+    ids), so that the gather kernels take their 256-edge batches, at widths
+    of one to sixteen lane groups, with heads, operators and plan options
+    (segment length, source slabs, item order, mid-length cut): each case
+    against the oracle on every row."""
+    rng = np.random.default_rng(5000 + seed)
+    kind = ("uniform", "rmat", "blocked")[seed % 3]
+    n = int(rng.integers(64, 1500))
+    avg = int(rng.integers(64, 400))
+    if kind == "uniform":
+        csr = synth.uniform_graph(rng, n, n * avg)
+    elif kind == "rmat":
+        scale = max(1, int(np.ceil(np.log2(n))))
+        csr = synth.rmat_graph(np.random.SeedSequence(5000 + seed), rng, scale, n, n * avg,
+                               workers=1)
+    else:
+        csr = _blocked_graph(rng, n, 2 * avg)
+    F = int(rng.choice((16, 20, 32, 48, 64, 96, 100, 128, 256)))
+    heads = int(rng.choice([h for h in (1, 2, 4, 8) if F % h == 0]))
+    nnz_total = None
+    g = csr
+    if seed % 5 == 2:  # the transposed graph with edge ids
+        g, nnz_total = csr_to_csc(csr), csr.nnz
+    x = rng.standard_normal((g.num_cols, F)).astype(np.float32)
+    xd = rng.standard_normal((g.num_rows, F)).astype(np.float32)
+    if heads > 1:
+        x = x.reshape(g.num_cols, heads, F // heads)
+        xd = xd.reshape(g.num_rows, heads, F // heads)
+    G = fg.Graph.from_csr(g, nnz_total=nnz_total or 0)
+    if rng.random() < 0.2:
+        plan = None
+    else:
+        plan = fg.Plan(G, F, segment_edges=int(rng.choice([0, 100, 512, 2048, 8192])),
+                       source_slab_rows=int(rng.choice([0, -2, 300])),
+                       item_order=int(rng.choice([0, 1, 3])),
+                       band_row_edges=int(rng.choice([0, -1, 100])))
+        say("plan", plan.info())
+    ops = rng.choice(["sum", "mul", "max", "sddmm", "softmax", "gat", "mlp", "sddmm_softmax"],
+                     size=3, replace=False)
+    say("seed", seed, kind, "n", n, "nnz", g.nnz, "F", F, "heads", heads, "ops", list(ops))
+    _check_ops(rng, ops, g, G, x, xd, plan, heads, nnz_total)
+
+
+def _check_ops(rng, ops, g, G, x, xd, plan, heads, nnz_total):
+    """Each of ops on graph g (G on the device) against the oracle on every
+    row; draws its extra inputs from rng."""
+    n, F = g.num_rows, int(np.prod(x.shape[1:]))
+    square = g.num_rows == g.num_cols
+    nt = nnz_total or g.nnz
     for op in ops:
         if op == "sum":
             check_spmm(g, G, x, plan=plan, heads=heads, nnz_total=nnz_total)
